@@ -1,0 +1,217 @@
+/*
+ * decomoe.h - C ABI of the MI355X (gfx950) hot path of DecoMoE's RCEP MoE layer.
+ *
+ * The library computes one MoE invocation of a multimodal MoE decoder layer
+ * in the paper's notation (Sec. 3.1 and Sec. 3.3; Algorithm 2):
+ *
+ *   logits  a = x W_r + b over all E (reordered) experts        moe_route
+ *   full-pool Top-k R_i and renormalised weights (Eq. 10)         moe_route
+ *   activated mass s (Eq. 11), prefix length K (Eq. 12),
+ *   Mean-Mass calibration order pi (Eqs. 8, 9)                    moe_calibrate_prefix
+ *   prefix-restricted re-route inside [0, K)                      moe_route
+ *   grouping of the T*k assignments by expert                     moe_dispatch
+ *   SwiGLU expert MLPs over the dispatched rows                   moe_expert_ffn
+ *   weighted combine back to token order                          moe_combine
+ *   SAVB visual-block removal from the hidden state (Sec. 3.2)   drop_visual_block
+ *
+ * Conventions shared by every entry point
+ *   - Every array pointer is a DEVICE pointer owned by the caller; the
+ *     library never allocates, frees or retains device memory.  Arrays are
+ *     row-major and contiguous.  Scratch memory comes from the caller as
+ *     (ws, ws_bytes); moe_workspace_size() returns a sufficient size.
+ *   - Activations and expert weights are MOE_F32 or MOE_BF16 (the `dtype`
+ *     argument); router weights, bias, logits and routing weights are
+ *     float32; masses are float64; indices, counts and lengths are int32.
+ *   - Every call is asynchronous on `stream` (a hipStream_t; NULL is the
+ *     null stream) and never synchronises with the host.  Data-dependent
+ *     sizes (K, per-expert counts) stay on the device; grids are sized from
+ *     the host-side upper bounds passed in.
+ *   - Errors: arguments are validated on the host before anything is
+ *     launched; on error nothing is launched and a negative MOE_E* code is
+ *     returned.  A launch failure reported by the HIP runtime returns
+ *     MOE_EHIP.  Contents of device arrays (indices, K values) are not
+ *     validated on the host; the kernels clamp or skip out-of-range entries
+ *     as documented per function so that no access leaves its array.
+ *   - Outputs must not overlap inputs or each other (MOE_EALIAS), except
+ *     where stated.
+ *   - Array pointers must be 16-byte aligned (MOE_EINVAL otherwise);
+ *     drop_visual_block only needs element alignment.
+ *   - All results are deterministic: repeated calls on the same inputs give
+ *     bitwise-identical outputs (no floating-point atomics anywhere).
+ */
+#ifndef DECOMOE_H
+#define DECOMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t* hipStream_t;
+
+typedef enum moe_dtype { MOE_F32 = 0, MOE_BF16 = 1 } moe_dtype;
+
+enum {
+  MOE_OK = 0,
+  MOE_EINVAL = -1,       /* a size or value argument is out of range        */
+  MOE_EALIAS = -2,       /* an output overlaps an input or another output   */
+  MOE_EWORKSPACE = -3,   /* ws is NULL or ws_bytes is too small             */
+  MOE_EHIP = -4,         /* the HIP runtime reported a launch error         */
+  MOE_EUNSUPPORTED = -5  /* valid per the method but not supported here     */
+};
+
+/* Human-readable text of a status code (static storage, never NULL). */
+const char* moe_status_string(int status);
+
+/* Bytes of scratch sufficient for every entry point called with sizes up to
+ * T tokens, E experts, k slots, hidden size d, expert width m and n_seg
+ * segments.  Returns 0 for invalid sizes. */
+size_t moe_workspace_size(int T, int E, int k, int d, int m, int n_seg);
+
+/*
+ * moe_route - router logits and Top-k routing (Eq. 1; Eq. 10; the
+ * prefix-restricted re-route after Eq. 12 and Algorithm 2).
+ *
+ *   x          [T, d] token rows (dtype) or NULL.  If x != NULL the logits
+ *              a = x W_r + b are computed in float32 and written to
+ *              `logits`.  If x == NULL, `logits` is an INPUT (e.g. the
+ *              logits of a previous full-pool call) and w_r, bias are unused.
+ *   w_r        [d, E] float32 router weights (reordered expert order).
+ *   bias       [E] float32 or NULL (no bias).
+ *   seg_offsets[n_seg + 1] int32 token offsets of the invocations
+ *              (segments), non-decreasing from 0 to T; NULL means one
+ *              segment [0, T) and n_seg is then ignored.
+ *   K_dev      [n_seg] int32 prefix length per segment, or NULL for K = E
+ *              (full-pool routing).  Each K is clamped to [k, E].
+ *   logits     [T, E] float32 (output if x != NULL, input otherwise).
+ *   topk_idx   [T, k] int32: per token the k experts with the largest
+ *              logits among experts [0, K), in descending logit order,
+ *              equal logits to the lower expert index.  Softmax is strictly
+ *              increasing, so this is the Top-k of the probabilities.
+ *   topk_w     [T, k] float32: the softmax over [0, K) restricted to the
+ *              selected experts and renormalised, i.e. the softmax of the
+ *              k selected logits; each row sums to 1.
+ * Limits: 1 <= k <= min(E, 32); 1 <= E <= 1024; T >= 0; d >= 1; for bf16 x,
+ * d % 8 == 0.  Logits must be finite.  x == NULL with logits == NULL is
+ * MOE_EINVAL.
+ */
+int moe_route(const void* x, moe_dtype dtype, const float* w_r, const float* bias,
+              int T, int d, int E, int k,
+              const int32_t* seg_offsets, int n_seg, const int32_t* K_dev,
+              float* logits, int32_t* topk_idx, float* topk_w,
+              hipStream_t stream);
+
+/*
+ * moe_calibrate_prefix - activated mass, prefix length and Mean-Mass order
+ * (Eqs. 8, 9, 11 and 12).
+ *
+ *   topk_idx, topk_w  [T, k] full-pool routing (moe_route with K_dev = NULL).
+ *   seg_offsets       [n_seg + 1] segment offsets or NULL (one segment).
+ *   p                 routed-mass fraction, 0 < p <= 1.
+ *   mass              [n_seg, E] float64 output: s_e of each segment (Eq. 11).
+ *   K_out             [n_seg] int32 output or NULL: K = max(k, K_hat) with
+ *                     K_hat the shortest prefix whose running fp64 sum c_K
+ *                     satisfies c_K >= p * c_E (Eq. 12).  A segment with no
+ *                     tokens gets K = k.
+ *   order             [E] int32 output or NULL: the Mean-Mass order pi
+ *                     (Eq. 9) with the segments taken as calibration cases:
+ *                     each non-empty segment contributes its routed mass
+ *                     s_e / len (Eq. 8), the case masses are averaged in
+ *                     segment order, and experts are sorted by descending
+ *                     mean, equal means keeping the lower index first.
+ *                     order[j] is the expert placed at position j.  With no
+ *                     non-empty segment the order is the identity.
+ * Each segment's masses are one float64 running sum per expert in ascending
+ * token order, and c_K one running sum in expert order, so K depends on the
+ * inputs only (no reduction-order effects).  Index entries outside [0, E)
+ * are skipped.  No workspace is needed.
+ */
+int moe_calibrate_prefix(const int32_t* topk_idx, const float* topk_w,
+                         int T, int E, int k,
+                         const int32_t* seg_offsets, int n_seg, double p,
+                         double* mass, int32_t* K_out, int32_t* order,
+                         hipStream_t stream);
+
+/*
+ * moe_dispatch - group the T*k (token, slot) assignments by expert
+ * (Algorithm 2: only the selected experts are evaluated).
+ *
+ *   topk_idx     [T, k] int32 expert per slot.
+ *   x            [T, d] token rows (dtype) or NULL (then x_perm is not written).
+ *   counts       [E] int32: rows per expert.
+ *   offsets      [E + 1] int32: exclusive prefix sum of counts.
+ *   src_of_row   [T*k] int32: dispatched row r -> assignment t*k + j.
+ *   row_of_slot  [T*k] int32: assignment t*k + j -> dispatched row r.
+ *   x_perm       [T*k, d] (dtype): x_perm[r] = x[src_of_row[r] / k].
+ * The grouping is a stable counting sort: within an expert rows ascend by
+ * token.  Entries of topk_idx outside [0, E) are dropped (not counted, no
+ * row), so offsets[E] < T*k flags them.  Needs ws.
+ */
+int moe_dispatch(const int32_t* topk_idx, int T, int k, int E,
+                 const void* x, moe_dtype dtype, int d,
+                 int32_t* counts, int32_t* offsets,
+                 int32_t* src_of_row, int32_t* row_of_slot, void* x_perm,
+                 void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * moe_expert_ffn - SwiGLU expert MLPs over the dispatched rows, experts
+ * [0, K) only (Algorithm 2; gate, up and down projections as counted in
+ * App. A.3, Eq. 15).
+ *
+ *   x_perm     [rows_max, d] dispatched rows (dtype), grouped by `offsets`.
+ *   offsets    [E + 1] int32 from moe_dispatch.
+ *   K_dev      [n_K] int32 or NULL: experts e >= max(K_dev[0..n_K)) are not
+ *              evaluated (their rows, of which prefix routing leaves none,
+ *              are left unwritten); NULL evaluates all E experts.
+ *   rows_max   upper bound of offsets[E] (normally T*k).
+ *   w_gate_up  [E, 2m, d] (dtype): rows [0, m) gate, [m, 2m) up projection.
+ *   w_down     [E, d, m] (dtype).
+ *   y_perm     [rows_max, d] (dtype) output: for row r of expert e,
+ *              y = W_down[e] (SiLU(W_gate[e] x) * (W_up[e] x)),
+ *              SiLU(z) = z / (1 + exp(-z)).
+ * Arithmetic: bf16 inputs use bf16 MFMA with float32 accumulation; the
+ * intermediate SiLU(g)*u is formed in float32 and rounded once to dtype
+ * before the down projection; y is rounded once to dtype.  float32 inputs
+ * use float32 arithmetic throughout.
+ * Limits (bf16): d % 128 == 0 and m % 64 == 0, else MOE_EUNSUPPORTED.
+ * Offsets are clamped to [0, rows_max].  Needs ws.
+ */
+int moe_expert_ffn(const void* x_perm, moe_dtype dtype, const int32_t* offsets, int E,
+                   const int32_t* K_dev, int n_K, int rows_max, int d, int m,
+                   const void* w_gate_up, const void* w_down, void* y_perm,
+                   void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * moe_combine - weighted combine back to token order (Algorithm 2).
+ *
+ *   y_perm       [T*k, d] expert outputs per dispatched row (dtype).
+ *   row_of_slot  [T*k] int32 from moe_dispatch.
+ *   topk_w       [T, k] float32 routing weights.
+ *   out          [T, d] (dtype): out_t = sum_{j<k} w_{t,j} y_perm[row_of_slot[t*k+j]],
+ *                accumulated in float32 in slot order, rounded once.
+ * Slots whose row index lies outside [0, T*k) contribute nothing.
+ */
+int moe_combine(const void* y_perm, moe_dtype dtype, const int32_t* row_of_slot,
+                const float* topk_w, int T, int k, int d, void* out,
+                hipStream_t stream);
+
+/*
+ * drop_visual_block - SAVB visual-block removal from the hidden state
+ * (Sec. 3.2: at the exit the complete visual block leaves the sequence;
+ * Algorithm 2).
+ *
+ *   h    [S, d] hidden rows (dtype); the visual block is rows [v0, v1).
+ *   out  [S - (v1 - v0), d]: rows [0, v0) then [v1, S) of h, order kept,
+ *        copied bit for bit.  out must not overlap h (MOE_EALIAS).
+ * Needs 0 <= v0 <= v1 <= S.  The exit decision itself is the caller's.
+ */
+int drop_visual_block(const void* h, moe_dtype dtype, int S, int d, int v0, int v1,
+                      void* out, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DECOMOE_H */

@@ -1,0 +1,159 @@
+"""Thin ctypes binding of libdecomoe.so (C ABI in include/decomoe.h).
+
+Argument marshalling only: every step of the path runs in the HIP kernels
+of the library.  Functions carry the C names; array arguments are torch
+tensors on the GPU (their ``data_ptr()`` is passed), sizes are taken from
+the tensors, and the stream defaults to torch's current stream.  A non-zero
+status raises ``MoeError``.  There is no fallback: without the built
+library every call raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libdecomoe.so")
+
+MOE_F32, MOE_BF16 = 0, 1
+STATUS = {0: "MOE_OK", -1: "MOE_EINVAL", -2: "MOE_EALIAS", -3: "MOE_EWORKSPACE",
+          -4: "MOE_EHIP", -5: "MOE_EUNSUPPORTED"}
+
+EXPORTS = ("moe_status_string", "moe_workspace_size", "moe_route", "moe_calibrate_prefix",
+           "moe_dispatch", "moe_expert_ffn", "moe_combine", "drop_visual_block")
+
+
+class MoeError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__(f"{fn} returned {STATUS.get(status, status)}: {_status_text(status)}")
+
+
+_lib = None
+_P, _I, _D, _S = ctypes.c_void_p, ctypes.c_int, ctypes.c_double, ctypes.c_size_t
+
+
+def load() -> ctypes.CDLL:
+    """Load the in-tree library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_38823_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    sig = {
+        "moe_status_string": (ctypes.c_char_p, [_I]),
+        "moe_workspace_size": (_S, [_I, _I, _I, _I, _I, _I]),
+        "moe_route": (_I, [_P, _I, _P, _P, _I, _I, _I, _I, _P, _I, _P, _P, _P, _P, _P]),
+        "moe_calibrate_prefix": (_I, [_P, _P, _I, _I, _I, _P, _I, _D, _P, _P, _P, _P]),
+        "moe_dispatch": (_I, [_P, _I, _I, _I, _P, _I, _I, _P, _P, _P, _P, _P, _P, _S, _P]),
+        "moe_expert_ffn": (_I, [_P, _I, _P, _I, _P, _I, _I, _I, _I, _P, _P, _P, _P, _S, _P]),
+        "moe_combine": (_I, [_P, _I, _P, _P, _I, _I, _I, _P, _P]),
+        "drop_visual_block": (_I, [_P, _I, _I, _I, _I, _I, _P, _P]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype, f.argtypes = res, args
+    _lib = lib
+    return lib
+
+
+def _status_text(status: int) -> str:
+    try:
+        return load().moe_status_string(status).decode()
+    except Exception:
+        return "?"
+
+
+def _p(t):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("device arrays are passed as torch tensors")
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError("arrays must be contiguous GPU tensors")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+
+
+def _dt(t) -> int:
+    if t.dtype == torch.bfloat16:
+        return MOE_BF16
+    if t.dtype == torch.float32:
+        return MOE_F32
+    raise TypeError(f"unsupported activation dtype {t.dtype}")
+
+
+def _check(fn: str, status: int):
+    if status != 0:
+        raise MoeError(fn, status)
+
+
+def _nseg(seg_offsets):
+    return 1 if seg_offsets is None else seg_offsets.numel() - 1
+
+
+def moe_workspace_size(T: int, E: int, k: int, d: int, m: int, n_seg: int = 1) -> int:
+    return int(load().moe_workspace_size(T, E, k, d, m, n_seg))
+
+
+def moe_route(x, w_r, bias, k, logits, topk_idx, topk_w, seg_offsets=None, K_dev=None,
+              stream=None):
+    """x [T, d] or None (then `logits` [T, E] is an input)."""
+    T, E = logits.shape
+    d = x.shape[1] if x is not None else 0
+    dt = _dt(x) if x is not None else MOE_F32
+    _check("moe_route", load().moe_route(
+        _p(x), dt, _p(w_r) if x is not None else None, _p(bias) if x is not None else None,
+        T, d, E, k, _p(seg_offsets), _nseg(seg_offsets), _p(K_dev),
+        _p(logits), _p(topk_idx), _p(topk_w), _stream(stream)))
+
+
+def moe_calibrate_prefix(topk_idx, topk_w, E, p, mass, K_out=None, order=None,
+                         seg_offsets=None, stream=None):
+    T, k = topk_idx.shape
+    _check("moe_calibrate_prefix", load().moe_calibrate_prefix(
+        _p(topk_idx), _p(topk_w), T, E, k, _p(seg_offsets), _nseg(seg_offsets), float(p),
+        _p(mass), _p(K_out), _p(order), _stream(stream)))
+
+
+def moe_dispatch(topk_idx, E, x, counts, offsets, src_of_row, row_of_slot, x_perm, ws,
+                 stream=None):
+    T, k = topk_idx.shape
+    d = x.shape[1] if x is not None else 0
+    dt = _dt(x) if x is not None else MOE_F32
+    _check("moe_dispatch", load().moe_dispatch(
+        _p(topk_idx), T, k, E, _p(x), dt, d, _p(counts), _p(offsets), _p(src_of_row),
+        _p(row_of_slot), _p(x_perm), _p(ws), ws.numel() * ws.element_size() if ws is not None else 0,
+        _stream(stream)))
+
+
+def moe_expert_ffn(x_perm, offsets, w_gate_up, w_down, y_perm, ws, K_dev=None, stream=None):
+    rows_max, d = x_perm.shape
+    E, two_m, _ = w_gate_up.shape
+    n_K = K_dev.numel() if K_dev is not None else 0
+    _check("moe_expert_ffn", load().moe_expert_ffn(
+        _p(x_perm), _dt(x_perm), _p(offsets), E, _p(K_dev), n_K, rows_max, d, two_m // 2,
+        _p(w_gate_up), _p(w_down), _p(y_perm), _p(ws), ws.numel() * ws.element_size(),
+        _stream(stream)))
+
+
+def moe_combine(y_perm, row_of_slot, topk_w, out, stream=None):
+    T, k = topk_w.shape
+    d = out.shape[1]
+    _check("moe_combine", load().moe_combine(
+        _p(y_perm), _dt(y_perm), _p(row_of_slot), _p(topk_w), T, k, d, _p(out), _stream(stream)))
+
+
+def drop_visual_block(h, v0, v1, out, stream=None):
+    S, d = h.shape
+    _check("drop_visual_block", load().drop_visual_block(
+        _p(h), _dt(h), S, d, v0, v1, _p(out), _stream(stream)))

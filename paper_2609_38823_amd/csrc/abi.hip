@@ -1,0 +1,208 @@
+// Exported C ABI: host-side validation, then the launches.  Nothing here
+// allocates, frees or synchronises.
+#include "common.hpp"
+
+#include "../../include/decomoe.h"
+
+namespace {
+
+using decomoe::dispatch_ws_bytes;
+using decomoe::ffn_ws_bytes;
+
+constexpr int kMaxE = 1024;
+constexpr int kMaxK = 32;
+
+struct Range {
+  uintptr_t lo, hi;  // [lo, hi)
+};
+Range rng(const void* p, size_t bytes) {
+  uintptr_t a = reinterpret_cast<uintptr_t>(p);
+  return Range{a, a + bytes};
+}
+bool overlap(Range a, Range b) {
+  if (a.lo == a.hi || b.lo == b.hi || !a.lo || !b.lo) return false;
+  return a.lo < b.hi && b.lo < a.hi;
+}
+// true if any output overlaps any input or another output
+bool any_alias(std::initializer_list<Range> outs, std::initializer_list<Range> ins) {
+  for (auto o = outs.begin(); o != outs.end(); ++o) {
+    for (const Range& i : ins)
+      if (overlap(*o, i)) return true;
+    for (auto o2 = o + 1; o2 != outs.end(); ++o2)
+      if (overlap(*o, *o2)) return true;
+  }
+  return false;
+}
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned_all(std::initializer_list<const void*> ps) {
+  for (const void* p : ps)
+    if (p && !aligned16(p)) return false;
+  return true;
+}
+int elt_size(moe_dtype dt) { return dt == MOE_BF16 ? 2 : 4; }
+bool valid_dtype(moe_dtype dt) { return dt == MOE_F32 || dt == MOE_BF16; }
+int hip_status(hipError_t e) { return e == hipSuccess ? MOE_OK : MOE_EHIP; }
+size_t a256(size_t b) { return (b + 255) & ~size_t(255); }
+
+}  // namespace
+
+extern "C" {
+
+const char* moe_status_string(int status) {
+  switch (status) {
+    case MOE_OK: return "ok";
+    case MOE_EINVAL: return "invalid argument (size, range or pointer)";
+    case MOE_EALIAS: return "an output overlaps an input or another output";
+    case MOE_EWORKSPACE: return "workspace missing or too small";
+    case MOE_EHIP: return "HIP runtime reported a launch error";
+    case MOE_EUNSUPPORTED: return "shape not supported by this build";
+    default: return "unknown status";
+  }
+}
+
+size_t moe_workspace_size(int T, int E, int k, int d, int m, int n_seg) {
+  if (T < 0 || E < 1 || E > kMaxE || k < 1 || k > E || d < 1 || m < 1 || n_seg < 1) return 0;
+  size_t rows = (size_t)T * k;
+  size_t a = a256(dispatch_ws_bytes(T, k, E));
+  size_t b = ffn_ws_bytes(true, (int)rows, E, d, m);
+  size_t c = ffn_ws_bytes(false, (int)rows, E, d, m);
+  size_t w = a > b ? a : b;
+  w = w > c ? w : c;
+  return w < 256 ? 256 : w;
+}
+
+int moe_route(const void* x, moe_dtype dtype, const float* w_r, const float* bias, int T, int d,
+              int E, int k, const int32_t* seg_offsets, int n_seg, const int32_t* K_dev,
+              float* logits, int32_t* topk_idx, float* topk_w, hipStream_t stream) {
+  if (T < 0 || E < 1 || E > kMaxE || k < 1 || k > E) return MOE_EINVAL;
+  if (k > kMaxK) return MOE_EUNSUPPORTED;
+  if (!seg_offsets) n_seg = 1;
+  if (n_seg < 1) return MOE_EINVAL;
+  if (!logits) return MOE_EINVAL;
+  if (x) {
+    if (!valid_dtype(dtype) || d < 1 || !w_r) return MOE_EINVAL;
+    if (dtype == MOE_BF16 && d % 8 != 0) return MOE_EINVAL;
+  }
+  if (T == 0) return MOE_OK;
+  if (!topk_idx || !topk_w) return MOE_EINVAL;
+  if (!aligned_all({x, w_r, bias, seg_offsets, K_dev, logits, topk_idx, topk_w})) return MOE_EINVAL;
+  const size_t nl = (size_t)T * E * 4, nk = (size_t)T * k * 4;
+  Range in_x = x ? rng(x, (size_t)T * d * elt_size(dtype)) : Range{0, 0};
+  Range in_w = x ? rng(w_r, (size_t)d * E * 4) : Range{0, 0};
+  Range in_b = (x && bias) ? rng(bias, (size_t)E * 4) : Range{0, 0};
+  Range in_s = seg_offsets ? rng(seg_offsets, (size_t)(n_seg + 1) * 4) : Range{0, 0};
+  Range in_k = K_dev ? rng(K_dev, (size_t)n_seg * 4) : Range{0, 0};
+  if (x) {
+    if (any_alias({rng(logits, nl), rng(topk_idx, nk), rng(topk_w, nk)}, {in_x, in_w, in_b, in_s, in_k}))
+      return MOE_EALIAS;
+    hipError_t e = decomoe::launch_router_logits(x, dtype == MOE_BF16, w_r, bias, T, d, E, logits, stream);
+    if (e != hipSuccess) return MOE_EHIP;
+  } else {
+    if (any_alias({rng(topk_idx, nk), rng(topk_w, nk)}, {rng(logits, nl), in_s, in_k})) return MOE_EALIAS;
+  }
+  return hip_status(decomoe::launch_topk(logits, T, E, k, seg_offsets, n_seg, K_dev, topk_idx,
+                                         topk_w, stream));
+}
+
+int moe_calibrate_prefix(const int32_t* topk_idx, const float* topk_w, int T, int E, int k,
+                         const int32_t* seg_offsets, int n_seg, double p, double* mass,
+                         int32_t* K_out, int32_t* order, hipStream_t stream) {
+  if (T < 0 || E < 1 || E > kMaxE || k < 1 || k > E) return MOE_EINVAL;
+  if (!seg_offsets) n_seg = 1;
+  if (n_seg < 1) return MOE_EINVAL;
+  if (!(p > 0.0 && p <= 1.0)) return MOE_EINVAL;
+  if (!mass || (T > 0 && (!topk_idx || !topk_w))) return MOE_EINVAL;
+  if (!aligned_all({topk_idx, topk_w, seg_offsets, mass, K_out, order})) return MOE_EINVAL;
+  const size_t nk = (size_t)T * k * 4;
+  Range in_i = T ? rng(topk_idx, nk) : Range{0, 0};
+  Range in_w = T ? rng(topk_w, nk) : Range{0, 0};
+  Range in_s = seg_offsets ? rng(seg_offsets, (size_t)(n_seg + 1) * 4) : Range{0, 0};
+  Range o_k = K_out ? rng(K_out, (size_t)n_seg * 4) : Range{0, 0};
+  Range o_o = order ? rng(order, (size_t)E * 4) : Range{0, 0};
+  if (any_alias({rng(mass, (size_t)n_seg * E * 8), o_k, o_o}, {in_i, in_w, in_s})) return MOE_EALIAS;
+  return hip_status(decomoe::launch_calibrate(topk_idx, topk_w, T, E, k, seg_offsets, n_seg, p,
+                                              mass, K_out, order, stream));
+}
+
+int moe_dispatch(const int32_t* topk_idx, int T, int k, int E, const void* x, moe_dtype dtype,
+                 int d, int32_t* counts, int32_t* offsets, int32_t* src_of_row,
+                 int32_t* row_of_slot, void* x_perm, void* ws, size_t ws_bytes,
+                 hipStream_t stream) {
+  if (T < 0 || E < 1 || E > kMaxE || k < 1 || k > E) return MOE_EINVAL;
+  if ((size_t)T * k > (size_t)INT32_MAX) return MOE_EUNSUPPORTED;
+  if (!counts || !offsets) return MOE_EINVAL;
+  if (T > 0 && (!topk_idx || !src_of_row || !row_of_slot)) return MOE_EINVAL;
+  if (x && (!valid_dtype(dtype) || d < 1 || (T > 0 && !x_perm))) return MOE_EINVAL;
+  if (!aligned_all({topk_idx, x, counts, offsets, src_of_row, row_of_slot, x_perm, ws}))
+    return MOE_EINVAL;
+  const size_t need = dispatch_ws_bytes(T, k, E);
+  if (need > 0 && (!ws || ws_bytes < need)) return MOE_EWORKSPACE;
+  const size_t A = (size_t)T * k;
+  Range in_i = rng(topk_idx, A * 4);
+  Range in_x = x ? rng(x, (size_t)T * d * elt_size(dtype)) : Range{0, 0};
+  Range o_xp = x ? rng(x_perm, A * d * elt_size(dtype)) : Range{0, 0};
+  Range o_ws = rng(ws, need);
+  if (any_alias({rng(counts, (size_t)E * 4), rng(offsets, (size_t)(E + 1) * 4), rng(src_of_row, A * 4),
+                 rng(row_of_slot, A * 4), o_xp, o_ws},
+                {in_i, in_x}))
+    return MOE_EALIAS;
+  return hip_status(decomoe::launch_dispatch(topk_idx, T, k, E, x, elt_size(dtype), d, counts,
+                                             offsets, src_of_row, row_of_slot, x_perm, ws, stream));
+}
+
+int moe_expert_ffn(const void* x_perm, moe_dtype dtype, const int32_t* offsets, int E,
+                   const int32_t* K_dev, int n_K, int rows_max, int d, int m,
+                   const void* w_gate_up, const void* w_down, void* y_perm, void* ws,
+                   size_t ws_bytes, hipStream_t stream) {
+  if (!valid_dtype(dtype) || E < 1 || E > kMaxE || rows_max < 0 || d < 1 || m < 1) return MOE_EINVAL;
+  if (K_dev && n_K < 1) return MOE_EINVAL;
+  if (!offsets || !w_gate_up || !w_down) return MOE_EINVAL;
+  if (rows_max > 0 && (!x_perm || !y_perm)) return MOE_EINVAL;
+  const bool bf16 = dtype == MOE_BF16;
+  if (bf16 && (d % 128 != 0 || m % 64 != 0)) return MOE_EUNSUPPORTED;
+  if (!aligned_all({x_perm, offsets, K_dev, w_gate_up, w_down, y_perm, ws})) return MOE_EINVAL;
+  if (rows_max == 0) return MOE_OK;
+  const size_t need = ffn_ws_bytes(bf16, rows_max, E, d, m);
+  if (!ws || ws_bytes < need) return MOE_EWORKSPACE;
+  const int es = elt_size(dtype);
+  Range o_y = rng(y_perm, (size_t)rows_max * d * es);
+  Range o_ws = rng(ws, need);
+  Range in_k = K_dev ? rng(K_dev, (size_t)n_K * 4) : Range{0, 0};
+  if (any_alias({o_y, o_ws},
+                {rng(x_perm, (size_t)rows_max * d * es), rng(offsets, (size_t)(E + 1) * 4), in_k,
+                 rng(w_gate_up, (size_t)E * 2 * m * d * es), rng(w_down, (size_t)E * d * m * es)}))
+    return MOE_EALIAS;
+  return hip_status(decomoe::launch_expert_ffn(x_perm, bf16, offsets, E, K_dev, n_K, rows_max, d,
+                                               m, w_gate_up, w_down, y_perm, ws, stream));
+}
+
+int moe_combine(const void* y_perm, moe_dtype dtype, const int32_t* row_of_slot,
+                const float* topk_w, int T, int k, int d, void* out, hipStream_t stream) {
+  if (!valid_dtype(dtype) || T < 0 || k < 1 || k > kMaxE || d < 1) return MOE_EINVAL;
+  if ((size_t)T * k > (size_t)INT32_MAX) return MOE_EUNSUPPORTED;
+  if (T == 0) return MOE_OK;
+  if (!y_perm || !row_of_slot || !topk_w || !out) return MOE_EINVAL;
+  if (!aligned_all({y_perm, row_of_slot, topk_w, out})) return MOE_EINVAL;
+  const int es = elt_size(dtype);
+  const size_t A = (size_t)T * k;
+  if (any_alias({rng(out, (size_t)T * d * es)},
+                {rng(y_perm, A * d * es), rng(row_of_slot, A * 4), rng(topk_w, A * 4)}))
+    return MOE_EALIAS;
+  return hip_status(decomoe::launch_combine(y_perm, dtype == MOE_BF16, row_of_slot, topk_w, T, k,
+                                            d, out, stream));
+}
+
+int drop_visual_block(const void* h, moe_dtype dtype, int S, int d, int v0, int v1, void* out,
+                      hipStream_t stream) {
+  if (!valid_dtype(dtype) || S < 0 || d < 1) return MOE_EINVAL;
+  if (!(0 <= v0 && v0 <= v1 && v1 <= S)) return MOE_EINVAL;
+  const int rows_out = S - (v1 - v0);
+  if (rows_out == 0) return MOE_OK;
+  if (!h || !out) return MOE_EINVAL;
+  const int es = elt_size(dtype);
+  if ((reinterpret_cast<uintptr_t>(h) | reinterpret_cast<uintptr_t>(out)) % es) return MOE_EINVAL;
+  if (overlap(rng(out, (size_t)rows_out * d * es), rng(h, (size_t)S * d * es))) return MOE_EALIAS;
+  return hip_status(decomoe::launch_drop_rows(h, es, S, d, v0, v1, out, stream));
+}
+
+}  // extern "C"

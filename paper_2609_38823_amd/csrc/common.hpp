@@ -1,0 +1,60 @@
+// Shared device helpers and launcher declarations of the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace decomoe {
+
+constexpr int kWave = 64;  // CDNA wavefront width
+
+// ---- bf16 <-> f32 (bf16 is the upper half of an IEEE binary32) ----------
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+  return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+// round to nearest, ties to even; NaN stays NaN
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+}
+
+__device__ __forceinline__ int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
+
+// segment containing token t: the last s with seg_offsets[s] <= t
+__device__ __forceinline__ int find_segment(const int32_t* seg_offsets, int n_seg, int t) {
+  int lo = 0, hi = n_seg - 1;
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (seg_offsets[mid] <= t) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// ---- launchers (host side; return hipError_t of the launch) -------------
+hipError_t launch_router_logits(const void* x, bool x_bf16, const float* w_r, const float* bias,
+                                int T, int d, int E, float* logits, hipStream_t s);
+hipError_t launch_topk(const float* logits, int T, int E, int k, const int32_t* seg_offsets,
+                       int n_seg, const int32_t* K_dev, int32_t* idx, float* w, hipStream_t s);
+hipError_t launch_calibrate(const int32_t* idx, const float* w, int T, int E, int k,
+                            const int32_t* seg_offsets, int n_seg, double p, double* mass,
+                            int32_t* K_out, int32_t* order, hipStream_t s);
+size_t dispatch_ws_bytes(int T, int k, int E);
+hipError_t launch_dispatch(const int32_t* idx, int T, int k, int E, const void* x, int elt, int d,
+                           int32_t* counts, int32_t* offsets, int32_t* src_of_row,
+                           int32_t* row_of_slot, void* x_perm, void* ws, hipStream_t s);
+size_t ffn_ws_bytes(bool bf16, int rows_max, int E, int d, int m);
+hipError_t launch_expert_ffn(const void* x_perm, bool bf16, const int32_t* offsets, int E,
+                             const int32_t* K_dev, int n_K, int rows_max, int d, int m,
+                             const void* w_gate_up, const void* w_down, void* y_perm, void* ws,
+                             hipStream_t s);
+hipError_t launch_combine(const void* y_perm, bool bf16, const int32_t* row_of_slot,
+                          const float* w, int T, int k, int d, void* out, hipStream_t s);
+hipError_t launch_drop_rows(const void* h, int elt, int S, int d, int v0, int v1, void* out,
+                            hipStream_t s);
+
+}  // namespace decomoe

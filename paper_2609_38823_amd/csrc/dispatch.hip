@@ -1,0 +1,206 @@
+// Dispatch: stable counting sort of the T*k (token, slot) assignments by
+// expert, then a token-major row gather (Algorithm 2: only the selected
+// experts see a token).
+//
+//   1. chunk histograms      one workgroup per 1024 assignments, LDS counters
+//   2. scan                  counts, offsets and each chunk's base per expert
+//   3. ranks                 per wavefront, 64 assignments per round: lanes
+//                            holding the same expert are found with ballots
+//                            over the key bits; rank = lanes below with the
+//                            same key; stable because chunks, waves and
+//                            rounds follow assignment order
+//   4. gather                each token row is read once and written to its
+//                            k dispatched rows with 16-byte stores
+#include "common.hpp"
+
+namespace decomoe {
+namespace {
+
+constexpr int DP_CHUNK = 1024;  // assignments per chunk
+constexpr int DP_THREADS = 256;  // 4 wavefronts, 256 assignments each
+constexpr int DP_PER_WAVE = DP_CHUNK / (DP_THREADS / kWave);
+
+__global__ __launch_bounds__(DP_THREADS) void dispatch_hist_kernel(const int32_t* __restrict__ idx,
+                                                                   int A, int E,
+                                                                   int32_t* __restrict__ hist) {
+  __shared__ int h[1024];
+  for (int e = threadIdx.x; e < E; e += DP_THREADS) h[e] = 0;
+  __syncthreads();
+  const int a0 = blockIdx.x * DP_CHUNK;
+  for (int i = threadIdx.x; i < DP_CHUNK; i += DP_THREADS) {
+    int a = a0 + i;
+    if (a < A) {
+      int e = idx[a];
+      if (e >= 0 && e < E) atomicAdd(&h[e], 1);
+    }
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < E; e += DP_THREADS) hist[(size_t)blockIdx.x * E + e] = h[e];
+}
+
+// one workgroup of 1024 threads; thread e owns expert e
+__global__ __launch_bounds__(1024) void dispatch_scan_kernel(const int32_t* __restrict__ hist,
+                                                             int n_chunks, int E,
+                                                             int32_t* __restrict__ base,
+                                                             int32_t* __restrict__ counts,
+                                                             int32_t* __restrict__ offsets) {
+  __shared__ int sc[1024];
+  const int e = threadIdx.x;
+  int cnt = 0;
+  if (e < E)
+    for (int c = 0; c < n_chunks; ++c) cnt += hist[(size_t)c * E + e];
+  sc[e] = e < E ? cnt : 0;
+  __syncthreads();
+  // inclusive Hillis-Steele scan over the 1024 counters
+  for (int off = 1; off < 1024; off <<= 1) {
+    int v = e >= off ? sc[e - off] : 0;
+    __syncthreads();
+    sc[e] += v;
+    __syncthreads();
+  }
+  if (e < E) {
+    int run = sc[e] - cnt;  // exclusive
+    counts[e] = cnt;
+    offsets[e] = run;
+    for (int c = 0; c < n_chunks; ++c) {
+      base[(size_t)c * E + e] = run;
+      run += hist[(size_t)c * E + e];
+    }
+    if (e == E - 1) offsets[E] = run;
+  }
+}
+
+__global__ __launch_bounds__(DP_THREADS) void dispatch_rank_kernel(
+    const int32_t* __restrict__ idx, int A, int E, int key_bits, const int32_t* __restrict__ base,
+    int32_t* __restrict__ src_of_row, int32_t* __restrict__ row_of_slot) {
+  constexpr int NW = DP_THREADS / kWave;
+  __shared__ int run[NW][1024];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int a_chunk = blockIdx.x * DP_CHUNK;
+  // per-wave histograms of this chunk
+  for (int i = threadIdx.x; i < NW * 1024; i += DP_THREADS) (&run[0][0])[i] = 0;
+  __syncthreads();
+  for (int i = 0; i < DP_PER_WAVE; i += kWave) {
+    int a = a_chunk + wv * DP_PER_WAVE + i + lane;
+    if (a < A) {
+      int e = idx[a];
+      if (e >= 0 && e < E) atomicAdd(&run[wv][e], 1);
+    }
+  }
+  __syncthreads();
+  // turn them into each wave's starting row per expert
+  for (int e = threadIdx.x; e < E; e += DP_THREADS) {
+    int r = base[(size_t)blockIdx.x * E + e];
+#pragma unroll
+    for (int w2 = 0; w2 < NW; ++w2) {
+      int c = run[w2][e];
+      run[w2][e] = r;
+      r += c;
+    }
+  }
+  __syncthreads();
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int i = 0; i < DP_PER_WAVE; i += kWave) {
+    int a = a_chunk + wv * DP_PER_WAVE + i + lane;
+    int e = a < A ? idx[a] : -1;
+    bool valid = e >= 0 && e < E;
+    uint64_t peers = __ballot(valid);
+#pragma unroll 1
+    for (int b = 0; b < key_bits; ++b) {
+      bool bit = (e >> b) & 1;
+      uint64_t m = __ballot(bit);
+      peers &= bit ? m : ~m;
+    }
+    if (valid) {
+      int r = run[wv][e] + __popcll(peers & lt_mask);
+      src_of_row[r] = a;
+      row_of_slot[a] = r;
+      // the highest lane of the group advances the expert's counter
+      if ((63 - __clzll(peers)) == lane) run[wv][e] += __popcll(peers);
+    } else if (a < A) {
+      row_of_slot[a] = -1;
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
+// token-major gather: each token row is read once (VEC-sized vectors, rows
+// of `chunks` vectors) and stored to its k dispatched rows.  A block covers
+// one token when a row has >= 256 vectors, else `rpb` whole tokens.
+template <typename VEC>
+__global__ __launch_bounds__(256) void dispatch_gather_kernel(const VEC* __restrict__ x, int T,
+                                                              int k, int chunks, int rpb,
+                                                              const int32_t* __restrict__ row_of_slot,
+                                                              VEC* __restrict__ x_perm) {
+  const int A = T * k;
+  int t, c0, cstep;
+  if (chunks >= 256) {
+    t = blockIdx.x;
+    c0 = threadIdx.x;
+    cstep = 256;
+  } else {
+    int tl = threadIdx.x / chunks;
+    if (tl >= rpb) return;
+    t = blockIdx.x * rpb + tl;
+    c0 = threadIdx.x % chunks;
+    cstep = chunks;
+  }
+  if (t >= T) return;
+  for (int c = c0; c < chunks; c += cstep) {
+    VEC v = x[(size_t)t * chunks + c];
+    for (int j = 0; j < k; ++j) {
+      int r = row_of_slot[(size_t)t * k + j];
+      if (r >= 0 && r < A) x_perm[(size_t)r * chunks + c] = v;
+    }
+  }
+}
+}  // namespace
+
+size_t dispatch_ws_bytes(int T, int k, int E) {
+  size_t A = (size_t)T * k;
+  size_t n_chunks = (A + DP_CHUNK - 1) / DP_CHUNK;
+  return 2 * n_chunks * (size_t)E * sizeof(int32_t);
+}
+
+hipError_t launch_dispatch(const int32_t* idx, int T, int k, int E, const void* x, int elt, int d,
+                           int32_t* counts, int32_t* offsets, int32_t* src_of_row,
+                           int32_t* row_of_slot, void* x_perm, void* ws, hipStream_t s) {
+  const int A = T * k;
+  const int n_chunks = (A + DP_CHUNK - 1) / DP_CHUNK;
+  int32_t* hist = static_cast<int32_t*>(ws);
+  int32_t* base = hist + (size_t)n_chunks * E;
+  if (n_chunks > 0) {
+    dispatch_hist_kernel<<<n_chunks, DP_THREADS, 0, s>>>(idx, A, E, hist);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+  }
+  dispatch_scan_kernel<<<1, 1024, 0, s>>>(hist, n_chunks, E, base, counts, offsets);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess || n_chunks == 0) return err;
+  int key_bits = 0;
+  while ((1 << key_bits) < E) ++key_bits;
+  dispatch_rank_kernel<<<n_chunks, DP_THREADS, 0, s>>>(idx, A, E, key_bits, base, src_of_row,
+                                                        row_of_slot);
+  err = hipGetLastError();
+  if (err != hipSuccess || !x) return err;
+  const size_t row_bytes = (size_t)d * elt;
+  if (row_bytes % 16 == 0) {
+    int chunks = (int)(row_bytes / 16);
+    int rpb = chunks >= 256 ? 1 : 256 / chunks;
+    dispatch_gather_kernel<uint4><<<(T + rpb - 1) / rpb, 256, 0, s>>>(
+        static_cast<const uint4*>(x), T, k, chunks, rpb, row_of_slot, static_cast<uint4*>(x_perm));
+  } else if (row_bytes % 4 == 0) {
+    int chunks = (int)(row_bytes / 4);
+    int rpb = chunks >= 256 ? 1 : 256 / chunks;
+    dispatch_gather_kernel<uint32_t><<<(T + rpb - 1) / rpb, 256, 0, s>>>(
+        static_cast<const uint32_t*>(x), T, k, chunks, rpb, row_of_slot, static_cast<uint32_t*>(x_perm));
+  } else {
+    int chunks = (int)(row_bytes / 2);
+    int rpb = chunks >= 256 ? 1 : 256 / chunks;
+    dispatch_gather_kernel<uint16_t><<<(T + rpb - 1) / rpb, 256, 0, s>>>(
+        static_cast<const uint16_t*>(x), T, k, chunks, rpb, row_of_slot, static_cast<uint16_t*>(x_perm));
+  }
+  return hipGetLastError();
+}
+
+}  // namespace decomoe

@@ -21,6 +21,8 @@ with a fixed key per role, so any array can be regenerated independently.
 
 from __future__ import annotations
 
+import os
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass, field
 
 import numpy as np
@@ -133,13 +135,18 @@ def layer_params(shape: LayerShape, seed: int = 0, layer: int = 0) -> dict:
     bias = None
     if shape.zipf_alpha is not None:
         bias = zipf_bias(E, shape.zipf_s, shape.zipf_alpha, _rng(seed, _S_PARAMS, layer, _P_BIAS))
-    g_gu = _rng(seed, _S_PARAMS, layer, _P_GU)
-    g_dn = _rng(seed, _S_PARAMS, layer, _P_DOWN)
     w_gate_up = np.empty((E, 2 * m, d), np.float32)
     w_down = np.empty((E, d, m), np.float32)
-    for e in range(E):  # per expert keeps the float32 temporaries small
-        w_gate_up[e] = _store(_normal(g_gu, (2 * m, d), shape.w_std), shape.dtype)
-        w_down[e] = _store(_normal(g_dn, (d, m), shape.w_std), shape.dtype)
+
+    def fill(e):  # one independent stream per expert and tensor
+        w_gate_up[e] = _store(_normal(_rng(seed, _S_PARAMS, layer, _P_GU, e), (2 * m, d), shape.w_std),
+                              shape.dtype)
+        w_down[e] = _store(_normal(_rng(seed, _S_PARAMS, layer, _P_DOWN, e), (d, m), shape.w_std),
+                           shape.dtype)
+
+    workers = max(1, min(16, len(os.sched_getaffinity(0))))
+    with ThreadPoolExecutor(max_workers=workers) as ex:
+        list(ex.map(fill, range(E)))
     return dict(w_r=w_r, bias=bias, w_gate_up=w_gate_up, w_down=w_down)
 
 
@@ -170,3 +177,50 @@ def logits_with_ties(T: int, E: int, seed: int = 0, levels: int = 4) -> np.ndarr
     levels, so that exact ties between experts are common."""
     rng = _rng(seed, 9, T, E)
     return (rng.integers(0, levels, size=(T, E)).astype(np.float32) * np.float32(0.5))
+
+
+# --------------------------------------------------------------------------
+# Stage-level inputs: arrays shaped like the intermediate results of the
+# layer, drawn directly, so that each stage can be fed identical inputs on
+# both sides.
+# --------------------------------------------------------------------------
+def zipf_probs(E: int, s: float, rng: np.random.Generator) -> np.ndarray:
+    """Zipf(s) popularity over E experts in a seeded random order."""
+    r = np.arange(1, E + 1, dtype=np.float64) ** (-s)
+    pr = np.empty(E)
+    pr[rng.permutation(E)] = r / r.sum()
+    return pr
+
+
+def synthetic_routing(T: int, E: int, k: int, seed: int = 0, zipf_s: float = 1.1,
+                      K: int | None = None):
+    """Routing-shaped arrays: idx [T, k] int32 with k distinct experts per
+    token drawn without replacement from [0, K) (K = E by default) with
+    Zipf-skewed popularity, and weights w [T, k] float32 in (0, 1]."""
+    K = E if K is None else K
+    rng = _rng(seed, 10, T, E, k, K)
+    pr = zipf_probs(K, zipf_s, rng)
+    # sampling without replacement: the k largest of log(p) + Gumbel noise
+    keys = np.log(pr)[None, :] + rng.gumbel(size=(T, K))
+    idx = np.argsort(-keys, axis=1, kind="stable")[:, :k].astype(np.int32)
+    w = (1.0 - rng.random((T, k), dtype=np.float32)).astype(np.float32)
+    return idx, w
+
+
+def synthetic_counts(E: int, rows: int, seed: int = 0, zipf_s: float = 1.1, K: int | None = None):
+    """Rows per expert: a multinomial draw of `rows` rows over experts [0, K)
+    with Zipf-skewed probabilities (experts >= K get none)."""
+    K = E if K is None else K
+    rng = _rng(seed, 11, E, rows, K)
+    counts = np.zeros(E, np.int64)
+    counts[:K] = rng.multinomial(rows, zipf_probs(K, zipf_s, rng))
+    return counts
+
+
+def synthetic_rows(n: int, d: int, dtype: str, seed: int = 0, std: float = 1.0) -> np.ndarray:
+    """n rows ~ N(0, std^2) in the storage precision."""
+    return _store(_normal(_rng(seed, 12, n, d), (n, d), std), dtype)
+
+
+def synthetic_permutation(n: int, seed: int = 0) -> np.ndarray:
+    return _rng(seed, 13, n).permutation(n).astype(np.int32)

@@ -1,0 +1,154 @@
+"""Dense-span and RCEP-span MoE layers composed from the C-ABI calls.
+
+Everything computed here runs in libdecomoe.so; this module only owns device
+buffers (torch tensors used as plain device memory) and issues the calls in
+the order of Algorithm 2 of the paper:
+
+  dense span (before the visual exit):
+      moe_route(x) -> moe_dispatch -> moe_expert_ffn -> moe_combine
+  RCEP span (from the visual exit on):
+      moe_route(x) [full pool] -> moe_calibrate_prefix [s, K]
+      -> moe_route(logits, K) [prefix re-route] -> moe_dispatch
+      -> moe_expert_ffn(K) -> moe_combine
+
+All calls are asynchronous on one stream and K never leaves the device.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import abi
+
+_TORCH_DT = {"f32": torch.float32, "bf16": torch.bfloat16}
+
+
+def to_device(a: np.ndarray | None, dtype: torch.dtype, device="cuda"):
+    """Upload a float32 numpy array (bf16 layers: values already bf16-exact)."""
+    if a is None:
+        return None
+    return torch.from_numpy(np.ascontiguousarray(a)).to(device).to(dtype).contiguous()
+
+
+def apply_order(params: dict, order: np.ndarray) -> dict:
+    """Physical expert reorder (Sec. 3.3 after Eq. 9; Algorithm 1): new
+    expert j is native expert order[j] in the router columns, the bias, and
+    the gate/up and down tensors.  Done once on the host when the layer is
+    loaded: it moves storage and computes nothing."""
+    order = np.asarray(order)
+    return dict(
+        w_r=np.ascontiguousarray(params["w_r"][:, order]),
+        bias=None if params["bias"] is None else np.ascontiguousarray(params["bias"][order]),
+        w_gate_up=np.ascontiguousarray(params["w_gate_up"][order]),
+        w_down=np.ascontiguousarray(params["w_down"][order]),
+    )
+
+
+def calibrate_order_router(x_text: torch.Tensor, w_r: np.ndarray, bias, k: int,
+                           seg_offsets=None) -> np.ndarray:
+    """Mean-Mass order (Eqs. 8, 9) of one layer from the full-pool routing
+    of calibration text rows on the native-order router; each segment is
+    one calibration case.  Only the router weights are needed."""
+    T = x_text.shape[0]
+    E = w_r.shape[1]
+    n_seg = 1 if seg_offsets is None else seg_offsets.numel() - 1
+    dev = x_text.device
+    logits = torch.empty((T, E), dtype=torch.float32, device=dev)
+    idx = torch.empty((T, k), dtype=torch.int32, device=dev)
+    w = torch.empty((T, k), dtype=torch.float32, device=dev)
+    mass = torch.empty((n_seg, E), dtype=torch.float64, device=dev)
+    order = torch.empty((E,), dtype=torch.int32, device=dev)
+    abi.moe_route(x_text, to_device(w_r, torch.float32, dev), to_device(bias, torch.float32, dev), k,
+                  logits, idx, w)
+    abi.moe_calibrate_prefix(idx, w, E, 1.0, mass, order=order, seg_offsets=seg_offsets)
+    return order.cpu().numpy()
+
+
+class Buffers:
+    """Device buffers of one invocation size (T tokens, n_seg segments)."""
+
+    def __init__(self, T: int, d: int, E: int, m: int, k: int, dt: torch.dtype, n_seg: int = 1,
+                 device="cuda"):
+        i32, f32 = torch.int32, torch.float32
+        A = T * k
+        self.T, self.n_seg = T, n_seg
+        self.logits = torch.empty((T, E), dtype=f32, device=device)
+        self.idx_full = torch.empty((T, k), dtype=i32, device=device)
+        self.w_full = torch.empty((T, k), dtype=f32, device=device)
+        self.mass = torch.empty((n_seg, E), dtype=torch.float64, device=device)
+        self.K = torch.empty((n_seg,), dtype=i32, device=device)
+        self.idx = torch.empty((T, k), dtype=i32, device=device)
+        self.w = torch.empty((T, k), dtype=f32, device=device)
+        self.counts = torch.empty((E,), dtype=i32, device=device)
+        self.offsets = torch.empty((E + 1,), dtype=i32, device=device)
+        self.src_of_row = torch.empty((A,), dtype=i32, device=device)
+        self.row_of_slot = torch.empty((A,), dtype=i32, device=device)
+        self.x_perm = torch.empty((A, d), dtype=dt, device=device)
+        self.y_perm = torch.empty((A, d), dtype=dt, device=device)
+        self.out = torch.empty((T, d), dtype=dt, device=device)
+        nbytes = abi.moe_workspace_size(T, E, k, d, m, n_seg)
+        self.ws = torch.empty((nbytes,), dtype=torch.uint8, device=device)
+
+
+class MoELayer:
+    """One MoE layer's parameters on the device, in reordered expert order."""
+
+    def __init__(self, params: dict, k: int, dtype: str, device="cuda"):
+        self.dt = _TORCH_DT[dtype]
+        self.k = k
+        self.d, self.E = params["w_r"].shape
+        self.m = params["w_down"].shape[2]
+        self.w_r = to_device(params["w_r"], torch.float32, device)
+        self.bias = to_device(params["bias"], torch.float32, device)
+        self.w_gate_up = to_device(params["w_gate_up"], self.dt, device)
+        self.w_down = to_device(params["w_down"], self.dt, device)
+        self.device = device
+        self._bufs: dict = {}
+
+    def buffers(self, T: int, n_seg: int = 1) -> Buffers:
+        key = (T, n_seg)
+        if key not in self._bufs:
+            self._bufs[key] = Buffers(T, self.d, self.E, self.m, self.k, self.dt, n_seg, self.device)
+        return self._bufs[key]
+
+    # -- stages ------------------------------------------------------------
+    # `mark`, if given, is called after each ABI call (e.g. to record events)
+    def _experts(self, x, b: Buffers, idx, w, K_dev=None, stream=None, mark=None):
+        mark = mark or (lambda: None)
+        abi.moe_dispatch(idx, self.E, x, b.counts, b.offsets, b.src_of_row, b.row_of_slot,
+                         b.x_perm, b.ws, stream=stream)
+        mark()
+        abi.moe_expert_ffn(b.x_perm, b.offsets, self.w_gate_up, self.w_down, b.y_perm, b.ws,
+                           K_dev=K_dev, stream=stream)
+        mark()
+        abi.moe_combine(b.y_perm, b.row_of_slot, w, b.out, stream=stream)
+        mark()
+
+    def forward_dense(self, x: torch.Tensor, b: Buffers | None = None, stream=None,
+                      mark=None) -> Buffers:
+        """Full expert pool (layers before the visual exit)."""
+        b = b or self.buffers(x.shape[0])
+        abi.moe_route(x, self.w_r, self.bias, self.k, b.logits, b.idx, b.w, stream=stream)
+        if mark:
+            mark()
+        self._experts(x, b, b.idx, b.w, stream=stream, mark=mark)
+        return b
+
+    def forward_rcep(self, x: torch.Tensor, p: float, seg_offsets=None, b: Buffers | None = None,
+                     stream=None, mark=None) -> Buffers:
+        """Prefix-restricted layer (from the visual exit on, Algorithm 2)."""
+        n_seg = 1 if seg_offsets is None else seg_offsets.numel() - 1
+        b = b or self.buffers(x.shape[0], n_seg)
+        mk = mark or (lambda: None)
+        abi.moe_route(x, self.w_r, self.bias, self.k, b.logits, b.idx_full, b.w_full,
+                      stream=stream)
+        mk()
+        abi.moe_calibrate_prefix(b.idx_full, b.w_full, self.E, p, b.mass, K_out=b.K,
+                                 seg_offsets=seg_offsets, stream=stream)
+        mk()
+        abi.moe_route(None, None, None, self.k, b.logits, b.idx, b.w, seg_offsets=seg_offsets,
+                      K_dev=b.K, stream=stream)
+        mk()
+        self._experts(x, b, b.idx, b.w, K_dev=b.K, stream=stream, mark=mark)
+        return b

@@ -1,0 +1,124 @@
+"""C-ABI contract checks that need no GPU: the library loads, exports every
+function that include/decomoe.h declares, and rejects invalid arguments on
+the host before anything is launched (only rejected calls are made here)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from _util import ROOT, ensure_built
+
+HEADER = os.path.join(ROOT, "include", "decomoe.h")
+EINVAL, EALIAS, EWORKSPACE, EUNSUPPORTED = -1, -2, -3, -5
+F32, BF16 = 0, 1
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    names = re.findall(r"^[A-Za-z_][\w\s\*]*?\b([a-z_][a-z0-9_]*)\s*\(", src, flags=re.M)
+    return sorted(set(n for n in names if n not in ("if", "while", "for")))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return ensure_built()
+
+
+def test_header_declares_the_boundary():
+    assert declared_functions() == sorted([
+        "drop_visual_block", "moe_calibrate_prefix", "moe_combine", "moe_dispatch",
+        "moe_expert_ffn", "moe_route", "moe_status_string", "moe_workspace_size"])
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_binding_names_match_header():
+    from paper_2609_38823_amd import abi
+    assert sorted(abi.EXPORTS) == declared_functions()
+    for name in declared_functions():
+        if name != "moe_status_string":
+            assert callable(getattr(abi, name))
+
+
+def test_status_strings(lib):
+    for code in (0, -1, -2, -3, -4, -5, 7):
+        assert lib.moe_status_string(code)
+
+
+def test_workspace_size(lib):
+    assert lib.moe_workspace_size(4096, 128, 8, 2048, 768, 1) > 4096 * 8 * 768 * 2
+    assert lib.moe_workspace_size(0, 128, 8, 2048, 768, 1) >= 256
+    assert lib.moe_workspace_size(16, 128, 0, 2048, 768, 1) == 0  # k < 1
+    assert lib.moe_workspace_size(16, 2000, 8, 2048, 768, 1) == 0  # E > 1024
+
+
+# fake, never dereferenced, 16-byte aligned addresses
+P1, P2, P3, P4, P5, P6, P7 = (ctypes.c_void_p(0x10000 * i) for i in range(1, 8))
+NULL = None
+
+
+def test_route_rejects(lib):
+    # k > E, E > 1024, k > 32
+    assert lib.moe_route(P1, BF16, P2, NULL, 8, 64, 4, 5, NULL, 1, NULL, P3, P4, P5, NULL) == EINVAL
+    assert lib.moe_route(P1, BF16, P2, NULL, 8, 64, 2000, 5, NULL, 1, NULL, P3, P4, P5, NULL) == EINVAL
+    assert lib.moe_route(P1, BF16, P2, NULL, 8, 64, 128, 33, NULL, 1, NULL, P3, P4, P5, NULL) == EUNSUPPORTED
+    # bf16 rows need d % 8 == 0; logits must be given; misaligned pointer
+    assert lib.moe_route(P1, BF16, P2, NULL, 8, 60, 128, 8, NULL, 1, NULL, P3, P4, P5, NULL) == EINVAL
+    assert lib.moe_route(P1, BF16, P2, NULL, 8, 64, 128, 8, NULL, 1, NULL, NULL, P4, P5, NULL) == EINVAL
+    assert lib.moe_route(ctypes.c_void_p(0x10002), BF16, P2, NULL, 8, 64, 128, 8, NULL, 1, NULL,
+                         P3, P4, P5, NULL) == EINVAL
+    # outputs overlapping inputs: logits on top of x
+    assert lib.moe_route(P1, BF16, P2, NULL, 8, 64, 128, 8, NULL, 1, NULL, P1, P4, P5, NULL) == EALIAS
+    # logits-input mode: topk_w overlapping logits
+    assert lib.moe_route(NULL, F32, NULL, NULL, 8, 0, 128, 8, NULL, 1, NULL, P3, P4, P3, NULL) == EALIAS
+    # T == 0 launches nothing
+    assert lib.moe_route(P1, BF16, P2, NULL, 0, 64, 128, 8, NULL, 1, NULL, P3, P4, P5, NULL) == 0
+
+
+def test_calibrate_rejects(lib):
+    for p in (0.0, -1.0, 1.5, float("nan")):
+        assert lib.moe_calibrate_prefix(P1, P2, 8, 16, 2, NULL, 1, p, P3, P4, NULL, NULL) == EINVAL
+    assert lib.moe_calibrate_prefix(P1, P2, 8, 16, 20, NULL, 1, 0.9, P3, P4, NULL, NULL) == EINVAL
+    assert lib.moe_calibrate_prefix(P1, P2, 8, 16, 2, P5, 0, 0.9, P3, P4, NULL, NULL) == EINVAL
+    assert lib.moe_calibrate_prefix(P1, P2, 8, 16, 2, NULL, 1, 0.9, P1, P4, NULL, NULL) == EALIAS
+
+
+def test_dispatch_rejects(lib):
+    assert lib.moe_dispatch(P1, 8, 2, 16, P2, F32, 32, P3, P4, P5, P6, P7, NULL, 0, NULL) == EWORKSPACE
+    assert lib.moe_dispatch(P1, 8, 2, 16, P2, F32, 32, P3, P4, P5, P6, P7, ctypes.c_void_p(0x900000), 8,
+                            NULL) == EWORKSPACE
+    assert lib.moe_dispatch(P1, 8, 20, 16, P2, F32, 32, P3, P4, P5, P6, P7, NULL, 0, NULL) == EINVAL
+    assert lib.moe_dispatch(P1, 8, 2, 16, P2, F32, 32, P3, P4, P5, P6, P2, ctypes.c_void_p(0x900000),
+                            1 << 20, NULL) == EALIAS
+
+
+def test_ffn_rejects(lib):
+    ws = ctypes.c_void_p(0x1000000)
+    assert lib.moe_expert_ffn(P1, BF16, P2, 16, NULL, 0, 64, 100, 64, P3, P4, P5, ws, 1 << 30, NULL) == EUNSUPPORTED
+    assert lib.moe_expert_ffn(P1, BF16, P2, 16, NULL, 0, 64, 128, 48, P3, P4, P5, ws, 1 << 30, NULL) == EUNSUPPORTED
+    assert lib.moe_expert_ffn(P1, BF16, P2, 16, P6, 0, 64, 128, 64, P3, P4, P5, ws, 1 << 30, NULL) == EINVAL
+    assert lib.moe_expert_ffn(P1, BF16, P2, 16, NULL, 0, 64, 128, 64, P3, P4, P5, ws, 16, NULL) == EWORKSPACE
+    assert lib.moe_expert_ffn(P1, 7, P2, 16, NULL, 0, 64, 128, 64, P3, P4, P5, ws, 1 << 30, NULL) == EINVAL
+
+
+def test_combine_and_drop_reject(lib):
+    assert lib.moe_combine(P1, BF16, P2, P3, 8, 2, 64, P1, NULL) == EALIAS
+    assert lib.moe_combine(P1, BF16, P2, P3, 8, 0, 64, P4, NULL) == EINVAL
+    assert lib.drop_visual_block(P1, BF16, 10, 64, 5, 4, P2, NULL) == EINVAL
+    assert lib.drop_visual_block(P1, BF16, 10, 64, 0, 11, P2, NULL) == EINVAL
+    assert lib.drop_visual_block(P1, BF16, 10, 64, 0, 4, P1, NULL) == EALIAS
+    assert lib.drop_visual_block(P1, BF16, 10, 64, 0, 10, P2, NULL) == 0  # nothing left to copy
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    from paper_2609_38823_amd import abi
+    monkeypatch.setattr(abi, "_lib", None)
+    monkeypatch.setattr(abi, "LIB_PATH", str(tmp_path / "absent.so"))
+    with pytest.raises(RuntimeError, match="missing"):
+        abi.load()
