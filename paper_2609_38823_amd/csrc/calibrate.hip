@@ -1,9 +1,10 @@
 // Activated mass, prefix length and Mean-Mass order (Eqs. 8, 9, 11, 12).
 //
 // One workgroup per invocation (segment).  The segment's renormalised Top-k
-// weights are scattered, 32 tokens at a time, into a dense LDS table
+// weights are scattered, up to 128 tokens per pass, into a dense LDS table
 // [token][expert]; thread e then adds its column to a float64 running sum in
-// ascending token order.  Every expert's mass is therefore one sequential
+// ascending token order.  The next pass's entries are fetched into registers
+// while the current pass is summed.  Every expert's mass is therefore one sequential
 // float64 sum in token order (no atomics, no tree), and the running prefix
 // sum over experts that decides K is sequential too.
 #include "common.hpp"
@@ -12,13 +13,24 @@ namespace decomoe {
 namespace {
 
 constexpr int CAL_THREADS = 256;
-constexpr int CAL_TABLE = 4096;  // doubles in the LDS table (32 KB)
+constexpr int CAL_TABLE = 16384;  // doubles in the dense LDS table (128 KB)
+constexpr int CAL_STAGE = 1024;   // routing entries staged per pass
+constexpr int CAL_EPT = CAL_STAGE / CAL_THREADS;
+
+// Tokens per pass: the table holds sub x E doubles and the stage sub x k entries.
+__host__ __device__ inline int cal_sub(int E, int k) {
+  int s = CAL_TABLE / E;
+  if (s * k > CAL_STAGE) s = CAL_STAGE / k;
+  return s < 128 ? s : 128;
+}
 
 __global__ __launch_bounds__(CAL_THREADS) void segment_mass_kernel(
     const int32_t* __restrict__ idx, const float* __restrict__ w, int T, int E, int k,
     const int32_t* __restrict__ seg_offsets, double p, double* __restrict__ mass,
     int32_t* __restrict__ K_out) {
   __shared__ double table[CAL_TABLE];
+  __shared__ int stage_e[CAL_STAGE];
+  __shared__ float stage_w[CAL_STAGE];
   __shared__ double smass[1024];
   const int seg = blockIdx.x;
   const int tid = threadIdx.x;
@@ -27,35 +39,54 @@ __global__ __launch_bounds__(CAL_THREADS) void segment_mass_kernel(
     lo = clampi(seg_offsets[seg], 0, T);
     hi = clampi(seg_offsets[seg + 1], lo, T);
   }
-  const int sub = CAL_TABLE / E;  // tokens per pass (E <= 1024 => >= 4)
+  const int sub = cal_sub(E, k);
   constexpr int EPT = 1024 / CAL_THREADS;  // experts per thread, at most 4
   double acc[EPT] = {};
 
+  // one pass's entries, prefetched into registers one pass ahead
+  int pe[CAL_EPT];
+  float pw[CAL_EPT];
+  auto fetch = [&](int t0) {
+    const int n = min(sub, hi - t0) * k;
+    const size_t base = (size_t)t0 * k;
+#pragma unroll
+    for (int j = 0; j < CAL_EPT; ++j) {
+      const int i = tid + j * CAL_THREADS;
+      pe[j] = i < n ? idx[base + i] : -1;
+      pw[j] = i < n ? w[base + i] : 0.f;
+    }
+  };
+
   for (int i = tid; i < sub * E; i += CAL_THREADS) table[i] = 0.0;
-  __syncthreads();
+  if (lo < hi) fetch(lo);
   for (int t0 = lo; t0 < hi; t0 += sub) {
     const int nt = min(sub, hi - t0);
-    // scatter: one thread per token of the pass, slots in order
+#pragma unroll
+    for (int j = 0; j < CAL_EPT; ++j) {
+      stage_e[tid + j * CAL_THREADS] = pe[j];
+      stage_w[tid + j * CAL_THREADS] = pw[j];
+    }
+    __syncthreads();
+    if (t0 + sub < hi) fetch(t0 + sub);
+    // one thread per token adds its slots in slot order
     if (tid < nt) {
-      const int t = t0 + tid;
       for (int j = 0; j < k; ++j) {
-        int e = idx[(size_t)t * k + j];
-        if (e >= 0 && e < E) table[tid * E + e] += static_cast<double>(w[(size_t)t * k + j]);
+        const int e = stage_e[tid * k + j];
+        if (e >= 0 && e < E) table[tid * E + e] += static_cast<double>(stage_w[tid * k + j]);
       }
     }
     __syncthreads();
+    // expert columns: one float64 running sum per expert, ascending token
 #pragma unroll
     for (int c = 0; c < EPT; ++c) {
-      int e = tid + c * CAL_THREADS;
+      const int e = tid + c * CAL_THREADS;
       if (e < E)
         for (int r = 0; r < nt; ++r) acc[c] += table[r * E + e];
     }
     __syncthreads();
-    // the scattering thread clears what it wrote
     if (tid < nt) {
-      const int t = t0 + tid;
       for (int j = 0; j < k; ++j) {
-        int e = idx[(size_t)t * k + j];
+        const int e = stage_e[tid * k + j];
         if (e >= 0 && e < E) table[tid * E + e] = 0.0;
       }
     }
@@ -63,7 +94,7 @@ __global__ __launch_bounds__(CAL_THREADS) void segment_mass_kernel(
   }
 #pragma unroll
   for (int c = 0; c < EPT; ++c) {
-    int e = tid + c * CAL_THREADS;
+    const int e = tid + c * CAL_THREADS;
     if (e < E) {
       mass[(size_t)seg * E + e] = acc[c];
       smass[e] = acc[c];

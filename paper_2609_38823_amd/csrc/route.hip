@@ -7,19 +7,103 @@
 namespace decomoe {
 
 // ---------------------------------------------------------------------------
-// logits[T, E] = x[T, d] W_r[d, E] + b, float32 accumulation.
-// Block tile: 32 tokens x 64 experts, k-step 32; 256 threads, each thread
-// owns 2 tokens x 4 experts.  x (bf16 or f32) is widened to f32 in LDS.
+// logits[T, E] = x[T, d] W_r[d, E] + b on float32 MFMA (v_mfma_f32_16x16x4f32).
+// Workgroup tile: 16 tokens x 64 experts; the four wavefronts split the
+// d-range into quarters and their partial tiles are added in LDS in the
+// fixed order w0 + w1 + w2 + w3 (deterministic).  Within a 32-wide k chunk
+// lane l (token l%16, lane group q = l/16) loads 8 consecutive x values and
+// MFMA step s consumes k = 8q + s on both operands, so each x row is read
+// with one 16-byte (bf16) or two 16-byte (f32) loads per chunk.
+// Needs d % 128 == 0 (four quarters of whole chunks).
 // ---------------------------------------------------------------------------
 namespace {
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+constexpr int RM_T = 16, RM_E = 64;
+
+template <bool XBF16>
+__global__ __launch_bounds__(256) void router_logits_mfma_kernel(const void* __restrict__ xv,
+                                                                 const float* __restrict__ w_r,
+                                                                 const float* __restrict__ bias,
+                                                                 int T, int d, int E,
+                                                                 float* __restrict__ logits) {
+  __shared__ f32x4 part[4][4][64];  // [wave][n-frag][lane]
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int e0 = blockIdx.x * RM_E, t0 = blockIdx.y * RM_T;
+  const int q = lane >> 4, r16 = lane & 15;
+  const int t = min(t0 + r16, T - 1);  // padding tokens re-read the last row
+  const int quarter = d >> 2;
+  const int kb = wv * quarter, ke = kb + quarter;
+  int ecol[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) ecol[j] = min(e0 + j * 16 + r16, E - 1);
+
+  f32x4 acc[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int k0 = kb; k0 < ke; k0 += 32) {
+    const int kk = k0 + 8 * q;
+    float xa[8];
+    if constexpr (XBF16) {
+      const uint4 v = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(xv) + (size_t)t * d + kk);
+      const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        xa[2 * i] = __uint_as_float(u[i] << 16);
+        xa[2 * i + 1] = __uint_as_float(u[i] & 0xffff0000u);
+      }
+    } else {
+      const float4* src = reinterpret_cast<const float4*>(static_cast<const float*>(xv) + (size_t)t * d + kk);
+      const float4 a0 = src[0], a1 = src[1];
+      xa[0] = a0.x; xa[1] = a0.y; xa[2] = a0.z; xa[3] = a0.w;
+      xa[4] = a1.x; xa[5] = a1.y; xa[6] = a1.z; xa[7] = a1.w;
+    }
+    float wb[4][8];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int s = 0; s < 8; ++s) wb[j][s] = w_r[(size_t)(kk + s) * E + ecol[j]];
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[s], wb[j][s], acc[j], 0, 0, 0);
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) part[wv][j][lane] = acc[j];
+  __syncthreads();
+  // 4 n-frags x 64 lanes = 256 threads; each adds the four quarters in order
+  {
+    const int j = threadIdx.x >> 6, l = threadIdx.x & 63;
+    f32x4 s = part[0][j][l];
+    s += part[1][j][l];
+    s += part[2][j][l];
+    s += part[3][j][l];
+    const int e = e0 + j * 16 + (l & 15);
+    if (e < E) {
+      const float b = bias ? bias[e] : 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int tt = t0 + 4 * (l >> 4) + i;
+        if (tt < T) logits[(size_t)tt * E + e] = s[i] + b;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Fallback for d % 128 != 0: LDS-tiled float32 SIMT kernel, 32 tokens x 64
+// experts per workgroup, 2 x 4 outputs per thread.  Loads are clamped to
+// valid addresses instead of branched around.
+// ---------------------------------------------------------------------------
 constexpr int RT_T = 32, RT_E = 64, RT_K = 32;
 
 template <bool XBF16>
-__global__ __launch_bounds__(256) void router_logits_kernel(const void* __restrict__ xv,
-                                                            const float* __restrict__ w_r,
-                                                            const float* __restrict__ bias,
-                                                            int T, int d, int E,
-                                                            float* __restrict__ logits) {
+__global__ __launch_bounds__(256) void router_logits_simt_kernel(const void* __restrict__ xv,
+                                                                 const float* __restrict__ w_r,
+                                                                 const float* __restrict__ bias,
+                                                                 int T, int d, int E,
+                                                                 float* __restrict__ logits) {
   __shared__ float xs[RT_K][RT_T + 4];  // transposed: xs[k][token]
   __shared__ float wsm[RT_K][RT_E + 4];
   const int tid = threadIdx.x;
@@ -28,34 +112,31 @@ __global__ __launch_bounds__(256) void router_logits_kernel(const void* __restri
   float acc[2][4] = {};
 
   for (int k0 = 0; k0 < d; k0 += RT_K) {
-    // x tile: 32 tokens x 32 k = 1024 values, 4 per thread
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      int lin = i * 256 + tid;
-      int tt = lin >> 5, kk = lin & 31;
-      int t = t0 + tt, kg = k0 + kk;
-      float v = 0.f;
-      if (t < T && kg < d) {
-        if constexpr (XBF16)
-          v = bf16_to_f32(static_cast<const uint16_t*>(xv)[(size_t)t * d + kg]);
-        else
-          v = static_cast<const float*>(xv)[(size_t)t * d + kg];
-      }
-      xs[kk][tt] = v;
+      const int lin = i * 256 + tid;
+      const int tt = lin >> 5, kk = lin & 31;
+      const int t = min(t0 + tt, T - 1), kg = min(k0 + kk, d - 1);
+      float v;
+      if constexpr (XBF16)
+        v = bf16_to_f32(static_cast<const uint16_t*>(xv)[(size_t)t * d + kg]);
+      else
+        v = static_cast<const float*>(xv)[(size_t)t * d + kg];
+      xs[kk][tt] = (k0 + kk < d) ? v : 0.f;
     }
-    // W tile: 32 k x 64 experts = 2048 values, 8 per thread, coalesced rows
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      int lin = i * 256 + tid;
-      int kk = lin >> 6, ee = lin & 63;
-      int kg = k0 + kk, e = e0 + ee;
-      wsm[kk][ee] = (kg < d && e < E) ? w_r[(size_t)kg * E + e] : 0.f;
+      const int lin = i * 256 + tid;
+      const int kk = lin >> 6, ee = lin & 63;
+      const int kg = min(k0 + kk, d - 1), e = min(e0 + ee, E - 1);
+      const float v = w_r[(size_t)kg * E + e];
+      wsm[kk][ee] = (k0 + kk < d) ? v : 0.f;
     }
     __syncthreads();
 #pragma unroll 8
     for (int kk = 0; kk < RT_K; ++kk) {
-      float2 a = *reinterpret_cast<const float2*>(&xs[kk][ty * 2]);
-      float4 b = *reinterpret_cast<const float4*>(&wsm[kk][tx * 4]);
+      const float2 a = *reinterpret_cast<const float2*>(&xs[kk][ty * 2]);
+      const float4 b = *reinterpret_cast<const float4*>(&wsm[kk][tx * 4]);
       acc[0][0] = fmaf(a.x, b.x, acc[0][0]);
       acc[0][1] = fmaf(a.x, b.y, acc[0][1]);
       acc[0][2] = fmaf(a.x, b.z, acc[0][2]);
@@ -69,11 +150,11 @@ __global__ __launch_bounds__(256) void router_logits_kernel(const void* __restri
   }
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
-    int t = t0 + ty * 2 + i;
+    const int t = t0 + ty * 2 + i;
     if (t >= T) continue;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      int e = e0 + tx * 4 + j;
+      const int e = e0 + tx * 4 + j;
       if (e < E) logits[(size_t)t * E + e] = acc[i][j] + (bias ? bias[e] : 0.f);
     }
   }
@@ -143,11 +224,19 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ log
 
 hipError_t launch_router_logits(const void* x, bool x_bf16, const float* w_r, const float* bias,
                                 int T, int d, int E, float* logits, hipStream_t s) {
-  dim3 grid((E + RT_E - 1) / RT_E, (T + RT_T - 1) / RT_T);
-  if (x_bf16)
-    router_logits_kernel<true><<<grid, 256, 0, s>>>(x, w_r, bias, T, d, E, logits);
-  else
-    router_logits_kernel<false><<<grid, 256, 0, s>>>(x, w_r, bias, T, d, E, logits);
+  if (d % 128 == 0) {
+    dim3 grid((E + RM_E - 1) / RM_E, (T + RM_T - 1) / RM_T);
+    if (x_bf16)
+      router_logits_mfma_kernel<true><<<grid, 256, 0, s>>>(x, w_r, bias, T, d, E, logits);
+    else
+      router_logits_mfma_kernel<false><<<grid, 256, 0, s>>>(x, w_r, bias, T, d, E, logits);
+  } else {
+    dim3 grid((E + RT_E - 1) / RT_E, (T + RT_T - 1) / RT_T);
+    if (x_bf16)
+      router_logits_simt_kernel<true><<<grid, 256, 0, s>>>(x, w_r, bias, T, d, E, logits);
+    else
+      router_logits_simt_kernel<false><<<grid, 256, 0, s>>>(x, w_r, bias, T, d, E, logits);
+  }
   return hipGetLastError();
 }
 

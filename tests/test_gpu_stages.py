@@ -138,11 +138,21 @@ def robust_tokens(a_ref, k, delta):
     return (-np.diff(srt, axis=1)).min(axis=1) > 2 * delta
 
 
-@pytest.mark.parametrize("name,T", [("tiny_f32", 512), ("tiny_f32", 37), ("qwen3vl_dense_4096", 4096),
-                                    ("qwen3vl_dense_4096", 77)])
+ODD_F32 = I.LayerShape(d=40, E=24, m=8, k=3, dtype="f32", zipf_alpha=0.35)
+ODD_BF16 = I.LayerShape(d=104, E=200, m=8, k=8, dtype="bf16", zipf_alpha=0.35)
+ROUTER_CASES = [("tiny_f32", 512), ("tiny_f32", 37), ("qwen3vl_dense_4096", 4096),
+                ("qwen3vl_dense_4096", 77), ("qwen3vl_rcep_512", 1), ("odd_f32", 99), ("odd_bf16", 333)]
+
+
+@pytest.mark.parametrize("name,T", ROUTER_CASES)
 def test_router_logits_and_free_running_topk(name, T):
-    wl = I.WORKLOADS[name]
-    sh = wl.shape
+    if name == "odd_f32":
+        wl, sh = I.Workload(name, ODD_F32, T, 0, 0.9), ODD_F32
+    elif name == "odd_bf16":
+        wl, sh = I.Workload(name, ODD_BF16, T, 0, 0.9), ODD_BF16
+    else:
+        wl = I.WORKLOADS[name]
+        sh = wl.shape
     rp = I.router_params(sh, seed=wl.seed)
     x = I.tokens(sh, T, seed=wl.seed)
     logits, idx, w = f32((T, sh.E)), i32((T, sh.k)), f32((T, sh.k))
