@@ -175,7 +175,7 @@ int moe_dispatch(const int32_t* topk_idx, int T, int k, int E,
  * intermediate SiLU(g)*u is formed in float32 and rounded once to dtype
  * before the down projection; y is rounded once to dtype.  float32 inputs
  * use float32 arithmetic throughout.
- * Limits (bf16): d % 128 == 0 and m % 64 == 0, else MOE_EUNSUPPORTED.
+ * Limits (bf16): d % 256 == 0 and m % 128 == 0, else MOE_EUNSUPPORTED.
  * Offsets are clamped to [0, rows_max].  Needs ws.
  */
 int moe_expert_ffn(const void* x_perm, moe_dtype dtype, const int32_t* offsets, int E,

@@ -159,7 +159,9 @@ int moe_expert_ffn(const void* x_perm, moe_dtype dtype, const int32_t* offsets, 
   if (!offsets || !w_gate_up || !w_down) return MOE_EINVAL;
   if (rows_max > 0 && (!x_perm || !y_perm)) return MOE_EINVAL;
   const bool bf16 = dtype == MOE_BF16;
-  if (bf16 && (d % 128 != 0 || m % 64 != 0)) return MOE_EUNSUPPORTED;
+  if (bf16 && (d % 256 != 0 || m % 128 != 0)) return MOE_EUNSUPPORTED;
+  // the GEMM addresses one expert's weights with 32-bit buffer offsets
+  if ((size_t)2 * m * d * elt_size(dtype) > (size_t)INT32_MAX) return MOE_EUNSUPPORTED;
   if (!aligned_all({x_perm, offsets, K_dev, w_gate_up, w_down, y_perm, ws})) return MOE_EINVAL;
   if (rows_max == 0) return MOE_OK;
   const size_t need = ffn_ws_bytes(bf16, rows_max, E, d, m);

@@ -24,19 +24,24 @@ namespace kern {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-struct Tile {
-  int expert, row0, rows, pad;
-};
 
 // ---------------------------------------------------------------------------
 // M-tile list.  Experts e < Klim with rows [offsets[e], offsets[e+1]) (clamped
-// to [0, rows_max]) become ceil(rows / bm) tiles, expert-major.
+// to [0, rows_max]) become ceil(rows / bm) tiles, expert-major.  For each of
+// the two GEMMs (nn0, nn1 n-tiles) it also writes the work list: one item per
+// (m-tile, n-tile), ordered expert-major, then n-tile, then m-tile, so that a
+// workgroup needs a single load to know its work.
 // ---------------------------------------------------------------------------
+struct Work {
+  int expert, row0, rows, nt;
+};
+
 __global__ __launch_bounds__(1024) void ffn_tiles_kernel(const int32_t* __restrict__ offsets,
                                                          int E, const int32_t* __restrict__ K_dev,
-                                                         int n_K, int rows_max, int bm,
-                                                         Tile* __restrict__ tiles, int max_tiles,
-                                                         int32_t* __restrict__ n_tiles) {
+                                                         int n_K, int rows_max, int bm, int max_tiles,
+                                                         int nn0, int nn1, Work* __restrict__ work0,
+                                                         Work* __restrict__ work1,
+                                                         int32_t* __restrict__ n_work) {
   __shared__ int sc[1024];
   const int e = threadIdx.x;
   int Klim = E;
@@ -59,48 +64,68 @@ __global__ __launch_bounds__(1024) void ffn_tiles_kernel(const int32_t* __restri
     sc[e] += v;
     __syncthreads();
   }
+  const int total = min(sc[1023], max_tiles);
   const int start = sc[e] - nt;
-  for (int i = 0; i < nt; ++i) {
-    int ti = start + i;
-    if (ti < max_tiles) {
-      int r0 = lo + i * bm;
-      tiles[ti] = Tile{e, r0, min(bm, hi - r0), 0};
-    }
+  const int cnt = max(0, min(nt, total - start));  // tiles of this expert kept
+  for (int o = 0; o < nn0 * cnt; ++o) {
+    const int mt = o % cnt, r0 = lo + mt * bm;
+    work0[nn0 * start + o] = Work{e, r0, min(bm, hi - r0), o / cnt};
   }
-  if (e == 1023) *n_tiles = min(sc[1023], max_tiles);
+  for (int o = 0; o < nn1 * cnt; ++o) {
+    const int mt = o % cnt, r0 = lo + mt * bm;
+    work1[nn1 * start + o] = Work{e, r0, min(bm, hi - r0), o / cnt};
+  }
+  if (e == 1023) {
+    n_work[0] = total * nn0;
+    n_work[1] = total * nn1;
+  }
 }
 
 // ---------------------------------------------------------------------------
 // bf16 MFMA grouped GEMM
 //
-// Block tile BM rows x BN weight rows, k-step 64; 4 wavefronts in 2 x 2, each
-// owning (BM/2) x (BN/2) outputs as 16x16 fragments of
-// v_mfma_f32_16x16x32_bf16.  Operand tiles stream from global memory straight
-// into LDS with global_load_lds_dwordx4 through a 3-stage ring (three
-// separate LDS arrays, so the compiler's wait tracking keeps the two younger
-// stages in flight while the oldest is consumed).  Each 128-byte LDS row holds
-// one tile row's 64 k-values as eight 16-byte chunks, chunk c stored at
-// position c ^ ((row >> 1) & 7): the 16 rows read by one quarter-wavefront
-// then hit 16 distinct bank groups.
+// Block tile BM token rows x BN weight rows, k-step 32; the 4 wavefronts
+// split the weight rows, so each owns BM x (BN/4) outputs as 32x32 fragments
+// of v_mfma_f32_32x32x16_bf16 (float32 accumulation; BM = 128, BN = 512
+// gives 128x128 per wavefront, 256 accumulator registers, and 64 bytes of
+// LDS reads per 32 MFMA cycles -- half the LDS bandwidth of a 64x64 tile).
+// Operand tiles stream from global memory straight into LDS with
+// buffer_load_dwordx4 ... lds through a 3-stage ring of separate LDS arrays
+// (the compiler's wait tracking then keeps the younger stage in flight while
+// the oldest is consumed).  Each 64-byte LDS row holds one tile row's 32
+// k-values as four 16-byte chunks, chunk c stored at position
+// c ^ ((row >> 2) & 3): the 16 rows read by one quarter-wavefront hit 16
+// distinct bank groups.  The two 16-wide k-substeps of a stage are
+// software-pipelined in registers.
 // ---------------------------------------------------------------------------
-constexpr int BK = 64, NTHR = 256, STAGES = 3;
-constexpr int LDS_STAGE_MAX = (128 + 256) * BK * 2;  // bytes, largest tile pair
+constexpr int BK = 32, NTHR = 256;
+constexpr int LDS_STAGE_MAX = (128 + 512) * BK * 2;  // bytes, largest tile pair
 
 __shared__ __attribute__((aligned(1024))) char ring0[LDS_STAGE_MAX];
 __shared__ __attribute__((aligned(1024))) char ring1[LDS_STAGE_MAX];
 __shared__ __attribute__((aligned(1024))) char ring2[LDS_STAGE_MAX];
 
-__device__ __forceinline__ int swz_off(int row, int chunk) {
-  return row * 128 + ((chunk ^ ((row >> 1) & 7)) << 4);
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// SiLU(g) * u with the hardware exp2 and reciprocal (about 1 ulp each; the
+// result is rounded to bf16 afterwards)
+__device__ __forceinline__ float swiglu_f(float g, float u) {
+  const float e = __builtin_amdgcn_exp2f(-g * 1.4426950408889634f);
+  return g * __builtin_amdgcn_rcpf(1.f + e) * u;
 }
 
-__device__ __forceinline__ float silu_f(float g) { return g / (1.f + expf(-g)); }
+// 16-byte buffer -> LDS copy per lane (buffer_load_dwordx4 ... lds): lane l
+// writes lds + 16 l, reading rsrc.base + voff + soff.  A non-template wrapper:
+// the host compilation pass rejects this builtin inside a kernel template.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, void* lds_wave_base, int voff,
+                                      int soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, lds_wave_base, 16, voff, soff, 0, 0);
+}
 
-// 16-byte global -> LDS copy per lane (global_load_lds_dwordx4): lane l writes
-// lds + 16 l.  A non-template wrapper: the host compilation pass rejects this
-// builtin inside a kernel template.
-__device__ __forceinline__ void dma16(const void* gsrc, void* lds_wave_base) {
-  __builtin_amdgcn_global_load_lds(gsrc, lds_wave_base, 16, 0, 0);
+// raw buffer resource over [base, base + bytes); dword3 is the CDNA raw-buffer
+// format (32-bit data, no swizzle)
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
 }
 
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
@@ -111,131 +136,123 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
-template <int MODE, int BM, int BN>
-struct GemmCfg {
-  static constexpr int MI = BM / 32;         // 16-row fragments per wave
-  static constexpr int NI = BN / 32;         // 16-col fragments per wave
-  static constexpr int ROWS = BM + BN;       // LDS rows per stage (A then B)
-  static constexpr int GROUPS = ROWS / 8;    // 1 KB DMA groups per stage
-  static constexpr int GPW = GROUPS / 4;     // DMA instructions per wave per stage
-  static_assert(GROUPS % 4 == 0, "stage must split evenly over 4 waves");
-  static_assert(ROWS * 128 <= LDS_STAGE_MAX, "stage too large");
-};
-
 // MODE 0: A = x_perm [rows, d], W = w_gate_up [E, 2m, d], C = h [rows, m];
 //         the B tile's first BN/2 rows are gate rows nt*BN/2.., the rest the
-//         matching up rows m + nt*BN/2..; C gets BN/2 columns
+//         matching up rows m + nt*BN/2..; C gets BN/2 columns.  Wavefront w
+//         owns h columns [w BN/8, (w+1) BN/8) of the tile: its gate and up
+//         fragments hold the same (row, column) in the same registers.
 // MODE 1: A = h [rows, m], W = w_down [E, d, m], C = y_perm [rows, d];
-//         B rows nt*BN.., C gets BN columns
-template <int MODE, int BM, int BN>
+//         B rows nt*BN.., C gets BN columns; wavefront w owns [w BN/4, ..).
+template <int MODE, int BM, int BN, int TAIL>
 __global__ __launch_bounds__(NTHR, 1) void ffn_gemm_bf16_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ W, uint16_t* __restrict__ C,
-    const Tile* __restrict__ tiles, const int32_t* __restrict__ n_tiles, int d, int m,
-    int n_tiles_n) {
-  using Cfg = GemmCfg<MODE, BM, BN>;
-  constexpr int MI = Cfg::MI, NI = Cfg::NI, GPW = Cfg::GPW;
+    const Work* __restrict__ work, const int32_t* __restrict__ n_work, int d, int m) {
+  constexpr int MI = BM / 32;             // 32-row fragments per wave (all tile rows)
+  constexpr int NI = BN / 128;            // 32-col fragments per wave
+  constexpr int AG = BM / 16;             // 1 KB DMA groups (16 rows) of the A tile
+  constexpr int BG = BN / 16;
+  constexpr int GPW = (AG + BG) / 4;      // DMA instructions per wave per stage
+  static_assert(AG % 4 == 0 && BG % 8 == 0, "groups split over 4 waves");
+  static_assert(MODE == 1 || NI % 2 == 0, "gate/up fragments come in pairs");
+  static_assert((BM + BN) * BK * 2 <= LDS_STAGE_MAX, "stage too large");
 
-  const int nt = blockIdx.x % n_tiles_n;
-  const int mt = blockIdx.x / n_tiles_n;
-  if (mt >= *n_tiles) return;
-  const Tile tile = tiles[mt];
+  // XCD-aware order.  Workgroup b runs on XCD b % 8, so XCD x is given the
+  // contiguous range [x n/8, (x+1) n/8) of the n-item work list
+  // (expert-major, then n-tile, then m-tile): the m-tiles that share a
+  // weight tile, and the n-tiles that share an expert's rows, run together
+  // and meet in one L2, and every XCD gets an equal share.
+  const int nw = n_work[MODE];
+  const int per_xcd = (nw + 7) >> 3;
+  const int slot = blockIdx.x >> 3;
+  if (slot >= per_xcd) return;
+  const int L = (blockIdx.x & 7) * per_xcd + slot;
+  if (L >= nw) return;
+  const Work wk = work[L];
+  const int nt = wk.nt;
   const int Kdim = MODE == 0 ? d : m;
   const int ldc = MODE == 0 ? m : d;
-  const uint16_t* Wexp = W + (size_t)tile.expert * (size_t)(MODE == 0 ? 2 * m : d) * Kdim;
+  const uint16_t* Wexp = W + (size_t)wk.expert * (size_t)(MODE == 0 ? 2 * m : d) * Kdim;
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wv = tid >> 6;
-  const int wm = wv >> 1, wn = wv & 1;
-  const int r16 = lane & 15, kq = lane >> 4;
+  const int lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-  // ---- DMA source pointers: this lane's row and swizzled chunk per group --
-  // group g (8 rows) of the stage: rows [8g, 8g+8); lane -> row 8g + lane/8,
-  // LDS chunk lane%8, global chunk (lane%8) ^ ((row >> 1) & 7)
-  const uint16_t* src[GPW];
+  // ---- DMA: group g = 16 rows x 64 bytes; wave wv issues groups wv, wv+4, ...
+  // of the A tile and of the B tile; lane -> row 16 g + lane/4, LDS chunk
+  // lane%4, global chunk (lane%4) ^ ((row >> 2) & 3) -- the same for every
+  // group of a lane since groups start at multiples of 16 rows.  Per-lane
+  // byte offsets go in VGPRs; k and the group's row offset in the scalar
+  // offset.
+  const int lrow = lane >> 2;
+  const int swz_c = (lane & 3) ^ ((lrow >> 2) & 3);
+  // A: rows of this tile; padding rows (past wk.rows) re-read row 0
+  const __amdgpu_buffer_rsrc_t a_rs = make_rsrc(A + (size_t)wk.row0 * Kdim, (uint32_t)wk.rows * Kdim * 2);
+  int a_voff[AG / 4];
 #pragma unroll
-  for (int q = 0; q < GPW; ++q) {
-    const int g = wv * GPW + q;
-    const int r = g * 8 + (lane >> 3);
-    const int c = (lane & 7) ^ ((r >> 1) & 7);
-    const uint16_t* rowp;
-    if (r < BM) {
-      const int rr = r < tile.rows ? r : 0;  // padding rows re-read row 0
-      rowp = A + (size_t)(tile.row0 + rr) * Kdim;
-    } else {
-      const int b = r - BM;
-      int wrow;
-      if (MODE == 0)
-        wrow = b < BN / 2 ? nt * (BN / 2) + b : m + nt * (BN / 2) + (b - BN / 2);
-      else
-        wrow = nt * BN + b;
-      rowp = Wexp + (size_t)wrow * Kdim;
-    }
-    src[q] = rowp + c * 8;
+  for (int q = 0; q < AG / 4; ++q) {
+    const int r = wv * 16 + lrow + 64 * q;
+    a_voff[q] = ((r < wk.rows ? r : 0) * Kdim + swz_c * 8) * 2;
   }
+  // B: the expert's weight matrix; for MODE 0 the up half (groups
+  // q >= BG/8) lives m - BN/2 rows further down
+  const int ncolsW = MODE == 0 ? 2 * m : d;
+  const __amdgpu_buffer_rsrc_t b_rs = make_rsrc(Wexp, (uint32_t)ncolsW * Kdim * 2);
+  const int b_voff = (((MODE == 0 ? nt * (BN / 2) : nt * BN) + wv * 16 + lrow) * Kdim + swz_c * 8) * 2;
+  const int b_step = 64 * Kdim * 2;
+  const int b_jump = MODE == 0 ? (m - BN / 2) * Kdim * 2 : 0;
 
   auto issue = [&](char* stage, int k0) {
 #pragma unroll
-    for (int q = 0; q < GPW; ++q) {
-      const int g = wv * GPW + q;
-      dma16(src[q] + k0, stage + g * 1024);
-    }
+    for (int q = 0; q < AG / 4; ++q) dma16(a_rs, stage + (wv + 4 * q) * 1024, a_voff[q], k0 * 2);
+#pragma unroll
+    for (int q = 0; q < BG / 4; ++q)
+      dma16(b_rs, stage + BM * 64 + (wv + 4 * q) * 1024, b_voff,
+            q * b_step + (q >= BG / 8 ? b_jump : 0) + k0 * 2);
   };
 
-  f32x4 acc[MI][NI];
+  f32x16 acc[MI][NI];
 #pragma unroll
   for (int i = 0; i < MI; ++i)
 #pragma unroll
-    for (int j = 0; j < NI; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < NI; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  // LDS byte offsets of this lane's fragment rows (chunk applied per k-step)
-  int arow[MI], brow[NI];
-#pragma unroll
-  for (int mi = 0; mi < MI; ++mi) arow[mi] = wm * (BM / 2) + mi * 16 + r16;
-#pragma unroll
-  for (int ni = 0; ni < NI; ++ni) {
+  // ---- fragments.  32x32x16: lane l supplies row (l % 32), k = 8 (l / 32)
+  // .. +8 of its substep, i.e. chunk 2 s + l/32 of the stage.  Fragment row
+  // groups start at multiples of 32 rows, so the swizzle term is
+  // ((l % 32) >> 2) & 3 for all of them: one per-lane base per substep.
+  const int r32 = lane & 31, kh = lane >> 5;
+  const int sw = (r32 >> 2) & 3;
+  const int lane_off0 = r32 * 64 + ((kh ^ sw) << 4);
+  const int lane_off1 = r32 * 64 + (((2 + kh) ^ sw) << 4);
+  auto brow0 = [&](int ni) {
     int b;
     if (MODE == 0)  // half gate, half up, same h columns
-      b = ni < NI / 2 ? wn * (BN / 4) + ni * 16 : BN / 2 + wn * (BN / 4) + (ni - NI / 2) * 16;
+      b = ni < NI / 2 ? wv * (BN / 8) + ni * 32 : BN / 2 + wv * (BN / 8) + (ni - NI / 2) * 32;
     else
-      b = wn * (BN / 2) + ni * 16;
-    brow[ni] = BM + b + r16;
-  }
-
-  // fragments of k-substep ks (32 k-values): 16 bytes per lane per fragment
-  auto load_frags = [&](const char* stage, int ks, bf16x8 (&af)[MI], bf16x8 (&bfr)[NI]) {
-    const int c = ks * 4 + kq;
+      b = wv * (BN / 4) + ni * 32;
+    return (BM + b) * 64;
+  };
+  auto load_frags = [&](const char* stage, int s, bf16x8 (&af)[MI], bf16x8 (&bfr)[NI]) {
+    const char* base = stage + (s ? lane_off1 : lane_off0);
 #pragma unroll
-    for (int mi = 0; mi < MI; ++mi)
-      af[mi] = *reinterpret_cast<const bf16x8*>(stage + swz_off(arow[mi], c));
+    for (int mi = 0; mi < MI; ++mi) af[mi] = *reinterpret_cast<const bf16x8*>(base + mi * 32 * 64);
 #pragma unroll
-    for (int ni = 0; ni < NI; ++ni)
-      bfr[ni] = *reinterpret_cast<const bf16x8*>(stage + swz_off(brow[ni], c));
+    for (int ni = 0; ni < NI; ++ni) bfr[ni] = *reinterpret_cast<const bf16x8*>(base + brow0(ni));
   };
   auto mma = [&](const bf16x8 (&af)[MI], const bf16x8 (&bfr)[NI]) {
 #pragma unroll
     for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
       for (int ni = 0; ni < NI; ++ni)
-        acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[mi], bfr[ni], acc[mi][ni], 0, 0, 0);
+        acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[ni], af[mi], acc[mi][ni], 0, 0, 0);
   };
-  // k-substep 0's fragments are read first; substep 1's twelve reads are
-  // issued one after each of substep 0's first MFMAs, so at most 15 LDS reads
-  // are outstanding (the counter limit) and they land under the MFMAs
   auto compute = [&](const char* stage) {
     bf16x8 a0[MI], b0[NI], a1[MI], b1[NI];
     load_frags(stage, 0, a0, b0);
-    __builtin_amdgcn_sched_barrier(0);
-    const int c1 = 4 + kq;
-#pragma unroll
-    for (int j = 0; j < MI * NI; ++j) {
-      acc[j / NI][j % NI] =
-          __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0[j / NI], b0[j % NI], acc[j / NI][j % NI], 0, 0, 0);
-      if (j < MI)
-        a1[j] = *reinterpret_cast<const bf16x8*>(stage + swz_off(arow[j], c1));
-      else if (j < MI + NI)
-        b1[j - MI] = *reinterpret_cast<const bf16x8*>(stage + swz_off(brow[j - MI], c1));
-      __builtin_amdgcn_sched_barrier(0);
-    }
+    load_frags(stage, 1, a1, b1);
+    mma(a0, b0);
     mma(a1, b1);
   };
 
@@ -249,7 +266,6 @@ __global__ __launch_bounds__(NTHR, 1) void ffn_gemm_bf16_kernel(
     issue(nxt, (it + 2) * BK);
     compute(cur);
   };
-  // drain steps: nothing left to issue
   auto step_tail = [&](char* cur, bool last) {
     if (last)
       wait_vmcnt<0>();
@@ -259,10 +275,7 @@ __global__ __launch_bounds__(NTHR, 1) void ffn_gemm_bf16_kernel(
     compute(cur);
   };
 
-  if (nk < 2) {  // a single k-step: no pipeline
-    issue(ring0, 0);
-    step_tail(ring0, true);
-  } else {
+  // nk >= 4: the entry point requires d and m to be multiples of 128
   issue(ring0, 0);
   issue(ring1, BK);
   int it = 0;
@@ -271,65 +284,63 @@ __global__ __launch_bounds__(NTHR, 1) void ffn_gemm_bf16_kernel(
     step_issue(it + 1, ring1, ring0);
     step_issue(it + 2, ring2, ring1);
   }
-  // 1 to 4 iterations remain (it is a multiple of 3, so rings are static)
-  const int rem = nk - it;
-  if (rem >= 3) {
+  // TAIL = (nk - 2) % 3, fixed per instantiation, so the last 2 + TAIL
+  // iterations have static rings and a single code path
+  if (TAIL == 2) {
     step_issue(it, ring0, ring2);
-    if (rem == 4) {
-      step_issue(it + 1, ring1, ring0);
-      step_tail(ring2, false);
-      step_tail(ring0, true);
-    } else {
-      step_tail(ring1, false);
-      step_tail(ring2, true);
-    }
-  } else if (rem == 2) {
+    step_issue(it + 1, ring1, ring0);
+    step_tail(ring2, false);
+    step_tail(ring0, true);
+  } else if (TAIL == 1) {
+    step_issue(it, ring0, ring2);
+    step_tail(ring1, false);
+    step_tail(ring2, true);
+  } else {
     step_tail(ring0, false);
     step_tail(ring1, true);
-  } else if (rem == 1) {
-    step_tail(ring0, true);
-  }
   }
 
-  // ---- epilogue: bf16 tile staged in LDS, then 16-byte coalesced stores ----
-  __syncthreads();  // every wave is done reading the ring
-  uint16_t* ctile = reinterpret_cast<uint16_t*>(ring0);
-  constexpr int CW = MODE == 0 ? BN / 2 : BN;  // output columns of the tile
-  if (MODE == 0) {
+  // ---- epilogue.  The weight fragment is the MFMA's first operand, so
+  // acc[mi][ni] = W_frag X_frag^T: lane l holds token row mi*32 + l%32 and,
+  // for e = 4g + t, output column 8g + 4(l/32) + t of the fragment -- four
+  // consecutive columns per g.  Each wave stages its 32-row slices through
+  // its own LDS region with 8-byte writes and stores full 16-byte chunks.
+  __syncthreads();  // every wave is done with the ring
+  constexpr int FO = MODE == 0 ? NI / 2 : NI;  // output fragments per wave
+  constexpr int CWV = FO * 32;                 // output columns per wave
+  constexpr int RS = CWV * 2 + 16;             // padded LDS row stride (bytes)
+  static_assert(4 * 32 * RS <= LDS_STAGE_MAX, "epilogue staging fits in one ring stage");
+  char* reg = ring0 + wv * 32 * RS;
+  const int colbase = MODE == 0 ? nt * (BN / 2) + wv * (BN / 8) : nt * BN + wv * (BN / 4);
 #pragma unroll
-    for (int mi = 0; mi < MI; ++mi)
+  for (int mi = 0; mi < MI; ++mi) {
 #pragma unroll
-      for (int f = 0; f < NI / 2; ++f)
+    for (int f = 0; f < FO; ++f)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = wm * (BM / 2) + mi * 16 + kq * 4 + i;
-          const int col = wn * (BN / 4) + f * 16 + r16;
-          const float hv = silu_f(acc[mi][f][i]) * acc[mi][f + NI / 2][i];
-          ctile[row * CW + col] = f32_to_bf16(hv);
-        }
-  } else {
+      for (int g = 0; g < 4; ++g) {
+        float v[4];
 #pragma unroll
-    for (int mi = 0; mi < MI; ++mi)
+        for (int t = 0; t < 4; ++t)
+          v[t] = MODE == 0 ? swiglu_f(acc[mi][f][4 * g + t], acc[mi][f + NI / 2][4 * g + t])
+                           : acc[mi][f][4 * g + t];
+        const uint2 pk = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+        *reinterpret_cast<uint2*>(reg + r32 * RS + (f * 32 + 8 * g + 4 * kh) * 2) = pk;
+      }
+    // read back row-major 16-byte chunks (same wave: LDS order suffices)
+    constexpr int CPR = CWV / 8;  // chunks per row
 #pragma unroll
-      for (int ni = 0; ni < NI; ++ni)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = wm * (BM / 2) + mi * 16 + kq * 4 + i;
-          const int col = wn * (BN / 2) + ni * 16 + r16;
-          ctile[row * CW + col] = f32_to_bf16(acc[mi][ni][i]);
-        }
-  }
-  __syncthreads();
-  constexpr int CPR = CW / 8;  // 16-byte chunks per output row
-#pragma unroll
-  for (int i = 0; i < BM * CPR / NTHR; ++i) {
-    const int lin = i * NTHR + tid;
-    const int row = lin / CPR, ch = lin % CPR;
-    if (row < tile.rows)
-      *reinterpret_cast<uint4*>(C + (size_t)(tile.row0 + row) * ldc + nt * CW + ch * 8) =
-          reinterpret_cast<const uint4*>(ctile)[row * CPR + ch];
+    for (int i = 0; i < 32 * CPR / 64; ++i) {
+      const int lin = i * 64 + lane;
+      const int rr = lin / CPR, ch = lin % CPR;
+      const int row = mi * 32 + rr;
+      const uint4 val = *reinterpret_cast<const uint4*>(reg + rr * RS + ch * 16);
+      if (row < wk.rows)
+        *reinterpret_cast<uint4*>(C + (size_t)(wk.row0 + row) * ldc + colbase + ch * 8) = val;
+    }
   }
 }
+
+__device__ __forceinline__ float silu_f(float g) { return g / (1.f + expf(-g)); }
 
 // ---------------------------------------------------------------------------
 // float32 SIMT path: 32x32 output tiles, k-step 32, 256 threads x 2x2 outputs
@@ -340,15 +351,15 @@ template <int MODE>
 __global__ __launch_bounds__(256) void ffn_gemm_f32_kernel(const float* __restrict__ A,
                                                            const float* __restrict__ W,
                                                            float* __restrict__ C,
-                                                           const Tile* __restrict__ tiles,
-                                                           const int32_t* __restrict__ n_tiles,
-                                                           int d, int m, int n_tiles_n) {
+                                                           const Work* __restrict__ work,
+                                                           const int32_t* __restrict__ n_work,
+                                                           int d, int m) {
   __shared__ float as[FBM][FBK + 1];
   __shared__ float bs[2][FBN][FBK + 1];  // MODE 0: gate, up; MODE 1: down only
-  const int nt = blockIdx.x % n_tiles_n;
-  const int mt = blockIdx.x / n_tiles_n;
-  if (mt >= *n_tiles) return;
-  const Tile tile = tiles[mt];
+  if ((int)blockIdx.x >= n_work[MODE]) return;
+  const Work wk = work[blockIdx.x];
+  const int nt = wk.nt;
+  struct { int row0, rows, expert; } tile{wk.row0, wk.rows, wk.expert};
   const int Kdim = MODE == 0 ? d : m;
   const int Ncols = MODE == 0 ? m : d;
   const float* Wexp = W + (size_t)tile.expert * (size_t)(MODE == 0 ? 2 * m : d) * Kdim;
@@ -393,13 +404,13 @@ __global__ __launch_bounds__(256) void ffn_gemm_f32_kernel(const float* __restri
 }  // namespace kern
 
 namespace {
-using kern::Tile;
-using kern::ffn_tiles_kernel;
 using kern::FBM;
 using kern::FBN;
 using kern::NTHR;
+using kern::Work;
 using kern::ffn_gemm_bf16_kernel;
 using kern::ffn_gemm_f32_kernel;
+using kern::ffn_tiles_kernel;
 
 size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
 int max_tiles_for(int rows_max, int E, int bm) { return (rows_max + bm - 1) / bm + E; }
@@ -408,28 +419,75 @@ int max_tiles_for(int rows_max, int E, int bm) { return (rows_max + bm - 1) / bm
 // else 64 (weight-streaming shapes with few rows per expert)
 int pick_bm(int rows_max, int E) { return rows_max >= 160 * E ? 128 : 64; }
 
+// n-tiles per GEMM: bf16 uses 256 weight rows per tile when they divide the
+// expert's rows, else 128; float32 uses 32 output columns
+// bf16 weight-row tile: 512 when it divides the expert's rows, else 256
+// (gate/up: 2m, down: d); `wide` selects 512
+void n_tiles_of(bool bf16, int d, int m, int& nn0, int& nn1, bool& wide0, bool& wide1) {
+  if (bf16) {
+    wide0 = (2 * m) % 512 == 0;
+    wide1 = d % 512 == 0;
+    nn0 = 2 * m / (wide0 ? 512 : 256);
+    nn1 = d / (wide1 ? 512 : 256);
+  } else {
+    wide0 = wide1 = false;
+    nn0 = (m + FBN - 1) / FBN;
+    nn1 = (d + FBN - 1) / FBN;
+  }
+}
+
+struct FfnWs {
+  int32_t* n_work;
+  Work* work0;
+  Work* work1;
+  void* h;
+};
+
+FfnWs carve(void* ws, bool bf16, int rows_max, int E, int d, int m) {
+  const int cap = max_tiles_for(rows_max, E, bf16 ? 64 : FBM);
+  const size_t c0 = (size_t)cap * ((m + FBN - 1) / FBN) + 8;  // >= any nn0 * tiles
+  const size_t c1 = (size_t)cap * ((d + FBN - 1) / FBN) + 8;
+  char* p = static_cast<char*>(ws);
+  FfnWs w;
+  w.n_work = reinterpret_cast<int32_t*>(p);
+  p += 256;
+  w.work0 = reinterpret_cast<Work*>(p);
+  p += align256(c0 * sizeof(Work));
+  w.work1 = reinterpret_cast<Work*>(p);
+  p += align256(c1 * sizeof(Work));
+  w.h = p;
+  return w;
+}
+
 // kernels are instantiated here, outside any function template (device stubs
 // of kernels first instantiated inside a template launcher are not emitted)
-#define FFN_GEMM(MODE, BM, BN) \
-  ffn_gemm_bf16_kernel<MODE, BM, BN><<<max_tiles * nn, NTHR, 0, s>>>(A, W, C, tiles, n_tiles, d, m, nn)
+#define FFN_GEMM(MODE, BM, BN)                                                                    \
+  do {                                                                                            \
+    if (tail == 0)                                                                                \
+      ffn_gemm_bf16_kernel<MODE, BM, BN, 0><<<grid, NTHR, 0, s>>>(A, W, C, work, n_work, d, m); \
+    else if (tail == 1)                                                                           \
+      ffn_gemm_bf16_kernel<MODE, BM, BN, 1><<<grid, NTHR, 0, s>>>(A, W, C, work, n_work, d, m); \
+    else                                                                                          \
+      ffn_gemm_bf16_kernel<MODE, BM, BN, 2><<<grid, NTHR, 0, s>>>(A, W, C, work, n_work, d, m); \
+  } while (0)
 
-hipError_t launch_gemm(int mode, int bm, const uint16_t* A, const uint16_t* W, uint16_t* C,
-                       const Tile* tiles, const int32_t* n_tiles, int d, int m, int max_tiles,
-                       hipStream_t s) {
-  const int ncols = mode == 0 ? 2 * m : d;  // weight rows of one expert
-  const bool wide = ncols % 256 == 0;
-  const int nn = ncols / (wide ? 256 : 128);
+hipError_t launch_gemm(int mode, int bm, bool wide, int n_items_max, const uint16_t* A,
+                       const uint16_t* W, uint16_t* C, const Work* work, const int32_t* n_work,
+                       int d, int m, hipStream_t s) {
+  const int grid = (n_items_max + 7) & ~7;  // whole XCD rounds
+  const int nk = (mode == 0 ? d : m) / kern::BK;
+  const int tail = (nk - 2) % 3;
   if (mode == 0) {
     if (bm == 128) {
-      if (wide) FFN_GEMM(0, 128, 256); else FFN_GEMM(0, 128, 128);
+      if (wide) FFN_GEMM(0, 128, 512); else FFN_GEMM(0, 128, 256);
     } else {
-      if (wide) FFN_GEMM(0, 64, 256); else FFN_GEMM(0, 64, 128);
+      if (wide) FFN_GEMM(0, 64, 512); else FFN_GEMM(0, 64, 256);
     }
   } else {
     if (bm == 128) {
-      if (wide) FFN_GEMM(1, 128, 256); else FFN_GEMM(1, 128, 128);
+      if (wide) FFN_GEMM(1, 128, 512); else FFN_GEMM(1, 128, 256);
     } else {
-      if (wide) FFN_GEMM(1, 64, 256); else FFN_GEMM(1, 64, 128);
+      if (wide) FFN_GEMM(1, 64, 512); else FFN_GEMM(1, 64, 256);
     }
   }
   return hipGetLastError();
@@ -438,11 +496,11 @@ hipError_t launch_gemm(int mode, int bm, const uint16_t* A, const uint16_t* W, u
 }  // namespace
 
 size_t ffn_ws_bytes(bool bf16, int rows_max, int E, int d, int m) {
-  (void)d;
-  const int bm = bf16 ? 64 : FBM;  // the smallest tile height gives the longest list
-  size_t tiles = align256((size_t)max_tiles_for(rows_max, E, bm) * sizeof(Tile));
-  size_t h = align256((size_t)rows_max * m * (bf16 ? 2 : 4));
-  return 256 + tiles + h;
+  const int cap = max_tiles_for(rows_max, E, bf16 ? 64 : FBM);
+  const size_t c0 = (size_t)cap * ((m + FBN - 1) / FBN) + 8;
+  const size_t c1 = (size_t)cap * ((d + FBN - 1) / FBN) + 8;
+  return 256 + align256(c0 * sizeof(Work)) + align256(c1 * sizeof(Work)) +
+         align256((size_t)rows_max * m * (bf16 ? 2 : 4));
 }
 
 hipError_t launch_expert_ffn(const void* x_perm, bool bf16, const int32_t* offsets, int E,
@@ -451,33 +509,31 @@ hipError_t launch_expert_ffn(const void* x_perm, bool bf16, const int32_t* offse
                              hipStream_t s) {
   const int bm = bf16 ? pick_bm(rows_max, E) : FBM;
   const int max_tiles = max_tiles_for(rows_max, E, bm);
-  const int list_cap = max_tiles_for(rows_max, E, bf16 ? 64 : FBM);
-  char* p = static_cast<char*>(ws);
-  int32_t* n_tiles = reinterpret_cast<int32_t*>(p);
-  Tile* tiles = reinterpret_cast<Tile*>(p + 256);
-  void* h = p + 256 + align256((size_t)list_cap * sizeof(Tile));
-  ffn_tiles_kernel<<<1, 1024, 0, s>>>(offsets, E, K_dev, n_K, rows_max, bm, tiles, max_tiles, n_tiles);
+  int nn0, nn1;
+  bool wide0, wide1;
+  n_tiles_of(bf16, d, m, nn0, nn1, wide0, wide1);
+  FfnWs w = carve(ws, bf16, rows_max, E, d, m);
+  ffn_tiles_kernel<<<1, 1024, 0, s>>>(offsets, E, K_dev, n_K, rows_max, bm, max_tiles, nn0, nn1,
+                                      w.work0, w.work1, w.n_work);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   if (bf16) {
-    const auto* xp = static_cast<const uint16_t*>(x_perm);
-    const auto* wgu = static_cast<const uint16_t*>(w_gate_up);
-    const auto* wd = static_cast<const uint16_t*>(w_down);
-    auto* hh = static_cast<uint16_t*>(h);
-    auto* y = static_cast<uint16_t*>(y_perm);
-    err = launch_gemm(0, bm, xp, wgu, hh, tiles, n_tiles, d, m, max_tiles, s);
-    if (err == hipSuccess) err = launch_gemm(1, bm, hh, wd, y, tiles, n_tiles, d, m, max_tiles, s);
-    return err;
+    err = launch_gemm(0, bm, wide0, max_tiles * nn0, static_cast<const uint16_t*>(x_perm),
+                      static_cast<const uint16_t*>(w_gate_up), static_cast<uint16_t*>(w.h),
+                      w.work0, w.n_work, d, m, s);
+    if (err != hipSuccess) return err;
+    return launch_gemm(1, bm, wide1, max_tiles * nn1, static_cast<const uint16_t*>(w.h),
+                       static_cast<const uint16_t*>(w_down), static_cast<uint16_t*>(y_perm),
+                       w.work1, w.n_work, d, m, s);
   }
-  const int n0 = (m + FBN - 1) / FBN, n1 = (d + FBN - 1) / FBN;
-  ffn_gemm_f32_kernel<0><<<max_tiles * n0, 256, 0, s>>>(
+  ffn_gemm_f32_kernel<0><<<max_tiles * nn0, 256, 0, s>>>(
       static_cast<const float*>(x_perm), static_cast<const float*>(w_gate_up),
-      static_cast<float*>(h), tiles, n_tiles, d, m, n0);
+      static_cast<float*>(w.h), w.work0, w.n_work, d, m);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
-  ffn_gemm_f32_kernel<1><<<max_tiles * n1, 256, 0, s>>>(
-      static_cast<const float*>(h), static_cast<const float*>(w_down),
-      static_cast<float*>(y_perm), tiles, n_tiles, d, m, n1);
+  ffn_gemm_f32_kernel<1><<<max_tiles * nn1, 256, 0, s>>>(
+      static_cast<const float*>(w.h), static_cast<const float*>(w_down),
+      static_cast<float*>(y_perm), w.work1, w.n_work, d, m);
   return hipGetLastError();
 }
 

@@ -101,10 +101,11 @@ def test_dispatch_rejects(lib):
 def test_ffn_rejects(lib):
     ws = ctypes.c_void_p(0x1000000)
     assert lib.moe_expert_ffn(P1, BF16, P2, 16, NULL, 0, 64, 100, 64, P3, P4, P5, ws, 1 << 30, NULL) == EUNSUPPORTED
-    assert lib.moe_expert_ffn(P1, BF16, P2, 16, NULL, 0, 64, 128, 48, P3, P4, P5, ws, 1 << 30, NULL) == EUNSUPPORTED
-    assert lib.moe_expert_ffn(P1, BF16, P2, 16, P6, 0, 64, 128, 64, P3, P4, P5, ws, 1 << 30, NULL) == EINVAL
-    assert lib.moe_expert_ffn(P1, BF16, P2, 16, NULL, 0, 64, 128, 64, P3, P4, P5, ws, 16, NULL) == EWORKSPACE
-    assert lib.moe_expert_ffn(P1, 7, P2, 16, NULL, 0, 64, 128, 64, P3, P4, P5, ws, 1 << 30, NULL) == EINVAL
+    assert lib.moe_expert_ffn(P1, BF16, P2, 16, NULL, 0, 64, 256, 64, P3, P4, P5, ws, 1 << 30, NULL) == EUNSUPPORTED
+    assert lib.moe_expert_ffn(P1, BF16, P2, 16, NULL, 0, 64, 128, 128, P3, P4, P5, ws, 1 << 30, NULL) == EUNSUPPORTED
+    assert lib.moe_expert_ffn(P1, BF16, P2, 16, P6, 0, 64, 256, 128, P3, P4, P5, ws, 1 << 30, NULL) == EINVAL
+    assert lib.moe_expert_ffn(P1, BF16, P2, 16, NULL, 0, 64, 256, 128, P3, P4, P5, ws, 16, NULL) == EWORKSPACE
+    assert lib.moe_expert_ffn(P1, 7, P2, 16, NULL, 0, 64, 256, 128, P3, P4, P5, ws, 1 << 30, NULL) == EINVAL
 
 
 def test_combine_and_drop_reject(lib):

@@ -298,7 +298,7 @@ FFN_CASES = [
     (16, 256, 128, "f32", 1024, None, None),
     (8, 2048, 768, "bf16", 1500, None, [0, 1, 127, 128, 129, 300, 700, 115]),
     (6, 2048, 768, "bf16", 900, 4, None),
-    (3, 128, 64, "bf16", 300, None, [255, 0, 45]),
+    (3, 256, 128, "bf16", 300, None, [255, 0, 45]),
     (128, 256, 128, "bf16", 4096, None, None),
     (5, 40, 12, "f32", 77, None, None),
 ]
