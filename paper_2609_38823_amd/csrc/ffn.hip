@@ -90,9 +90,10 @@ __global__ __launch_bounds__(1024) void ffn_tiles_kernel(const int32_t* __restri
 // gives 128x128 per wavefront, 256 accumulator registers, and 64 bytes of
 // LDS reads per 32 MFMA cycles -- half the LDS bandwidth of a 64x64 tile).
 // Operand tiles stream from global memory straight into LDS with
-// buffer_load_dwordx4 ... lds through a 3-stage ring of separate LDS arrays
-// (the compiler's wait tracking then keeps the younger stage in flight while
-// the oldest is consumed).  Each 64-byte LDS row holds one tile row's 32
+// buffer_load_dwordx4 ... lds through a 4-stage ring of separate LDS arrays
+// (the compiler's wait tracking then keeps the three younger stages in flight
+// while the oldest is consumed; with about 3 us of loaded memory latency,
+// stages in flight rather than bandwidth set the pace).  Each 64-byte LDS row holds one tile row's 32
 // k-values as four 16-byte chunks, chunk c stored at position
 // c ^ ((row >> 2) & 3): the 16 rows read by one quarter-wavefront hit 16
 // distinct bank groups.  The two 16-wide k-substeps of a stage are
@@ -104,6 +105,7 @@ constexpr int LDS_STAGE_MAX = (128 + 512) * BK * 2;  // bytes, largest tile pair
 __shared__ __attribute__((aligned(1024))) char ring0[LDS_STAGE_MAX];
 __shared__ __attribute__((aligned(1024))) char ring1[LDS_STAGE_MAX];
 __shared__ __attribute__((aligned(1024))) char ring2[LDS_STAGE_MAX];
+__shared__ __attribute__((aligned(1024))) char ring3[LDS_STAGE_MAX];
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
@@ -257,20 +259,23 @@ __global__ __launch_bounds__(NTHR, 1) void ffn_gemm_bf16_kernel(
   };
 
   const int nk = Kdim / BK;
-  // steady-state step: wait until stage `cur` has landed (one younger stage
+  // steady-state step: wait until stage `cur` has landed (two younger stages
   // still in flight), barrier (every wave is also done with the stage read in
-  // the previous step), refill that stage with iteration it+2, consume `cur`
+  // the previous step), refill that stage with iteration it+3, consume `cur`
   auto step_issue = [&](int it, char* cur, char* nxt) {
-    wait_vmcnt<GPW>();
+    wait_vmcnt<2 * GPW>();
     __builtin_amdgcn_s_barrier();
-    issue(nxt, (it + 2) * BK);
+    issue(nxt, (it + 3) * BK);
     compute(cur);
   };
-  auto step_tail = [&](char* cur, bool last) {
-    if (last)
-      wait_vmcnt<0>();
-    else
+  // drain steps: `left` younger stages still in flight
+  auto step_tail = [&](char* cur, int left) {
+    if (left == 2)
+      wait_vmcnt<2 * GPW>();
+    else if (left == 1)
       wait_vmcnt<GPW>();
+    else
+      wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
     compute(cur);
   };
@@ -278,26 +283,35 @@ __global__ __launch_bounds__(NTHR, 1) void ffn_gemm_bf16_kernel(
   // nk >= 4: the entry point requires d and m to be multiples of 128
   issue(ring0, 0);
   issue(ring1, BK);
+  issue(ring2, 2 * BK);
   int it = 0;
-  for (; it + 5 <= nk; it += 3) {  // branch-free body: every step issues
-    step_issue(it, ring0, ring2);
+  for (; it + 7 <= nk; it += 4) {  // branch-free body: every step issues
+    step_issue(it, ring0, ring3);
     step_issue(it + 1, ring1, ring0);
     step_issue(it + 2, ring2, ring1);
+    step_issue(it + 3, ring3, ring2);
   }
-  // TAIL = (nk - 2) % 3, fixed per instantiation, so the last 2 + TAIL
-  // iterations have static rings and a single code path
-  if (TAIL == 2) {
-    step_issue(it, ring0, ring2);
-    step_issue(it + 1, ring1, ring0);
-    step_tail(ring2, false);
-    step_tail(ring0, true);
+  // TAIL = (nk - 3) % 4, fixed per instantiation: the last 3 + TAIL
+  // iterations (it is a multiple of 4, so rings are static) take one path
+  if (TAIL >= 1) step_issue(it, ring0, ring3);
+  if (TAIL >= 2) step_issue(it + 1, ring1, ring0);
+  if (TAIL >= 3) step_issue(it + 2, ring2, ring1);
+  if (TAIL == 0) {
+    step_tail(ring0, 2);
+    step_tail(ring1, 1);
+    step_tail(ring2, 0);
   } else if (TAIL == 1) {
-    step_issue(it, ring0, ring2);
-    step_tail(ring1, false);
-    step_tail(ring2, true);
+    step_tail(ring1, 2);
+    step_tail(ring2, 1);
+    step_tail(ring3, 0);
+  } else if (TAIL == 2) {
+    step_tail(ring2, 2);
+    step_tail(ring3, 1);
+    step_tail(ring0, 0);
   } else {
-    step_tail(ring0, false);
-    step_tail(ring1, true);
+    step_tail(ring3, 2);
+    step_tail(ring0, 1);
+    step_tail(ring1, 0);
   }
 
   // ---- epilogue.  The weight fragment is the MFMA's first operand, so
@@ -467,8 +481,10 @@ FfnWs carve(void* ws, bool bf16, int rows_max, int E, int d, int m) {
       ffn_gemm_bf16_kernel<MODE, BM, BN, 0><<<grid, NTHR, 0, s>>>(A, W, C, work, n_work, d, m); \
     else if (tail == 1)                                                                           \
       ffn_gemm_bf16_kernel<MODE, BM, BN, 1><<<grid, NTHR, 0, s>>>(A, W, C, work, n_work, d, m); \
-    else                                                                                          \
+    else if (tail == 2)                                                                           \
       ffn_gemm_bf16_kernel<MODE, BM, BN, 2><<<grid, NTHR, 0, s>>>(A, W, C, work, n_work, d, m); \
+    else                                                                                          \
+      ffn_gemm_bf16_kernel<MODE, BM, BN, 3><<<grid, NTHR, 0, s>>>(A, W, C, work, n_work, d, m); \
   } while (0)
 
 hipError_t launch_gemm(int mode, int bm, bool wide, int n_items_max, const uint16_t* A,
@@ -476,7 +492,7 @@ hipError_t launch_gemm(int mode, int bm, bool wide, int n_items_max, const uint1
                        int d, int m, hipStream_t s) {
   const int grid = (n_items_max + 7) & ~7;  // whole XCD rounds
   const int nk = (mode == 0 ? d : m) / kern::BK;
-  const int tail = (nk - 2) % 3;
+  const int tail = (nk - 3) % 4;
   if (mode == 0) {
     if (bm == 128) {
       if (wide) FFN_GEMM(0, 128, 512); else FFN_GEMM(0, 128, 256);
