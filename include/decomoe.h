@@ -11,6 +11,8 @@
  *   prefix-restricted re-route inside [0, K)                      moe_route
  *   grouping of the T*k assignments by expert                     moe_dispatch
  *   SwiGLU expert MLPs over the dispatched rows                   moe_expert_ffn
+ *     (same, on weights re-laid out once at load time)            moe_expert_ffn_packed,
+ *                                                                 moe_pack_expert_weights
  *   weighted combine back to token order                          moe_combine
  *   SAVB visual-block removal from the hidden state (Sec. 3.2)   drop_visual_block
  *
@@ -182,6 +184,42 @@ int moe_expert_ffn(const void* x_perm, moe_dtype dtype, const int32_t* offsets, 
                    const int32_t* K_dev, int n_K, int rows_max, int d, int m,
                    const void* w_gate_up, const void* w_down, void* y_perm,
                    void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * moe_pack_expert_weights - one-time re-layout of bf16 expert weights for
+ * moe_expert_ffn_packed, done when a layer is loaded (like the physical
+ * Mean-Mass reorder of the expert parameters, Sec. 3.3 and Algorithm 1, it
+ * moves storage and computes nothing).
+ *
+ *   w         [E, rows, cols] bf16, row-major (w_gate_up: rows 2m, cols d;
+ *             w_down: rows d, cols m).
+ *   w_packed  E * rows * cols bf16 output, caller-owned, same size as w,
+ *             must not overlap it.  For expert e, row r, column c it holds
+ *             w[e, r, c] at element offset
+ *               e*rows*cols + ((c/16) * (rows/32) + r/32) * 512
+ *                 + 8 * ((r % 32) + 32 * ((c % 16) / 8)) + c % 8,
+ *             i.e. 1 KB blocks that are the first operand of one
+ *             32x32x16 bf16 MFMA (lane l: row 32 rb + l % 32, columns
+ *             16 kb + 8 (l / 32) .. +8), blocks of one 16-wide column slice
+ *             in row order.
+ * bf16 only (MOE_EUNSUPPORTED for float32); rows % 32 == 0 and
+ * cols % 16 == 0, else MOE_EUNSUPPORTED.  No workspace.
+ */
+int moe_pack_expert_weights(const void* w, moe_dtype dtype, int E, int rows, int cols,
+                            void* w_packed, hipStream_t stream);
+
+/*
+ * moe_expert_ffn_packed - moe_expert_ffn on packed weights: the same
+ * arguments, results and limits, with w_gate_up_packed and w_down_packed
+ * produced by moe_pack_expert_weights from [E, 2m, d] and [E, d, m].  The
+ * weight operand then streams from HBM in contiguous runs straight into
+ * registers.  bf16 only (MOE_EUNSUPPORTED for float32).  Needs ws
+ * (moe_workspace_size).
+ */
+int moe_expert_ffn_packed(const void* x_perm, moe_dtype dtype, const int32_t* offsets, int E,
+                          const int32_t* K_dev, int n_K, int rows_max, int d, int m,
+                          const void* w_gate_up_packed, const void* w_down_packed,
+                          void* y_perm, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * moe_combine - weighted combine back to token order (Algorithm 2).

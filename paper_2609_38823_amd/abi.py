@@ -23,7 +23,8 @@ STATUS = {0: "MOE_OK", -1: "MOE_EINVAL", -2: "MOE_EALIAS", -3: "MOE_EWORKSPACE",
           -4: "MOE_EHIP", -5: "MOE_EUNSUPPORTED"}
 
 EXPORTS = ("moe_status_string", "moe_workspace_size", "moe_route", "moe_calibrate_prefix",
-           "moe_dispatch", "moe_expert_ffn", "moe_combine", "drop_visual_block")
+           "moe_dispatch", "moe_expert_ffn", "moe_expert_ffn_packed", "moe_pack_expert_weights",
+           "moe_combine", "drop_visual_block")
 
 
 class MoeError(RuntimeError):
@@ -51,6 +52,8 @@ def load() -> ctypes.CDLL:
         "moe_calibrate_prefix": (_I, [_P, _P, _I, _I, _I, _P, _I, _D, _P, _P, _P, _P]),
         "moe_dispatch": (_I, [_P, _I, _I, _I, _P, _I, _I, _P, _P, _P, _P, _P, _P, _S, _P]),
         "moe_expert_ffn": (_I, [_P, _I, _P, _I, _P, _I, _I, _I, _I, _P, _P, _P, _P, _S, _P]),
+        "moe_expert_ffn_packed": (_I, [_P, _I, _P, _I, _P, _I, _I, _I, _I, _P, _P, _P, _P, _S, _P]),
+        "moe_pack_expert_weights": (_I, [_P, _I, _I, _I, _I, _P, _P]),
         "moe_combine": (_I, [_P, _I, _P, _P, _I, _I, _I, _P, _P]),
         "drop_visual_block": (_I, [_P, _I, _I, _I, _I, _I, _P, _P]),
     }
@@ -144,6 +147,27 @@ def moe_expert_ffn(x_perm, offsets, w_gate_up, w_down, y_perm, ws, K_dev=None, s
         _p(x_perm), _dt(x_perm), _p(offsets), E, _p(K_dev), n_K, rows_max, d, two_m // 2,
         _p(w_gate_up), _p(w_down), _p(y_perm), _p(ws), ws.numel() * ws.element_size(),
         _stream(stream)))
+
+
+def moe_expert_ffn_packed(x_perm, offsets, w_gate_up_packed, w_down_packed, y_perm, ws, K_dev=None,
+                          stream=None):
+    """Packed weights keep the shapes of the row-major tensors they came from."""
+    rows_max, d = x_perm.shape
+    E, two_m, _ = w_gate_up_packed.shape
+    n_K = K_dev.numel() if K_dev is not None else 0
+    _check("moe_expert_ffn_packed", load().moe_expert_ffn_packed(
+        _p(x_perm), _dt(x_perm), _p(offsets), E, _p(K_dev), n_K, rows_max, d, two_m // 2,
+        _p(w_gate_up_packed), _p(w_down_packed), _p(y_perm), _p(ws), ws.numel() * ws.element_size(),
+        _stream(stream)))
+
+
+def moe_pack_expert_weights(w, w_packed, stream=None):
+    """w [E, rows, cols] -> w_packed (same shape and dtype, packed contents)."""
+    E, rows, cols = w.shape
+    if tuple(w_packed.shape) != (E, rows, cols) or w_packed.dtype != w.dtype:
+        raise ValueError("w_packed must have the shape and dtype of w")
+    _check("moe_pack_expert_weights", load().moe_pack_expert_weights(
+        _p(w), _dt(w), E, rows, cols, _p(w_packed), _stream(stream)))
 
 
 def moe_combine(y_perm, row_of_slot, topk_w, out, stream=None):

@@ -44,6 +44,36 @@ bool valid_dtype(moe_dtype dt) { return dt == MOE_F32 || dt == MOE_BF16; }
 int hip_status(hipError_t e) { return e == hipSuccess ? MOE_OK : MOE_EHIP; }
 size_t a256(size_t b) { return (b + 255) & ~size_t(255); }
 
+// validation shared by the row-major and packed expert FFN entry points
+int expert_ffn(const void* x_perm, moe_dtype dtype, const int32_t* offsets, int E,
+               const int32_t* K_dev, int n_K, int rows_max, int d, int m,
+               const void* w_gate_up, const void* w_down, bool packed, void* y_perm, void* ws,
+               size_t ws_bytes, hipStream_t stream) {
+  if (!valid_dtype(dtype) || E < 1 || E > kMaxE || rows_max < 0 || d < 1 || m < 1) return MOE_EINVAL;
+  if (K_dev && n_K < 1) return MOE_EINVAL;
+  if (!offsets || !w_gate_up || !w_down) return MOE_EINVAL;
+  if (rows_max > 0 && (!x_perm || !y_perm)) return MOE_EINVAL;
+  const bool bf16 = dtype == MOE_BF16;
+  if (bf16 && (d % 256 != 0 || m % 128 != 0)) return MOE_EUNSUPPORTED;
+  // the GEMM addresses one expert's weights with 32-bit buffer offsets
+  if ((size_t)2 * m * d * elt_size(dtype) > (size_t)INT32_MAX) return MOE_EUNSUPPORTED;
+  if (!aligned_all({x_perm, offsets, K_dev, w_gate_up, w_down, y_perm, ws})) return MOE_EINVAL;
+  if (rows_max == 0) return MOE_OK;
+  const size_t need = ffn_ws_bytes(bf16, rows_max, E, d, m);
+  if (!ws || ws_bytes < need) return MOE_EWORKSPACE;
+  const int es = elt_size(dtype);
+  Range o_y = rng(y_perm, (size_t)rows_max * d * es);
+  Range o_ws = rng(ws, need);
+  Range in_k = K_dev ? rng(K_dev, (size_t)n_K * 4) : Range{0, 0};
+  if (any_alias({o_y, o_ws},
+                {rng(x_perm, (size_t)rows_max * d * es), rng(offsets, (size_t)(E + 1) * 4), in_k,
+                 rng(w_gate_up, (size_t)E * 2 * m * d * es), rng(w_down, (size_t)E * d * m * es)}))
+    return MOE_EALIAS;
+  return hip_status(decomoe::launch_expert_ffn(x_perm, bf16, offsets, E, K_dev, n_K, rows_max, d,
+                                               m, w_gate_up, w_down, packed, y_perm, ws,
+                                               stream));
+}
+
 }  // namespace
 
 extern "C" {
@@ -154,28 +184,29 @@ int moe_expert_ffn(const void* x_perm, moe_dtype dtype, const int32_t* offsets, 
                    const int32_t* K_dev, int n_K, int rows_max, int d, int m,
                    const void* w_gate_up, const void* w_down, void* y_perm, void* ws,
                    size_t ws_bytes, hipStream_t stream) {
-  if (!valid_dtype(dtype) || E < 1 || E > kMaxE || rows_max < 0 || d < 1 || m < 1) return MOE_EINVAL;
-  if (K_dev && n_K < 1) return MOE_EINVAL;
-  if (!offsets || !w_gate_up || !w_down) return MOE_EINVAL;
-  if (rows_max > 0 && (!x_perm || !y_perm)) return MOE_EINVAL;
-  const bool bf16 = dtype == MOE_BF16;
-  if (bf16 && (d % 256 != 0 || m % 128 != 0)) return MOE_EUNSUPPORTED;
-  // the GEMM addresses one expert's weights with 32-bit buffer offsets
-  if ((size_t)2 * m * d * elt_size(dtype) > (size_t)INT32_MAX) return MOE_EUNSUPPORTED;
-  if (!aligned_all({x_perm, offsets, K_dev, w_gate_up, w_down, y_perm, ws})) return MOE_EINVAL;
-  if (rows_max == 0) return MOE_OK;
-  const size_t need = ffn_ws_bytes(bf16, rows_max, E, d, m);
-  if (!ws || ws_bytes < need) return MOE_EWORKSPACE;
-  const int es = elt_size(dtype);
-  Range o_y = rng(y_perm, (size_t)rows_max * d * es);
-  Range o_ws = rng(ws, need);
-  Range in_k = K_dev ? rng(K_dev, (size_t)n_K * 4) : Range{0, 0};
-  if (any_alias({o_y, o_ws},
-                {rng(x_perm, (size_t)rows_max * d * es), rng(offsets, (size_t)(E + 1) * 4), in_k,
-                 rng(w_gate_up, (size_t)E * 2 * m * d * es), rng(w_down, (size_t)E * d * m * es)}))
-    return MOE_EALIAS;
-  return hip_status(decomoe::launch_expert_ffn(x_perm, bf16, offsets, E, K_dev, n_K, rows_max, d,
-                                               m, w_gate_up, w_down, y_perm, ws, stream));
+  return expert_ffn(x_perm, dtype, offsets, E, K_dev, n_K, rows_max, d, m, w_gate_up, w_down,
+                    false, y_perm, ws, ws_bytes, stream);
+}
+
+int moe_expert_ffn_packed(const void* x_perm, moe_dtype dtype, const int32_t* offsets, int E,
+                          const int32_t* K_dev, int n_K, int rows_max, int d, int m,
+                          const void* w_gate_up_packed, const void* w_down_packed, void* y_perm,
+                          void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (dtype != MOE_BF16) return valid_dtype(dtype) ? MOE_EUNSUPPORTED : MOE_EINVAL;
+  return expert_ffn(x_perm, dtype, offsets, E, K_dev, n_K, rows_max, d, m, w_gate_up_packed,
+                    w_down_packed, true, y_perm, ws, ws_bytes, stream);
+}
+
+int moe_pack_expert_weights(const void* w, moe_dtype dtype, int E, int rows, int cols,
+                            void* w_packed, hipStream_t stream) {
+  if (!valid_dtype(dtype) || E < 0 || rows < 0 || cols < 0) return MOE_EINVAL;
+  if (dtype != MOE_BF16) return MOE_EUNSUPPORTED;
+  if (rows % 32 != 0 || cols % 16 != 0) return MOE_EUNSUPPORTED;
+  const size_t bytes = (size_t)E * rows * cols * 2;
+  if (bytes == 0) return MOE_OK;
+  if (!w || !w_packed || !aligned_all({w, w_packed})) return MOE_EINVAL;
+  if (overlap(rng(w, bytes), rng(w_packed, bytes))) return MOE_EALIAS;
+  return hip_status(decomoe::launch_pack_weights(w, E, rows, cols, w_packed, stream));
 }
 
 int moe_combine(const void* y_perm, moe_dtype dtype, const int32_t* row_of_slot,

@@ -12,15 +12,15 @@ constexpr int kWave = 64;  // CDNA wavefront width
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
   return __uint_as_float(static_cast<uint32_t>(b) << 16);
 }
-// round to nearest, ties to even; NaN stays NaN
+// round to nearest, ties to even (gfx950 converts in hardware:
+// v_cvt_pk_bf16_f32); NaN stays NaN
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return static_cast<uint16_t>(u >> 16);
+  return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
 }
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+  const bf16x2_t v = {static_cast<__bf16>(lo), static_cast<__bf16>(hi)};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 __device__ __forceinline__ int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
@@ -50,8 +50,9 @@ hipError_t launch_dispatch(const int32_t* idx, int T, int k, int E, const void* 
 size_t ffn_ws_bytes(bool bf16, int rows_max, int E, int d, int m);
 hipError_t launch_expert_ffn(const void* x_perm, bool bf16, const int32_t* offsets, int E,
                              const int32_t* K_dev, int n_K, int rows_max, int d, int m,
-                             const void* w_gate_up, const void* w_down, void* y_perm, void* ws,
-                             hipStream_t s);
+                             const void* w_gate_up, const void* w_down, bool packed, void* y_perm,
+                             void* ws, hipStream_t s);
+hipError_t launch_pack_weights(const void* w, int E, int R, int K, void* out, hipStream_t s);
 hipError_t launch_combine(const void* y_perm, bool bf16, const int32_t* row_of_slot,
                           const float* w, int T, int k, int d, void* out, hipStream_t s);
 hipError_t launch_drop_rows(const void* h, int elt, int S, int d, int v0, int v1, void* out,

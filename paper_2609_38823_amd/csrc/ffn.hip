@@ -14,6 +14,8 @@
 // 64x64, LDS double buffered with an XOR swizzle of the 16-byte chunks
 // (conflict-free ds_read_b128 of the MFMA fragments), float32 accumulation.
 // float32: a plain LDS-tiled SIMT kernel (correctness path for small layers).
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace decomoe {
@@ -138,6 +140,58 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// Epilogue of the bf16 GEMM kernels.  The weight fragment is the MFMA's first
+// operand, so acc[mi][ni] = W_frag X_frag^T: lane l holds token row
+// mi*32 + l%32 and, for e = 4g + t, output column 8g + 4(l/32) + t of the
+// fragment -- four consecutive columns per g.  MODE 0 pairs gate fragment f
+// with up fragment f + NI/2 and writes SiLU(g) * u.  Each wavefront stages
+// its 32-row slices through its own LDS region `reg` with 8-byte writes,
+// reads them back as row-major 16-byte chunks and writes them with buffer
+// stores, which drop the rows past the tile's last valid row (no branches,
+// so all reads of a slice are in flight together).
+template <int MODE, int MI, int NI>
+__device__ __forceinline__ void store_tile(const f32x16 (&acc)[MI][NI], char* reg, uint16_t* C,
+                                           int ldc, const Work& wk, int colbase, int lane) {
+  constexpr int FO = MODE == 0 ? NI / 2 : NI;  // output fragments per wavefront
+  constexpr int CWV = FO * 32;                 // output columns per wavefront
+  constexpr int RS = CWV * 2 + 16;             // padded LDS row stride (bytes)
+  constexpr int CPR = CWV / 8;                 // 16-byte chunks per row
+  constexpr int NST = 32 * CPR / 64;           // chunks per lane per 32-row slice
+  const int r32 = lane & 31, kh = lane >> 5;
+  const __amdgpu_buffer_rsrc_t c_rs =
+      make_rsrc(C + (size_t)wk.row0 * ldc, (uint32_t)wk.rows * (uint32_t)ldc * 2);
+#pragma unroll
+  for (int mi = 0; mi < MI; ++mi) {
+#pragma unroll
+    for (int f = 0; f < FO; ++f)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        float v[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          v[t] = MODE == 0 ? swiglu_f(acc[mi][f][4 * g + t], acc[mi][f + NI / 2][4 * g + t])
+                           : acc[mi][f][4 * g + t];
+        const uint2 pk = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+        *reinterpret_cast<uint2*>(reg + r32 * RS + (f * 32 + 8 * g + 4 * kh) * 2) = pk;
+      }
+    // same wavefront: LDS order makes the writes visible to these reads
+    u32x4 val[NST];
+#pragma unroll
+    for (int i = 0; i < NST; ++i) {
+      const int lin = i * 64 + lane;
+      val[i] = *reinterpret_cast<const u32x4*>(reg + (lin / CPR) * RS + (lin % CPR) * 16);
+    }
+#pragma unroll
+    for (int i = 0; i < NST; ++i) {
+      const int lin = i * 64 + lane;
+      const int row = mi * 32 + lin / CPR;
+      __builtin_amdgcn_raw_buffer_store_b128(val[i], c_rs, (row * ldc + colbase + (lin % CPR) * 8) * 2, 0, 0);
+    }
+  }
+}
+
 // MODE 0: A = x_perm [rows, d], W = w_gate_up [E, 2m, d], C = h [rows, m];
 //         the B tile's first BN/2 rows are gate rows nt*BN/2.., the rest the
 //         matching up rows m + nt*BN/2..; C gets BN/2 columns.  Wavefront w
@@ -145,7 +199,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 //         fragments hold the same (row, column) in the same registers.
 // MODE 1: A = h [rows, m], W = w_down [E, d, m], C = y_perm [rows, d];
 //         B rows nt*BN.., C gets BN columns; wavefront w owns [w BN/4, ..).
-template <int MODE, int BM, int BN, int TAIL>
+template <int MODE, int BM, int BN>
 __global__ __launch_bounds__(NTHR, 1) void ffn_gemm_bf16_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ W, uint16_t* __restrict__ C,
     const Work* __restrict__ work, const int32_t* __restrict__ n_work, int d, int m) {
@@ -250,108 +304,298 @@ __global__ __launch_bounds__(NTHR, 1) void ffn_gemm_bf16_kernel(
       for (int ni = 0; ni < NI; ++ni)
         acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[ni], af[mi], acc[mi][ni], 0, 0, 0);
   };
-  auto compute = [&](const char* stage) {
-    bf16x8 a0[MI], b0[NI], a1[MI], b1[NI];
-    load_frags(stage, 0, a0, b0);
-    load_frags(stage, 1, a1, b1);
+  // Interleave the fragment reads of the next substep with the MFMAs of the
+  // current one (one wavefront per SIMD: nothing else hides LDS latency).
+  // The scheduling group pattern is MFMA x R, ds_read x 1, repeated.
+  constexpr int NMF = MI * NI, NRD = MI + NI;
+  constexpr int RPER = NMF / NRD > 0 ? NMF / NRD : 1;
+  auto interleave = [&]() {
+#pragma unroll
+    for (int i = 0; i < NRD; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, RPER, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);     // DS read
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, NMF - RPER * NRD, 0);
+  };
+
+  // Pipeline: four LDS stages of BK = 32 k-values; stages it+1..it+3 are in
+  // flight while stage it is consumed.  Each stage is two 16-wide substeps
+  // with register double buffering:
+  //   MFMA(substep 0 of it)  || read substep 1 of it
+  //   wait for stage it+1, lgkmcnt(0), barrier (every wave is done with the
+  //   stage of it, and stage it+1 has landed for every wave)
+  //   refill the stage of it with it+4
+  //   MFMA(substep 1 of it)  || read substep 0 of it+1
+  // LEFT = stages allowed in flight at the wait (2 in the steady state);
+  // LEFT < 0 marks the last iteration.
+  bf16x8 a0[MI], b0[NI], a1[MI], b1[NI];
+  auto step = [&](auto ISSUE, auto LEFT, int it, char* cur, char* nxt) {
+    load_frags(cur, 1, a1, b1);
     mma(a0, b0);
+    interleave();
+    if constexpr (decltype(LEFT)::value >= 0) {
+      wait_vmcnt<decltype(LEFT)::value * GPW>();
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): reads of `cur` are complete
+      __builtin_amdgcn_s_barrier();
+      if constexpr (decltype(ISSUE)::value) issue(cur, (it + 4) * BK);
+      load_frags(nxt, 0, a0, b0);
+    }
     mma(a1, b1);
+    if constexpr (decltype(LEFT)::value >= 0) interleave();
   };
+  using T0 = std::integral_constant<int, 0>;
+  using T1 = std::integral_constant<int, 1>;
+  using L2 = std::integral_constant<int, 2>;
+  using L1 = std::integral_constant<int, 1>;
+  using L0 = std::integral_constant<int, 0>;
+  using LE = std::integral_constant<int, -1>;
 
+  // Kdim / BK is a multiple of 4 (the entry point requires d and m to be
+  // multiples of 128), so the ring position of every step is static
   const int nk = Kdim / BK;
-  // steady-state step: wait until stage `cur` has landed (two younger stages
-  // still in flight), barrier (every wave is also done with the stage read in
-  // the previous step), refill that stage with iteration it+3, consume `cur`
-  auto step_issue = [&](int it, char* cur, char* nxt) {
-    wait_vmcnt<2 * GPW>();
-    __builtin_amdgcn_s_barrier();
-    issue(nxt, (it + 3) * BK);
-    compute(cur);
-  };
-  // drain steps: `left` younger stages still in flight
-  auto step_tail = [&](char* cur, int left) {
-    if (left == 2)
-      wait_vmcnt<2 * GPW>();
-    else if (left == 1)
-      wait_vmcnt<GPW>();
-    else
-      wait_vmcnt<0>();
-    __builtin_amdgcn_s_barrier();
-    compute(cur);
-  };
-
-  // nk >= 4: the entry point requires d and m to be multiples of 128
   issue(ring0, 0);
   issue(ring1, BK);
   issue(ring2, 2 * BK);
-  int it = 0;
-  for (; it + 7 <= nk; it += 4) {  // branch-free body: every step issues
-    step_issue(it, ring0, ring3);
-    step_issue(it + 1, ring1, ring0);
-    step_issue(it + 2, ring2, ring1);
-    step_issue(it + 3, ring3, ring2);
+  issue(ring3, 3 * BK);
+  wait_vmcnt<3 * GPW>();
+  __builtin_amdgcn_s_barrier();
+  load_frags(ring0, 0, a0, b0);
+  for (int it = 0; it + 4 < nk; it += 4) {  // branch-free body: every step refills
+    step(T1{}, L2{}, it, ring0, ring1);
+    step(T1{}, L2{}, it + 1, ring1, ring2);
+    step(T1{}, L2{}, it + 2, ring2, ring3);
+    step(T1{}, L2{}, it + 3, ring3, ring0);
   }
-  // TAIL = (nk - 3) % 4, fixed per instantiation: the last 3 + TAIL
-  // iterations (it is a multiple of 4, so rings are static) take one path
-  if (TAIL >= 1) step_issue(it, ring0, ring3);
-  if (TAIL >= 2) step_issue(it + 1, ring1, ring0);
-  if (TAIL >= 3) step_issue(it + 2, ring2, ring1);
-  if (TAIL == 0) {
-    step_tail(ring0, 2);
-    step_tail(ring1, 1);
-    step_tail(ring2, 0);
-  } else if (TAIL == 1) {
-    step_tail(ring1, 2);
-    step_tail(ring2, 1);
-    step_tail(ring3, 0);
-  } else if (TAIL == 2) {
-    step_tail(ring2, 2);
-    step_tail(ring3, 1);
-    step_tail(ring0, 0);
-  } else {
-    step_tail(ring3, 2);
-    step_tail(ring0, 1);
-    step_tail(ring1, 0);
-  }
+  step(T0{}, L2{}, nk - 4, ring0, ring1);
+  step(T0{}, L1{}, nk - 3, ring1, ring2);
+  step(T0{}, L0{}, nk - 2, ring2, ring3);
+  step(T0{}, LE{}, nk - 1, ring3, ring0);
 
-  // ---- epilogue.  The weight fragment is the MFMA's first operand, so
-  // acc[mi][ni] = W_frag X_frag^T: lane l holds token row mi*32 + l%32 and,
-  // for e = 4g + t, output column 8g + 4(l/32) + t of the fragment -- four
-  // consecutive columns per g.  Each wave stages its 32-row slices through
-  // its own LDS region with 8-byte writes and stores full 16-byte chunks.
+  // ---- epilogue, staged through this wavefront's part of ring0
   __syncthreads();  // every wave is done with the ring
-  constexpr int FO = MODE == 0 ? NI / 2 : NI;  // output fragments per wave
-  constexpr int CWV = FO * 32;                 // output columns per wave
-  constexpr int RS = CWV * 2 + 16;             // padded LDS row stride (bytes)
-  static_assert(4 * 32 * RS <= LDS_STAGE_MAX, "epilogue staging fits in one ring stage");
-  char* reg = ring0 + wv * 32 * RS;
+  constexpr int RS_MAX = (BN / 4) * 2 + 16;
+  static_assert(4 * 32 * RS_MAX <= LDS_STAGE_MAX, "epilogue staging fits in one ring stage");
   const int colbase = MODE == 0 ? nt * (BN / 2) + wv * (BN / 8) : nt * BN + wv * (BN / 4);
+  store_tile<MODE, MI, NI>(acc, ring0 + wv * 32 * RS_MAX, C, ldc, wk, colbase, lane);
+}
+
+// ---------------------------------------------------------------------------
+// Packed expert weights.  A [R, K] bf16 weight matrix is stored as MFMA
+// fragments: the 16 bytes at element offset ((kb * (R / 32)) + rb) * 512 + 8 l
+// hold row 32 rb + l % 32, columns 16 kb + 8 (l / 32) .. +8 -- exactly what
+// lane l supplies as the first operand of v_mfma_f32_32x32x16_bf16.  Every
+// fragment is 1 KB contiguous and the fragments of one 16-wide k-slice
+// follow each other in row order, so a wavefront loads its weight operand
+// straight into registers with fully coalesced 1 KB loads, and the weight
+// rows of one tile and k-step are a few contiguous runs in HBM.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void pack_weights_kernel(const uint4* __restrict__ w, int R, int K,
+                                                           size_t n_chunks, uint4* __restrict__ out) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;  // output chunk
+  if (i >= n_chunks) return;
+  const int l = (int)(i & 63);
+  size_t f = i >> 6;  // fragment index over (expert, kb, rb)
+  const int RB = R / 32, KB = K / 16;
+  const int rb = (int)(f % RB);
+  f /= RB;
+  const int kb = (int)(f % KB);
+  const size_t e = f / KB;
+  const int row = rb * 32 + (l & 31);
+  const int col8 = kb * 2 + (l >> 5);  // 8-element column chunk
+  out[i] = w[(e * R + row) * (size_t)(K / 8) + col8];
+}
+
+// ---------------------------------------------------------------------------
+// bf16 MFMA grouped GEMM on packed weights
+//
+// Same tiles, work list and epilogue as the kernel above; the weight operand
+// bypasses LDS.  Per k-step of 32, wavefront wv loads its 2 x NI weight
+// fragments (NI 32-row blocks x two 16-wide substeps, 1 KB each) into a ring
+// of four register stages, three k-steps ahead.  Only the token-row tile A,
+// which all four wavefronts share, goes through LDS (global -> LDS
+// transfers into a ring of four stages, as above).  LDS then carries A only:
+// a quarter of the bytes the shared-B layout moves, and the fragment reads
+// per MFMA halve.
+// ---------------------------------------------------------------------------
+__shared__ __attribute__((aligned(1024))) char aring0[128 * BK * 2];
+__shared__ __attribute__((aligned(1024))) char aring1[128 * BK * 2];
+__shared__ __attribute__((aligned(1024))) char aring2[128 * BK * 2];
+__shared__ __attribute__((aligned(1024))) char aring3[128 * BK * 2];
+constexpr int OSTAGE = 4 * 32 * (128 * 2 + 16);  // epilogue staging, largest wave slice
+__shared__ __attribute__((aligned(1024))) char ostage[OSTAGE];
+
+__device__ __forceinline__ u32x4 load_frag(__amdgpu_buffer_rsrc_t rs, int voff, int soff) {
+  return __builtin_amdgcn_raw_buffer_load_b128(rs, voff, soff, 0);
+}
+
+template <int MODE, int BM, int BN>
+__global__ __launch_bounds__(NTHR, 1) void ffn_gemm_packed_kernel(
+    const uint16_t* __restrict__ A, const uint16_t* __restrict__ Wp, uint16_t* __restrict__ C,
+    const Work* __restrict__ work, const int32_t* __restrict__ n_work, int d, int m) {
+  constexpr int MI = BM / 32;  // 32-row token fragments (all tile rows)
+  constexpr int NI = BN / 128; // 32-row weight fragments per wavefront
+  constexpr int AG = BM / 16;  // 1 KB DMA groups (16 rows x 64 B) of the A tile
+  constexpr int GA = AG / 4;   // A transfers per wavefront per k-step
+  constexpr int GB = 2 * NI;   // weight fragment loads per wavefront per k-step
+  static_assert(AG % 4 == 0 && (MODE == 1 || NI % 2 == 0), "tile shape");
+  static_assert(BM * BK * 2 <= (int)sizeof(aring0), "A stage too large");
+
+  // XCD-aware order (as above)
+  const int nw = n_work[MODE];
+  const int per_xcd = (nw + 7) >> 3;
+  const int slot = blockIdx.x >> 3;
+  if (slot >= per_xcd) return;
+  const int L = (blockIdx.x & 7) * per_xcd + slot;
+  if (L >= nw) return;
+  const Work wk = work[L];
+  const int nt = wk.nt;
+  const int Kdim = MODE == 0 ? d : m;
+  const int R = MODE == 0 ? 2 * m : d;  // rows of the expert's weight matrix
+  const int ldc = MODE == 0 ? m : d;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  // ---- A: global -> LDS, 16 rows x 64 bytes per wave instruction, chunk
+  // swizzle c ^ ((row >> 2) & 3); padding rows re-read row 0
+  const int lrow = lane >> 2;
+  const int swz_c = (lane & 3) ^ ((lrow >> 2) & 3);
+  const __amdgpu_buffer_rsrc_t a_rs = make_rsrc(A + (size_t)wk.row0 * Kdim, (uint32_t)wk.rows * Kdim * 2);
+  int a_voff[GA];
 #pragma unroll
-  for (int mi = 0; mi < MI; ++mi) {
-#pragma unroll
-    for (int f = 0; f < FO; ++f)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        float v[4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t)
-          v[t] = MODE == 0 ? swiglu_f(acc[mi][f][4 * g + t], acc[mi][f + NI / 2][4 * g + t])
-                           : acc[mi][f][4 * g + t];
-        const uint2 pk = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
-        *reinterpret_cast<uint2*>(reg + r32 * RS + (f * 32 + 8 * g + 4 * kh) * 2) = pk;
-      }
-    // read back row-major 16-byte chunks (same wave: LDS order suffices)
-    constexpr int CPR = CWV / 8;  // chunks per row
-#pragma unroll
-    for (int i = 0; i < 32 * CPR / 64; ++i) {
-      const int lin = i * 64 + lane;
-      const int rr = lin / CPR, ch = lin % CPR;
-      const int row = mi * 32 + rr;
-      const uint4 val = *reinterpret_cast<const uint4*>(reg + rr * RS + ch * 16);
-      if (row < wk.rows)
-        *reinterpret_cast<uint4*>(C + (size_t)(wk.row0 + row) * ldc + colbase + ch * 8) = val;
-    }
+  for (int q = 0; q < GA; ++q) {
+    const int r = wv * 16 + lrow + 64 * q;
+    a_voff[q] = ((r < wk.rows ? r : 0) * Kdim + swz_c * 8) * 2;
   }
+  auto issue_a = [&](char* stage, int k0) {
+#pragma unroll
+    for (int q = 0; q < GA; ++q) dma16(a_rs, stage + (wv + 4 * q) * 1024, a_voff[q], k0 * 2);
+  };
+
+  // ---- B: this wavefront's NI 32-row blocks of the expert's packed matrix
+  const __amdgpu_buffer_rsrc_t b_rs =
+      make_rsrc(Wp + (size_t)wk.expert * R * Kdim, (uint32_t)R * Kdim * 2);
+  const int RB = R / 32;
+  int rb[NI];
+#pragma unroll
+  for (int ni = 0; ni < NI; ++ni) {
+    if (MODE == 0)  // half gate, half up rows of the same h columns
+      rb[ni] = ni < NI / 2 ? (nt * (BN / 2) + wv * (BN / 8)) / 32 + ni
+                           : (m + nt * (BN / 2) + wv * (BN / 8)) / 32 + ni - NI / 2;
+    else
+      rb[ni] = (nt * BN + wv * (BN / 4)) / 32 + ni;
+  }
+  const int b_voff = lane * 16;
+  auto load_b = [&](u32x4 (&b)[2][NI], int ks) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int ni = 0; ni < NI; ++ni) b[h][ni] = load_frag(b_rs, b_voff, ((2 * ks + h) * RB + rb[ni]) * 1024);
+  };
+
+  f32x16 acc[MI][NI];
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int j = 0; j < NI; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  // A fragments (see the kernel above for the lane layout)
+  const int r32 = lane & 31, kh = lane >> 5;
+  const int sw = (r32 >> 2) & 3;
+  const int lane_off0 = r32 * 64 + ((kh ^ sw) << 4);
+  const int lane_off1 = r32 * 64 + (((2 + kh) ^ sw) << 4);
+  auto load_a = [&](const char* stage, int s, bf16x8 (&af)[MI]) {
+    const char* base = stage + (s ? lane_off1 : lane_off0);
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi) af[mi] = *reinterpret_cast<const bf16x8*>(base + mi * 32 * 64);
+  };
+  auto mma = [&](const bf16x8 (&af)[MI], const u32x4 (&bfr)[NI]) {
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < NI; ++ni)
+        acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, bfr[ni]), af[mi],
+                                                              acc[mi][ni], 0, 0, 0);
+  };
+  constexpr int NMF = MI * NI, NRD = MI;
+  constexpr int RPER = NMF / NRD;
+  auto interleave = [&]() {
+#pragma unroll
+    for (int i = 0; i < NRD; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, RPER, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);     // DS read
+    }
+  };
+
+  // Issue order of vector-memory operations (one in-order counter):
+  //   prologue  A0 A1 A2 A3 B0 B1 B2
+  //   step i    A(i+4) B(i+3)      while i + 4 < nk
+  //   step nk-4 B(nk-1)
+  // so at the wait of step i for A(i+1) the operations issued after it are
+  // B(i) and two full steps: 6 NI + 2 GA (the prologue steps have at least
+  // as many), then 6 NI + GA and 4 NI in the last two waiting steps.
+  // Scheduling barriers keep the compiler from reordering these groups.
+  u32x4 bq0[2][NI], bq1[2][NI], bq2[2][NI], bq3[2][NI];
+  bf16x8 a0[MI], a1[MI];
+  auto step = [&](auto ISSUE_A, auto ISSUE_B, auto WAITN, int it, char* cur, char* nxt,
+                  const u32x4 (&bc)[2][NI], u32x4 (&bn)[2][NI]) {
+    load_a(cur, 1, a1);
+    mma(a0, bc[0]);
+    interleave();
+    if constexpr (decltype(WAITN)::value >= 0) {
+      wait_vmcnt<decltype(WAITN)::value>();
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): reads of `cur` are complete
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (decltype(ISSUE_A)::value) issue_a(cur, (it + 4) * BK);
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (decltype(ISSUE_B)::value) load_b(bn, it + 3);
+      __builtin_amdgcn_sched_barrier(0);
+      load_a(nxt, 0, a0);
+    }
+    mma(a1, bc[1]);
+    if constexpr (decltype(WAITN)::value >= 0) interleave();
+  };
+  using N0 = std::integral_constant<int, 0>;
+  using N1 = std::integral_constant<int, 1>;
+  using WS = std::integral_constant<int, 6 * NI + 2 * GA>;
+  using W3 = std::integral_constant<int, 6 * NI + GA>;
+  using W2 = std::integral_constant<int, 4 * NI>;
+  using WE = std::integral_constant<int, -1>;
+  static_assert(6 * NI + 2 * GA < 64, "vmcnt range");
+
+  const int nk = Kdim / BK;  // a multiple of 4, at least 4
+  issue_a(aring0, 0);
+  issue_a(aring1, BK);
+  issue_a(aring2, 2 * BK);
+  issue_a(aring3, 3 * BK);
+  __builtin_amdgcn_sched_barrier(0);
+  load_b(bq0, 0);
+  load_b(bq1, 1);
+  load_b(bq2, 2);
+  __builtin_amdgcn_sched_barrier(0);
+  wait_vmcnt<3 * GA + 3 * GB>();  // A0 landed
+  __builtin_amdgcn_s_barrier();
+  load_a(aring0, 0, a0);
+  for (int it = 0; it + 4 < nk; it += 4) {  // branch-free body: every step refills
+    step(N1{}, N1{}, WS{}, it, aring0, aring1, bq0, bq3);
+    step(N1{}, N1{}, WS{}, it + 1, aring1, aring2, bq1, bq0);
+    step(N1{}, N1{}, WS{}, it + 2, aring2, aring3, bq2, bq1);
+    step(N1{}, N1{}, WS{}, it + 3, aring3, aring0, bq3, bq2);
+  }
+  step(N0{}, N1{}, WS{}, nk - 4, aring0, aring1, bq0, bq3);
+  step(N0{}, N0{}, W3{}, nk - 3, aring1, aring2, bq1, bq0);
+  step(N0{}, N0{}, W2{}, nk - 2, aring2, aring3, bq2, bq1);
+  step(N0{}, N0{}, WE{}, nk - 1, aring3, aring0, bq3, bq2);
+
+  // ---- epilogue, staged through this wavefront's part of `ostage`
+  constexpr int RS_MAX = (BN / 4) * 2 + 16;
+  static_assert(4 * 32 * RS_MAX <= OSTAGE, "epilogue staging");
+  const int colbase = MODE == 0 ? nt * (BN / 2) + wv * (BN / 8) : nt * BN + wv * (BN / 4);
+  store_tile<MODE, MI, NI>(acc, ostage + wv * 32 * RS_MAX, C, ldc, wk, colbase, lane);
 }
 
 __device__ __forceinline__ float silu_f(float g) { return g / (1.f + expf(-g)); }
@@ -424,6 +668,8 @@ using kern::NTHR;
 using kern::Work;
 using kern::ffn_gemm_bf16_kernel;
 using kern::ffn_gemm_f32_kernel;
+using kern::ffn_gemm_packed_kernel;
+using kern::pack_weights_kernel;
 using kern::ffn_tiles_kernel;
 
 size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
@@ -475,24 +721,18 @@ FfnWs carve(void* ws, bool bf16, int rows_max, int E, int d, int m) {
 
 // kernels are instantiated here, outside any function template (device stubs
 // of kernels first instantiated inside a template launcher are not emitted)
-#define FFN_GEMM(MODE, BM, BN)                                                                    \
-  do {                                                                                            \
-    if (tail == 0)                                                                                \
-      ffn_gemm_bf16_kernel<MODE, BM, BN, 0><<<grid, NTHR, 0, s>>>(A, W, C, work, n_work, d, m); \
-    else if (tail == 1)                                                                           \
-      ffn_gemm_bf16_kernel<MODE, BM, BN, 1><<<grid, NTHR, 0, s>>>(A, W, C, work, n_work, d, m); \
-    else if (tail == 2)                                                                           \
-      ffn_gemm_bf16_kernel<MODE, BM, BN, 2><<<grid, NTHR, 0, s>>>(A, W, C, work, n_work, d, m); \
-    else                                                                                          \
-      ffn_gemm_bf16_kernel<MODE, BM, BN, 3><<<grid, NTHR, 0, s>>>(A, W, C, work, n_work, d, m); \
+#define FFN_GEMM(MODE, BM, BN)                                                               \
+  do {                                                                                       \
+    if (packed)                                                                              \
+      ffn_gemm_packed_kernel<MODE, BM, BN><<<grid, NTHR, 0, s>>>(A, W, C, work, n_work, d, m); \
+    else                                                                                     \
+      ffn_gemm_bf16_kernel<MODE, BM, BN><<<grid, NTHR, 0, s>>>(A, W, C, work, n_work, d, m);   \
   } while (0)
 
-hipError_t launch_gemm(int mode, int bm, bool wide, int n_items_max, const uint16_t* A,
+hipError_t launch_gemm(int mode, int bm, bool wide, bool packed, int n_items_max, const uint16_t* A,
                        const uint16_t* W, uint16_t* C, const Work* work, const int32_t* n_work,
                        int d, int m, hipStream_t s) {
   const int grid = (n_items_max + 7) & ~7;  // whole XCD rounds
-  const int nk = (mode == 0 ? d : m) / kern::BK;
-  const int tail = (nk - 3) % 4;
   if (mode == 0) {
     if (bm == 128) {
       if (wide) FFN_GEMM(0, 128, 512); else FFN_GEMM(0, 128, 256);
@@ -521,8 +761,8 @@ size_t ffn_ws_bytes(bool bf16, int rows_max, int E, int d, int m) {
 
 hipError_t launch_expert_ffn(const void* x_perm, bool bf16, const int32_t* offsets, int E,
                              const int32_t* K_dev, int n_K, int rows_max, int d, int m,
-                             const void* w_gate_up, const void* w_down, void* y_perm, void* ws,
-                             hipStream_t s) {
+                             const void* w_gate_up, const void* w_down, bool packed, void* y_perm,
+                             void* ws, hipStream_t s) {
   const int bm = bf16 ? pick_bm(rows_max, E) : FBM;
   const int max_tiles = max_tiles_for(rows_max, E, bm);
   int nn0, nn1;
@@ -534,11 +774,11 @@ hipError_t launch_expert_ffn(const void* x_perm, bool bf16, const int32_t* offse
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   if (bf16) {
-    err = launch_gemm(0, bm, wide0, max_tiles * nn0, static_cast<const uint16_t*>(x_perm),
+    err = launch_gemm(0, bm, wide0, packed, max_tiles * nn0, static_cast<const uint16_t*>(x_perm),
                       static_cast<const uint16_t*>(w_gate_up), static_cast<uint16_t*>(w.h),
                       w.work0, w.n_work, d, m, s);
     if (err != hipSuccess) return err;
-    return launch_gemm(1, bm, wide1, max_tiles * nn1, static_cast<const uint16_t*>(w.h),
+    return launch_gemm(1, bm, wide1, packed, max_tiles * nn1, static_cast<const uint16_t*>(w.h),
                        static_cast<const uint16_t*>(w_down), static_cast<uint16_t*>(y_perm),
                        w.work1, w.n_work, d, m, s);
   }
@@ -550,6 +790,14 @@ hipError_t launch_expert_ffn(const void* x_perm, bool bf16, const int32_t* offse
   ffn_gemm_f32_kernel<1><<<max_tiles * nn1, 256, 0, s>>>(
       static_cast<const float*>(w.h), static_cast<const float*>(w_down),
       static_cast<float*>(y_perm), w.work1, w.n_work, d, m);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_weights(const void* w, int E, int R, int K, void* out, hipStream_t s) {
+  const size_t n_chunks = (size_t)E * R * (K / 8);
+  if (n_chunks == 0) return hipSuccess;
+  pack_weights_kernel<<<(unsigned)((n_chunks + 255) / 256), 256, 0, s>>>(
+      static_cast<const uint4*>(w), R, K, n_chunks, static_cast<uint4*>(out));
   return hipGetLastError();
 }
 

@@ -6,6 +6,7 @@ the order of Algorithm 2 of the paper:
 
   dense span (before the visual exit):
       moe_route(x) -> moe_dispatch -> moe_expert_ffn -> moe_combine
+      (bf16 layers: moe_expert_ffn_packed on weights packed at load time)
   RCEP span (from the visual exit on):
       moe_route(x) [full pool] -> moe_calibrate_prefix [s, K]
       -> moe_route(logits, K) [prefix re-route] -> moe_dispatch
@@ -103,6 +104,14 @@ class MoELayer:
         self.bias = to_device(params["bias"], torch.float32, device)
         self.w_gate_up = to_device(params["w_gate_up"], self.dt, device)
         self.w_down = to_device(params["w_down"], self.dt, device)
+        # bf16 layers keep the expert weights in the packed fragment layout
+        # (moe_pack_expert_weights), re-laid out once here like the reorder
+        self.packed = self.dt == torch.bfloat16 and self.m % 128 == 0 and self.d % 256 == 0
+        if self.packed:
+            wgu, wd = torch.empty_like(self.w_gate_up), torch.empty_like(self.w_down)
+            abi.moe_pack_expert_weights(self.w_gate_up, wgu)
+            abi.moe_pack_expert_weights(self.w_down, wd)
+            self.w_gate_up, self.w_down = wgu, wd
         self.device = device
         self._bufs: dict = {}
 
@@ -119,8 +128,8 @@ class MoELayer:
         abi.moe_dispatch(idx, self.E, x, b.counts, b.offsets, b.src_of_row, b.row_of_slot,
                          b.x_perm, b.ws, stream=stream)
         mark()
-        abi.moe_expert_ffn(b.x_perm, b.offsets, self.w_gate_up, self.w_down, b.y_perm, b.ws,
-                           K_dev=K_dev, stream=stream)
+        ffn = abi.moe_expert_ffn_packed if self.packed else abi.moe_expert_ffn
+        ffn(b.x_perm, b.offsets, self.w_gate_up, self.w_down, b.y_perm, b.ws, K_dev=K_dev, stream=stream)
         mark()
         abi.moe_combine(b.y_perm, b.row_of_slot, w, b.out, stream=stream)
         mark()

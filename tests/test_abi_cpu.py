@@ -30,7 +30,8 @@ def lib():
 def test_header_declares_the_boundary():
     assert declared_functions() == sorted([
         "drop_visual_block", "moe_calibrate_prefix", "moe_combine", "moe_dispatch",
-        "moe_expert_ffn", "moe_route", "moe_status_string", "moe_workspace_size"])
+        "moe_expert_ffn", "moe_expert_ffn_packed", "moe_pack_expert_weights", "moe_route",
+        "moe_status_string", "moe_workspace_size"])
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -106,6 +107,28 @@ def test_ffn_rejects(lib):
     assert lib.moe_expert_ffn(P1, BF16, P2, 16, P6, 0, 64, 256, 128, P3, P4, P5, ws, 1 << 30, NULL) == EINVAL
     assert lib.moe_expert_ffn(P1, BF16, P2, 16, NULL, 0, 64, 256, 128, P3, P4, P5, ws, 16, NULL) == EWORKSPACE
     assert lib.moe_expert_ffn(P1, 7, P2, 16, NULL, 0, 64, 256, 128, P3, P4, P5, ws, 1 << 30, NULL) == EINVAL
+
+
+def test_packed_ffn_and_pack_reject(lib):
+    ws = ctypes.c_void_p(0x1000000)
+    # packed weights are bf16 only; same shape limits as the row-major call
+    assert lib.moe_expert_ffn_packed(P1, F32, P2, 16, NULL, 0, 64, 256, 128, P3, P4, P5, ws, 1 << 30,
+                                     NULL) == EUNSUPPORTED
+    assert lib.moe_expert_ffn_packed(P1, 7, P2, 16, NULL, 0, 64, 256, 128, P3, P4, P5, ws, 1 << 30,
+                                     NULL) == EINVAL
+    assert lib.moe_expert_ffn_packed(P1, BF16, P2, 16, NULL, 0, 64, 256, 64, P3, P4, P5, ws, 1 << 30,
+                                     NULL) == EUNSUPPORTED
+    assert lib.moe_expert_ffn_packed(P1, BF16, P2, 16, NULL, 0, 64, 256, 128, P3, P4, P5, ws, 16,
+                                     NULL) == EWORKSPACE
+    assert lib.moe_expert_ffn_packed(P1, BF16, P2, 16, NULL, 0, 64, 256, 128, P3, P4, P1, ws, 1 << 30,
+                                     NULL) == EALIAS
+    # pack: bf16 only, rows % 32 and cols % 16, no overlap, nothing to do for empty
+    assert lib.moe_pack_expert_weights(P1, F32, 4, 64, 64, P2, NULL) == EUNSUPPORTED
+    assert lib.moe_pack_expert_weights(P1, BF16, 4, 48, 64, P2, NULL) == EUNSUPPORTED
+    assert lib.moe_pack_expert_weights(P1, BF16, 4, 64, 40, P2, NULL) == EUNSUPPORTED
+    assert lib.moe_pack_expert_weights(P1, BF16, 4, 64, 64, P1, NULL) == EALIAS
+    assert lib.moe_pack_expert_weights(P1, BF16, -1, 64, 64, P2, NULL) == EINVAL
+    assert lib.moe_pack_expert_weights(P1, BF16, 0, 64, 64, P2, NULL) == 0
 
 
 def test_combine_and_drop_reject(lib):

@@ -327,6 +327,55 @@ def test_expert_ffn(E, d, m, dt, rows, K, cnt):
 
 
 # ---------------------------------------------------------------------------
+# packed expert weights: layout, then the packed FFN against the row-major one
+# ---------------------------------------------------------------------------
+def packed_layout(w):
+    """The documented fragment layout, written with reshapes: element (e, r, c)
+    goes to e*R*C + ((c//16)*(R//32) + r//32)*512 + 8*(r%32 + 32*((c%16)//8)) + c%8."""
+    E, R, C = w.shape
+    v = w.reshape(E, R // 32, 32, C // 16, 2, 8)          # e, rb, r, kb, h, c
+    return np.ascontiguousarray(v.transpose(0, 3, 1, 4, 2, 5)).reshape(E, R, C)  # e, kb, rb, h, r, c
+
+
+@pytest.mark.parametrize("E,R,C", [(3, 64, 48), (2, 1536, 2048), (5, 2048, 768), (1, 32, 16)])
+def test_pack_expert_weights_layout(E, R, C):
+    rng = np.random.default_rng(R + C)
+    w = rng.integers(0, 1 << 16, size=(E, R, C), dtype=np.uint16)
+    wt = dev(w.view(np.int16)).view(torch.bfloat16)
+    out = torch.empty_like(wt)
+    abi.moe_pack_expert_weights(wt, out)
+    torch.cuda.synchronize()
+    got = out.view(torch.int16).cpu().numpy().view(np.uint16)
+    assert np.array_equal(got, packed_layout(w))
+
+
+@pytest.mark.parametrize("E,d,m,dt,rows,K,cnt", [c for c in FFN_CASES if c[3] == "bf16"])
+def test_expert_ffn_packed(E, d, m, dt, rows, K, cnt):
+    sh = I.LayerShape(d=d, E=E, m=m, k=1, dtype=dt)
+    prm = I.layer_params(sh, seed=E + d)
+    counts = np.array(cnt, np.int64) if cnt is not None else I.synthetic_counts(E, rows, seed=rows)
+    rows = int(counts.sum())
+    offsets = dev(np.concatenate([[0], np.cumsum(counts)]).astype(np.int32))
+    xp = dev(I.synthetic_rows(rows, d, dt, seed=rows + 1), TDT[dt])
+    wgu, wd = dev(prm["w_gate_up"], TDT[dt]), dev(prm["w_down"], TDT[dt])
+    wgu_p, wd_p = torch.empty_like(wgu), torch.empty_like(wd)
+    abi.moe_pack_expert_weights(wgu, wgu_p)
+    abi.moe_pack_expert_weights(wd, wd_p)
+    ws = torch.empty(abi.moe_workspace_size(rows, E, 1, d, m, 1), dtype=torch.uint8, device="cuda")
+    K_dev = dev(np.array([K], np.int32)) if K is not None else None
+    y_ref = torch.full((rows, d), 7.0, dtype=TDT[dt], device="cuda")
+    y = torch.full((rows, d), 7.0, dtype=TDT[dt], device="cuda")
+    abi.moe_expert_ffn(xp, offsets, wgu, wd, y_ref, ws, K_dev=K_dev)
+    abi.moe_expert_ffn_packed(xp, offsets, wgu_p, wd_p, y, ws, K_dev=K_dev)
+    # same fragments, same k order, same float32 accumulation: bitwise equal
+    assert torch.equal(y.view(torch.int16), y_ref.view(torch.int16))
+    expert_of_row = np.repeat(np.arange(E), counts)
+    live = expert_of_row < (K if K is not None else E)
+    ref = oracle.expert_ffn_rows(host(xp)[live], expert_of_row[live], prm["w_gate_up"], prm["w_down"])
+    assert rel_inf(host(y)[live], ref) <= TOL[dt]
+
+
+# ---------------------------------------------------------------------------
 # moe_combine
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("T,k,d,dt", [(512, 2, 256, "f32"), (4096, 8, 2048, "bf16"), (1, 8, 2048, "bf16"),
