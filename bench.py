@@ -220,7 +220,7 @@ def main() -> int:
     f, b = fb("ffn", T, touched_d)
     ffn_roof = roofline(f, b, stage_ms["ffn"] * 1e-3)
     ffn_roof["traffic"] = None
-    ffn_roof["kernel"] = ("moe_expert_ffn_packed @ dense 4096 rows (ffn_tiles + gate/up GEMM + down GEMM "
+    ffn_roof["kernel"] = ("moe_expert_ffn_packed @ dense 4096 rows (gate/up GEMM + down GEMM launches "
                           "on packed bf16 weights)")
     ffn_roof["mfma_frac"] = f / (stage_ms["ffn"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS
 

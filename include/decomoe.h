@@ -95,6 +95,10 @@ size_t moe_workspace_size(int T, int E, int k, int d, int m, int n_seg);
  *   topk_w     [T, k] float32: the softmax over [0, K) restricted to the
  *              selected experts and renormalised, i.e. the softmax of the
  *              k selected logits; each row sums to 1.
+ *   ws         scratch (moe_workspace_size): when x != NULL and T is small
+ *              the logits are computed in d-range splits whose partial sums
+ *              are added in a fixed order (deterministic); NULL is allowed
+ *              when no split is needed, else MOE_EWORKSPACE.
  * Limits: 1 <= k <= min(E, 32); 1 <= E <= 1024; T >= 0; d >= 1; for bf16 x,
  * d % 8 == 0.  Logits must be finite.  x == NULL with logits == NULL is
  * MOE_EINVAL.
@@ -103,7 +107,7 @@ int moe_route(const void* x, moe_dtype dtype, const float* w_r, const float* bia
               int T, int d, int E, int k,
               const int32_t* seg_offsets, int n_seg, const int32_t* K_dev,
               float* logits, int32_t* topk_idx, float* topk_w,
-              hipStream_t stream);
+              void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * moe_calibrate_prefix - activated mass, prefix length and Mean-Mass order
@@ -125,16 +129,20 @@ int moe_route(const void* x, moe_dtype dtype, const float* w_r, const float* bia
  *                     mean, equal means keeping the lower index first.
  *                     order[j] is the expert placed at position j.  With no
  *                     non-empty segment the order is the identity.
+ * A token's experts are distinct in moe_route output; an expert repeated
+ * within a token enters as the sum of its weights (summed in unspecified
+ * order when it repeats three times or more).
  * Each segment's masses are one float64 running sum per expert in ascending
  * token order, and c_K one running sum in expert order, so K depends on the
  * inputs only (no reduction-order effects).  Index entries outside [0, E)
- * are skipped.  No workspace is needed.
+ * are skipped.  Limits: 1 <= k <= min(E, 32).  ws / ws_bytes: scratch per
+ * moe_workspace_size; this build needs none (NULL, 0 are accepted).
  */
 int moe_calibrate_prefix(const int32_t* topk_idx, const float* topk_w,
                          int T, int E, int k,
                          const int32_t* seg_offsets, int n_seg, double p,
                          double* mass, int32_t* K_out, int32_t* order,
-                         hipStream_t stream);
+                         void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * moe_dispatch - group the T*k (token, slot) assignments by expert

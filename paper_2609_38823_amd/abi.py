@@ -48,8 +48,8 @@ def load() -> ctypes.CDLL:
     sig = {
         "moe_status_string": (ctypes.c_char_p, [_I]),
         "moe_workspace_size": (_S, [_I, _I, _I, _I, _I, _I]),
-        "moe_route": (_I, [_P, _I, _P, _P, _I, _I, _I, _I, _P, _I, _P, _P, _P, _P, _P]),
-        "moe_calibrate_prefix": (_I, [_P, _P, _I, _I, _I, _P, _I, _D, _P, _P, _P, _P]),
+        "moe_route": (_I, [_P, _I, _P, _P, _I, _I, _I, _I, _P, _I, _P, _P, _P, _P, _P, _S, _P]),
+        "moe_calibrate_prefix": (_I, [_P, _P, _I, _I, _I, _P, _I, _D, _P, _P, _P, _P, _S, _P]),
         "moe_dispatch": (_I, [_P, _I, _I, _I, _P, _I, _I, _P, _P, _P, _P, _P, _P, _S, _P]),
         "moe_expert_ffn": (_I, [_P, _I, _P, _I, _P, _I, _I, _I, _I, _P, _P, _P, _P, _S, _P]),
         "moe_expert_ffn_packed": (_I, [_P, _I, _P, _I, _P, _I, _I, _I, _I, _P, _P, _P, _P, _S, _P]),
@@ -108,7 +108,11 @@ def moe_workspace_size(T: int, E: int, k: int, d: int, m: int, n_seg: int = 1) -
     return int(load().moe_workspace_size(T, E, k, d, m, n_seg))
 
 
-def moe_route(x, w_r, bias, k, logits, topk_idx, topk_w, seg_offsets=None, K_dev=None,
+def _nbytes(ws):
+    return ws.numel() * ws.element_size() if ws is not None else 0
+
+
+def moe_route(x, w_r, bias, k, logits, topk_idx, topk_w, seg_offsets=None, K_dev=None, ws=None,
               stream=None):
     """x [T, d] or None (then `logits` [T, E] is an input)."""
     T, E = logits.shape
@@ -117,15 +121,15 @@ def moe_route(x, w_r, bias, k, logits, topk_idx, topk_w, seg_offsets=None, K_dev
     _check("moe_route", load().moe_route(
         _p(x), dt, _p(w_r) if x is not None else None, _p(bias) if x is not None else None,
         T, d, E, k, _p(seg_offsets), _nseg(seg_offsets), _p(K_dev),
-        _p(logits), _p(topk_idx), _p(topk_w), _stream(stream)))
+        _p(logits), _p(topk_idx), _p(topk_w), _p(ws), _nbytes(ws), _stream(stream)))
 
 
-def moe_calibrate_prefix(topk_idx, topk_w, E, p, mass, K_out=None, order=None,
+def moe_calibrate_prefix(topk_idx, topk_w, E, p, mass, ws, K_out=None, order=None,
                          seg_offsets=None, stream=None):
     T, k = topk_idx.shape
     _check("moe_calibrate_prefix", load().moe_calibrate_prefix(
         _p(topk_idx), _p(topk_w), T, E, k, _p(seg_offsets), _nseg(seg_offsets), float(p),
-        _p(mass), _p(K_out), _p(order), _stream(stream)))
+        _p(mass), _p(K_out), _p(order), _p(ws), _nbytes(ws), _stream(stream)))
 
 
 def moe_dispatch(topk_idx, E, x, counts, offsets, src_of_row, row_of_slot, x_perm, ws,

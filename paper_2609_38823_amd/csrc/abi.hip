@@ -6,8 +6,10 @@
 
 namespace {
 
+using decomoe::calibrate_ws_bytes;
 using decomoe::dispatch_ws_bytes;
 using decomoe::ffn_ws_bytes;
+using decomoe::route_ws_bytes;
 
 constexpr int kMaxE = 1024;
 constexpr int kMaxK = 32;
@@ -93,17 +95,18 @@ const char* moe_status_string(int status) {
 size_t moe_workspace_size(int T, int E, int k, int d, int m, int n_seg) {
   if (T < 0 || E < 1 || E > kMaxE || k < 1 || k > E || d < 1 || m < 1 || n_seg < 1) return 0;
   size_t rows = (size_t)T * k;
-  size_t a = a256(dispatch_ws_bytes(T, k, E));
-  size_t b = ffn_ws_bytes(true, (int)rows, E, d, m);
-  size_t c = ffn_ws_bytes(false, (int)rows, E, d, m);
-  size_t w = a > b ? a : b;
-  w = w > c ? w : c;
-  return w < 256 ? 256 : w;
+  size_t w = 256;
+  for (size_t b : {a256(dispatch_ws_bytes(T, k, E)), ffn_ws_bytes(true, (int)rows, E, d, m),
+                   ffn_ws_bytes(false, (int)rows, E, d, m), a256(route_ws_bytes(T, d, E)),
+                   a256(calibrate_ws_bytes(T, E))})
+    w = b > w ? b : w;
+  return w;
 }
 
 int moe_route(const void* x, moe_dtype dtype, const float* w_r, const float* bias, int T, int d,
               int E, int k, const int32_t* seg_offsets, int n_seg, const int32_t* K_dev,
-              float* logits, int32_t* topk_idx, float* topk_w, hipStream_t stream) {
+              float* logits, int32_t* topk_idx, float* topk_w, void* ws, size_t ws_bytes,
+              hipStream_t stream) {
   if (T < 0 || E < 1 || E > kMaxE || k < 1 || k > E) return MOE_EINVAL;
   if (k > kMaxK) return MOE_EUNSUPPORTED;
   if (!seg_offsets) n_seg = 1;
@@ -115,43 +118,51 @@ int moe_route(const void* x, moe_dtype dtype, const float* w_r, const float* bia
   }
   if (T == 0) return MOE_OK;
   if (!topk_idx || !topk_w) return MOE_EINVAL;
-  if (!aligned_all({x, w_r, bias, seg_offsets, K_dev, logits, topk_idx, topk_w})) return MOE_EINVAL;
+  if (!aligned_all({x, w_r, bias, seg_offsets, K_dev, logits, topk_idx, topk_w, ws})) return MOE_EINVAL;
+  const size_t need = x ? route_ws_bytes(T, d, E) : 0;
+  if (need && (!ws || ws_bytes < need)) return MOE_EWORKSPACE;
   const size_t nl = (size_t)T * E * 4, nk = (size_t)T * k * 4;
+  Range o_ws = need ? rng(ws, need) : Range{0, 0};
   Range in_x = x ? rng(x, (size_t)T * d * elt_size(dtype)) : Range{0, 0};
   Range in_w = x ? rng(w_r, (size_t)d * E * 4) : Range{0, 0};
   Range in_b = (x && bias) ? rng(bias, (size_t)E * 4) : Range{0, 0};
   Range in_s = seg_offsets ? rng(seg_offsets, (size_t)(n_seg + 1) * 4) : Range{0, 0};
   Range in_k = K_dev ? rng(K_dev, (size_t)n_seg * 4) : Range{0, 0};
   if (x) {
-    if (any_alias({rng(logits, nl), rng(topk_idx, nk), rng(topk_w, nk)}, {in_x, in_w, in_b, in_s, in_k}))
+    if (any_alias({rng(logits, nl), rng(topk_idx, nk), rng(topk_w, nk), o_ws},
+                  {in_x, in_w, in_b, in_s, in_k}))
       return MOE_EALIAS;
-    hipError_t e = decomoe::launch_router_logits(x, dtype == MOE_BF16, w_r, bias, T, d, E, logits, stream);
-    if (e != hipSuccess) return MOE_EHIP;
   } else {
     if (any_alias({rng(topk_idx, nk), rng(topk_w, nk)}, {rng(logits, nl), in_s, in_k})) return MOE_EALIAS;
   }
-  return hip_status(decomoe::launch_topk(logits, T, E, k, seg_offsets, n_seg, K_dev, topk_idx,
-                                         topk_w, stream));
+  return hip_status(decomoe::launch_route(x, dtype == MOE_BF16, w_r, bias, T, d, E, k, seg_offsets,
+                                          n_seg, K_dev, logits, topk_idx, topk_w, ws, stream));
 }
 
 int moe_calibrate_prefix(const int32_t* topk_idx, const float* topk_w, int T, int E, int k,
                          const int32_t* seg_offsets, int n_seg, double p, double* mass,
-                         int32_t* K_out, int32_t* order, hipStream_t stream) {
+                         int32_t* K_out, int32_t* order, void* ws, size_t ws_bytes,
+                         hipStream_t stream) {
   if (T < 0 || E < 1 || E > kMaxE || k < 1 || k > E) return MOE_EINVAL;
+  if (k > kMaxK) return MOE_EUNSUPPORTED;
   if (!seg_offsets) n_seg = 1;
   if (n_seg < 1) return MOE_EINVAL;
   if (!(p > 0.0 && p <= 1.0)) return MOE_EINVAL;
   if (!mass || (T > 0 && (!topk_idx || !topk_w))) return MOE_EINVAL;
-  if (!aligned_all({topk_idx, topk_w, seg_offsets, mass, K_out, order})) return MOE_EINVAL;
+  if (!aligned_all({topk_idx, topk_w, seg_offsets, mass, K_out, order, ws})) return MOE_EINVAL;
+  const size_t need = calibrate_ws_bytes(T, E);
+  if (need && (!ws || ws_bytes < need)) return MOE_EWORKSPACE;
   const size_t nk = (size_t)T * k * 4;
   Range in_i = T ? rng(topk_idx, nk) : Range{0, 0};
   Range in_w = T ? rng(topk_w, nk) : Range{0, 0};
   Range in_s = seg_offsets ? rng(seg_offsets, (size_t)(n_seg + 1) * 4) : Range{0, 0};
   Range o_k = K_out ? rng(K_out, (size_t)n_seg * 4) : Range{0, 0};
   Range o_o = order ? rng(order, (size_t)E * 4) : Range{0, 0};
-  if (any_alias({rng(mass, (size_t)n_seg * E * 8), o_k, o_o}, {in_i, in_w, in_s})) return MOE_EALIAS;
+  Range o_ws = need ? rng(ws, need) : Range{0, 0};
+  if (any_alias({rng(mass, (size_t)n_seg * E * 8), o_k, o_o, o_ws}, {in_i, in_w, in_s}))
+    return MOE_EALIAS;
   return hip_status(decomoe::launch_calibrate(topk_idx, topk_w, T, E, k, seg_offsets, n_seg, p,
-                                              mass, K_out, order, stream));
+                                              mass, K_out, order, ws, stream));
 }
 
 int moe_dispatch(const int32_t* topk_idx, int T, int k, int E, const void* x, moe_dtype dtype,

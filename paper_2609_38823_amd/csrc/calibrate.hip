@@ -1,27 +1,32 @@
 // Activated mass, prefix length and Mean-Mass order (Eqs. 8, 9, 11, 12).
 //
-// One workgroup per invocation (segment).  The segment's renormalised Top-k
-// weights are scattered, up to 128 tokens per pass, into a dense LDS table
-// [token][expert]; thread e then adds its column to a float64 running sum in
-// ascending token order.  The next pass's entries are fetched into registers
-// while the current pass is summed.  Every expert's mass is therefore one sequential
-// float64 sum in token order (no atomics, no tree), and the running prefix
-// sum over experts that decides K is sequential too.
+//   mass     one workgroup per invocation (segment) stages the routing
+//            entries of up to 8192 / k tokens with one bulk load, then walks
+//            them in chunks: the chunk's routed weights are scattered into a dense
+//            LDS table [token][expert] (float64), then thread e adds column
+//            e to its running sum in ascending token order and clears it --
+//            one float64 running sum per expert over the tokens, the same
+//            sequence of additions as the plain definition (zeros of
+//            unrouted tokens add nothing).  One thread then forms the running
+//            sum c_K over the experts and wave 0 finds K with a ballot.
+//   order    Mean-Mass order over the segments taken as calibration cases
 #include "common.hpp"
 
 namespace decomoe {
 namespace {
 
-constexpr int CAL_THREADS = 256;
-constexpr int CAL_TABLE = 16384;  // doubles in the dense LDS table (128 KB)
-constexpr int CAL_STAGE = 1024;   // routing entries staged per pass
-constexpr int CAL_EPT = CAL_STAGE / CAL_THREADS;
+constexpr int CAL_THREADS = 1024;
+constexpr int CAL_TABLE = 8192;  // doubles in the LDS table (64 KB)
+constexpr int CAL_STAGE = 8192;  // routing entries staged per bulk load (64 KB)
 
-// Tokens per pass: the table holds sub x E doubles and the stage sub x k entries.
-__host__ __device__ inline int cal_sub(int E, int k) {
-  int s = CAL_TABLE / E;
-  if (s * k > CAL_STAGE) s = CAL_STAGE / k;
-  return s < 128 ? s : 128;
+constexpr int CAL_ENT = 1024;   // routing entries scattered per chunk (one per thread)
+
+// Tokens per chunk: the table holds ch x E doubles and a chunk holds at most
+// CAL_ENT routing entries.
+__host__ __device__ inline int cal_chunk(int E, int k) {
+  int c = CAL_TABLE / E;
+  if (c * k > CAL_ENT) c = CAL_ENT / k;
+  return c < 64 ? c : 64;
 }
 
 __global__ __launch_bounds__(CAL_THREADS) void segment_mass_kernel(
@@ -29,9 +34,9 @@ __global__ __launch_bounds__(CAL_THREADS) void segment_mass_kernel(
     const int32_t* __restrict__ seg_offsets, double p, double* __restrict__ mass,
     int32_t* __restrict__ K_out) {
   __shared__ double table[CAL_TABLE];
-  __shared__ int stage_e[CAL_STAGE];
-  __shared__ float stage_w[CAL_STAGE];
   __shared__ double smass[1024];
+  __shared__ int st_e[CAL_STAGE];
+  __shared__ float st_w[CAL_STAGE];
   const int seg = blockIdx.x;
   const int tid = threadIdx.x;
   int lo = 0, hi = T;
@@ -39,80 +44,100 @@ __global__ __launch_bounds__(CAL_THREADS) void segment_mass_kernel(
     lo = clampi(seg_offsets[seg], 0, T);
     hi = clampi(seg_offsets[seg + 1], lo, T);
   }
-  const int sub = cal_sub(E, k);
-  constexpr int EPT = 1024 / CAL_THREADS;  // experts per thread, at most 4
-  double acc[EPT] = {};
-
-  // one pass's entries, prefetched into registers one pass ahead
-  int pe[CAL_EPT];
-  float pw[CAL_EPT];
-  auto fetch = [&](int t0) {
-    const int n = min(sub, hi - t0) * k;
-    const size_t base = (size_t)t0 * k;
+  const int ch = cal_chunk(E, k);
+  const int super_t = (CAL_STAGE / k) / ch * ch;  // tokens staged per bulk load
+  for (int i = tid; i < ch * E; i += CAL_THREADS) table[i] = 0.0;
+  double acc = 0.0;
+  for (int s0 = lo; s0 < hi; s0 += super_t) {
+    // stage the routing entries of up to super_t tokens with one bulk load
+    const int n_ent = min(super_t, hi - s0) * k;
+    __syncthreads();  // previous stage fully consumed
+    {
+      constexpr int SPT = CAL_STAGE / CAL_THREADS;  // all loads in flight together
+      int re[SPT];
+      float rw[SPT];
 #pragma unroll
-    for (int j = 0; j < CAL_EPT; ++j) {
-      const int i = tid + j * CAL_THREADS;
-      pe[j] = i < n ? idx[base + i] : -1;
-      pw[j] = i < n ? w[base + i] : 0.f;
-    }
-  };
-
-  for (int i = tid; i < sub * E; i += CAL_THREADS) table[i] = 0.0;
-  if (lo < hi) fetch(lo);
-  for (int t0 = lo; t0 < hi; t0 += sub) {
-    const int nt = min(sub, hi - t0);
+      for (int q = 0; q < SPT; ++q) {
+        const int i = tid + q * CAL_THREADS;
+        re[q] = i < n_ent ? idx[(size_t)s0 * k + i] : -1;
+        rw[q] = i < n_ent ? w[(size_t)s0 * k + i] : 0.f;
+      }
 #pragma unroll
-    for (int j = 0; j < CAL_EPT; ++j) {
-      stage_e[tid + j * CAL_THREADS] = pe[j];
-      stage_w[tid + j * CAL_THREADS] = pw[j];
-    }
-    __syncthreads();
-    if (t0 + sub < hi) fetch(t0 + sub);
-    // one thread per token adds its slots in slot order
-    if (tid < nt) {
-      for (int j = 0; j < k; ++j) {
-        const int e = stage_e[tid * k + j];
-        if (e >= 0 && e < E) table[tid * E + e] += static_cast<double>(stage_w[tid * k + j]);
+      for (int q = 0; q < SPT; ++q) {
+        st_e[tid + q * CAL_THREADS] = re[q];
+        st_w[tid + q * CAL_THREADS] = rw[q];
       }
     }
     __syncthreads();
-    // expert columns: one float64 running sum per expert, ascending token
+    for (int t0 = s0; t0 < min(s0 + super_t, hi); t0 += ch) {
+      const int nt = min(ch, hi - t0);
+      // scatter: a token's experts are distinct (Top-k), so each cell gets
+      // one addition onto 0.0 and holds the weight exactly; a repeated
+      // expert adds its weights into the cell
 #pragma unroll
-    for (int c = 0; c < EPT; ++c) {
-      const int e = tid + c * CAL_THREADS;
-      if (e < E)
-        for (int r = 0; r < nt; ++r) acc[c] += table[r * E + e];
-    }
-    __syncthreads();
-    if (tid < nt) {
-      for (int j = 0; j < k; ++j) {
-        const int e = stage_e[tid * k + j];
-        if (e >= 0 && e < E) table[tid * E + e] = 0.0;
+      for (int q = 0; q < CAL_ENT / CAL_THREADS; ++q) {
+        const int j = tid + q * CAL_THREADS;
+        if (j < nt * k) {
+          const int i = (t0 - s0) * k + j;
+          const int e = st_e[i];
+          if (e >= 0 && e < E) atomicAdd(&table[(j / k) * E + e], static_cast<double>(st_w[i]));
+        }
       }
+      __syncthreads();
+      // column sums: thread e adds column e in ascending token order, then
+      // clears it for the next chunk
+      if (tid < E) {
+        double a = acc;
+#pragma unroll 8
+        for (int r = 0; r < nt; ++r) {
+          a += table[r * E + tid];
+          table[r * E + tid] = 0.0;
+        }
+        acc = a;
+      }
+      __syncthreads();
     }
-    __syncthreads();
   }
-#pragma unroll
-  for (int c = 0; c < EPT; ++c) {
-    const int e = tid + c * CAL_THREADS;
-    if (e < E) {
-      mass[(size_t)seg * E + e] = acc[c];
-      smass[e] = acc[c];
-    }
+  if (tid < E) {
+    mass[(size_t)seg * E + tid] = acc;
+    smass[tid] = acc;
   }
   __syncthreads();
-  if (tid == 0 && K_out) {
-    // c_K running sum in expert order; tot = c_E; first K with c_K >= p*tot
-    double run = 0.0;
-    for (int e = 0; e < E; ++e) {
-      run += smass[e];
-      table[e] = run;
+  if (K_out) {
+    // c_K: one running sum in expert order by a single thread (the same
+    // sequence of float64 additions as the definition), 8 masses per batch
+    // of LDS reads; the c_K go to LDS and wave 0 finds the first K with
+    // c_K >= p * tot by a ballot
+    double* cbuf = table;  // the table is free now
+    __shared__ double s_tot;
+    if (tid == 0) {
+      double run = 0.0;
+      for (int e0 = 0; e0 < E; e0 += 8) {
+        double v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = e0 + j < E ? smass[e0 + j] : 0.0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (e0 + j < E) {
+            run += v[j];
+            cbuf[e0 + j] = run;
+          }
+      }
+      s_tot = run;  // tot = c_E
     }
-    const double thr = p * run;
-    int k_hat = E;
-    for (int K = 1; K <= E; ++K)
-      if (table[K - 1] >= thr) { k_hat = K; break; }
-    K_out[seg] = k_hat > k ? k_hat : k;
+    __syncthreads();
+    if (tid < kWave) {
+      const double thr = p * s_tot;
+      int k_hat = E;
+      for (int e0 = 0; e0 < E; e0 += kWave) {
+        const unsigned long long hit = __ballot(e0 + tid < E && cbuf[e0 + tid] >= thr);
+        if (hit) {
+          k_hat = e0 + __ffsll((long long)hit);  // K = index + 1
+          break;
+        }
+      }
+      if (tid == 0) K_out[seg] = k_hat > k ? k_hat : k;
+    }
   }
 }
 
@@ -153,9 +178,16 @@ __global__ __launch_bounds__(1024) void mean_mass_order_kernel(
 }
 }  // namespace
 
+size_t calibrate_ws_bytes(int T, int E) {
+  (void)T;
+  (void)E;
+  return 0;  // the dense table lives in LDS
+}
+
 hipError_t launch_calibrate(const int32_t* idx, const float* w, int T, int E, int k,
                             const int32_t* seg_offsets, int n_seg, double p, double* mass,
-                            int32_t* K_out, int32_t* order, hipStream_t s) {
+                            int32_t* K_out, int32_t* order, void* ws, hipStream_t s) {
+  (void)ws;
   segment_mass_kernel<<<n_seg, CAL_THREADS, 0, s>>>(idx, w, T, E, k, seg_offsets, p, mass, K_out);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess || !order) return err;

@@ -36,13 +36,16 @@ __device__ __forceinline__ int find_segment(const int32_t* seg_offsets, int n_se
 }
 
 // ---- launchers (host side; return hipError_t of the launch) -------------
-hipError_t launch_router_logits(const void* x, bool x_bf16, const float* w_r, const float* bias,
-                                int T, int d, int E, float* logits, hipStream_t s);
-hipError_t launch_topk(const float* logits, int T, int E, int k, const int32_t* seg_offsets,
-                       int n_seg, const int32_t* K_dev, int32_t* idx, float* w, hipStream_t s);
+size_t route_ws_bytes(int T, int d, int E);
+// logits (x != NULL) and Top-k in one call; x == NULL reads `logits`
+hipError_t launch_route(const void* x, bool x_bf16, const float* w_r, const float* bias, int T,
+                        int d, int E, int k, const int32_t* seg_offsets, int n_seg,
+                        const int32_t* K_dev, float* logits, int32_t* idx, float* w, void* ws,
+                        hipStream_t s);
+size_t calibrate_ws_bytes(int T, int E);
 hipError_t launch_calibrate(const int32_t* idx, const float* w, int T, int E, int k,
                             const int32_t* seg_offsets, int n_seg, double p, double* mass,
-                            int32_t* K_out, int32_t* order, hipStream_t s);
+                            int32_t* K_out, int32_t* order, void* ws, hipStream_t s);
 size_t dispatch_ws_bytes(int T, int k, int E);
 hipError_t launch_dispatch(const int32_t* idx, int T, int k, int E, const void* x, int elt, int d,
                            int32_t* counts, int32_t* offsets, int32_t* src_of_row,

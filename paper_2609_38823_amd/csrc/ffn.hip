@@ -3,16 +3,22 @@
 // projections as in App. A.3, Eq. 15).
 //
 //   tiles     a one-workgroup kernel turns the per-expert row ranges into a
-//             list of (expert, first row, rows) M-tiles on the device, so no
-//             host synchronisation is needed on K or on the counts
+//             list of (expert, first row, rows, n-tile) work items on the
+//             device, so no host synchronisation is needed on K or on the
+//             counts
 //   gate_up   H[r, :] = SiLU(X W_gate^T) * (X W_up^T) for the rows of one
-//             M-tile; the gate and up weight rows of the same h columns sit
-//             in one B tile, so SwiGLU is applied in registers
+//             M-tile; the gate and up weight rows of the same h columns are
+//             owned by the same wavefront, so SwiGLU is applied in registers
 //   down      Y = H W_down^T
 //
-// bf16: v_mfma_f32_16x16x32_bf16, 128x128x64 block tiles, 4 wavefronts of
-// 64x64, LDS double buffered with an XOR swizzle of the 16-byte chunks
-// (conflict-free ds_read_b128 of the MFMA fragments), float32 accumulation.
+// bf16: v_mfma_f32_32x32x16_bf16 with float32 accumulation; 4 wavefronts per
+// workgroup, each owning BM token rows x (BN/4) weight rows.  Two variants:
+//   row-major weights  both operands stream global -> LDS (buffer_load ...
+//                      lds) through a 4-stage ring; BN = 512 or 256
+//   packed weights     the weight operand streams from the fragment layout
+//                      of moe_pack_expert_weights straight into registers;
+//                      only the token rows use LDS; BN = 256 at two
+//                      workgroups per CU
 // float32: a plain LDS-tiled SIMT kernel (correctness path for small layers).
 #include <type_traits>
 
@@ -28,59 +34,103 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 
 // ---------------------------------------------------------------------------
-// M-tile list.  Experts e < Klim with rows [offsets[e], offsets[e+1]) (clamped
-// to [0, rows_max]) become ceil(rows / bm) tiles, expert-major.  For each of
-// the two GEMMs (nn0, nn1 n-tiles) it also writes the work list: one item per
-// (m-tile, n-tile), ordered expert-major, then n-tile, then m-tile, so that a
-// workgroup needs a single load to know its work.
+// Work items.  Experts e < Klim (Klim = max K_dev, or E) with rows
+// [offsets[e], offsets[e+1]) (clamped to [0, rows_max]) become ceil(rows/bm)
+// M-tiles; with nn n-tiles per GEMM the work list is ordered expert-major,
+// then n-tile, then m-tile, and holds at most max_tiles * nn items.  Every
+// workgroup derives its own item from the offsets (a block-wide scan over
+// the experts), so no host synchronisation on K or on the counts is needed
+// and no separate launch builds the list.
 // ---------------------------------------------------------------------------
 struct Work {
   int expert, row0, rows, nt;
 };
 
-__global__ __launch_bounds__(1024) void ffn_tiles_kernel(const int32_t* __restrict__ offsets,
-                                                         int E, const int32_t* __restrict__ K_dev,
-                                                         int n_K, int rows_max, int bm, int max_tiles,
-                                                         int nn0, int nn1, Work* __restrict__ work0,
-                                                         Work* __restrict__ work1,
-                                                         int32_t* __restrict__ n_work) {
-  __shared__ int sc[1024];
-  const int e = threadIdx.x;
-  int Klim = E;
-  if (K_dev) {
-    Klim = 0;
-    for (int i = 0; i < n_K; ++i) Klim = max(Klim, K_dev[i]);
-    Klim = clampi(Klim, 0, E);
-  }
-  int lo = 0, hi = 0, nt = 0;
-  if (e < Klim) {
-    lo = clampi(offsets[e], 0, rows_max);
-    hi = clampi(offsets[e + 1], lo, rows_max);
-    nt = (hi - lo + bm - 1) / bm;
-  }
-  sc[e] = nt;
+struct Tiles {
+  const int32_t* offsets;
+  const int32_t* K_dev;
+  int E, n_K, rows_max, bm, max_tiles, nn;
+};
+
+constexpr int NTHR = 256;  // threads per GEMM workgroup (4 wavefronts)
+
+// Fills `out` with work item L and returns true, or returns false (for the
+// whole workgroup) when L is past the end of the list.  With `xcd`, L follows
+// the XCD-aware order: workgroup b runs on XCD b % 8, so XCD x is given the
+// contiguous range [x n/8, (x+1) n/8) of the n-item list -- the m-tiles that
+// share a weight tile, and the n-tiles that share an expert's rows, run
+// together and meet in one L2, and every XCD gets an equal share.
+// Otherwise L = blockIdx.x.  Supports E <= 4 * NTHR.  `lds` is 64 bytes of
+// LDS that the caller may reuse as soon as this returns.
+__device__ __forceinline__ bool find_work(const Tiles& tl, bool xcd, Work& out, char* lds) {
+  int* s_part = reinterpret_cast<int*>(lds);           // [NTHR / 64]
+  int& s_klim = reinterpret_cast<int*>(lds)[NTHR / 64];
+  Work& s_wk = *reinterpret_cast<Work*>(lds + 32);
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  if (tid == 0) s_klim = 0;
   __syncthreads();
-  for (int off = 1; off < 1024; off <<= 1) {
-    int v = e >= off ? sc[e - off] : 0;
-    __syncthreads();
-    sc[e] += v;
-    __syncthreads();
+  int Klim = tl.E;
+  if (tl.K_dev) {
+    int mx = 0;
+    for (int i = tid; i < tl.n_K; i += NTHR) mx = max(mx, tl.K_dev[i]);
+    if (mx > 0) atomicMax(&s_klim, mx);
   }
-  const int total = min(sc[1023], max_tiles);
-  const int start = sc[e] - nt;
-  const int cnt = max(0, min(nt, total - start));  // tiles of this expert kept
-  for (int o = 0; o < nn0 * cnt; ++o) {
-    const int mt = o % cnt, r0 = lo + mt * bm;
-    work0[nn0 * start + o] = Work{e, r0, min(bm, hi - r0), o / cnt};
+  int lo[4], hi[4], cnt[4], local = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = 4 * tid + q;
+    lo[q] = hi[q] = 0;
+    if (e < tl.E) {
+      lo[q] = clampi(tl.offsets[e], 0, tl.rows_max);
+      hi[q] = clampi(tl.offsets[e + 1], lo[q], tl.rows_max);
+    }
   }
-  for (int o = 0; o < nn1 * cnt; ++o) {
-    const int mt = o % cnt, r0 = lo + mt * bm;
-    work1[nn1 * start + o] = Work{e, r0, min(bm, hi - r0), o / cnt};
+  __syncthreads();
+  if (tl.K_dev) Klim = clampi(s_klim, 0, tl.E);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    cnt[q] = 4 * tid + q < Klim ? (hi[q] - lo[q] + tl.bm - 1) / tl.bm : 0;
+    local += cnt[q];
   }
-  if (e == 1023) {
-    n_work[0] = total * nn0;
-    n_work[1] = total * nn1;
+  int incl = local;  // inclusive scan over the wavefront
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += y;
   }
+  if (lane == 63) s_part[wv] = incl;
+  __syncthreads();
+  int base = 0, total = 0;
+#pragma unroll
+  for (int i = 0; i < NTHR / 64; ++i) {
+    if (i < wv) base += s_part[i];
+    total += s_part[i];
+  }
+  total = min(total, tl.max_tiles);
+  const int n_items = total * tl.nn;
+  int L = blockIdx.x;
+  if (xcd) {
+    const int per_xcd = (n_items + 7) >> 3;
+    const int slot = blockIdx.x >> 3;
+    if (slot >= per_xcd) return false;
+    L = (blockIdx.x & 7) * per_xcd + slot;
+  }
+  if (L >= n_items) return false;
+  int start = base + incl - local;  // first tile of this thread's first expert
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int c = min(cnt[q], max(0, total - start));  // tiles kept
+    if (c > 0 && L >= tl.nn * start && L < tl.nn * (start + c)) {
+      const int o = L - tl.nn * start;
+      const int r0 = lo[q] + (o % c) * tl.bm;
+      s_wk = Work{4 * tid + q, r0, min(tl.bm, hi[q] - r0), o / c};
+    }
+    start += cnt[q];
+  }
+  __syncthreads();
+  out = s_wk;
+  __syncthreads();  // every thread holds its copy before the caller reuses `lds`
+  return true;
 }
 
 // ---------------------------------------------------------------------------
@@ -101,7 +151,7 @@ __global__ __launch_bounds__(1024) void ffn_tiles_kernel(const int32_t* __restri
 // distinct bank groups.  The two 16-wide k-substeps of a stage are
 // software-pipelined in registers.
 // ---------------------------------------------------------------------------
-constexpr int BK = 32, NTHR = 256;
+constexpr int BK = 32;
 constexpr int LDS_STAGE_MAX = (128 + 512) * BK * 2;  // bytes, largest tile pair
 
 __shared__ __attribute__((aligned(1024))) char ring0[LDS_STAGE_MAX];
@@ -202,7 +252,7 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[MI][NI], char* re
 template <int MODE, int BM, int BN>
 __global__ __launch_bounds__(NTHR, 1) void ffn_gemm_bf16_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ W, uint16_t* __restrict__ C,
-    const Work* __restrict__ work, const int32_t* __restrict__ n_work, int d, int m) {
+    const Tiles tl, int d, int m) {
   constexpr int MI = BM / 32;             // 32-row fragments per wave (all tile rows)
   constexpr int NI = BN / 128;            // 32-col fragments per wave
   constexpr int AG = BM / 16;             // 1 KB DMA groups (16 rows) of the A tile
@@ -212,18 +262,8 @@ __global__ __launch_bounds__(NTHR, 1) void ffn_gemm_bf16_kernel(
   static_assert(MODE == 1 || NI % 2 == 0, "gate/up fragments come in pairs");
   static_assert((BM + BN) * BK * 2 <= LDS_STAGE_MAX, "stage too large");
 
-  // XCD-aware order.  Workgroup b runs on XCD b % 8, so XCD x is given the
-  // contiguous range [x n/8, (x+1) n/8) of the n-item work list
-  // (expert-major, then n-tile, then m-tile): the m-tiles that share a
-  // weight tile, and the n-tiles that share an expert's rows, run together
-  // and meet in one L2, and every XCD gets an equal share.
-  const int nw = n_work[MODE];
-  const int per_xcd = (nw + 7) >> 3;
-  const int slot = blockIdx.x >> 3;
-  if (slot >= per_xcd) return;
-  const int L = (blockIdx.x & 7) * per_xcd + slot;
-  if (L >= nw) return;
-  const Work wk = work[L];
+  Work wk;
+  if (!find_work(tl, true, wk, ring3)) return;
   const int nt = wk.nt;
   const int Kdim = MODE == 0 ? d : m;
   const int ldc = MODE == 0 ? m : d;
@@ -429,9 +469,9 @@ __device__ __forceinline__ u32x4 load_frag(__amdgpu_buffer_rsrc_t rs, int voff, 
 }
 
 template <int MODE, int BM, int BN>
-__global__ __launch_bounds__(NTHR, 1) void ffn_gemm_packed_kernel(
+__global__ __launch_bounds__(NTHR, BN == 256 ? 2 : 1) void ffn_gemm_packed_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ Wp, uint16_t* __restrict__ C,
-    const Work* __restrict__ work, const int32_t* __restrict__ n_work, int d, int m) {
+    const Tiles tl, int d, int m) {
   constexpr int MI = BM / 32;  // 32-row token fragments (all tile rows)
   constexpr int NI = BN / 128; // 32-row weight fragments per wavefront
   constexpr int AG = BM / 16;  // 1 KB DMA groups (16 rows x 64 B) of the A tile
@@ -440,14 +480,8 @@ __global__ __launch_bounds__(NTHR, 1) void ffn_gemm_packed_kernel(
   static_assert(AG % 4 == 0 && (MODE == 1 || NI % 2 == 0), "tile shape");
   static_assert(BM * BK * 2 <= (int)sizeof(aring0), "A stage too large");
 
-  // XCD-aware order (as above)
-  const int nw = n_work[MODE];
-  const int per_xcd = (nw + 7) >> 3;
-  const int slot = blockIdx.x >> 3;
-  if (slot >= per_xcd) return;
-  const int L = (blockIdx.x & 7) * per_xcd + slot;
-  if (L >= nw) return;
-  const Work wk = work[L];
+  Work wk;
+  if (!find_work(tl, true, wk, ostage)) return;
   const int nt = wk.nt;
   const int Kdim = MODE == 0 ? d : m;
   const int R = MODE == 0 ? 2 * m : d;  // rows of the expert's weight matrix
@@ -609,13 +643,12 @@ template <int MODE>
 __global__ __launch_bounds__(256) void ffn_gemm_f32_kernel(const float* __restrict__ A,
                                                            const float* __restrict__ W,
                                                            float* __restrict__ C,
-                                                           const Work* __restrict__ work,
-                                                           const int32_t* __restrict__ n_work,
-                                                           int d, int m) {
+                                                           const Tiles tl, int d, int m) {
   __shared__ float as[FBM][FBK + 1];
   __shared__ float bs[2][FBN][FBK + 1];  // MODE 0: gate, up; MODE 1: down only
-  if ((int)blockIdx.x >= n_work[MODE]) return;
-  const Work wk = work[blockIdx.x];
+  __shared__ __attribute__((aligned(16))) char wl[64];
+  Work wk;
+  if (!find_work(tl, false, wk, wl)) return;
   const int nt = wk.nt;
   struct { int row0, rows, expert; } tile{wk.row0, wk.rows, wk.expert};
   const int Kdim = MODE == 0 ? d : m;
@@ -665,12 +698,11 @@ namespace {
 using kern::FBM;
 using kern::FBN;
 using kern::NTHR;
-using kern::Work;
+using kern::Tiles;
 using kern::ffn_gemm_bf16_kernel;
 using kern::ffn_gemm_f32_kernel;
 using kern::ffn_gemm_packed_kernel;
 using kern::pack_weights_kernel;
-using kern::ffn_tiles_kernel;
 
 size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
 int max_tiles_for(int rows_max, int E, int bm) { return (rows_max + bm - 1) / bm + E; }
@@ -679,14 +711,14 @@ int max_tiles_for(int rows_max, int E, int bm) { return (rows_max + bm - 1) / bm
 // else 64 (weight-streaming shapes with few rows per expert)
 int pick_bm(int rows_max, int E) { return rows_max >= 160 * E ? 128 : 64; }
 
-// n-tiles per GEMM: bf16 uses 256 weight rows per tile when they divide the
-// expert's rows, else 128; float32 uses 32 output columns
-// bf16 weight-row tile: 512 when it divides the expert's rows, else 256
-// (gate/up: 2m, down: d); `wide` selects 512
-void n_tiles_of(bool bf16, int d, int m, int& nn0, int& nn1, bool& wide0, bool& wide1) {
+// n-tiles per GEMM.  bf16 weight-row tile: 512 when it divides the expert's
+// rows (gate/up: 2m, down: d), else 256 -- `wide` selects 512; the packed
+// kernel always runs 256-row tiles at two workgroups per CU.  float32: 32
+// output columns.
+void n_tiles_of(bool bf16, bool packed, int d, int m, int& nn0, int& nn1, bool& wide0, bool& wide1) {
   if (bf16) {
-    wide0 = (2 * m) % 512 == 0;
-    wide1 = d % 512 == 0;
+    wide0 = !packed && (2 * m) % 512 == 0;
+    wide1 = !packed && d % 512 == 0;
     nn0 = 2 * m / (wide0 ? 512 : 256);
     nn1 = d / (wide1 ? 512 : 256);
   } else {
@@ -696,43 +728,19 @@ void n_tiles_of(bool bf16, int d, int m, int& nn0, int& nn1, bool& wide0, bool& 
   }
 }
 
-struct FfnWs {
-  int32_t* n_work;
-  Work* work0;
-  Work* work1;
-  void* h;
-};
-
-FfnWs carve(void* ws, bool bf16, int rows_max, int E, int d, int m) {
-  const int cap = max_tiles_for(rows_max, E, bf16 ? 64 : FBM);
-  const size_t c0 = (size_t)cap * ((m + FBN - 1) / FBN) + 8;  // >= any nn0 * tiles
-  const size_t c1 = (size_t)cap * ((d + FBN - 1) / FBN) + 8;
-  char* p = static_cast<char*>(ws);
-  FfnWs w;
-  w.n_work = reinterpret_cast<int32_t*>(p);
-  p += 256;
-  w.work0 = reinterpret_cast<Work*>(p);
-  p += align256(c0 * sizeof(Work));
-  w.work1 = reinterpret_cast<Work*>(p);
-  p += align256(c1 * sizeof(Work));
-  w.h = p;
-  return w;
-}
-
 // kernels are instantiated here, outside any function template (device stubs
 // of kernels first instantiated inside a template launcher are not emitted)
-#define FFN_GEMM(MODE, BM, BN)                                                               \
-  do {                                                                                       \
-    if (packed)                                                                              \
-      ffn_gemm_packed_kernel<MODE, BM, BN><<<grid, NTHR, 0, s>>>(A, W, C, work, n_work, d, m); \
-    else                                                                                     \
-      ffn_gemm_bf16_kernel<MODE, BM, BN><<<grid, NTHR, 0, s>>>(A, W, C, work, n_work, d, m);   \
+#define FFN_GEMM(MODE, BM, BN)                                                        \
+  do {                                                                                \
+    if (packed)                                                                       \
+      ffn_gemm_packed_kernel<MODE, BM, 256><<<grid, NTHR, 0, s>>>(A, W, C, tl, d, m); \
+    else                                                                              \
+      ffn_gemm_bf16_kernel<MODE, BM, BN><<<grid, NTHR, 0, s>>>(A, W, C, tl, d, m);    \
   } while (0)
 
-hipError_t launch_gemm(int mode, int bm, bool wide, bool packed, int n_items_max, const uint16_t* A,
-                       const uint16_t* W, uint16_t* C, const Work* work, const int32_t* n_work,
-                       int d, int m, hipStream_t s) {
-  const int grid = (n_items_max + 7) & ~7;  // whole XCD rounds
+hipError_t launch_gemm(int mode, int bm, bool wide, bool packed, const Tiles& tl, const uint16_t* A,
+                       const uint16_t* W, uint16_t* C, int d, int m, hipStream_t s) {
+  const int grid = (tl.max_tiles * tl.nn + 7) & ~7;  // whole XCD rounds
   if (mode == 0) {
     if (bm == 128) {
       if (wide) FFN_GEMM(0, 128, 512); else FFN_GEMM(0, 128, 256);
@@ -751,12 +759,11 @@ hipError_t launch_gemm(int mode, int bm, bool wide, bool packed, int n_items_max
 #undef FFN_GEMM
 }  // namespace
 
+// workspace: the intermediate h [rows_max, m]
 size_t ffn_ws_bytes(bool bf16, int rows_max, int E, int d, int m) {
-  const int cap = max_tiles_for(rows_max, E, bf16 ? 64 : FBM);
-  const size_t c0 = (size_t)cap * ((m + FBN - 1) / FBN) + 8;
-  const size_t c1 = (size_t)cap * ((d + FBN - 1) / FBN) + 8;
-  return 256 + align256(c0 * sizeof(Work)) + align256(c1 * sizeof(Work)) +
-         align256((size_t)rows_max * m * (bf16 ? 2 : 4));
+  (void)E;
+  (void)d;
+  return align256((size_t)rows_max * m * (bf16 ? 2 : 4));
 }
 
 hipError_t launch_expert_ffn(const void* x_perm, bool bf16, const int32_t* offsets, int E,
@@ -764,32 +771,29 @@ hipError_t launch_expert_ffn(const void* x_perm, bool bf16, const int32_t* offse
                              const void* w_gate_up, const void* w_down, bool packed, void* y_perm,
                              void* ws, hipStream_t s) {
   const int bm = bf16 ? pick_bm(rows_max, E) : FBM;
-  const int max_tiles = max_tiles_for(rows_max, E, bm);
   int nn0, nn1;
   bool wide0, wide1;
-  n_tiles_of(bf16, d, m, nn0, nn1, wide0, wide1);
-  FfnWs w = carve(ws, bf16, rows_max, E, d, m);
-  ffn_tiles_kernel<<<1, 1024, 0, s>>>(offsets, E, K_dev, n_K, rows_max, bm, max_tiles, nn0, nn1,
-                                      w.work0, w.work1, w.n_work);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess) return err;
+  n_tiles_of(bf16, packed, d, m, nn0, nn1, wide0, wide1);
+  Tiles t0{offsets, K_dev, E, K_dev ? n_K : 0, rows_max, bm, max_tiles_for(rows_max, E, bm), nn0};
+  Tiles t1 = t0;
+  t1.nn = nn1;
+  void* h = ws;
+  hipError_t err;
   if (bf16) {
-    err = launch_gemm(0, bm, wide0, packed, max_tiles * nn0, static_cast<const uint16_t*>(x_perm),
-                      static_cast<const uint16_t*>(w_gate_up), static_cast<uint16_t*>(w.h),
-                      w.work0, w.n_work, d, m, s);
+    err = launch_gemm(0, bm, wide0, packed, t0, static_cast<const uint16_t*>(x_perm),
+                      static_cast<const uint16_t*>(w_gate_up), static_cast<uint16_t*>(h), d, m, s);
     if (err != hipSuccess) return err;
-    return launch_gemm(1, bm, wide1, packed, max_tiles * nn1, static_cast<const uint16_t*>(w.h),
-                       static_cast<const uint16_t*>(w_down), static_cast<uint16_t*>(y_perm),
-                       w.work1, w.n_work, d, m, s);
+    return launch_gemm(1, bm, wide1, packed, t1, static_cast<const uint16_t*>(h),
+                       static_cast<const uint16_t*>(w_down), static_cast<uint16_t*>(y_perm), d, m, s);
   }
-  ffn_gemm_f32_kernel<0><<<max_tiles * nn0, 256, 0, s>>>(
-      static_cast<const float*>(x_perm), static_cast<const float*>(w_gate_up),
-      static_cast<float*>(w.h), w.work0, w.n_work, d, m);
+  ffn_gemm_f32_kernel<0><<<t0.max_tiles * nn0, NTHR, 0, s>>>(
+      static_cast<const float*>(x_perm), static_cast<const float*>(w_gate_up), static_cast<float*>(h),
+      t0, d, m);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
-  ffn_gemm_f32_kernel<1><<<max_tiles * nn1, 256, 0, s>>>(
-      static_cast<const float*>(w.h), static_cast<const float*>(w_down),
-      static_cast<float*>(y_perm), w.work1, w.n_work, d, m);
+  ffn_gemm_f32_kernel<1><<<t1.max_tiles * nn1, NTHR, 0, s>>>(
+      static_cast<const float*>(h), static_cast<const float*>(w_down), static_cast<float*>(y_perm),
+      t1, d, m);
   return hipGetLastError();
 }
 

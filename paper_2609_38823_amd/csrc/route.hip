@@ -15,6 +15,11 @@ namespace decomoe {
 // MFMA step s consumes k = 8q + s on both operands, so each x row is read
 // with one 16-byte (bf16) or two 16-byte (f32) loads per chunk.
 // Needs d % 128 == 0 (four quarters of whole chunks).
+//
+// Split-K (small T, too few tiles to fill the chip): blockIdx.z = c takes the
+// d-range [c d/S, (c+1) d/S) and writes its partial tile, without bias, to
+// part[c][T][E]; the Top-k kernel adds the S partials in order c = 0..S-1,
+// adds the bias and writes the logits.  Needs d % (128 S) == 0.
 // ---------------------------------------------------------------------------
 namespace {
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -25,14 +30,16 @@ __global__ __launch_bounds__(256) void router_logits_mfma_kernel(const void* __r
                                                                  const float* __restrict__ w_r,
                                                                  const float* __restrict__ bias,
                                                                  int T, int d, int E,
-                                                                 float* __restrict__ logits) {
+                                                                 float* __restrict__ logits,
+                                                                 float* __restrict__ split_part) {
   __shared__ f32x4 part[4][4][64];  // [wave][n-frag][lane]
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int e0 = blockIdx.x * RM_E, t0 = blockIdx.y * RM_T;
   const int q = lane >> 4, r16 = lane & 15;
   const int t = min(t0 + r16, T - 1);  // padding tokens re-read the last row
-  const int quarter = d >> 2;
-  const int kb = wv * quarter, ke = kb + quarter;
+  const int dch = d / gridDim.z;       // this split's d-range
+  const int quarter = dch >> 2;
+  const int kb = blockIdx.z * dch + wv * quarter, ke = kb + quarter;
   int ecol[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) ecol[j] = min(e0 + j * 16 + r16, E - 1);
@@ -81,11 +88,20 @@ __global__ __launch_bounds__(256) void router_logits_mfma_kernel(const void* __r
     s += part[3][j][l];
     const int e = e0 + j * 16 + (l & 15);
     if (e < E) {
-      const float b = bias ? bias[e] : 0.f;
+      if (split_part) {  // partial tile of split blockIdx.z, no bias
+        float* dst = split_part + (size_t)blockIdx.z * T * E;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int tt = t0 + 4 * (l >> 4) + i;
-        if (tt < T) logits[(size_t)tt * E + e] = s[i] + b;
+        for (int i = 0; i < 4; ++i) {
+          const int tt = t0 + 4 * (l >> 4) + i;
+          if (tt < T) dst[(size_t)tt * E + e] = s[i];
+        }
+      } else {
+        const float b = bias ? bias[e] : 0.f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int tt = t0 + 4 * (l >> 4) + i;
+          if (tt < T) logits[(size_t)tt * E + e] = s[i] + b;
+        }
       }
     }
   }
@@ -172,9 +188,13 @@ __device__ __forceinline__ void better(float& v, int& i, float ov, int oi) {
   if (ov > v || (ov == v && oi < i)) { v = ov; i = oi; }
 }
 
-__global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ logits, int T, int E,
+// With `part` (split-K router), the logits are first formed here as
+// (part[0] + part[1] + ... + part[S-1]) + b, written to `logits`, and used.
+__global__ __launch_bounds__(256) void topk_kernel(float* __restrict__ logits, int T, int E,
                                                    int k, const int32_t* __restrict__ seg_offsets,
                                                    int n_seg, const int32_t* __restrict__ K_dev,
+                                                   const float* __restrict__ part, int S,
+                                                   const float* __restrict__ bias,
                                                    int32_t* __restrict__ idx, float* __restrict__ w) {
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -184,9 +204,20 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ log
     int s = seg_offsets ? find_segment(seg_offsets, n_seg, t) : 0;
     Klim = clampi(K_dev[s], k, E);
   }
-  const float* row = logits + (size_t)t * E;
+  float* row = logits + (size_t)t * E;
   float v[TK_MAXC];
   uint32_t alive = 0;
+  if (part) {
+#pragma unroll
+    for (int c = 0; c < TK_MAXC; ++c) {
+      const int e = lane + c * 64;
+      if (e < E) {
+        float a = part[(size_t)t * E + e];
+        for (int sp = 1; sp < S; ++sp) a += part[((size_t)sp * T + t) * E + e];
+        row[e] = a + (bias ? bias[e] : 0.f);
+      }
+    }
+  }
 #pragma unroll
   for (int c = 0; c < TK_MAXC; ++c) {
     int e = lane + c * 64;
@@ -222,27 +253,48 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ log
 }
 }  // namespace
 
-hipError_t launch_router_logits(const void* x, bool x_bf16, const float* w_r, const float* bias,
-                                int T, int d, int E, float* logits, hipStream_t s) {
-  if (d % 128 == 0) {
-    dim3 grid((E + RM_E - 1) / RM_E, (T + RM_T - 1) / RM_T);
-    if (x_bf16)
-      router_logits_mfma_kernel<true><<<grid, 256, 0, s>>>(x, w_r, bias, T, d, E, logits);
-    else
-      router_logits_mfma_kernel<false><<<grid, 256, 0, s>>>(x, w_r, bias, T, d, E, logits);
-  } else {
-    dim3 grid((E + RT_E - 1) / RT_E, (T + RT_T - 1) / RT_T);
-    if (x_bf16)
-      router_logits_simt_kernel<true><<<grid, 256, 0, s>>>(x, w_r, bias, T, d, E, logits);
-    else
-      router_logits_simt_kernel<false><<<grid, 256, 0, s>>>(x, w_r, bias, T, d, E, logits);
-  }
-  return hipGetLastError();
+// Split factor of the router's d-range: enough workgroups to cover the chip
+// (about 512), in whole 128-wide quarters of d.  1 = no split.
+int router_splits(int T, int d, int E) {
+  if (d % 128 != 0) return 1;
+  const int tiles = ((E + RM_E - 1) / RM_E) * ((T + RM_T - 1) / RM_T);
+  int S = 1;
+  while (tiles * S < 512 && d % (128 * 2 * S) == 0) S *= 2;
+  return S;
 }
 
-hipError_t launch_topk(const float* logits, int T, int E, int k, const int32_t* seg_offsets,
-                       int n_seg, const int32_t* K_dev, int32_t* idx, float* w, hipStream_t s) {
-  topk_kernel<<<(T + 3) / 4, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, idx, w);
+size_t route_ws_bytes(int T, int d, int E) {
+  const int S = router_splits(T, d, E);
+  return S > 1 ? (size_t)S * T * E * sizeof(float) : 0;
+}
+
+hipError_t launch_route(const void* x, bool x_bf16, const float* w_r, const float* bias, int T,
+                        int d, int E, int k, const int32_t* seg_offsets, int n_seg,
+                        const int32_t* K_dev, float* logits, int32_t* idx, float* w, void* ws,
+                        hipStream_t s) {
+  float* part = nullptr;
+  int S = 1;
+  if (x) {
+    if (d % 128 == 0) {
+      S = router_splits(T, d, E);
+      if (S > 1) part = static_cast<float*>(ws);
+      dim3 grid((E + RM_E - 1) / RM_E, (T + RM_T - 1) / RM_T, S);
+      if (x_bf16)
+        router_logits_mfma_kernel<true><<<grid, 256, 0, s>>>(x, w_r, bias, T, d, E, logits, part);
+      else
+        router_logits_mfma_kernel<false><<<grid, 256, 0, s>>>(x, w_r, bias, T, d, E, logits, part);
+    } else {
+      dim3 grid((E + RT_E - 1) / RT_E, (T + RT_T - 1) / RT_T);
+      if (x_bf16)
+        router_logits_simt_kernel<true><<<grid, 256, 0, s>>>(x, w_r, bias, T, d, E, logits);
+      else
+        router_logits_simt_kernel<false><<<grid, 256, 0, s>>>(x, w_r, bias, T, d, E, logits);
+    }
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+  }
+  topk_kernel<<<(T + 3) / 4, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S,
+                                          bias, idx, w);
   return hipGetLastError();
 }
 

@@ -60,9 +60,11 @@ def calibrate_order_router(x_text: torch.Tensor, w_r: np.ndarray, bias, k: int,
     w = torch.empty((T, k), dtype=torch.float32, device=dev)
     mass = torch.empty((n_seg, E), dtype=torch.float64, device=dev)
     order = torch.empty((E,), dtype=torch.int32, device=dev)
+    ws = torch.empty(abi.moe_workspace_size(T, E, k, x_text.shape[1], 1, n_seg), dtype=torch.uint8,
+                     device=dev)
     abi.moe_route(x_text, to_device(w_r, torch.float32, dev), to_device(bias, torch.float32, dev), k,
-                  logits, idx, w)
-    abi.moe_calibrate_prefix(idx, w, E, 1.0, mass, order=order, seg_offsets=seg_offsets)
+                  logits, idx, w, ws=ws)
+    abi.moe_calibrate_prefix(idx, w, E, 1.0, mass, ws, order=order, seg_offsets=seg_offsets)
     return order.cpu().numpy()
 
 
@@ -138,7 +140,7 @@ class MoELayer:
                       mark=None) -> Buffers:
         """Full expert pool (layers before the visual exit)."""
         b = b or self.buffers(x.shape[0])
-        abi.moe_route(x, self.w_r, self.bias, self.k, b.logits, b.idx, b.w, stream=stream)
+        abi.moe_route(x, self.w_r, self.bias, self.k, b.logits, b.idx, b.w, ws=b.ws, stream=stream)
         if mark:
             mark()
         self._experts(x, b, b.idx, b.w, stream=stream, mark=mark)
@@ -150,10 +152,10 @@ class MoELayer:
         n_seg = 1 if seg_offsets is None else seg_offsets.numel() - 1
         b = b or self.buffers(x.shape[0], n_seg)
         mk = mark or (lambda: None)
-        abi.moe_route(x, self.w_r, self.bias, self.k, b.logits, b.idx_full, b.w_full,
+        abi.moe_route(x, self.w_r, self.bias, self.k, b.logits, b.idx_full, b.w_full, ws=b.ws,
                       stream=stream)
         mk()
-        abi.moe_calibrate_prefix(b.idx_full, b.w_full, self.E, p, b.mass, K_out=b.K,
+        abi.moe_calibrate_prefix(b.idx_full, b.w_full, self.E, p, b.mass, b.ws, K_out=b.K,
                                  seg_offsets=seg_offsets, stream=stream)
         mk()
         abi.moe_route(None, None, None, self.k, b.logits, b.idx, b.w, seg_offsets=seg_offsets,

@@ -61,33 +61,50 @@ def test_workspace_size(lib):
 
 # fake, never dereferenced, 16-byte aligned addresses
 P1, P2, P3, P4, P5, P6, P7 = (ctypes.c_void_p(0x10000 * i) for i in range(1, 8))
+WS = ctypes.c_void_p(0x40000000)
 NULL = None
 
 
 def test_route_rejects(lib):
     # k > E, E > 1024, k > 32
-    assert lib.moe_route(P1, BF16, P2, NULL, 8, 64, 4, 5, NULL, 1, NULL, P3, P4, P5, NULL) == EINVAL
-    assert lib.moe_route(P1, BF16, P2, NULL, 8, 64, 2000, 5, NULL, 1, NULL, P3, P4, P5, NULL) == EINVAL
-    assert lib.moe_route(P1, BF16, P2, NULL, 8, 64, 128, 33, NULL, 1, NULL, P3, P4, P5, NULL) == EUNSUPPORTED
+    assert lib.moe_route(P1, BF16, P2, NULL, 8, 64, 4, 5, NULL, 1, NULL, P3, P4, P5, NULL, 0, NULL) == EINVAL
+    assert lib.moe_route(P1, BF16, P2, NULL, 8, 64, 2000, 5, NULL, 1, NULL, P3, P4, P5, NULL, 0, NULL) == EINVAL
+    assert lib.moe_route(P1, BF16, P2, NULL, 8, 64, 128, 33, NULL, 1, NULL, P3, P4, P5, NULL, 0, NULL) == EUNSUPPORTED
     # bf16 rows need d % 8 == 0; logits must be given; misaligned pointer
-    assert lib.moe_route(P1, BF16, P2, NULL, 8, 60, 128, 8, NULL, 1, NULL, P3, P4, P5, NULL) == EINVAL
-    assert lib.moe_route(P1, BF16, P2, NULL, 8, 64, 128, 8, NULL, 1, NULL, NULL, P4, P5, NULL) == EINVAL
+    assert lib.moe_route(P1, BF16, P2, NULL, 8, 60, 128, 8, NULL, 1, NULL, P3, P4, P5, NULL, 0, NULL) == EINVAL
+    assert lib.moe_route(P1, BF16, P2, NULL, 8, 64, 128, 8, NULL, 1, NULL, NULL, P4, P5, NULL, 0, NULL) == EINVAL
     assert lib.moe_route(ctypes.c_void_p(0x10002), BF16, P2, NULL, 8, 64, 128, 8, NULL, 1, NULL,
-                         P3, P4, P5, NULL) == EINVAL
+                         P3, P4, P5, NULL, 0, NULL) == EINVAL
     # outputs overlapping inputs: logits on top of x
-    assert lib.moe_route(P1, BF16, P2, NULL, 8, 64, 128, 8, NULL, 1, NULL, P1, P4, P5, NULL) == EALIAS
+    assert lib.moe_route(P1, BF16, P2, NULL, 8, 64, 128, 8, NULL, 1, NULL, P1, P4, P5, NULL, 0, NULL) == EALIAS
     # logits-input mode: topk_w overlapping logits
-    assert lib.moe_route(NULL, F32, NULL, NULL, 8, 0, 128, 8, NULL, 1, NULL, P3, P4, P3, NULL) == EALIAS
+    assert lib.moe_route(NULL, F32, NULL, NULL, 8, 0, 128, 8, NULL, 1, NULL, P3, P4, P3, NULL, 0, NULL) == EALIAS
     # T == 0 launches nothing
-    assert lib.moe_route(P1, BF16, P2, NULL, 0, 64, 128, 8, NULL, 1, NULL, P3, P4, P5, NULL) == 0
+    assert lib.moe_route(P1, BF16, P2, NULL, 0, 64, 128, 8, NULL, 1, NULL, P3, P4, P5, NULL, 0, NULL) == 0
+
+
+def test_route_and_calibrate_need_workspace(lib):
+    # few tokens and d % 128 == 0: the router splits d and needs ws
+    assert lib.moe_route(P1, BF16, P2, NULL, 8, 2048, 128, 8, NULL, 1, NULL, P3, P4, P5, NULL, 0,
+                         NULL) == EWORKSPACE
+    assert lib.moe_route(P1, BF16, P2, NULL, 8, 2048, 128, 8, NULL, 1, NULL, P3, P4, P5, WS, 64,
+                         NULL) == EWORKSPACE
+    assert lib.moe_route(P1, BF16, P2, NULL, 8, 2048, 128, 8, NULL, 1, NULL, P3, P4, P5, P2, 1 << 30,
+                         NULL) == EALIAS  # ws over w_r
+    assert lib.moe_calibrate_prefix(P1, P2, 8, 16, 2, NULL, 1, 0.9, P3, P1, NULL, NULL, 0,
+                                    NULL) == EALIAS  # K_out over topk_idx; no scratch needed
+    assert lib.moe_calibrate_prefix(P1, P2, 8, 16, 40, NULL, 1, 0.9, P3, P4, NULL, WS, 1 << 30,
+                                    NULL) == EINVAL  # k > E
+    assert lib.moe_calibrate_prefix(P1, P2, 8, 64, 40, NULL, 1, 0.9, P3, P4, NULL, WS, 1 << 30,
+                                    NULL) == EUNSUPPORTED  # k > 32
 
 
 def test_calibrate_rejects(lib):
     for p in (0.0, -1.0, 1.5, float("nan")):
-        assert lib.moe_calibrate_prefix(P1, P2, 8, 16, 2, NULL, 1, p, P3, P4, NULL, NULL) == EINVAL
-    assert lib.moe_calibrate_prefix(P1, P2, 8, 16, 20, NULL, 1, 0.9, P3, P4, NULL, NULL) == EINVAL
-    assert lib.moe_calibrate_prefix(P1, P2, 8, 16, 2, P5, 0, 0.9, P3, P4, NULL, NULL) == EINVAL
-    assert lib.moe_calibrate_prefix(P1, P2, 8, 16, 2, NULL, 1, 0.9, P1, P4, NULL, NULL) == EALIAS
+        assert lib.moe_calibrate_prefix(P1, P2, 8, 16, 2, NULL, 1, p, P3, P4, NULL, WS, 1 << 30, NULL) == EINVAL
+    assert lib.moe_calibrate_prefix(P1, P2, 8, 16, 20, NULL, 1, 0.9, P3, P4, NULL, WS, 1 << 30, NULL) == EINVAL
+    assert lib.moe_calibrate_prefix(P1, P2, 8, 16, 2, P5, 0, 0.9, P3, P4, NULL, WS, 1 << 30, NULL) == EINVAL
+    assert lib.moe_calibrate_prefix(P1, P2, 8, 16, 2, NULL, 1, 0.9, P1, P4, NULL, WS, 1 << 30, NULL) == EALIAS
 
 
 def test_dispatch_rejects(lib):

@@ -54,6 +54,12 @@ def f32(shape):
     return torch.full(shape, float("nan"), dtype=torch.float32, device="cuda")
 
 
+def ws_for(T, E, k, d, m=1, n_seg=1):
+    """Workspace for any entry point at these sizes (moe_workspace_size)."""
+    return torch.empty(abi.moe_workspace_size(max(T, 1), E, k, d, m, n_seg), dtype=torch.uint8,
+                       device="cuda")
+
+
 # ---------------------------------------------------------------------------
 # drop_visual_block (Sec. 3.2, Algorithm 2): bitwise row compaction
 # ---------------------------------------------------------------------------
@@ -140,8 +146,11 @@ def robust_tokens(a_ref, k, delta):
 
 ODD_F32 = I.LayerShape(d=40, E=24, m=8, k=3, dtype="f32", zipf_alpha=0.35)
 ODD_BF16 = I.LayerShape(d=104, E=200, m=8, k=8, dtype="bf16", zipf_alpha=0.35)
+# d-range splits: tiny 512 / 37 -> 2, qwen 4096 -> 1, 512 -> 8, 77, 64 and 1 -> 16;
+# the odd shapes take the SIMT kernel
 ROUTER_CASES = [("tiny_f32", 512), ("tiny_f32", 37), ("qwen3vl_dense_4096", 4096),
-                ("qwen3vl_dense_4096", 77), ("qwen3vl_rcep_512", 1), ("odd_f32", 99), ("odd_bf16", 333)]
+                ("qwen3vl_rcep_512", 512), ("qwen3vl_dense_4096", 77), ("qwen3vl_decode64", 64),
+                ("qwen3vl_rcep_512", 1), ("odd_f32", 99), ("odd_bf16", 333)]
 
 
 @pytest.mark.parametrize("name,T", ROUTER_CASES)
@@ -157,7 +166,7 @@ def test_router_logits_and_free_running_topk(name, T):
     x = I.tokens(sh, T, seed=wl.seed)
     logits, idx, w = f32((T, sh.E)), i32((T, sh.k)), f32((T, sh.k))
     abi.moe_route(dev(x, TDT[sh.dtype]), dev(rp["w_r"]), dev(rp["bias"]) if rp["bias"] is not None else None,
-                  sh.k, logits, idx, w)
+                  sh.k, logits, idx, w, ws=ws_for(T, sh.E, sh.k, sh.d))
     a_ref = oracle.router_logits(x, rp["w_r"], rp["bias"])
     a_gpu = host(logits).astype(np.float64)
     # every logit within the rigorous float32 dot-product error bound
@@ -221,7 +230,8 @@ def test_calibrate_prefix_exact(T, E, k, segs, p):
     K, order = i32((n_seg,)), i32((E,))
     idx_d = dev(idx) if T else torch.empty((0, k), dtype=torch.int32, device="cuda")
     w_d = dev(w) if T else torch.empty((0, k), dtype=torch.float32, device="cuda")
-    abi.moe_calibrate_prefix(idx_d, w_d, E, p, mass, K_out=K, order=order, seg_offsets=seg_dev)
+    abi.moe_calibrate_prefix(idx_d, w_d, E, p, mass, ws_for(T, E, k, 8), K_out=K, order=order,
+                             seg_offsets=seg_dev)
     rm, rK, ro = oracle_calibrate(idx, w, E, k, segs, p)
     gm = host(mass)
     np.testing.assert_array_equal(gm.view(np.uint64), rm.view(np.uint64))  # bitwise
@@ -237,7 +247,7 @@ def test_calibrate_worked_example_golden():
     for c in g["cases"]:
         mass = torch.empty((1, g["E"]), dtype=torch.float64, device="cuda")
         K = i32((1,))
-        abi.moe_calibrate_prefix(idx, w, g["E"], c["p"], mass, K_out=K)
+        abi.moe_calibrate_prefix(idx, w, g["E"], c["p"], mass, ws_for(4, g["E"], 1, 8), K_out=K)
         np.testing.assert_array_equal(host(mass)[0], g["mass"])
         assert int(host(K)[0]) == c["K"], c["why"]
     rr = g["prefix_reroute_at_p_0.75"]
