@@ -1,0 +1,109 @@
+"""HBM traffic of the expert FFN from rocprofv3 counter passes.
+
+Two `rocprofv3 --pmc` passes over `bench.py --traffic-run` (one with
+FETCH_SIZE, one with WRITE_SIZE; the counters of one pass must fit the
+hardware) record, per dispatch, the KiB the L2 fetched from and wrote to
+memory.  The same run copies a known number of bytes with
+drop_visual_block (a plain row copy: N bytes read, N written), which gives
+the factor between what the counter reads and the bytes actually moved.
+
+    python -m paper_2609_38823_amd.profiling FETCH_DIR WRITE_DIR OUT_PREFIX
+
+writes OUT_PREFIX.json (read by bench.py) and OUT_PREFIX.txt.  The JSON
+records a hash of the GEMM sources; bench.py reports the traffic only while
+the sources still hash the same.
+"""
+
+from __future__ import annotations
+
+import collections
+import csv
+import glob
+import hashlib
+import json
+import os
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+KERNEL_SOURCES = ("csrc/ffn.hip", "csrc/common.hpp")
+COPY_BYTES = 65536 * 2048 * 2  # the --traffic-run copy: 65536 bf16 rows of 2048
+
+
+def source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(HERE, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def _short(name: str) -> str:
+    name = name.replace("decomoe::(anonymous namespace)::", "").replace("decomoe::kern::", "")
+    name = name.replace("void ", "")
+    out, depth = "", 0
+    for ch in name:
+        if ch == "(" and out.count("<") == out.count(">"):
+            break
+        out += ch
+    return out
+
+
+def per_kernel(pass_dir: str, counter: str) -> dict:
+    """Mean counter value (KiB per dispatch) by (kernel, grid size)."""
+    vals = collections.defaultdict(list)
+    for f in glob.glob(os.path.join(pass_dir, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] == counter:
+                vals[(_short(r["Kernel_Name"]), int(r["Grid_Size"]))].append(float(r["Counter_Value"]))
+    return {k: sum(v) / len(v) for k, v in vals.items()}
+
+
+def main(argv) -> int:
+    fetch_dir, write_dir, out = argv
+    fetch = per_kernel(fetch_dir, "FETCH_SIZE")
+    write = per_kernel(write_dir, "WRITE_SIZE")
+    copy_key = max((k for k in fetch if k[0].startswith("drop_rows_kernel")), key=lambda k: k[1])
+    f_scale = COPY_BYTES / (fetch[copy_key] * 1024.0)
+    w_scale = COPY_BYTES / (write[copy_key] * 1024.0)
+    gemm = {k: v for k, v in fetch.items() if k[0].startswith("ffn_gemm_packed_kernel")}
+    # the bench's FFN call at 4096 rows: the largest grids of the two GEMM modes
+    per_mode = {}
+    for (name, grid), kib in gemm.items():
+        mode = name.split("<")[1].split(",")[0]
+        if mode not in per_mode or grid > per_mode[mode][1]:
+            per_mode[mode] = (name, grid)
+    rows, total = [], 0.0
+    for mode in sorted(per_mode):
+        key = per_mode[mode]
+        fb = fetch[key] * 1024.0 * f_scale
+        wb = write.get(key, 0.0) * 1024.0 * w_scale
+        total += fb + wb
+        rows.append(dict(kernel=key[0], grid=key[1], fetch_bytes=fb, write_bytes=wb,
+                         fetch_kib_raw=fetch[key], write_kib_raw=write.get(key, 0.0)))
+    res = dict(source_sha256=source_hash(), copy_bytes=COPY_BYTES,
+               copy_fetch_kib_raw=fetch[copy_key], copy_write_kib_raw=write[copy_key],
+               fetch_scale=f_scale, write_scale=w_scale, kernels=rows, traffic_bytes_per_call=total)
+    with open(out + ".json", "w") as f:
+        json.dump(res, f, indent=1)
+    with open(out + ".txt", "w") as f:
+        f.write("# HBM traffic of moe_expert_ffn_packed @ 4096 rows (Qwen3-VL-MoE layer), per launch\n")
+        f.write("# commands (from the repository root R, one pass each):\n")
+        f.write("#   cd /tmp && rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/gpurun_out/pmc_fetch -o p"
+                " -- python3 $R/bench.py --traffic-run\n")
+        f.write("#   cd /tmp && rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/gpurun_out/pmc_write -o p"
+                " -- python3 $R/bench.py --traffic-run\n")
+        f.write("#   python -m paper_2609_38823_amd.profiling gpurun_out/pmc_fetch gpurun_out/pmc_write "
+                + os.path.relpath(out) + "\n")
+        f.write(f"# copy calibration: drop_visual_block of {COPY_BYTES} B: FETCH_SIZE {fetch[copy_key]:.0f} KiB,"
+                f" WRITE_SIZE {write[copy_key]:.0f} KiB -> scale fetch {f_scale:.3f}, write {w_scale:.3f}\n")
+        for r in rows:
+            f.write(f"{r['kernel']:40s} grid {r['grid']:8d}  fetch {r['fetch_bytes'] / 1e6:9.1f} MB"
+                    f"  write {r['write_bytes'] / 1e6:9.1f} MB  (raw {r['fetch_kib_raw']:.0f} / "
+                    f"{r['write_kib_raw']:.0f} KiB)\n")
+        f.write(f"total per moe_expert_ffn_packed call: {total / 1e6:.1f} MB\n")
+    print(open(out + ".txt").read())
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main(sys.argv[1:]))
