@@ -221,8 +221,8 @@ int moe_pack_expert_weights(const void* w, moe_dtype dtype, int E, int rows, int
  * arguments, results and limits, with w_gate_up_packed and w_down_packed
  * produced by moe_pack_expert_weights from [E, 2m, d] and [E, d, m].  The
  * weight operand then streams from HBM in contiguous runs straight into
- * registers.  bf16 only (MOE_EUNSUPPORTED for float32).  Needs ws
- * (moe_workspace_size).
+ * registers.  bf16 only (MOE_EUNSUPPORTED for float32); d % 256 == 0 and
+ * m % 256 == 0, else MOE_EUNSUPPORTED.  Needs ws (moe_workspace_size).
  */
 int moe_expert_ffn_packed(const void* x_perm, moe_dtype dtype, const int32_t* offsets, int E,
                           const int32_t* K_dev, int n_K, int rows_max, int d, int m,

@@ -204,6 +204,7 @@ int moe_expert_ffn_packed(const void* x_perm, moe_dtype dtype, const int32_t* of
                           const void* w_gate_up_packed, const void* w_down_packed, void* y_perm,
                           void* ws, size_t ws_bytes, hipStream_t stream) {
   if (dtype != MOE_BF16) return valid_dtype(dtype) ? MOE_EUNSUPPORTED : MOE_EINVAL;
+  if (d % 256 != 0 || m % 256 != 0) return (d > 0 && m > 0) ? MOE_EUNSUPPORTED : MOE_EINVAL;
   return expert_ffn(x_perm, dtype, offsets, E, K_dev, n_K, rows_max, d, m, w_gate_up_packed,
                     w_down_packed, true, y_perm, ws, ws_bytes, stream);
 }

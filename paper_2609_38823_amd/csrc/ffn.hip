@@ -128,7 +128,12 @@ __device__ __forceinline__ bool find_work(const Tiles& tl, bool xcd, Work& out, 
     start += cnt[q];
   }
   __syncthreads();
-  out = s_wk;
+  // uniform across the workgroup: keep the fields in scalar registers (they
+  // form buffer descriptors and offsets)
+  out.expert = __builtin_amdgcn_readfirstlane(s_wk.expert);
+  out.row0 = __builtin_amdgcn_readfirstlane(s_wk.row0);
+  out.rows = __builtin_amdgcn_readfirstlane(s_wk.rows);
+  out.nt = __builtin_amdgcn_readfirstlane(s_wk.nt);
   __syncthreads();  // every thread holds its copy before the caller reuses `lds`
   return true;
 }
@@ -448,63 +453,75 @@ __global__ __launch_bounds__(256) void pack_weights_kernel(const uint4* __restri
 // ---------------------------------------------------------------------------
 // bf16 MFMA grouped GEMM on packed weights
 //
-// Same tiles, work list and epilogue as the kernel above; the weight operand
-// bypasses LDS.  Per k-step of 32, wavefront wv loads its 2 x NI weight
-// fragments (NI 32-row blocks x two 16-wide substeps, 1 KB each) into a ring
-// of four register stages, three k-steps ahead.  Only the token-row tile A,
-// which all four wavefronts share, goes through LDS (global -> LDS
-// transfers into a ring of four stages, as above).  LDS then carries A only:
-// a quarter of the bytes the shared-B layout moves, and the fragment reads
-// per MFMA halve.
+// Same MFMA tiles, work items and epilogue as the kernel above; the weight
+// operand bypasses LDS.  Per k-step of 32, wavefront wv loads its 2 x NI
+// weight fragments (NI 32-row blocks x two 16-wide substeps, 1 KB each,
+// fully coalesced) into a ring of four register stages, three k-steps
+// ahead.  Only the token-row tile A, which all four wavefronts share, goes
+// through LDS: global -> LDS transfers of whole 128-byte row segments
+// (A stages of 64 k-values, 8 rows per wave instruction) into a ring of
+// four stages, three stages (192 k-values) ahead.  In LDS a 128-byte row
+// holds 8 chunks of 16 bytes, chunk c stored at c ^ ((row >> 1) & 7): the
+// 16 rows read by one quarter-wavefront hit 16 distinct bank groups.
+//
+// Waits: before a new A stage is read, each wavefront reads one word of
+// its own part of that stage (the compiler then waits exactly for that
+// transfer), then all wavefronts meet at a barrier.  The weight registers
+// are waited for by the compiler where the MFMAs use them.
 // ---------------------------------------------------------------------------
-__shared__ __attribute__((aligned(1024))) char aring0[128 * BK * 2];
-__shared__ __attribute__((aligned(1024))) char aring1[128 * BK * 2];
-__shared__ __attribute__((aligned(1024))) char aring2[128 * BK * 2];
-__shared__ __attribute__((aligned(1024))) char aring3[128 * BK * 2];
-constexpr int OSTAGE = 4 * 32 * (128 * 2 + 16);  // epilogue staging, largest wave slice
-__shared__ __attribute__((aligned(1024))) char ostage[OSTAGE];
+constexpr int AK = 64;                    // k-values per A stage
+constexpr int ASLOT = 128 * AK * 2;       // bytes per A stage (BM <= 128)
+__shared__ __attribute__((aligned(1024))) char aring0[ASLOT];
+__shared__ __attribute__((aligned(1024))) char aring1[ASLOT];
+__shared__ __attribute__((aligned(1024))) char aring2[ASLOT];
+__shared__ __attribute__((aligned(1024))) char aring3[ASLOT];
 
 __device__ __forceinline__ u32x4 load_frag(__amdgpu_buffer_rsrc_t rs, int voff, int soff) {
   return __builtin_amdgcn_raw_buffer_load_b128(rs, voff, soff, 0);
 }
 
 template <int MODE, int BM, int BN>
-__global__ __launch_bounds__(NTHR, BN == 256 ? 2 : 1) void ffn_gemm_packed_kernel(
+__global__ __launch_bounds__(NTHR, 2) void ffn_gemm_packed_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ Wp, uint16_t* __restrict__ C,
     const Tiles tl, int d, int m) {
-  constexpr int MI = BM / 32;  // 32-row token fragments (all tile rows)
-  constexpr int NI = BN / 128; // 32-row weight fragments per wavefront
-  constexpr int AG = BM / 16;  // 1 KB DMA groups (16 rows x 64 B) of the A tile
-  constexpr int GA = AG / 4;   // A transfers per wavefront per k-step
-  constexpr int GB = 2 * NI;   // weight fragment loads per wavefront per k-step
-  static_assert(AG % 4 == 0 && (MODE == 1 || NI % 2 == 0), "tile shape");
-  static_assert(BM * BK * 2 <= (int)sizeof(aring0), "A stage too large");
+  static_assert(BN == 256, "two workgroups per CU: 64 weight rows per wavefront");
+  constexpr int MI = BM / 32;   // 32-row token fragments (all tile rows)
+  constexpr int NI = BN / 128;  // 32-row weight fragments per wavefront
+  constexpr int AGW = BM / 32;  // A transfers (8 rows x 128 B) per wavefront per stage
+  static_assert(MI >= 1 && AGW >= 1 && (MODE == 1 || NI % 2 == 0), "tile shape");
 
   Work wk;
-  if (!find_work(tl, true, wk, ostage)) return;
+  if (!find_work(tl, true, wk, aring3)) return;
   const int nt = wk.nt;
   const int Kdim = MODE == 0 ? d : m;
   const int R = MODE == 0 ? 2 * m : d;  // rows of the expert's weight matrix
+  const int nk = Kdim / BK;             // k-steps of 32: a multiple of 8
   const int ldc = MODE == 0 ? m : d;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-  // ---- A: global -> LDS, 16 rows x 64 bytes per wave instruction, chunk
-  // swizzle c ^ ((row >> 2) & 3); padding rows re-read row 0
-  const int lrow = lane >> 2;
-  const int swz_c = (lane & 3) ^ ((lrow >> 2) & 3);
+  // ---- A: transfer q of wave wv covers tile rows 8 g .. 8 g + 7, g = wv + 4 q;
+  // lane l fills LDS row 8 g + l / 8, physical chunk l % 8, with logical
+  // chunk (l % 8) ^ ((row >> 1) & 7).  Padding rows re-read row 0.
   const __amdgpu_buffer_rsrc_t a_rs = make_rsrc(A + (size_t)wk.row0 * Kdim, (uint32_t)wk.rows * Kdim * 2);
-  int a_voff[GA];
+  int a_voff[AGW];
 #pragma unroll
-  for (int q = 0; q < GA; ++q) {
-    const int r = wv * 16 + lrow + 64 * q;
-    a_voff[q] = ((r < wk.rows ? r : 0) * Kdim + swz_c * 8) * 2;
+  for (int q = 0; q < AGW; ++q) {
+    const int row = 8 * (wv + 4 * q) + (lane >> 3);
+    const int c = (lane & 7) ^ ((row >> 1) & 7);
+    a_voff[q] = ((row < wk.rows ? row : 0) * Kdim + c * 8) * 2;
   }
-  auto issue_a = [&](char* stage, int k0) {
+  auto issue_a = [&](char* stage, int js) {
 #pragma unroll
-    for (int q = 0; q < GA; ++q) dma16(a_rs, stage + (wv + 4 * q) * 1024, a_voff[q], k0 * 2);
+    for (int q = 0; q < AGW; ++q) dma16(a_rs, stage + (wv + 4 * q) * 1024, a_voff[q], js * AK * 2);
+  };
+  // one word of this wavefront's first transfer of a stage: reading it makes
+  // the compiler wait for this wavefront's transfers into that stage
+  auto own_word = [&](const char* stage) {
+    const int v = *reinterpret_cast<const int*>(stage + wv * 1024 + lane * 4);
+    asm volatile("" ::"v"(v));
   };
 
   // ---- B: this wavefront's NI 32-row blocks of the expert's packed matrix
@@ -536,15 +553,16 @@ __global__ __launch_bounds__(NTHR, BN == 256 ? 2 : 1) void ffn_gemm_packed_kerne
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  // A fragments (see the kernel above for the lane layout)
+  // ---- A fragments: lane l supplies row l % 32 of each 32-row block and
+  // logical chunk 2 s + l / 32 of substep s (0..3) of the stage
   const int r32 = lane & 31, kh = lane >> 5;
-  const int sw = (r32 >> 2) & 3;
-  const int lane_off0 = r32 * 64 + ((kh ^ sw) << 4);
-  const int lane_off1 = r32 * 64 + (((2 + kh) ^ sw) << 4);
-  auto load_a = [&](const char* stage, int s, bf16x8 (&af)[MI]) {
-    const char* base = stage + (s ? lane_off1 : lane_off0);
+  int a_lane[4];
 #pragma unroll
-    for (int mi = 0; mi < MI; ++mi) af[mi] = *reinterpret_cast<const bf16x8*>(base + mi * 32 * 64);
+  for (int s4 = 0; s4 < 4; ++s4) a_lane[s4] = r32 * 128 + (((2 * s4 + kh) ^ ((r32 >> 1) & 7)) << 4);
+  auto load_a = [&](const char* stage, int s4, bf16x8 (&af)[MI]) {
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+      af[mi] = *reinterpret_cast<const bf16x8*>(stage + mi * 32 * 128 + a_lane[s4]);
   };
   auto mma = [&](const bf16x8 (&af)[MI], const u32x4 (&bfr)[NI]) {
 #pragma unroll
@@ -554,82 +572,92 @@ __global__ __launch_bounds__(NTHR, BN == 256 ? 2 : 1) void ffn_gemm_packed_kerne
         acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, bfr[ni]), af[mi],
                                                               acc[mi][ni], 0, 0, 0);
   };
-  constexpr int NMF = MI * NI, NRD = MI;
-  constexpr int RPER = NMF / NRD;
+  constexpr int NMF = MI * NI;
   auto interleave = [&]() {
 #pragma unroll
-    for (int i = 0; i < NRD; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, RPER, 0);  // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);     // DS read
+    for (int i = 0; i < MI; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, NMF / MI, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);         // DS read
     }
   };
 
-  // Issue order of vector-memory operations (one in-order counter):
-  //   prologue  A0 A1 A2 A3 B0 B1 B2
-  //   step i    A(i+4) B(i+3)      while i + 4 < nk
-  //   step nk-4 B(nk-1)
-  // so at the wait of step i for A(i+1) the operations issued after it are
-  // B(i) and two full steps: 6 NI + 2 GA (the prologue steps have at least
-  // as many), then 6 NI + GA and 4 NI in the last two waiting steps.
-  // Scheduling barriers keep the compiler from reordering these groups.
-  u32x4 bq0[2][NI], bq1[2][NI], bq2[2][NI], bq3[2][NI];
+  // ---- k-step i (32 k-values): A stage i / 2, substeps 2 (i % 2) and +1;
+  // weights in register stage i % 4.  At the end of an A stage (odd i) the
+  // next stage is awaited and the finished one refilled with stage + 4.
+  //   ODD          i is the second half of an A stage
+  //   ISSUE_A      refill the finished A stage
+  //   ISSUE_B      load the weights of k-step i + 3
+  //   LAST         the final k-step (nothing follows)
   bf16x8 a0[MI], a1[MI];
-  auto step = [&](auto ISSUE_A, auto ISSUE_B, auto WAITN, int it, char* cur, char* nxt,
+  u32x4 bq0[2][NI], bq1[2][NI], bq2[2][NI], bq3[2][NI];
+  auto step = [&](auto ODD, auto ISSUE_A, auto ISSUE_B, auto LAST, int i, char* cur, char* nxt,
                   const u32x4 (&bc)[2][NI], u32x4 (&bn)[2][NI]) {
-    load_a(cur, 1, a1);
+    constexpr bool odd = decltype(ODD)::value;
+    load_a(cur, odd ? 3 : 1, a1);
     mma(a0, bc[0]);
     interleave();
-    if constexpr (decltype(WAITN)::value >= 0) {
-      wait_vmcnt<decltype(WAITN)::value>();
-      __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): reads of `cur` are complete
-      __builtin_amdgcn_s_barrier();
+    if constexpr (!decltype(LAST)::value) {
+      if constexpr (odd) {
+        own_word(nxt);
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): reads of `cur` are complete
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (decltype(ISSUE_A)::value) issue_a(cur, i / 2 + 4);
+      }
       __builtin_amdgcn_sched_barrier(0);
-      if constexpr (decltype(ISSUE_A)::value) issue_a(cur, (it + 4) * BK);
+      if constexpr (decltype(ISSUE_B)::value) load_b(bn, i + 3);
       __builtin_amdgcn_sched_barrier(0);
-      if constexpr (decltype(ISSUE_B)::value) load_b(bn, it + 3);
-      __builtin_amdgcn_sched_barrier(0);
-      load_a(nxt, 0, a0);
+      load_a(odd ? nxt : cur, odd ? 0 : 2, a0);
     }
     mma(a1, bc[1]);
-    if constexpr (decltype(WAITN)::value >= 0) interleave();
+    if constexpr (!decltype(LAST)::value) interleave();
   };
-  using N0 = std::integral_constant<int, 0>;
-  using N1 = std::integral_constant<int, 1>;
-  using WS = std::integral_constant<int, 6 * NI + 2 * GA>;
-  using W3 = std::integral_constant<int, 6 * NI + GA>;
-  using W2 = std::integral_constant<int, 4 * NI>;
-  using WE = std::integral_constant<int, -1>;
-  static_assert(6 * NI + 2 * GA < 64, "vmcnt range");
+  using F = std::integral_constant<bool, false>;
+  using Tr = std::integral_constant<bool, true>;
 
-  const int nk = Kdim / BK;  // a multiple of 4, at least 4
+  // body of 8 k-steps = 4 A stages in slots 0..3; every issue active
+  auto body = [&](int i) {
+    step(F{}, F{}, Tr{}, F{}, i + 0, aring0, aring0, bq0, bq3);
+    step(Tr{}, Tr{}, Tr{}, F{}, i + 1, aring0, aring1, bq1, bq0);
+    step(F{}, F{}, Tr{}, F{}, i + 2, aring1, aring1, bq2, bq1);
+    step(Tr{}, Tr{}, Tr{}, F{}, i + 3, aring1, aring2, bq3, bq2);
+    step(F{}, F{}, Tr{}, F{}, i + 4, aring2, aring2, bq0, bq3);
+    step(Tr{}, Tr{}, Tr{}, F{}, i + 5, aring2, aring3, bq1, bq0);
+    step(F{}, F{}, Tr{}, F{}, i + 6, aring3, aring3, bq2, bq1);
+    step(Tr{}, Tr{}, Tr{}, F{}, i + 7, aring3, aring0, bq3, bq2);
+  };
+
   issue_a(aring0, 0);
-  issue_a(aring1, BK);
-  issue_a(aring2, 2 * BK);
-  issue_a(aring3, 3 * BK);
+  issue_a(aring1, 1);
+  issue_a(aring2, 2);
+  issue_a(aring3, 3);
   __builtin_amdgcn_sched_barrier(0);
   load_b(bq0, 0);
   load_b(bq1, 1);
   load_b(bq2, 2);
   __builtin_amdgcn_sched_barrier(0);
-  wait_vmcnt<3 * GA + 3 * GB>();  // A0 landed
+  own_word(aring0);
   __builtin_amdgcn_s_barrier();
   load_a(aring0, 0, a0);
-  for (int it = 0; it + 4 < nk; it += 4) {  // branch-free body: every step refills
-    step(N1{}, N1{}, WS{}, it, aring0, aring1, bq0, bq3);
-    step(N1{}, N1{}, WS{}, it + 1, aring1, aring2, bq1, bq0);
-    step(N1{}, N1{}, WS{}, it + 2, aring2, aring3, bq2, bq1);
-    step(N1{}, N1{}, WS{}, it + 3, aring3, aring0, bq3, bq2);
-  }
-  step(N0{}, N1{}, WS{}, nk - 4, aring0, aring1, bq0, bq3);
-  step(N0{}, N0{}, W3{}, nk - 3, aring1, aring2, bq1, bq0);
-  step(N0{}, N0{}, W2{}, nk - 2, aring2, aring3, bq2, bq1);
-  step(N0{}, N0{}, WE{}, nk - 1, aring3, aring0, bq3, bq2);
+  int i = 0;
+  for (; i + 8 < nk; i += 8) body(i);
+  // last 8 k-steps: no A refills; weights up to k-step nk - 1
+  step(F{}, F{}, Tr{}, F{}, i + 0, aring0, aring0, bq0, bq3);
+  step(Tr{}, F{}, Tr{}, F{}, i + 1, aring0, aring1, bq1, bq0);
+  step(F{}, F{}, Tr{}, F{}, i + 2, aring1, aring1, bq2, bq1);
+  step(Tr{}, F{}, Tr{}, F{}, i + 3, aring1, aring2, bq3, bq2);
+  step(F{}, F{}, Tr{}, F{}, i + 4, aring2, aring2, bq0, bq3);
+  step(Tr{}, F{}, F{}, F{}, i + 5, aring2, aring3, bq1, bq0);
+  step(F{}, F{}, F{}, F{}, i + 6, aring3, aring3, bq2, bq1);
+  step(Tr{}, F{}, F{}, Tr{}, i + 7, aring3, aring0, bq3, bq2);
 
-  // ---- epilogue, staged through this wavefront's part of `ostage`
-  constexpr int RS_MAX = (BN / 4) * 2 + 16;
-  static_assert(4 * 32 * RS_MAX <= OSTAGE, "epilogue staging");
+  // ---- epilogue, staged through A slots 0 (waves 0, 1) and 1 (waves 2, 3)
+  __syncthreads();  // every wave is done with the A ring
+  constexpr int RS = (BN / 4) * 2 + 16;
+  static_assert(2 * 32 * RS <= ASLOT, "epilogue staging fits two waves per A slot");
+  char* reg = (wv < 2 ? aring0 : aring1) + (wv & 1) * 32 * RS;
   const int colbase = MODE == 0 ? nt * (BN / 2) + wv * (BN / 8) : nt * BN + wv * (BN / 4);
-  store_tile<MODE, MI, NI>(acc, ostage + wv * 32 * RS_MAX, C, ldc, wk, colbase, lane);
+  store_tile<MODE, MI, NI>(acc, reg, C, ldc, wk, colbase, lane);
 }
 
 __device__ __forceinline__ float silu_f(float g) { return g / (1.f + expf(-g)); }

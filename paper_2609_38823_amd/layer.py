@@ -108,7 +108,7 @@ class MoELayer:
         self.w_down = to_device(params["w_down"], self.dt, device)
         # bf16 layers keep the expert weights in the packed fragment layout
         # (moe_pack_expert_weights), re-laid out once here like the reorder
-        self.packed = self.dt == torch.bfloat16 and self.m % 128 == 0 and self.d % 256 == 0
+        self.packed = self.dt == torch.bfloat16 and self.m % 256 == 0 and self.d % 256 == 0
         if self.packed:
             wgu, wd = torch.empty_like(self.w_gate_up), torch.empty_like(self.w_down)
             abi.moe_pack_expert_weights(self.w_gate_up, wgu)

@@ -135,9 +135,11 @@ def test_packed_ffn_and_pack_reject(lib):
                                      NULL) == EINVAL
     assert lib.moe_expert_ffn_packed(P1, BF16, P2, 16, NULL, 0, 64, 256, 64, P3, P4, P5, ws, 1 << 30,
                                      NULL) == EUNSUPPORTED
-    assert lib.moe_expert_ffn_packed(P1, BF16, P2, 16, NULL, 0, 64, 256, 128, P3, P4, P5, ws, 16,
+    assert lib.moe_expert_ffn_packed(P1, BF16, P2, 16, NULL, 0, 64, 256, 128, P3, P4, P5, ws, 1 << 30,
+                                     NULL) == EUNSUPPORTED  # m % 256 != 0
+    assert lib.moe_expert_ffn_packed(P1, BF16, P2, 16, NULL, 0, 64, 256, 256, P3, P4, P5, ws, 16,
                                      NULL) == EWORKSPACE
-    assert lib.moe_expert_ffn_packed(P1, BF16, P2, 16, NULL, 0, 64, 256, 128, P3, P4, P1, ws, 1 << 30,
+    assert lib.moe_expert_ffn_packed(P1, BF16, P2, 16, NULL, 0, 64, 256, 256, P3, P4, P1, ws, 1 << 30,
                                      NULL) == EALIAS
     # pack: bf16 only, rows % 32 and cols % 16, no overlap, nothing to do for empty
     assert lib.moe_pack_expert_weights(P1, F32, 4, 64, 64, P2, NULL) == EUNSUPPORTED

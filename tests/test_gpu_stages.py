@@ -359,7 +359,13 @@ def test_pack_expert_weights_layout(E, R, C):
     assert np.array_equal(got, packed_layout(w))
 
 
-@pytest.mark.parametrize("E,d,m,dt,rows,K,cnt", [c for c in FFN_CASES if c[3] == "bf16"])
+PACKED_CASES = [c for c in FFN_CASES if c[3] == "bf16" and c[2] % 256 == 0] + [
+    (4, 512, 256, "bf16", 700, None, [300, 0, 1, 399]),  # one 8-k-step body, ragged tails
+    (2, 2048, 768, "bf16", 1700, None, [1600, 100]),       # many tiles of one expert
+]
+
+
+@pytest.mark.parametrize("E,d,m,dt,rows,K,cnt", PACKED_CASES)
 def test_expert_ffn_packed(E, d, m, dt, rows, K, cnt):
     sh = I.LayerShape(d=d, E=E, m=m, k=1, dtype=dt)
     prm = I.layer_params(sh, seed=E + d)
