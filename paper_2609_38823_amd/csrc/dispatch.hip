@@ -11,6 +11,7 @@
 //                            rounds follow assignment order
 //   4. gather                each token row is read once and written to its
 //                            k dispatched rows with 16-byte stores
+// Up to 8192 assignments, steps 1-3 run in one workgroup (one launch).
 #include "common.hpp"
 
 namespace decomoe {
@@ -124,6 +125,86 @@ __global__ __launch_bounds__(DP_THREADS) void dispatch_rank_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// Single-workgroup counting sort for up to DS_MAX assignments (one launch
+// instead of histogram + scan + rank): the 16 wavefronts take contiguous
+// slices in assignment order, count their slice per expert in LDS, one
+// scan turns the counts into offsets and each wavefront's starting row per
+// expert, and the wavefronts rank their slices with the ballot scheme
+// above.  Same result as the multi-workgroup path (a stable sort).
+// ---------------------------------------------------------------------------
+constexpr int DS_THREADS = 1024;
+constexpr int DS_WAVES = DS_THREADS / kWave;
+constexpr int DS_MAX = 8192;  // beyond this the multi-workgroup path is faster
+
+__global__ __launch_bounds__(DS_THREADS) void dispatch_sort_small_kernel(
+    const int32_t* __restrict__ idx, int A, int E, int key_bits, int32_t* __restrict__ counts,
+    int32_t* __restrict__ offsets, int32_t* __restrict__ src_of_row,
+    int32_t* __restrict__ row_of_slot) {
+  __shared__ int wh[DS_WAVES][1024];  // per-wave counts, then per-wave starting rows
+  __shared__ int part[DS_WAVES];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int per = (A + DS_WAVES - 1) / DS_WAVES;
+  const int lo = min(A, wv * per), hi = min(A, lo + per);
+  for (int i = tid; i < DS_WAVES * 1024; i += DS_THREADS) (&wh[0][0])[i] = 0;
+  __syncthreads();
+  for (int a = lo + lane; a < hi; a += kWave) {
+    const int e = idx[a];
+    if (e >= 0 && e < E) atomicAdd(&wh[wv][e], 1);
+  }
+  __syncthreads();
+  // thread e: total count, then an exclusive scan over the experts
+  int cnt = 0;
+  if (tid < E)
+#pragma unroll
+    for (int w = 0; w < DS_WAVES; ++w) cnt += wh[w][tid];
+  int incl = cnt;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int y = __shfl_up(incl, off, kWave);
+    if (lane >= off) incl += y;
+  }
+  if (lane == kWave - 1) part[wv] = incl;
+  __syncthreads();
+  int base = 0;
+  for (int w = 0; w < wv; ++w) base += part[w];
+  if (tid < E) {
+    int r = base + incl - cnt;  // exclusive offset of expert tid
+    counts[tid] = cnt;
+    offsets[tid] = r;
+    if (tid == E - 1) offsets[E] = r + cnt;
+#pragma unroll
+    for (int w = 0; w < DS_WAVES; ++w) {
+      const int c = wh[w][tid];
+      wh[w][tid] = r;
+      r += c;
+    }
+  }
+  __syncthreads();
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int a0 = lo; a0 < hi; a0 += kWave) {
+    const int a = a0 + lane;
+    const int e = a < hi ? idx[a] : -1;
+    const bool valid = e >= 0 && e < E;
+    uint64_t peers = __ballot(valid);
+#pragma unroll 1
+    for (int b = 0; b < key_bits; ++b) {
+      const bool bit = (e >> b) & 1;
+      const uint64_t msk = __ballot(bit);
+      peers &= bit ? msk : ~msk;
+    }
+    if (valid) {
+      const int r = wh[wv][e] + __popcll(peers & lt_mask);
+      src_of_row[r] = a;
+      row_of_slot[a] = r;
+      if ((63 - __clzll(peers)) == lane) wh[wv][e] += __popcll(peers);
+    } else if (a < hi) {
+      row_of_slot[a] = -1;
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
 // token-major gather: each token row is read once (VEC-sized vectors, rows
 // of `chunks` vectors) and stored to its k dispatched rows.  A block covers
 // one token when a row has >= 256 vectors, else `rpb` whole tokens.
@@ -169,20 +250,27 @@ hipError_t launch_dispatch(const int32_t* idx, int T, int k, int E, const void* 
   const int n_chunks = (A + DP_CHUNK - 1) / DP_CHUNK;
   int32_t* hist = static_cast<int32_t*>(ws);
   int32_t* base = hist + (size_t)n_chunks * E;
-  if (n_chunks > 0) {
-    dispatch_hist_kernel<<<n_chunks, DP_THREADS, 0, s>>>(idx, A, E, hist);
-    hipError_t err = hipGetLastError();
-    if (err != hipSuccess) return err;
-  }
-  dispatch_scan_kernel<<<1, 1024, 0, s>>>(hist, n_chunks, E, base, counts, offsets);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess || n_chunks == 0) return err;
   int key_bits = 0;
   while ((1 << key_bits) < E) ++key_bits;
-  dispatch_rank_kernel<<<n_chunks, DP_THREADS, 0, s>>>(idx, A, E, key_bits, base, src_of_row,
-                                                        row_of_slot);
-  err = hipGetLastError();
-  if (err != hipSuccess || !x) return err;
+  hipError_t err;
+  if (A <= DS_MAX) {
+    dispatch_sort_small_kernel<<<1, DS_THREADS, 0, s>>>(idx, A, E, key_bits, counts, offsets,
+                                                        src_of_row, row_of_slot);
+    err = hipGetLastError();
+    if (err != hipSuccess || A == 0) return err;
+  } else {
+    dispatch_hist_kernel<<<n_chunks, DP_THREADS, 0, s>>>(idx, A, E, hist);
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    dispatch_scan_kernel<<<1, 1024, 0, s>>>(hist, n_chunks, E, base, counts, offsets);
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    dispatch_rank_kernel<<<n_chunks, DP_THREADS, 0, s>>>(idx, A, E, key_bits, base, src_of_row,
+                                                          row_of_slot);
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+  }
+  if (!x) return err;
   const size_t row_bytes = (size_t)d * elt;
   if (row_bytes % 16 == 0) {
     int chunks = (int)(row_bytes / 16);

@@ -457,7 +457,8 @@ __global__ __launch_bounds__(256) void pack_weights_kernel(const uint4* __restri
 // operand bypasses LDS.  Per k-step of 32, wavefront wv loads its 2 x NI
 // weight fragments (NI 32-row blocks x two 16-wide substeps, 1 KB each,
 // fully coalesced) into a ring of four register stages, three k-steps
-// ahead.  Only the token-row tile A, which all four wavefronts share, goes
+// ahead (issued as soon as a stage's registers are free, at the top of the
+// k-step after their last use).  Only the token-row tile A, which all four wavefronts share, goes
 // through LDS: global -> LDS transfers of whole 128-byte row segments
 // (A stages of 64 k-values, 8 rows per wave instruction) into a ring of
 // four stages, three stages (192 k-values) ahead.  In LDS a 128-byte row
@@ -593,6 +594,9 @@ __global__ __launch_bounds__(NTHR, 2) void ffn_gemm_packed_kernel(
   auto step = [&](auto ODD, auto ISSUE_A, auto ISSUE_B, auto LAST, int i, char* cur, char* nxt,
                   const u32x4 (&bc)[2][NI], u32x4 (&bn)[2][NI]) {
     constexpr bool odd = decltype(ODD)::value;
+    // the weight registers of k-step i - 1 are free: refill them first
+    if constexpr (decltype(ISSUE_B)::value) load_b(bn, i + 3);
+    __builtin_amdgcn_sched_barrier(0);
     load_a(cur, odd ? 3 : 1, a1);
     mma(a0, bc[0]);
     interleave();
@@ -603,10 +607,8 @@ __global__ __launch_bounds__(NTHR, 2) void ffn_gemm_packed_kernel(
         __builtin_amdgcn_s_barrier();
         __builtin_amdgcn_sched_barrier(0);
         if constexpr (decltype(ISSUE_A)::value) issue_a(cur, i / 2 + 4);
+        __builtin_amdgcn_sched_barrier(0);
       }
-      __builtin_amdgcn_sched_barrier(0);
-      if constexpr (decltype(ISSUE_B)::value) load_b(bn, i + 3);
-      __builtin_amdgcn_sched_barrier(0);
       load_a(odd ? nxt : cur, odd ? 0 : 2, a0);
     }
     mma(a1, bc[1]);

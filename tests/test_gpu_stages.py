@@ -270,6 +270,10 @@ def test_calibrate_worked_example_golden():
     (3000, 1000, 4, 64, "bf16", None),
     (129, 5, 5, 6, "bf16", None),
     (1000, 64, 2, 10, "f32", None),
+    # more than 8192 assignments (also 4096 x 8 and 3000 x 4 above): the
+    # multi-workgroup histogram/scan/rank path
+    (9000, 128, 8, 64, "bf16", None),
+    (8193, 1000, 8, 16, "f32", 999),
 ])
 def test_dispatch_exact(T, E, k, d, dt, K):
     idx, _ = I.synthetic_routing(T, E, k, seed=3 * T + E, K=K)
