@@ -482,10 +482,9 @@ __device__ __forceinline__ u32x4 load_frag(__amdgpu_buffer_rsrc_t rs, int voff, 
 }
 
 template <int MODE, int BM, int BN>
-__global__ __launch_bounds__(NTHR, 2) void ffn_gemm_packed_kernel(
+__global__ __launch_bounds__(NTHR, BN == 256 ? 2 : 1) void ffn_gemm_packed_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ Wp, uint16_t* __restrict__ C,
     const Tiles tl, int d, int m) {
-  static_assert(BN == 256, "two workgroups per CU: 64 weight rows per wavefront");
   constexpr int MI = BM / 32;   // 32-row token fragments (all tile rows)
   constexpr int NI = BN / 128;  // 32-row weight fragments per wavefront
   constexpr int AGW = BM / 32;  // A transfers (8 rows x 128 B) per wavefront per stage
@@ -653,11 +652,11 @@ __global__ __launch_bounds__(NTHR, 2) void ffn_gemm_packed_kernel(
   step(F{}, F{}, F{}, F{}, i + 6, aring3, aring3, bq2, bq1);
   step(Tr{}, F{}, F{}, Tr{}, i + 7, aring3, aring0, bq3, bq2);
 
-  // ---- epilogue, staged through A slots 0 (waves 0, 1) and 1 (waves 2, 3)
+  // ---- epilogue, wave w staged through A slot w
   __syncthreads();  // every wave is done with the A ring
   constexpr int RS = (BN / 4) * 2 + 16;
-  static_assert(2 * 32 * RS <= ASLOT, "epilogue staging fits two waves per A slot");
-  char* reg = (wv < 2 ? aring0 : aring1) + (wv & 1) * 32 * RS;
+  static_assert(32 * RS <= ASLOT, "epilogue staging fits one wave per A slot");
+  char* reg = wv == 0 ? aring0 : wv == 1 ? aring1 : wv == 2 ? aring2 : aring3;
   const int colbase = MODE == 0 ? nt * (BN / 2) + wv * (BN / 8) : nt * BN + wv * (BN / 4);
   store_tile<MODE, MI, NI>(acc, reg, C, ldc, wk, colbase, lane);
 }
