@@ -39,35 +39,41 @@ __global__ __launch_bounds__(DP_THREADS) void dispatch_hist_kernel(const int32_t
   for (int e = threadIdx.x; e < E; e += DP_THREADS) hist[(size_t)blockIdx.x * E + e] = h[e];
 }
 
-// one workgroup of 1024 threads; thread e owns expert e
+// one workgroup of 1024 threads; thread e owns expert e.  The chunk
+// columns are read 16 at a time (independent loads in flight), the scan over
+// the experts is a wavefront scan plus the wavefront totals.
 __global__ __launch_bounds__(1024) void dispatch_scan_kernel(const int32_t* __restrict__ hist,
                                                              int n_chunks, int E,
                                                              int32_t* __restrict__ base,
                                                              int32_t* __restrict__ counts,
                                                              int32_t* __restrict__ offsets) {
-  __shared__ int sc[1024];
-  const int e = threadIdx.x;
+  __shared__ int part[1024 / kWave];
+  const int e = threadIdx.x, lane = e & 63, wv = e >> 6;
   int cnt = 0;
-  if (e < E)
-    for (int c = 0; c < n_chunks; ++c) cnt += hist[(size_t)c * E + e];
-  sc[e] = e < E ? cnt : 0;
-  __syncthreads();
-  // inclusive Hillis-Steele scan over the 1024 counters
-  for (int off = 1; off < 1024; off <<= 1) {
-    int v = e >= off ? sc[e - off] : 0;
-    __syncthreads();
-    sc[e] += v;
-    __syncthreads();
-  }
   if (e < E) {
-    int run = sc[e] - cnt;  // exclusive
+#pragma unroll 16
+    for (int c = 0; c < n_chunks; ++c) cnt += hist[(size_t)c * E + e];
+  }
+  int incl = cnt;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int y = __shfl_up(incl, off, kWave);
+    if (lane >= off) incl += y;
+  }
+  if (lane == kWave - 1) part[wv] = incl;
+  __syncthreads();
+  int run = incl - cnt;  // exclusive within the wavefront
+  for (int w = 0; w < wv; ++w) run += part[w];
+  if (e < E) {
     counts[e] = cnt;
     offsets[e] = run;
+    if (e == E - 1) offsets[E] = run + cnt;
+#pragma unroll 16
     for (int c = 0; c < n_chunks; ++c) {
+      const int h = hist[(size_t)c * E + e];
       base[(size_t)c * E + e] = run;
-      run += hist[(size_t)c * E + e];
+      run += h;
     }
-    if (e == E - 1) offsets[E] = run;
   }
 }
 

@@ -182,14 +182,53 @@ __global__ __launch_bounds__(256) void router_logits_simt_kernel(const void* __r
 // arg-max (value descending, index ascending on ties) pick the slots in
 // order.  Weights are the softmax of the k selected logits.
 // ---------------------------------------------------------------------------
-constexpr int TK_MAXC = 16;  // E <= 1024 = 16 values per lane
+constexpr int TK_MAXC = 16;  // E <= 1024 = 16 values per lane (MAXC: per instantiation)
 
 __device__ __forceinline__ void better(float& v, int& i, float ov, int oi) {
   if (ov > v || (ov == v && oi < i)) { v = ov; i = oi; }
 }
 
+// (value, index) of lane l -> the wavefront's best pair in every lane
+// without LDS round trips: DPP moves within each row of 16 lanes (quad
+// swaps, then the half-row and row mirrors pair the groups), then the four
+// row results are read with v_readlane and combined (the same in every
+// lane).  `better` is a total order on pairs, so the pairing order does not
+// change the result.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+template <int CTRL>
+__device__ __forceinline__ void dpp_better(float& v, int& i) {
+  better(v, i, dpp_f<CTRL>(v), __builtin_amdgcn_mov_dpp(i, CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float lane_f(float v, int l) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+}
+__device__ __forceinline__ void wave_best(float& v, int& i) {
+  dpp_better<0xB1>(v, i);   // quad_perm [1, 0, 3, 2]
+  dpp_better<0x4E>(v, i);   // quad_perm [2, 3, 0, 1]
+  dpp_better<0x141>(v, i);  // row_half_mirror
+  dpp_better<0x140>(v, i);  // row_mirror
+  float bv = lane_f(v, 0);
+  int bi = __builtin_amdgcn_readlane(i, 0);
+#pragma unroll
+  for (int r = 1; r < 4; ++r) better(bv, bi, lane_f(v, 16 * r), __builtin_amdgcn_readlane(i, 16 * r));
+  v = bv;
+  i = bi;
+}
+// sum over the wavefront: row sums by DPP, then the four rows in order
+__device__ __forceinline__ float wave_sum(float v) {
+  v += dpp_f<0xB1>(v);
+  v += dpp_f<0x4E>(v);
+  v += dpp_f<0x141>(v);
+  v += dpp_f<0x140>(v);
+  return ((lane_f(v, 0) + lane_f(v, 16)) + lane_f(v, 32)) + lane_f(v, 48);
+}
+
 // With `part` (split-K router), the logits are first formed here as
 // (part[0] + part[1] + ... + part[S-1]) + b, written to `logits`, and used.
+template <int MAXC>  // values per lane: E <= 64 MAXC
 __global__ __launch_bounds__(256) void topk_kernel(float* __restrict__ logits, int T, int E,
                                                    int k, const int32_t* __restrict__ seg_offsets,
                                                    int n_seg, const int32_t* __restrict__ K_dev,
@@ -205,11 +244,11 @@ __global__ __launch_bounds__(256) void topk_kernel(float* __restrict__ logits, i
     Klim = clampi(K_dev[s], k, E);
   }
   float* row = logits + (size_t)t * E;
-  float v[TK_MAXC];
+  float v[MAXC];
   uint32_t alive = 0;
   if (part) {
 #pragma unroll
-    for (int c = 0; c < TK_MAXC; ++c) {
+    for (int c = 0; c < MAXC; ++c) {
       const int e = lane + c * 64;
       if (e < E) {
         float a = part[(size_t)t * E + e];
@@ -219,7 +258,7 @@ __global__ __launch_bounds__(256) void topk_kernel(float* __restrict__ logits, i
     }
   }
 #pragma unroll
-  for (int c = 0; c < TK_MAXC; ++c) {
+  for (int c = 0; c < MAXC; ++c) {
     int e = lane + c * 64;
     v[c] = -FLT_MAX;
     if (e < Klim) { v[c] = row[e]; alive |= 1u << c; }
@@ -230,22 +269,16 @@ __global__ __launch_bounds__(256) void topk_kernel(float* __restrict__ logits, i
     float bv = -INFINITY;
     int bi = 0x7fffffff;
 #pragma unroll
-    for (int c = 0; c < TK_MAXC; ++c)
+    for (int c = 0; c < MAXC; ++c)
       if (alive & (1u << c)) better(bv, bi, v[c], lane + c * 64);
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-      float ov = __shfl_xor(bv, off, 64);
-      int oi = __shfl_xor(bi, off, 64);
-      better(bv, bi, ov, oi);
-    }
+    wave_best(bv, bi);
     if (bi < E && (bi & 63) == lane) alive &= ~(1u << (bi >> 6));
     if (lane == r) { my_v = bv; my_i = bi; }
   }
-  const float v0 = __shfl(my_v, 0, 64);
+  const float v0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_v), 0));
   float ex = lane < k ? expf(my_v - v0) : 0.f;
   float sum = ex;
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) sum += __shfl_xor(sum, off, 64);
+  sum = wave_sum(sum);
   if (lane < k) {
     idx[(size_t)t * k + lane] = my_i;
     w[(size_t)t * k + lane] = ex / sum;
@@ -293,8 +326,14 @@ hipError_t launch_route(const void* x, bool x_bf16, const float* w_r, const floa
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
   }
-  topk_kernel<<<(T + 3) / 4, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S,
-                                          bias, idx, w);
+  const int blocks = (T + 3) / 4;
+  if (E <= 128)
+    topk_kernel<2><<<blocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w);
+  else if (E <= 256)
+    topk_kernel<4><<<blocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w);
+  else
+    topk_kernel<TK_MAXC><<<blocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias,
+                                                idx, w);
   return hipGetLastError();
 }
 
