@@ -18,7 +18,20 @@ step).  Every ABI call is bracketed by HIP events on the stream it runs on,
 giving per-stage times and the roofline of the dominant kernel (the expert
 FFN).  The CPU oracle is timed on the same step as the CPU baseline.
 
+Other workloads (one JSON line each, same fields):
+
+  --workload stack48   48-layer stack over 7680 visual + 512 text rows, exit
+                       at layer 20 (dense layers 0-19 on 8192 rows, RCEP
+                       layers 20-47 on 512 rows, p = 0.9); value = prefill
+                       tokens/s through the 48 MoE layers
+  --workload decode64  64 decode tokens through the same 48 layers, RCEP in
+                       every layer (p = 0.85), one HIP graph per step;
+                       value = decode tokens/s
+  --workload stress    routing, dispatch and combine of the same layer at
+                       65536 rows (bandwidth shape); value = rows/s
+
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+                       [--workload layer|stack48|decode64|stress]
 """
 
 from __future__ import annotations
@@ -126,12 +139,18 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--traffic-run", action="store_true",
                     help="only run the dense layer and a known-size copy (for rocprofv3 counter passes)")
+    ap.add_argument("--workload", default="layer", choices=["layer", "stack48", "decode64", "stress"])
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU only: the path has no multi-GPU execution in this build "
-              "(see the design notes for how it would shard); run with --gpus 1", file=sys.stderr)
+        print("bench.py measures one GPU only: the path has no multi-GPU execution "
+              "(the design notes describe how it would shard); run with --gpus 1", file=sys.stderr)
         return 2
+    fn = {"layer": bench_layer, "stack48": bench_stack48, "decode64": bench_decode64,
+          "stress": bench_stress}[args.workload]
+    return fn(args)
 
+
+def bench_layer(args) -> int:
     import torch
 
     from paper_2609_38823_amd import abi, inputs as I
@@ -290,6 +309,309 @@ def main() -> int:
     }
     print(json.dumps(line), flush=True)
     return 0
+
+
+# --------------------------------------------------------------------------
+# Other workloads
+# --------------------------------------------------------------------------
+def _setup_gpu():
+    import torch
+
+    from paper_2609_38823_amd import abi
+
+    if not os.path.exists(abi.LIB_PATH):
+        from paper_2609_38823_amd import build
+        build.build()
+    abi.load()
+    torch.cuda.set_device(0)
+
+
+def _log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def _build_stack(wl):
+    from paper_2609_38823_amd.stack import MoEStack
+    t0 = time.perf_counter()
+    st = MoEStack(wl, progress=lambda l: _log(f"layer {l} loaded") if l % 8 == 7 else None)
+    return st, time.perf_counter() - t0
+
+
+def _line(metric, value, unit, args, ms_step, config, roof, cpu, **extra):
+    line = {"metric": metric, "value": value, "unit": unit, "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+            "config": config, "roofline": roof, "cpu_baseline": cpu}
+    line.update(extra)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def _timed_layer(st, l, h, rcep, p, stream):
+    """One layer with events after each ABI call; returns per-call ms and
+    the buffers (h is left unmodified: the layer writes a scratch copy)."""
+    import torch
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(12)]
+    it = iter(ev)
+    first = next(it)
+    first.record(stream)
+    used = [first]
+
+    def mark():
+        e = next(it)
+        e.record(stream)
+        used.append(e)
+
+    dst = torch.empty_like(h)
+    b = st.layer_forward(l, h, dst, rcep, p, mark=mark)
+    torch.cuda.synchronize()
+    return [used[i].elapsed_time(used[i + 1]) for i in range(len(used) - 1)], b
+
+
+def bench_stack48(args) -> int:
+    """48-layer prefill: 20 dense layers over 8192 rows, the visual drop,
+    28 RCEP layers over the 512 text rows."""
+    import torch
+
+    from paper_2609_38823_amd import inputs as I
+    _setup_gpu()
+    wl = I.WORKLOADS["qwen3vl_stack48_8192"]
+    sh = wl.shape
+    d, E, m, k = sh.d, sh.E, sh.m, sh.k
+    st, setup_s = _build_stack(wl)
+    x_np = I.tokens(sh, wl.T, seed=wl.seed)
+    x = torch.from_numpy(x_np).cuda().to(torch.bfloat16)
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        st.forward(x, wl.n_visual, wl.p, wl.exit_layer)
+    torch.cuda.synchronize()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    evs[0].record(stream)
+    for s in range(args.steps):
+        st.forward(x, wl.n_visual, wl.p, wl.exit_layer)
+        evs[s + 1].record(stream)
+    torch.cuda.synchronize()
+    step_ms = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
+    ms = float(np.mean(step_ms))
+    Ks = st.K_trace[:, 0].cpu().numpy()[wl.exit_layer:]
+    # per-call times of one dense layer (8192 rows) and one RCEP layer (512)
+    h_text = torch.empty((wl.T - wl.n_visual, d), dtype=torch.bfloat16, device="cuda")
+    from paper_2609_38823_amd import abi
+    abi.drop_visual_block(x, 0, wl.n_visual, h_text)
+    dense_calls, bd = _timed_layer(st, 0, x, False, wl.p, stream)
+    rcep_calls, br = _timed_layer(st, wl.exit_layer, h_text, True, wl.p, stream)
+    touched = int((bd.counts.cpu() > 0).sum())
+    K20 = int(st.K_trace[wl.exit_layer, 0].cpu())
+    f, b = stage_flops_bytes("ffn", wl.T, d, E, m, k, touched, E)
+    ffn_ms = dense_calls[2]
+    roof = roofline(f, b, ffn_ms * 1e-3)
+    roof["kernel"] = "moe_expert_ffn_packed @ dense 8192 rows (layer 0 of the stack)"
+    roof["traffic"] = None
+    roof["mfma_frac"] = f / (ffn_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS
+    per_tok = 2 * d * E + 6 * k * d * m
+    alg_flops = per_tok * (wl.T * wl.exit_layer + (wl.T - wl.n_visual) * (wl.layers - wl.exit_layer))
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = _oracle_stack_sample(st, x_np, wl)
+    names_d = ["route", "dispatch", "ffn", "combine_residual"]
+    names_r = ["route_full", "calibrate", "route_prefix", "dispatch", "ffn", "combine_residual"]
+    return _line(
+        "MoE-stack prefill tokens/s (48 MoE layers, SAVB exit at layer 20, RCEP p 0.9)",
+        wl.T / (ms * 1e-3), "tokens/s", args, ms,
+        {"workload": "Qwen3-VL-MoE 48-layer MoE stack (d 2048, 128 experts x 768, top-8, bf16): "
+                     "8192 prefill rows (7680 visual + 512 text); layers 0-19 dense over 8192 rows, "
+                     "visual rows dropped at the entrance of layer 20, layers 20-47 RCEP over 512 rows",
+         "seed": wl.seed, "zipf_alpha": sh.zipf_alpha, "exit_layer": wl.exit_layer},
+        roof, cpu,
+        tflops=alg_flops / (ms * 1e-3) / 1e12, K_per_rcep_layer=[int(v) for v in Ks],
+        K_mean=float(np.mean(Ks)), step_ms_min=float(np.min(step_ms)),
+        dense_layer_8192={n: round(v, 4) for n, v in zip(names_d, dense_calls)},
+        rcep_layer_512={n: round(v, 4) for n, v in zip(names_r, rcep_calls)},
+        touched_dense=touched, K_rcep_layer_512=K20, setup_s=round(setup_s, 1))
+
+
+def _oracle_stack_sample(st, x_np, wl):
+    """The oracle on one dense layer (8192 rows) and one RCEP layer (512
+    rows) of the stack, extrapolated to the stack's 20 + 28 layers."""
+    import oracle
+    import torch
+
+    from paper_2609_38823_amd import inputs as I
+
+    def params(l):
+        rp = I.router_params(st.sh, wl.seed, l)
+        gu, dn = I.device_expert_weights(st.sh, wl.seed, l)
+        gu_h, dn_h = gu.float().cpu().numpy(), dn.float().cpu().numpy()
+        del gu, dn
+        torch.cuda.empty_cache()
+        w_r, bias, wgu, wd = oracle.permute_experts(st.orders[l], rp["w_r"], rp["bias"], gu_h, dn_h)
+        return w_r, bias, wgu, wd
+
+    k = st.sh.k
+    w_r, bias, wgu, wd = params(0)
+    t0 = time.perf_counter()
+    oracle.moe_layer_dense(x_np, w_r, bias, wgu, wd, k)
+    t_dense = time.perf_counter() - t0
+    w_r, bias, wgu, wd = params(wl.exit_layer)
+    t0 = time.perf_counter()
+    oracle.moe_layer_rcep(x_np[wl.n_visual:], w_r, bias, wgu, wd, k, wl.p)
+    t_rcep = time.perf_counter() - t0
+    sec = t_dense * wl.exit_layer + t_rcep * (wl.layers - wl.exit_layer)
+    info = cpu_info()
+    return dict(value=wl.T / sec, unit="tokens/s", cores=info.get("blas_threads") or info["affinity_cores"],
+                kind="oracle", sample=("one dense layer over 8192 rows and one RCEP layer over 512 rows, "
+                                       "timed, extrapolated x20 + x28 (numpy float64)"),
+                seconds_measured=round(t_dense + t_rcep, 3), extrapolated=True, **info)
+
+
+def bench_decode64(args) -> int:
+    """64 decode tokens through 48 RCEP layers, one HIP graph per step."""
+    import torch
+
+    from paper_2609_38823_amd import inputs as I
+    _setup_gpu()
+    wl = I.WORKLOADS["qwen3vl_decode64"]
+    sh = wl.shape
+    d, E, m, k = sh.d, sh.E, sh.m, sh.k
+    st, setup_s = _build_stack(I.WORKLOADS["qwen3vl_stack48_8192"])
+    x_np = I.tokens(sh, wl.T, seed=wl.seed, stream="decode")
+    x = torch.from_numpy(x_np).cuda().to(torch.bfloat16)
+    stream = torch.cuda.current_stream()
+    # touched experts per layer (eager, outside the timed region)
+    touched = []
+    h = x.clone()
+    for l in range(st.L):
+        dst = torch.empty_like(h)
+        b = st.layer_forward(l, h, dst, True, wl.p)
+        touched.append(int((b.counts.cpu() > 0).sum()))
+        h = dst
+    Ks = st.K_trace[:, 0].cpu().numpy()
+    # eager step time
+    for _ in range(2):
+        st.forward(x, 0, wl.p, exit_layer=0)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        st.forward(x, 0, wl.p, exit_layer=0)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    eager_ms = e0.elapsed_time(e1) / args.steps
+    g, _ = st.capture_decode(x, wl.p)
+    for _ in range(args.warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    evs[0].record(stream)
+    for s in range(args.steps):
+        g.replay()
+        evs[s + 1].record(stream)
+    torch.cuda.synchronize()
+    step_ms = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
+    ms = float(np.mean(step_ms))
+    A = wl.T * k
+    wbytes = sum(t * 3 * d * m * 2 for t in touched)
+    nbytes = wbytes + st.L * (2 * A * d * 2 + 3 * wl.T * d * 2 + d * E * 4)
+    ach = nbytes / (ms * 1e-3) / 1e9
+    roof = dict(bound="hbm", achieved=ach, peak=PEAK_HBM_GBS, unit="GB/s", frac=ach / PEAK_HBM_GBS,
+                traffic=None, kernel="whole decode step (48 layers, weight streaming of touched experts)")
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = _oracle_decode_sample(st, x_np, wl)
+    return _line(
+        "MoE-stack decode tokens/s (64 tokens x 48 MoE layers, RCEP p 0.85, HIP graph)",
+        wl.T / (ms * 1e-3), "tokens/s", args, ms,
+        {"workload": "Qwen3-VL-MoE 48-layer MoE stack (d 2048, 128 experts x 768, top-8, bf16): "
+                     "decode of 64 single text tokens, RCEP in all 48 layers, one K per layer",
+         "seed": wl.seed, "zipf_alpha": sh.zipf_alpha},
+        roof, cpu, eager_ms_per_step=eager_ms, step_ms_min=float(np.min(step_ms)),
+        K_per_layer=[int(v) for v in Ks], touched_per_layer=touched,
+        weight_bytes_per_step=wbytes, setup_s=round(setup_s, 1))
+
+
+def _oracle_decode_sample(st, x_np, wl):
+    """The oracle's decode over the first 4 layers, extrapolated to 48."""
+    import oracle
+    import torch
+
+    from paper_2609_38823_amd import inputs as I
+    n = 4
+    sec = 0.0
+    h = np.asarray(x_np, np.float64)
+    for l in range(n):
+        rp = I.router_params(st.sh, st.wl.seed, l)
+        gu, dn = I.device_expert_weights(st.sh, st.wl.seed, l)
+        gu_h, dn_h = gu.float().cpu().numpy(), dn.float().cpu().numpy()
+        del gu, dn
+        torch.cuda.empty_cache()
+        w_r, bias, wgu, wd = oracle.permute_experts(st.orders[l], rp["w_r"], rp["bias"], gu_h, dn_h)
+        t0 = time.perf_counter()
+        h = h + oracle.moe_layer_rcep(h, w_r, bias, wgu, wd, st.sh.k, wl.p)["out"]
+        sec += time.perf_counter() - t0
+    sec *= st.L / n
+    info = cpu_info()
+    return dict(value=wl.T / sec, unit="tokens/s", cores=info.get("blas_threads") or info["affinity_cores"],
+                kind="oracle", sample="decode of the 64 tokens through layers 0-3, timed, extrapolated x12 "
+                                      "(numpy float64)", extrapolated=True, **info)
+
+
+def bench_stress(args) -> int:
+    """Routing, dispatch and combine of the layer at 65536 rows."""
+    import torch
+
+    from paper_2609_38823_amd import abi, inputs as I
+    from paper_2609_38823_amd.layer import Buffers, to_device
+    _setup_gpu()
+    wl = I.WORKLOADS["qwen3vl_dense_4096"]
+    sh = wl.shape
+    d, E, m, k = sh.d, sh.E, sh.m, sh.k
+    T = 65536
+    rp = I.router_params(sh, wl.seed)
+    w_r, bias = to_device(rp["w_r"], torch.float32), to_device(rp["bias"], torch.float32)
+    x = to_device(I.tokens(sh, T, seed=1), torch.bfloat16)
+    b = Buffers(T, d, E, m, k, torch.bfloat16)
+    stream = torch.cuda.current_stream()
+    names = ["route_full", "dispatch", "combine"]
+
+    def step(ev=None):
+        it = iter(ev) if ev is not None else None
+
+        def mark():
+            if it is not None:
+                next(it).record(stream)
+
+        mark()
+        abi.moe_route(x, w_r, bias, k, b.logits, b.idx, b.w, ws=b.ws)
+        mark()
+        abi.moe_dispatch(b.idx, E, x, b.counts, b.offsets, b.src_of_row, b.row_of_slot, b.x_perm, b.ws)
+        mark()
+        abi.moe_combine(b.x_perm, b.row_of_slot, b.w, b.out)  # dispatched rows stand in for y_perm
+        mark()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    for s in range(args.steps):
+        step(evs[s])
+    torch.cuda.synchronize()
+    st_ms = {n: float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs])) for i, n in enumerate(names)}
+    ms = sum(st_ms.values())
+    rep = {}
+    for n in names:
+        f, nb = stage_flops_bytes(n, T, d, E, m, k, E, E)
+        rep[n] = dict(ms=round(st_ms[n], 4), roofline=roofline(f, nb, st_ms[n] * 1e-3),
+                      gflop=round(f / 1e9, 3), mb=round(nb / 1e6, 3))
+    f, nb = stage_flops_bytes("dispatch", T, d, E, m, k, E, E)
+    roof = roofline(f, nb, st_ms["dispatch"] * 1e-3)
+    roof["kernel"] = "moe_dispatch @ 65536 rows (counting sort + row gather)"
+    roof["traffic"] = None
+    return _line(
+        "Routing + dispatch + combine rows/s at 65536 rows (bandwidth shape of the MoE layer)",
+        T / (ms * 1e-3), "rows/s", args, ms,
+        {"workload": "Qwen3-VL-MoE MoE layer shape (d 2048, 128 experts, top-8, bf16, fp32 router) at "
+                     "65536 rows: moe_route (full pool), moe_dispatch, moe_combine (no expert FFN)",
+         "seed": 1}, roof, None, stages=rep)
 
 
 if __name__ == "__main__":

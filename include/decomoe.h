@@ -14,7 +14,9 @@
  *     (same, on weights re-laid out once at load time)            moe_expert_ffn_packed,
  *                                                                 moe_pack_expert_weights
  *   weighted combine back to token order                          moe_combine
+ *     (same, plus the residual of a stack of MoE blocks)          moe_combine_residual
  *   SAVB visual-block removal from the hidden state (Sec. 3.2)   drop_visual_block
+ *   physical expert reorder by pi at load time (Algorithm 1)      moe_permute_experts
  *
  * Conventions shared by every entry point
  *   - Every array pointer is a DEVICE pointer owned by the caller; the
@@ -37,7 +39,7 @@
  *   - Outputs must not overlap inputs or each other (MOE_EALIAS), except
  *     where stated.
  *   - Array pointers must be 16-byte aligned (MOE_EINVAL otherwise);
- *     drop_visual_block only needs element alignment.
+ *     drop_visual_block and moe_permute_experts only need element alignment.
  *   - All results are deterministic: repeated calls on the same inputs give
  *     bitwise-identical outputs (no floating-point atomics anywhere).
  */
@@ -242,6 +244,42 @@ int moe_expert_ffn_packed(const void* x_perm, moe_dtype dtype, const int32_t* of
 int moe_combine(const void* y_perm, moe_dtype dtype, const int32_t* row_of_slot,
                 const float* topk_w, int T, int k, int d, void* out,
                 hipStream_t stream);
+
+/*
+ * moe_combine_residual - moe_combine followed by the residual connection of
+ * a stack of MoE blocks (the hidden stream h <- h + MoE(h) between the
+ * layers of Algorithm 2):
+ *
+ *   out_t = residual_t + sum_{j<k} w_{t,j} y_perm[row_of_slot[t*k+j]],
+ *
+ * the weighted sum accumulated in float32 in slot order, the residual added
+ * in float32, then rounded once to dtype.  `residual` [T, d] (dtype) may be
+ * `out` itself (in-place update of the hidden state); any other overlap of
+ * out with an input is MOE_EALIAS.  Same arguments and limits otherwise.
+ */
+int moe_combine_residual(const void* y_perm, moe_dtype dtype, const int32_t* row_of_slot,
+                         const float* topk_w, int T, int k, int d, const void* residual,
+                         void* out, hipStream_t stream);
+
+/*
+ * moe_permute_experts - physical reorder of one layer's expert parameters by
+ * the Mean-Mass order pi (Sec. 3.3 after Eq. 9; Algorithm 1): new expert j
+ * is native expert order[j] in
+ *   w_r        [d, E] float32 router weights (columns permuted),
+ *   bias       [E] float32,
+ *   w_gate_up  [E, 2m, d] (dtype) and w_down [E, d, m] (dtype) (blocks permuted).
+ * `order` [E] int32 is a device array, e.g. moe_calibrate_prefix's order
+ * output; it must be a permutation of [0, E).  An entry outside [0, E)
+ * yields zeros for that new expert (no out-of-range read); duplicates are
+ * not detected.  Each input/output pair may be NULL/NULL to skip that
+ * tensor (one of a pair NULL without the other is MOE_EINVAL).  Outputs
+ * must not overlap any input (MOE_EALIAS).  Runs once when a layer is
+ * loaded; it moves storage and computes nothing.  No workspace.
+ */
+int moe_permute_experts(const int32_t* order, int E, int d, int m, moe_dtype dtype,
+                        const float* w_r, const float* bias, const void* w_gate_up,
+                        const void* w_down, float* w_r_out, float* bias_out,
+                        void* w_gate_up_out, void* w_down_out, hipStream_t stream);
 
 /*
  * drop_visual_block - SAVB visual-block removal from the hidden state

@@ -52,6 +52,7 @@ __all__ = [
     "drop_visual_block",
     "moe_layer_dense",
     "moe_layer_rcep",
+    "moe_stack",
     "segment_of_tokens",
 ]
 
@@ -372,3 +373,37 @@ def moe_layer_rcep(x, w_r, bias, w_gate_up, w_down, k, p, seg_offsets=None,
                idx=idx, w=w)
     res.update(_experts_and_combine(x, idx, w, w_gate_up, w_down, E))
     return res
+
+
+# --------------------------------------------------------------------------
+# A stack of MoE blocks (Algorithm 2's loop over layers)
+# --------------------------------------------------------------------------
+def moe_stack(h, layers, k, p, exit_layer=None, v0=0, v1=0, seg_offsets=None):
+    """Algorithm 2 over a stack of MoE blocks with the residual stream
+    h <- h + MoE_l(h) between blocks (the blocks' attention sublayers are
+    not part of this stack).
+
+    ``layers`` holds each layer's reordered parameters (dicts with w_r,
+    bias, w_gate_up, w_down).  READING (exit placement): ``exit_layer`` is
+    the first text-only layer; the visual rows [v0, v1) are removed at its
+    entrance (SAVB, Sec. 3.2), layers before it run the dense span over all
+    rows and layers from it on run the RCEP span (Sec. 3.3).  None: no exit,
+    every layer dense.  0 with v0 == v1: RCEP in every layer (decode).
+
+    Returns the final hidden rows and, per layer, K (None for dense layers).
+    """
+    h = np.asarray(h, F64)
+    Ks = []
+    for l, prm in enumerate(layers):
+        rcep = exit_layer is not None and l >= exit_layer
+        if exit_layer is not None and l == exit_layer:
+            h = drop_visual_block(h, v0, v1)
+        if rcep:
+            r = moe_layer_rcep(h, prm["w_r"], prm["bias"], prm["w_gate_up"], prm["w_down"], k, p,
+                               seg_offsets=seg_offsets)
+            Ks.append(r["K"])
+        else:
+            r = moe_layer_dense(h, prm["w_r"], prm["bias"], prm["w_gate_up"], prm["w_down"], k)
+            Ks.append(None)
+        h = h + r["out"]
+    return h, Ks

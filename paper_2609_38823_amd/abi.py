@@ -24,7 +24,7 @@ STATUS = {0: "MOE_OK", -1: "MOE_EINVAL", -2: "MOE_EALIAS", -3: "MOE_EWORKSPACE",
 
 EXPORTS = ("moe_status_string", "moe_workspace_size", "moe_route", "moe_calibrate_prefix",
            "moe_dispatch", "moe_expert_ffn", "moe_expert_ffn_packed", "moe_pack_expert_weights",
-           "moe_combine", "drop_visual_block")
+           "moe_combine", "moe_combine_residual", "drop_visual_block", "moe_permute_experts")
 
 
 class MoeError(RuntimeError):
@@ -55,6 +55,8 @@ def load() -> ctypes.CDLL:
         "moe_expert_ffn_packed": (_I, [_P, _I, _P, _I, _P, _I, _I, _I, _I, _P, _P, _P, _P, _S, _P]),
         "moe_pack_expert_weights": (_I, [_P, _I, _I, _I, _I, _P, _P]),
         "moe_combine": (_I, [_P, _I, _P, _P, _I, _I, _I, _P, _P]),
+        "moe_combine_residual": (_I, [_P, _I, _P, _P, _I, _I, _I, _P, _P, _P]),
+        "moe_permute_experts": (_I, [_P, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
         "drop_visual_block": (_I, [_P, _I, _I, _I, _I, _I, _P, _P]),
     }
     for name, (res, args) in sig.items():
@@ -185,3 +187,31 @@ def drop_visual_block(h, v0, v1, out, stream=None):
     S, d = h.shape
     _check("drop_visual_block", load().drop_visual_block(
         _p(h), _dt(h), S, d, v0, v1, _p(out), _stream(stream)))
+
+
+def moe_combine_residual(y_perm, row_of_slot, topk_w, residual, out, stream=None):
+    """out = residual + combine(...); `out` may be `residual` (in place)."""
+    T, k = topk_w.shape
+    d = out.shape[1]
+    _check("moe_combine_residual", load().moe_combine_residual(
+        _p(y_perm), _dt(y_perm), _p(row_of_slot), _p(topk_w), T, k, d, _p(residual), _p(out),
+        _stream(stream)))
+
+
+def moe_permute_experts(order, w_r=None, bias=None, w_gate_up=None, w_down=None, w_r_out=None,
+                        bias_out=None, w_gate_up_out=None, w_down_out=None, d=None, m=None,
+                        stream=None):
+    """New expert j <- native expert order[j] (order: [E] int32 device
+    tensor) for each given input/output pair."""
+    E = order.numel()
+    if w_r is not None:
+        d = w_r.shape[0]
+    if w_gate_up is not None:
+        d, m = w_gate_up.shape[2], w_gate_up.shape[1] // 2
+    elif w_down is not None:
+        d, m = w_down.shape[1], w_down.shape[2]
+    ref = w_gate_up if w_gate_up is not None else w_down
+    dt = _dt(ref) if ref is not None else MOE_F32
+    _check("moe_permute_experts", load().moe_permute_experts(
+        _p(order), E, d or 1, m or 1, dt, _p(w_r), _p(bias), _p(w_gate_up), _p(w_down),
+        _p(w_r_out), _p(bias_out), _p(w_gate_up_out), _p(w_down_out), _stream(stream)))

@@ -234,7 +234,63 @@ int moe_combine(const void* y_perm, moe_dtype dtype, const int32_t* row_of_slot,
                 {rng(y_perm, A * d * es), rng(row_of_slot, A * 4), rng(topk_w, A * 4)}))
     return MOE_EALIAS;
   return hip_status(decomoe::launch_combine(y_perm, dtype == MOE_BF16, row_of_slot, topk_w, T, k,
-                                            d, out, stream));
+                                            d, nullptr, out, stream));
+}
+
+int moe_combine_residual(const void* y_perm, moe_dtype dtype, const int32_t* row_of_slot,
+                         const float* topk_w, int T, int k, int d, const void* residual,
+                         void* out, hipStream_t stream) {
+  if (!valid_dtype(dtype) || T < 0 || k < 1 || k > kMaxE || d < 1) return MOE_EINVAL;
+  if ((size_t)T * k > (size_t)INT32_MAX) return MOE_EUNSUPPORTED;
+  if (T == 0) return MOE_OK;
+  if (!y_perm || !row_of_slot || !topk_w || !residual || !out) return MOE_EINVAL;
+  if (!aligned_all({y_perm, row_of_slot, topk_w, residual, out})) return MOE_EINVAL;
+  const int es = elt_size(dtype);
+  const size_t A = (size_t)T * k;
+  const Range o = rng(out, (size_t)T * d * es), r = rng(residual, (size_t)T * d * es);
+  // out may be residual itself, but not a shifted view of it
+  if (r.lo != o.lo && overlap(o, r)) return MOE_EALIAS;
+  if (any_alias({o}, {rng(y_perm, A * d * es), rng(row_of_slot, A * 4), rng(topk_w, A * 4)}))
+    return MOE_EALIAS;
+  return hip_status(decomoe::launch_combine(y_perm, dtype == MOE_BF16, row_of_slot, topk_w, T, k,
+                                            d, residual, out, stream));
+}
+
+int moe_permute_experts(const int32_t* order, int E, int d, int m, moe_dtype dtype,
+                        const float* w_r, const float* bias, const void* w_gate_up,
+                        const void* w_down, float* w_r_out, float* bias_out,
+                        void* w_gate_up_out, void* w_down_out, hipStream_t stream) {
+  if (!valid_dtype(dtype) || E < 1 || E > kMaxE || d < 1 || m < 1 || !order) return MOE_EINVAL;
+  if (!w_r != !w_r_out || !bias != !bias_out || !w_gate_up != !w_gate_up_out ||
+      !w_down != !w_down_out)
+    return MOE_EINVAL;
+  const int es = elt_size(dtype);
+  const size_t b_gu = (size_t)2 * m * d * es, b_dn = (size_t)d * m * es;
+  if ((reinterpret_cast<uintptr_t>(order) | reinterpret_cast<uintptr_t>(w_r) |
+       reinterpret_cast<uintptr_t>(bias) | reinterpret_cast<uintptr_t>(w_r_out) |
+       reinterpret_cast<uintptr_t>(bias_out)) % 4)
+    return MOE_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(w_gate_up) | reinterpret_cast<uintptr_t>(w_down) |
+       reinterpret_cast<uintptr_t>(w_gate_up_out) | reinterpret_cast<uintptr_t>(w_down_out)) % es)
+    return MOE_EINVAL;
+  const Range o_r = w_r ? rng(w_r_out, (size_t)d * E * 4) : Range{0, 0};
+  const Range o_b = bias ? rng(bias_out, (size_t)E * 4) : Range{0, 0};
+  const Range o_gu = w_gate_up ? rng(w_gate_up_out, E * b_gu) : Range{0, 0};
+  const Range o_dn = w_down ? rng(w_down_out, E * b_dn) : Range{0, 0};
+  if (any_alias({o_r, o_b, o_gu, o_dn},
+                {rng(order, (size_t)E * 4), w_r ? rng(w_r, (size_t)d * E * 4) : Range{0, 0},
+                 bias ? rng(bias, (size_t)E * 4) : Range{0, 0},
+                 w_gate_up ? rng(w_gate_up, E * b_gu) : Range{0, 0},
+                 w_down ? rng(w_down, E * b_dn) : Range{0, 0}}))
+    return MOE_EALIAS;
+  hipError_t e = hipSuccess;
+  if (w_r) e = decomoe::launch_permute_columns(w_r, order, d, E, w_r_out, stream);
+  if (e == hipSuccess && bias) e = decomoe::launch_permute_columns(bias, order, 1, E, bias_out, stream);
+  if (e == hipSuccess && w_gate_up)
+    e = decomoe::launch_permute_blocks(w_gate_up, order, E, b_gu, w_gate_up_out, stream);
+  if (e == hipSuccess && w_down)
+    e = decomoe::launch_permute_blocks(w_down, order, E, b_dn, w_down_out, stream);
+  return hip_status(e);
 }
 
 int drop_visual_block(const void* h, moe_dtype dtype, int S, int d, int v0, int v1, void* out,

@@ -6,13 +6,17 @@ namespace decomoe {
 namespace {
 
 // out[t] = sum_j w[t, j] * y[row_of_slot[t*k + j]], float32 accumulation in
-// slot order.  Each thread owns one 16-byte vector of the row (8 bf16 or 4
-// f32); a block covers one token row, or several when rows are short.
-template <bool BF16>
+// slot order; with RES the residual row is added to the float32 sum before
+// the one rounding (res may be out itself: each thread reads its vector of
+// res before it writes the same vector of out).  Each thread owns one 16-byte
+// vector of the row (8 bf16 or 4 f32); a block covers one token row, or
+// several when rows are short.
+template <bool BF16, bool RES>
 __global__ __launch_bounds__(256) void combine_kernel(const uint4* __restrict__ y,
                                                       const int32_t* __restrict__ row_of_slot,
                                                       const float* __restrict__ w, int T, int k,
-                                                      int chunks, int rpb, uint4* __restrict__ out) {
+                                                      int chunks, int rpb, const uint4* res,
+                                                      uint4* out) {
   int t, c0, cstep;
   if (chunks >= 256) {
     t = blockIdx.x;
@@ -48,6 +52,22 @@ __global__ __launch_bounds__(256) void combine_kernel(const uint4* __restrict__ 
         acc[3] = fmaf(wj, __uint_as_float(v.w), acc[3]);
       }
     }
+    if constexpr (RES) {
+      const uint4 v = res[(size_t)t * chunks + c];
+      if constexpr (BF16) {
+        const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          acc[2 * q] += __uint_as_float(u[q] << 16);
+          acc[2 * q + 1] += __uint_as_float(u[q] & 0xffff0000u);
+        }
+      } else {
+        acc[0] += __uint_as_float(v.x);
+        acc[1] += __uint_as_float(v.y);
+        acc[2] += __uint_as_float(v.z);
+        acc[3] += __uint_as_float(v.w);
+      }
+    }
     uint4 o;
     if constexpr (BF16) {
       o = make_uint4(pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]),
@@ -61,11 +81,12 @@ __global__ __launch_bounds__(256) void combine_kernel(const uint4* __restrict__ 
 }
 
 // element-wise fallback when rows are not whole 16-byte vectors
-template <bool BF16>
+template <bool BF16, bool RES>
 __global__ __launch_bounds__(256) void combine_scalar_kernel(const void* __restrict__ yv,
                                                              const int32_t* __restrict__ row_of_slot,
                                                              const float* __restrict__ w, int T,
-                                                             int k, int d, void* __restrict__ outv) {
+                                                             int k, int d, const void* resv,
+                                                             void* outv) {
   const size_t n = (size_t)T * d;
   const int A = T * k;
   for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) {
@@ -78,6 +99,8 @@ __global__ __launch_bounds__(256) void combine_scalar_kernel(const void* __restr
                        : static_cast<const float*>(yv)[(size_t)r * d + c];
       acc = fmaf(w[(size_t)t * k + j], yv_, acc);
     }
+    if constexpr (RES)
+      acc += BF16 ? bf16_to_f32(static_cast<const uint16_t*>(resv)[i]) : static_cast<const float*>(resv)[i];
     if (BF16)
       static_cast<uint16_t*>(outv)[i] = f32_to_bf16(acc);
     else
@@ -110,28 +133,43 @@ hipError_t drop_rows_launch(const void* h, int rows_out, int chunks, int v0, int
 }
 }  // namespace
 
-hipError_t launch_combine(const void* y_perm, bool bf16, const int32_t* row_of_slot,
-                          const float* w, int T, int k, int d, void* out, hipStream_t s) {
+namespace {
+template <bool RES>
+hipError_t combine_launch(const void* y_perm, bool bf16, const int32_t* row_of_slot,
+                          const float* w, int T, int k, int d, const void* res, void* out,
+                          hipStream_t s) {
   const size_t row_bytes = (size_t)d * (bf16 ? 2 : 4);
   if (row_bytes % 16 == 0) {
     const int chunks = (int)(row_bytes / 16);
     const int rpb = chunks >= 256 ? 1 : 256 / chunks;
     const int grid = (T + rpb - 1) / rpb;
+    auto y = static_cast<const uint4*>(y_perm);
+    auto r = static_cast<const uint4*>(res);
+    auto o = static_cast<uint4*>(out);
     if (bf16)
-      combine_kernel<true><<<grid, 256, 0, s>>>(static_cast<const uint4*>(y_perm), row_of_slot, w,
-                                                T, k, chunks, rpb, static_cast<uint4*>(out));
+      combine_kernel<true, RES><<<grid, 256, 0, s>>>(y, row_of_slot, w, T, k, chunks, rpb, r, o);
     else
-      combine_kernel<false><<<grid, 256, 0, s>>>(static_cast<const uint4*>(y_perm), row_of_slot, w,
-                                                 T, k, chunks, rpb, static_cast<uint4*>(out));
+      combine_kernel<false, RES><<<grid, 256, 0, s>>>(y, row_of_slot, w, T, k, chunks, rpb, r, o);
   } else {
     size_t blocks = ((size_t)T * d + 255) / 256;
     if (blocks > 65536) blocks = 65536;
     if (bf16)
-      combine_scalar_kernel<true><<<(unsigned)blocks, 256, 0, s>>>(y_perm, row_of_slot, w, T, k, d, out);
+      combine_scalar_kernel<true, RES><<<(unsigned)blocks, 256, 0, s>>>(y_perm, row_of_slot, w, T,
+                                                                        k, d, res, out);
     else
-      combine_scalar_kernel<false><<<(unsigned)blocks, 256, 0, s>>>(y_perm, row_of_slot, w, T, k, d, out);
+      combine_scalar_kernel<false, RES><<<(unsigned)blocks, 256, 0, s>>>(y_perm, row_of_slot, w,
+                                                                         T, k, d, res, out);
   }
   return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_combine(const void* y_perm, bool bf16, const int32_t* row_of_slot,
+                          const float* w, int T, int k, int d, const void* residual, void* out,
+                          hipStream_t s) {
+  if (residual)
+    return combine_launch<true>(y_perm, bf16, row_of_slot, w, T, k, d, residual, out, s);
+  return combine_launch<false>(y_perm, bf16, row_of_slot, w, T, k, d, nullptr, out, s);
 }
 
 hipError_t launch_drop_rows(const void* h, int elt, int S, int d, int v0, int v1, void* out,

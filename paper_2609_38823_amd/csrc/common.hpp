@@ -57,7 +57,15 @@ hipError_t launch_expert_ffn(const void* x_perm, bool bf16, const int32_t* offse
                              void* ws, hipStream_t s);
 hipError_t launch_pack_weights(const void* w, int E, int R, int K, void* out, hipStream_t s);
 hipError_t launch_combine(const void* y_perm, bool bf16, const int32_t* row_of_slot,
-                          const float* w, int T, int k, int d, void* out, hipStream_t s);
+                          const float* w, int T, int k, int d, const void* residual, void* out,
+                          hipStream_t s);
+// out block j = in block order[j] for E blocks of `block_bytes` (zeros when
+// order[j] lies outside [0, E))
+hipError_t launch_permute_blocks(const void* in, const int32_t* order, int E, size_t block_bytes,
+                                 void* out, hipStream_t s);
+// out[r, j] = in[r, order[j]] for a [rows, E] float32 matrix (0 when out of range)
+hipError_t launch_permute_columns(const float* in, const int32_t* order, int rows, int E,
+                                  float* out, hipStream_t s);
 hipError_t launch_drop_rows(const void* h, int elt, int S, int d, int v0, int v1, void* out,
                             hipStream_t s);
 

@@ -75,6 +75,9 @@ WORKLOADS = {
     # 48-layer stack over 7680 visual + 512 text rows, exit at layer 20
     "qwen3vl_stack48_8192": Workload("qwen3vl_stack48_8192", QWEN3_VL_MOE, T=8192, n_visual=7680,
                                      p=0.9, layers=48, exit_layer=20),
+    # tiny fp32 stack: 6 layers over 384 visual + 128 text rows, exit at layer 3
+    "tiny_stack_f32": Workload("tiny_stack_f32", TINY, T=512, n_visual=384, p=0.9, layers=6,
+                               exit_layer=3),
     # decode: 64 single text tokens through 48 layers
     "qwen3vl_decode64": Workload("qwen3vl_decode64", QWEN3_VL_MOE, T=64, n_visual=0, p=0.85,
                                  layers=48),
@@ -148,6 +151,32 @@ def layer_params(shape: LayerShape, seed: int = 0, layer: int = 0) -> dict:
     with ThreadPoolExecutor(max_workers=workers) as ex:
         list(ex.map(fill, range(E)))
     return dict(w_r=w_r, bias=bias, w_gate_up=w_gate_up, w_down=w_down)
+
+
+def device_expert_weights(shape: LayerShape, seed: int = 0, layer: int = 0, device="cuda"):
+    """Expert weights of one layer of a deep stack, drawn on the device.
+
+    A 48-layer stack holds 48 * E * 3 * d * m values (29 G at the
+    Qwen3-VL-MoE shape), too many to draw on the host in the time of a test,
+    so stacks draw them with torch's device generator: N(0, w_std^2) in
+    float32 from a generator seeded per (seed, layer, tensor), then rounded
+    to the storage precision (round to nearest even for bf16).  Returns
+    (w_gate_up [E, 2m, d], w_down [E, d, m]) torch tensors in native expert
+    order.  Checks on the CPU copy the same tensors to the host.
+    """
+    import torch
+
+    dt = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
+    out = []
+    for tensor, shp in ((_P_GU, (shape.E, 2 * shape.m, shape.d)), (_P_DOWN, (shape.E, shape.d, shape.m))):
+        g = torch.Generator(device=device)
+        g.manual_seed(int(np.random.SeedSequence(seed, spawn_key=(_S_PARAMS, layer, tensor, 7))
+                          .generate_state(1, np.uint64)[0] >> np.uint64(1)))
+        w = torch.randn(shp, generator=g, device=device, dtype=torch.float32)
+        w.mul_(shape.w_std)
+        out.append(w.to(dt) if dt != torch.float32 else w)
+        del w
+    return tuple(out)
 
 
 def router_params(shape: LayerShape, seed: int = 0, layer: int = 0) -> dict:

@@ -98,19 +98,44 @@ class MoELayer:
     """One MoE layer's parameters on the device, in reordered expert order."""
 
     def __init__(self, params: dict, k: int, dtype: str, device="cuda"):
+        dt = _TORCH_DT[dtype]
+        self._setup(to_device(params["w_r"], torch.float32, device),
+                    to_device(params["bias"], torch.float32, device),
+                    to_device(params["w_gate_up"], dt, device), to_device(params["w_down"], dt, device),
+                    k, dtype, device)
+
+    @classmethod
+    def from_native(cls, w_r: np.ndarray, bias, w_gate_up: torch.Tensor, w_down: torch.Tensor,
+                    order, k: int, dtype: str, device="cuda") -> "MoELayer":
+        """Load a layer whose expert weights are already on the device in
+        native order: the Mean-Mass order (Eq. 9) is applied on the device
+        (moe_permute_experts) and the weights are then packed.  The native
+        weight tensors are consumed (reused as the packed storage)."""
+        self = cls.__new__(cls)
+        o = torch.as_tensor(np.asarray(order), dtype=torch.int32).to(device)
+        w_r_n = to_device(w_r, torch.float32, device)
+        b_n = to_device(bias, torch.float32, device)
+        w_r_p = torch.empty_like(w_r_n)
+        b_p = torch.empty_like(b_n) if b_n is not None else None
+        gu = torch.empty_like(w_gate_up)
+        dn = torch.empty_like(w_down)
+        abi.moe_permute_experts(o, w_r_n, b_n, w_gate_up, w_down, w_r_p, b_p, gu, dn)
+        self._setup(w_r_p, b_p, gu, dn, k, dtype, device, spare=(w_gate_up, w_down))
+        return self
+
+    def _setup(self, w_r, bias, w_gate_up, w_down, k, dtype, device, spare=None):
         self.dt = _TORCH_DT[dtype]
         self.k = k
-        self.d, self.E = params["w_r"].shape
-        self.m = params["w_down"].shape[2]
-        self.w_r = to_device(params["w_r"], torch.float32, device)
-        self.bias = to_device(params["bias"], torch.float32, device)
-        self.w_gate_up = to_device(params["w_gate_up"], self.dt, device)
-        self.w_down = to_device(params["w_down"], self.dt, device)
+        self.d, self.E = w_r.shape
+        self.m = w_down.shape[2]
+        self.w_r, self.bias = w_r, bias
+        self.w_gate_up, self.w_down = w_gate_up, w_down
         # bf16 layers keep the expert weights in the packed fragment layout
         # (moe_pack_expert_weights), re-laid out once here like the reorder
         self.packed = self.dt == torch.bfloat16 and self.m % 256 == 0 and self.d % 256 == 0
         if self.packed:
-            wgu, wd = torch.empty_like(self.w_gate_up), torch.empty_like(self.w_down)
+            wgu, wd = spare if spare is not None else (torch.empty_like(w_gate_up),
+                                                       torch.empty_like(w_down))
             abi.moe_pack_expert_weights(self.w_gate_up, wgu)
             abi.moe_pack_expert_weights(self.w_down, wd)
             self.w_gate_up, self.w_down = wgu, wd
@@ -124,8 +149,11 @@ class MoELayer:
         return self._bufs[key]
 
     # -- stages ------------------------------------------------------------
-    # `mark`, if given, is called after each ABI call (e.g. to record events)
-    def _experts(self, x, b: Buffers, idx, w, K_dev=None, stream=None, mark=None):
+    # `mark`, if given, is called after each ABI call (e.g. to record events).
+    # With `residual`, the combine writes out = residual + MoE(x) into `out`
+    # (default b.out); `out` may be `residual` itself (in-place hidden state).
+    def _experts(self, x, b: Buffers, idx, w, K_dev=None, stream=None, mark=None, residual=None,
+                 out=None):
         mark = mark or (lambda: None)
         abi.moe_dispatch(idx, self.E, x, b.counts, b.offsets, b.src_of_row, b.row_of_slot,
                          b.x_perm, b.ws, stream=stream)
@@ -133,33 +161,40 @@ class MoELayer:
         ffn = abi.moe_expert_ffn_packed if self.packed else abi.moe_expert_ffn
         ffn(b.x_perm, b.offsets, self.w_gate_up, self.w_down, b.y_perm, b.ws, K_dev=K_dev, stream=stream)
         mark()
-        abi.moe_combine(b.y_perm, b.row_of_slot, w, b.out, stream=stream)
+        out = b.out if out is None else out
+        if residual is None:
+            abi.moe_combine(b.y_perm, b.row_of_slot, w, out, stream=stream)
+        else:
+            abi.moe_combine_residual(b.y_perm, b.row_of_slot, w, residual, out, stream=stream)
         mark()
 
     def forward_dense(self, x: torch.Tensor, b: Buffers | None = None, stream=None,
-                      mark=None) -> Buffers:
+                      mark=None, residual=None, out=None) -> Buffers:
         """Full expert pool (layers before the visual exit)."""
         b = b or self.buffers(x.shape[0])
         abi.moe_route(x, self.w_r, self.bias, self.k, b.logits, b.idx, b.w, ws=b.ws, stream=stream)
         if mark:
             mark()
-        self._experts(x, b, b.idx, b.w, stream=stream, mark=mark)
+        self._experts(x, b, b.idx, b.w, stream=stream, mark=mark, residual=residual, out=out)
         return b
 
     def forward_rcep(self, x: torch.Tensor, p: float, seg_offsets=None, b: Buffers | None = None,
-                     stream=None, mark=None) -> Buffers:
-        """Prefix-restricted layer (from the visual exit on, Algorithm 2)."""
+                     stream=None, mark=None, residual=None, out=None, K_out=None) -> Buffers:
+        """Prefix-restricted layer (from the visual exit on, Algorithm 2).
+        K_out ([n_seg] int32, default b.K) receives the prefix lengths."""
         n_seg = 1 if seg_offsets is None else seg_offsets.numel() - 1
         b = b or self.buffers(x.shape[0], n_seg)
+        K = b.K if K_out is None else K_out
         mk = mark or (lambda: None)
         abi.moe_route(x, self.w_r, self.bias, self.k, b.logits, b.idx_full, b.w_full, ws=b.ws,
                       stream=stream)
         mk()
-        abi.moe_calibrate_prefix(b.idx_full, b.w_full, self.E, p, b.mass, b.ws, K_out=b.K,
+        abi.moe_calibrate_prefix(b.idx_full, b.w_full, self.E, p, b.mass, b.ws, K_out=K,
                                  seg_offsets=seg_offsets, stream=stream)
         mk()
         abi.moe_route(None, None, None, self.k, b.logits, b.idx, b.w, seg_offsets=seg_offsets,
-                      K_dev=b.K, stream=stream)
+                      K_dev=K, stream=stream)
         mk()
-        self._experts(x, b, b.idx, b.w, K_dev=b.K, stream=stream, mark=mark)
+        self._experts(x, b, b.idx, b.w, K_dev=K, stream=stream, mark=mark, residual=residual,
+                      out=out)
         return b

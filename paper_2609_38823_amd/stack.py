@@ -1,0 +1,131 @@
+"""A stack of MoE blocks on the device: the per-layer loop of Algorithm 2.
+
+Prefill (the 48-layer stack over 7680 visual + 512 text rows):
+
+    layers [0, exit)   dense span over all rows      h <- h + MoE_l(h)
+    entrance of exit   drop_visual_block             h <- h[text rows]
+    layers [exit, L)   RCEP span over the text rows  h <- h + MoE_l(h)
+
+Decode (64 single text tokens): the RCEP span in every layer, captured once
+as a HIP graph and replayed per step.
+
+The residual connection is folded into each layer's combine
+(moe_combine_residual), so a layer is route -> [calibrate -> re-route] ->
+dispatch -> expert FFN -> combine+residual, all in libdecomoe.so, with K
+kept on the device per layer (``K_trace``).  The blocks' attention
+sublayers are not part of this stack.
+
+Calibration (Eqs. 8, 9): 512 calibration rows enter layer 0 and are carried
+through the stack with the full expert pool (dense span), so each layer's
+Mean-Mass order comes from the full-pool routing of the calibration rows'
+own hidden states at that layer (one calibration case).  The order is
+applied on the device (moe_permute_experts) before the weights are packed.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import abi, inputs as I
+from .layer import Buffers, MoELayer, calibrate_order_router, to_device
+
+
+class MoEStack:
+    """Device-resident stack of ``n_layers`` MoE layers of one workload's shape."""
+
+    def __init__(self, wl: I.Workload, n_layers: int | None = None, calib_rows: int = 512,
+                 device="cuda", progress=None):
+        sh = wl.shape
+        self.wl, self.sh = wl, sh
+        self.L = n_layers or wl.layers
+        self.device = device
+        self.dt = torch.bfloat16 if sh.dtype == "bf16" else torch.float32
+        self.layers: list[MoELayer] = []
+        self.orders: list[np.ndarray] = []
+        self._bufs: dict = {}
+        self._h: dict = {}
+        # calib_h[l]: the calibration rows entering layer l
+        self.calib_h: list[torch.Tensor] = []
+        calib = to_device(I.tokens(sh, calib_rows, seed=wl.seed, stream="calib"), self.dt, device)
+        for l in range(self.L):
+            rp = I.router_params(sh, wl.seed, l)
+            self.calib_h.append(calib)
+            order = calibrate_order_router(calib, rp["w_r"], rp["bias"], sh.k)
+            gu, dn = I.device_expert_weights(sh, wl.seed, l, device)
+            layer = MoELayer.from_native(rp["w_r"], rp["bias"], gu, dn, order, sh.k, sh.dtype, device)
+            self.layers.append(layer)
+            self.orders.append(order)
+            del gu, dn
+            nxt = torch.empty_like(calib)
+            layer.forward_dense(calib, b=self.buffers(calib_rows), residual=calib, out=nxt)
+            calib = nxt
+            if progress:
+                progress(l)
+        # row l, column 0: K of layer l when it runs the RCEP span (rows are
+        # 16 bytes so that every row is an aligned ABI array)
+        self.K_trace = torch.zeros((self.L, 4), dtype=torch.int32, device=device)
+
+    def buffers(self, T: int) -> Buffers:
+        """Work buffers for T rows, shared by all layers (one stream)."""
+        if T not in self._bufs:
+            sh = self.sh
+            self._bufs[T] = Buffers(T, sh.d, sh.E, sh.m, sh.k, self.dt, 1, self.device)
+        return self._bufs[T]
+
+    def hidden(self, T: int, tag: str = "h") -> torch.Tensor:
+        key = (T, tag)
+        if key not in self._h:
+            self._h[key] = torch.empty((T, self.sh.d), dtype=self.dt, device=self.device)
+        return self._h[key]
+
+    def layer_forward(self, l: int, src: torch.Tensor, dst: torch.Tensor, rcep: bool, p: float,
+                      stream=None, mark=None) -> Buffers:
+        """One block: dst = src + MoE_l(src); dst may be src (in place)."""
+        b = self.buffers(src.shape[0])
+        layer = self.layers[l]
+        if rcep:
+            return layer.forward_rcep(src, p, b=b, stream=stream, mark=mark, residual=src, out=dst,
+                                      K_out=self.K_trace[l, :1])
+        return layer.forward_dense(src, b=b, stream=stream, mark=mark, residual=src, out=dst)
+
+    def forward(self, x: torch.Tensor, n_visual: int, p: float, exit_layer: int | None,
+                stream=None, hook=None) -> torch.Tensor:
+        """Run the stack over x [T, d] (visual rows [0, n_visual) first).
+
+        exit_layer is the first text-only layer: the visual rows are removed
+        at its entrance and it and every later layer run the RCEP span;
+        None runs every layer dense.  x itself is not modified.  Returns the
+        final hidden rows (a buffer owned by the stack).  ``hook(l, src)``,
+        if given, is called before layer l with its input rows.
+        """
+        T = x.shape[0]
+        src = x
+        h = self.hidden(T)
+        for l in range(self.L):
+            if exit_layer is not None and l == exit_layer and n_visual > 0:
+                ht = self.hidden(T - n_visual, "text")
+                abi.drop_visual_block(src, 0, n_visual, ht, stream=stream)
+                src, h = ht, ht
+            if hook:
+                hook(l, src)
+            rcep = exit_layer is not None and l >= exit_layer
+            dst = h if src is x else src
+            self.layer_forward(l, src, dst, rcep, p, stream=stream)
+            src = dst
+        return src
+
+    def capture_decode(self, x: torch.Tensor, p: float):
+        """Capture one decode step (RCEP in every layer) over the static
+        input rows x as a HIP graph.  Returns (graph, out): replaying the
+        graph reads x and leaves the final hidden rows in out."""
+        side = torch.cuda.Stream(device=self.device)
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            self.forward(x, 0, p, exit_layer=0)  # buffers exist before capture
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            out = self.forward(x, 0, p, exit_layer=0)
+        return g, out

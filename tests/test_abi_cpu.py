@@ -29,9 +29,9 @@ def lib():
 
 def test_header_declares_the_boundary():
     assert declared_functions() == sorted([
-        "drop_visual_block", "moe_calibrate_prefix", "moe_combine", "moe_dispatch",
-        "moe_expert_ffn", "moe_expert_ffn_packed", "moe_pack_expert_weights", "moe_route",
-        "moe_status_string", "moe_workspace_size"])
+        "drop_visual_block", "moe_calibrate_prefix", "moe_combine", "moe_combine_residual",
+        "moe_dispatch", "moe_expert_ffn", "moe_expert_ffn_packed", "moe_pack_expert_weights",
+        "moe_permute_experts", "moe_route", "moe_status_string", "moe_workspace_size"])
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -157,6 +157,37 @@ def test_combine_and_drop_reject(lib):
     assert lib.drop_visual_block(P1, BF16, 10, 64, 0, 11, P2, NULL) == EINVAL
     assert lib.drop_visual_block(P1, BF16, 10, 64, 0, 4, P1, NULL) == EALIAS
     assert lib.drop_visual_block(P1, BF16, 10, 64, 0, 10, P2, NULL) == 0  # nothing left to copy
+
+
+def test_combine_residual_rejects(lib):
+    # residual shifted by one row inside out: neither in place nor disjoint
+    assert lib.moe_combine_residual(P1, BF16, P2, P3, 8, 2, 64, ctypes.c_void_p(P4.value + 128), P4, NULL) == EALIAS
+    assert lib.moe_combine_residual(P1, BF16, P2, P3, 8, 2, 64, P4, P1, NULL) == EALIAS
+    assert lib.moe_combine_residual(P1, BF16, P2, P3, 8, 2, 64, None, P4, NULL) == EINVAL
+    assert lib.moe_combine_residual(P1, BF16, P2, P3, 8, 0, 64, P4, P4, NULL) == EINVAL
+    assert lib.moe_combine_residual(P1, BF16, P2, P3, 0, 2, 64, P4, P4, NULL) == 0  # T = 0
+
+
+def test_permute_experts_rejects(lib):
+    nul = None
+    # a pair with only one side given
+    assert lib.moe_permute_experts(P1, 4, 64, 32, BF16, P2, nul, nul, nul, nul, nul, nul, nul,
+                                   NULL) == EINVAL
+    # output overlapping its input
+    assert lib.moe_permute_experts(P1, 4, 64, 32, BF16, nul, nul, P2, nul, nul, nul, P2, nul,
+                                   NULL) == EALIAS
+    # output overlapping the order array
+    assert lib.moe_permute_experts(P1, 4, 64, 32, BF16, nul, nul, P2, nul, nul, nul, P1, nul,
+                                   NULL) == EALIAS
+    assert lib.moe_permute_experts(nul, 4, 64, 32, BF16, nul, nul, P2, nul, nul, nul, P3, nul,
+                                   NULL) == EINVAL
+    assert lib.moe_permute_experts(P1, 0, 64, 32, BF16, nul, nul, P2, nul, nul, nul, P3, nul,
+                                   NULL) == EINVAL
+    assert lib.moe_permute_experts(P1, 2000, 64, 32, BF16, nul, nul, P2, nul, nul, nul, P3, nul,
+                                   NULL) == EINVAL
+    # misaligned bf16 weights
+    assert lib.moe_permute_experts(P1, 4, 64, 32, BF16, nul, nul, ctypes.c_void_p(P2.value + 1), nul, nul, nul, P3, nul,
+                                   NULL) == EINVAL
 
 
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):
