@@ -6,6 +6,7 @@ visual exit (Algorithm 2 of the paper), on synthetic inputs already
 resident in HBM:
 
   dense span   moe_route -> moe_dispatch -> moe_expert_ffn -> moe_combine
+               (bf16: moe_route_packed, moe_expert_ffn_packed)
                over 4096 rows (3584 visual + 512 text), all 128 experts
   SAVB exit    drop_visual_block removes the 3584 visual rows
   RCEP span    moe_route (full pool) -> moe_calibrate_prefix (K, p = 0.9)
@@ -568,6 +569,8 @@ def bench_stress(args) -> int:
     T = 65536
     rp = I.router_params(sh, wl.seed)
     w_r, bias = to_device(rp["w_r"], torch.float32), to_device(rp["bias"], torch.float32)
+    w_rp = torch.empty((3 * d * E,), dtype=torch.bfloat16, device="cuda")
+    abi.moe_pack_router(w_r, w_rp)
     x = to_device(I.tokens(sh, T, seed=1), torch.bfloat16)
     b = Buffers(T, d, E, m, k, torch.bfloat16)
     stream = torch.cuda.current_stream()
@@ -581,7 +584,7 @@ def bench_stress(args) -> int:
                 next(it).record(stream)
 
         mark()
-        abi.moe_route(x, w_r, bias, k, b.logits, b.idx, b.w, ws=b.ws)
+        abi.moe_route_packed(x, w_rp, bias, k, b.logits, b.idx, b.w, ws=b.ws)
         mark()
         abi.moe_dispatch(b.idx, E, x, b.counts, b.offsets, b.src_of_row, b.row_of_slot, b.x_perm, b.ws)
         mark()
@@ -610,7 +613,7 @@ def bench_stress(args) -> int:
         "Routing + dispatch + combine rows/s at 65536 rows (bandwidth shape of the MoE layer)",
         T / (ms * 1e-3), "rows/s", args, ms,
         {"workload": "Qwen3-VL-MoE MoE layer shape (d 2048, 128 experts, top-8, bf16, fp32 router) at "
-                     "65536 rows: moe_route (full pool), moe_dispatch, moe_combine (no expert FFN)",
+                     "65536 rows: moe_route_packed (full pool), moe_dispatch, moe_combine (no expert FFN)",
          "seed": 1}, roof, None, stages=rep)
 
 

@@ -5,6 +5,8 @@
  * in the paper's notation (Sec. 3.1 and Sec. 3.3; Algorithm 2):
  *
  *   logits  a = x W_r + b over all E (reordered) experts        moe_route
+ *     (bf16 x: split router weights on bf16 MFMA)                 moe_route_packed,
+ *                                                                 moe_pack_router
  *   full-pool Top-k R_i and renormalised weights (Eq. 10)         moe_route
  *   activated mass s (Eq. 11), prefix length K (Eq. 12),
  *   Mean-Mass calibration order pi (Eqs. 8, 9)                    moe_calibrate_prefix
@@ -110,6 +112,40 @@ int moe_route(const void* x, moe_dtype dtype, const float* w_r, const float* bia
               const int32_t* seg_offsets, int n_seg, const int32_t* K_dev,
               float* logits, int32_t* topk_idx, float* topk_w,
               void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * moe_pack_router - one-time split of the float32 router weights into three
+ * bf16 terms for moe_route_packed, done when a layer is loaded (like the
+ * reorder of Algorithm 1 it is a property of the stored parameters).
+ *
+ *   w_r         [d, E] float32 router weights.
+ *   w_r_packed  d * E * 3 bf16 (6 d E bytes), caller-owned, must not
+ *               overlap w_r.  With W1 = bf16(W), W2 = bf16(W - W1),
+ *               W3 = bf16(W - W1 - W2) (round to nearest even), the 1 KB
+ *               block ((eb * (d / 16) + kb) * 3 + p) holds term p + 1 for
+ *               experts 32 eb .. + 32 and k-values 16 kb .. + 16: element
+ *               8 l + j is expert 32 eb + l % 32, k = 16 kb + 8 (l / 32) + j.
+ * Needs E % 32 == 0 and d % 64 == 0 (else MOE_EUNSUPPORTED).  No workspace.
+ */
+int moe_pack_router(const float* w_r, int d, int E, void* w_r_packed, hipStream_t stream);
+
+/*
+ * moe_route_packed - moe_route for bf16 token rows with the router weights
+ * given as moe_pack_router's three-term split: the logits are
+ * x W1 + x W2 + x W3 on bf16 MFMA with float32 accumulation.  Each product
+ * is exact in float32 and W1 + W2 + W3 equals W to within 2^-24 |W|, so the
+ * float32 logits of Eq. 1 are reproduced to within a small multiple of
+ * float32 rounding: |a - a_exact| <= (gamma_{3d} + 2^-23) sum_j |x_j W_je|.
+ * The Top-k, the weights and every other argument are those of moe_route.
+ * x must be non-NULL and bf16 (float32 x: MOE_EUNSUPPORTED; a prefix
+ * re-route with x == NULL goes through moe_route).  Needs E % 32 == 0 and
+ * d % 64 == 0 (else MOE_EUNSUPPORTED).  ws as for moe_route (its split
+ * partials, moe_workspace_size covers both).
+ */
+int moe_route_packed(const void* x, moe_dtype dtype, const void* w_r_packed, const float* bias,
+                     int T, int d, int E, int k, const int32_t* seg_offsets, int n_seg,
+                     const int32_t* K_dev, float* logits, int32_t* topk_idx, float* topk_w,
+                     void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * moe_calibrate_prefix - activated mass, prefix length and Mean-Mass order

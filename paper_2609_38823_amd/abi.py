@@ -22,7 +22,8 @@ MOE_F32, MOE_BF16 = 0, 1
 STATUS = {0: "MOE_OK", -1: "MOE_EINVAL", -2: "MOE_EALIAS", -3: "MOE_EWORKSPACE",
           -4: "MOE_EHIP", -5: "MOE_EUNSUPPORTED"}
 
-EXPORTS = ("moe_status_string", "moe_workspace_size", "moe_route", "moe_calibrate_prefix",
+EXPORTS = ("moe_status_string", "moe_workspace_size", "moe_route", "moe_route_packed",
+           "moe_pack_router", "moe_calibrate_prefix",
            "moe_dispatch", "moe_expert_ffn", "moe_expert_ffn_packed", "moe_pack_expert_weights",
            "moe_combine", "moe_combine_residual", "drop_visual_block", "moe_permute_experts")
 
@@ -49,6 +50,8 @@ def load() -> ctypes.CDLL:
         "moe_status_string": (ctypes.c_char_p, [_I]),
         "moe_workspace_size": (_S, [_I, _I, _I, _I, _I, _I]),
         "moe_route": (_I, [_P, _I, _P, _P, _I, _I, _I, _I, _P, _I, _P, _P, _P, _P, _P, _S, _P]),
+        "moe_route_packed": (_I, [_P, _I, _P, _P, _I, _I, _I, _I, _P, _I, _P, _P, _P, _P, _P, _S, _P]),
+        "moe_pack_router": (_I, [_P, _I, _I, _P, _P]),
         "moe_calibrate_prefix": (_I, [_P, _P, _I, _I, _I, _P, _I, _D, _P, _P, _P, _P, _S, _P]),
         "moe_dispatch": (_I, [_P, _I, _I, _I, _P, _I, _I, _P, _P, _P, _P, _P, _P, _S, _P]),
         "moe_expert_ffn": (_I, [_P, _I, _P, _I, _P, _I, _I, _I, _I, _P, _P, _P, _P, _S, _P]),
@@ -124,6 +127,24 @@ def moe_route(x, w_r, bias, k, logits, topk_idx, topk_w, seg_offsets=None, K_dev
         _p(x), dt, _p(w_r) if x is not None else None, _p(bias) if x is not None else None,
         T, d, E, k, _p(seg_offsets), _nseg(seg_offsets), _p(K_dev),
         _p(logits), _p(topk_idx), _p(topk_w), _p(ws), _nbytes(ws), _stream(stream)))
+
+
+def moe_route_packed(x, w_r_packed, bias, k, logits, topk_idx, topk_w, seg_offsets=None, K_dev=None,
+                     ws=None, stream=None):
+    """x [T, d] bf16; w_r_packed from moe_pack_router (d * E * 3 bf16)."""
+    T, E = logits.shape
+    d = x.shape[1]
+    _check("moe_route_packed", load().moe_route_packed(
+        _p(x), _dt(x), _p(w_r_packed), _p(bias), T, d, E, k, _p(seg_offsets), _nseg(seg_offsets),
+        _p(K_dev), _p(logits), _p(topk_idx), _p(topk_w), _p(ws), _nbytes(ws), _stream(stream)))
+
+
+def moe_pack_router(w_r, w_r_packed, stream=None):
+    """w_r [d, E] float32 -> w_r_packed (3 d E bf16, any shape)."""
+    d, E = w_r.shape
+    if w_r_packed.numel() * w_r_packed.element_size() != 6 * d * E:
+        raise ValueError("w_r_packed must hold 3 * d * E bf16 values")
+    _check("moe_pack_router", load().moe_pack_router(_p(w_r), d, E, _p(w_r_packed), _stream(stream)))
 
 
 def moe_calibrate_prefix(topk_idx, topk_w, E, p, mass, ws, K_out=None, order=None,

@@ -45,6 +45,8 @@ int elt_size(moe_dtype dt) { return dt == MOE_BF16 ? 2 : 4; }
 bool valid_dtype(moe_dtype dt) { return dt == MOE_F32 || dt == MOE_BF16; }
 int hip_status(hipError_t e) { return e == hipSuccess ? MOE_OK : MOE_EHIP; }
 size_t a256(size_t b) { return (b + 255) & ~size_t(255); }
+// shapes of the three-term bf16 router (32-expert blocks, 64-wide k stages)
+bool router_packable(int d, int E) { return E % 32 == 0 && d % 64 == 0; }
 
 // validation shared by the row-major and packed expert FFN entry points
 int expert_ffn(const void* x_perm, moe_dtype dtype, const int32_t* offsets, int E,
@@ -98,33 +100,38 @@ size_t moe_workspace_size(int T, int E, int k, int d, int m, int n_seg) {
   size_t w = 256;
   for (size_t b : {a256(dispatch_ws_bytes(T, k, E)), ffn_ws_bytes(true, (int)rows, E, d, m),
                    ffn_ws_bytes(false, (int)rows, E, d, m), a256(route_ws_bytes(T, d, E)),
+                   a256(router_packable(d, E) ? decomoe::route_x3_ws_bytes(T, d, E) : 0),
                    a256(calibrate_ws_bytes(T, E))})
     w = b > w ? b : w;
   return w;
 }
 
-int moe_route(const void* x, moe_dtype dtype, const float* w_r, const float* bias, int T, int d,
-              int E, int k, const int32_t* seg_offsets, int n_seg, const int32_t* K_dev,
-              float* logits, int32_t* topk_idx, float* topk_w, void* ws, size_t ws_bytes,
-              hipStream_t stream) {
+namespace {
+// shared by moe_route (float32 router weights) and moe_route_packed
+// (three-term bf16 split of them, from moe_pack_router)
+int route(const void* x, moe_dtype dtype, const float* w_r, const void* w_r_packed,
+          const float* bias, int T, int d, int E, int k, const int32_t* seg_offsets, int n_seg,
+          const int32_t* K_dev, float* logits, int32_t* topk_idx, float* topk_w, void* ws,
+          size_t ws_bytes, hipStream_t stream) {
   if (T < 0 || E < 1 || E > kMaxE || k < 1 || k > E) return MOE_EINVAL;
   if (k > kMaxK) return MOE_EUNSUPPORTED;
   if (!seg_offsets) n_seg = 1;
   if (n_seg < 1) return MOE_EINVAL;
   if (!logits) return MOE_EINVAL;
   if (x) {
-    if (!valid_dtype(dtype) || d < 1 || !w_r) return MOE_EINVAL;
+    if (!valid_dtype(dtype) || d < 1 || (!w_r && !w_r_packed)) return MOE_EINVAL;
     if (dtype == MOE_BF16 && d % 8 != 0) return MOE_EINVAL;
   }
   if (T == 0) return MOE_OK;
   if (!topk_idx || !topk_w) return MOE_EINVAL;
-  if (!aligned_all({x, w_r, bias, seg_offsets, K_dev, logits, topk_idx, topk_w, ws})) return MOE_EINVAL;
-  const size_t need = x ? route_ws_bytes(T, d, E) : 0;
+  if (!aligned_all({x, w_r, w_r_packed, bias, seg_offsets, K_dev, logits, topk_idx, topk_w, ws}))
+    return MOE_EINVAL;
+  const size_t need = !x ? 0 : w_r_packed ? decomoe::route_x3_ws_bytes(T, d, E) : route_ws_bytes(T, d, E);
   if (need && (!ws || ws_bytes < need)) return MOE_EWORKSPACE;
   const size_t nl = (size_t)T * E * 4, nk = (size_t)T * k * 4;
   Range o_ws = need ? rng(ws, need) : Range{0, 0};
   Range in_x = x ? rng(x, (size_t)T * d * elt_size(dtype)) : Range{0, 0};
-  Range in_w = x ? rng(w_r, (size_t)d * E * 4) : Range{0, 0};
+  Range in_w = !x ? Range{0, 0} : w_r_packed ? rng(w_r_packed, (size_t)d * E * 6) : rng(w_r, (size_t)d * E * 4);
   Range in_b = (x && bias) ? rng(bias, (size_t)E * 4) : Range{0, 0};
   Range in_s = seg_offsets ? rng(seg_offsets, (size_t)(n_seg + 1) * 4) : Range{0, 0};
   Range in_k = K_dev ? rng(K_dev, (size_t)n_seg * 4) : Range{0, 0};
@@ -135,8 +142,40 @@ int moe_route(const void* x, moe_dtype dtype, const float* w_r, const float* bia
   } else {
     if (any_alias({rng(topk_idx, nk), rng(topk_w, nk)}, {rng(logits, nl), in_s, in_k})) return MOE_EALIAS;
   }
-  return hip_status(decomoe::launch_route(x, dtype == MOE_BF16, w_r, bias, T, d, E, k, seg_offsets,
-                                          n_seg, K_dev, logits, topk_idx, topk_w, ws, stream));
+  return hip_status(decomoe::launch_route(x, dtype == MOE_BF16, w_r, x ? w_r_packed : nullptr, bias,
+                                          T, d, E, k, seg_offsets, n_seg, K_dev, logits, topk_idx,
+                                          topk_w, ws, stream));
+}
+}  // namespace
+
+int moe_route(const void* x, moe_dtype dtype, const float* w_r, const float* bias, int T, int d,
+              int E, int k, const int32_t* seg_offsets, int n_seg, const int32_t* K_dev,
+              float* logits, int32_t* topk_idx, float* topk_w, void* ws, size_t ws_bytes,
+              hipStream_t stream) {
+  if (x && !w_r) return MOE_EINVAL;
+  return route(x, dtype, w_r, nullptr, bias, T, d, E, k, seg_offsets, n_seg, K_dev, logits,
+               topk_idx, topk_w, ws, ws_bytes, stream);
+}
+
+int moe_route_packed(const void* x, moe_dtype dtype, const void* w_r_packed, const float* bias,
+                     int T, int d, int E, int k, const int32_t* seg_offsets, int n_seg,
+                     const int32_t* K_dev, float* logits, int32_t* topk_idx, float* topk_w,
+                     void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!x || !w_r_packed) return MOE_EINVAL;
+  if (!valid_dtype(dtype)) return MOE_EINVAL;
+  if (dtype != MOE_BF16) return MOE_EUNSUPPORTED;
+  if (E < 1 || d < 1) return MOE_EINVAL;
+  if (!router_packable(d, E)) return MOE_EUNSUPPORTED;
+  return route(x, dtype, nullptr, w_r_packed, bias, T, d, E, k, seg_offsets, n_seg, K_dev, logits,
+               topk_idx, topk_w, ws, ws_bytes, stream);
+}
+
+int moe_pack_router(const float* w_r, int d, int E, void* w_r_packed, hipStream_t stream) {
+  if (d < 1 || E < 1 || E > kMaxE || !w_r || !w_r_packed) return MOE_EINVAL;
+  if (!router_packable(d, E)) return MOE_EUNSUPPORTED;
+  if (!aligned_all({w_r, w_r_packed})) return MOE_EINVAL;
+  if (overlap(rng(w_r, (size_t)d * E * 4), rng(w_r_packed, (size_t)d * E * 6))) return MOE_EALIAS;
+  return hip_status(decomoe::launch_pack_router(w_r, d, E, w_r_packed, stream));
 }
 
 int moe_calibrate_prefix(const int32_t* topk_idx, const float* topk_w, int T, int E, int k,

@@ -37,11 +37,18 @@ __device__ __forceinline__ int find_segment(const int32_t* seg_offsets, int n_se
 
 // ---- launchers (host side; return hipError_t of the launch) -------------
 size_t route_ws_bytes(int T, int d, int E);
-// logits (x != NULL) and Top-k in one call; x == NULL reads `logits`
-hipError_t launch_route(const void* x, bool x_bf16, const float* w_r, const float* bias, int T,
-                        int d, int E, int k, const int32_t* seg_offsets, int n_seg,
-                        const int32_t* K_dev, float* logits, int32_t* idx, float* w, void* ws,
-                        hipStream_t s);
+// logits (x != NULL; from w_r_packed when given, else w_r) and Top-k in one
+// call; x == NULL reads `logits`
+hipError_t launch_route(const void* x, bool x_bf16, const float* w_r, const void* w_r_packed,
+                        const float* bias, int T, int d, int E, int k, const int32_t* seg_offsets,
+                        int n_seg, const int32_t* K_dev, float* logits, int32_t* idx, float* w,
+                        void* ws, hipStream_t s);
+// bf16 x (three-term split router weights): packing and the logits kernel;
+// `part`/`S` receive the split partials the Top-k kernel has to add
+size_t route_x3_ws_bytes(int T, int d, int E);
+hipError_t launch_pack_router(const float* w_r, int d, int E, void* out, hipStream_t s);
+hipError_t launch_router_x3(const void* x, const void* w_packed, const float* bias, int T, int d,
+                            int E, float* logits, void* ws, float*& part, int& S, hipStream_t s);
 size_t calibrate_ws_bytes(int T, int E);
 hipError_t launch_calibrate(const int32_t* idx, const float* w, int T, int E, int k,
                             const int32_t* seg_offsets, int n_seg, double p, double* mass,

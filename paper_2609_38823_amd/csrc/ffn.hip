@@ -470,25 +470,39 @@ __global__ __launch_bounds__(256) void pack_weights_kernel(const uint4* __restri
 // transfer), then all wavefronts meet at a barrier.  The weight registers
 // are waited for by the compiler where the MFMAs use them.
 // ---------------------------------------------------------------------------
-constexpr int AK = 64;                    // k-values per A stage
-constexpr int ASLOT = 128 * AK * 2;       // bytes per A stage (BM <= 128)
-__shared__ __attribute__((aligned(1024))) char aring0[ASLOT];
-__shared__ __attribute__((aligned(1024))) char aring1[ASLOT];
-__shared__ __attribute__((aligned(1024))) char aring2[ASLOT];
-__shared__ __attribute__((aligned(1024))) char aring3[ASLOT];
+constexpr int AK = 64;  // k-values per A stage
+
+// LDS bytes per A stage: BM rows of AK bf16, and at least one wavefront's
+// epilogue staging (32 rows of BN / 4 values plus padding); 1 KB multiples
+template <int BM, int BN>
+constexpr int a_slot() {
+  constexpr int a = BM * AK * 2, e = 32 * ((BN / 4) * 2 + 16);
+  return ((a > e ? a : e) + 1023) & ~1023;
+}
+// workgroups per CU: 128-row tiles need the register file of two; 64-row
+// tiles fit three (LDS: 3 x 32 KB)
+template <int BM>
+constexpr int packed_occupancy() { return BM >= 128 ? 2 : 3; }
 
 __device__ __forceinline__ u32x4 load_frag(__amdgpu_buffer_rsrc_t rs, int voff, int soff) {
   return __builtin_amdgcn_raw_buffer_load_b128(rs, voff, soff, 0);
 }
 
 template <int MODE, int BM, int BN>
-__global__ __launch_bounds__(NTHR, BN == 256 ? 2 : 1) void ffn_gemm_packed_kernel(
+__global__ __launch_bounds__(NTHR, packed_occupancy<BM>()) void ffn_gemm_packed_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ Wp, uint16_t* __restrict__ C,
     const Tiles tl, int d, int m) {
   constexpr int MI = BM / 32;   // 32-row token fragments (all tile rows)
   constexpr int NI = BN / 128;  // 32-row weight fragments per wavefront
   constexpr int AGW = BM / 32;  // A transfers (8 rows x 128 B) per wavefront per stage
   static_assert(MI >= 1 && AGW >= 1 && (MODE == 1 || NI % 2 == 0), "tile shape");
+
+  constexpr int ASLOT = a_slot<BM, BN>();
+  __shared__ __attribute__((aligned(1024))) char aring[4 * ASLOT];
+  char* const aring0 = aring;
+  char* const aring1 = aring + ASLOT;
+  char* const aring2 = aring + 2 * ASLOT;
+  char* const aring3 = aring + 3 * ASLOT;
 
   Work wk;
   if (!find_work(tl, true, wk, aring3)) return;

@@ -252,7 +252,16 @@ __global__ __launch_bounds__(256) void topk_kernel(float* __restrict__ logits, i
       const int e = lane + c * 64;
       if (e < E) {
         float a = part[(size_t)t * E + e];
-        for (int sp = 1; sp < S; ++sp) a += part[((size_t)sp * T + t) * E + e];
+        // partials in order sp = 1..S-1; loads issued four at a time
+        for (int sp = 1; sp < S; sp += 4) {
+          float pv[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            pv[u] = sp + u < S ? part[((size_t)(sp + u) * T + t) * E + e] : 0.f;
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            if (sp + u < S) a += pv[u];
+        }
         row[e] = a + (bias ? bias[e] : 0.f);
       }
     }
@@ -284,6 +293,122 @@ __global__ __launch_bounds__(256) void topk_kernel(float* __restrict__ logits, i
     w[(size_t)t * k + lane] = ex / sum;
   }
 }
+
+// ---------------------------------------------------------------------------
+// Top-k for E <= 16 MAXC (MAXC 8 or 16): four tokens per wavefront, one row
+// of 16 lanes per token.  Lane j of a row holds experts j, j + 16, ...; a
+// round's arg-max is a lane-local scan plus four DPP moves inside the row
+// (quad swaps, half-row and row mirrors), so the 16 lanes end with the
+// row's best pair and no value leaves the row.  Round r's winner is kept by
+// lane r % 16 in slot r / 16 (k <= 32).  Same selection order, tie rule and
+// weights as topk_kernel.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void row_best(float& v, int& i) {
+  dpp_better<0xB1>(v, i);   // quad_perm [1, 0, 3, 2]
+  dpp_better<0x4E>(v, i);   // quad_perm [2, 3, 0, 1]
+  dpp_better<0x141>(v, i);  // row_half_mirror
+  dpp_better<0x140>(v, i);  // row_mirror
+}
+__device__ __forceinline__ float row_sum(float v) {
+  v += dpp_f<0xB1>(v);
+  v += dpp_f<0x4E>(v);
+  v += dpp_f<0x141>(v);
+  v += dpp_f<0x140>(v);
+  return v;
+}
+
+template <int MAXC>
+__global__ __launch_bounds__(256) void topk_row_kernel(float* __restrict__ logits, int T, int E,
+                                                       int k, const int32_t* __restrict__ seg_offsets,
+                                                       int n_seg, const int32_t* __restrict__ K_dev,
+                                                       const float* __restrict__ part, int S,
+                                                       const float* __restrict__ bias,
+                                                       int32_t* __restrict__ idx, float* __restrict__ w) {
+  const int j = threadIdx.x & 15;
+  const int t = blockIdx.x * 16 + (threadIdx.x >> 4);
+  if (t >= T) return;  // the whole row of 16 lanes leaves together
+  int Klim = E;
+  if (K_dev) {
+    const int sg = seg_offsets ? find_segment(seg_offsets, n_seg, t) : 0;
+    Klim = clampi(K_dev[sg], k, E);
+  }
+  float* row = logits + (size_t)t * E;
+  float v[MAXC];
+  if (part) {
+    // partials in order sp = 0..S-1, then the bias; every load of a lane
+    // is issued before the additions
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+      const int e = j + 16 * c;
+      v[c] = e < E ? part[(size_t)t * E + e] : 0.f;
+    }
+    for (int sp = 1; sp < S; sp += 4) {  // four partials' loads in flight together
+      float pv[4][MAXC];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int c = 0; c < MAXC; ++c) {
+          const int e = j + 16 * c;
+          pv[u][c] = (sp + u < S && e < E) ? part[((size_t)(sp + u) * T + t) * E + e] : 0.f;
+        }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (sp + u < S) {
+#pragma unroll
+          for (int c = 0; c < MAXC; ++c) v[c] += pv[u][c];
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+      const int e = j + 16 * c;
+      if (e < E) {
+        v[c] += bias ? bias[e] : 0.f;
+        row[e] = v[c];
+      }
+    }
+  } else {
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+      const int e = j + 16 * c;
+      v[c] = e < E ? row[e] : 0.f;
+    }
+  }
+  uint32_t alive = 0;
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c)
+    if (j + 16 * c < Klim) alive |= 1u << c;
+  float my_v[2] = {0.f, 0.f};
+  int my_i[2] = {0, 0};
+  float v0 = 0.f;
+  for (int r = 0; r < k; ++r) {
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c)
+      if (alive & (1u << c)) better(bv, bi, v[c], j + 16 * c);
+    row_best(bv, bi);
+    if (bi < E && (bi & 15) == j) alive &= ~(1u << (bi >> 4));
+    if (r == 0) v0 = bv;
+    if ((r & 15) == j) {
+      my_v[r >> 4] = bv;
+      my_i[r >> 4] = bi;
+    }
+  }
+  float ex[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) ex[q] = j + 16 * q < k ? expf(my_v[q] - v0) : 0.f;
+  // slots in order r = 0..k-1: lanes hold r = j and r = j + 16; the row sum
+  // adds the k exponentials (the same total in every lane of the row)
+  const float sum = row_sum(ex[0] + ex[1]);
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int r = j + 16 * q;
+    if (r < k) {
+      idx[(size_t)t * k + r] = my_i[q];
+      w[(size_t)t * k + r] = ex[q] / sum;
+    }
+  }
+}
 }  // namespace
 
 // Split factor of the router's d-range: enough workgroups to cover the chip
@@ -301,13 +426,16 @@ size_t route_ws_bytes(int T, int d, int E) {
   return S > 1 ? (size_t)S * T * E * sizeof(float) : 0;
 }
 
-hipError_t launch_route(const void* x, bool x_bf16, const float* w_r, const float* bias, int T,
-                        int d, int E, int k, const int32_t* seg_offsets, int n_seg,
-                        const int32_t* K_dev, float* logits, int32_t* idx, float* w, void* ws,
-                        hipStream_t s) {
+hipError_t launch_route(const void* x, bool x_bf16, const float* w_r, const void* w_r_packed,
+                        const float* bias, int T, int d, int E, int k, const int32_t* seg_offsets,
+                        int n_seg, const int32_t* K_dev, float* logits, int32_t* idx, float* w,
+                        void* ws, hipStream_t s) {
   float* part = nullptr;
   int S = 1;
-  if (x) {
+  if (x && w_r_packed) {
+    hipError_t err = launch_router_x3(x, w_r_packed, bias, T, d, E, logits, ws, part, S, s);
+    if (err != hipSuccess) return err;
+  } else if (x) {
     if (d % 128 == 0) {
       S = router_splits(T, d, E);
       if (S > 1) part = static_cast<float*>(ws);
@@ -326,9 +454,16 @@ hipError_t launch_route(const void* x, bool x_bf16, const float* w_r, const floa
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
   }
-  const int blocks = (T + 3) / 4;
-  if (E <= 128)
+  // many tokens: four per wavefront (fewer instructions per token); few
+  // tokens: one per wavefront (more independent wavefronts, shorter chains)
+  const int blocks = (T + 3) / 4, rblocks = (T + 15) / 16;
+  const bool rows = T >= 16384;
+  if (E <= 128 && rows)
+    topk_row_kernel<8><<<rblocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w);
+  else if (E <= 128)
     topk_kernel<2><<<blocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w);
+  else if (E <= 256 && rows)
+    topk_row_kernel<16><<<rblocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w);
   else if (E <= 256)
     topk_kernel<4><<<blocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w);
   else

@@ -6,7 +6,8 @@ the order of Algorithm 2 of the paper:
 
   dense span (before the visual exit):
       moe_route(x) -> moe_dispatch -> moe_expert_ffn -> moe_combine
-      (bf16 layers: moe_expert_ffn_packed on weights packed at load time)
+      (bf16 layers: moe_route_packed and moe_expert_ffn_packed on router
+      and expert weights packed at load time)
   RCEP span (from the visual exit on):
       moe_route(x) [full pool] -> moe_calibrate_prefix [s, K]
       -> moe_route(logits, K) [prefix re-route] -> moe_dispatch
@@ -139,8 +140,22 @@ class MoELayer:
             abi.moe_pack_expert_weights(self.w_gate_up, wgu)
             abi.moe_pack_expert_weights(self.w_down, wd)
             self.w_gate_up, self.w_down = wgu, wd
+        # bf16 layers with 32-expert blocks route on bf16 MFMA with the
+        # router weights split in three bf16 terms (moe_pack_router)
+        self.w_r_packed = None
+        if self.dt == torch.bfloat16 and self.E % 32 == 0 and self.d % 64 == 0:
+            self.w_r_packed = torch.empty((3 * self.d * self.E,), dtype=torch.bfloat16, device=device)
+            abi.moe_pack_router(self.w_r, self.w_r_packed)
         self.device = device
         self._bufs: dict = {}
+
+    def _route(self, x, b: Buffers, idx, w, stream=None):
+        """Router logits into b.logits and the full-pool Top-k."""
+        if self.w_r_packed is not None:
+            abi.moe_route_packed(x, self.w_r_packed, self.bias, self.k, b.logits, idx, w, ws=b.ws,
+                                 stream=stream)
+        else:
+            abi.moe_route(x, self.w_r, self.bias, self.k, b.logits, idx, w, ws=b.ws, stream=stream)
 
     def buffers(self, T: int, n_seg: int = 1) -> Buffers:
         key = (T, n_seg)
@@ -172,7 +187,7 @@ class MoELayer:
                       mark=None, residual=None, out=None) -> Buffers:
         """Full expert pool (layers before the visual exit)."""
         b = b or self.buffers(x.shape[0])
-        abi.moe_route(x, self.w_r, self.bias, self.k, b.logits, b.idx, b.w, ws=b.ws, stream=stream)
+        self._route(x, b, b.idx, b.w, stream=stream)
         if mark:
             mark()
         self._experts(x, b, b.idx, b.w, stream=stream, mark=mark, residual=residual, out=out)
@@ -186,8 +201,7 @@ class MoELayer:
         b = b or self.buffers(x.shape[0], n_seg)
         K = b.K if K_out is None else K_out
         mk = mark or (lambda: None)
-        abi.moe_route(x, self.w_r, self.bias, self.k, b.logits, b.idx_full, b.w_full, ws=b.ws,
-                      stream=stream)
+        self._route(x, b, b.idx_full, b.w_full, stream=stream)
         mk()
         abi.moe_calibrate_prefix(b.idx_full, b.w_full, self.E, p, b.mass, b.ws, K_out=K,
                                  seg_offsets=seg_offsets, stream=stream)

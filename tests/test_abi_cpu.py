@@ -31,7 +31,8 @@ def test_header_declares_the_boundary():
     assert declared_functions() == sorted([
         "drop_visual_block", "moe_calibrate_prefix", "moe_combine", "moe_combine_residual",
         "moe_dispatch", "moe_expert_ffn", "moe_expert_ffn_packed", "moe_pack_expert_weights",
-        "moe_permute_experts", "moe_route", "moe_status_string", "moe_workspace_size"])
+        "moe_pack_router", "moe_permute_experts", "moe_route", "moe_route_packed", "moe_status_string",
+        "moe_workspace_size"])
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -188,6 +189,30 @@ def test_permute_experts_rejects(lib):
     # misaligned bf16 weights
     assert lib.moe_permute_experts(P1, 4, 64, 32, BF16, nul, nul, ctypes.c_void_p(P2.value + 1), nul, nul, nul, P3, nul,
                                    NULL) == EINVAL
+
+
+def test_packed_router_rejects(lib):
+    # float32 x, E % 32, d % 64, no x
+    assert lib.moe_route_packed(P1, F32, P2, NULL, 8, 64, 32, 2, NULL, 1, NULL, P3, P4, P5, WS, 1 << 20,
+                                NULL) == EUNSUPPORTED
+    assert lib.moe_route_packed(P1, BF16, P2, NULL, 8, 64, 48, 2, NULL, 1, NULL, P3, P4, P5, WS, 1 << 20,
+                                NULL) == EUNSUPPORTED
+    assert lib.moe_route_packed(P1, BF16, P2, NULL, 8, 96, 32, 2, NULL, 1, NULL, P3, P4, P5, WS, 1 << 20,
+                                NULL) == EUNSUPPORTED
+    assert lib.moe_route_packed(NULL, BF16, P2, NULL, 8, 64, 32, 2, NULL, 1, NULL, P3, P4, P5, WS, 1 << 20,
+                                NULL) == EINVAL
+    # logits overlapping the packed weights
+    assert lib.moe_route_packed(P1, BF16, P2, NULL, 8, 64, 32, 2, NULL, 1, NULL, P2, P4, P5, WS, 1 << 20,
+                                NULL) == EALIAS
+    # a split needs workspace (T = 8: 8 splits of the 2048-wide d-range)
+    assert lib.moe_route_packed(P1, BF16, P2, NULL, 8, 2048, 128, 8, NULL, 1, NULL, P3, P4, P5, NULL, 0,
+                                NULL) == EWORKSPACE
+    assert lib.moe_pack_router(P1, 64, 48, P2, NULL) == EUNSUPPORTED
+    assert lib.moe_pack_router(P1, 96, 32, P2, NULL) == EUNSUPPORTED
+    assert lib.moe_pack_router(P1, 2048, 128, ctypes.c_void_p(P1.value + 1024), NULL) == EALIAS
+    assert lib.moe_pack_router(NULL, 64, 32, P2, NULL) == EINVAL
+    # the workspace covers the packed router's split partials
+    assert lib.moe_workspace_size(64, 128, 8, 2048, 768, 1) >= 8 * 64 * 128 * 4
 
 
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):

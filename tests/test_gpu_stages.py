@@ -46,6 +46,12 @@ def host(t):
     return t.cpu().numpy()
 
 
+def host_bits(t):
+    """uint16 bit patterns of a bf16 device tensor."""
+    torch.cuda.synchronize()
+    return t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+
 def i32(shape):
     return torch.full(shape, -7, dtype=torch.int32, device="cuda")
 
@@ -81,8 +87,10 @@ def test_drop_visual_block_bitwise(dt, S, d, v0, v1):
 # ---------------------------------------------------------------------------
 # moe_route, logits-input mode: Top-k and weights on given logits
 # ---------------------------------------------------------------------------
+# T >= 16384 takes the four-tokens-per-wavefront kernel (8 or 16 values per
+# lane; k > 16 uses the second slot of every lane)
 ROUTE_CASES = [(1, 16, 2), (37, 16, 2), (5, 7, 7), (129, 64, 1), (512, 128, 8), (4096, 128, 8),
-               (300, 1000, 32), (70, 65, 3)]
+               (300, 1000, 32), (70, 65, 3), (16384, 128, 8), (16390, 200, 20), (16385, 100, 32)]
 
 
 @pytest.mark.parametrize("ties", [False, True])
@@ -103,6 +111,8 @@ def test_topk_on_given_logits(T, E, k, ties):
     (64, 128, 8, list(range(65)), None),  # one token per segment
     (200, 128, 8, [0, 0, 50, 50, 130, 200], [8, 40, 3, 128, 200]),  # empty segments, clamping
     (33, 10, 4, [0, 33], [4]),  # K == k
+    (16390, 256, 17, [0, 8000, 8000, 16390], [100, 5, 256]),  # row kernel, 16 values per lane
+    (16384, 128, 8, [0, 16384], [84]),
 ])
 def test_prefix_reroute_on_given_logits(T, E, k, segs, Ks):
     a = I.synthetic_rows(T, E, "f32", seed=7 * T + E)
@@ -185,6 +195,78 @@ def test_router_logits_and_free_running_topk(name, T):
     chosen = np.take_along_axis(a_ref, gi.astype(np.int64), axis=1)
     assert np.all(chosen >= (kth - 2 * delta)[:, None])
     np.testing.assert_allclose(host(w)[ok], ref_w[ok], rtol=2e-5, atol=1e-6)
+
+
+# ---------------------------------------------------------------------------
+# moe_pack_router / moe_route_packed: three-term bf16 split of W_r on MFMA
+# ---------------------------------------------------------------------------
+def split3_np(w):
+    """W1 = bf16(W), W2 = bf16(W - W1), W3 = bf16(W - W1 - W2) (float32
+    differences, exact)."""
+    w = np.asarray(w, np.float32)
+    w1 = I.round_to_bf16(w)
+    r1 = (w - w1).astype(np.float32)
+    w2 = I.round_to_bf16(r1)
+    w3 = I.round_to_bf16((r1 - w2).astype(np.float32))
+    return w1, w2, w3
+
+
+def pack_router_np(w):
+    """The documented layout: element 8 l + j of block ((eb KB + kb) 3 + p)
+    is term p of W[16 kb + 8 (l / 32) + j, 32 eb + l % 32]."""
+    d, E = w.shape
+    KB = d // 16
+    l, j = np.arange(64), np.arange(8)
+    k_idx = 16 * np.arange(KB)[:, None, None] + 8 * (l // 32)[None, :, None] + j[None, None, :]
+    out = np.empty((E // 32, KB, 3, 64, 8), np.float32)
+    for p, P in enumerate(split3_np(w)):
+        for eb in range(E // 32):
+            out[eb, :, p] = P[k_idx, 32 * eb + (l % 32)[None, :, None]]
+    return out.reshape(-1)
+
+
+E96_BF16 = I.LayerShape(d=256, E=96, m=8, k=4, dtype="bf16", zipf_alpha=0.35)  # 3 of 4 waves busy
+D64_BF16 = I.LayerShape(d=64, E=32, m=8, k=2, dtype="bf16", zipf_alpha=None)   # one 64-wide stage
+
+
+# 64-row tiles at 4096 (4 splits) and 8192 (2) and 65536 (1); 32-row tiles
+# with 8 splits below; the small shapes cover idle wavefronts and S = 1
+# with a single stage
+@pytest.mark.parametrize("shape,T", [("qwen", 4096), ("qwen", 8192), ("qwen", 512), ("qwen", 77),
+                                     ("qwen", 64), ("qwen", 1), ("e96", 333), ("d64", 50),
+                                     ("qwen", 65536)])
+def test_route_packed(shape, T):
+    sh = {"qwen": I.QWEN3_VL_MOE, "e96": E96_BF16, "d64": D64_BF16}[shape]
+    rp = I.router_params(sh, seed=3)
+    x = I.tokens(sh, T, seed=T)
+    w_r = dev(rp["w_r"])
+    wp = torch.empty((3 * sh.d * sh.E,), dtype=torch.bfloat16, device="cuda")
+    abi.moe_pack_router(w_r, wp)
+    np.testing.assert_array_equal(host_bits(wp), I.bf16_bits(pack_router_np(rp["w_r"])))
+    logits, idx, w = f32((T, sh.E)), i32((T, sh.k)), f32((T, sh.k))
+    bias = dev(rp["bias"]) if rp["bias"] is not None else None
+    abi.moe_route_packed(dev(x, torch.bfloat16), wp, bias, sh.k, logits, idx, w,
+                         ws=ws_for(T, sh.E, sh.k, sh.d))
+    a_gpu = host(logits).astype(np.float64)
+    rows = np.arange(T) if T <= 8192 else np.random.default_rng(1).choice(T, 4096, replace=False)
+    a_ref = oracle.router_logits(x[rows], rp["w_r"], rp["bias"])
+    a_gpu = a_gpu[rows]
+    # bound: 3d exact products accumulated in float32 plus up to 32 split
+    # partials and the bias (gamma_{3d+40}), plus the split's own
+    # representation error 2^-24 |W| per term (2^-23 with margin)
+    mag = np.abs(x[rows].astype(np.float64)) @ np.abs(rp["w_r"].astype(np.float64))
+    full = mag + (np.abs(rp["bias"].astype(np.float64))[None, :] if rp["bias"] is not None else 0)
+    assert np.all(np.abs(a_gpu - a_ref) <= gamma(3 * sh.d + 40) * full + 2.0 ** -23 * mag)
+    delta = np.abs(a_gpu - a_ref).max(axis=1)
+    ok = robust_tokens(a_ref, sh.k, delta)
+    ref_idx, ref_w = oracle.full_pool_route(a_ref, sh.k)
+    gi = host(idx)[rows]
+    np.testing.assert_array_equal(gi[ok], ref_idx[ok])
+    assert ok.mean() > 0.99
+    # teacher-forced: the Top-k of the GPU's own logits is exact
+    tf_idx, tf_w = oracle.full_pool_route(a_gpu, sh.k)
+    np.testing.assert_array_equal(gi, tf_idx)
+    np.testing.assert_allclose(host(w)[rows], tf_w, rtol=2e-5, atol=1e-6)
 
 
 # ---------------------------------------------------------------------------
@@ -366,6 +448,10 @@ def test_pack_expert_weights_layout(E, R, C):
 PACKED_CASES = [c for c in FFN_CASES if c[3] == "bf16" and c[2] % 256 == 0] + [
     (4, 512, 256, "bf16", 700, None, [300, 0, 1, 399]),  # one 8-k-step body, ragged tails
     (2, 2048, 768, "bf16", 1700, None, [1600, 100]),       # many tiles of one expert
+    # few rows per expert (decode-like weight streaming)
+    (128, 2048, 768, "bf16", 512, None, None),             # 64 tokens x top-8
+    (16, 512, 256, "bf16", 200, None, [0, 1, 31, 32, 33, 63, 40] + [0] * 9),  # ragged tails
+    (6, 2048, 768, "bf16", 60, 4, None),                   # experts >= K skipped
 ]
 
 
