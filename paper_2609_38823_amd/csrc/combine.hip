@@ -33,23 +33,36 @@ __global__ __launch_bounds__(256) void combine_kernel(const uint4* __restrict__ 
   const int A = T * k;
   for (int c = c0; c < chunks; c += cstep) {
     float acc[8] = {};
-    for (int j = 0; j < k; ++j) {
-      const int r = row_of_slot[(size_t)t * k + j];
-      if (r < 0 || r >= A) continue;
-      const float wj = w[(size_t)t * k + j];
-      const uint4 v = y[(size_t)r * chunks + c];
-      if constexpr (BF16) {
-        const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+    // slots in groups of 8: the group's row loads are all issued before the
+    // accumulation (a slot outside [0, T*k) reads row 0 and adds nothing)
+    for (int j0 = 0; j0 < k; j0 += 8) {
+      uint4 v[8];
+      float wj[8];
+      bool ok[8];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          acc[2 * q] = fmaf(wj, __uint_as_float(u[q] << 16), acc[2 * q]);
-          acc[2 * q + 1] = fmaf(wj, __uint_as_float(u[q] & 0xffff0000u), acc[2 * q + 1]);
+      for (int u = 0; u < 8; ++u) {
+        const int j = j0 + u;
+        const int r = j < k ? row_of_slot[(size_t)t * k + j] : -1;
+        ok[u] = r >= 0 && r < A;
+        wj[u] = j < k ? w[(size_t)t * k + j] : 0.f;
+        v[u] = y[(size_t)(ok[u] ? r : 0) * chunks + c];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (!ok[u]) continue;
+        if constexpr (BF16) {
+          const uint32_t q4[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            acc[2 * q] = fmaf(wj[u], __uint_as_float(q4[q] << 16), acc[2 * q]);
+            acc[2 * q + 1] = fmaf(wj[u], __uint_as_float(q4[q] & 0xffff0000u), acc[2 * q + 1]);
+          }
+        } else {
+          acc[0] = fmaf(wj[u], __uint_as_float(v[u].x), acc[0]);
+          acc[1] = fmaf(wj[u], __uint_as_float(v[u].y), acc[1]);
+          acc[2] = fmaf(wj[u], __uint_as_float(v[u].z), acc[2]);
+          acc[3] = fmaf(wj[u], __uint_as_float(v[u].w), acc[3]);
         }
-      } else {
-        acc[0] = fmaf(wj, __uint_as_float(v.x), acc[0]);
-        acc[1] = fmaf(wj, __uint_as_float(v.y), acc[1]);
-        acc[2] = fmaf(wj, __uint_as_float(v.z), acc[2]);
-        acc[3] = fmaf(wj, __uint_as_float(v.w), acc[3]);
       }
     }
     if constexpr (RES) {

@@ -39,22 +39,44 @@ __global__ __launch_bounds__(DP_THREADS) void dispatch_hist_kernel(const int32_t
   for (int e = threadIdx.x; e < E; e += DP_THREADS) hist[(size_t)blockIdx.x * E + e] = h[e];
 }
 
-// one workgroup of 1024 threads; thread e owns expert e.  The chunk
-// columns are read 16 at a time (independent loads in flight), the scan over
-// the experts is a wavefront scan plus the wavefront totals.
+// one workgroup of 1024 threads.  Thread (p, e), tid = p E + e, owns expert e
+// and the p-th of P = 1024 / E contiguous ranges of chunks: it sums its
+// range (16 independent loads in flight), the P partial sums of an expert
+// are combined in LDS, the scan over the experts is a wavefront scan plus
+// the wavefront totals, and each thread then writes the chunk bases of its
+// range.  Every sum runs in chunk order, so the bases are those of a
+// sequential scan.
 __global__ __launch_bounds__(1024) void dispatch_scan_kernel(const int32_t* __restrict__ hist,
                                                              int n_chunks, int E,
                                                              int32_t* __restrict__ base,
                                                              int32_t* __restrict__ counts,
                                                              int32_t* __restrict__ offsets) {
+  __shared__ int s_cnt[1024];          // [p][e] partial sums, then prefixes over p
+  __shared__ int s_off[1024];          // [e] exclusive offsets
   __shared__ int part[1024 / kWave];
-  const int e = threadIdx.x, lane = e & 63, wv = e >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int P = 1024 / E;              // E <= 1024
+  const int p = tid / E, e = tid - p * E;
+  const bool mine = p < P;
+  const int per = (n_chunks + P - 1) / P;
+  const int c0 = min(n_chunks, p * per), c1 = min(n_chunks, c0 + per);
   int cnt = 0;
-  if (e < E) {
+  if (mine) {
 #pragma unroll 16
-    for (int c = 0; c < n_chunks; ++c) cnt += hist[(size_t)c * E + e];
+    for (int c = c0; c < c1; ++c) cnt += hist[(size_t)c * E + e];
+    s_cnt[tid] = cnt;
   }
-  int incl = cnt;
+  __syncthreads();
+  // threads 0..E-1: the expert totals and the per-range prefixes
+  int tot = 0;
+  if (tid < E) {
+    for (int q = 0; q < P; ++q) {
+      const int v = s_cnt[q * E + tid];
+      s_cnt[q * E + tid] = tot;
+      tot += v;
+    }
+  }
+  int incl = tot;
 #pragma unroll
   for (int off = 1; off < kWave; off <<= 1) {
     const int y = __shfl_up(incl, off, kWave);
@@ -62,14 +84,19 @@ __global__ __launch_bounds__(1024) void dispatch_scan_kernel(const int32_t* __re
   }
   if (lane == kWave - 1) part[wv] = incl;
   __syncthreads();
-  int run = incl - cnt;  // exclusive within the wavefront
-  for (int w = 0; w < wv; ++w) run += part[w];
-  if (e < E) {
-    counts[e] = cnt;
-    offsets[e] = run;
-    if (e == E - 1) offsets[E] = run + cnt;
+  if (tid < E) {
+    int run = incl - tot;  // exclusive within the wavefront
+    for (int w = 0; w < wv; ++w) run += part[w];
+    s_off[tid] = run;
+    counts[tid] = tot;
+    offsets[tid] = run;
+    if (tid == E - 1) offsets[E] = run + tot;
+  }
+  __syncthreads();
+  if (mine) {
+    int run = s_off[e] + s_cnt[tid];
 #pragma unroll 16
-    for (int c = 0; c < n_chunks; ++c) {
+    for (int c = c0; c < c1; ++c) {
       const int h = hist[(size_t)c * E + e];
       base[(size_t)c * E + e] = run;
       run += h;
