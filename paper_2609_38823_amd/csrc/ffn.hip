@@ -573,98 +573,122 @@ __global__ __launch_bounds__(NTHR, packed_occupancy<BM>()) void ffn_gemm_packed_
   int a_lane[4];
 #pragma unroll
   for (int s4 = 0; s4 < 4; ++s4) a_lane[s4] = r32 * 128 + (((2 * s4 + kh) ^ ((r32 >> 1) & 7)) << 4);
-  auto load_a = [&](const char* stage, int s4, bf16x8 (&af)[MI]) {
-#pragma unroll
-    for (int mi = 0; mi < MI; ++mi)
-      af[mi] = *reinterpret_cast<const bf16x8*>(stage + mi * 32 * 128 + a_lane[s4]);
-  };
-  auto mma = [&](const bf16x8 (&af)[MI], const u32x4 (&bfr)[NI]) {
-#pragma unroll
-    for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-      for (int ni = 0; ni < NI; ++ni)
-        acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, bfr[ni]), af[mi],
-                                                              acc[mi][ni], 0, 0, 0);
-  };
-  constexpr int NMF = MI * NI;
-  auto interleave = [&]() {
-#pragma unroll
-    for (int i = 0; i < MI; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, NMF / MI, 0);  // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);         // DS read
-    }
-  };
-
-  // ---- k-step i (32 k-values): A stage i / 2, substeps 2 (i % 2) and +1;
-  // weights in register stage i % 4.  At the end of an A stage (odd i) the
-  // next stage is awaited and the finished one refilled with stage + 4.
-  //   ODD          i is the second half of an A stage
-  //   ISSUE_A      refill the finished A stage
-  //   ISSUE_B      load the weights of k-step i + 3
-  //   LAST         the final k-step (nothing follows)
-  bf16x8 a0[MI], a1[MI];
+  // The pipeline runs with MA = the item's 32-row token blocks that hold
+  // rows (a tile's last item of an expert is often short): blocks past them
+  // would only multiply padding, so their fragment reads and MFMAs are left
+  // out (their accumulators stay zero and their rows are not stored).
   u32x4 bq0[2][NI], bq1[2][NI], bq2[2][NI], bq3[2][NI];
-  auto step = [&](auto ODD, auto ISSUE_A, auto ISSUE_B, auto LAST, int i, char* cur, char* nxt,
-                  const u32x4 (&bc)[2][NI], u32x4 (&bn)[2][NI]) {
-    constexpr bool odd = decltype(ODD)::value;
-    // the weight registers of k-step i - 1 are free: refill them first
-    if constexpr (decltype(ISSUE_B)::value) load_b(bn, i + 3);
-    __builtin_amdgcn_sched_barrier(0);
-    load_a(cur, odd ? 3 : 1, a1);
-    mma(a0, bc[0]);
-    interleave();
-    if constexpr (!decltype(LAST)::value) {
-      if constexpr (odd) {
-        own_word(nxt);
-        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): reads of `cur` are complete
-        __builtin_amdgcn_s_barrier();
-        __builtin_amdgcn_sched_barrier(0);
-        if constexpr (decltype(ISSUE_A)::value) issue_a(cur, i / 2 + 4);
-        __builtin_amdgcn_sched_barrier(0);
+  auto pipeline = [&](auto MAC) {
+    constexpr int MA = decltype(MAC)::value;
+    auto load_a = [&](const char* stage, int s4, bf16x8 (&af)[MI]) {
+  #pragma unroll
+      for (int mi = 0; mi < MA; ++mi)
+        af[mi] = *reinterpret_cast<const bf16x8*>(stage + mi * 32 * 128 + a_lane[s4]);
+    };
+    auto mma = [&](const bf16x8 (&af)[MI], const u32x4 (&bfr)[NI]) {
+  #pragma unroll
+      for (int mi = 0; mi < MA; ++mi)
+  #pragma unroll
+        for (int ni = 0; ni < NI; ++ni)
+          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, bfr[ni]), af[mi],
+                                                                acc[mi][ni], 0, 0, 0);
+    };
+    auto interleave = [&]() {
+  #pragma unroll
+      for (int i = 0; i < MA; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, NI, 0);        // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);         // DS read
       }
-      load_a(odd ? nxt : cur, odd ? 0 : 2, a0);
-    }
-    mma(a1, bc[1]);
-    if constexpr (!decltype(LAST)::value) interleave();
-  };
-  using F = std::integral_constant<bool, false>;
-  using Tr = std::integral_constant<bool, true>;
+    };
 
-  // body of 8 k-steps = 4 A stages in slots 0..3; every issue active
-  auto body = [&](int i) {
+    // ---- k-step i (32 k-values): A stage i / 2, substeps 2 (i % 2) and +1;
+    // weights in register stage i % 4.  At the end of an A stage (odd i) the
+    // next stage is awaited and the finished one refilled with stage + 4.
+    //   ODD          i is the second half of an A stage
+    //   ISSUE_A      refill the finished A stage
+    //   ISSUE_B      load the weights of k-step i + 3
+    //   LAST         the final k-step (nothing follows)
+    bf16x8 a0[MI], a1[MI];
+    auto step = [&](auto ODD, auto ISSUE_A, auto ISSUE_B, auto LAST, int i, char* cur, char* nxt,
+                    const u32x4 (&bc)[2][NI], u32x4 (&bn)[2][NI]) {
+      constexpr bool odd = decltype(ODD)::value;
+      // the weight registers of k-step i - 1 are free: refill them first
+      if constexpr (decltype(ISSUE_B)::value) load_b(bn, i + 3);
+      __builtin_amdgcn_sched_barrier(0);
+      load_a(cur, odd ? 3 : 1, a1);
+      mma(a0, bc[0]);
+      interleave();
+      if constexpr (!decltype(LAST)::value) {
+        if constexpr (odd) {
+          own_word(nxt);
+          __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): reads of `cur` are complete
+          __builtin_amdgcn_s_barrier();
+          __builtin_amdgcn_sched_barrier(0);
+          if constexpr (decltype(ISSUE_A)::value) issue_a(cur, i / 2 + 4);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        load_a(odd ? nxt : cur, odd ? 0 : 2, a0);
+      }
+      mma(a1, bc[1]);
+      if constexpr (!decltype(LAST)::value) interleave();
+    };
+    using F = std::integral_constant<bool, false>;
+    using Tr = std::integral_constant<bool, true>;
+
+    // body of 8 k-steps = 4 A stages in slots 0..3; every issue active
+    auto body = [&](int i) {
+      step(F{}, F{}, Tr{}, F{}, i + 0, aring0, aring0, bq0, bq3);
+      step(Tr{}, Tr{}, Tr{}, F{}, i + 1, aring0, aring1, bq1, bq0);
+      step(F{}, F{}, Tr{}, F{}, i + 2, aring1, aring1, bq2, bq1);
+      step(Tr{}, Tr{}, Tr{}, F{}, i + 3, aring1, aring2, bq3, bq2);
+      step(F{}, F{}, Tr{}, F{}, i + 4, aring2, aring2, bq0, bq3);
+      step(Tr{}, Tr{}, Tr{}, F{}, i + 5, aring2, aring3, bq1, bq0);
+      step(F{}, F{}, Tr{}, F{}, i + 6, aring3, aring3, bq2, bq1);
+      step(Tr{}, Tr{}, Tr{}, F{}, i + 7, aring3, aring0, bq3, bq2);
+    };
+
+    issue_a(aring0, 0);
+    issue_a(aring1, 1);
+    issue_a(aring2, 2);
+    issue_a(aring3, 3);
+    __builtin_amdgcn_sched_barrier(0);
+    load_b(bq0, 0);
+    load_b(bq1, 1);
+    load_b(bq2, 2);
+    __builtin_amdgcn_sched_barrier(0);
+    own_word(aring0);
+    __builtin_amdgcn_s_barrier();
+    load_a(aring0, 0, a0);
+    int i = 0;
+    for (; i + 8 < nk; i += 8) body(i);
+    // last 8 k-steps: no A refills; weights up to k-step nk - 1
     step(F{}, F{}, Tr{}, F{}, i + 0, aring0, aring0, bq0, bq3);
-    step(Tr{}, Tr{}, Tr{}, F{}, i + 1, aring0, aring1, bq1, bq0);
+    step(Tr{}, F{}, Tr{}, F{}, i + 1, aring0, aring1, bq1, bq0);
     step(F{}, F{}, Tr{}, F{}, i + 2, aring1, aring1, bq2, bq1);
-    step(Tr{}, Tr{}, Tr{}, F{}, i + 3, aring1, aring2, bq3, bq2);
+    step(Tr{}, F{}, Tr{}, F{}, i + 3, aring1, aring2, bq3, bq2);
     step(F{}, F{}, Tr{}, F{}, i + 4, aring2, aring2, bq0, bq3);
-    step(Tr{}, Tr{}, Tr{}, F{}, i + 5, aring2, aring3, bq1, bq0);
-    step(F{}, F{}, Tr{}, F{}, i + 6, aring3, aring3, bq2, bq1);
-    step(Tr{}, Tr{}, Tr{}, F{}, i + 7, aring3, aring0, bq3, bq2);
+    step(Tr{}, F{}, F{}, F{}, i + 5, aring2, aring3, bq1, bq0);
+    step(F{}, F{}, F{}, F{}, i + 6, aring3, aring3, bq2, bq1);
+    step(Tr{}, F{}, F{}, Tr{}, i + 7, aring3, aring0, bq3, bq2);
   };
-
-  issue_a(aring0, 0);
-  issue_a(aring1, 1);
-  issue_a(aring2, 2);
-  issue_a(aring3, 3);
-  __builtin_amdgcn_sched_barrier(0);
-  load_b(bq0, 0);
-  load_b(bq1, 1);
-  load_b(bq2, 2);
-  __builtin_amdgcn_sched_barrier(0);
-  own_word(aring0);
-  __builtin_amdgcn_s_barrier();
-  load_a(aring0, 0, a0);
-  int i = 0;
-  for (; i + 8 < nk; i += 8) body(i);
-  // last 8 k-steps: no A refills; weights up to k-step nk - 1
-  step(F{}, F{}, Tr{}, F{}, i + 0, aring0, aring0, bq0, bq3);
-  step(Tr{}, F{}, Tr{}, F{}, i + 1, aring0, aring1, bq1, bq0);
-  step(F{}, F{}, Tr{}, F{}, i + 2, aring1, aring1, bq2, bq1);
-  step(Tr{}, F{}, Tr{}, F{}, i + 3, aring1, aring2, bq3, bq2);
-  step(F{}, F{}, Tr{}, F{}, i + 4, aring2, aring2, bq0, bq3);
-  step(Tr{}, F{}, F{}, F{}, i + 5, aring2, aring3, bq1, bq0);
-  step(F{}, F{}, F{}, F{}, i + 6, aring3, aring3, bq2, bq1);
-  step(Tr{}, F{}, F{}, Tr{}, i + 7, aring3, aring0, bq3, bq2);
+  const int ma = (wk.rows + 31) >> 5;
+  if constexpr (MI == 4) {
+    if (ma >= 4)
+      pipeline(std::integral_constant<int, 4>{});
+    else if (ma == 3)
+      pipeline(std::integral_constant<int, 3>{});
+    else if (ma == 2)
+      pipeline(std::integral_constant<int, 2>{});
+    else
+      pipeline(std::integral_constant<int, 1>{});
+  } else if constexpr (MI == 2) {
+    if (ma >= 2)
+      pipeline(std::integral_constant<int, 2>{});
+    else
+      pipeline(std::integral_constant<int, 1>{});
+  } else {
+    pipeline(std::integral_constant<int, MI>{});
+  }
 
   // ---- epilogue, wave w staged through A slot w
   __syncthreads();  // every wave is done with the A ring
