@@ -403,6 +403,24 @@ def bench_stack48(args) -> int:
     rcep_calls, br = _timed_layer(st, wl.exit_layer, h_text, True, wl.p, stream)
     touched = int((bd.counts.cpu() > 0).sum())
     K20 = int(st.K_trace[wl.exit_layer, 0].cpu())
+    # one SAVB gate evaluation (Eqs. 2-3) on the 512 text rows entering a
+    # candidate layer: the cost a gate-decided exit adds per candidate
+    gp = I.gate_params(d, seed=wl.seed, layer=wl.exit_layer)
+    gd = {k2: torch.from_numpy(v).cuda() for k2, v in gp.items()}
+    text_rows = x[wl.n_visual:]
+    g_p = torch.empty((4,), dtype=torch.float32, device="cuda")
+    g_f = torch.empty((4,), dtype=torch.int32, device="cuda")
+    g_ws = torch.empty((abi.moe_savb_workspace_size(wl.T - wl.n_visual, d, 512),), dtype=torch.uint8,
+                       device="cuda")
+    for _ in range(3):
+        abi.moe_savb_gate(text_rows, gd["w1"], gd["b1"], gd["w2"], gd["b2"], 0.5, g_p[:1], g_f[:1], g_ws)
+    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    g0.record(stream)
+    for _ in range(20):
+        abi.moe_savb_gate(text_rows, gd["w1"], gd["b1"], gd["w2"], gd["b2"], 0.5, g_p[:1], g_f[:1], g_ws)
+    g1.record(stream)
+    torch.cuda.synchronize()
+    gate_us = g0.elapsed_time(g1) / 20 * 1e3
     f, b = stage_flops_bytes("ffn", wl.T, d, E, m, k, touched, E)
     ffn_ms = dense_calls[2]
     roof = roofline(f, b, ffn_ms * 1e-3)
@@ -428,7 +446,8 @@ def bench_stack48(args) -> int:
         K_mean=float(np.mean(Ks)), step_ms_min=float(np.min(step_ms)),
         dense_layer_8192={n: round(v, 4) for n, v in zip(names_d, dense_calls)},
         rcep_layer_512={n: round(v, 4) for n, v in zip(names_r, rcep_calls)},
-        touched_dense=touched, K_rcep_layer_512=K20, setup_s=round(setup_s, 1))
+        touched_dense=touched, K_rcep_layer_512=K20, savb_gate_us=round(gate_us, 2),
+        savb_gate_candidates_before_exit=len(range(0, wl.exit_layer, 4)), setup_s=round(setup_s, 1))
 
 
 def _oracle_stack_sample(st, x_np, wl):

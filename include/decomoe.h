@@ -18,6 +18,8 @@
  *   weighted combine back to token order                          moe_combine
  *     (same, plus the residual of a stack of MoE blocks)          moe_combine_residual
  *   SAVB visual-block removal from the hidden state (Sec. 3.2)   drop_visual_block
+ *   SAVB exit gate (Eqs. 2, 3) and its device-decided removal     moe_savb_gate,
+ *                                                                 drop_visual_block_if
  *   physical expert reorder by pi at load time (Algorithm 1)      moe_permute_experts
  *
  * Conventions shared by every entry point
@@ -329,6 +331,42 @@ int moe_permute_experts(const int32_t* order, int E, int d, int m, moe_dtype dty
  */
 int drop_visual_block(const void* h, moe_dtype dtype, int S, int d, int v0, int v1,
                       void* out, hipStream_t stream);
+
+/*
+ * moe_savb_gate - the SAVB visual-exit gate at one candidate layer
+ * (Sec. 3.2, Eqs. 2 and 3).
+ *
+ *   text_rows  [n, d] (dtype): the incoming hidden states of the n text
+ *              tokens, contiguous (e.g. h + t0 * d for text rows [t0, t0+n)).
+ *   x          = [mean of text rows 0 .. n-2; text row n-1] (width 2d;
+ *              n == 1: the mean part is zero), formed in float32.
+ *   w1 [hid, 2d], b1 [hid] or NULL, w2 [2, hid], b2 [2] or NULL: float32
+ *              weights of the two-class MLP g(x) = W2 relu(W1 x + b1) + b2
+ *              (the hidden activation is a reading: the paper gives the
+ *              layer sizes only).
+ *   feature    [2d] float32 output x, or NULL.
+ *   p_exit     [1] float32: softmax(g(x))_1, class 1 being the exit class.
+ *   exit_flag  [1] int32: 1 if p_exit >= theta (compared in float64), else 0.
+ * Every sum has a fixed order (deterministic).  Needs ws of
+ * moe_savb_workspace_size(n, d, hid) bytes.  Limits: n >= 1, 1 <= d <= 8192,
+ * hid >= 1, theta not NaN.  Device pointers; nothing is read back on the host.
+ */
+size_t moe_savb_workspace_size(int n, int d, int hid);
+int moe_savb_gate(const void* text_rows, moe_dtype dtype, int n, int d, const float* w1,
+                  const float* b1, int hid, const float* w2, const float* b2, double theta,
+                  float* feature, float* p_exit, int32_t* exit_flag, void* ws, size_t ws_bytes,
+                  hipStream_t stream);
+
+/*
+ * drop_visual_block_if - drop_visual_block decided on the device: the rows
+ * outside [v0, v1) are written to `out` when *exit_flag != 0 (the gate
+ * triggered); otherwise nothing is written.  exit_flag is a device int32
+ * (moe_savb_gate's output), read by the kernel; the host never waits for it.
+ * Same limits and errors as drop_visual_block; out must not overlap h or the
+ * flag.
+ */
+int drop_visual_block_if(const void* h, moe_dtype dtype, int S, int d, int v0, int v1,
+                         const int32_t* exit_flag, void* out, hipStream_t stream);
 
 #ifdef __cplusplus
 }

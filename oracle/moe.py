@@ -53,6 +53,8 @@ __all__ = [
     "moe_layer_dense",
     "moe_layer_rcep",
     "moe_stack",
+    "savb_gate_feature",
+    "savb_gate",
     "segment_of_tokens",
 ]
 
@@ -407,3 +409,39 @@ def moe_stack(h, layers, k, p, exit_layer=None, v0=0, v1=0, seg_offsets=None):
             Ks.append(None)
         h = h + r["out"]
     return h, Ks
+
+
+# --------------------------------------------------------------------------
+# SAVB exit gate (Sec. 3.2, Eqs. 2 and 3)
+# --------------------------------------------------------------------------
+def savb_gate_feature(text_rows):
+    """Gate feature of Eq. 2: x = [mean of the first n - 1 text states;
+    the final text state], width 2d.
+
+    READING: with a single text token (n = 1) the mean over no rows is the
+    zero vector.
+    """
+    t = np.asarray(text_rows, F64)
+    n, d = t.shape
+    if n < 1:
+        raise ValueError("need at least one text row")
+    pooled = t[:n - 1].sum(axis=0) / (n - 1) if n > 1 else np.zeros(d, F64)
+    return np.concatenate([pooled, t[n - 1]])
+
+
+def savb_gate(text_rows, w1, b1, w2, b2, theta):
+    """Exit probability and decision of Eq. 3: p_exit = softmax(g(x))_1,
+    Exit = 1[p_exit >= theta], for the two-class MLP
+    g(x) = W2 act(W1 x + b1) + b2 (hidden width of W1's rows; App. A.3
+    counts its two products).
+
+    READING: the hidden activation is ReLU (the paper names the layer sizes,
+    not the activation); class 1 is the exit class.
+    Returns (p_exit, exit, x, z).
+    """
+    x = savb_gate_feature(text_rows)
+    hid = np.maximum(np.asarray(w1, F64) @ x + np.asarray(b1, F64), 0.0)
+    z = np.asarray(w2, F64) @ hid + np.asarray(b2, F64)
+    q = softmax(z[None, :])[0]
+    p_exit = float(q[1])
+    return p_exit, bool(p_exit >= theta), x, z

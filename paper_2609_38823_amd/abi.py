@@ -25,7 +25,8 @@ STATUS = {0: "MOE_OK", -1: "MOE_EINVAL", -2: "MOE_EALIAS", -3: "MOE_EWORKSPACE",
 EXPORTS = ("moe_status_string", "moe_workspace_size", "moe_route", "moe_route_packed",
            "moe_pack_router", "moe_calibrate_prefix",
            "moe_dispatch", "moe_expert_ffn", "moe_expert_ffn_packed", "moe_pack_expert_weights",
-           "moe_combine", "moe_combine_residual", "drop_visual_block", "moe_permute_experts")
+           "moe_combine", "moe_combine_residual", "drop_visual_block", "moe_permute_experts",
+           "moe_savb_workspace_size", "moe_savb_gate", "drop_visual_block_if")
 
 
 class MoeError(RuntimeError):
@@ -61,6 +62,9 @@ def load() -> ctypes.CDLL:
         "moe_combine_residual": (_I, [_P, _I, _P, _P, _I, _I, _I, _P, _P, _P]),
         "moe_permute_experts": (_I, [_P, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
         "drop_visual_block": (_I, [_P, _I, _I, _I, _I, _I, _P, _P]),
+        "moe_savb_workspace_size": (_S, [_I, _I, _I]),
+        "moe_savb_gate": (_I, [_P, _I, _I, _I, _P, _P, _I, _P, _P, _D, _P, _P, _P, _P, _S, _P]),
+        "drop_visual_block_if": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -236,3 +240,22 @@ def moe_permute_experts(order, w_r=None, bias=None, w_gate_up=None, w_down=None,
     _check("moe_permute_experts", load().moe_permute_experts(
         _p(order), E, d or 1, m or 1, dt, _p(w_r), _p(bias), _p(w_gate_up), _p(w_down),
         _p(w_r_out), _p(bias_out), _p(w_gate_up_out), _p(w_down_out), _stream(stream)))
+
+
+def moe_savb_workspace_size(n: int, d: int, hid: int) -> int:
+    return int(load().moe_savb_workspace_size(n, d, hid))
+
+
+def moe_savb_gate(text_rows, w1, b1, w2, b2, theta, p_exit, exit_flag, ws, feature=None, stream=None):
+    """text_rows [n, d] (bf16 or float32); w1 [hid, 2d]; w2 [2, hid]."""
+    n, d = text_rows.shape
+    hid = w1.shape[0]
+    _check("moe_savb_gate", load().moe_savb_gate(
+        _p(text_rows), _dt(text_rows), n, d, _p(w1), _p(b1), hid, _p(w2), _p(b2), float(theta),
+        _p(feature), _p(p_exit), _p(exit_flag), _p(ws), _nbytes(ws), _stream(stream)))
+
+
+def drop_visual_block_if(h, v0, v1, exit_flag, out, stream=None):
+    S, d = h.shape
+    _check("drop_visual_block_if", load().drop_visual_block_if(
+        _p(h), _dt(h), S, d, v0, v1, _p(exit_flag), _p(out), _stream(stream)))

@@ -332,6 +332,46 @@ int moe_permute_experts(const int32_t* order, int E, int d, int m, moe_dtype dty
   return hip_status(e);
 }
 
+size_t moe_savb_workspace_size(int n, int d, int hid) {
+  if (n < 1 || d < 1 || hid < 1) return 0;
+  return a256(decomoe::savb_ws_bytes(n, d, hid));
+}
+
+int moe_savb_gate(const void* text_rows, moe_dtype dtype, int n, int d, const float* w1,
+                  const float* b1, int hid, const float* w2, const float* b2, double theta,
+                  float* feature, float* p_exit, int32_t* exit_flag, void* ws, size_t ws_bytes,
+                  hipStream_t stream) {
+  if (!valid_dtype(dtype) || n < 1 || d < 1 || d > 8192 || hid < 1) return MOE_EINVAL;
+  if (!(theta == theta)) return MOE_EINVAL;  // NaN
+  if (!text_rows || !w1 || !w2 || !p_exit || !exit_flag || !ws) return MOE_EINVAL;
+  if (!aligned_all({text_rows, w1, b1, w2, b2, feature, p_exit, exit_flag, ws})) return MOE_EINVAL;
+  const size_t need = decomoe::savb_ws_bytes(n, d, hid);
+  if (ws_bytes < need) return MOE_EWORKSPACE;
+  const Range o_f = feature ? rng(feature, (size_t)2 * d * 4) : Range{0, 0};
+  if (any_alias({o_f, rng(p_exit, 4), rng(exit_flag, 4), rng(ws, need)},
+                {rng(text_rows, (size_t)n * d * elt_size(dtype)), rng(w1, (size_t)hid * 2 * d * 4),
+                 b1 ? rng(b1, (size_t)hid * 4) : Range{0, 0}, rng(w2, (size_t)2 * hid * 4),
+                 b2 ? rng(b2, 8) : Range{0, 0}}))
+    return MOE_EALIAS;
+  return hip_status(decomoe::launch_savb_gate(text_rows, dtype == MOE_BF16, n, d, w1, b1, hid, w2, b2,
+                                              theta, feature, p_exit, exit_flag, ws, stream));
+}
+
+int drop_visual_block_if(const void* h, moe_dtype dtype, int S, int d, int v0, int v1,
+                         const int32_t* exit_flag, void* out, hipStream_t stream) {
+  if (!valid_dtype(dtype) || S < 0 || d < 1) return MOE_EINVAL;
+  if (!(0 <= v0 && v0 <= v1 && v1 <= S)) return MOE_EINVAL;
+  if (!exit_flag || (reinterpret_cast<uintptr_t>(exit_flag) & 3)) return MOE_EINVAL;
+  const int rows_out = S - (v1 - v0);
+  if (rows_out == 0) return MOE_OK;
+  if (!h || !out) return MOE_EINVAL;
+  const int es = elt_size(dtype);
+  if ((reinterpret_cast<uintptr_t>(h) | reinterpret_cast<uintptr_t>(out)) % es) return MOE_EINVAL;
+  if (overlap(rng(out, (size_t)rows_out * d * es), rng(h, (size_t)S * d * es))) return MOE_EALIAS;
+  if (overlap(rng(out, (size_t)rows_out * d * es), rng(exit_flag, 4))) return MOE_EALIAS;
+  return hip_status(decomoe::launch_drop_rows_if(h, es, S, d, v0, v1, exit_flag, out, stream));
+}
+
 int drop_visual_block(const void* h, moe_dtype dtype, int S, int d, int v0, int v1, void* out,
                       hipStream_t stream) {
   if (!valid_dtype(dtype) || S < 0 || d < 1) return MOE_EINVAL;

@@ -75,5 +75,13 @@ hipError_t launch_permute_columns(const float* in, const int32_t* order, int row
                                   float* out, hipStream_t s);
 hipError_t launch_drop_rows(const void* h, int elt, int S, int d, int v0, int v1, void* out,
                             hipStream_t s);
+// SAVB gate (Eqs. 2, 3) over n contiguous text rows, and the flag-driven drop
+size_t savb_ws_bytes(int n, int d, int hid);
+hipError_t launch_savb_gate(const void* rows, bool bf16, int n, int d, const float* w1,
+                            const float* b1, int hid, const float* w2, const float* b2, double theta,
+                            float* feature, float* p_exit, int32_t* exit_flag, void* ws,
+                            hipStream_t s);
+hipError_t launch_drop_rows_if(const void* h, int elt, int S, int d, int v0, int v1,
+                               const int32_t* flag, void* out, hipStream_t s);
 
 }  // namespace decomoe

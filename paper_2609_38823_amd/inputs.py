@@ -28,7 +28,7 @@ from dataclasses import dataclass, field
 import numpy as np
 
 # stream roles (first element of the spawn key)
-_S_TOKENS, _S_PARAMS, _S_CALIB, _S_DECODE = 0, 1, 2, 3
+_S_TOKENS, _S_PARAMS, _S_CALIB, _S_DECODE, _S_GATE = 0, 1, 2, 3, 4
 # parameter sub-streams
 _P_WR, _P_BIAS, _P_GU, _P_DOWN = 0, 1, 2, 3
 
@@ -177,6 +177,15 @@ def device_expert_weights(shape: LayerShape, seed: int = 0, layer: int = 0, devi
         out.append(w.to(dt) if dt != torch.float32 else w)
         del w
     return tuple(out)
+
+
+def gate_params(d: int, hid: int = 512, seed: int = 0, layer: int = 0, std: float = 0.02) -> dict:
+    """Random SAVB gate weights of one candidate layer: the two-class MLP
+    2d -> hid -> 2 with w1 [hid, 2d], b1 [hid], w2 [2, hid], b2 [2], all
+    N(0, std^2) in float32."""
+    rng = _rng(seed, _S_GATE, layer)
+    return dict(w1=_normal(rng, (hid, 2 * d), std), b1=_normal(rng, (hid,), std),
+                w2=_normal(rng, (2, hid), std), b2=_normal(rng, (2,), std))
 
 
 def router_params(shape: LayerShape, seed: int = 0, layer: int = 0) -> dict:

@@ -9,6 +9,9 @@ Prefill (the 48-layer stack over 7680 visual + 512 text rows):
 Decode (64 single text tokens): the RCEP span in every layer, captured once
 as a HIP graph and replayed per step.
 
+Gated prefill (``forward_gated``): the SAVB gate (Eqs. 2-3) runs at
+candidate layers and its device flag decides the exit layer.
+
 The residual connection is folded into each layer's combine
 (moe_combine_residual), so a layer is route -> [calibrate -> re-route] ->
 dispatch -> expert FFN -> combine+residual, all in libdecomoe.so, with K
@@ -114,6 +117,46 @@ class MoEStack:
             self.layer_forward(l, src, dst, rcep, p, stream=stream)
             src = dst
         return src
+
+    def forward_gated(self, x: torch.Tensor, n_visual: int, p: float, gates: dict, theta: float,
+                      stream=None):
+        """Algorithm 2 with the SAVB gate choosing the exit (Sec. 3.2).
+
+        Before each candidate layer l (the keys of ``gates``: per layer a
+        dict of device tensors w1, b1, w2, b2) while the visual block is
+        still present, moe_savb_gate evaluates Eqs. 2-3 on the text rows.
+        Its flag is read on the host once per candidate -- the only host
+        wait, since it fixes the row count of the layers that follow; on an
+        exit, drop_visual_block_if removes the visual rows and layers l..
+        run the RCEP span.  Returns (final rows, exit layer or None,
+        [(layer, p_exit)] of the evaluated candidates).
+        """
+        T = x.shape[0]
+        src = x
+        h = self.hidden(T)
+        d = self.sh.d
+        n_text = T - n_visual
+        hid = next(iter(gates.values()))["w1"].shape[0] if gates else 1
+        p_dev = torch.empty((4,), dtype=torch.float32, device=self.device)
+        flag = torch.empty((4,), dtype=torch.int32, device=self.device)
+        ws = torch.empty((abi.moe_savb_workspace_size(max(n_text, 1), d, hid),), dtype=torch.uint8,
+                         device=self.device)
+        exit_layer, trace = None, []
+        for l in range(self.L):
+            if exit_layer is None and l in gates and n_visual > 0 and n_text > 0:
+                g = gates[l]
+                abi.moe_savb_gate(src[n_visual:], g["w1"], g["b1"], g["w2"], g["b2"], theta, p_dev[:1],
+                                  flag[:1], ws, stream=stream)
+                fired = int(flag[0].item())  # host wait: the next layers' row count
+                trace.append((l, float(p_dev[0].item())))
+                if fired:
+                    ht = self.hidden(n_text, "text")
+                    abi.drop_visual_block_if(src, 0, n_visual, flag[:1], ht, stream=stream)
+                    src, h, exit_layer = ht, ht, l
+            dst = h if src is x else src
+            self.layer_forward(l, src, dst, exit_layer is not None, p, stream=stream)
+            src = dst
+        return src, exit_layer, trace
 
     def capture_decode(self, x: torch.Tensor, p: float):
         """Capture one decode step (RCEP in every layer) over the static

@@ -31,8 +31,8 @@ def test_header_declares_the_boundary():
     assert declared_functions() == sorted([
         "drop_visual_block", "moe_calibrate_prefix", "moe_combine", "moe_combine_residual",
         "moe_dispatch", "moe_expert_ffn", "moe_expert_ffn_packed", "moe_pack_expert_weights",
-        "moe_pack_router", "moe_permute_experts", "moe_route", "moe_route_packed", "moe_status_string",
-        "moe_workspace_size"])
+        "moe_pack_router", "moe_permute_experts", "moe_route", "moe_route_packed", "moe_savb_gate",
+        "moe_savb_workspace_size", "moe_status_string", "moe_workspace_size", "drop_visual_block_if"])
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -213,6 +213,27 @@ def test_packed_router_rejects(lib):
     assert lib.moe_pack_router(NULL, 64, 32, P2, NULL) == EINVAL
     # the workspace covers the packed router's split partials
     assert lib.moe_workspace_size(64, 128, 8, 2048, 768, 1) >= 8 * 64 * 128 * 4
+
+
+def test_savb_gate_rejects(lib):
+    lib.moe_savb_workspace_size.restype = ctypes.c_size_t
+    assert lib.moe_savb_workspace_size(512, 2048, 512) >= 16 * 2048 * 4 + 512 * 4
+    assert lib.moe_savb_workspace_size(0, 2048, 512) == 0
+    th = ctypes.c_double(0.5)
+    nan = ctypes.c_double(float("nan"))
+    big = ctypes.c_size_t(1 << 30)
+    # n = 0, d > 8192, NaN theta, no workspace
+    assert lib.moe_savb_gate(P1, BF16, 0, 64, P2, NULL, 16, P3, NULL, th, NULL, P4, P5, WS, big, NULL) == EINVAL
+    assert lib.moe_savb_gate(P1, BF16, 4, 9000, P2, NULL, 16, P3, NULL, th, NULL, P4, P5, WS, big, NULL) == EINVAL
+    assert lib.moe_savb_gate(P1, BF16, 4, 64, P2, NULL, 16, P3, NULL, nan, NULL, P4, P5, WS, big, NULL) == EINVAL
+    assert lib.moe_savb_gate(P1, BF16, 40, 64, P2, NULL, 16, P3, NULL, th, NULL, P4, P5, WS,
+                             ctypes.c_size_t(16), NULL) == EWORKSPACE
+    # the flag written over the weights
+    assert lib.moe_savb_gate(P1, BF16, 4, 64, P2, NULL, 16, P3, NULL, th, NULL, P4, P2, WS, big, NULL) == EALIAS
+    # drop_visual_block_if: misaligned flag, output over the flag
+    assert lib.drop_visual_block_if(P1, BF16, 10, 64, 0, 4, ctypes.c_void_p(P3.value + 2), P2, NULL) == EINVAL
+    assert lib.drop_visual_block_if(P1, BF16, 10, 64, 0, 4, P2, P2, NULL) == EALIAS
+    assert lib.drop_visual_block_if(P1, BF16, 10, 64, 5, 4, P3, P2, NULL) == EINVAL
 
 
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):

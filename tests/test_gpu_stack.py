@@ -208,6 +208,43 @@ def test_tiny_stack_f32_teacher_forced_and_free_running():
     assert rel_inf(final, ref) <= TOL["f32"]
 
 
+def test_tiny_stack_gated_exit():
+    """SAVB gate at candidate layers 1..5 of the tiny stack: every evaluated
+    p_exit matches the oracle's gate on the GPU's text rows entering that
+    layer (teacher-forced), the stack exits at the first candidate whose
+    p_exit reaches theta, and the result equals the fixed-exit stack at
+    that layer bit for bit."""
+    wl = I.WORKLOADS["tiny_stack_f32"]
+    sh = wl.shape
+    st = MoEStack(wl)
+    x_np = I.tokens(sh, wl.T, seed=wl.seed)
+    x = torch.from_numpy(x_np).cuda()
+    gp = {l: I.gate_params(sh.d, seed=wl.seed, layer=l, std=0.1) for l in range(1, st.L)}
+    gates = {l: {k: torch.from_numpy(v).cuda() for k, v in g.items()} for l, g in gp.items()}
+    # pass 1: theta above 1 never exits; it records p_exit at every candidate
+    _, ex0, trace0 = st.forward_gated(x, wl.n_visual, wl.p, gates, 2.0)
+    assert ex0 is None and [l for l, _ in trace0] == list(range(1, st.L))
+    # the rows entering each candidate layer, from the ungated (all dense) run
+    h = x
+    for l in range(st.L):
+        if l in gp:
+            text = host(h)[wl.n_visual:]
+            p_ref, _, _, _ = oracle.savb_gate(text, gp[l]["w1"], gp[l]["b1"], gp[l]["w2"], gp[l]["b2"], 0.5)
+            assert abs(dict(trace0)[l] - p_ref) <= 1e-5
+        dst = torch.empty_like(h)
+        st.layer_forward(l, h, dst, False, wl.p)
+        h = dst
+    # pass 2: theta = the largest p_exit seen -> exit at its first candidate
+    ps = [pv for _, pv in trace0]
+    theta = max(ps)
+    expect = trace0[ps.index(theta)][0]
+    out, ex, trace = st.forward_gated(x, wl.n_visual, wl.p, gates, theta)
+    assert ex == expect and trace[-1][0] == expect
+    got = host(out).copy()  # the stack reuses its buffers
+    ref = st.forward(x, wl.n_visual, wl.p, expect)
+    np.testing.assert_array_equal(got, host(ref))
+
+
 @pytest.fixture(scope="module")
 def stack48():
     wl = I.WORKLOADS["qwen3vl_stack48_8192"]
