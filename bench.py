@@ -30,9 +30,14 @@ Other workloads (one JSON line each, same fields):
                        value = decode tokens/s
   --workload stress    routing, dispatch and combine of the same layer at
                        65536 rows (bandwidth shape); value = rows/s
+  --workload variants  synthetic analogs of the component ablation (dense,
+                       visual exit only, fixed exit at 28, fixed prefix of
+                       50, full) on the 48-layer stack, expert orders at
+                       keep ratios and the p sweep; value = speedup of the
+                       full method over the dense stack
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
-                       [--workload layer|stack48|decode64|stress]
+                       [--workload layer|stack48|decode64|stress|variants]
 """
 
 from __future__ import annotations
@@ -140,14 +145,15 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--traffic-run", action="store_true",
                     help="only run the dense layer and a known-size copy (for rocprofv3 counter passes)")
-    ap.add_argument("--workload", default="layer", choices=["layer", "stack48", "decode64", "stress"])
+    ap.add_argument("--workload", default="layer",
+                    choices=["layer", "stack48", "decode64", "stress", "variants"])
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the path has no multi-GPU execution "
               "(the design notes describe how it would shard); run with --gpus 1", file=sys.stderr)
         return 2
     fn = {"layer": bench_layer, "stack48": bench_stack48, "decode64": bench_decode64,
-          "stress": bench_stress}[args.workload]
+          "stress": bench_stress, "variants": bench_variants}[args.workload]
     return fn(args)
 
 
@@ -243,6 +249,31 @@ def bench_layer(args) -> int:
 
     touched_512 = int((bx.counts.cpu() > 0).sum())
 
+    # the paper's dense-equivalent executor on the RCEP span (App. A.3): every
+    # text token through all K retained experts, weights applied afterwards
+    from paper_2609_38823_amd.layer import Buffers as _B
+    Tt = T - V
+    bq = _B(Tt, d, E, m, E, torch.bfloat16)
+    idx_d = torch.empty((Tt, E), dtype=torch.int32, device="cuda")
+    w_d = torch.empty((Tt, E), dtype=torch.float32, device="cuda")
+
+    def dense_equiv():
+        abi.moe_expand_dense_routing(br.idx, br.w, E, idx_d, w_d, K_dev=br.K)
+        abi.moe_dispatch(idx_d, E, h_text, bq.counts, bq.offsets, bq.src_of_row, bq.row_of_slot,
+                         bq.x_perm, bq.ws)
+        abi.moe_expert_ffn_packed(bq.x_perm, bq.offsets, layer.w_gate_up, layer.w_down, bq.y_perm, bq.ws,
+                                  K_dev=br.K)
+        abi.moe_combine(bq.y_perm, bq.row_of_slot, w_d, bq.out)
+
+    for _ in range(args.warmup):
+        dense_equiv()
+    e0.record(stream)
+    for _ in range(args.steps):
+        dense_equiv()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    dense_equiv_ms = e0.elapsed_time(e1) / args.steps
+
     def fb(stage, T_, touched, K_=E):
         return stage_flops_bytes(stage, T_, d, E, m, k, touched, K_)
 
@@ -264,6 +295,11 @@ def bench_layer(args) -> int:
         "rcep@512": dict(ms=round(rcep_ms, 4), tokens_per_s=(T - V) / rcep_ms * 1e3,
                          tflops=per_tok_flops * (T - V) / rcep_ms / 1e9, K=K, touched_experts=touched_r,
                          paper_dense_equiv_tflops=(2 * d * E + 6 * K * d * m) * (T - V) / rcep_ms / 1e9),
+        "rcep@512 experts, dense-equivalent executor": dict(
+            ms=round(dense_equiv_ms, 4), K=K, expert_gflop=6 * K * d * m * (T - V) / 1e9,
+            sparse_expert_ms=round(stage_ms["r.dispatch"] + stage_ms["r.ffn"] + stage_ms["r.combine"], 4),
+            note="expand + dispatch (k = E) + expert FFN over experts [0, K) + combine; the RCEP "
+                 "span's sparse dispatch/FFN/combine for comparison"),
         "dense@512": dict(ms=round(dense512_ms, 4), tokens_per_s=(T - V) / dense512_ms * 1e3,
                           tflops=per_tok_flops * (T - V) / dense512_ms / 1e9, touched_experts=touched_512,
                           paper_dense_equiv_tflops=(2 * d * E + 6 * E * d * m) * (T - V) / dense512_ms / 1e9),
@@ -634,6 +670,120 @@ def bench_stress(args) -> int:
         {"workload": "Qwen3-VL-MoE MoE layer shape (d 2048, 128 experts, top-8, bf16, fp32 router) at "
                      "65536 rows: moe_route_packed (full pool), moe_dispatch, moe_combine (no expert FFN)",
          "seed": 1}, roof, None, stages=rep)
+
+
+def bench_variants(args) -> int:
+    """Component ablation analogs on the stack, expert-order analysis at
+    keep ratios and the p sweep (one JSON line)."""
+    import torch
+
+    from paper_2609_38823_amd import abi, inputs as I
+    from paper_2609_38823_amd.layer import MoELayer, apply_order, calibrate_order_router, to_device
+    _setup_gpu()
+    stream = torch.cuda.current_stream()
+    wl = I.WORKLOADS["qwen3vl_stack48_8192"]
+    sh = wl.shape
+    d, E, m, k = sh.d, sh.E, sh.m, sh.k
+    st, setup_s = _build_stack(wl)
+    x_np = I.tokens(sh, wl.T, seed=wl.seed)
+    x = torch.from_numpy(x_np).cuda().to(torch.bfloat16)
+    Tt = wl.T - wl.n_visual
+    K50 = torch.full((4,), 50, dtype=torch.int32, device="cuda")
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            out = fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / args.steps, out
+
+    variants = {
+        "dense (no exit, all experts)": dict(exit_layer=None),
+        "visual exit only (exit 20, all experts)": dict(exit_layer=20, after_exit="dense"),
+        "fixed exit at 28 + RCEP": dict(exit_layer=28),
+        "exit 20 + fixed prefix of 50": dict(exit_layer=20, after_exit="fixed", K_fixed=K50),
+        "exit 20 + RCEP (full)": dict(exit_layer=20),
+    }
+    rows = {}
+    ref_text = None
+    wbytes = 3 * d * m * 2
+    for name, kw in variants.items():
+        ms, out = timed(lambda: st.forward(x, wl.n_visual, wl.p, **kw))
+        final = out.float()
+        text = final[wl.n_visual:] if final.shape[0] == wl.T else final
+        text = text.cpu().numpy().astype(np.float64)
+        if ref_text is None:
+            ref_text = text
+        ex = kw.get("exit_layer")
+        Ks = st.K_trace[:, 0].cpu().numpy()
+        if ex is None:
+            touched = [E] * st.L
+        elif kw.get("after_exit") == "dense":
+            touched = [E] * st.L
+        elif kw.get("after_exit") == "fixed":
+            touched = [E] * ex + [50] * (st.L - ex)
+        else:
+            touched = [E] * ex + [int(v) for v in Ks[ex:]]
+        rows[name] = dict(ms=round(ms, 3), tokens_per_s=wl.T / ms * 1e3,
+                          mean_experts_after_exit=float(np.mean(touched[ex:])) if ex is not None else float(E),
+                          expert_weight_gb_per_step=sum(touched) * wbytes / 1e9,
+                          text_rows_rel_l2_vs_dense=float(np.linalg.norm(text - ref_text) / np.linalg.norm(ref_text)))
+    speedup = rows["dense (no exit, all experts)"]["ms"] / rows["exit 20 + RCEP (full)"]["ms"]
+
+    # p sweep over the stack (exit 20): mean K of the 28 RCEP layers
+    p_sweep = {}
+    for pv in (0.1, 0.3, 0.5, 0.7, 0.8, 0.9, 0.95, 1.0):
+        st.forward(x, wl.n_visual, pv, 20)
+        Ks = st.K_trace[20:, 0].cpu().numpy()
+        p_sweep[str(pv)] = dict(mean_K=float(Ks.mean()), min_K=int(Ks.min()), max_K=int(Ks.max()))
+
+    # expert orders at keep ratios on one layer (the Qwen layer's 512 text
+    # rows): routed mass covered by the first K experts of each order, and the
+    # layer output with that fixed prefix against the full pool
+    lw = I.WORKLOADS["qwen3vl_dense_4096"]
+    prm = I.layer_params(sh, seed=lw.seed)
+    xt_np = I.tokens(sh, lw.T, seed=lw.seed)[lw.n_visual:]
+    xt = torch.from_numpy(xt_np).cuda().to(torch.bfloat16)
+    orders = {"native": np.arange(E),
+              "random": np.random.default_rng(7).permutation(E),
+              "RCEP (Mean-Mass)": calibrate_order_router(xt, prm["w_r"], prm["bias"], k)}
+    # activated mass per native expert from the full-pool routing (device)
+    lay0 = MoELayer(prm, k, sh.dtype)
+    b0 = lay0.forward_rcep(xt, 1.0)
+    s_native = b0.mass[0].cpu().numpy()
+    dense_out = lay0.forward_dense(xt).out.float().cpu().numpy().astype(np.float64)
+    del lay0
+    torch.cuda.empty_cache()
+    keep = (0.1, 0.2, 0.3, 0.4, 0.5)
+    order_rows = {}
+    for oname, order in orders.items():
+        lay = MoELayer(apply_order(prm, order), k, sh.dtype)
+        s_o = s_native[order]
+        res = {}
+        for r in keep:
+            K = int(round(r * E))
+            Kd = torch.full((4,), K, dtype=torch.int32, device="cuda")
+            out = lay.forward_prefix(xt, Kd).out.float().cpu().numpy().astype(np.float64)
+            res[str(r)] = dict(K=K, mass_covered=float(s_o[:K].sum() / s_o.sum()),
+                               weight_mb=K * wbytes / 1e6,
+                               out_rel_l2_vs_full_pool=float(np.linalg.norm(out - dense_out) /
+                                                             np.linalg.norm(dense_out)))
+        order_rows[oname] = res
+        del lay
+        torch.cuda.empty_cache()
+
+    return _line(
+        "Synthetic component ablation: speedup of exit 20 + RCEP over the dense 48-layer stack",
+        speedup, "x", args, rows["exit 20 + RCEP (full)"]["ms"],
+        {"workload": "Qwen3-VL-MoE 48-layer MoE stack (d 2048, 128 experts x 768, top-8, bf16), 8192 "
+                     "prefill rows (7680 visual + 512 text); order analysis on one layer's 512 text rows",
+         "seed": wl.seed, "zipf_alpha": sh.zipf_alpha},
+        None, None, ablation=rows, p_sweep_stack=p_sweep, orders_at_keep_ratio=order_rows,
+        setup_s=round(setup_s, 1))
 
 
 if __name__ == "__main__":

@@ -18,6 +18,7 @@
  *   weighted combine back to token order                          moe_combine
  *     (same, plus the residual of a stack of MoE blocks)          moe_combine_residual
  *   SAVB visual-block removal from the hidden state (Sec. 3.2)   drop_visual_block
+ *   dense-equivalent routing of the paper's executor (App. A.3)   moe_expand_dense_routing
  *   SAVB exit gate (Eqs. 2, 3) and its device-decided removal     moe_savb_gate,
  *                                                                 drop_visual_block_if
  *   physical expert reorder by pi at load time (Algorithm 1)      moe_permute_experts
@@ -331,6 +332,24 @@ int moe_permute_experts(const int32_t* order, int E, int d, int m, moe_dtype dty
  */
 int drop_visual_block(const void* h, moe_dtype dtype, int S, int d, int v0, int v1,
                       void* out, hipStream_t stream);
+
+/*
+ * moe_expand_dense_routing - the routing of the paper's dense-equivalent
+ * executor (App. A.3: a dense batched product over every physically
+ * retained expert, sparse routing weights applied afterwards), for
+ * comparison with the sparse path.  With K = K_dev[0] (clamped to [0, E];
+ * NULL: K = E):
+ *   idx_dense [T, E] int32: slot j of token t is expert j if j < K, else -1
+ *                            (moe_dispatch drops it);
+ *   w_dense   [T, E] float32: the weight topk_w gave expert j for token t, or
+ *                            0 when it was not among the token's k experts.
+ * Then moe_dispatch (k = E) -> moe_expert_ffn -> moe_combine (k = E)
+ * evaluates every token on experts [0, K): the same output as the sparse
+ * path in exact arithmetic, at K/k times its expert FLOPs.  No workspace.
+ */
+int moe_expand_dense_routing(const int32_t* topk_idx, const float* topk_w, int T, int k, int E,
+                             const int32_t* K_dev, int32_t* idx_dense, float* w_dense,
+                             hipStream_t stream);
 
 /*
  * moe_savb_gate - the SAVB visual-exit gate at one candidate layer

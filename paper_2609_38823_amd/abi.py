@@ -26,7 +26,8 @@ EXPORTS = ("moe_status_string", "moe_workspace_size", "moe_route", "moe_route_pa
            "moe_pack_router", "moe_calibrate_prefix",
            "moe_dispatch", "moe_expert_ffn", "moe_expert_ffn_packed", "moe_pack_expert_weights",
            "moe_combine", "moe_combine_residual", "drop_visual_block", "moe_permute_experts",
-           "moe_savb_workspace_size", "moe_savb_gate", "drop_visual_block_if")
+           "moe_savb_workspace_size", "moe_savb_gate", "drop_visual_block_if",
+           "moe_expand_dense_routing")
 
 
 class MoeError(RuntimeError):
@@ -65,6 +66,7 @@ def load() -> ctypes.CDLL:
         "moe_savb_workspace_size": (_S, [_I, _I, _I]),
         "moe_savb_gate": (_I, [_P, _I, _I, _I, _P, _P, _I, _P, _P, _D, _P, _P, _P, _P, _S, _P]),
         "drop_visual_block_if": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P]),
+        "moe_expand_dense_routing": (_I, [_P, _P, _I, _I, _I, _P, _P, _P, _P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -259,3 +261,9 @@ def drop_visual_block_if(h, v0, v1, exit_flag, out, stream=None):
     S, d = h.shape
     _check("drop_visual_block_if", load().drop_visual_block_if(
         _p(h), _dt(h), S, d, v0, v1, _p(exit_flag), _p(out), _stream(stream)))
+
+
+def moe_expand_dense_routing(topk_idx, topk_w, E, idx_dense, w_dense, K_dev=None, stream=None):
+    T, k = topk_idx.shape
+    _check("moe_expand_dense_routing", load().moe_expand_dense_routing(
+        _p(topk_idx), _p(topk_w), T, k, E, _p(K_dev), _p(idx_dense), _p(w_dense), _stream(stream)))

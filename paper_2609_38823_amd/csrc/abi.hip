@@ -332,6 +332,21 @@ int moe_permute_experts(const int32_t* order, int E, int d, int m, moe_dtype dty
   return hip_status(e);
 }
 
+int moe_expand_dense_routing(const int32_t* topk_idx, const float* topk_w, int T, int k, int E,
+                             const int32_t* K_dev, int32_t* idx_dense, float* w_dense,
+                             hipStream_t stream) {
+  if (T < 0 || k < 1 || E < 1 || E > kMaxE) return MOE_EINVAL;
+  if (T == 0) return MOE_OK;
+  if (!topk_idx || !topk_w || !idx_dense || !w_dense) return MOE_EINVAL;
+  if (!aligned_all({topk_idx, topk_w, K_dev, idx_dense, w_dense})) return MOE_EINVAL;
+  const size_t nk = (size_t)T * k * 4, ne = (size_t)T * E * 4;
+  if (any_alias({rng(idx_dense, ne), rng(w_dense, ne)},
+                {rng(topk_idx, nk), rng(topk_w, nk), K_dev ? rng(K_dev, 4) : Range{0, 0}}))
+    return MOE_EALIAS;
+  return hip_status(decomoe::launch_expand_dense(topk_idx, topk_w, T, k, E, K_dev, idx_dense, w_dense,
+                                                 stream));
+}
+
 size_t moe_savb_workspace_size(int n, int d, int hid) {
   if (n < 1 || d < 1 || hid < 1) return 0;
   return a256(decomoe::savb_ws_bytes(n, d, hid));

@@ -57,6 +57,8 @@ size_t dispatch_ws_bytes(int T, int k, int E);
 hipError_t launch_dispatch(const int32_t* idx, int T, int k, int E, const void* x, int elt, int d,
                            int32_t* counts, int32_t* offsets, int32_t* src_of_row,
                            int32_t* row_of_slot, void* x_perm, void* ws, hipStream_t s);
+hipError_t launch_expand_dense(const int32_t* idx, const float* w, int T, int k, int E,
+                               const int32_t* K_dev, int32_t* idx_dense, float* w_dense, hipStream_t s);
 size_t ffn_ws_bytes(bool bf16, int rows_max, int E, int d, int m);
 hipError_t launch_expert_ffn(const void* x_perm, bool bf16, const int32_t* offsets, int E,
                              const int32_t* K_dev, int n_K, int rows_max, int d, int m,

@@ -268,6 +268,27 @@ __global__ __launch_bounds__(256) void dispatch_gather_kernel(const VEC* __restr
     }
   }
 }
+
+// Dense-equivalent routing (App. A.3, the convention of a dense batched
+// product over every retained expert): slot j of token t is expert j for
+// j < K (else dropped, -1), weighted by the routing weight the sparse
+// routing gave expert j (0 when it was not selected).
+__global__ __launch_bounds__(256) void expand_dense_kernel(const int32_t* __restrict__ idx,
+                                                           const float* __restrict__ w, int T, int k,
+                                                           int E, const int32_t* __restrict__ K_dev,
+                                                           int32_t* __restrict__ idx_dense,
+                                                           float* __restrict__ w_dense) {
+  const size_t n = (size_t)T * E;
+  const int K = K_dev ? clampi(K_dev[0], 0, E) : E;
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) {
+    const int t = (int)(i / E), j = (int)(i % E);
+    float wj = 0.f;
+    for (int s = 0; s < k; ++s)
+      if (idx[(size_t)t * k + s] == j) wj += w[(size_t)t * k + s];
+    idx_dense[i] = j < K ? j : -1;
+    w_dense[i] = wj;
+  }
+}
 }  // namespace
 
 size_t dispatch_ws_bytes(int T, int k, int E) {
@@ -321,6 +342,16 @@ hipError_t launch_dispatch(const int32_t* idx, int T, int k, int E, const void* 
     dispatch_gather_kernel<uint16_t><<<(T + rpb - 1) / rpb, 256, 0, s>>>(
         static_cast<const uint16_t*>(x), T, k, chunks, rpb, row_of_slot, static_cast<uint16_t*>(x_perm));
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_expand_dense(const int32_t* idx, const float* w, int T, int k, int E,
+                               const int32_t* K_dev, int32_t* idx_dense, float* w_dense, hipStream_t s) {
+  const size_t n = (size_t)T * E;
+  if (n == 0) return hipSuccess;
+  size_t blocks = (n + 255) / 256;
+  if (blocks > 16384) blocks = 16384;
+  expand_dense_kernel<<<(unsigned)blocks, 256, 0, s>>>(idx, w, T, k, E, K_dev, idx_dense, w_dense);
   return hipGetLastError();
 }
 

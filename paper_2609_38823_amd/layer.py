@@ -193,6 +193,23 @@ class MoELayer:
         self._experts(x, b, b.idx, b.w, stream=stream, mark=mark, residual=residual, out=out)
         return b
 
+    def forward_prefix(self, x: torch.Tensor, K_dev: torch.Tensor, b: Buffers | None = None,
+                       stream=None, mark=None, residual=None, out=None) -> Buffers:
+        """A given prefix length instead of Eq. 12 (the fixed-prefix variant
+        of the component ablation): logits over all E experts, Top-k inside
+        [0, K_dev[0]), experts [0, K) only."""
+        b = b or self.buffers(x.shape[0])
+        if self.w_r_packed is not None:
+            abi.moe_route_packed(x, self.w_r_packed, self.bias, self.k, b.logits, b.idx, b.w, K_dev=K_dev,
+                                 ws=b.ws, stream=stream)
+        else:
+            abi.moe_route(x, self.w_r, self.bias, self.k, b.logits, b.idx, b.w, K_dev=K_dev, ws=b.ws,
+                          stream=stream)
+        if mark:
+            mark()
+        self._experts(x, b, b.idx, b.w, K_dev=K_dev, stream=stream, mark=mark, residual=residual, out=out)
+        return b
+
     def forward_rcep(self, x: torch.Tensor, p: float, seg_offsets=None, b: Buffers | None = None,
                      stream=None, mark=None, residual=None, out=None, K_out=None) -> Buffers:
         """Prefix-restricted layer (from the visual exit on, Algorithm 2).

@@ -83,17 +83,22 @@ class MoEStack:
         return self._h[key]
 
     def layer_forward(self, l: int, src: torch.Tensor, dst: torch.Tensor, rcep: bool, p: float,
-                      stream=None, mark=None) -> Buffers:
-        """One block: dst = src + MoE_l(src); dst may be src (in place)."""
+                      stream=None, mark=None, K_fixed: torch.Tensor | None = None) -> Buffers:
+        """One block: dst = src + MoE_l(src); dst may be src (in place).
+        rcep: the RCEP span (Eq. 12's K, or K_fixed when given); else the
+        full expert pool."""
         b = self.buffers(src.shape[0])
         layer = self.layers[l]
+        if rcep and K_fixed is not None:
+            return layer.forward_prefix(src, K_fixed, b=b, stream=stream, mark=mark, residual=src, out=dst)
         if rcep:
             return layer.forward_rcep(src, p, b=b, stream=stream, mark=mark, residual=src, out=dst,
                                       K_out=self.K_trace[l, :1])
         return layer.forward_dense(src, b=b, stream=stream, mark=mark, residual=src, out=dst)
 
     def forward(self, x: torch.Tensor, n_visual: int, p: float, exit_layer: int | None,
-                stream=None, hook=None) -> torch.Tensor:
+                stream=None, hook=None, after_exit: str = "rcep", K_fixed: torch.Tensor | None = None
+                ) -> torch.Tensor:
         """Run the stack over x [T, d] (visual rows [0, n_visual) first).
 
         exit_layer is the first text-only layer: the visual rows are removed
@@ -101,6 +106,9 @@ class MoEStack:
         None runs every layer dense.  x itself is not modified.  Returns the
         final hidden rows (a buffer owned by the stack).  ``hook(l, src)``,
         if given, is called before layer l with its input rows.
+        after_exit selects the layers from the exit on (component ablation):
+        "rcep" (Eq. 12), "dense" (all experts: the visual exit alone) or
+        "fixed" (the prefix length K_fixed[0]).
         """
         T = x.shape[0]
         src = x
@@ -112,9 +120,10 @@ class MoEStack:
                 src, h = ht, ht
             if hook:
                 hook(l, src)
-            rcep = exit_layer is not None and l >= exit_layer
+            rcep = exit_layer is not None and l >= exit_layer and after_exit != "dense"
             dst = h if src is x else src
-            self.layer_forward(l, src, dst, rcep, p, stream=stream)
+            self.layer_forward(l, src, dst, rcep, p, stream=stream,
+                               K_fixed=K_fixed if after_exit == "fixed" else None)
             src = dst
         return src
 

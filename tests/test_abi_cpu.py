@@ -32,7 +32,8 @@ def test_header_declares_the_boundary():
         "drop_visual_block", "moe_calibrate_prefix", "moe_combine", "moe_combine_residual",
         "moe_dispatch", "moe_expert_ffn", "moe_expert_ffn_packed", "moe_pack_expert_weights",
         "moe_pack_router", "moe_permute_experts", "moe_route", "moe_route_packed", "moe_savb_gate",
-        "moe_savb_workspace_size", "moe_status_string", "moe_workspace_size", "drop_visual_block_if"])
+        "moe_savb_workspace_size", "moe_status_string", "moe_workspace_size", "drop_visual_block_if",
+        "moe_expand_dense_routing"])
 
 
 def test_every_declared_symbol_is_exported(lib):

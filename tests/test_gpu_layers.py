@@ -198,3 +198,40 @@ def test_decode_64_layer():
     x = I.tokens(sh, wl.T, seed=wl.seed, stream="decode")
     xd = torch.from_numpy(x).cuda().to(torch.bfloat16)
     check_rcep(layer, rp, x, xd, sh.k, wl.p, "bf16")
+
+
+def test_dense_equivalent_executor_matches_sparse(qwen):
+    """The paper's dense-equivalent execution (App. A.3): every text token
+    through all K retained experts with the sparse routing weights applied
+    afterwards (zero for unselected experts) gives the sparse layer's
+    output; each retained expert gets every token."""
+    wl, x, rp, layer = qwen
+    sh = wl.shape
+    text = x[wl.n_visual:]
+    T, E = text.shape[0], sh.E
+    xd = torch.from_numpy(text).cuda().to(torch.bfloat16)
+    b = layer.forward_rcep(xd, 0.9)
+    out_sparse = host(b.out).copy()
+    K = int(host(b.K)[0])
+    idx_d = torch.empty((T, E), dtype=torch.int32, device="cuda")
+    w_d = torch.empty((T, E), dtype=torch.float32, device="cuda")
+    abi.moe_expand_dense_routing(b.idx, b.w, E, idx_d, w_d, K_dev=b.K)
+    gi, gw = host(idx_d), host(w_d)
+    slots = np.arange(E)[None, :].repeat(T, axis=0)
+    np.testing.assert_array_equal(gi, np.where(slots < K, slots, -1))
+    ref_w = np.zeros((T, E), np.float32)
+    np.put_along_axis(ref_w, host(b.idx).astype(np.int64), host(b.w), axis=1)
+    np.testing.assert_array_equal(gw, ref_w)
+    from paper_2609_38823_amd.layer import Buffers
+    bd = Buffers(T, sh.d, E, sh.m, E, torch.bfloat16)
+    abi.moe_dispatch(idx_d, E, xd, bd.counts, bd.offsets, bd.src_of_row, bd.row_of_slot, bd.x_perm, bd.ws)
+    counts = host(bd.counts)
+    assert (counts[:K] == T).all() and (counts[K:] == 0).all()
+    abi.moe_expert_ffn_packed(bd.x_perm, bd.offsets, layer.w_gate_up, layer.w_down, bd.y_perm, bd.ws,
+                              K_dev=b.K)
+    abi.moe_combine(bd.y_perm, bd.row_of_slot, w_d, bd.out)
+    out_dense = host(bd.out)
+    assert rel_inf(out_dense, out_sparse) <= 2e-2
+    # the same eight products per element, summed in another order: within
+    # a few bf16 units of the sparse result
+    assert np.abs(out_dense - out_sparse).max() <= 4 * 2.0 ** -8 * np.abs(out_sparse).max()
