@@ -465,10 +465,15 @@ __global__ __launch_bounds__(256) void pack_weights_kernel(const uint4* __restri
 // holds 8 chunks of 16 bytes, chunk c stored at c ^ ((row >> 1) & 7): the
 // 16 rows read by one quarter-wavefront hit 16 distinct bank groups.
 //
-// Waits: before a new A stage is read, each wavefront reads one word of
-// its own part of that stage (the compiler then waits exactly for that
-// transfer), then all wavefronts meet at a barrier.  The weight registers
-// are waited for by the compiler where the MFMAs use them.
+// Waits: the compiler waits for the weight registers where the MFMAs use
+// them, but not for global -> LDS transfers, so every read of an A stage
+// must follow a wait that covers this wavefront's transfers of that stage,
+// and then a barrier (covering every wavefront's part).  In the loop the
+// weight wait does it: the vector-memory counter completes in issue order,
+// and stage j's transfers (issued at the end of k-step 2j - 7) precede the
+// weights of k-step 2j - 1 (issued at its top, three steps earlier), whose
+// MFMAs wait for them before the barrier that ends k-step 2j - 1.  Before
+// stage 0 nothing has waited yet: the prologue waits explicitly.
 // ---------------------------------------------------------------------------
 constexpr int AK = 64;  // k-values per A stage
 
@@ -530,12 +535,6 @@ __global__ __launch_bounds__(NTHR, packed_occupancy<BM>()) void ffn_gemm_packed_
   auto issue_a = [&](char* stage, int js) {
 #pragma unroll
     for (int q = 0; q < AGW; ++q) dma16(a_rs, stage + (wv + 4 * q) * 1024, a_voff[q], js * AK * 2);
-  };
-  // one word of this wavefront's first transfer of a stage: reading it makes
-  // the compiler wait for this wavefront's transfers into that stage
-  auto own_word = [&](const char* stage) {
-    const int v = *reinterpret_cast<const int*>(stage + wv * 1024 + lane * 4);
-    asm volatile("" ::"v"(v));
   };
 
   // ---- B: this wavefront's NI 32-row blocks of the expert's packed matrix
@@ -620,7 +619,8 @@ __global__ __launch_bounds__(NTHR, packed_occupancy<BM>()) void ffn_gemm_packed_
       interleave();
       if constexpr (!decltype(LAST)::value) {
         if constexpr (odd) {
-          own_word(nxt);
+          // nxt's transfers are complete (see the waits above): the weight
+          // wait of this k-step's first MFMAs covered them
           __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): reads of `cur` are complete
           __builtin_amdgcn_s_barrier();
           __builtin_amdgcn_sched_barrier(0);
@@ -656,7 +656,9 @@ __global__ __launch_bounds__(NTHR, packed_occupancy<BM>()) void ffn_gemm_packed_
     load_b(bq1, 1);
     load_b(bq2, 2);
     __builtin_amdgcn_sched_barrier(0);
-    own_word(aring0);
+    // stage 0 complete: its transfers precede the 3 AGW transfers of stages
+    // 1..3 and the 6 NI weight loads of k-steps 0..2
+    wait_vmcnt<3 * AGW + 6 * NI>();
     __builtin_amdgcn_s_barrier();
     load_a(aring0, 0, a0);
     int i = 0;

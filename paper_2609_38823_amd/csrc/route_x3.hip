@@ -43,6 +43,14 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_
 __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, void* lds, int voff, int soff) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, lds, 16, voff, soff, 0, 0);
 }
+// wait until at most N vector-memory operations of this wavefront are
+// outstanding (gfx9 encoding: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] |
+// vmcnt_hi[15:14])
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
 
 // one thread per (expert block, k block, lane): 8 weights, three fragments
 __global__ __launch_bounds__(256) void pack_router_kernel(const float* __restrict__ w_r, int d, int E,
@@ -114,10 +122,6 @@ __global__ __launch_bounds__(256, 2) void router_x3_kernel(const uint16_t* __res
 #pragma unroll
     for (int q = 0; q < MI; ++q) dma16(x_rs, slot + (wv + 4 * q) * 1024, x_voff[q], st * XS_K * 2);
   };
-  auto own_word = [&](int st) {
-    const int v = *reinterpret_cast<const int*>(ring + (st & 3) * SLOT + wv * 1024 + lane * 4);
-    asm volatile("" ::"v"(v));
-  };
   const int r32 = lane & 31, kh = lane >> 5;
   int x_lane[4];
 #pragma unroll
@@ -140,12 +144,16 @@ __global__ __launch_bounds__(256, 2) void router_x3_kernel(const uint16_t* __res
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[i][e] = 0.f;
 
-  // stage st: wait for its token rows (own transfer, then every wavefront),
-  // refill the slot freed by stage st - 1 with stage st + 3 (ISSUE_X), load
-  // the weights of stage st + 1 (LOAD_W), then 4 x 3 MI MFMAs.  The flags
-  // are compile-time so that the compiler's waits count exactly.
+  // stage st: barrier (every wavefront's token rows of the stage are in
+  // LDS), refill the slot freed by stage st - 1 with stage st + 3
+  // (ISSUE_X), load the weights of stage st + 1 (LOAD_W), then 4 x 3 MI
+  // MFMAs.  The flags are compile-time so that the compiler's waits count
+  // exactly.  The compiler waits for the weight registers, not for global ->
+  // LDS transfers; the vector-memory counter completes in issue order, and
+  // stage st's transfers precede the weights of stage st - 1, which the
+  // MFMAs of stage st - 1 waited for before this barrier.  Stage 0 waits
+  // explicitly (below).
   auto stage = [&](auto ISSUE_X, auto LOAD_W, int st, const u32x4 (&wc)[4][3], u32x4 (&wn)[4][3]) {
-    own_word(st);
     __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's reads of the previous stage
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
@@ -170,15 +178,15 @@ __global__ __launch_bounds__(256, 2) void router_x3_kernel(const uint16_t* __res
   using Tr = std::integral_constant<bool, true>;
 
   u32x4 wA[4][3], wB[4][3];
-  if (n_st >= 3) {
-    issue_x(0);
-    issue_x(1);
-    issue_x(2);
-  } else {
-    issue_x(0);
-    if (n_st == 2) issue_x(1);
-  }
+  // three stages always (past the split's end the loads stay inside the
+  // buffer or read zeros at its end, into slots no stage reads), so that the
+  // wait for stage 0 counts exactly: 2 MI transfers and 12 weight loads
+  // follow it
+  issue_x(0);
+  issue_x(1);
+  issue_x(2);
   load_w(wA, 0);
+  wait_vm<2 * MI + 12>();
   int st = 0;
   for (; st + 4 < n_st; st += 2) {  // every refill and load in range
     stage(Tr{}, Tr{}, st, wA, wB);
@@ -205,6 +213,7 @@ __global__ __launch_bounds__(256, 2) void router_x3_kernel(const uint16_t* __res
       break;
   }
 
+  wait_vm<0>();                // transfers of stages past the split's end
   if (eb_raw >= n_eb) return;  // no barrier follows
   // lane l: token t0 + l % 32 (+ 32 mi), experts 32 eb + 8 g + 4 (l / 32) + 0..3
 #pragma unroll
