@@ -484,16 +484,20 @@ constexpr int a_slot() {
   constexpr int a = BM * AK * 2, e = 32 * ((BN / 4) * 2 + 16);
   return ((a > e ? a : e) + 1023) & ~1023;
 }
-// workgroups per CU: 128-row tiles need the register file of two; 64-row
-// tiles fit three (LDS: 3 x 32 KB)
+// weight-register ring depth: 4 stages (three k-steps ahead) for 128-row
+// tiles; 64-row tiles (few rows per expert: weight streaming) run 8 stages,
+// seven k-steps ahead, to keep more weight bytes in flight
 template <int BM>
-constexpr int packed_occupancy() { return BM >= 128 ? 2 : 3; }
+constexpr int packed_nb() { return BM >= 128 ? 4 : 8; }
+// workgroups per CU: the register file holds two of either kind
+template <int BM>
+constexpr int packed_occupancy() { return 2; }
 
 __device__ __forceinline__ u32x4 load_frag(__amdgpu_buffer_rsrc_t rs, int voff, int soff) {
   return __builtin_amdgcn_raw_buffer_load_b128(rs, voff, soff, 0);
 }
 
-template <int MODE, int BM, int BN>
+template <int MODE, int BM, int BN, int NB = packed_nb<BM>()>
 __global__ __launch_bounds__(NTHR, packed_occupancy<BM>()) void ffn_gemm_packed_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ Wp, uint16_t* __restrict__ C,
     const Tiles tl, int d, int m) {
@@ -576,7 +580,9 @@ __global__ __launch_bounds__(NTHR, packed_occupancy<BM>()) void ffn_gemm_packed_
   // rows (a tile's last item of an expert is often short): blocks past them
   // would only multiply padding, so their fragment reads and MFMAs are left
   // out (their accumulators stay zero and their rows are not stored).
-  u32x4 bq0[2][NI], bq1[2][NI], bq2[2][NI], bq3[2][NI];
+  static_assert(NB == 4 || NB == 8, "weight ring of 4 or 8 stages");
+  constexpr int LA = NB - 1;  // weight lookahead in k-steps
+  u32x4 bq[NB][2][NI];
   auto pipeline = [&](auto MAC) {
     constexpr int MA = decltype(MAC)::value;
     auto load_a = [&](const char* stage, int s4, bf16x8 (&af)[MI]) {
@@ -608,19 +614,25 @@ __global__ __launch_bounds__(NTHR, packed_occupancy<BM>()) void ffn_gemm_packed_
     //   ISSUE_B      load the weights of k-step i + 3
     //   LAST         the final k-step (nothing follows)
     bf16x8 a0[MI], a1[MI];
-    auto step = [&](auto ODD, auto ISSUE_A, auto ISSUE_B, auto LAST, int i, char* cur, char* nxt,
-                    const u32x4 (&bc)[2][NI], u32x4 (&bn)[2][NI]) {
+    // WAIT (8-stage ring only): at the barrier of an odd k-step, at most WAIT
+    // younger vector-memory operations may be outstanding -- exactly the
+    // ones issued after the transfers of the stage read next (see below)
+    auto step = [&](auto ODD, auto ISSUE_A, auto ISSUE_B, auto LAST, auto WAIT, int i, char* cur,
+                    char* nxt, const u32x4 (&bc)[2][NI], u32x4 (&bn)[2][NI]) {
       constexpr bool odd = decltype(ODD)::value;
       // the weight registers of k-step i - 1 are free: refill them first
-      if constexpr (decltype(ISSUE_B)::value) load_b(bn, i + 3);
+      if constexpr (decltype(ISSUE_B)::value) load_b(bn, i + LA);
       __builtin_amdgcn_sched_barrier(0);
       load_a(cur, odd ? 3 : 1, a1);
       mma(a0, bc[0]);
       interleave();
       if constexpr (!decltype(LAST)::value) {
         if constexpr (odd) {
-          // nxt's transfers are complete (see the waits above): the weight
-          // wait of this k-step's first MFMAs covered them
+          // nxt's transfers are complete (see the waits above): with 4
+          // weight stages the weight wait of this k-step's first MFMAs
+          // covered them; with 8 the weights of k-step i were issued before
+          // them, so the wait is explicit
+          if constexpr (NB == 8) wait_vmcnt<decltype(WAIT)::value>();
           __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): reads of `cur` are complete
           __builtin_amdgcn_s_barrier();
           __builtin_amdgcn_sched_barrier(0);
@@ -635,16 +647,21 @@ __global__ __launch_bounds__(NTHR, packed_occupancy<BM>()) void ffn_gemm_packed_
     using F = std::integral_constant<bool, false>;
     using Tr = std::integral_constant<bool, true>;
 
-    // body of 8 k-steps = 4 A stages in slots 0..3; every issue active
+    // body of 8 k-steps = 4 A stages in slots 0..3; every issue active.
+    // k-step i reads weight slot i % NB and refills slot (i - 1) % NB with
+    // k-step i + LA.  Stage j's transfers leave at the end of k-step 2j - 7;
+    // by the barrier of k-step 2j - 1 the loads issued after them are the
+    // weights of six k-steps and the transfers of two stages.
+    using WB = std::integral_constant<int, 12 * NI + 2 * AGW>;
     auto body = [&](int i) {
-      step(F{}, F{}, Tr{}, F{}, i + 0, aring0, aring0, bq0, bq3);
-      step(Tr{}, Tr{}, Tr{}, F{}, i + 1, aring0, aring1, bq1, bq0);
-      step(F{}, F{}, Tr{}, F{}, i + 2, aring1, aring1, bq2, bq1);
-      step(Tr{}, Tr{}, Tr{}, F{}, i + 3, aring1, aring2, bq3, bq2);
-      step(F{}, F{}, Tr{}, F{}, i + 4, aring2, aring2, bq0, bq3);
-      step(Tr{}, Tr{}, Tr{}, F{}, i + 5, aring2, aring3, bq1, bq0);
-      step(F{}, F{}, Tr{}, F{}, i + 6, aring3, aring3, bq2, bq1);
-      step(Tr{}, Tr{}, Tr{}, F{}, i + 7, aring3, aring0, bq3, bq2);
+      step(F{}, F{}, Tr{}, F{}, WB{}, i + 0, aring0, aring0, bq[0 % NB], bq[(NB - 1) % NB]);
+      step(Tr{}, Tr{}, Tr{}, F{}, WB{}, i + 1, aring0, aring1, bq[1 % NB], bq[0 % NB]);
+      step(F{}, F{}, Tr{}, F{}, WB{}, i + 2, aring1, aring1, bq[2 % NB], bq[1 % NB]);
+      step(Tr{}, Tr{}, Tr{}, F{}, WB{}, i + 3, aring1, aring2, bq[3 % NB], bq[2 % NB]);
+      step(F{}, F{}, Tr{}, F{}, WB{}, i + 4, aring2, aring2, bq[4 % NB], bq[3 % NB]);
+      step(Tr{}, Tr{}, Tr{}, F{}, WB{}, i + 5, aring2, aring3, bq[5 % NB], bq[4 % NB]);
+      step(F{}, F{}, Tr{}, F{}, WB{}, i + 6, aring3, aring3, bq[6 % NB], bq[5 % NB]);
+      step(Tr{}, Tr{}, Tr{}, F{}, WB{}, i + 7, aring3, aring0, bq[7 % NB], bq[6 % NB]);
     };
 
     issue_a(aring0, 0);
@@ -652,26 +669,38 @@ __global__ __launch_bounds__(NTHR, packed_occupancy<BM>()) void ffn_gemm_packed_
     issue_a(aring2, 2);
     issue_a(aring3, 3);
     __builtin_amdgcn_sched_barrier(0);
-    load_b(bq0, 0);
-    load_b(bq1, 1);
-    load_b(bq2, 2);
+#pragma unroll
+    for (int q = 0; q < LA; ++q) load_b(bq[q], q);
     __builtin_amdgcn_sched_barrier(0);
     // stage 0 complete: its transfers precede the 3 AGW transfers of stages
-    // 1..3 and the 6 NI weight loads of k-steps 0..2
-    wait_vmcnt<3 * AGW + 6 * NI>();
+    // 1..3 and the 2 NI LA weight loads of k-steps 0..LA-1
+    wait_vmcnt<3 * AGW + 2 * NI * LA>();
     __builtin_amdgcn_s_barrier();
     load_a(aring0, 0, a0);
     int i = 0;
     for (; i + 8 < nk; i += 8) body(i);
-    // last 8 k-steps: no A refills; weights up to k-step nk - 1
-    step(F{}, F{}, Tr{}, F{}, i + 0, aring0, aring0, bq0, bq3);
-    step(Tr{}, F{}, Tr{}, F{}, i + 1, aring0, aring1, bq1, bq0);
-    step(F{}, F{}, Tr{}, F{}, i + 2, aring1, aring1, bq2, bq1);
-    step(Tr{}, F{}, Tr{}, F{}, i + 3, aring1, aring2, bq3, bq2);
-    step(F{}, F{}, Tr{}, F{}, i + 4, aring2, aring2, bq0, bq3);
-    step(Tr{}, F{}, F{}, F{}, i + 5, aring2, aring3, bq1, bq0);
-    step(F{}, F{}, F{}, F{}, i + 6, aring3, aring3, bq2, bq1);
-    step(Tr{}, F{}, F{}, Tr{}, i + 7, aring3, aring0, bq3, bq2);
+    // last 8 k-steps: no A refills; weights up to k-step nk - 1 (tail step t
+    // loads while t + LA <= 7).  With 8 weight stages only t = 0 loads, and
+    // the odd tail barriers wait for stages issued in the body: after them
+    // come 10 NI + 2 AGW, 6 NI + AGW and 2 NI operations (t = 1, 3, 5);
+    // when the body did not run (nk = 8) more follow, so these bounds still
+    // suffice
+    constexpr bool B1 = 1 + LA <= 7, B2 = 2 + LA <= 7, B3 = 3 + LA <= 7, B4 = 4 + LA <= 7;
+    using T1 = std::integral_constant<int, 10 * NI + 2 * AGW>;
+    using T3 = std::integral_constant<int, 6 * NI + AGW>;
+    using T5 = std::integral_constant<int, 2 * NI>;
+    using BC1 = std::integral_constant<bool, B1>;
+    using BC2 = std::integral_constant<bool, B2>;
+    using BC3 = std::integral_constant<bool, B3>;
+    using BC4 = std::integral_constant<bool, B4>;
+    step(F{}, F{}, Tr{}, F{}, WB{}, i + 0, aring0, aring0, bq[0 % NB], bq[(NB - 1) % NB]);
+    step(Tr{}, F{}, BC1{}, F{}, T1{}, i + 1, aring0, aring1, bq[1 % NB], bq[0 % NB]);
+    step(F{}, F{}, BC2{}, F{}, WB{}, i + 2, aring1, aring1, bq[2 % NB], bq[1 % NB]);
+    step(Tr{}, F{}, BC3{}, F{}, T3{}, i + 3, aring1, aring2, bq[3 % NB], bq[2 % NB]);
+    step(F{}, F{}, BC4{}, F{}, WB{}, i + 4, aring2, aring2, bq[4 % NB], bq[3 % NB]);
+    step(Tr{}, F{}, F{}, F{}, T5{}, i + 5, aring2, aring3, bq[5 % NB], bq[4 % NB]);
+    step(F{}, F{}, F{}, F{}, WB{}, i + 6, aring3, aring3, bq[6 % NB], bq[5 % NB]);
+    step(Tr{}, F{}, F{}, Tr{}, WB{}, i + 7, aring3, aring0, bq[7 % NB], bq[6 % NB]);
   };
   const int ma = (wk.rows + 31) >> 5;
   if constexpr (MI == 4) {
