@@ -482,8 +482,34 @@ def bench_stack48(args) -> int:
         K_mean=float(np.mean(Ks)), step_ms_min=float(np.min(step_ms)),
         dense_layer_8192={n: round(v, 4) for n, v in zip(names_d, dense_calls)},
         rcep_layer_512={n: round(v, 4) for n, v in zip(names_r, rcep_calls)},
+        paper_flops_replay=paper_prefill_flops(wl.T, wl.T - wl.n_visual, wl.exit_layer, Ks, wl.layers, E, d, m,
+                                               n_gate=len(range(0, wl.exit_layer, 4)) + 1),
         touched_dense=touched, K_rcep_layer_512=K20, savb_gate_us=round(gate_us, 2),
         savb_gate_candidates_before_exit=len(range(0, wl.exit_layer, 4)), setup_s=round(setup_s, 1))
+
+
+def paper_prefill_flops(S: int, T: int, exit_layer: int, Ks, L: int, E: int, d: int, m: int,
+                        q: int = 4096, kv: int = 512, n_gate: int = 0, gate_hidden: int = 512) -> dict:
+    """The paper's decoder FLOPs replay for one prefill (App. A.3,
+    Eqs. 13-15 and the SAVB MLP term), with its dense-equivalent expert
+    convention C_expert(K) = 6 K d m: layers before the exit at (S, E), from
+    the exit on at (T, K_l); the baseline runs every layer at (S, E).  The
+    attention projection sizes q and kv are the paper's Qwen3-VL-MoE values;
+    the attention itself is not part of this build, only of this replay."""
+    c_proj = 2 * (d * q + 2 * d * kv + q * d)
+    c_router = 2 * d * E
+
+    def layer(n, K):
+        return n * c_proj + 2 * q * n * (n + 1) + n * (c_router + 6 * K * d * m)
+
+    base = L * layer(S, E)
+    method = exit_layer * layer(S, E) + sum(layer(T, int(K)) for K in Ks)
+    gate = n_gate * (2 * (2 * d) * gate_hidden + 2 * gate_hidden * 2)
+    total = method + gate
+    return dict(baseline_tflop=base / 1e12, decomoe_tflop=total / 1e12, gate_tflop=gate / 1e12,
+                saving=1.0 - total / base, q=q, kv=kv,
+                convention="paper's replay: dense-equivalent experts (6 K d m per token), attention "
+                           "terms included, one prefill, exit at the given layer")
 
 
 def _oracle_stack_sample(st, x_np, wl):

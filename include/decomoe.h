@@ -170,8 +170,10 @@ int moe_route_packed(const void* x, moe_dtype dtype, const void* w_r_packed, con
  *                     mean, equal means keeping the lower index first.
  *                     order[j] is the expert placed at position j.  With no
  *                     non-empty segment the order is the identity.
- * A token's experts are distinct in moe_route output; an expert repeated
- * within a token enters as the sum of its weights (summed in unspecified
+ * A token's experts are distinct in moe_route output.  An expert repeated
+ * within a token: in segments of up to 8192 entries (with E <= 512) its
+ * weights are added one by one in slot order, like distinct experts; in
+ * larger segments they are first summed within the token (in unspecified
  * order when it repeats three times or more).
  * Each segment's masses are one float64 running sum per expert in ascending
  * token order, and c_K one running sum in expert order, so K depends on the

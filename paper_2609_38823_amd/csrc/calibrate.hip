@@ -1,14 +1,16 @@
 // Activated mass, prefix length and Mean-Mass order (Eqs. 8, 9, 11, 12).
 //
 //   mass     one workgroup per invocation (segment) stages the routing
-//            entries of up to 8192 / k tokens with one bulk load, then walks
-//            them in chunks: the chunk's routed weights are scattered into a dense
-//            LDS table [token][expert] (float64), then thread e adds column
-//            e to its running sum in ascending token order and clears it --
-//            one float64 running sum per expert over the tokens, the same
-//            sequence of additions as the plain definition (zeros of
-//            unrouted tokens add nothing).  One thread then forms the running
-//            sum c_K over the experts and wave 0 finds K with a ballot.
+//            entries with one bulk load.  Up to 8192 entries (and E <= 512):
+//            a stable counting sort in LDS groups them by expert, token order
+//            kept, and thread e adds its expert's weights in that order.
+//            Larger segments are walked in chunks: the chunk's weights are
+//            scattered into a dense LDS table [token][expert] (float64) and
+//            thread e adds column e in ascending token order.  Either way one
+//            float64 running sum per expert over the tokens: the sequence of
+//            additions of the plain definition (unrouted tokens add zeros,
+//            which change nothing).  One thread then forms the running sum
+//            c_K over the experts and wave 0 finds K with a ballot.
 //   order    Mean-Mass order over the segments taken as calibration cases
 #include "common.hpp"
 
@@ -29,21 +31,110 @@ __host__ __device__ inline int cal_chunk(int E, int k) {
   return c < 64 ? c : 64;
 }
 
+constexpr int CAL_WAVES = CAL_THREADS / kWave;
+constexpr int CAL_SORT_E = 512;  // the sorted path keeps [waves][E] counts in half the table
+
 __global__ __launch_bounds__(CAL_THREADS) void segment_mass_kernel(
-    const int32_t* __restrict__ idx, const float* __restrict__ w, int T, int E, int k,
+    const int32_t* __restrict__ idx, const float* __restrict__ w, int T, int E, int k, int key_bits,
     const int32_t* __restrict__ seg_offsets, double p, double* __restrict__ mass,
     int32_t* __restrict__ K_out) {
   __shared__ double table[CAL_TABLE];
   __shared__ double smass[1024];
   __shared__ int st_e[CAL_STAGE];
   __shared__ float st_w[CAL_STAGE];
+  __shared__ int s_cnt[1024], s_off[1024];
+  __shared__ int part[CAL_WAVES];
   const int seg = blockIdx.x;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   int lo = 0, hi = T;
   if (seg_offsets) {
     lo = clampi(seg_offsets[seg], 0, T);
     hi = clampi(seg_offsets[seg + 1], lo, T);
   }
+  const int n_all = (hi - lo) * k;
+  if (n_all <= CAL_STAGE && E <= CAL_SORT_E) {
+    // ---- sorted path: the segment's entries are grouped by expert with a
+    // stable counting sort in LDS (token order kept within an expert), then
+    // thread e adds its expert's weights in that order -- the sequence of
+    // float64 additions of the definition minus the additions of zero
+    int* wh = reinterpret_cast<int*>(table);                      // [waves][E]
+    float* sorted = reinterpret_cast<float*>(table) + CAL_WAVES * CAL_SORT_E;  // [CAL_STAGE]
+    {
+      constexpr int SPT = CAL_STAGE / CAL_THREADS;
+      int re[SPT];
+      float rw[SPT];
+#pragma unroll
+      for (int q = 0; q < SPT; ++q) {
+        const int i = tid + q * CAL_THREADS;
+        re[q] = i < n_all ? idx[(size_t)lo * k + i] : -1;
+        rw[q] = i < n_all ? w[(size_t)lo * k + i] : 0.f;
+      }
+#pragma unroll
+      for (int q = 0; q < SPT; ++q) {
+        st_e[tid + q * CAL_THREADS] = re[q];
+        st_w[tid + q * CAL_THREADS] = rw[q];
+      }
+    }
+    for (int i = tid; i < CAL_WAVES * E; i += CAL_THREADS) wh[i] = 0;
+    __syncthreads();
+    const int per = ((n_all + CAL_WAVES - 1) / CAL_WAVES + kWave - 1) / kWave * kWave;
+    const int a_lo = min(n_all, wv * per), a_hi = min(n_all, a_lo + per);
+    for (int a = a_lo + lane; a < a_hi; a += kWave) {
+      const int e = st_e[a];
+      if (e >= 0 && e < E) atomicAdd(&wh[wv * E + e], 1);
+    }
+    __syncthreads();
+    int cnt = 0;
+    if (tid < E)
+      for (int q = 0; q < CAL_WAVES; ++q) cnt += wh[q * E + tid];
+    int incl = cnt;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      const int y = __shfl_up(incl, off, kWave);
+      if (lane >= off) incl += y;
+    }
+    if (lane == kWave - 1) part[wv] = incl;
+    __syncthreads();
+    if (tid < E) {
+      int r = incl - cnt;
+      for (int q = 0; q < wv; ++q) r += part[q];
+      s_cnt[tid] = cnt;
+      s_off[tid] = r;
+      for (int q = 0; q < CAL_WAVES; ++q) {  // per-wave starting positions
+        const int c = wh[q * E + tid];
+        wh[q * E + tid] = r;
+        r += c;
+      }
+    }
+    __syncthreads();
+    const uint64_t lt_mask = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+    for (int a0 = a_lo; a0 < a_hi; a0 += kWave) {
+      const int a = a0 + lane;
+      const int e = a < a_hi ? st_e[a] : -1;
+      const bool valid = e >= 0 && e < E;
+      uint64_t peers = __ballot(valid);
+      for (int b = 0; b < key_bits; ++b) {
+        const bool bit = (e >> b) & 1;
+        const uint64_t msk = __ballot(bit);
+        peers &= bit ? msk : ~msk;
+      }
+      if (valid) {
+        sorted[wh[wv * E + e] + __popcll(peers & lt_mask)] = st_w[a];
+        if ((63 - __clzll(peers)) == lane) wh[wv * E + e] += __popcll(peers);
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+    __syncthreads();
+    if (tid < E) {
+      double a = 0.0;
+      const int b0 = s_off[tid], b1 = b0 + s_cnt[tid];
+#pragma unroll 8
+      for (int j = b0; j < b1; ++j) a += static_cast<double>(sorted[j]);
+      mass[(size_t)seg * E + tid] = a;
+      smass[tid] = a;
+    }
+    __syncthreads();
+  } else {
   const int ch = cal_chunk(E, k);
   const int super_t = (CAL_STAGE / k) / ch * ch;  // tokens staged per bulk load
   for (int i = tid; i < ch * E; i += CAL_THREADS) table[i] = 0.0;
@@ -103,6 +194,7 @@ __global__ __launch_bounds__(CAL_THREADS) void segment_mass_kernel(
     smass[tid] = acc;
   }
   __syncthreads();
+  }  // chunked path
   if (K_out) {
     // c_K: one running sum in expert order by a single thread (the same
     // sequence of float64 additions as the definition), 8 masses per batch
@@ -188,7 +280,10 @@ hipError_t launch_calibrate(const int32_t* idx, const float* w, int T, int E, in
                             const int32_t* seg_offsets, int n_seg, double p, double* mass,
                             int32_t* K_out, int32_t* order, void* ws, hipStream_t s) {
   (void)ws;
-  segment_mass_kernel<<<n_seg, CAL_THREADS, 0, s>>>(idx, w, T, E, k, seg_offsets, p, mass, K_out);
+  int key_bits = 0;
+  while ((1 << key_bits) < E) ++key_bits;
+  segment_mass_kernel<<<n_seg, CAL_THREADS, 0, s>>>(idx, w, T, E, k, key_bits, seg_offsets, p, mass,
+                                                    K_out);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess || !order) return err;
   mean_mass_order_kernel<<<1, 1024, 0, s>>>(mass, T, E, seg_offsets, n_seg, order);
