@@ -450,13 +450,19 @@ def bench_stack48(args) -> int:
                        device="cuda")
     for _ in range(3):
         abi.moe_savb_gate(text_rows, gd["w1"], gd["b1"], gd["w2"], gd["b2"], 0.5, g_p[:1], g_f[:1], g_ws)
-    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    g0.record(stream)
+    # one call at a time (as in the stack, where the flag is read after each
+    # evaluation): the GPU time of the call's four launches, host overhead
+    # excluded
+    g_t = []
     for _ in range(20):
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        g0.record(stream)
         abi.moe_savb_gate(text_rows, gd["w1"], gd["b1"], gd["w2"], gd["b2"], 0.5, g_p[:1], g_f[:1], g_ws)
-    g1.record(stream)
-    torch.cuda.synchronize()
-    gate_us = g0.elapsed_time(g1) / 20 * 1e3
+        g1.record(stream)
+        torch.cuda.synchronize()
+        g_t.append(g0.elapsed_time(g1))
+    gate_us = float(np.median(g_t)) * 1e3
     f, b = stage_flops_bytes("ffn", wl.T, d, E, m, k, touched, E)
     ffn_ms = dense_calls[2]
     roof = roofline(f, b, ffn_ms * 1e-3)

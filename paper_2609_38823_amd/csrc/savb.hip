@@ -3,9 +3,10 @@
 //
 //   pool     the n - 1 preceding text rows are summed per column in float32,
 //            rows split over blockIdx.y (each split sums its rows in order)
-//   hidden   every workgroup forms the feature x = [sum / (n - 1); row n - 1]
-//            in LDS (the splits added in order, then one division), and each
-//            wavefront one hidden unit relu(W1[u] . x + b1[u])
+//   feature  x = [sum / (n - 1); row n - 1] (the splits added in order,
+//            then one scaling), one column per thread
+//   hidden   every workgroup loads x into LDS and each wavefront forms one
+//            hidden unit relu(W1[u] . x + b1[u])
 //   decide   one workgroup: the two class logits, p_exit = softmax(z)_1 and
 //            the exit flag p_exit >= theta (compared in float64)
 // Every sum has a fixed order, so the gate is deterministic.
@@ -47,32 +48,63 @@ __global__ __launch_bounds__(256) void savb_pool_kernel(const void* __restrict__
   partial[(size_t)blockIdx.y * d + c] = acc;
 }
 
-// x in LDS, then wavefront w of block b computes hidden unit 4 b + w
+// x[c] = (sum of the splits' partials, in split order) / (n - 1) and
+// x[d + c] = text row n - 1, one column per thread; the partial loads of a
+// column are all issued before the additions
 template <bool BF16>
-__global__ __launch_bounds__(256) void savb_hidden_kernel(const void* __restrict__ rows, int n, int d,
-                                                          int splits, const float* __restrict__ partial,
+__global__ __launch_bounds__(256) void savb_feature_kernel(const void* __restrict__ rows, int n, int d,
+                                                           int splits, const float* __restrict__ partial,
+                                                           float* __restrict__ x) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= d) return;
+  float v[16];
+#pragma unroll
+  for (int q = 0; q < 16; ++q) v[q] = q < splits ? partial[(size_t)q * d + c] : 0.f;
+  float s = 0.f;
+#pragma unroll
+  for (int q = 0; q < 16; ++q)
+    if (q < splits) s += v[q];
+  x[c] = n > 1 ? s * (1.f / static_cast<float>(n - 1)) : 0.f;
+  x[d + c] = BF16 ? bf16_to_f32(static_cast<const uint16_t*>(rows)[(size_t)(n - 1) * d + c])
+                  : static_cast<const float*>(rows)[(size_t)(n - 1) * d + c];
+}
+
+// x into LDS, then wavefront w of block b computes hidden unit 4 b + w
+__global__ __launch_bounds__(256) void savb_hidden_kernel(const float* __restrict__ x, int d,
                                                           const float* __restrict__ w1,
                                                           const float* __restrict__ b1, int hid,
-                                                          float* __restrict__ hidden,
-                                                          float* __restrict__ feature) {
+                                                          float* __restrict__ hidden) {
   extern __shared__ float xs[];  // [2d]
-  const float inv = n > 1 ? 1.f / static_cast<float>(n - 1) : 0.f;
-  for (int c = threadIdx.x; c < d; c += 256) {
-    float s = 0.f;
-    for (int q = 0; q < splits; ++q) s += partial[(size_t)q * d + c];
-    xs[c] = s * inv;
-    xs[d + c] = BF16 ? bf16_to_f32(static_cast<const uint16_t*>(rows)[(size_t)(n - 1) * d + c])
-                     : static_cast<const float*>(rows)[(size_t)(n - 1) * d + c];
-  }
+  for (int c = threadIdx.x; c < 2 * d; c += 256) xs[c] = x[c];
   __syncthreads();
-  if (feature && blockIdx.x == 0)
-    for (int c = threadIdx.x; c < 2 * d; c += 256) feature[c] = xs[c];
   const int lane = threadIdx.x & 63;
   const int u = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (u >= hid) return;
   const float* wr = w1 + (size_t)u * 2 * d;
   float acc = 0.f;
-  for (int c = lane; c < 2 * d; c += 64) acc = fmaf(wr[c], xs[c], acc);
+  if ((d & 127) == 0 && (reinterpret_cast<uintptr_t>(wr) & 15) == 0) {
+    // 16-byte loads, eight in flight per lane: lane l takes columns
+    // 4 (l + 64 j) .. + 4 for j = 0, 1, ...
+    const float4* w4 = reinterpret_cast<const float4*>(wr);
+    const int n4 = (2 * d) >> 2;
+    for (int j0 = lane; j0 < n4; j0 += 64 * 8) {
+      float4 v[8];
+#pragma unroll
+      for (int u8 = 0; u8 < 8; ++u8) v[u8] = j0 + 64 * u8 < n4 ? w4[j0 + 64 * u8] : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int u8 = 0; u8 < 8; ++u8) {
+        const int c = 4 * (j0 + 64 * u8);
+        if (j0 + 64 * u8 < n4) {
+          acc = fmaf(v[u8].x, xs[c], acc);
+          acc = fmaf(v[u8].y, xs[c + 1], acc);
+          acc = fmaf(v[u8].z, xs[c + 2], acc);
+          acc = fmaf(v[u8].w, xs[c + 3], acc);
+        }
+      }
+    }
+  } else {
+    for (int c = lane; c < 2 * d; c += 64) acc = fmaf(wr[c], xs[c], acc);
+  }
   // lanes in order: the sum of lane partials is formed by lane 0
   for (int off = 32; off >= 1; off >>= 1) acc += __shfl_down(acc, off, 64);
   if (lane == 0) hidden[u] = fmaxf(acc + (b1 ? b1[u] : 0.f), 0.f);
@@ -128,7 +160,7 @@ hipError_t drop_if_launch(const void* h, int rows_out, int chunks, int v0, int n
 
 size_t savb_ws_bytes(int n, int d, int hid) {
   const int splits = savb_splits(n);
-  return ((size_t)splits * d + (size_t)hid) * sizeof(float);
+  return ((size_t)splits * d + (size_t)hid + (size_t)2 * d) * sizeof(float);
 }
 
 hipError_t launch_savb_gate(const void* rows, bool bf16, int n, int d, const float* w1,
@@ -148,13 +180,19 @@ hipError_t launch_savb_gate(const void* rows, bool bf16, int n, int d, const flo
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
+  float* x = hidden + hid;  // the feature (also the caller's copy when given)
+  if (feature) x = feature;
+  const unsigned fb = (unsigned)((d + 255) / 256);
+  if (bf16)
+    savb_feature_kernel<true><<<fb, 256, 0, s>>>(rows, n, d, splits, partial, x);
+  else
+    savb_feature_kernel<false><<<fb, 256, 0, s>>>(rows, n, d, splits, partial, x);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   const unsigned hb = (unsigned)((hid + 3) / 4);
   const size_t lds = (size_t)2 * d * sizeof(float);
-  if (bf16)
-    savb_hidden_kernel<true><<<hb, 256, lds, s>>>(rows, n, d, splits, partial, w1, b1, hid, hidden, feature);
-  else
-    savb_hidden_kernel<false><<<hb, 256, lds, s>>>(rows, n, d, splits, partial, w1, b1, hid, hidden, feature);
-  hipError_t e = hipGetLastError();
+  savb_hidden_kernel<<<hb, 256, lds, s>>>(x, d, w1, b1, hid, hidden);
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   savb_decide_kernel<<<1, 128, 0, s>>>(hidden, hid, w2, b2, theta, p_exit, exit_flag);
   return hipGetLastError();
