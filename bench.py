@@ -450,9 +450,9 @@ def bench_stack48(args) -> int:
                        device="cuda")
     for _ in range(3):
         abi.moe_savb_gate(text_rows, gd["w1"], gd["b1"], gd["w2"], gd["b2"], 0.5, g_p[:1], g_f[:1], g_ws)
-    # one call at a time (as in the stack, where the flag is read after each
-    # evaluation): the GPU time of the call's four launches, host overhead
-    # excluded
+    # one call at a time on an idle stream (as in the stack, where the flag is
+    # read after each evaluation): event time from the call's start to the
+    # end of its four launches, launch latency included
     g_t = []
     for _ in range(20):
         g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
