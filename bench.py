@@ -6,13 +6,14 @@ visual exit (Algorithm 2 of the paper), on synthetic inputs already
 resident in HBM:
 
   dense span   moe_route -> moe_dispatch -> moe_expert_ffn -> moe_combine
-               (bf16: moe_route_packed, moe_expert_ffn_packed)
+               (bf16: moe_route_packed, moe_dispatch without the row copy,
+               moe_expert_ffn_packed_gather reading the token rows itself)
                over 4096 rows (3584 visual + 512 text), all 128 experts
   SAVB exit    drop_visual_block removes the 3584 visual rows
   RCEP span    moe_route (full pool) -> moe_calibrate_prefix (K, p = 0.9)
                -> moe_route (prefix re-route) -> moe_dispatch
                -> moe_expert_ffn (experts [0, K)) -> moe_combine
-               over the 512 text rows
+               over the 512 text rows (bf16: the same packed calls)
 
 value = MoE-layer tokens per second over the step (4096 + 512 rows per
 step).  Every ABI call is bracketed by HIP events on the stream it runs on,
@@ -58,10 +59,13 @@ PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0  # MI355X HBM3E
 
 
-def stage_flops_bytes(stage: str, T: int, d: int, E: int, m: int, k: int, touched: int, K: int):
+def stage_flops_bytes(stage: str, T: int, d: int, E: int, m: int, k: int, touched: int, K: int,
+                      gather: bool = True):
     """Algorithmic FLOPs and HBM bytes of one ABI call (bf16 rows, fp32
     router and routing arrays).  Sizes per row and per expert are listed in
-    the design notes."""
+    the design notes.  With `gather` (layers on packed weights) the dispatch
+    only groups the assignments and the expert GEMM reads the token rows
+    through src_of_row; otherwise the dispatch copies them to x_perm."""
     A = T * k
     if stage == "route_full":
         return 2.0 * T * d * E, T * d * 2 + d * E * 4 + E * 4 + T * E * 4 + 2 * T * k * 4
@@ -70,9 +74,10 @@ def stage_flops_bytes(stage: str, T: int, d: int, E: int, m: int, k: int, touche
     if stage == "calibrate":
         return 0.0, 2 * T * k * 4 + E * 8 + 4
     if stage == "dispatch":
-        return 0.0, T * k * 4 + (E + 1) * 8 + 2 * A * 4 + T * d * 2 + A * d * 2
+        return 0.0, T * k * 4 + (E + 1) * 8 + 2 * A * 4 + (0 if gather else T * d * 2 + A * d * 2)
     if stage == "ffn":
-        return 6.0 * A * d * m, touched * 3 * d * m * 2 + 2 * A * d * 2 + (E + 1) * 4
+        rows_in = T * d * 2 + A * 4 if gather else A * d * 2
+        return 6.0 * A * d * m, touched * 3 * d * m * 2 + rows_in + A * d * 2 + (E + 1) * 4
     if stage == "combine":
         return 2.0 * A * d, A * d * 2 + A * 4 + A * 4 + T * d * 2
     if stage == "drop":
@@ -253,16 +258,16 @@ def bench_layer(args) -> int:
     # text token through all K retained experts, weights applied afterwards
     from paper_2609_38823_amd.layer import Buffers as _B
     Tt = T - V
-    bq = _B(Tt, d, E, m, E, torch.bfloat16)
+    bq = _B(Tt, d, E, m, E, torch.bfloat16, x_perm=False)
     idx_d = torch.empty((Tt, E), dtype=torch.int32, device="cuda")
     w_d = torch.empty((Tt, E), dtype=torch.float32, device="cuda")
 
     def dense_equiv():
         abi.moe_expand_dense_routing(br.idx, br.w, E, idx_d, w_d, K_dev=br.K)
-        abi.moe_dispatch(idx_d, E, h_text, bq.counts, bq.offsets, bq.src_of_row, bq.row_of_slot,
-                         bq.x_perm, bq.ws)
-        abi.moe_expert_ffn_packed(bq.x_perm, bq.offsets, layer.w_gate_up, layer.w_down, bq.y_perm, bq.ws,
-                                  K_dev=br.K)
+        abi.moe_dispatch(idx_d, E, None, bq.counts, bq.offsets, bq.src_of_row, bq.row_of_slot,
+                         None, bq.ws)
+        abi.moe_expert_ffn_packed_gather(h_text, E, bq.src_of_row, bq.offsets, layer.w_gate_up,
+                                         layer.w_down, bq.y_perm, bq.ws, K_dev=br.K)
         abi.moe_combine(bq.y_perm, bq.row_of_slot, w_d, bq.out)
 
     for _ in range(args.warmup):
@@ -307,8 +312,8 @@ def bench_layer(args) -> int:
     f, b = fb("ffn", T, touched_d)
     ffn_roof = roofline(f, b, stage_ms["ffn"] * 1e-3)
     ffn_roof["traffic"] = measured_traffic()
-    ffn_roof["kernel"] = ("moe_expert_ffn_packed @ dense 4096 rows (gate/up GEMM + down GEMM launches "
-                          "on packed bf16 weights)")
+    ffn_roof["kernel"] = ("moe_expert_ffn_packed_gather @ dense 4096 rows (gate/up GEMM reading the token "
+                          "rows through src_of_row + down GEMM, on packed bf16 weights)")
     ffn_roof["mfma_frac"] = f / (stage_ms["ffn"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS
 
     cpu = None
@@ -466,7 +471,7 @@ def bench_stack48(args) -> int:
     f, b = stage_flops_bytes("ffn", wl.T, d, E, m, k, touched, E)
     ffn_ms = dense_calls[2]
     roof = roofline(f, b, ffn_ms * 1e-3)
-    roof["kernel"] = "moe_expert_ffn_packed @ dense 8192 rows (layer 0 of the stack)"
+    roof["kernel"] = "moe_expert_ffn_packed_gather @ dense 8192 rows (layer 0 of the stack)"
     roof["traffic"] = None
     roof["mfma_frac"] = f / (ffn_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS
     per_tok = 2 * d * E + 6 * k * d * m
@@ -689,10 +694,10 @@ def bench_stress(args) -> int:
     ms = sum(st_ms.values())
     rep = {}
     for n in names:
-        f, nb = stage_flops_bytes(n, T, d, E, m, k, E, E)
+        f, nb = stage_flops_bytes(n, T, d, E, m, k, E, E, gather=False)
         rep[n] = dict(ms=round(st_ms[n], 4), roofline=roofline(f, nb, st_ms[n] * 1e-3),
                       gflop=round(f / 1e9, 3), mb=round(nb / 1e6, 3))
-    f, nb = stage_flops_bytes("dispatch", T, d, E, m, k, E, E)
+    f, nb = stage_flops_bytes("dispatch", T, d, E, m, k, E, E, gather=False)
     roof = roofline(f, nb, st_ms["dispatch"] * 1e-3)
     roof["kernel"] = "moe_dispatch @ 65536 rows (counting sort + row gather)"
     roof["traffic"] = None

@@ -15,6 +15,7 @@
  *   SwiGLU expert MLPs over the dispatched rows                   moe_expert_ffn
  *     (same, on weights re-laid out once at load time)            moe_expert_ffn_packed,
  *                                                                 moe_pack_expert_weights
+ *     (same, the dispatch gather folded into the GEMM)            moe_expert_ffn_packed_gather
  *   weighted combine back to token order                          moe_combine
  *     (same, plus the residual of a stack of MoE blocks)          moe_combine_residual
  *   SAVB visual-block removal from the hidden state (Sec. 3.2)   drop_visual_block
@@ -271,6 +272,29 @@ int moe_expert_ffn_packed(const void* x_perm, moe_dtype dtype, const int32_t* of
                           const int32_t* K_dev, int n_K, int rows_max, int d, int m,
                           const void* w_gate_up_packed, const void* w_down_packed,
                           void* y_perm, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * moe_expert_ffn_packed_gather - moe_expert_ffn_packed with the row gather
+ * of moe_dispatch folded into the expert GEMM (Algorithm 2: the selected
+ * experts evaluate their tokens):
+ *
+ *   x           [T, d] bf16 token rows (not dispatched).
+ *   k           slots per token (as given to moe_dispatch).
+ *   src_of_row  [T*k] int32 from moe_dispatch: dispatched row r is token
+ *               src_of_row[r] / k (an index outside [0, T) reads token 0).
+ *   offsets, K_dev, n_K, weights, y_perm, ws: as moe_expert_ffn_packed,
+ *               with rows_max = T*k.
+ * y_perm is bitwise what moe_dispatch (with x) followed by
+ * moe_expert_ffn_packed gives, but x_perm is never formed: call moe_dispatch
+ * with x = NULL.  bf16 only; d % 256 == 0 and m % 256 == 0, T*d*2 and T*k
+ * below 2^31, else MOE_EUNSUPPORTED.  y_perm and ws must not overlap any
+ * input (MOE_EALIAS).  Needs ws (moe_workspace_size).
+ */
+int moe_expert_ffn_packed_gather(const void* x, moe_dtype dtype, int T, int k,
+                                 const int32_t* src_of_row, const int32_t* offsets, int E,
+                                 const int32_t* K_dev, int n_K, int d, int m,
+                                 const void* w_gate_up_packed, const void* w_down_packed,
+                                 void* y_perm, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * moe_combine - weighted combine back to token order (Algorithm 2).

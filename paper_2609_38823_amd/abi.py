@@ -24,7 +24,8 @@ STATUS = {0: "MOE_OK", -1: "MOE_EINVAL", -2: "MOE_EALIAS", -3: "MOE_EWORKSPACE",
 
 EXPORTS = ("moe_status_string", "moe_workspace_size", "moe_route", "moe_route_packed",
            "moe_pack_router", "moe_calibrate_prefix",
-           "moe_dispatch", "moe_expert_ffn", "moe_expert_ffn_packed", "moe_pack_expert_weights",
+           "moe_dispatch", "moe_expert_ffn", "moe_expert_ffn_packed", "moe_expert_ffn_packed_gather",
+           "moe_pack_expert_weights",
            "moe_combine", "moe_combine_residual", "drop_visual_block", "moe_permute_experts",
            "moe_savb_workspace_size", "moe_savb_gate", "drop_visual_block_if",
            "moe_expand_dense_routing")
@@ -58,6 +59,8 @@ def load() -> ctypes.CDLL:
         "moe_dispatch": (_I, [_P, _I, _I, _I, _P, _I, _I, _P, _P, _P, _P, _P, _P, _S, _P]),
         "moe_expert_ffn": (_I, [_P, _I, _P, _I, _P, _I, _I, _I, _I, _P, _P, _P, _P, _S, _P]),
         "moe_expert_ffn_packed": (_I, [_P, _I, _P, _I, _P, _I, _I, _I, _I, _P, _P, _P, _P, _S, _P]),
+        "moe_expert_ffn_packed_gather": (_I, [_P, _I, _I, _I, _P, _P, _I, _P, _I, _I, _I, _P, _P, _P, _P,
+                                              _S, _P]),
         "moe_pack_expert_weights": (_I, [_P, _I, _I, _I, _I, _P, _P]),
         "moe_combine": (_I, [_P, _I, _P, _P, _I, _I, _I, _P, _P]),
         "moe_combine_residual": (_I, [_P, _I, _P, _P, _I, _I, _I, _P, _P, _P]),
@@ -190,6 +193,18 @@ def moe_expert_ffn_packed(x_perm, offsets, w_gate_up_packed, w_down_packed, y_pe
     n_K = K_dev.numel() if K_dev is not None else 0
     _check("moe_expert_ffn_packed", load().moe_expert_ffn_packed(
         _p(x_perm), _dt(x_perm), _p(offsets), E, _p(K_dev), n_K, rows_max, d, two_m // 2,
+        _p(w_gate_up_packed), _p(w_down_packed), _p(y_perm), _p(ws), ws.numel() * ws.element_size(),
+        _stream(stream)))
+
+
+def moe_expert_ffn_packed_gather(x, k, src_of_row, offsets, w_gate_up_packed, w_down_packed, y_perm,
+                                 ws, K_dev=None, stream=None):
+    """Token rows read from x through src_of_row (moe_dispatch with x=None)."""
+    T, d = x.shape
+    E, two_m, _ = w_gate_up_packed.shape
+    n_K = K_dev.numel() if K_dev is not None else 0
+    _check("moe_expert_ffn_packed_gather", load().moe_expert_ffn_packed_gather(
+        _p(x), _dt(x), T, k, _p(src_of_row), _p(offsets), E, _p(K_dev), n_K, d, two_m // 2,
         _p(w_gate_up_packed), _p(w_down_packed), _p(y_perm), _p(ws), ws.numel() * ws.element_size(),
         _stream(stream)))
 

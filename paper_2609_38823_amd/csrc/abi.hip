@@ -248,6 +248,42 @@ int moe_expert_ffn_packed(const void* x_perm, moe_dtype dtype, const int32_t* of
                     w_down_packed, true, y_perm, ws, ws_bytes, stream);
 }
 
+int moe_expert_ffn_packed_gather(const void* x, moe_dtype dtype, int T, int k,
+                                 const int32_t* src_of_row, const int32_t* offsets, int E,
+                                 const int32_t* K_dev, int n_K, int d, int m,
+                                 const void* w_gate_up_packed, const void* w_down_packed,
+                                 void* y_perm, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!valid_dtype(dtype) || T < 0 || k < 1 || E < 1 || E > kMaxE || k > E || d < 1 || m < 1)
+    return MOE_EINVAL;
+  if (dtype != MOE_BF16) return MOE_EUNSUPPORTED;
+  if (d % 256 != 0 || m % 256 != 0) return MOE_EUNSUPPORTED;
+  // token rows and dispatched rows are addressed with 32-bit offsets
+  if ((size_t)T * k > (size_t)INT32_MAX || (size_t)T * d * 2 > (size_t)INT32_MAX)
+    return MOE_EUNSUPPORTED;
+  if ((size_t)2 * m * d * 2 > (size_t)INT32_MAX) return MOE_EUNSUPPORTED;
+  if (K_dev && n_K < 1) return MOE_EINVAL;
+  if (!offsets || !w_gate_up_packed || !w_down_packed) return MOE_EINVAL;
+  const int rows_max = T * k;
+  if (rows_max > 0 && (!x || !src_of_row || !y_perm)) return MOE_EINVAL;
+  if (!aligned_all({x, src_of_row, offsets, K_dev, w_gate_up_packed, w_down_packed, y_perm, ws}))
+    return MOE_EINVAL;
+  if (rows_max == 0) return MOE_OK;
+  const size_t need = ffn_ws_bytes(true, rows_max, E, d, m);
+  if (!ws || ws_bytes < need) return MOE_EWORKSPACE;
+  Range o_y = rng(y_perm, (size_t)rows_max * d * 2);
+  Range o_ws = rng(ws, need);
+  Range in_k = K_dev ? rng(K_dev, (size_t)n_K * 4) : Range{0, 0};
+  if (any_alias({o_y, o_ws},
+                {rng(x, (size_t)T * d * 2), rng(src_of_row, (size_t)rows_max * 4),
+                 rng(offsets, (size_t)(E + 1) * 4), in_k,
+                 rng(w_gate_up_packed, (size_t)E * 2 * m * d * 2),
+                 rng(w_down_packed, (size_t)E * d * m * 2)}))
+    return MOE_EALIAS;
+  return hip_status(decomoe::launch_expert_ffn(x, true, offsets, E, K_dev, n_K, rows_max, d, m,
+                                               w_gate_up_packed, w_down_packed, true, y_perm, ws,
+                                               stream, decomoe::RowGather{src_of_row, k, T}));
+}
+
 int moe_pack_expert_weights(const void* w, moe_dtype dtype, int E, int rows, int cols,
                             void* w_packed, hipStream_t stream) {
   if (!valid_dtype(dtype) || E < 0 || rows < 0 || cols < 0) return MOE_EINVAL;

@@ -60,10 +60,17 @@ hipError_t launch_dispatch(const int32_t* idx, int T, int k, int E, const void* 
 hipError_t launch_expand_dense(const int32_t* idx, const float* w, int T, int k, int E,
                                const int32_t* K_dev, int32_t* idx_dense, float* w_dense, hipStream_t s);
 size_t ffn_ws_bytes(bool bf16, int rows_max, int E, int d, int m);
-hipError_t launch_expert_ffn(const void* x_perm, bool bf16, const int32_t* offsets, int E,
+// Token rows of the gate/up GEMM: x_perm [rows_max, d] when src_of_row is
+// NULL; else x [T, d] with dispatched row r read from x[src_of_row[r] / k]
+// (packed weights only)
+struct RowGather {
+  const int32_t* src_of_row;
+  int k, T;
+};
+hipError_t launch_expert_ffn(const void* a_rows, bool bf16, const int32_t* offsets, int E,
                              const int32_t* K_dev, int n_K, int rows_max, int d, int m,
                              const void* w_gate_up, const void* w_down, bool packed, void* y_perm,
-                             void* ws, hipStream_t s);
+                             void* ws, hipStream_t s, RowGather gather = RowGather{nullptr, 1, 0});
 hipError_t launch_pack_weights(const void* w, int E, int R, int K, void* out, hipStream_t s);
 hipError_t launch_combine(const void* y_perm, bool bf16, const int32_t* row_of_slot,
                           const float* w, int T, int k, int d, const void* residual, void* out,

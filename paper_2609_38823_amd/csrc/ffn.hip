@@ -497,10 +497,14 @@ __device__ __forceinline__ u32x4 load_frag(__amdgpu_buffer_rsrc_t rs, int voff, 
   return __builtin_amdgcn_raw_buffer_load_b128(rs, voff, soff, 0);
 }
 
+// With gather.src_of_row (gate/up only), A is the token matrix x [gather.T,
+// d] and tile row r is token src_of_row[row0 + r] / gather.k: the dispatch
+// gather happens in the token-row transfers, which take a per-lane offset
+// anyway, and x_perm is never formed.
 template <int MODE, int BM, int BN, int NB = packed_nb<BM>()>
 __global__ __launch_bounds__(NTHR, packed_occupancy<BM>()) void ffn_gemm_packed_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ Wp, uint16_t* __restrict__ C,
-    const Tiles tl, int d, int m) {
+    const Tiles tl, int d, int m, const RowGather gather) {
   constexpr int MI = BM / 32;   // 32-row token fragments (all tile rows)
   constexpr int NI = BN / 128;  // 32-row weight fragments per wavefront
   constexpr int AGW = BM / 32;  // A transfers (8 rows x 128 B) per wavefront per stage
@@ -527,14 +531,25 @@ __global__ __launch_bounds__(NTHR, packed_occupancy<BM>()) void ffn_gemm_packed_
 
   // ---- A: transfer q of wave wv covers tile rows 8 g .. 8 g + 7, g = wv + 4 q;
   // lane l fills LDS row 8 g + l / 8, physical chunk l % 8, with logical
-  // chunk (l % 8) ^ ((row >> 1) & 7).  Padding rows re-read row 0.
-  const __amdgpu_buffer_rsrc_t a_rs = make_rsrc(A + (size_t)wk.row0 * Kdim, (uint32_t)wk.rows * Kdim * 2);
+  // chunk (l % 8) ^ ((row >> 1) & 7).  Padding rows re-read the tile's row 0
+  // (gathered: token 0); a gathered token index outside [0, T) reads token 0.
+  const bool gat = MODE == 0 && gather.src_of_row != nullptr;
+  const __amdgpu_buffer_rsrc_t a_rs =
+      gat ? make_rsrc(A, (uint32_t)gather.T * Kdim * 2)
+          : make_rsrc(A + (size_t)wk.row0 * Kdim, (uint32_t)wk.rows * Kdim * 2);
   int a_voff[AGW];
 #pragma unroll
   for (int q = 0; q < AGW; ++q) {
     const int row = 8 * (wv + 4 * q) + (lane >> 3);
     const int c = (lane & 7) ^ ((row >> 1) & 7);
-    a_voff[q] = ((row < wk.rows ? row : 0) * Kdim + c * 8) * 2;
+    int src = 0;
+    if (gat) {
+      if (row < wk.rows) src = gather.src_of_row[wk.row0 + row] / gather.k;
+      if ((unsigned)src >= (unsigned)gather.T) src = 0;
+    } else {
+      src = row < wk.rows ? row : 0;
+    }
+    a_voff[q] = (src * Kdim + c * 8) * 2;
   }
   auto issue_a = [&](char* stage, int js) {
 #pragma unroll
@@ -828,16 +843,17 @@ void n_tiles_of(bool bf16, bool packed, int d, int m, int& nn0, int& nn1, bool& 
 
 // kernels are instantiated here, outside any function template (device stubs
 // of kernels first instantiated inside a template launcher are not emitted)
-#define FFN_GEMM(MODE, BM, BN)                                                        \
-  do {                                                                                \
-    if (packed)                                                                       \
-      ffn_gemm_packed_kernel<MODE, BM, 256><<<grid, NTHR, 0, s>>>(A, W, C, tl, d, m); \
-    else                                                                              \
-      ffn_gemm_bf16_kernel<MODE, BM, BN><<<grid, NTHR, 0, s>>>(A, W, C, tl, d, m);    \
+#define FFN_GEMM(MODE, BM, BN)                                                          \
+  do {                                                                                  \
+    if (packed)                                                                         \
+      ffn_gemm_packed_kernel<MODE, BM, 256><<<grid, NTHR, 0, s>>>(A, W, C, tl, d, m, g); \
+    else                                                                                \
+      ffn_gemm_bf16_kernel<MODE, BM, BN><<<grid, NTHR, 0, s>>>(A, W, C, tl, d, m);      \
   } while (0)
 
 hipError_t launch_gemm(int mode, int bm, bool wide, bool packed, const Tiles& tl, const uint16_t* A,
-                       const uint16_t* W, uint16_t* C, int d, int m, hipStream_t s) {
+                       const uint16_t* W, uint16_t* C, int d, int m, hipStream_t s,
+                       const RowGather g) {
   const int grid = (tl.max_tiles * tl.nn + 7) & ~7;  // whole XCD rounds
   if (mode == 0) {
     if (bm == 128) {
@@ -867,7 +883,8 @@ size_t ffn_ws_bytes(bool bf16, int rows_max, int E, int d, int m) {
 hipError_t launch_expert_ffn(const void* x_perm, bool bf16, const int32_t* offsets, int E,
                              const int32_t* K_dev, int n_K, int rows_max, int d, int m,
                              const void* w_gate_up, const void* w_down, bool packed, void* y_perm,
-                             void* ws, hipStream_t s) {
+                             void* ws, hipStream_t s, RowGather gather) {
+  if (gather.src_of_row && !(bf16 && packed)) return hipErrorInvalidValue;
   const int bm = bf16 ? pick_bm(rows_max, E) : FBM;
   int nn0, nn1;
   bool wide0, wide1;
@@ -879,10 +896,12 @@ hipError_t launch_expert_ffn(const void* x_perm, bool bf16, const int32_t* offse
   hipError_t err;
   if (bf16) {
     err = launch_gemm(0, bm, wide0, packed, t0, static_cast<const uint16_t*>(x_perm),
-                      static_cast<const uint16_t*>(w_gate_up), static_cast<uint16_t*>(h), d, m, s);
+                      static_cast<const uint16_t*>(w_gate_up), static_cast<uint16_t*>(h), d, m, s,
+                      gather);
     if (err != hipSuccess) return err;
     return launch_gemm(1, bm, wide1, packed, t1, static_cast<const uint16_t*>(h),
-                       static_cast<const uint16_t*>(w_down), static_cast<uint16_t*>(y_perm), d, m, s);
+                       static_cast<const uint16_t*>(w_down), static_cast<uint16_t*>(y_perm), d, m, s,
+                       RowGather{nullptr, 1, 0});
   }
   ffn_gemm_f32_kernel<0><<<t0.max_tiles * nn0, NTHR, 0, s>>>(
       static_cast<const float*>(x_perm), static_cast<const float*>(w_gate_up), static_cast<float*>(h),

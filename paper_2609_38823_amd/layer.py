@@ -6,8 +6,9 @@ the order of Algorithm 2 of the paper:
 
   dense span (before the visual exit):
       moe_route(x) -> moe_dispatch -> moe_expert_ffn -> moe_combine
-      (bf16 layers: moe_route_packed and moe_expert_ffn_packed on router
-      and expert weights packed at load time)
+      (bf16 layers: moe_route_packed and moe_expert_ffn_packed_gather on
+      router and expert weights packed at load time; the dispatch then only
+      groups the assignments and the expert GEMM reads the token rows)
   RCEP span (from the visual exit on):
       moe_route(x) [full pool] -> moe_calibrate_prefix [s, K]
       -> moe_route(logits, K) [prefix re-route] -> moe_dispatch
@@ -73,7 +74,7 @@ class Buffers:
     """Device buffers of one invocation size (T tokens, n_seg segments)."""
 
     def __init__(self, T: int, d: int, E: int, m: int, k: int, dt: torch.dtype, n_seg: int = 1,
-                 device="cuda"):
+                 device="cuda", x_perm: bool = True):
         i32, f32 = torch.int32, torch.float32
         A = T * k
         self.T, self.n_seg = T, n_seg
@@ -88,7 +89,9 @@ class Buffers:
         self.offsets = torch.empty((E + 1,), dtype=i32, device=device)
         self.src_of_row = torch.empty((A,), dtype=i32, device=device)
         self.row_of_slot = torch.empty((A,), dtype=i32, device=device)
-        self.x_perm = torch.empty((A, d), dtype=dt, device=device)
+        # dispatched token rows; layers on packed weights gather them inside
+        # the expert GEMM and need none
+        self.x_perm = torch.empty((A, d), dtype=dt, device=device) if x_perm else None
         self.y_perm = torch.empty((A, d), dtype=dt, device=device)
         self.out = torch.empty((T, d), dtype=dt, device=device)
         nbytes = abi.moe_workspace_size(T, E, k, d, m, n_seg)
@@ -160,7 +163,8 @@ class MoELayer:
     def buffers(self, T: int, n_seg: int = 1) -> Buffers:
         key = (T, n_seg)
         if key not in self._bufs:
-            self._bufs[key] = Buffers(T, self.d, self.E, self.m, self.k, self.dt, n_seg, self.device)
+            self._bufs[key] = Buffers(T, self.d, self.E, self.m, self.k, self.dt, n_seg, self.device,
+                                      x_perm=not self.packed)
         return self._bufs[key]
 
     # -- stages ------------------------------------------------------------
@@ -170,11 +174,20 @@ class MoELayer:
     def _experts(self, x, b: Buffers, idx, w, K_dev=None, stream=None, mark=None, residual=None,
                  out=None):
         mark = mark or (lambda: None)
-        abi.moe_dispatch(idx, self.E, x, b.counts, b.offsets, b.src_of_row, b.row_of_slot,
-                         b.x_perm, b.ws, stream=stream)
-        mark()
-        ffn = abi.moe_expert_ffn_packed if self.packed else abi.moe_expert_ffn
-        ffn(b.x_perm, b.offsets, self.w_gate_up, self.w_down, b.y_perm, b.ws, K_dev=K_dev, stream=stream)
+        if self.packed:
+            # the expert GEMM reads the token rows through src_of_row: the
+            # dispatch only groups the assignments
+            abi.moe_dispatch(idx, self.E, None, b.counts, b.offsets, b.src_of_row, b.row_of_slot,
+                             None, b.ws, stream=stream)
+            mark()
+            abi.moe_expert_ffn_packed_gather(x, idx.shape[1], b.src_of_row, b.offsets, self.w_gate_up,
+                                             self.w_down, b.y_perm, b.ws, K_dev=K_dev, stream=stream)
+        else:
+            abi.moe_dispatch(idx, self.E, x, b.counts, b.offsets, b.src_of_row, b.row_of_slot,
+                             b.x_perm, b.ws, stream=stream)
+            mark()
+            abi.moe_expert_ffn(b.x_perm, b.offsets, self.w_gate_up, self.w_down, b.y_perm, b.ws,
+                               K_dev=K_dev, stream=stream)
         mark()
         out = b.out if out is None else out
         if residual is None:

@@ -73,7 +73,8 @@ class MoEStack:
         """Work buffers for T rows, shared by all layers (one stream)."""
         if T not in self._bufs:
             sh = self.sh
-            self._bufs[T] = Buffers(T, sh.d, sh.E, sh.m, sh.k, self.dt, 1, self.device)
+            packed = bool(self.layers) and self.layers[0].packed
+            self._bufs[T] = Buffers(T, sh.d, sh.E, sh.m, sh.k, self.dt, 1, self.device, x_perm=not packed)
         return self._bufs[T]
 
     def hidden(self, T: int, tag: str = "h") -> torch.Tensor:

@@ -33,7 +33,7 @@ def test_header_declares_the_boundary():
         "moe_dispatch", "moe_expert_ffn", "moe_expert_ffn_packed", "moe_pack_expert_weights",
         "moe_pack_router", "moe_permute_experts", "moe_route", "moe_route_packed", "moe_savb_gate",
         "moe_savb_workspace_size", "moe_status_string", "moe_workspace_size", "drop_visual_block_if",
-        "moe_expand_dense_routing"])
+        "moe_expand_dense_routing", "moe_expert_ffn_packed_gather"])
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -150,6 +150,34 @@ def test_packed_ffn_and_pack_reject(lib):
     assert lib.moe_pack_expert_weights(P1, BF16, 4, 64, 64, P1, NULL) == EALIAS
     assert lib.moe_pack_expert_weights(P1, BF16, -1, 64, 64, P2, NULL) == EINVAL
     assert lib.moe_pack_expert_weights(P1, BF16, 0, 64, 64, P2, NULL) == 0
+
+
+def test_gather_ffn_rejects(lib):
+    ws = ctypes.c_void_p(0x1000000)
+    f = lib.moe_expert_ffn_packed_gather
+    # (x, dtype, T, k, src_of_row, offsets, E, K_dev, n_K, d, m, w_gu, w_dn, y_perm, ws, ws_bytes, s)
+    ok = (P1, BF16, 16, 2, P2, P3, 16, NULL, 0, 256, 256, P4, P5, P6, ws, 1 << 30, NULL)
+
+    def call(**kw):
+        names = ["x", "dt", "T", "k", "src", "off", "E", "K", "nK", "d", "m", "wgu", "wdn", "y", "ws",
+                 "wsb", "s"]
+        a = dict(zip(names, ok))
+        a.update(kw)
+        return f(*[a[n] for n in names])
+
+    assert call(dt=F32) == EUNSUPPORTED
+    assert call(dt=7) == EINVAL
+    assert call(m=128) == EUNSUPPORTED
+    assert call(d=384) == EUNSUPPORTED
+    assert call(k=0) == EINVAL and call(k=17) == EINVAL and call(T=-1) == EINVAL
+    assert call(K=P7, nK=0) == EINVAL
+    assert call(src=NULL) == EINVAL and call(x=NULL) == EINVAL and call(y=NULL) == EINVAL
+    assert call(wsb=16) == EWORKSPACE
+    assert call(y=P1) == EALIAS      # y_perm on top of x
+    assert call(ws=P2) == EALIAS     # workspace on top of src_of_row
+    assert call(T=1 << 20, d=2048) == EUNSUPPORTED  # T*d*2 >= 2^31
+    assert call(T=0) == 0            # nothing to do
+    assert call(x=ctypes.c_void_p(0x10002)) == EINVAL  # misaligned
 
 
 def test_combine_and_drop_reject(lib):

@@ -482,6 +482,83 @@ def test_expert_ffn_packed(E, d, m, dt, rows, K, cnt):
 
 
 # ---------------------------------------------------------------------------
+# moe_expert_ffn_packed_gather: the dispatch gather inside the GEMM
+# ---------------------------------------------------------------------------
+GATHER_CASES = [
+    # T, E, k, d, m, K
+    (512, 128, 8, 2048, 768, None),   # 512 text rows, full pool (64-row tiles)
+    (512, 128, 8, 2048, 768, 84),     # prefix of 84 experts
+    (4096, 128, 8, 2048, 768, None),  # 4096 rows (128-row tiles)
+    (37, 6, 3, 512, 256, None),       # ragged, few experts
+    (1, 16, 2, 256, 256, None),       # a single token
+    (300, 4, 2, 512, 256, 3),         # experts >= K skipped
+]
+
+
+@pytest.mark.parametrize("T,E,k,d,m,K", GATHER_CASES)
+def test_expert_ffn_packed_gather(T, E, k, d, m, K):
+    sh = I.LayerShape(d=d, E=E, m=m, k=k, dtype="bf16")
+    prm = I.layer_params(sh, seed=E + d + k)
+    idx, _ = I.synthetic_routing(T, E, k, seed=T + 11 * E, K=K)
+    assert idx.shape == (T, k)
+    x = dev(I.synthetic_rows(T, d, "bf16", seed=T + d), torch.bfloat16)
+    A = T * k
+    counts, offsets, src, ros = i32((E,)), i32((E + 1,)), i32((A,)), i32((A,))
+    xp = torch.empty((A, d), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(abi.moe_workspace_size(T, E, k, d, m, 1), dtype=torch.uint8, device="cuda")
+    wgu, wd = dev(prm["w_gate_up"], torch.bfloat16), dev(prm["w_down"], torch.bfloat16)
+    wgu_p, wd_p = torch.empty_like(wgu), torch.empty_like(wd)
+    abi.moe_pack_expert_weights(wgu, wgu_p)
+    abi.moe_pack_expert_weights(wd, wd_p)
+    K_dev = dev(np.array([K], np.int32)) if K is not None else None
+    y_ref = torch.full((A, d), 7.0, dtype=torch.bfloat16, device="cuda")
+    y = torch.full((A, d), 7.0, dtype=torch.bfloat16, device="cuda")
+    abi.moe_dispatch(dev(idx), E, x, counts, offsets, src, ros, xp, ws)
+    abi.moe_expert_ffn_packed(xp, offsets, wgu_p, wd_p, y_ref, ws, K_dev=K_dev)
+    # the same dispatch without the row copy, then the gathering GEMM
+    counts2, offsets2, src2, ros2 = i32((E,)), i32((E + 1,)), i32((A,)), i32((A,))
+    abi.moe_dispatch(dev(idx), E, None, counts2, offsets2, src2, ros2, None, ws)
+    assert torch.equal(src2, src) and torch.equal(offsets2, offsets)
+    abi.moe_expert_ffn_packed_gather(x, k, src2, offsets2, wgu_p, wd_p, y, ws, K_dev=K_dev)
+    assert torch.equal(y.view(torch.int16), y_ref.view(torch.int16))
+    # against the oracle on the live rows (every row when small, else a sample)
+    rs = host(src)
+    e_of_row = np.repeat(np.arange(E), host(counts))
+    live = np.flatnonzero(e_of_row < (K if K is not None else E))
+    if live.size > 2048:
+        live = np.random.default_rng(T).choice(live, 2048, replace=False)
+    ref = oracle.expert_ffn_rows(host(x)[rs[live] // k], e_of_row[live], prm["w_gate_up"], prm["w_down"])
+    assert rel_inf(host(y)[live], ref) <= TOL["bf16"]
+
+
+def test_expert_ffn_packed_gather_out_of_range_rows_read_token_zero():
+    T, E, k, d, m = 64, 4, 2, 512, 256
+    sh = I.LayerShape(d=d, E=E, m=m, k=k, dtype="bf16")
+    prm = I.layer_params(sh, seed=5)
+    idx, _ = I.synthetic_routing(T, E, k, seed=6)
+    x = dev(I.synthetic_rows(T, d, "bf16", seed=7), torch.bfloat16)
+    A = T * k
+    counts, offsets, src, ros = i32((E,)), i32((E + 1,)), i32((A,)), i32((A,))
+    ws = torch.empty(abi.moe_workspace_size(T, E, k, d, m, 1), dtype=torch.uint8, device="cuda")
+    abi.moe_dispatch(dev(idx), E, None, counts, offsets, src, ros, None, ws)
+    bad = torch.tensor([3, 40, 77], dtype=torch.long, device="cuda")
+    src[bad] = torch.tensor([-5, A, A + 1000], dtype=torch.int32, device="cuda")
+    wgu, wd = dev(prm["w_gate_up"], torch.bfloat16), dev(prm["w_down"], torch.bfloat16)
+    wgu_p, wd_p = torch.empty_like(wgu), torch.empty_like(wd)
+    abi.moe_pack_expert_weights(wgu, wgu_p)
+    abi.moe_pack_expert_weights(wd, wd_p)
+    y = torch.empty((A, d), dtype=torch.bfloat16, device="cuda")
+    abi.moe_expert_ffn_packed_gather(x, k, src, offsets, wgu_p, wd_p, y, ws)
+    # the row-copy path on the rows the gather reads (token 0 for bad entries)
+    s_h = host(src).astype(np.int64) // k
+    s_h[(s_h < 0) | (s_h >= T)] = 0
+    xp = x[torch.as_tensor(s_h, device="cuda")].contiguous()
+    y_ref = torch.empty_like(y)
+    abi.moe_expert_ffn_packed(xp, offsets, wgu_p, wd_p, y_ref, ws)
+    assert torch.equal(y.view(torch.int16), y_ref.view(torch.int16))
+
+
+# ---------------------------------------------------------------------------
 # moe_combine
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("T,k,d,dt", [(512, 2, 256, "f32"), (4096, 8, 2048, "bf16"), (1, 8, 2048, "bf16"),
