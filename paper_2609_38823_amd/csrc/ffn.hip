@@ -14,11 +14,15 @@
 // bf16: v_mfma_f32_32x32x16_bf16 with float32 accumulation; 4 wavefronts per
 // workgroup, each owning BM token rows x (BN/4) weight rows.  Two variants:
 //   row-major weights  both operands stream global -> LDS (buffer_load ...
-//                      lds) through a 4-stage ring; BN = 512 or 256
+//                      lds) through a 4-stage ring; BN = 512 or 256; one
+//                      launch per GEMM
 //   packed weights     the weight operand streams from the fragment layout
 //                      of moe_pack_expert_weights straight into registers;
 //                      only the token rows use LDS; BN = 256 at two
-//                      workgroups per CU
+//                      workgroups per CU; both GEMMs in one persistent launch
+//                      with per-XCD work queues (the down GEMM of a token
+//                      tile starts as soon as its h is complete), or one
+//                      launch per GEMM where the XCD count is unknown
 // float32: a plain LDS-tiled SIMT kernel (correctness path for small layers).
 #include <type_traits>
 
@@ -497,35 +501,39 @@ __device__ __forceinline__ u32x4 load_frag(__amdgpu_buffer_rsrc_t rs, int voff, 
   return __builtin_amdgcn_raw_buffer_load_b128(rs, voff, soff, 0);
 }
 
+// One work item: the BM x BN output tile `wk` of one GEMM.  `aring` is the
+// workgroup's LDS: four A stages of a_slot<BM, BN>() bytes.  The caller
+// synchronises the workgroup before the item reuses it.
 // With gather.src_of_row (gate/up only), A is the token matrix x [gather.T,
 // d] and tile row r is token src_of_row[row0 + r] / gather.k: the dispatch
 // gather happens in the token-row transfers, which take a per-lane offset
 // anyway, and x_perm is never formed.
 template <int MODE, int BM, int BN, int NB = packed_nb<BM>()>
-__global__ __launch_bounds__(NTHR, packed_occupancy<BM>()) void ffn_gemm_packed_kernel(
-    const uint16_t* __restrict__ A, const uint16_t* __restrict__ Wp, uint16_t* __restrict__ C,
-    const Tiles tl, int d, int m, const RowGather gather) {
+__device__ __forceinline__ void packed_item(const uint16_t* __restrict__ A, const uint16_t* __restrict__ Wp,
+                                            uint16_t* __restrict__ C, const Work wk, int d, int m,
+                                            const RowGather gather, char* aring) {
   constexpr int MI = BM / 32;   // 32-row token fragments (all tile rows)
   constexpr int NI = BN / 128;  // 32-row weight fragments per wavefront
   constexpr int AGW = BM / 32;  // A transfers (8 rows x 128 B) per wavefront per stage
   static_assert(MI >= 1 && AGW >= 1 && (MODE == 1 || NI % 2 == 0), "tile shape");
 
   constexpr int ASLOT = a_slot<BM, BN>();
-  __shared__ __attribute__((aligned(1024))) char aring[4 * ASLOT];
   char* const aring0 = aring;
   char* const aring1 = aring + ASLOT;
   char* const aring2 = aring + 2 * ASLOT;
   char* const aring3 = aring + 3 * ASLOT;
 
-  Work wk;
-  if (!find_work(tl, true, wk, aring3)) return;
   const int nt = wk.nt;
   const int Kdim = MODE == 0 ? d : m;
   const int R = MODE == 0 ? 2 * m : d;  // rows of the expert's weight matrix
   const int nk = Kdim / BK;             // k-steps of 32: a multiple of 8
   const int ldc = MODE == 0 ? m : d;
 
-  const int tid = threadIdx.x;
+  // the lane offsets below are recomputed per item: an opaque copy of the
+  // thread index keeps them from being hoisted out of a persistent kernel's
+  // item loop (where they would stay live across items and spill)
+  int tid = threadIdx.x;
+  asm volatile("" : "+v"(tid));
   const int lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
 
@@ -745,6 +753,215 @@ __global__ __launch_bounds__(NTHR, packed_occupancy<BM>()) void ffn_gemm_packed_
   store_tile<MODE, MI, NI>(acc, reg, C, ldc, wk, colbase, lane);
 }
 
+// Two launches on packed weights (one per GEMM): items from find_work.
+template <int MODE, int BM>
+__global__ __launch_bounds__(NTHR, 2) void ffn_gemm_packed_kernel(
+    const uint16_t* __restrict__ A, const uint16_t* __restrict__ Wp, uint16_t* __restrict__ C,
+    const Tiles tl, int d, int m, const RowGather gather) {
+  __shared__ __attribute__((aligned(1024))) char aring[4 * a_slot<BM, 256>()];
+  Work wk;
+  if (!find_work(tl, true, wk, aring)) return;
+  packed_item<MODE, BM, 256>(A, Wp, C, wk, d, m, gather, aring);
+}
+
+// ---------------------------------------------------------------------------
+// Persistent expert FFN: one launch runs both GEMMs, per XCD.
+//
+// The m-tiles (numbered expert-major, as in find_work) are split into n_xcc
+// contiguous ranges of about equal estimated cost, one per XCD; a workgroup
+// serves the range of the XCD it runs on (the XCC_ID hardware register),
+// claiming items from that XCD's counter: first the nn0 gate/up items of
+// every tile in the range (expert-major, then n-tile, then m-tile, so the
+// m-tiles that share a weight tile run together), then its nn1 down items.
+// A down item of tile t reads the h rows of t, written by the nn0 gate/up
+// items of t, which ran on the same XCD and so behind the same L2: each of
+// them waits for its stores (vmcnt 0), then bumps done[t]; the down item's
+// workgroup polls done[t] until it reaches nn0 and only then loads h.  No
+// vector L1 can hold a stale h line: h lines of a tile are first read after
+// its count is complete, and different tiles and n-tiles never share a line
+// (h rows are whole 128-byte lines, n-tile column blocks are 256 bytes).
+// The wait always ends: within a queue items are claimed in order, so when a
+// down item is claimed every gate/up item of its range has been claimed by a
+// running workgroup, and gate/up items wait for nothing.  The poll is still
+// bounded (FFN_SPIN_LIMIT) so that a broken invariant cannot hang the device.
+//   ctr[16 x]     claim counter of XCD x (own 64-byte line)
+//   ctr[128 + t]  gate/up items of m-tile t completed
+// ctr (128 + max_tiles ints) is zeroed by clear_kernel before each launch.
+// Cost of a tile: 4 + its active 32-row blocks, plus 2 for the first tile of
+// an expert (the weight fetch that its later m-tiles find in L2).  (Claiming
+// the next item while the current one runs does not pay: the claim is older
+// than the item's transfers, so the first counted wait of the pipeline waits
+// for it too.)
+// ---------------------------------------------------------------------------
+constexpr int FFN_MAXE = 1024;
+constexpr int FFN_SPIN_LIMIT = 1 << 22;
+constexpr int FFN_CTR_TILES = 128;  // ctr index of done[0]
+
+struct XcdRange {
+  int a0, a1;  // tiles [a0, a1) of this XCD
+};
+
+// tstart[e] = first m-tile of expert e (experts >= Klim have none),
+// tstart[E] = the tile count; returns this XCD's tile range.  part: 2 NTHR /
+// 64 + 3 ints of LDS.
+__device__ XcdRange plan_tiles(const Tiles& tl, int xcc, int n_xcc, int* tstart, int* part) {
+  constexpr int NW = NTHR / 64;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  int& s_klim = part[2 * NW];
+  int& s_a0 = part[2 * NW + 1];
+  int& s_a1 = part[2 * NW + 2];
+  if (tid == 0) s_klim = 0;
+  __syncthreads();
+  if (tl.K_dev) {
+    int mx = 0;
+    for (int i = tid; i < tl.n_K; i += NTHR) mx = max(mx, tl.K_dev[i]);
+    if (mx > 0) atomicMax(&s_klim, mx);
+  }
+  int rows[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = 4 * tid + q;
+    rows[q] = 0;
+    if (e < tl.E) {
+      const int lo = clampi(tl.offsets[e], 0, tl.rows_max);
+      rows[q] = clampi(tl.offsets[e + 1], lo, tl.rows_max) - lo;
+    }
+  }
+  __syncthreads();
+  const int Klim = tl.K_dev ? clampi(s_klim, 0, tl.E) : tl.E;
+  constexpr int FULL = 4;  // + BM / 32 below
+  const int full_cost = FULL + tl.bm / 32, bonus = 2;
+  int cnt[4], cost[4], lc = 0, lw = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int c = 4 * tid + q < Klim ? (rows[q] + tl.bm - 1) / tl.bm : 0;
+    cnt[q] = c;
+    cost[q] = c == 0 ? 0 : bonus + (c - 1) * full_cost + FULL + (rows[q] - (c - 1) * tl.bm + 31) / 32;
+    lc += c;
+    lw += cost[q];
+  }
+  int ic = lc, iw = lw;  // inclusive scans over the wavefront
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int yc = __shfl_up(ic, off, 64), yw = __shfl_up(iw, off, 64);
+    if (lane >= off) {
+      ic += yc;
+      iw += yw;
+    }
+  }
+  if (lane == 63) {
+    part[wv] = ic;
+    part[NW + wv] = iw;
+  }
+  __syncthreads();
+  int bc = 0, bw = 0, total = 0, W = 0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    if (i < wv) {
+      bc += part[i];
+      bw += part[NW + i];
+    }
+    total += part[i];
+    W += part[NW + i];
+  }
+  total = min(total, tl.max_tiles);
+  // cost boundaries of this XCD; A(C) = tiles whose cumulative cost is <= C
+  const int C0 = (int)((long long)xcc * W / n_xcc), C1 = (int)((long long)(xcc + 1) * W / n_xcc);
+  if (tid == 0) {
+    s_a0 = xcc == 0 ? 0 : total;
+    s_a1 = total;
+  }
+  __syncthreads();
+  int start = bc + ic - lc, P = bw + iw - lw;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = 4 * tid + q;
+    if (e < tl.E) tstart[e] = min(start, total);
+    if (cnt[q] > 0) {
+      // tiles of this expert counted by A(C) for P <= C < P + cost
+      auto count = [&](int C) { return C - P - bonus < 0 ? 0 : min((C - P - bonus) / full_cost, cnt[q] - 1); };
+      if (xcc > 0 && P <= C0 && C0 < P + cost[q]) s_a0 = min(start + count(C0), total);
+      if (xcc + 1 < n_xcc && P <= C1 && C1 < P + cost[q]) s_a1 = min(start + count(C1), total);
+    }
+    start += cnt[q];
+    P += cost[q];
+  }
+  if (tid == 0) tstart[tl.E] = total;
+  __syncthreads();
+  return XcdRange{s_a0, s_a1};
+}
+
+__global__ void clear_kernel(int* __restrict__ p, int n) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
+}
+
+template <int BM>
+__global__ __launch_bounds__(NTHR, 2) void ffn_fused_kernel(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ Wgu, const uint16_t* __restrict__ Wdn,
+    uint16_t* __restrict__ H, uint16_t* __restrict__ Y, const Tiles tl, int nn1, int d, int m,
+    const RowGather gather, int n_xcc, int* __restrict__ ctr) {
+  constexpr int BN = 256;
+  constexpr int ASLOT = a_slot<BM, BN>();
+  __shared__ __attribute__((aligned(1024))) char aring[4 * ASLOT];
+  __shared__ int s_tstart[FFN_MAXE + 1];
+  __shared__ int s_part[2 * (NTHR / 64) + 3];
+  __shared__ int s_item;
+
+  // the XCD this workgroup runs on (hardware register XCC_ID, bits 3:0)
+  const int xcc = (int)(__builtin_amdgcn_s_getreg((3 << 11) | 20) % (unsigned)n_xcc);
+  const XcdRange rg = plan_tiles(tl, xcc, n_xcc, s_tstart, s_part);
+  const int ntile = rg.a1 - rg.a0;
+  const int n_gu = ntile * tl.nn, n_all = n_gu + ntile * nn1;
+  const int tid = threadIdx.x;
+  int* const claim = ctr + 16 * xcc;
+  for (;;) {
+    __syncthreads();  // the previous item is done with LDS and s_item
+    if (tid == 0) s_item = atomicAdd(claim, 1);
+    __syncthreads();
+    const int j = __builtin_amdgcn_readfirstlane(s_item);
+    if (j >= n_all) break;
+    const bool down = j >= n_gu;
+    const int nn = down ? nn1 : tl.nn;
+    const int jm = down ? j - n_gu : j;
+    // the expert holding tile a0 + jm / nn; its tiles in this range are
+    // [t_lo, t_lo + c), items [nn (t_lo - a0), nn (t_lo - a0 + c))
+    const int tq = rg.a0 + jm / nn;
+    int a = 0, b = tl.E;  // tstart[a] <= tq < tstart[b]
+    while (b - a > 1) {
+      const int mid = (a + b) >> 1;
+      if (s_tstart[mid] <= tq) a = mid; else b = mid;
+    }
+    const int t_lo = max(s_tstart[a], rg.a0);
+    const int c = min(s_tstart[a + 1], rg.a1) - t_lo;
+    const int o = jm - nn * (t_lo - rg.a0);
+    const int t = t_lo + o % c;
+    const int lo = clampi(tl.offsets[a], 0, tl.rows_max);
+    const int hi = clampi(tl.offsets[a + 1], lo, tl.rows_max);
+    const int r0 = lo + (t - s_tstart[a]) * BM;
+    Work wk;
+    wk.expert = __builtin_amdgcn_readfirstlane(a);
+    wk.row0 = __builtin_amdgcn_readfirstlane(r0);
+    wk.rows = __builtin_amdgcn_readfirstlane(min(BM, hi - r0));
+    wk.nt = __builtin_amdgcn_readfirstlane(o / c);
+    int* const done = ctr + FFN_CTR_TILES + t;
+    if (!down) {
+      packed_item<0, BM, BN>(X, Wgu, H, wk, d, m, gather, aring);
+      __builtin_amdgcn_s_waitcnt(0);  // this wavefront's h stores are complete (in L2)
+      __syncthreads();
+      if (tid == 0) __hip_atomic_fetch_add(done, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+      if (tid == 0) {
+        for (int n = 0; n < FFN_SPIN_LIMIT; ++n) {
+          if (__hip_atomic_load(done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= tl.nn) break;
+          __builtin_amdgcn_s_sleep(4);
+        }
+      }
+      __syncthreads();
+      packed_item<1, BM, BN>(H, Wdn, Y, wk, d, m, RowGather{nullptr, 1, 0}, aring);
+    }
+  }
+}
+
 __device__ __forceinline__ float silu_f(float g) { return g / (1.f + expf(-g)); }
 
 // ---------------------------------------------------------------------------
@@ -814,6 +1031,9 @@ using kern::NTHR;
 using kern::Tiles;
 using kern::ffn_gemm_bf16_kernel;
 using kern::ffn_gemm_f32_kernel;
+using kern::FFN_CTR_TILES;
+using kern::clear_kernel;
+using kern::ffn_fused_kernel;
 using kern::ffn_gemm_packed_kernel;
 using kern::pack_weights_kernel;
 
@@ -843,17 +1063,12 @@ void n_tiles_of(bool bf16, bool packed, int d, int m, int& nn0, int& nn1, bool& 
 
 // kernels are instantiated here, outside any function template (device stubs
 // of kernels first instantiated inside a template launcher are not emitted)
-#define FFN_GEMM(MODE, BM, BN)                                                          \
-  do {                                                                                  \
-    if (packed)                                                                         \
-      ffn_gemm_packed_kernel<MODE, BM, 256><<<grid, NTHR, 0, s>>>(A, W, C, tl, d, m, g); \
-    else                                                                                \
-      ffn_gemm_bf16_kernel<MODE, BM, BN><<<grid, NTHR, 0, s>>>(A, W, C, tl, d, m);      \
-  } while (0)
+#define FFN_GEMM(MODE, BM, BN)                                                   \
+  ffn_gemm_bf16_kernel<MODE, BM, BN><<<grid, NTHR, 0, s>>>(A, W, C, tl, d, m)
 
-hipError_t launch_gemm(int mode, int bm, bool wide, bool packed, const Tiles& tl, const uint16_t* A,
-                       const uint16_t* W, uint16_t* C, int d, int m, hipStream_t s,
-                       const RowGather g) {
+// row-major bf16 weights: one launch per GEMM
+hipError_t launch_gemm(int mode, int bm, bool wide, const Tiles& tl, const uint16_t* A,
+                       const uint16_t* W, uint16_t* C, int d, int m, hipStream_t s) {
   const int grid = (tl.max_tiles * tl.nn + 7) & ~7;  // whole XCD rounds
   if (mode == 0) {
     if (bm == 128) {
@@ -871,13 +1086,72 @@ hipError_t launch_gemm(int mode, int bm, bool wide, bool packed, const Tiles& tl
   return hipGetLastError();
 }
 #undef FFN_GEMM
+
+// Persistent launch geometry: two workgroups per compute unit and the XCD
+// count (false when the runtime cannot report them)
+bool persistent_shape(int& grid, int& n_xcc) {
+  int dev = 0, cus = 0, nx = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return false;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+    return false;
+  if (hipDeviceGetAttribute(&nx, hipDeviceAttributeNumberOfXccs, dev) != hipSuccess || nx < 1 || nx > 8)
+    return false;
+  grid = 2 * cus;
+  n_xcc = nx;
+  return true;
+}
+
+#define FFN_PACKED(MODE, BM)                                                      \
+  ffn_gemm_packed_kernel<MODE, BM><<<(t.max_tiles * t.nn + 7) & ~7, NTHR, 0, s>>>( \
+      A, W, C, t, d, m, g)
+
+// packed bf16 weights: both GEMMs in one persistent launch per call (after
+// zeroing its counters), or one launch per GEMM when the XCD layout is unknown
+hipError_t launch_packed(int bm, const Tiles& t0, int nn1, const uint16_t* X, const uint16_t* Wgu,
+                         const uint16_t* Wdn, uint16_t* H, uint16_t* Y, int d, int m,
+                         const RowGather g0, int* ctr, hipStream_t s) {
+  int grid = 0, n_xcc = 0;
+  if (persistent_shape(grid, n_xcc)) {
+    const int n_ctr = FFN_CTR_TILES + t0.max_tiles;
+    clear_kernel<<<(n_ctr + 255) / 256 < 64 ? (n_ctr + 255) / 256 : 64, 256, 0, s>>>(ctr, n_ctr);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (bm == 128)
+      ffn_fused_kernel<128><<<grid, NTHR, 0, s>>>(X, Wgu, Wdn, H, Y, t0, nn1, d, m, g0, n_xcc, ctr);
+    else
+      ffn_fused_kernel<64><<<grid, NTHR, 0, s>>>(X, Wgu, Wdn, H, Y, t0, nn1, d, m, g0, n_xcc, ctr);
+    return hipGetLastError();
+  }
+  {
+    const Tiles& t = t0;
+    const uint16_t* A = X;
+    const uint16_t* W = Wgu;
+    uint16_t* C = H;
+    const RowGather g = g0;
+    if (bm == 128) FFN_PACKED(0, 128); else FFN_PACKED(0, 64);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  {
+    Tiles t = t0;
+    t.nn = nn1;
+    const uint16_t* A = H;
+    const uint16_t* W = Wdn;
+    uint16_t* C = Y;
+    const RowGather g{nullptr, 1, 0};
+    if (bm == 128) FFN_PACKED(1, 128); else FFN_PACKED(1, 64);
+  }
+  return hipGetLastError();
+}
+#undef FFN_PACKED
 }  // namespace
 
-// workspace: the intermediate h [rows_max, m]
+// workspace: the intermediate h [rows_max, m], then (bf16) the counters of
+// the persistent kernel, 128 + max_tiles ints (sized for the smaller tile)
 size_t ffn_ws_bytes(bool bf16, int rows_max, int E, int d, int m) {
-  (void)E;
   (void)d;
-  return align256((size_t)rows_max * m * (bf16 ? 2 : 4));
+  const size_t h = align256((size_t)rows_max * m * (bf16 ? 2 : 4));
+  return bf16 ? h + align256((size_t)(kern::FFN_CTR_TILES + max_tiles_for(rows_max, E, 64)) * 4) : h;
 }
 
 hipError_t launch_expert_ffn(const void* x_perm, bool bf16, const int32_t* offsets, int E,
@@ -894,14 +1168,18 @@ hipError_t launch_expert_ffn(const void* x_perm, bool bf16, const int32_t* offse
   t1.nn = nn1;
   void* h = ws;
   hipError_t err;
+  if (bf16 && packed) {
+    int* ctr = reinterpret_cast<int*>(static_cast<char*>(ws) + align256((size_t)rows_max * m * 2));
+    return launch_packed(bm, t0, nn1, static_cast<const uint16_t*>(x_perm),
+                        static_cast<const uint16_t*>(w_gate_up), static_cast<const uint16_t*>(w_down),
+                        static_cast<uint16_t*>(h), static_cast<uint16_t*>(y_perm), d, m, gather, ctr, s);
+  }
   if (bf16) {
-    err = launch_gemm(0, bm, wide0, packed, t0, static_cast<const uint16_t*>(x_perm),
-                      static_cast<const uint16_t*>(w_gate_up), static_cast<uint16_t*>(h), d, m, s,
-                      gather);
+    err = launch_gemm(0, bm, wide0, t0, static_cast<const uint16_t*>(x_perm),
+                      static_cast<const uint16_t*>(w_gate_up), static_cast<uint16_t*>(h), d, m, s);
     if (err != hipSuccess) return err;
-    return launch_gemm(1, bm, wide1, packed, t1, static_cast<const uint16_t*>(h),
-                       static_cast<const uint16_t*>(w_down), static_cast<uint16_t*>(y_perm), d, m, s,
-                       RowGather{nullptr, 1, 0});
+    return launch_gemm(1, bm, wide1, t1, static_cast<const uint16_t*>(h),
+                       static_cast<const uint16_t*>(w_down), static_cast<uint16_t*>(y_perm), d, m, s);
   }
   ffn_gemm_f32_kernel<0><<<t0.max_tiles * nn0, NTHR, 0, s>>>(
       static_cast<const float*>(x_perm), static_cast<const float*>(w_gate_up), static_cast<float*>(h),
