@@ -65,16 +65,21 @@ def main(argv) -> int:
     copy_key = max((k for k in fetch if k[0].startswith("drop_rows_kernel")), key=lambda k: k[1])
     f_scale = COPY_BYTES / (fetch[copy_key] * 1024.0)
     w_scale = COPY_BYTES / (write[copy_key] * 1024.0)
-    gemm = {k: v for k, v in fetch.items() if k[0].startswith("ffn_gemm_packed_kernel")}
-    # the bench's FFN call at 4096 rows: the largest grids of the two GEMM modes
-    per_mode = {}
-    for (name, grid), kib in gemm.items():
-        mode = name.split("<")[1].split(",")[0]
-        if mode not in per_mode or grid > per_mode[mode][1]:
-            per_mode[mode] = (name, grid)
+    # the bench's FFN call at 4096 rows (128-row tiles): one persistent launch
+    # running both GEMMs, or, where it is not used, the largest grids of the
+    # two per-GEMM launches
+    fused = [k for k in fetch if k[0].startswith("ffn_fused_kernel<128")]
+    if fused:
+        keys = [max(fused, key=lambda k: k[1])]
+    else:
+        per_mode = {}
+        for name, grid in (k for k in fetch if k[0].startswith("ffn_gemm_packed_kernel")):
+            mode = name.split("<")[1].split(",")[0]
+            if mode not in per_mode or grid > per_mode[mode][1]:
+                per_mode[mode] = (name, grid)
+        keys = [per_mode[mode] for mode in sorted(per_mode)]
     rows, total = [], 0.0
-    for mode in sorted(per_mode):
-        key = per_mode[mode]
+    for key in keys:
         fb = fetch[key] * 1024.0 * f_scale
         wb = write.get(key, 0.0) * 1024.0 * w_scale
         total += fb + wb
@@ -86,7 +91,7 @@ def main(argv) -> int:
     with open(out + ".json", "w") as f:
         json.dump(res, f, indent=1)
     with open(out + ".txt", "w") as f:
-        f.write("# HBM traffic of moe_expert_ffn_packed @ 4096 rows (Qwen3-VL-MoE layer), per launch\n")
+        f.write("# HBM traffic of moe_expert_ffn_packed_gather @ 4096 rows (Qwen3-VL-MoE layer), per call\n")
         f.write("# commands (from the repository root R, one pass each):\n")
         f.write("#   cd /tmp && rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/gpurun_out/pmc_fetch -o p"
                 " -- python3 $R/bench.py --traffic-run\n")
@@ -100,7 +105,7 @@ def main(argv) -> int:
             f.write(f"{r['kernel']:40s} grid {r['grid']:8d}  fetch {r['fetch_bytes'] / 1e6:9.1f} MB"
                     f"  write {r['write_bytes'] / 1e6:9.1f} MB  (raw {r['fetch_kib_raw']:.0f} / "
                     f"{r['write_kib_raw']:.0f} KiB)\n")
-        f.write(f"total per moe_expert_ffn_packed call: {total / 1e6:.1f} MB\n")
+        f.write(f"total per moe_expert_ffn_packed_gather call: {total / 1e6:.1f} MB\n")
     print(open(out + ".txt").read())
     return 0
 
