@@ -39,7 +39,7 @@ __global__ __launch_bounds__(CAL_THREADS) void segment_mass_kernel(
     const int32_t* __restrict__ seg_offsets, double p, double* __restrict__ mass,
     int32_t* __restrict__ K_out) {
   __shared__ double table[CAL_TABLE];
-  __shared__ double smass[1024];
+  __shared__ double smass[1024 + 32];  // zero past E (the c_K loop reads whole batches)
   __shared__ int st_e[CAL_STAGE];
   __shared__ float st_w[CAL_STAGE];
   __shared__ int s_cnt[1024], s_off[1024];
@@ -126,13 +126,18 @@ __global__ __launch_bounds__(CAL_THREADS) void segment_mass_kernel(
     }
     __syncthreads();
     if (tid < E) {
+      // one dependent float64 chain per expert (the latency of the
+      // additions, not of the LDS reads, bounds it)
       double a = 0.0;
       const int b0 = s_off[tid], b1 = b0 + s_cnt[tid];
 #pragma unroll 8
       for (int j = b0; j < b1; ++j) a += static_cast<double>(sorted[j]);
       mass[(size_t)seg * E + tid] = a;
       smass[tid] = a;
+    } else {
+      smass[tid] = 0.0;
     }
+    if (tid < 32) smass[1024 + tid] = 0.0;
     __syncthreads();
   } else {
   const int ch = cal_chunk(E, k);
@@ -192,28 +197,38 @@ __global__ __launch_bounds__(CAL_THREADS) void segment_mass_kernel(
   if (tid < E) {
     mass[(size_t)seg * E + tid] = acc;
     smass[tid] = acc;
+  } else {
+    smass[tid] = 0.0;
   }
+  if (tid < 32) smass[1024 + tid] = 0.0;
   __syncthreads();
   }  // chunked path
   if (K_out) {
     // c_K: one running sum in expert order by a single thread (the same
-    // sequence of float64 additions as the definition), 8 masses per batch
-    // of LDS reads; the c_K go to LDS and wave 0 finds the first K with
-    // c_K >= p * tot by a ballot
+    // sequence of float64 additions as the definition).  The masses come
+    // from LDS in batches of 16, the next batch read while the current one
+    // is added, with no per-element conditions (the masses past E are zero,
+    // and adding +0.0 to the non-negative running sum changes no bit); the
+    // c_K go to LDS and wave 0 finds the first K with c_K >= p * tot by a
+    // ballot
     double* cbuf = table;  // the table is free now
     __shared__ double s_tot;
     if (tid == 0) {
-      double run = 0.0;
-      for (int e0 = 0; e0 < E; e0 += 8) {
-        double v[8];
+      constexpr int B = 16;
+      const int Ep = (E + B - 1) / B * B;
+      double run = 0.0, v[B], nv[B];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] = e0 + j < E ? smass[e0 + j] : 0.0;
+      for (int j = 0; j < B; ++j) v[j] = smass[j];
+      for (int e0 = 0; e0 < Ep; e0 += B) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-          if (e0 + j < E) {
-            run += v[j];
-            cbuf[e0 + j] = run;
-          }
+        for (int j = 0; j < B; ++j) nv[j] = smass[e0 + B + j];
+#pragma unroll
+        for (int j = 0; j < B; ++j) {
+          run += v[j];
+          cbuf[e0 + j] = run;
+        }
+#pragma unroll
+        for (int j = 0; j < B; ++j) v[j] = nv[j];
       }
       s_tot = run;  // tot = c_E
     }
