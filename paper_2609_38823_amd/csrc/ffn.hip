@@ -787,8 +787,10 @@ __global__ __launch_bounds__(NTHR, 2) void ffn_gemm_packed_kernel(
 //   ctr[16 x]     claim counter of XCD x (own 64-byte line)
 //   ctr[128 + t]  gate/up items of m-tile t completed
 // ctr (128 + max_tiles ints) is zeroed by clear_kernel before each launch.
-// Cost of a tile: 4 + its active 32-row blocks, plus 2 for the first tile of
-// an expert (the weight fetch that its later m-tiles find in L2).  (Claiming
+// Cost of a tile: 4 + its active 32-row blocks; the first tile of an expert
+// costs more for the weight fetch that its later m-tiles find in L2: 2 with
+// 128-row tiles, a whole tile's cost with 64-row tiles (few rows per
+// expert, where an XCD's time follows the weight bytes it streams).  (Claiming
 // the next item while the current one runs does not pay: the claim is older
 // than the item's transfers, so the first counted wait of the pipeline waits
 // for it too.)
@@ -830,7 +832,7 @@ __device__ XcdRange plan_tiles(const Tiles& tl, int xcc, int n_xcc, int* tstart,
   __syncthreads();
   const int Klim = tl.K_dev ? clampi(s_klim, 0, tl.E) : tl.E;
   constexpr int FULL = 4;  // + BM / 32 below
-  const int full_cost = FULL + tl.bm / 32, bonus = 2;
+  const int full_cost = FULL + tl.bm / 32, bonus = tl.bm == 64 ? full_cost : 2;
   int cnt[4], cost[4], lc = 0, lw = 0;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
