@@ -445,7 +445,19 @@ def test_pack_expert_weights_layout(E, R, C):
     assert np.array_equal(got, packed_layout(w))
 
 
-PACKED_CASES = [c for c in FFN_CASES if c[3] == "bf16" and c[2] % 256 == 0] + [
+# token-tile distributions for the persistent kernel's per-XCD split: one
+# expert holding every row (128-row tiles), a single tile, more XCDs than
+# tiles, empty experts between full ones, and a prefix K with no rows past it
+SKEW_CASES = [
+    (128, 2048, 768, "bf16", 4096, None, [0] * 5 + [4096] + [0] * 122),  # 64-row tiles
+    (8, 2048, 768, "bf16", 4096, None, [0, 0, 0, 4096, 0, 0, 0, 0]),       # 128-row tiles
+    (8, 512, 256, "bf16", 20, None, [0, 0, 0, 20, 0, 0, 0, 0]),
+    (4, 512, 256, "bf16", 130, None, [0, 65, 0, 65]),
+    (32, 512, 256, "bf16", 6000, None, [1500, 0, 0, 1500, 0, 1500] + [0] * 25 + [1500]),
+    (16, 512, 256, "bf16", 3000, 5, [600, 600, 600, 600, 600] + [0] * 11),
+]
+
+PACKED_CASES = [c for c in FFN_CASES if c[3] == "bf16" and c[2] % 256 == 0] + SKEW_CASES + [
     (4, 512, 256, "bf16", 700, None, [300, 0, 1, 399]),  # one 8-k-step body, ragged tails
     (2, 2048, 768, "bf16", 1700, None, [1600, 100]),       # many tiles of one expert
     # few rows per expert (decode-like weight streaming)
