@@ -10,10 +10,11 @@ resident in HBM:
                moe_expert_ffn_packed_gather reading the token rows itself)
                over 4096 rows (3584 visual + 512 text), all 128 experts
   SAVB exit    drop_visual_block removes the 3584 visual rows
-  RCEP span    moe_route (full pool) -> moe_calibrate_prefix (K, p = 0.9)
-               -> moe_route (prefix re-route) -> moe_dispatch
-               -> moe_expert_ffn (experts [0, K)) -> moe_combine
-               over the 512 text rows (bf16: the same packed calls)
+  RCEP span    moe_route (full pool) -> moe_calibrate_route_prefix (s, K
+               with p = 0.9, then the prefix re-route, in one call)
+               -> moe_dispatch -> moe_expert_ffn (experts [0, K))
+               -> moe_combine over the 512 text rows (bf16: the same packed
+               calls)
 
 value = MoE-layer tokens per second over the step (4096 + 512 rows per
 step).  Every ABI call is bracketed by HIP events on the stream it runs on,
@@ -73,6 +74,8 @@ def stage_flops_bytes(stage: str, T: int, d: int, E: int, m: int, k: int, touche
         return 0.0, T * K * 4 + 2 * T * k * 4
     if stage == "calibrate":
         return 0.0, 2 * T * k * 4 + E * 8 + 4
+    if stage == "calibrate_route":  # masses, K and the prefix re-route in one call
+        return 0.0, 2 * T * k * 4 + E * 8 + 4 + T * K * 4 + 2 * T * k * 4
     if stage == "dispatch":
         return 0.0, T * k * 4 + (E + 1) * 8 + 2 * A * 4 + (0 if gather else T * d * 2 + A * d * 2)
     if stage == "ffn":
@@ -206,7 +209,7 @@ def bench_layer(args) -> int:
 
     stream = torch.cuda.current_stream()
     stages = ["route_full", "dispatch", "ffn", "combine", "drop",
-              "r.route_full", "r.calibrate", "r.route_prefix", "r.dispatch", "r.ffn", "r.combine"]
+              "r.route_full", "r.calibrate_route", "r.dispatch", "r.ffn", "r.combine"]
 
     def step(ev=None):
         marks = iter(ev) if ev is not None else None
@@ -480,7 +483,7 @@ def bench_stack48(args) -> int:
     if not args.no_cpu_baseline:
         cpu = _oracle_stack_sample(st, x_np, wl)
     names_d = ["route", "dispatch", "ffn", "combine_residual"]
-    names_r = ["route_full", "calibrate", "route_prefix", "dispatch", "ffn", "combine_residual"]
+    names_r = ["route_full", "calibrate_route", "dispatch", "ffn", "combine_residual"]
     return _line(
         "MoE-stack prefill tokens/s (48 MoE layers, SAVB exit at layer 20, RCEP p 0.9)",
         wl.T / (ms * 1e-3), "tokens/s", args, ms,

@@ -11,6 +11,7 @@
  *   activated mass s (Eq. 11), prefix length K (Eq. 12),
  *   Mean-Mass calibration order pi (Eqs. 8, 9)                    moe_calibrate_prefix
  *   prefix-restricted re-route inside [0, K)                      moe_route
+ *     (s, K and the re-route in one call)                         moe_calibrate_route_prefix
  *   grouping of the T*k assignments by expert                     moe_dispatch
  *   SwiGLU expert MLPs over the dispatched rows                   moe_expert_ffn
  *     (same, on weights re-laid out once at load time)            moe_expert_ffn_packed,
@@ -187,6 +188,34 @@ int moe_calibrate_prefix(const int32_t* topk_idx, const float* topk_w,
                          const int32_t* seg_offsets, int n_seg, double p,
                          double* mass, int32_t* K_out, int32_t* order,
                          void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * moe_calibrate_route_prefix - the RCEP routing of one invocation in one
+ * call: the activated mass and prefix length K (Eqs. 11, 12), then the
+ * prefix-restricted re-route of every token inside [0, K) (Sec. 3.3 after
+ * Eq. 12; Algorithm 2).
+ *
+ *   logits            [T, E] float32 router logits (from the full-pool
+ *                     moe_route / moe_route_packed call).
+ *   topk_idx_full,
+ *   topk_w_full       [T, k] full-pool routing of the same call.
+ *   p                 routed-mass fraction, 0 < p <= 1.
+ *   mass              [E] float64 output: s_e of the invocation.
+ *   K_out             [1] int32 output: K.
+ *   topk_idx, topk_w  [T, k] outputs: the re-routed experts (all < K) and
+ *                     their renormalised weights.
+ * Bitwise the same results as moe_calibrate_prefix (one segment, order =
+ * NULL) followed by moe_route on the logits with K_dev = K_out.  When
+ * T*k <= 8192 and E <= 512 it runs as one launch in which every workgroup
+ * forms the masses and K itself (a few thousand routing entries) before
+ * re-routing its share of the tokens; otherwise as those two launches.
+ * Outputs must not overlap the inputs (MOE_EALIAS).  Limits: 1 <= k <=
+ * min(E, 32), E <= 1024.  ws / ws_bytes: not needed (NULL, 0 accepted).
+ */
+int moe_calibrate_route_prefix(const float* logits, const int32_t* topk_idx_full,
+                               const float* topk_w_full, int T, int E, int k, double p,
+                               double* mass, int32_t* K_out, int32_t* topk_idx, float* topk_w,
+                               void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * moe_dispatch - group the T*k (token, slot) assignments by expert

@@ -23,7 +23,7 @@ STATUS = {0: "MOE_OK", -1: "MOE_EINVAL", -2: "MOE_EALIAS", -3: "MOE_EWORKSPACE",
           -4: "MOE_EHIP", -5: "MOE_EUNSUPPORTED"}
 
 EXPORTS = ("moe_status_string", "moe_workspace_size", "moe_route", "moe_route_packed",
-           "moe_pack_router", "moe_calibrate_prefix",
+           "moe_pack_router", "moe_calibrate_prefix", "moe_calibrate_route_prefix",
            "moe_dispatch", "moe_expert_ffn", "moe_expert_ffn_packed", "moe_expert_ffn_packed_gather",
            "moe_pack_expert_weights",
            "moe_combine", "moe_combine_residual", "drop_visual_block", "moe_permute_experts",
@@ -56,6 +56,7 @@ def load() -> ctypes.CDLL:
         "moe_route_packed": (_I, [_P, _I, _P, _P, _I, _I, _I, _I, _P, _I, _P, _P, _P, _P, _P, _S, _P]),
         "moe_pack_router": (_I, [_P, _I, _I, _P, _P]),
         "moe_calibrate_prefix": (_I, [_P, _P, _I, _I, _I, _P, _I, _D, _P, _P, _P, _P, _S, _P]),
+        "moe_calibrate_route_prefix": (_I, [_P, _P, _P, _I, _I, _I, _D, _P, _P, _P, _P, _P, _S, _P]),
         "moe_dispatch": (_I, [_P, _I, _I, _I, _P, _I, _I, _P, _P, _P, _P, _P, _P, _S, _P]),
         "moe_expert_ffn": (_I, [_P, _I, _P, _I, _P, _I, _I, _I, _I, _P, _P, _P, _P, _S, _P]),
         "moe_expert_ffn_packed": (_I, [_P, _I, _P, _I, _P, _I, _I, _I, _I, _P, _P, _P, _P, _S, _P]),
@@ -162,6 +163,15 @@ def moe_calibrate_prefix(topk_idx, topk_w, E, p, mass, ws, K_out=None, order=Non
     _check("moe_calibrate_prefix", load().moe_calibrate_prefix(
         _p(topk_idx), _p(topk_w), T, E, k, _p(seg_offsets), _nseg(seg_offsets), float(p),
         _p(mass), _p(K_out), _p(order), _p(ws), _nbytes(ws), _stream(stream)))
+
+
+def moe_calibrate_route_prefix(logits, idx_full, w_full, p, mass, K_out, idx, w, stream=None):
+    """Eqs. 11-12 and the prefix re-route of one invocation in one call."""
+    T, k = idx_full.shape
+    E = logits.shape[1]
+    _check("moe_calibrate_route_prefix", load().moe_calibrate_route_prefix(
+        _p(logits), _p(idx_full), _p(w_full), T, E, k, float(p), _p(mass), _p(K_out), _p(idx), _p(w),
+        None, 0, _stream(stream)))
 
 
 def moe_dispatch(topk_idx, E, x, counts, offsets, src_of_row, row_of_slot, x_perm, ws,

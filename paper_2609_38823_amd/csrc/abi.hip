@@ -204,6 +204,29 @@ int moe_calibrate_prefix(const int32_t* topk_idx, const float* topk_w, int T, in
                                               mass, K_out, order, ws, stream));
 }
 
+int moe_calibrate_route_prefix(const float* logits, const int32_t* topk_idx_full,
+                               const float* topk_w_full, int T, int E, int k, double p, double* mass,
+                               int32_t* K_out, int32_t* topk_idx, float* topk_w, void* ws,
+                               size_t ws_bytes, hipStream_t stream) {
+  (void)ws;
+  (void)ws_bytes;
+  if (T < 0 || E < 1 || E > kMaxE || k < 1 || k > E) return MOE_EINVAL;
+  if (k > kMaxK) return MOE_EUNSUPPORTED;
+  if (!(p > 0.0 && p <= 1.0)) return MOE_EINVAL;
+  if (!mass || !K_out) return MOE_EINVAL;
+  if (T > 0 && (!logits || !topk_idx_full || !topk_w_full || !topk_idx || !topk_w)) return MOE_EINVAL;
+  if (!aligned_all({logits, topk_idx_full, topk_w_full, mass, K_out, topk_idx, topk_w})) return MOE_EINVAL;
+  const size_t nl = (size_t)T * E * 4, nk = (size_t)T * k * 4;
+  Range in_l = T ? rng(logits, nl) : Range{0, 0};
+  Range in_i = T ? rng(topk_idx_full, nk) : Range{0, 0};
+  Range in_w = T ? rng(topk_w_full, nk) : Range{0, 0};
+  Range o_i = T ? rng(topk_idx, nk) : Range{0, 0};
+  Range o_w = T ? rng(topk_w, nk) : Range{0, 0};
+  if (any_alias({rng(mass, (size_t)E * 8), rng(K_out, 4), o_i, o_w}, {in_l, in_i, in_w})) return MOE_EALIAS;
+  return hip_status(decomoe::launch_calibrate_route(logits, topk_idx_full, topk_w_full, T, E, k, p, mass,
+                                                    K_out, topk_idx, topk_w, stream));
+}
+
 int moe_dispatch(const int32_t* topk_idx, int T, int k, int E, const void* x, moe_dtype dtype,
                  int d, int32_t* counts, int32_t* offsets, int32_t* src_of_row,
                  int32_t* row_of_slot, void* x_perm, void* ws, size_t ws_bytes,

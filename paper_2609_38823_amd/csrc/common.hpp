@@ -53,6 +53,12 @@ size_t calibrate_ws_bytes(int T, int E);
 hipError_t launch_calibrate(const int32_t* idx, const float* w, int T, int E, int k,
                             const int32_t* seg_offsets, int n_seg, double p, double* mass,
                             int32_t* K_out, int32_t* order, void* ws, hipStream_t s);
+// calibration (one segment) and prefix re-route in one launch when
+// calibrate_route_fused(T, E, k), else the two launches
+bool calibrate_route_fused(int T, int E, int k);
+hipError_t launch_calibrate_route(const float* logits, const int32_t* idx_full, const float* w_full,
+                                  int T, int E, int k, double p, double* mass, int32_t* K_out,
+                                  int32_t* idx, float* w, hipStream_t s);
 size_t dispatch_ws_bytes(int T, int k, int E);
 hipError_t launch_dispatch(const int32_t* idx, int T, int k, int E, const void* x, int elt, int d,
                            int32_t* counts, int32_t* offsets, int32_t* src_of_row,

@@ -1,6 +1,8 @@
 // Router logits and wavefront Top-k (Eq. 1; Eq. 10; prefix re-route of
 // Sec. 3.3 and Algorithm 2).
 #include "common.hpp"
+#include "mass_dev.hpp"
+#include "topk_dev.hpp"
 
 #include <float.h>
 
@@ -184,48 +186,6 @@ __global__ __launch_bounds__(256) void router_logits_simt_kernel(const void* __r
 // ---------------------------------------------------------------------------
 constexpr int TK_MAXC = 16;  // E <= 1024 = 16 values per lane (MAXC: per instantiation)
 
-__device__ __forceinline__ void better(float& v, int& i, float ov, int oi) {
-  if (ov > v || (ov == v && oi < i)) { v = ov; i = oi; }
-}
-
-// (value, index) of lane l -> the wavefront's best pair in every lane
-// without LDS round trips: DPP moves within each row of 16 lanes (quad
-// swaps, then the half-row and row mirrors pair the groups), then the four
-// row results are read with v_readlane and combined (the same in every
-// lane).  `better` is a total order on pairs, so the pairing order does not
-// change the result.
-template <int CTRL>
-__device__ __forceinline__ float dpp_f(float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
-}
-template <int CTRL>
-__device__ __forceinline__ void dpp_better(float& v, int& i) {
-  better(v, i, dpp_f<CTRL>(v), __builtin_amdgcn_mov_dpp(i, CTRL, 0xF, 0xF, false));
-}
-__device__ __forceinline__ float lane_f(float v, int l) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
-}
-__device__ __forceinline__ void wave_best(float& v, int& i) {
-  dpp_better<0xB1>(v, i);   // quad_perm [1, 0, 3, 2]
-  dpp_better<0x4E>(v, i);   // quad_perm [2, 3, 0, 1]
-  dpp_better<0x141>(v, i);  // row_half_mirror
-  dpp_better<0x140>(v, i);  // row_mirror
-  float bv = lane_f(v, 0);
-  int bi = __builtin_amdgcn_readlane(i, 0);
-#pragma unroll
-  for (int r = 1; r < 4; ++r) better(bv, bi, lane_f(v, 16 * r), __builtin_amdgcn_readlane(i, 16 * r));
-  v = bv;
-  i = bi;
-}
-// sum over the wavefront: row sums by DPP, then the four rows in order
-__device__ __forceinline__ float wave_sum(float v) {
-  v += dpp_f<0xB1>(v);
-  v += dpp_f<0x4E>(v);
-  v += dpp_f<0x141>(v);
-  v += dpp_f<0x140>(v);
-  return ((lane_f(v, 0) + lane_f(v, 16)) + lane_f(v, 32)) + lane_f(v, 48);
-}
-
 // With `part` (split-K router), the logits are first formed here as
 // (part[0] + part[1] + ... + part[S-1]) + b, written to `logits`, and used.
 template <int MAXC>  // values per lane: E <= 64 MAXC
@@ -244,8 +204,6 @@ __global__ __launch_bounds__(256) void topk_kernel(float* __restrict__ logits, i
     Klim = clampi(K_dev[s], k, E);
   }
   float* row = logits + (size_t)t * E;
-  float v[MAXC];
-  uint32_t alive = 0;
   if (part) {
 #pragma unroll
     for (int c = 0; c < MAXC; ++c) {
@@ -266,32 +224,7 @@ __global__ __launch_bounds__(256) void topk_kernel(float* __restrict__ logits, i
       }
     }
   }
-#pragma unroll
-  for (int c = 0; c < MAXC; ++c) {
-    int e = lane + c * 64;
-    v[c] = -FLT_MAX;
-    if (e < Klim) { v[c] = row[e]; alive |= 1u << c; }
-  }
-  float my_v = 0.f;
-  int my_i = 0;
-  for (int r = 0; r < k; ++r) {
-    float bv = -INFINITY;
-    int bi = 0x7fffffff;
-#pragma unroll
-    for (int c = 0; c < MAXC; ++c)
-      if (alive & (1u << c)) better(bv, bi, v[c], lane + c * 64);
-    wave_best(bv, bi);
-    if (bi < E && (bi & 63) == lane) alive &= ~(1u << (bi >> 6));
-    if (lane == r) { my_v = bv; my_i = bi; }
-  }
-  const float v0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_v), 0));
-  float ex = lane < k ? expf(my_v - v0) : 0.f;
-  float sum = ex;
-  sum = wave_sum(sum);
-  if (lane < k) {
-    idx[(size_t)t * k + lane] = my_i;
-    w[(size_t)t * k + lane] = ex / sum;
-  }
+  topk_select<MAXC>(row, E, k, Klim, lane, idx + (size_t)t * k, w + (size_t)t * k);
 }
 
 // ---------------------------------------------------------------------------
@@ -409,7 +342,65 @@ __global__ __launch_bounds__(256) void topk_row_kernel(float* __restrict__ logit
     }
   }
 }
+// ---------------------------------------------------------------------------
+// Calibration and prefix re-route of one invocation in one launch (Eqs. 11,
+// 12, then the re-route of Sec. 3.3).  Every workgroup forms the masses and
+// K itself -- the same float64 sums as segment_mass_kernel (mass_sorted,
+// prefix_K), over at most CAL_STAGE routing entries -- so no second launch
+// waits for one workgroup's result; workgroup 0 writes mass and K.  Then
+// wavefront w of workgroup b re-routes the tokens 16 b + w, 16 (b + grid) +
+// w, ... inside [0, K) exactly as topk_kernel does (topk_select).
+// ---------------------------------------------------------------------------
+template <int MAXC>
+__global__ __launch_bounds__(CAL_THREADS) void calibrate_route_kernel(
+    const float* __restrict__ logits, const int32_t* __restrict__ idx_full,
+    const float* __restrict__ w_full, int T, int E, int k, int key_bits, double p,
+    double* __restrict__ mass, int32_t* __restrict__ K_out, int32_t* __restrict__ idx,
+    float* __restrict__ w) {
+  __shared__ CalLds L;
+  const double a = mass_sorted(idx_full, w_full, 0, T * k, E, key_bits, L);
+  const int K = prefix_K(E, k, p, L);
+  const int tid = threadIdx.x;
+  if (blockIdx.x == 0) {
+    if (tid < E) mass[tid] = a;
+    if (tid == 0) K_out[0] = K;
+  }
+  const int lane = tid & 63;
+  const int Klim = clampi(K, k, E);
+  for (int t = blockIdx.x * CAL_WAVES + (tid >> 6); t < T; t += gridDim.x * CAL_WAVES)
+    topk_select<MAXC>(logits + (size_t)t * E, E, k, Klim, lane, idx + (size_t)t * k, w + (size_t)t * k);
+}
 }  // namespace
+
+bool calibrate_route_fused(int T, int E, int k) {
+  return T >= 1 && (size_t)T * k <= (size_t)CAL_STAGE && E <= CAL_SORT_E;
+}
+
+hipError_t launch_calibrate_route(const float* logits, const int32_t* idx_full, const float* w_full,
+                                  int T, int E, int k, double p, double* mass, int32_t* K_out,
+                                  int32_t* idx, float* w, hipStream_t s) {
+  if (!calibrate_route_fused(T, E, k)) {
+    hipError_t err = launch_calibrate(idx_full, w_full, T, E, k, nullptr, 1, p, mass, K_out, nullptr,
+                                      nullptr, s);
+    if (err != hipSuccess || T == 0) return err;
+    // logits are only read when the router is not run (x = NULL)
+    return launch_route(nullptr, false, nullptr, nullptr, nullptr, T, 0, E, k, nullptr, 1, K_out,
+                        const_cast<float*>(logits), idx, w, nullptr, s);
+  }
+  int key_bits = 0;
+  while ((1 << key_bits) < E) ++key_bits;
+  const unsigned grid = (unsigned)((T + CAL_WAVES - 1) / CAL_WAVES);
+  if (E <= 128)
+    calibrate_route_kernel<2><<<grid, CAL_THREADS, 0, s>>>(logits, idx_full, w_full, T, E, k, key_bits, p,
+                                                           mass, K_out, idx, w);
+  else if (E <= 256)
+    calibrate_route_kernel<4><<<grid, CAL_THREADS, 0, s>>>(logits, idx_full, w_full, T, E, k, key_bits, p,
+                                                           mass, K_out, idx, w);
+  else
+    calibrate_route_kernel<8><<<grid, CAL_THREADS, 0, s>>>(logits, idx_full, w_full, T, E, k, key_bits, p,
+                                                           mass, K_out, idx, w);
+  return hipGetLastError();
+}
 
 // Split factor of the router's d-range: enough workgroups to cover the chip
 // (about 512), in whole 128-wide quarters of d.  1 = no split.

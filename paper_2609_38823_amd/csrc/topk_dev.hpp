@@ -1,0 +1,94 @@
+// Wavefront Top-k primitives shared by the routing kernels (Eq. 10 and the
+// prefix re-route of Sec. 3.3): a total order on (value, index) pairs, DPP
+// arg-max and sum over a wavefront, and the selection of the k best of one
+// token's first Klim logits with their softmax weights.
+#pragma once
+
+#include <float.h>
+
+#include "common.hpp"
+
+namespace decomoe {
+namespace {
+
+__device__ __forceinline__ void better(float& v, int& i, float ov, int oi) {
+  if (ov > v || (ov == v && oi < i)) { v = ov; i = oi; }
+}
+
+// (value, index) of lane l -> the wavefront's best pair in every lane
+// without LDS round trips: DPP moves within each row of 16 lanes (quad
+// swaps, then the half-row and row mirrors pair the groups), then the four
+// row results are read with v_readlane and combined (the same in every
+// lane).  `better` is a total order on pairs, so the pairing order does not
+// change the result.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+template <int CTRL>
+__device__ __forceinline__ void dpp_better(float& v, int& i) {
+  better(v, i, dpp_f<CTRL>(v), __builtin_amdgcn_mov_dpp(i, CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float lane_f(float v, int l) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+}
+__device__ __forceinline__ void wave_best(float& v, int& i) {
+  dpp_better<0xB1>(v, i);   // quad_perm [1, 0, 3, 2]
+  dpp_better<0x4E>(v, i);   // quad_perm [2, 3, 0, 1]
+  dpp_better<0x141>(v, i);  // row_half_mirror
+  dpp_better<0x140>(v, i);  // row_mirror
+  float bv = lane_f(v, 0);
+  int bi = __builtin_amdgcn_readlane(i, 0);
+#pragma unroll
+  for (int r = 1; r < 4; ++r) better(bv, bi, lane_f(v, 16 * r), __builtin_amdgcn_readlane(i, 16 * r));
+  v = bv;
+  i = bi;
+}
+// sum over the wavefront: row sums by DPP, then the four rows in order
+__device__ __forceinline__ float wave_sum(float v) {
+  v += dpp_f<0xB1>(v);
+  v += dpp_f<0x4E>(v);
+  v += dpp_f<0x141>(v);
+  v += dpp_f<0x140>(v);
+  return ((lane_f(v, 0) + lane_f(v, 16)) + lane_f(v, 32)) + lane_f(v, 48);
+}
+
+// The k largest of row[0, Klim) of one token, one wavefront: lane l holds
+// experts l, l + 64, ...; k rounds of a wavefront arg-max (value descending,
+// index ascending on ties) pick the slots in order; the weights are the
+// softmax of the k selected logits.  Lane r < k writes slot r.
+template <int MAXC>  // values per lane: E <= 64 MAXC
+__device__ __forceinline__ void topk_select(const float* row, int E, int k, int Klim, int lane,
+                                            int32_t* idx_t, float* w_t) {
+  float v[MAXC];
+  uint32_t alive = 0;
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c) {
+    int e = lane + c * 64;
+    v[c] = -FLT_MAX;
+    if (e < Klim) { v[c] = row[e]; alive |= 1u << c; }
+  }
+  float my_v = 0.f;
+  int my_i = 0;
+  for (int r = 0; r < k; ++r) {
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c)
+      if (alive & (1u << c)) better(bv, bi, v[c], lane + c * 64);
+    wave_best(bv, bi);
+    if (bi < E && (bi & 63) == lane) alive &= ~(1u << (bi >> 6));
+    if (lane == r) { my_v = bv; my_i = bi; }
+  }
+  const float v0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_v), 0));
+  float ex = lane < k ? expf(my_v - v0) : 0.f;
+  float sum = ex;
+  sum = wave_sum(sum);
+  if (lane < k) {
+    idx_t[lane] = my_i;
+    w_t[lane] = ex / sum;
+  }
+}
+
+}  // namespace
+}  // namespace decomoe

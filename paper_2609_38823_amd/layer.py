@@ -13,6 +13,8 @@ the order of Algorithm 2 of the paper:
       moe_route(x) [full pool] -> moe_calibrate_prefix [s, K]
       -> moe_route(logits, K) [prefix re-route] -> moe_dispatch
       -> moe_expert_ffn(K) -> moe_combine
+      (one invocation: moe_calibrate_route_prefix does s, K and the
+      re-route in one call)
 
 All calls are asynchronous on one stream and K never leaves the device.
 """
@@ -233,11 +235,15 @@ class MoELayer:
         mk = mark or (lambda: None)
         self._route(x, b, b.idx_full, b.w_full, stream=stream)
         mk()
-        abi.moe_calibrate_prefix(b.idx_full, b.w_full, self.E, p, b.mass, b.ws, K_out=K,
-                                 seg_offsets=seg_offsets, stream=stream)
-        mk()
-        abi.moe_route(None, None, None, self.k, b.logits, b.idx, b.w, seg_offsets=seg_offsets,
-                      K_dev=K, stream=stream)
+        if seg_offsets is None:
+            # one invocation: masses, K and the prefix re-route in one call
+            abi.moe_calibrate_route_prefix(b.logits, b.idx_full, b.w_full, p, b.mass, K, b.idx, b.w,
+                                           stream=stream)
+        else:
+            abi.moe_calibrate_prefix(b.idx_full, b.w_full, self.E, p, b.mass, b.ws, K_out=K,
+                                     seg_offsets=seg_offsets, stream=stream)
+            abi.moe_route(None, None, None, self.k, b.logits, b.idx, b.w, seg_offsets=seg_offsets,
+                          K_dev=K, stream=stream)
         mk()
         self._experts(x, b, b.idx, b.w, K_dev=K, stream=stream, mark=mark, residual=residual,
                       out=out)

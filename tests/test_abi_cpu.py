@@ -33,7 +33,7 @@ def test_header_declares_the_boundary():
         "moe_dispatch", "moe_expert_ffn", "moe_expert_ffn_packed", "moe_pack_expert_weights",
         "moe_pack_router", "moe_permute_experts", "moe_route", "moe_route_packed", "moe_savb_gate",
         "moe_savb_workspace_size", "moe_status_string", "moe_workspace_size", "drop_visual_block_if",
-        "moe_expand_dense_routing", "moe_expert_ffn_packed_gather"])
+        "moe_expand_dense_routing", "moe_expert_ffn_packed_gather", "moe_calibrate_route_prefix"])
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -107,6 +107,20 @@ def test_calibrate_rejects(lib):
     assert lib.moe_calibrate_prefix(P1, P2, 8, 16, 20, NULL, 1, 0.9, P3, P4, NULL, WS, 1 << 30, NULL) == EINVAL
     assert lib.moe_calibrate_prefix(P1, P2, 8, 16, 2, P5, 0, 0.9, P3, P4, NULL, WS, 1 << 30, NULL) == EINVAL
     assert lib.moe_calibrate_prefix(P1, P2, 8, 16, 2, NULL, 1, 0.9, P1, P4, NULL, WS, 1 << 30, NULL) == EALIAS
+
+
+def test_calibrate_route_prefix_rejects(lib):
+    f = lib.moe_calibrate_route_prefix
+    # (logits, idx_full, w_full, T, E, k, p, mass, K_out, idx, w, ws, ws_bytes, s)
+    assert f(P1, P2, P3, 8, 16, 2, 0.0, P4, P5, P6, P7, NULL, 0, NULL) == EINVAL   # p outside (0, 1]
+    assert f(P1, P2, P3, 8, 16, 2, 1.5, P4, P5, P6, P7, NULL, 0, NULL) == EINVAL
+    assert f(P1, P2, P3, 8, 16, 17, 0.9, P4, P5, P6, P7, NULL, 0, NULL) == EINVAL  # k > E
+    assert f(P1, P2, P3, 8, 128, 33, 0.9, P4, P5, P6, P7, NULL, 0, NULL) == EUNSUPPORTED
+    assert f(P1, P2, P3, 8, 16, 2, 0.9, NULL, P5, P6, P7, NULL, 0, NULL) == EINVAL   # no mass
+    assert f(P1, P2, P3, 8, 16, 2, 0.9, P4, NULL, P6, P7, NULL, 0, NULL) == EINVAL   # no K_out
+    assert f(P1, P2, P3, 8, 16, 2, 0.9, P4, P5, P2, P7, NULL, 0, NULL) == EALIAS     # idx on idx_full
+    assert f(P1, P2, P3, 8, 16, 2, 0.9, P1, P5, P6, P7, NULL, 0, NULL) == EALIAS     # mass on logits
+    assert f(ctypes.c_void_p(0x10004), P2, P3, 8, 16, 2, 0.9, P4, P5, P6, P7, NULL, 0, NULL) == EINVAL
 
 
 def test_dispatch_rejects(lib):

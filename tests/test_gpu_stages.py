@@ -341,6 +341,43 @@ def test_calibrate_worked_example_golden():
 
 
 # ---------------------------------------------------------------------------
+# moe_calibrate_route_prefix: one call, bitwise the two calls it replaces
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("T,E,k,p", [
+    (512, 128, 8, 0.9),    # one launch (4096 entries)
+    (64, 128, 8, 0.85),    # one launch, decode-sized
+    (1, 16, 2, 0.5),       # a single token
+    (1024, 128, 8, 1.0),   # one launch at the 8192-entry limit, p = 1
+    (37, 300, 5, 0.7),     # E > 256: eight values per lane
+    (2000, 64, 8, 0.9),    # 16000 entries: the two-launch path
+    (100, 600, 4, 0.9),    # E > 512: the two-launch path
+])
+def test_calibrate_route_prefix_matches_two_calls(T, E, k, p):
+    logits = I.logits_with_ties(T, E, seed=T + E, levels=64)
+    lg = dev(logits)
+    idx_f, w_f = i32((T, k)), torch.empty((T, k), dtype=torch.float32, device="cuda")
+    abi.moe_route(None, None, None, k, lg, idx_f, w_f)
+    mass_a = torch.empty((1, E), dtype=torch.float64, device="cuda")
+    K_a = i32((1,))
+    idx_a, w_a = i32((T, k)), torch.empty((T, k), dtype=torch.float32, device="cuda")
+    ws = torch.empty(abi.moe_workspace_size(T, E, k, 64, 64, 1), dtype=torch.uint8, device="cuda")
+    abi.moe_calibrate_prefix(idx_f, w_f, E, p, mass_a, ws, K_out=K_a)
+    abi.moe_route(None, None, None, k, lg, idx_a, w_a, K_dev=K_a)
+    mass_b = torch.full((1, E), -1.0, dtype=torch.float64, device="cuda")
+    K_b = i32((1,))
+    idx_b, w_b = i32((T, k)), torch.empty((T, k), dtype=torch.float32, device="cuda")
+    abi.moe_calibrate_route_prefix(lg, idx_f, w_f, p, mass_b, K_b, idx_b, w_b)
+    torch.cuda.synchronize()
+    assert torch.equal(K_a, K_b)
+    assert torch.equal(mass_a.view(torch.int64), mass_b.view(torch.int64))
+    assert torch.equal(idx_a, idx_b)
+    assert torch.equal(w_a.view(torch.int32), w_b.view(torch.int32))
+    # and against the oracle's K on the same routing (Eqs. 11, 12)
+    s = oracle.activated_mass(host(idx_f), host(w_f).astype(np.float64), E)
+    assert int(K_b.cpu()[0]) == int(oracle.prefix_length(s, p, k))
+
+
+# ---------------------------------------------------------------------------
 # moe_dispatch: bit-exact counting sort and bitwise gather
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("T,E,k,d,dt,K", [
