@@ -24,6 +24,7 @@
 //                      tile starts as soon as its h is complete), or one
 //                      launch per GEMM where the XCD count is unknown
 // float32: a plain LDS-tiled SIMT kernel (correctness path for small layers).
+#include <cstdlib>
 #include <type_traits>
 
 #include "common.hpp"
@@ -1090,8 +1091,11 @@ hipError_t launch_gemm(int mode, int bm, bool wide, const Tiles& tl, const uint1
 #undef FFN_GEMM
 
 // Persistent launch geometry: two workgroups per compute unit and the XCD
-// count (false when the runtime cannot report them)
+// count (false when the runtime cannot report them, or when the environment
+// variable DECOMOE_FFN_TWO_LAUNCH is "1", which selects the two-launch path)
 bool persistent_shape(int& grid, int& n_xcc) {
+  const char* two = std::getenv("DECOMOE_FFN_TWO_LAUNCH");
+  if (two && two[0] == '1') return false;
   int dev = 0, cus = 0, nx = 0;
   if (hipGetDevice(&dev) != hipSuccess) return false;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)

@@ -580,6 +580,34 @@ def test_expert_ffn_packed_gather(T, E, k, d, m, K):
     assert rel_inf(host(y)[live], ref) <= TOL["bf16"]
 
 
+@pytest.mark.parametrize("T,E,k,d,m", [(512, 128, 8, 2048, 768), (4096, 128, 8, 2048, 768),
+                                       (37, 6, 3, 512, 256)])
+def test_packed_ffn_two_launch_fallback_matches_persistent(T, E, k, d, m, monkeypatch):
+    """The one-launch-per-GEMM path (used where the XCD count is unknown)
+    gives bitwise the persistent kernel's result."""
+    sh = I.LayerShape(d=d, E=E, m=m, k=k, dtype="bf16")
+    prm = I.layer_params(sh, seed=2)
+    idx, _ = I.synthetic_routing(T, E, k, seed=T + 1)
+    x = dev(I.synthetic_rows(T, d, "bf16", seed=T + 2), torch.bfloat16)
+    A = T * k
+    counts, offsets, src, ros = i32((E,)), i32((E + 1,)), i32((A,)), i32((A,))
+    ws = torch.empty(abi.moe_workspace_size(T, E, k, d, m, 1), dtype=torch.uint8, device="cuda")
+    abi.moe_dispatch(dev(idx), E, None, counts, offsets, src, ros, None, ws)
+    wgu, wd = dev(prm["w_gate_up"], torch.bfloat16), dev(prm["w_down"], torch.bfloat16)
+    wgu_p, wd_p = torch.empty_like(wgu), torch.empty_like(wd)
+    abi.moe_pack_expert_weights(wgu, wgu_p)
+    abi.moe_pack_expert_weights(wd, wd_p)
+    y1 = torch.full((A, d), 7.0, dtype=torch.bfloat16, device="cuda")
+    y2 = torch.full((A, d), 7.0, dtype=torch.bfloat16, device="cuda")
+    abi.moe_expert_ffn_packed_gather(x, k, src, offsets, wgu_p, wd_p, y1, ws)
+    torch.cuda.synchronize()
+    monkeypatch.setenv("DECOMOE_FFN_TWO_LAUNCH", "1")
+    abi.moe_expert_ffn_packed_gather(x, k, src, offsets, wgu_p, wd_p, y2, ws)
+    torch.cuda.synchronize()
+    monkeypatch.delenv("DECOMOE_FFN_TWO_LAUNCH")
+    assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+
+
 def test_expert_ffn_packed_gather_out_of_range_rows_read_token_zero():
     T, E, k, d, m = 64, 4, 2, 512, 256
     sh = I.LayerShape(d=d, E=E, m=m, k=k, dtype="bf16")
