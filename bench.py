@@ -102,17 +102,36 @@ def roofline(flops: float, nbytes: float, sec: float) -> dict:
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_moe_expert_ffn_qwen3vl_4096.json")
 
 
-def measured_traffic():
-    """HBM bytes per FFN call from the committed counter passes, or None
-    when the GEMM sources changed since they were taken."""
+def _counter_record():
+    """The committed counter passes' summary, or None when the GEMM sources
+    changed since they were taken."""
     try:
         from paper_2609_38823_amd.profiling import source_hash
         rec = json.load(open(TRAFFIC_FILE))
-        if rec.get("source_sha256") != source_hash():
-            return None
-        return rec["traffic_bytes_per_call"]
-    except (OSError, ValueError, KeyError):
+        return rec if rec.get("source_sha256") == source_hash() else None
+    except (OSError, ValueError):
         return None
+
+
+def measured_traffic():
+    """HBM bytes per FFN call from the committed counter passes, or None."""
+    rec = _counter_record()
+    return rec.get("traffic_bytes_per_call") if rec else None
+
+
+def measured_counters():
+    """MFMA counters of the expert GEMM and per-stage achieved GB/s of the
+    dense span at 4096 rows from the committed counter passes, or None."""
+    rec = _counter_record()
+    if not rec:
+        return None
+    m = rec.get("mfma") or {}
+    return dict(
+        mfma_busy_frac_at_peak_clock=m.get("mfma_busy_frac_at_peak_clock"),
+        mfma_util_rocprof=m.get("mfma_util_rocprof"),
+        mfma_flops_executed=m.get("mfma_flops_executed"),
+        stages_hbm_frac={r["stage"]: round(r["hbm_frac"], 3) for r in rec.get("stages", [])},
+        source="profiles/traffic_moe_expert_ffn_qwen3vl_4096.txt (rocprofv3 --pmc passes)")
 
 
 def cpu_info() -> dict:
@@ -315,6 +334,7 @@ def bench_layer(args) -> int:
     f, b = fb("ffn", T, touched_d)
     ffn_roof = roofline(f, b, stage_ms["ffn"] * 1e-3)
     ffn_roof["traffic"] = measured_traffic()
+    ffn_roof["counters"] = measured_counters()
     ffn_roof["kernel"] = ("moe_expert_ffn_packed_gather @ dense 4096 rows (gate/up GEMM reading the token "
                           "rows through src_of_row + down GEMM, on packed bf16 weights)")
     ffn_roof["mfma_frac"] = f / (stage_ms["ffn"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS
