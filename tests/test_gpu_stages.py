@@ -492,6 +492,7 @@ SKEW_CASES = [
     (4, 512, 256, "bf16", 130, None, [0, 65, 0, 65]),
     (32, 512, 256, "bf16", 6000, None, [1500, 0, 0, 1500, 0, 1500] + [0] * 25 + [1500]),
     (16, 512, 256, "bf16", 3000, 5, [600, 600, 600, 600, 600] + [0] * 11),
+    (1000, 256, 256, "bf16", 700, None, None),                        # 1000 experts, mostly empty
 ]
 
 PACKED_CASES = [c for c in FFN_CASES if c[3] == "bf16" and c[2] % 256 == 0] + SKEW_CASES + [
@@ -578,6 +579,32 @@ def test_expert_ffn_packed_gather(T, E, k, d, m, K):
         live = np.random.default_rng(T).choice(live, 2048, replace=False)
     ref = oracle.expert_ffn_rows(host(x)[rs[live] // k], e_of_row[live], prm["w_gate_up"], prm["w_down"])
     assert rel_inf(host(y)[live], ref) <= TOL["bf16"]
+
+
+def test_packed_ffn_per_segment_K_uses_the_largest():
+    """K_dev with one K per segment: experts below the largest K are
+    evaluated (the same result as that K alone), none above it."""
+    E, d, m = 12, 512, 256
+    sh = I.LayerShape(d=d, E=E, m=m, k=1, dtype="bf16")
+    prm = I.layer_params(sh, seed=9)
+    counts = np.array([40, 0, 70, 5, 130, 9, 1, 33, 0, 64, 2, 17], np.int64)
+    rows = int(counts.sum())
+    offsets = dev(np.concatenate([[0], np.cumsum(counts)]).astype(np.int32))
+    xp = dev(I.synthetic_rows(rows, d, "bf16", seed=10), torch.bfloat16)
+    wgu, wd = dev(prm["w_gate_up"], torch.bfloat16), dev(prm["w_down"], torch.bfloat16)
+    wgu_p, wd_p = torch.empty_like(wgu), torch.empty_like(wd)
+    abi.moe_pack_expert_weights(wgu, wgu_p)
+    abi.moe_pack_expert_weights(wd, wd_p)
+    ws = torch.empty(abi.moe_workspace_size(rows, E, 1, d, m, 3), dtype=torch.uint8, device="cuda")
+    y_seg = torch.full((rows, d), 7.0, dtype=torch.bfloat16, device="cuda")
+    y_one = torch.full((rows, d), 7.0, dtype=torch.bfloat16, device="cuda")
+    abi.moe_expert_ffn_packed(xp, offsets, wgu_p, wd_p, y_seg, ws, K_dev=dev(np.array([2, 7, 3], np.int32)))
+    abi.moe_expert_ffn_packed(xp, offsets, wgu_p, wd_p, y_one, ws, K_dev=dev(np.array([7], np.int32)))
+    torch.cuda.synchronize()
+    assert torch.equal(y_seg.view(torch.int16), y_one.view(torch.int16))
+    past = int(np.cumsum(counts)[6])  # rows of experts >= 7 are left unwritten
+    assert (host(y_seg)[past:] == 7.0).all()
+    assert not (host(y_seg)[:past] == 7.0).all(axis=1).any()
 
 
 @pytest.mark.parametrize("T,E,k,d,m", [(512, 128, 8, 2048, 768), (4096, 128, 8, 2048, 768),
