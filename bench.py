@@ -37,9 +37,15 @@ Other workloads (one JSON line each, same fields):
                        50, full) on the 48-layer stack, expert orders at
                        keep ratios and the p sweep; value = speedup of the
                        full method over the dense stack
+  --workload gemm_ceiling
+                       the expert FFN with every row on one expert (weights
+                       cache-resident) at 32768 and 65536 rows, beside the
+                       same SwiGLU through torch.matmul (the vendor GEMM
+                       library) on the same shapes; value = the packed FFN's
+                       TFLOP/s at 32768 rows
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
-                       [--workload layer|stack48|decode64|stress|variants]
+                       [--workload layer|stack48|decode64|stress|variants|gemm_ceiling]
 """
 
 from __future__ import annotations
@@ -173,14 +179,15 @@ def main() -> int:
     ap.add_argument("--traffic-run", action="store_true",
                     help="only run the dense layer and a known-size copy (for rocprofv3 counter passes)")
     ap.add_argument("--workload", default="layer",
-                    choices=["layer", "stack48", "decode64", "stress", "variants"])
+                    choices=["layer", "stack48", "decode64", "stress", "variants", "gemm_ceiling"])
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the path has no multi-GPU execution "
               "(the design notes describe how it would shard); run with --gpus 1", file=sys.stderr)
         return 2
     fn = {"layer": bench_layer, "stack48": bench_stack48, "decode64": bench_decode64,
-          "stress": bench_stress, "variants": bench_variants}[args.workload]
+          "stress": bench_stress, "variants": bench_variants,
+          "gemm_ceiling": bench_gemm_ceiling}[args.workload]
     return fn(args)
 
 
@@ -844,6 +851,92 @@ def bench_variants(args) -> int:
          "seed": wl.seed, "zipf_alpha": sh.zipf_alpha},
         None, None, ablation=rows, p_sweep_stack=p_sweep, orders_at_keep_ratio=order_rows,
         setup_s=round(setup_s, 1))
+
+
+
+def bench_gemm_ceiling(args) -> int:
+    """The packed expert FFN with all rows on one expert beside the vendor
+    GEMM library (torch.matmul) on the same SwiGLU shapes: what a library
+    bf16 GEMM reaches on this chip for the FFN's own contraction sizes."""
+    import torch
+
+    from paper_2609_38823_amd import abi, inputs as I
+    from paper_2609_38823_amd.layer import MoELayer, to_device
+    _setup_gpu()
+    stream = torch.cuda.current_stream()
+    wl = I.WORKLOADS["qwen3vl_dense_4096"]
+    sh = wl.shape
+    d, E, m, k = sh.d, sh.E, sh.m, sh.k
+    prm = I.layer_params(sh, seed=wl.seed)
+    layer = MoELayer(prm, k, sh.dtype)
+    # expert 0's weights, row-major, for the library: right operands stored
+    # contiguous as [K, N]
+    wguT = to_device(prm["w_gate_up"][0], torch.bfloat16).t().contiguous()  # [d, 2m]
+    wdnT = to_device(prm["w_down"][0], torch.bfloat16).t().contiguous()  # [m, d]
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / args.steps
+
+    def tf(flops, ms):
+        return dict(ms=round(ms, 4), tflops=round(flops / (ms * 1e-3) / 1e12, 1),
+                    frac_of_bf16_peak=round(flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 3))
+
+    res = {}
+    for rows in (32768, 65536):
+        x = to_device(I.synthetic_rows(rows, d, "bf16", seed=2), torch.bfloat16)
+        y = torch.empty((rows, d), dtype=torch.bfloat16, device="cuda")
+        y_lib = torch.empty_like(y)
+        gu = torch.empty((rows, 2 * m), dtype=torch.bfloat16, device="cuda")
+        ws = torch.empty((abi.moe_workspace_size(rows, E, 1, d, m, 1),), dtype=torch.uint8, device="cuda")
+        counts = np.zeros(E, np.int64)
+        counts[0] = rows
+        off = torch.from_numpy(np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)).cuda()
+        f_all, f_gu, f_dn = 6.0 * rows * d * m, 4.0 * rows * d * m, 2.0 * rows * d * m
+        ms_ffn = timed(lambda: abi.moe_expert_ffn_packed(x, off, layer.w_gate_up, layer.w_down, y, ws))
+        h = torch.empty((rows, m), dtype=torch.bfloat16, device="cuda")
+
+        def lib_swiglu():
+            torch.matmul(x, wguT, out=gu)
+            torch.mul(torch.nn.functional.silu(gu[:, :m]), gu[:, m:], out=h)
+            torch.matmul(h, wdnT, out=y_lib)
+
+        ms_lib = timed(lib_swiglu)
+        ms_gu = timed(lambda: torch.matmul(x, wguT, out=gu))
+        ms_dn = timed(lambda: torch.matmul(h, wdnT, out=y_lib))
+        lib_swiglu()
+        abi.moe_expert_ffn_packed(x, off, layer.w_gate_up, layer.w_down, y, ws)
+        torch.cuda.synchronize()
+        yf, lf = y.float(), y_lib.float()
+        rel = float((yf - lf).abs().max() / lf.abs().max())
+        res[str(rows)] = {
+            "packed FFN, one expert (both GEMMs, SiLU*up fused)": tf(f_all, ms_ffn),
+            "library SwiGLU (gate/up GEMM, SiLU*up, down GEMM)": tf(f_all, ms_lib),
+            "library gate/up GEMM alone": tf(f_gu, ms_gu),
+            "library down GEMM alone": tf(f_dn, ms_dn),
+            "max rel diff packed vs library output": rel,
+        }
+        _log(f"{rows} rows: packed {ms_ffn * 1e3:.1f} us, library SwiGLU {ms_lib * 1e3:.1f} us")
+        del x, y, y_lib, gu, ws, h
+        torch.cuda.empty_cache()
+    r32 = res["32768"]["packed FFN, one expert (both GEMMs, SiLU*up fused)"]
+    ach = r32["tflops"]
+    roof = {"bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": ach / PEAK_BF16_TFLOPS, "traffic": None,
+            "kernel": "moe_expert_ffn_packed, 32768 rows on one expert (ffn_fused_kernel<128>)"}
+    return _line(
+        "Expert FFN TFLOP/s with cache-resident weights, beside the vendor GEMM library on the same shapes",
+        ach, "TFLOP/s", args, r32["ms"],
+        {"workload": "one expert of the Qwen3-VL-MoE layer (d 2048, m 768, bf16) at 32768 and 65536 rows; "
+                     "the library leg is torch.matmul on the same operands plus torch's SiLU and product",
+         "seed": 2}, roof, None, cases=res)
 
 
 if __name__ == "__main__":
