@@ -78,7 +78,8 @@ const char* moe_status_string(int status);
 
 /* Bytes of scratch sufficient for every entry point called with sizes up to
  * T tokens, E experts, k slots, hidden size d, expert width m and n_seg
- * segments.  Returns 0 for invalid sizes. */
+ * segments.  Returns 0 for invalid sizes, including T * k above INT32_MAX
+ * (every entry point indexes the routing entries with 32-bit integers). */
 size_t moe_workspace_size(int T, int E, int k, int d, int m, int n_seg);
 
 /*

@@ -96,6 +96,8 @@ const char* moe_status_string(int status) {
 
 size_t moe_workspace_size(int T, int E, int k, int d, int m, int n_seg) {
   if (T < 0 || E < 1 || E > kMaxE || k < 1 || k > E || d < 1 || m < 1 || n_seg < 1) return 0;
+  // every entry point indexes the T * k routing entries with 32-bit ints
+  if ((size_t)T * k > (size_t)INT32_MAX) return 0;
   size_t rows = (size_t)T * k;
   size_t w = 256;
   for (size_t b : {a256(dispatch_ws_bytes(T, k, E)), ffn_ws_bytes(true, (int)rows, E, d, m),

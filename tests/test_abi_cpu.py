@@ -59,6 +59,8 @@ def test_workspace_size(lib):
     assert lib.moe_workspace_size(0, 128, 8, 2048, 768, 1) >= 256
     assert lib.moe_workspace_size(16, 128, 0, 2048, 768, 1) == 0  # k < 1
     assert lib.moe_workspace_size(16, 2000, 8, 2048, 768, 1) == 0  # E > 1024
+    assert lib.moe_workspace_size(2**28, 128, 8, 2048, 768, 1) == 0  # T * k above INT32_MAX
+    assert lib.moe_workspace_size(2**28 - 1, 128, 7, 2048, 768, 1) > 0
 
 
 # fake, never dereferenced, 16-byte aligned addresses

@@ -11,6 +11,8 @@ evaluates a seeded sample of tokens; the dense layer's routing is per token,
 so a sample needs no other rows.
 """
 
+from types import SimpleNamespace
+
 import numpy as np
 import pytest
 import torch
@@ -235,3 +237,37 @@ def test_dense_equivalent_executor_matches_sparse(qwen):
     # the same eight products per element, summed in another order: within
     # a few bf16 units of the sparse result
     assert np.abs(out_dense - out_sparse).max() <= 4 * 2.0 ** -8 * np.abs(out_sparse).max()
+
+
+def _sweep_cases():
+    """Seeded random layer shapes on both expert-FFN paths: bf16 with packed
+    weights (d, m multiples of 256) or row-major weights (m a multiple of 128
+    only), float32 with any d and m; routers on the split-weight, float32
+    MFMA and scalar paths by E and d."""
+    rng = np.random.default_rng(2609)
+    cases = []
+    for i in range(8):
+        E = int(rng.choice([4, 32, 64, 96, 160, 256]))
+        cases.append(("bf16", int(rng.choice([256, 512, 768])), E, int(rng.choice([128, 256, 384, 512])),
+                      int(rng.integers(1, min(8, E) + 1)), int(rng.choice([1, 37, 300, 1000])),
+                      float(rng.choice([0.5, 0.8, 0.9, 1.0])), bool(rng.integers(0, 2)), i))
+    for i in range(6):
+        E = int(rng.choice([3, 16, 50, 128]))
+        cases.append(("f32", int(rng.choice([24, 64, 200, 256])), E, int(rng.choice([12, 40, 96])),
+                      int(rng.integers(1, min(8, E) + 1)), int(rng.choice([1, 37, 300, 700])),
+                      float(rng.choice([0.5, 0.8, 0.9, 1.0])), bool(rng.integers(0, 2)), 100 + i))
+    return cases
+
+
+@pytest.mark.parametrize("dt,d,E,m,k,T,p,bias,seed", _sweep_cases())
+def test_layer_shape_sweep(dt, d, E, m, k, T, p, bias, seed):
+    """Dense and RCEP spans on random shapes against the oracle (same
+    protocol as the workload tests)."""
+    sh = I.LayerShape(d=d, E=E, m=m, k=k, dtype=dt, zipf_alpha=0.35 if bias else None)
+    wl = SimpleNamespace(shape=sh, seed=seed)
+    x = I.tokens(sh, T, seed=seed)
+    print(f"sweep case {dt} d={d} E={E} m={m} k={k} T={T} p={p} bias={bias}", flush=True)
+    rp, layer = calibrated_layer(wl, x)
+    xd = torch.from_numpy(x).cuda().to(TDT[dt])
+    check_dense(layer, rp, x, xd, k, dt)
+    check_rcep(layer, rp, x, xd, k, p, dt)
