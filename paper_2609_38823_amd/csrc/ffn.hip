@@ -494,9 +494,6 @@ constexpr int a_slot() {
 // seven k-steps ahead, to keep more weight bytes in flight
 template <int BM>
 constexpr int packed_nb() { return BM >= 128 ? 4 : 8; }
-// workgroups per CU: the register file holds two of either kind
-template <int BM>
-constexpr int packed_occupancy() { return 2; }
 
 __device__ __forceinline__ u32x4 load_frag(__amdgpu_buffer_rsrc_t rs, int voff, int soff) {
   return __builtin_amdgcn_raw_buffer_load_b128(rs, voff, soff, 0);
