@@ -176,13 +176,15 @@ def main(argv) -> int:
         json.dump(res, f, indent=1)
     with open(out + ".txt", "w") as f:
         f.write("# HBM traffic of moe_expert_ffn_packed_gather @ 4096 rows (Qwen3-VL-MoE layer), per call\n")
+        fd, wd = os.path.relpath(fetch_dir), os.path.relpath(write_dir)
+        md = os.path.relpath(mfma_dir) if mfma_dir else None
         f.write("# commands (from the repository root R, one pass each):\n")
-        f.write("#   cd /tmp && rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/gpurun_out/pmc_fetch -o p"
+        f.write(f"#   cd /tmp && rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/{fd} -o p"
                 " -- python3 $R/bench.py --traffic-run\n")
-        f.write("#   cd /tmp && rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/gpurun_out/pmc_write -o p"
+        f.write(f"#   cd /tmp && rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/{wd} -o p"
                 " -- python3 $R/bench.py --traffic-run\n")
-        f.write("#   python -m paper_2609_38823_amd.profiling gpurun_out/pmc_fetch gpurun_out/pmc_write "
-                + os.path.relpath(out) + (" gpurun_out/pmc_mfma" if mfma_dir else "") + "\n")
+        f.write(f"#   python -m paper_2609_38823_amd.profiling {fd} {wd} "
+                + os.path.relpath(out) + (f" {md}" if md else "") + "\n")
         f.write(f"# copy calibration: drop_visual_block of {COPY_BYTES} B: FETCH_SIZE {fetch[copy_key]:.0f} KiB,"
                 f" WRITE_SIZE {write[copy_key]:.0f} KiB -> scale fetch {f_scale:.3f}, write {w_scale:.3f}\n")
         for r in rows:
@@ -200,7 +202,7 @@ def main(argv) -> int:
             f.write("\n# expert GEMM MFMA counters (pass: SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE "
                     "SQ_INSTS_VALU_MFMA_MOPS_BF16)\n")
             f.write(f"#   cd /tmp && rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE "
-                    f"SQ_INSTS_VALU_MFMA_MOPS_BF16 --output-format csv -d $R/gpurun_out/pmc_mfma -o p -- "
+                    f"SQ_INSTS_VALU_MFMA_MOPS_BF16 --output-format csv -d $R/{md} -o p -- "
                     f"python3 $R/bench.py --traffic-run\n")
             f.write(f"{mfma['kernel']}: {mfma['mfma_flops_executed'] / 1e9:.1f} GFLOP of bf16 MFMA executed "
                     f"(309.2 algorithmic: the rest is 32-row padding) in {mfma['seconds'] * 1e6:.1f} us = "
