@@ -536,7 +536,7 @@ def paper_prefill_flops(S: int, T: int, exit_layer: int, Ks, L: int, E: int, d: 
     convention C_expert(K) = 6 K d m: layers before the exit at (S, E), from
     the exit on at (T, K_l); the baseline runs every layer at (S, E).  The
     attention projection sizes q and kv are the paper's Qwen3-VL-MoE values;
-    the attention itself is not part of this build, only of this replay."""
+    the attention itself is not computed here, only counted in this replay."""
     c_proj = 2 * (d * q + 2 * d * kv + q * d)
     c_router = 2 * d * E
 

@@ -182,7 +182,7 @@ int moe_route_packed(const void* x, moe_dtype dtype, const void* w_r_packed, con
  * token order, and c_K one running sum in expert order, so K depends on the
  * inputs only (no reduction-order effects).  Index entries outside [0, E)
  * are skipped.  Limits: 1 <= k <= min(E, 32).  ws / ws_bytes: scratch per
- * moe_workspace_size; this build needs none (NULL, 0 are accepted).
+ * moe_workspace_size; the current implementation needs none (NULL, 0 are accepted).
  */
 int moe_calibrate_prefix(const int32_t* topk_idx, const float* topk_w,
                          int T, int E, int k,

@@ -89,7 +89,7 @@ const char* moe_status_string(int status) {
     case MOE_EALIAS: return "an output overlaps an input or another output";
     case MOE_EWORKSPACE: return "workspace missing or too small";
     case MOE_EHIP: return "HIP runtime reported a launch error";
-    case MOE_EUNSUPPORTED: return "shape not supported by this build";
+    case MOE_EUNSUPPORTED: return "shape not supported by this library";
     default: return "unknown status";
   }
 }
