@@ -638,6 +638,7 @@ def bench_decode64(args) -> int:
     ach = nbytes / (ms * 1e-3) / 1e9
     roof = dict(bound="hbm", achieved=ach, peak=PEAK_HBM_GBS, unit="GB/s", frac=ach / PEAK_HBM_GBS,
                 traffic=None, kernel="whole decode step (48 layers, weight streaming of touched experts)")
+    variants = _decode_variants(st, x, wl, args, stream)
     cpu = None
     if not args.no_cpu_baseline:
         cpu = _oracle_decode_sample(st, x_np, wl)
@@ -649,7 +650,61 @@ def bench_decode64(args) -> int:
          "seed": wl.seed, "zipf_alpha": sh.zipf_alpha},
         roof, cpu, eager_ms_per_step=eager_ms, step_ms_min=float(np.min(step_ms)),
         K_per_layer=[int(v) for v in Ks], touched_per_layer=touched,
-        weight_bytes_per_step=wbytes, setup_s=round(setup_s, 1))
+        weight_bytes_per_step=wbytes, variants=variants, setup_s=round(setup_s, 1))
+
+
+def _decode_variants(st, x, wl, args, stream):
+    """Readings of the decode workload beside the batch-shared K (eager
+    steps, outside the timed value): one invocation per sequence (each of
+    the 64 tokens its own segment, so its own K; the expert FFN runs the
+    experts below the largest K) and RCEP only from layer 20 (layers 0-19
+    on the full pool)."""
+    import torch
+
+    T, E = x.shape[0], st.sh.E
+    seg = torch.arange(T + 1, dtype=torch.int32, device=x.device)
+    bufs = {}
+
+    def per_sequence(record=None):
+        h = x
+        for l, layer in enumerate(st.layers):
+            if l not in bufs:
+                bufs[l] = (layer.buffers(T, T), torch.empty_like(x))
+            b, dst = bufs[l]
+            layer.forward_rcep(h, wl.p, seg_offsets=seg, b=b, residual=h, out=dst)
+            if record is not None:
+                record(l, b)
+            h = dst
+        return h
+
+    Ks, touched = [], []
+    per_sequence(lambda l, b: (Ks.append(b.K[:T].cpu().numpy().copy()),
+                               touched.append(int((b.counts.cpu() > 0).sum()))))
+    Ks = np.stack(Ks)
+
+    def timed(fn):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / args.steps
+
+    ms_seq = timed(per_sequence)
+    ms_20 = timed(lambda: st.forward(x, 0, wl.p, exit_layer=20))
+    K20 = st.K_trace[20:, 0].cpu().numpy()
+    return {
+        "per-sequence K (64 invocations of one token)": dict(
+            ms_per_step=round(ms_seq, 3), tokens_per_s=T / (ms_seq * 1e-3),
+            K_min=int(Ks.min()), K_median=float(np.median(Ks)), K_max=int(Ks.max()),
+            touched_mean=float(np.mean(touched)), touched_per_layer=touched),
+        "RCEP from layer 20 (layers 0-19 on all experts)": dict(
+            ms_per_step=round(ms_20, 3), tokens_per_s=T / (ms_20 * 1e-3), K_mean_from_20=float(K20.mean())),
+    }
 
 
 def _oracle_decode_sample(st, x_np, wl):

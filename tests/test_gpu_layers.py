@@ -271,3 +271,40 @@ def test_layer_shape_sweep(dt, d, E, m, k, T, p, bias, seed):
     xd = torch.from_numpy(x).cuda().to(TDT[dt])
     check_dense(layer, rp, x, xd, k, dt)
     check_rcep(layer, rp, x, xd, k, p, dt)
+
+
+@pytest.mark.parametrize("sizes", [[1] * 64, [1, 7, 0, 20, 36]])
+def test_rcep_per_sequence_segments(qwen, sizes):
+    """One invocation per sequence (Eq. 11's token set is the segment): K per
+    segment from the oracle on the GPU's logits, each token re-routed inside
+    its own segment's prefix, the expert FFN over the experts below the
+    largest K, and the output against the oracle (64 decode tokens, one
+    segment per token or ragged segments with an empty one)."""
+    wl, _, rp, layer = qwen
+    sh = wl.shape
+    x_np = I.tokens(sh, 64, seed=5)
+    xd = torch.from_numpy(x_np).cuda().to(torch.bfloat16)
+    so = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    seg = torch.from_numpy(so).cuda()
+    p = 0.85
+    b = layer.forward_rcep(xd, p, seg_offsets=seg)
+    logits = host(b.logits).astype(np.float64)
+    idx_full, w_full = oracle.full_pool_route(logits, sh.k)
+    np.testing.assert_array_equal(host(b.idx_full), idx_full)
+    K = host(b.K).astype(np.int64)
+    K_ref = np.array([oracle.prefix_length(oracle.activated_mass(idx_full[lo:hi], w_full[lo:hi], sh.E),
+                                           p, sh.k) for lo, hi in zip(so[:-1], so[1:])])
+    for s, (lo, hi) in enumerate(zip(so[:-1], so[1:])):
+        mass = oracle.activated_mass(idx_full[lo:hi], w_full[lo:hi], sh.E)
+        assert K[s] == K_ref[s] or near_tie(mass, p, K_ref[s], sh.k), (s, K[s], K_ref[s])
+    ref = oracle.moe_layer_rcep(x_np, rp["w_r"], rp["bias"], rp["w_gate_up"], rp["w_down"], sh.k, p,
+                                seg_offsets=so, logits=logits, K_override=K)
+    gi = host(b.idx)
+    np.testing.assert_array_equal(gi, ref["idx"])
+    for s, (lo, hi) in enumerate(zip(so[:-1], so[1:])):
+        assert (gi[lo:hi] < K[s]).all()
+    counts = host(b.counts)
+    assert counts.sum() == 64 * sh.k and (counts[K.max():] == 0).all()
+    out = host(b.out)
+    assert rel_inf(out, ref["out"]) <= TOL["bf16"]
+    assert row_rel(out, ref["out"]) <= TOL["bf16"]
