@@ -265,6 +265,25 @@ def bench_layer(args) -> int:
     for i, name in enumerate(stages):
         stage_ms[name] = float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs]))
 
+    # the same step with the caches flushed first: a 512 MiB fill (twice the
+    # memory-side cache) before each step, each step timed by its own events
+    flush = torch.empty((512 << 20,), dtype=torch.uint8, device="cuda")
+    n_cold = min(args.steps, 10)
+    evc = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)] for _ in range(n_cold)]
+    for s in range(n_cold):
+        flush.fill_(s & 0xFF)
+        step(evc[s])
+    torch.cuda.synchronize()
+    del flush
+    warm_span = float(np.mean([e[0].elapsed_time(e[-1]) for e in evs]))
+    cold_span = float(np.mean([e[0].elapsed_time(e[-1]) for e in evc]))
+    cold_stage = {name: round(float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evc])), 4)
+                  for i, name in enumerate(stages)}
+    cache = {"warm_event_ms_per_step": round(warm_span, 4), "cold_event_ms_per_step": round(cold_span, 4),
+             "cold_tokens_per_s": (T + (T - V)) / (cold_span * 1e-3),
+             "cold_stage_ms": cold_stage, "cold_steps": n_cold,
+             "flush": "a 512 MiB fill before each cold step (the memory-side cache holds 256 MiB)"}
+
     # dense span over the 512 text rows alone (RCEP off), for the comparison
     K = int(br.K.cpu()[0])
     touched_d = int((bd.counts.cpu() > 0).sum())
@@ -377,6 +396,7 @@ def bench_layer(args) -> int:
         "cpu_baseline": cpu,
         "spans": spans,
         "stages": stage_rep,
+        "cache": cache,
         "setup_s": round(setup_s, 1),
     }
     print(json.dumps(line), flush=True)
