@@ -29,7 +29,11 @@
  *   - Every array pointer is a DEVICE pointer owned by the caller; the
  *     library never allocates, frees or retains device memory.  Arrays are
  *     row-major and contiguous.  Scratch memory comes from the caller as
- *     (ws, ws_bytes); moe_workspace_size() returns a sufficient size.
+ *     (ws, ws_bytes); moe_workspace_size() returns a sufficient size.  Its
+ *     contents need no initialisation and are not preserved between calls
+ *     (the expert FFN clears its own work counters on the stream first).
+ *     Calls ordered on one stream may share a workspace; calls that can run
+ *     concurrently (other streams) need workspaces of their own.
  *   - Activations and expert weights are MOE_F32 or MOE_BF16 (the `dtype`
  *     argument); router weights, bias, logits and routing weights are
  *     float32; masses are float64; indices, counts and lengths are int32.
