@@ -205,9 +205,12 @@ __global__ __launch_bounds__(256) void topk_kernel(float* __restrict__ logits, i
   }
   float* row = logits + (size_t)t * E;
   if (part) {
+    // the logits are selected from registers (no reload of the stored row)
+    float v[MAXC];
 #pragma unroll
     for (int c = 0; c < MAXC; ++c) {
       const int e = lane + c * 64;
+      v[c] = 0.f;
       if (e < E) {
         float a = part[(size_t)t * E + e];
         // partials in order sp = 1..S-1; loads issued four at a time
@@ -220,9 +223,12 @@ __global__ __launch_bounds__(256) void topk_kernel(float* __restrict__ logits, i
           for (int u = 0; u < 4; ++u)
             if (sp + u < S) a += pv[u];
         }
-        row[e] = a + (bias ? bias[e] : 0.f);
+        v[c] = a + (bias ? bias[e] : 0.f);
+        row[e] = v[c];
       }
     }
+    topk_select_vals<MAXC>(v, E, k, Klim, lane, idx + (size_t)t * k, w + (size_t)t * k);
+    return;
   }
   topk_select<MAXC>(row, E, k, Klim, lane, idx + (size_t)t * k, w + (size_t)t * k);
 }

@@ -53,20 +53,21 @@ __device__ __forceinline__ float wave_sum(float v) {
   return ((lane_f(v, 0) + lane_f(v, 16)) + lane_f(v, 32)) + lane_f(v, 48);
 }
 
-// The k largest of row[0, Klim) of one token, one wavefront: lane l holds
-// experts l, l + 64, ...; k rounds of a wavefront arg-max (value descending,
-// index ascending on ties) pick the slots in order; the weights are the
-// softmax of the k selected logits.  Lane r < k writes slot r.
+// The k largest of one token's logits [0, Klim), one wavefront: lane l
+// holds experts l, l + 64, ... in vals[c] (expert l + 64 c); k rounds of a
+// wavefront arg-max (value descending, index ascending on ties) pick the
+// slots in order; the weights are the softmax of the k selected logits.
+// Lane r < k writes slot r.  Values at experts >= Klim are never read.
 template <int MAXC>  // values per lane: E <= 64 MAXC
-__device__ __forceinline__ void topk_select(const float* row, int E, int k, int Klim, int lane,
-                                            int32_t* idx_t, float* w_t) {
+__device__ __forceinline__ void topk_select_vals(const float (&vals)[MAXC], int E, int k, int Klim, int lane,
+                                                 int32_t* idx_t, float* w_t) {
   float v[MAXC];
   uint32_t alive = 0;
 #pragma unroll
   for (int c = 0; c < MAXC; ++c) {
     int e = lane + c * 64;
     v[c] = -FLT_MAX;
-    if (e < Klim) { v[c] = row[e]; alive |= 1u << c; }
+    if (e < Klim) { v[c] = vals[c]; alive |= 1u << c; }
   }
   float my_v = 0.f;
   int my_i = 0;
@@ -88,6 +89,19 @@ __device__ __forceinline__ void topk_select(const float* row, int E, int k, int 
     idx_t[lane] = my_i;
     w_t[lane] = ex / sum;
   }
+}
+
+// the same on row[0, Klim) in memory
+template <int MAXC>
+__device__ __forceinline__ void topk_select(const float* row, int E, int k, int Klim, int lane,
+                                            int32_t* idx_t, float* w_t) {
+  float v[MAXC];
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c) {
+    const int e = lane + c * 64;
+    v[c] = e < Klim ? row[e] : 0.f;
+  }
+  topk_select_vals<MAXC>(v, E, k, Klim, lane, idx_t, w_t);
 }
 
 }  // namespace
