@@ -96,6 +96,24 @@ def _p(t):
     return t.data_ptr()
 
 
+def _typed(t, dtype):
+    if t is not None and isinstance(t, torch.Tensor) and t.dtype != dtype:
+        raise TypeError(f"expected a {dtype} tensor, got {t.dtype}")
+    return _p(t)
+
+
+def _i32(t):
+    return _typed(t, torch.int32)
+
+
+def _f32(t):
+    return _typed(t, torch.float32)
+
+
+def _f64(t):
+    return _typed(t, torch.float64)
+
+
 def _stream(stream):
     if stream is None:
         return torch.cuda.current_stream().cuda_stream
@@ -134,9 +152,9 @@ def moe_route(x, w_r, bias, k, logits, topk_idx, topk_w, seg_offsets=None, K_dev
     d = x.shape[1] if x is not None else 0
     dt = _dt(x) if x is not None else MOE_F32
     _check("moe_route", load().moe_route(
-        _p(x), dt, _p(w_r) if x is not None else None, _p(bias) if x is not None else None,
-        T, d, E, k, _p(seg_offsets), _nseg(seg_offsets), _p(K_dev),
-        _p(logits), _p(topk_idx), _p(topk_w), _p(ws), _nbytes(ws), _stream(stream)))
+        _p(x), dt, _f32(w_r) if x is not None else None, _f32(bias) if x is not None else None,
+        T, d, E, k, _i32(seg_offsets), _nseg(seg_offsets), _i32(K_dev),
+        _f32(logits), _i32(topk_idx), _f32(topk_w), _p(ws), _nbytes(ws), _stream(stream)))
 
 
 def moe_route_packed(x, w_r_packed, bias, k, logits, topk_idx, topk_w, seg_offsets=None, K_dev=None,
@@ -145,8 +163,8 @@ def moe_route_packed(x, w_r_packed, bias, k, logits, topk_idx, topk_w, seg_offse
     T, E = logits.shape
     d = x.shape[1]
     _check("moe_route_packed", load().moe_route_packed(
-        _p(x), _dt(x), _p(w_r_packed), _p(bias), T, d, E, k, _p(seg_offsets), _nseg(seg_offsets),
-        _p(K_dev), _p(logits), _p(topk_idx), _p(topk_w), _p(ws), _nbytes(ws), _stream(stream)))
+        _p(x), _dt(x), _p(w_r_packed), _f32(bias), T, d, E, k, _i32(seg_offsets), _nseg(seg_offsets),
+        _i32(K_dev), _f32(logits), _i32(topk_idx), _f32(topk_w), _p(ws), _nbytes(ws), _stream(stream)))
 
 
 def moe_pack_router(w_r, w_r_packed, stream=None):
@@ -154,15 +172,15 @@ def moe_pack_router(w_r, w_r_packed, stream=None):
     d, E = w_r.shape
     if w_r_packed.numel() * w_r_packed.element_size() != 6 * d * E:
         raise ValueError("w_r_packed must hold 3 * d * E bf16 values")
-    _check("moe_pack_router", load().moe_pack_router(_p(w_r), d, E, _p(w_r_packed), _stream(stream)))
+    _check("moe_pack_router", load().moe_pack_router(_f32(w_r), d, E, _p(w_r_packed), _stream(stream)))
 
 
 def moe_calibrate_prefix(topk_idx, topk_w, E, p, mass, ws, K_out=None, order=None,
                          seg_offsets=None, stream=None):
     T, k = topk_idx.shape
     _check("moe_calibrate_prefix", load().moe_calibrate_prefix(
-        _p(topk_idx), _p(topk_w), T, E, k, _p(seg_offsets), _nseg(seg_offsets), float(p),
-        _p(mass), _p(K_out), _p(order), _p(ws), _nbytes(ws), _stream(stream)))
+        _i32(topk_idx), _f32(topk_w), T, E, k, _i32(seg_offsets), _nseg(seg_offsets), float(p),
+        _f64(mass), _i32(K_out), _i32(order), _p(ws), _nbytes(ws), _stream(stream)))
 
 
 def moe_calibrate_route_prefix(logits, idx_full, w_full, p, mass, K_out, idx, w, stream=None):
@@ -170,7 +188,7 @@ def moe_calibrate_route_prefix(logits, idx_full, w_full, p, mass, K_out, idx, w,
     T, k = idx_full.shape
     E = logits.shape[1]
     _check("moe_calibrate_route_prefix", load().moe_calibrate_route_prefix(
-        _p(logits), _p(idx_full), _p(w_full), T, E, k, float(p), _p(mass), _p(K_out), _p(idx), _p(w),
+        _f32(logits), _i32(idx_full), _f32(w_full), T, E, k, float(p), _f64(mass), _i32(K_out), _i32(idx), _f32(w),
         None, 0, _stream(stream)))
 
 
@@ -180,8 +198,8 @@ def moe_dispatch(topk_idx, E, x, counts, offsets, src_of_row, row_of_slot, x_per
     d = x.shape[1] if x is not None else 0
     dt = _dt(x) if x is not None else MOE_F32
     _check("moe_dispatch", load().moe_dispatch(
-        _p(topk_idx), T, k, E, _p(x), dt, d, _p(counts), _p(offsets), _p(src_of_row),
-        _p(row_of_slot), _p(x_perm), _p(ws), ws.numel() * ws.element_size() if ws is not None else 0,
+        _i32(topk_idx), T, k, E, _p(x), dt, d, _i32(counts), _i32(offsets), _i32(src_of_row),
+        _i32(row_of_slot), _p(x_perm), _p(ws), ws.numel() * ws.element_size() if ws is not None else 0,
         _stream(stream)))
 
 
@@ -190,7 +208,7 @@ def moe_expert_ffn(x_perm, offsets, w_gate_up, w_down, y_perm, ws, K_dev=None, s
     E, two_m, _ = w_gate_up.shape
     n_K = K_dev.numel() if K_dev is not None else 0
     _check("moe_expert_ffn", load().moe_expert_ffn(
-        _p(x_perm), _dt(x_perm), _p(offsets), E, _p(K_dev), n_K, rows_max, d, two_m // 2,
+        _p(x_perm), _dt(x_perm), _i32(offsets), E, _i32(K_dev), n_K, rows_max, d, two_m // 2,
         _p(w_gate_up), _p(w_down), _p(y_perm), _p(ws), ws.numel() * ws.element_size(),
         _stream(stream)))
 
@@ -202,7 +220,7 @@ def moe_expert_ffn_packed(x_perm, offsets, w_gate_up_packed, w_down_packed, y_pe
     E, two_m, _ = w_gate_up_packed.shape
     n_K = K_dev.numel() if K_dev is not None else 0
     _check("moe_expert_ffn_packed", load().moe_expert_ffn_packed(
-        _p(x_perm), _dt(x_perm), _p(offsets), E, _p(K_dev), n_K, rows_max, d, two_m // 2,
+        _p(x_perm), _dt(x_perm), _i32(offsets), E, _i32(K_dev), n_K, rows_max, d, two_m // 2,
         _p(w_gate_up_packed), _p(w_down_packed), _p(y_perm), _p(ws), ws.numel() * ws.element_size(),
         _stream(stream)))
 
@@ -214,7 +232,7 @@ def moe_expert_ffn_packed_gather(x, k, src_of_row, offsets, w_gate_up_packed, w_
     E, two_m, _ = w_gate_up_packed.shape
     n_K = K_dev.numel() if K_dev is not None else 0
     _check("moe_expert_ffn_packed_gather", load().moe_expert_ffn_packed_gather(
-        _p(x), _dt(x), T, k, _p(src_of_row), _p(offsets), E, _p(K_dev), n_K, d, two_m // 2,
+        _p(x), _dt(x), T, k, _i32(src_of_row), _i32(offsets), E, _i32(K_dev), n_K, d, two_m // 2,
         _p(w_gate_up_packed), _p(w_down_packed), _p(y_perm), _p(ws), ws.numel() * ws.element_size(),
         _stream(stream)))
 
@@ -232,7 +250,7 @@ def moe_combine(y_perm, row_of_slot, topk_w, out, stream=None):
     T, k = topk_w.shape
     d = out.shape[1]
     _check("moe_combine", load().moe_combine(
-        _p(y_perm), _dt(y_perm), _p(row_of_slot), _p(topk_w), T, k, d, _p(out), _stream(stream)))
+        _p(y_perm), _dt(y_perm), _i32(row_of_slot), _f32(topk_w), T, k, d, _p(out), _stream(stream)))
 
 
 def drop_visual_block(h, v0, v1, out, stream=None):
@@ -246,7 +264,7 @@ def moe_combine_residual(y_perm, row_of_slot, topk_w, residual, out, stream=None
     T, k = topk_w.shape
     d = out.shape[1]
     _check("moe_combine_residual", load().moe_combine_residual(
-        _p(y_perm), _dt(y_perm), _p(row_of_slot), _p(topk_w), T, k, d, _p(residual), _p(out),
+        _p(y_perm), _dt(y_perm), _i32(row_of_slot), _f32(topk_w), T, k, d, _p(residual), _p(out),
         _stream(stream)))
 
 
@@ -265,8 +283,8 @@ def moe_permute_experts(order, w_r=None, bias=None, w_gate_up=None, w_down=None,
     ref = w_gate_up if w_gate_up is not None else w_down
     dt = _dt(ref) if ref is not None else MOE_F32
     _check("moe_permute_experts", load().moe_permute_experts(
-        _p(order), E, d or 1, m or 1, dt, _p(w_r), _p(bias), _p(w_gate_up), _p(w_down),
-        _p(w_r_out), _p(bias_out), _p(w_gate_up_out), _p(w_down_out), _stream(stream)))
+        _i32(order), E, d or 1, m or 1, dt, _f32(w_r), _f32(bias), _p(w_gate_up), _p(w_down),
+        _f32(w_r_out), _f32(bias_out), _p(w_gate_up_out), _p(w_down_out), _stream(stream)))
 
 
 def moe_savb_workspace_size(n: int, d: int, hid: int) -> int:
@@ -278,17 +296,17 @@ def moe_savb_gate(text_rows, w1, b1, w2, b2, theta, p_exit, exit_flag, ws, featu
     n, d = text_rows.shape
     hid = w1.shape[0]
     _check("moe_savb_gate", load().moe_savb_gate(
-        _p(text_rows), _dt(text_rows), n, d, _p(w1), _p(b1), hid, _p(w2), _p(b2), float(theta),
-        _p(feature), _p(p_exit), _p(exit_flag), _p(ws), _nbytes(ws), _stream(stream)))
+        _p(text_rows), _dt(text_rows), n, d, _f32(w1), _f32(b1), hid, _f32(w2), _f32(b2), float(theta),
+        _f32(feature), _f32(p_exit), _i32(exit_flag), _p(ws), _nbytes(ws), _stream(stream)))
 
 
 def drop_visual_block_if(h, v0, v1, exit_flag, out, stream=None):
     S, d = h.shape
     _check("drop_visual_block_if", load().drop_visual_block_if(
-        _p(h), _dt(h), S, d, v0, v1, _p(exit_flag), _p(out), _stream(stream)))
+        _p(h), _dt(h), S, d, v0, v1, _i32(exit_flag), _p(out), _stream(stream)))
 
 
 def moe_expand_dense_routing(topk_idx, topk_w, E, idx_dense, w_dense, K_dev=None, stream=None):
     T, k = topk_idx.shape
     _check("moe_expand_dense_routing", load().moe_expand_dense_routing(
-        _p(topk_idx), _p(topk_w), T, k, E, _p(K_dev), _p(idx_dense), _p(w_dense), _stream(stream)))
+        _i32(topk_idx), _f32(topk_w), T, k, E, _i32(K_dev), _i32(idx_dense), _f32(w_dense), _stream(stream)))

@@ -287,3 +287,20 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(abi, "LIB_PATH", str(tmp_path / "absent.so"))
     with pytest.raises(RuntimeError, match="missing"):
         abi.load()
+
+
+def test_binding_checks_array_dtypes():
+    """Typed array arguments (indices, routing weights, masses) are checked
+    before a pointer reaches the library."""
+    import torch
+
+    from paper_2609_38823_amd import abi
+    with pytest.raises(TypeError):
+        abi._i32(torch.zeros(3, dtype=torch.int64))
+    with pytest.raises(TypeError):
+        abi._f32(torch.zeros(3, dtype=torch.float64))
+    with pytest.raises(TypeError):
+        abi._f64(torch.zeros(3, dtype=torch.float32))
+    with pytest.raises(ValueError):  # right dtype, but not on the GPU
+        abi._i32(torch.zeros(3, dtype=torch.int32))
+    assert abi._i32(None) is None
