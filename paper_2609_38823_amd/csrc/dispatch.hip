@@ -11,7 +11,9 @@
 //                            rounds follow assignment order
 //   4. gather                each token row is read once and written to its
 //                            k dispatched rows with 16-byte stores
-// Up to 8192 assignments, steps 1-3 run in one workgroup (one launch).
+// Up to 8192 assignments, steps 1-3 run in one workgroup (one launch); up
+// to 64 chunks, steps 2 and 3 run in one launch (every rank workgroup
+// re-derives the totals and its chunk's bases from the histograms).
 #include "common.hpp"
 
 namespace decomoe {
@@ -104,35 +106,12 @@ __global__ __launch_bounds__(1024) void dispatch_scan_kernel(const int32_t* __re
   }
 }
 
-__global__ __launch_bounds__(DP_THREADS) void dispatch_rank_kernel(
-    const int32_t* __restrict__ idx, int A, int E, int key_bits, const int32_t* __restrict__ base,
-    int32_t* __restrict__ src_of_row, int32_t* __restrict__ row_of_slot) {
-  constexpr int NW = DP_THREADS / kWave;
-  __shared__ int run[NW][1024];
+// Ranks of one chunk's assignments from its per-wave starting rows `run`
+// (stable: waves and rounds follow assignment order).
+__device__ __forceinline__ void rank_chunk(const int32_t* __restrict__ idx, int A, int E, int key_bits,
+                                           int a_chunk, int (*run)[1024], int32_t* __restrict__ src_of_row,
+                                           int32_t* __restrict__ row_of_slot) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const int a_chunk = blockIdx.x * DP_CHUNK;
-  // per-wave histograms of this chunk
-  for (int i = threadIdx.x; i < NW * 1024; i += DP_THREADS) (&run[0][0])[i] = 0;
-  __syncthreads();
-  for (int i = 0; i < DP_PER_WAVE; i += kWave) {
-    int a = a_chunk + wv * DP_PER_WAVE + i + lane;
-    if (a < A) {
-      int e = idx[a];
-      if (e >= 0 && e < E) atomicAdd(&run[wv][e], 1);
-    }
-  }
-  __syncthreads();
-  // turn them into each wave's starting row per expert
-  for (int e = threadIdx.x; e < E; e += DP_THREADS) {
-    int r = base[(size_t)blockIdx.x * E + e];
-#pragma unroll
-    for (int w2 = 0; w2 < NW; ++w2) {
-      int c = run[w2][e];
-      run[w2][e] = r;
-      r += c;
-    }
-  }
-  __syncthreads();
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   for (int i = 0; i < DP_PER_WAVE; i += kWave) {
     int a = a_chunk + wv * DP_PER_WAVE + i + lane;
@@ -156,6 +135,118 @@ __global__ __launch_bounds__(DP_THREADS) void dispatch_rank_kernel(
     }
     __builtin_amdgcn_wave_barrier();
   }
+}
+
+// per-wave histograms of one chunk into run[w][e] (zeroed here)
+__device__ __forceinline__ void wave_hists(const int32_t* __restrict__ idx, int A, int E, int a_chunk,
+                                           int (*run)[1024]) {
+  constexpr int NW = DP_THREADS / kWave;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  for (int i = threadIdx.x; i < NW * 1024; i += DP_THREADS) (&run[0][0])[i] = 0;
+  __syncthreads();
+  for (int i = 0; i < DP_PER_WAVE; i += kWave) {
+    int a = a_chunk + wv * DP_PER_WAVE + i + lane;
+    if (a < A) {
+      int e = idx[a];
+      if (e >= 0 && e < E) atomicAdd(&run[wv][e], 1);
+    }
+  }
+}
+
+constexpr int DP_FUSE_CHUNKS = 64;  // scan folded into the ranks up to this many chunks
+
+// Steps 2 and 3 in one launch: workgroup c sums every chunk histogram per
+// expert in chunk order (the totals, and the part before chunk c), scans the
+// totals over the experts, and ranks chunk c; workgroup 0 also writes counts
+// and offsets.  Integer sums: the bases equal those of the scan kernel.
+__global__ __launch_bounds__(DP_THREADS) void dispatch_scan_rank_kernel(
+    const int32_t* __restrict__ idx, int A, int E, int key_bits, const int32_t* __restrict__ hist,
+    int n_chunks, int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
+    int32_t* __restrict__ src_of_row, int32_t* __restrict__ row_of_slot) {
+  constexpr int NW = DP_THREADS / kWave;
+  __shared__ int run[NW][1024];
+  __shared__ int s_tot[1024], s_base[1024];
+  __shared__ int part[NW];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int chunk = blockIdx.x;
+  for (int e = tid; e < E; e += DP_THREADS) {
+    int tot = 0, pre = 0;
+#pragma unroll 16
+    for (int c = 0; c < n_chunks; ++c) {
+      const int h = hist[(size_t)c * E + e];
+      pre += c < chunk ? h : 0;
+      tot += h;
+    }
+    s_tot[e] = tot;
+    s_base[e] = pre;
+  }
+  wave_hists(idx, A, E, chunk * DP_CHUNK, run);  // its barrier also publishes s_tot
+  // exclusive scan of the totals: thread t owns experts 4t .. 4t + 3 (E <= 1024)
+  int v[4], sum = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = 4 * tid + j;
+    v[j] = e < E ? s_tot[e] : 0;
+    sum += v[j];
+  }
+  int incl = sum;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int y = __shfl_up(incl, off, kWave);
+    if (lane >= off) incl += y;
+  }
+  if (lane == kWave - 1) part[wv] = incl;
+  __syncthreads();
+  int r0 = incl - sum;
+  for (int w = 0; w < wv; ++w) r0 += part[w];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = 4 * tid + j;
+    if (e < E) {
+      if (chunk == 0) {
+        counts[e] = v[j];
+        offsets[e] = r0;
+      }
+      s_base[e] += r0;
+    }
+    r0 += v[j];
+  }
+  if (chunk == 0 && tid == DP_THREADS - 1) offsets[E] = r0;
+  __syncthreads();
+  // each wave's starting row per expert
+  for (int e = tid; e < E; e += DP_THREADS) {
+    int r = s_base[e];
+#pragma unroll
+    for (int w2 = 0; w2 < NW; ++w2) {
+      int c = run[w2][e];
+      run[w2][e] = r;
+      r += c;
+    }
+  }
+  __syncthreads();
+  rank_chunk(idx, A, E, key_bits, chunk * DP_CHUNK, run, src_of_row, row_of_slot);
+}
+
+__global__ __launch_bounds__(DP_THREADS) void dispatch_rank_kernel(
+    const int32_t* __restrict__ idx, int A, int E, int key_bits, const int32_t* __restrict__ base,
+    int32_t* __restrict__ src_of_row, int32_t* __restrict__ row_of_slot) {
+  constexpr int NW = DP_THREADS / kWave;
+  __shared__ int run[NW][1024];
+  const int a_chunk = blockIdx.x * DP_CHUNK;
+  wave_hists(idx, A, E, a_chunk, run);
+  __syncthreads();
+  // turn them into each wave's starting row per expert
+  for (int e = threadIdx.x; e < E; e += DP_THREADS) {
+    int r = base[(size_t)blockIdx.x * E + e];
+#pragma unroll
+    for (int w2 = 0; w2 < NW; ++w2) {
+      int c = run[w2][e];
+      run[w2][e] = r;
+      r += c;
+    }
+  }
+  __syncthreads();
+  rank_chunk(idx, A, E, key_bits, a_chunk, run, src_of_row, row_of_slot);
 }
 
 // ---------------------------------------------------------------------------
@@ -316,11 +407,16 @@ hipError_t launch_dispatch(const int32_t* idx, int T, int k, int E, const void* 
     dispatch_hist_kernel<<<n_chunks, DP_THREADS, 0, s>>>(idx, A, E, hist);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
-    dispatch_scan_kernel<<<1, 1024, 0, s>>>(hist, n_chunks, E, base, counts, offsets);
-    err = hipGetLastError();
-    if (err != hipSuccess) return err;
-    dispatch_rank_kernel<<<n_chunks, DP_THREADS, 0, s>>>(idx, A, E, key_bits, base, src_of_row,
-                                                          row_of_slot);
+    if (n_chunks <= DP_FUSE_CHUNKS) {
+      dispatch_scan_rank_kernel<<<n_chunks, DP_THREADS, 0, s>>>(idx, A, E, key_bits, hist, n_chunks, counts,
+                                                                 offsets, src_of_row, row_of_slot);
+    } else {
+      dispatch_scan_kernel<<<1, 1024, 0, s>>>(hist, n_chunks, E, base, counts, offsets);
+      err = hipGetLastError();
+      if (err != hipSuccess) return err;
+      dispatch_rank_kernel<<<n_chunks, DP_THREADS, 0, s>>>(idx, A, E, key_bits, base, src_of_row,
+                                                            row_of_slot);
+    }
     err = hipGetLastError();
     if (err != hipSuccess) return err;
   }

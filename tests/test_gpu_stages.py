@@ -390,7 +390,10 @@ def test_calibrate_route_prefix_matches_two_calls(T, E, k, p):
     (129, 5, 5, 6, "bf16", None),
     (1000, 64, 2, 10, "f32", None),
     # more than 8192 assignments (also 4096 x 8 and 3000 x 4 above): the
-    # multi-workgroup histogram/scan/rank path
+    # multi-workgroup path, histograms then ranks with the scan folded in
+    # (up to 64 chunks of 1024: 8192 x 8 is the largest), or histograms,
+    # scan and ranks as three launches beyond that
+    (8192, 128, 8, 64, "bf16", None),
     (9000, 128, 8, 64, "bf16", None),
     (8193, 1000, 8, 16, "f32", 999),
 ])
