@@ -89,7 +89,8 @@ N_XCC = 8
 # kernels of the dense span at 4096 rows (the --traffic-run layer call)
 STAGES = [
     ("routing", [("router_x3_kernel<2>", None), ("topk_kernel<2>", 262144)]),
-    ("dispatch", [("dispatch_hist_kernel", None), ("dispatch_scan_kernel", None), ("dispatch_rank_kernel", None)]),
+    ("dispatch", [("dispatch_hist_kernel", None), ("dispatch_scan_rank_kernel", None), ("dispatch_scan_kernel", None),
+                  ("dispatch_rank_kernel", None)]),
     ("expert FFN", [("clear_kernel", None), ("ffn_fused_kernel<128>", None)]),
     ("combine", [("combine_kernel<true, false>", 1048576)]),
 ]
