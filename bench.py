@@ -439,25 +439,30 @@ def _line(metric, value, unit, args, ms_step, config, roof, cpu, **extra):
     return 0
 
 
-def _timed_layer(st, l, h, rcep, p, stream):
-    """One layer with events after each ABI call; returns per-call ms and
-    the buffers (h is left unmodified: the layer writes a scratch copy)."""
+def _timed_layer(st, l, h, rcep, p, stream, reps=6):
+    """One layer with events after each ABI call, run `reps` times back to
+    back; returns the per-call median ms over the repetitions after the
+    first (the GPU is then busy when each repetition's first event is
+    recorded, so no host launch gap enters the times) and the buffers (h
+    is left unmodified: the layer writes a scratch copy)."""
     import torch
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(12)]
-    it = iter(ev)
-    first = next(it)
-    first.record(stream)
-    used = [first]
-
-    def mark():
-        e = next(it)
-        e.record(stream)
-        used.append(e)
-
     dst = torch.empty_like(h)
-    b = st.layer_forward(l, h, dst, rcep, p, mark=mark)
+    runs = []
+    b = None
+    for _ in range(reps):
+        used = [torch.cuda.Event(enable_timing=True)]
+        used[0].record(stream)
+
+        def mark():
+            e = torch.cuda.Event(enable_timing=True)
+            e.record(stream)
+            used.append(e)
+
+        b = st.layer_forward(l, h, dst, rcep, p, mark=mark)
+        runs.append(used)
     torch.cuda.synchronize()
-    return [used[i].elapsed_time(used[i + 1]) for i in range(len(used) - 1)], b
+    per = [[u[i].elapsed_time(u[i + 1]) for i in range(len(u) - 1)] for u in runs[1:]]
+    return [float(np.median(c)) for c in zip(*per)], b
 
 
 def bench_stack48(args) -> int:
