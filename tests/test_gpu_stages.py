@@ -417,6 +417,39 @@ def test_dispatch_exact(T, E, k, d, dt, K):
     np.testing.assert_array_equal(host(xp).view(np.uint32), ref_xp.view(np.uint32))
 
 
+@pytest.mark.parametrize("T", [1000, 4096, 9000])
+def test_dispatch_drops_out_of_range_entries(T):
+    """Entries outside [0, E) get no row and row_of_slot -1; the valid ones
+    are grouped as a stable sort of the valid entries alone (one workgroup,
+    histograms then ranks with the scan folded in, and three launches)."""
+    E, k, d = 128, 8, 64
+    idx, _ = I.synthetic_routing(T, E, k, seed=T)
+    flat = idx.reshape(-1).copy()
+    rng = np.random.default_rng(T)
+    bad = rng.choice(flat.size, size=flat.size // 97, replace=False)
+    flat[bad] = rng.choice([-1, E, 1000, -7], size=bad.size)
+    idx = flat.reshape(T, k)
+    x = I.synthetic_rows(T, d, "bf16", seed=T + 1)
+    A = T * k
+    counts, offsets = i32((E,)), i32((E + 1,))
+    src, ros = i32((A,)), i32((A,))
+    xp = torch.zeros((A, d), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(abi.moe_workspace_size(T, E, k, d, 64, 1), dtype=torch.uint8, device="cuda")
+    abi.moe_dispatch(dev(idx), E, dev(x, torch.bfloat16), counts, offsets, src, ros, xp, ws)
+    valid = (flat >= 0) & (flat < E)
+    a_valid = np.nonzero(valid)[0]
+    order = a_valid[np.argsort(flat[a_valid], kind="stable")]
+    n = order.size
+    np.testing.assert_array_equal(host(counts), np.bincount(flat[a_valid], minlength=E))
+    np.testing.assert_array_equal(host(offsets), np.concatenate([[0], np.cumsum(host(counts))]))
+    assert int(host(offsets)[E]) == n < A
+    np.testing.assert_array_equal(host(src)[:n], order)
+    ro = host(ros)
+    assert (ro[~valid] == -1).all()
+    np.testing.assert_array_equal(ro[order], np.arange(n))
+    np.testing.assert_array_equal(host(xp)[:n].view(np.uint32), x[order // k].view(np.uint32))
+
+
 def test_dispatch_empty():
     counts, offsets = i32((16,)), i32((17,))
     e = torch.empty((0,), dtype=torch.int32, device="cuda")
