@@ -321,6 +321,50 @@ def test_calibrate_prefix_exact(T, E, k, segs, p):
     np.testing.assert_array_equal(host(order), ro)
 
 
+@pytest.mark.parametrize("T,E,k", [(300, 16, 2), (1500, 128, 8)])
+def test_calibrate_skips_out_of_range_entries(T, E, k):
+    """Routing entries with an expert outside [0, E) add nothing to the
+    masses: the result is bitwise that of the same routing with those
+    entries' weights set to zero (sorted path, and the chunked path above
+    8192 entries)."""
+    idx, w = I.synthetic_routing(T, E, k, seed=T + 5)
+    rng = np.random.default_rng(T)
+    bad = rng.choice(idx.size, size=idx.size // 53, replace=False)
+    idx_bad = idx.reshape(-1).copy()
+    idx_bad[bad] = rng.choice([-1, E, E + 100], size=bad.size)
+    w_clean = w.reshape(-1).copy()
+    w_clean[bad] = 0.0
+    idx_bad, w_clean = idx_bad.reshape(T, k), w_clean.reshape(T, k)
+    mass = torch.full((1, E), float("nan"), dtype=torch.float64, device="cuda")
+    K, order = i32((1,)), i32((E,))
+    abi.moe_calibrate_prefix(dev(idx_bad), dev(w), E, 0.9, mass, ws_for(T, E, k, 8), K_out=K, order=order)
+    rm, rK, ro = oracle_calibrate(idx, w_clean, E, k, [0, T], 0.9)
+    np.testing.assert_array_equal(host(mass).view(np.uint64), rm.view(np.uint64))
+    np.testing.assert_array_equal(host(K), rK)
+    np.testing.assert_array_equal(host(order), ro)
+
+
+def test_combine_skips_out_of_range_rows():
+    """Slots whose row index lies outside [0, T*k) contribute nothing: the
+    output equals the oracle's combine with those slots' weights at zero."""
+    T, k, d = 300, 8, 256
+    A = T * k
+    y = I.synthetic_rows(A, d, "bf16", seed=11)
+    ros = I.synthetic_permutation(A, seed=12).astype(np.int32)
+    _, w = I.synthetic_routing(T, 16, k, seed=13)
+    rng = np.random.default_rng(14)
+    bad = rng.choice(A, size=A // 41, replace=False)
+    ros_bad = ros.copy()
+    ros_bad[bad] = rng.choice([-1, A, A + 5000], size=bad.size)
+    w_clean = w.reshape(-1).copy()
+    w_clean[bad] = 0.0
+    out = torch.empty((T, d), dtype=torch.bfloat16, device="cuda")
+    abi.moe_combine(dev(y, torch.bfloat16), dev(ros_bad), dev(w), out)
+    ref = oracle.combine(y, ros, w_clean.reshape(T, k))
+    assert rel_inf(host(out), ref) <= TOL["bf16"]
+    assert row_rel(host(out), ref) <= TOL["bf16"]
+
+
 def test_calibrate_worked_example_golden():
     import json, os
     g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "prefix_worked_example.json")))
