@@ -611,6 +611,32 @@ def test_expert_ffn_packed(E, d, m, dt, rows, K, cnt):
     assert rel_inf(host(y)[live], ref) <= TOL[dt]
 
 
+def test_expert_ffn_clamps_offsets_to_rows_max():
+    """Offsets past rows_max are clamped: expert e evaluates rows
+    [min(off[e], R), min(off[e + 1], R)), so the experts beyond R get no rows
+    (row-major and packed paths, bitwise equal, and against the oracle)."""
+    E, d, m, R = 8, 256, 256, 300
+    sh = I.LayerShape(d=d, E=E, m=m, k=1, dtype="bf16")
+    prm = I.layer_params(sh, seed=77)
+    raw = np.array([0, 50, 120, 120, 200, 260, 400, 500, 600], np.int32)
+    xp = dev(I.synthetic_rows(R, d, "bf16", seed=78), torch.bfloat16)
+    wgu, wd = dev(prm["w_gate_up"], torch.bfloat16), dev(prm["w_down"], torch.bfloat16)
+    wgu_p, wd_p = torch.empty_like(wgu), torch.empty_like(wd)
+    abi.moe_pack_expert_weights(wgu, wgu_p)
+    abi.moe_pack_expert_weights(wd, wd_p)
+    ws = torch.empty(abi.moe_workspace_size(R, E, 1, d, m, 1), dtype=torch.uint8, device="cuda")
+    y_ref = torch.full((R, d), 7.0, dtype=torch.bfloat16, device="cuda")
+    y = torch.full((R, d), 7.0, dtype=torch.bfloat16, device="cuda")
+    abi.moe_expert_ffn(xp, dev(raw), wgu, wd, y_ref, ws)
+    abi.moe_expert_ffn_packed(xp, dev(raw), wgu_p, wd_p, y, ws)
+    assert torch.equal(y.view(torch.int16), y_ref.view(torch.int16))
+    off = np.minimum(raw, R)
+    expert_of_row = np.repeat(np.arange(E), np.diff(off))
+    assert expert_of_row.size == R
+    ref = oracle.expert_ffn_rows(host(xp), expert_of_row, prm["w_gate_up"], prm["w_down"])
+    assert rel_inf(host(y), ref) <= TOL["bf16"]
+
+
 # ---------------------------------------------------------------------------
 # moe_expert_ffn_packed_gather: the dispatch gather inside the GEMM
 # ---------------------------------------------------------------------------
