@@ -161,13 +161,40 @@ def cpu_info() -> dict:
 
 
 def run_oracle_step(x, text, params, k, p):
-    """The same step on the CPU oracle (test infrastructure, timed only)."""
+    """The same step on the CPU oracle (test infrastructure, timed only):
+    its step functions called in the order of the layer, each timed.
+    Returns (total seconds, seconds per stage)."""
     import oracle
+    import numpy as _np
+    wr, b, gu, dn = params["w_r"], params["bias"], params["w_gate_up"], params["w_down"]
+    E = wr.shape[1]
+    st = {}
+
+    def timed(name, fn, *a):
+        t = time.perf_counter()
+        r = fn(*a)
+        st[name] = st.get(name, 0.0) + time.perf_counter() - t
+        return r
+
+    def experts(xr, idx, w, K=None):
+        counts, offsets, src, ros = timed("dispatch", oracle.dispatch, idx, E)
+        exp_of_row = _np.asarray(idx).reshape(-1)[src]
+        y = timed("expert_ffn", oracle.expert_ffn_rows, _np.asarray(xr, _np.float64)[src // k], exp_of_row,
+                  gu, dn)
+        return timed("combine", oracle.combine, y, ros, w)
+
     t0 = time.perf_counter()
-    oracle.moe_layer_dense(x, params["w_r"], params["bias"], params["w_gate_up"], params["w_down"], k)
-    h = oracle.drop_visual_block(x, 0, x.shape[0] - text.shape[0])
-    oracle.moe_layer_rcep(h, params["w_r"], params["bias"], params["w_gate_up"], params["w_down"], k, p)
-    return time.perf_counter() - t0
+    a = timed("router_logits", oracle.router_logits, x, wr, b)
+    idx, w = timed("topk", oracle.full_pool_route, a, k)
+    experts(x, idx, w)
+    h = timed("drop", oracle.drop_visual_block, x, 0, x.shape[0] - text.shape[0])
+    a = timed("router_logits", oracle.router_logits, h, wr, b)
+    idx_f, w_f = timed("topk", oracle.full_pool_route, a, k)
+    mass = timed("mass_and_K", oracle.activated_mass, idx_f, w_f, E)
+    K = timed("mass_and_K", oracle.prefix_length, mass, p, k)
+    idx, w = timed("prefix_reroute", oracle.prefix_route, a, K, k)
+    experts(h, idx, w)
+    return time.perf_counter() - t0, {n: round(v, 4) for n, v in st.items()}
 
 
 def main() -> int:
@@ -367,12 +394,12 @@ def bench_layer(args) -> int:
 
     cpu = None
     if not args.no_cpu_baseline:
-        sec = run_oracle_step(x_np, x_np[V:], rprm, k, p)
+        sec, stage_s = run_oracle_step(x_np, x_np[V:], rprm, k, p)
         info = cpu_info()
         cpu = dict(value=(T + (T - V)) / sec, unit="tokens/s",
                    cores=info.get("blas_threads") or info["affinity_cores"], kind="oracle",
                    sample="one full step (dense 4096 rows + visual drop + RCEP 512 rows), numpy float64",
-                   seconds=round(sec, 3), **info)
+                   seconds=round(sec, 3), stage_seconds=stage_s, **info)
 
     tokens = T + (T - V)
     line = {
