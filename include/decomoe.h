@@ -38,7 +38,10 @@
  *     argument); router weights, bias, logits and routing weights are
  *     float32; masses are float64; indices, counts and lengths are int32.
  *   - Every call is asynchronous on `stream` (a hipStream_t; NULL is the
- *     null stream) and never synchronises with the host.  Data-dependent
+ *     null stream) and never synchronises with the host.  Calls launch on
+ *     the current HIP device (whose CU and XCD counts shape the expert
+ *     FFN's persistent launch); the stream and every array must belong to
+ *     that device.  Data-dependent
  *     sizes (K, per-expert counts) stay on the device; grids are sized from
  *     the host-side upper bounds passed in.
  *   - Errors: arguments are validated on the host before anything is
