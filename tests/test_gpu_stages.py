@@ -741,6 +741,39 @@ def test_packed_ffn_two_launch_fallback_matches_persistent(T, E, k, d, m, monkey
     assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
 
 
+@pytest.mark.parametrize("T", [4096, 512, 64])
+def test_persistent_ffn_repeated_calls_bitwise(T, monkeypatch):
+    """Back-to-back persistent calls on one workspace (its counters cleared
+    and reused every call) keep giving the two-launch path's bits: each of
+    40 calls is compared with it."""
+    E, k, d, m = 128, 8, 2048, 768
+    sh = I.LayerShape(d=d, E=E, m=m, k=k, dtype="bf16")
+    prm = I.layer_params(sh, seed=4)
+    idx, _ = I.synthetic_routing(T, E, k, seed=T + 9)
+    x = dev(I.synthetic_rows(T, d, "bf16", seed=T + 8), torch.bfloat16)
+    A = T * k
+    counts, offsets, src, ros = i32((E,)), i32((E + 1,)), i32((A,)), i32((A,))
+    ws = torch.empty(abi.moe_workspace_size(T, E, k, d, m, 1), dtype=torch.uint8, device="cuda")
+    abi.moe_dispatch(dev(idx), E, None, counts, offsets, src, ros, None, ws)
+    wgu, wd = dev(prm["w_gate_up"], torch.bfloat16), dev(prm["w_down"], torch.bfloat16)
+    wgu_p, wd_p = torch.empty_like(wgu), torch.empty_like(wd)
+    abi.moe_pack_expert_weights(wgu, wgu_p)
+    abi.moe_pack_expert_weights(wd, wd_p)
+    ref = torch.empty((A, d), dtype=torch.bfloat16, device="cuda")
+    monkeypatch.setenv("DECOMOE_FFN_TWO_LAUNCH", "1")
+    abi.moe_expert_ffn_packed_gather(x, k, src, offsets, wgu_p, wd_p, ref, ws)
+    torch.cuda.synchronize()
+    monkeypatch.delenv("DECOMOE_FFN_TWO_LAUNCH")
+    ys = [torch.empty((A, d), dtype=torch.bfloat16, device="cuda") for _ in range(4)]
+    for i in range(40):
+        abi.moe_expert_ffn_packed_gather(x, k, src, offsets, wgu_p, wd_p, ys[i % 4], ws)
+        if i % 4 == 3:
+            torch.cuda.synchronize()
+            for y in ys:
+                assert torch.equal(y.view(torch.int16), ref.view(torch.int16)), i
+                y.fill_(7.0)
+
+
 def test_expert_ffn_packed_gather_out_of_range_rows_read_token_zero():
     T, E, k, d, m = 64, 4, 2, 512, 256
     sh = I.LayerShape(d=d, E=E, m=m, k=k, dtype="bf16")
