@@ -582,25 +582,16 @@ def bench_stack48(args) -> int:
 
 
 def paper_prefill_flops(S: int, T: int, exit_layer: int, Ks, L: int, E: int, d: int, m: int,
-                        q: int = 4096, kv: int = 512, n_gate: int = 0, gate_hidden: int = 512) -> dict:
-    """The paper's decoder FLOPs replay for one prefill (App. A.3,
-    Eqs. 13-15 and the SAVB MLP term), with its dense-equivalent expert
-    convention C_expert(K) = 6 K d m: layers before the exit at (S, E), from
-    the exit on at (T, K_l); the baseline runs every layer at (S, E).  The
-    attention projection sizes q and kv are the paper's Qwen3-VL-MoE values;
-    the attention itself is not computed here, only counted in this replay."""
-    c_proj = 2 * (d * q + 2 * d * kv + q * d)
-    c_router = 2 * d * E
-
-    def layer(n, K):
-        return n * c_proj + 2 * q * n * (n + 1) + n * (c_router + 6 * K * d * m)
-
-    base = L * layer(S, E)
-    method = exit_layer * layer(S, E) + sum(layer(T, int(K)) for K in Ks)
-    gate = n_gate * (2 * (2 * d) * gate_hidden + 2 * gate_hidden * 2)
-    total = method + gate
-    return dict(baseline_tflop=base / 1e12, decomoe_tflop=total / 1e12, gate_tflop=gate / 1e12,
-                saving=1.0 - total / base, q=q, kv=kv,
+                        n_gate: int = 0) -> dict:
+    """The paper's decoder FLOPs replay for one prefill (App. A.3), from
+    paper_2609_38823_amd.flops: layers before the exit at (S, E), from the
+    exit on at (T, K_l); the baseline runs every layer at (S, E)."""
+    from paper_2609_38823_amd import flops as F
+    g = F.DecoderDims(d=d, E=E, m=m)
+    c = F.case_flops(g, L=L, S=S, V=S - T, exit_layer=exit_layer, K_prefill=[int(K) for K in Ks],
+                     n_gate=n_gate)
+    return dict(baseline_tflop=c["baseline"] / 1e12, decomoe_tflop=c["method"] / 1e12,
+                gate_tflop=c["method_gate"] / 1e12, saving=F.saving([c]), q=g.q, kv=g.kv,
                 convention="paper's replay: dense-equivalent experts (6 K d m per token), attention "
                            "terms included, one prefill, exit at the given layer")
 
@@ -862,7 +853,6 @@ def bench_variants(args) -> int:
     x_np = I.tokens(sh, wl.T, seed=wl.seed)
     x = torch.from_numpy(x_np).cuda().to(torch.bfloat16)
     Tt = wl.T - wl.n_visual
-    K50 = torch.full((4,), 50, dtype=torch.int32, device="cuda")
 
     def timed(fn):
         for _ in range(args.warmup):
@@ -879,7 +869,7 @@ def bench_variants(args) -> int:
         "dense (no exit, all experts)": dict(exit_layer=None),
         "visual exit only (exit 20, all experts)": dict(exit_layer=20, after_exit="dense"),
         "fixed exit at 28 + RCEP": dict(exit_layer=28),
-        "exit 20 + fixed prefix of 50": dict(exit_layer=20, after_exit="fixed", K_fixed=K50),
+        "exit 20 + fixed prefix of 50": dict(exit_layer=20, after_exit="fixed", K_fixed=50),
         "exit 20 + RCEP (full)": dict(exit_layer=20),
     }
     rows = {}
@@ -940,8 +930,7 @@ def bench_variants(args) -> int:
         res = {}
         for r in keep:
             K = int(round(r * E))
-            Kd = torch.full((4,), K, dtype=torch.int32, device="cuda")
-            out = lay.forward_prefix(xt, Kd).out.float().cpu().numpy().astype(np.float64)
+            out = lay.forward_prefix(xt, K).out.float().cpu().numpy().astype(np.float64)
             res[str(r)] = dict(K=K, mass_covered=float(s_o[:K].sum() / s_o.sum()),
                                weight_mb=K * wbytes / 1e6,
                                out_rel_l2_vs_full_pool=float(np.linalg.norm(out - dense_out) /

@@ -80,6 +80,14 @@ enum {
   MOE_EUNSUPPORTED = -5  /* valid per the method but not supported here     */
 };
 
+/* Launch paths of the expert FFN, as reported by moe_ffn_status. */
+enum {
+  MOE_FFN_PATH_PERSISTENT = 1, /* packed bf16: both GEMMs in one persistent launch */
+  MOE_FFN_PATH_TWO_LAUNCH = 2, /* packed bf16: one launch per GEMM                */
+  MOE_FFN_PATH_ROW_MAJOR = 3,  /* bf16 row-major weights                          */
+  MOE_FFN_PATH_F32 = 4         /* float32                                         */
+};
+
 /* Human-readable text of a status code (static storage, never NULL). */
 const char* moe_status_string(int status);
 
@@ -253,9 +261,13 @@ int moe_dispatch(const int32_t* topk_idx, int T, int k, int E,
  *
  *   x_perm     [rows_max, d] dispatched rows (dtype), grouped by `offsets`.
  *   offsets    [E + 1] int32 from moe_dispatch.
- *   K_dev      [n_K] int32 or NULL: experts e >= max(K_dev[0..n_K)) are not
- *              evaluated (their rows, of which prefix routing leaves none,
- *              are left unwritten); NULL evaluates all E experts.
+ *   K_dev      [n_K] int32 or NULL: experts e >= max(K_dev[0..n_K)), that
+ *              maximum clamped to [1, E], are not evaluated (their rows, of
+ *              which prefix routing leaves none, are left unwritten); NULL
+ *              evaluates all E experts.  moe_route raises a K below its k to
+ *              k, so K_dev must hold values >= that k (Eq. 12 gives
+ *              K >= k); moe_expert_ffn_packed_gather, which knows k,
+ *              clamps to [k, E] itself.
  *   rows_max   upper bound of offsets[E] (normally T*k).
  *   w_gate_up  [E, 2m, d] (dtype): rows [0, m) gate, [m, 2m) up projection.
  *   w_down     [E, d, m] (dtype).
@@ -323,7 +335,8 @@ int moe_expert_ffn_packed(const void* x_perm, moe_dtype dtype, const int32_t* of
  *               with rows_max = T*k.
  * y_perm is bitwise what moe_dispatch (with x) followed by
  * moe_expert_ffn_packed gives, but x_perm is never formed: call moe_dispatch
- * with x = NULL.  bf16 only; d % 256 == 0 and m % 256 == 0, T*d*2 and T*k
+ * with x = NULL.  Each K_dev value is clamped to [k, E], the clamp moe_route
+ * applies, so every expert the prefix re-route can select is evaluated.  bf16 only; d % 256 == 0 and m % 256 == 0, T*d*2 and T*k
  * below 2^31, else MOE_EUNSUPPORTED.  y_perm and ws must not overlap any
  * input (MOE_EALIAS).  Needs ws (moe_workspace_size).
  */
@@ -332,6 +345,27 @@ int moe_expert_ffn_packed_gather(const void* x, moe_dtype dtype, int T, int k,
                                  const int32_t* K_dev, int n_K, int d, int m,
                                  const void* w_gate_up_packed, const void* w_down_packed,
                                  void* y_perm, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * moe_ffn_status - how the last expert FFN call on a workspace ran
+ * (Algorithm 2: the first K expert MLPs are all evaluated).
+ *
+ *   ws, ws_bytes  the workspace given to that call (any moe_expert_ffn*).
+ *   status        [4] int32 device output, written on `stream` after the
+ *                 call's kernels:
+ *                   [0] waits of a down item for its h that ran out of polls
+ *                       (the item then read h anyway: its y rows may be wrong)
+ *                   [1] work items completed
+ *                   [2] work items in the call's plan
+ *                   [3] launch path (MOE_FFN_PATH_*)
+ *                 Items are counted on the persistent path only (elsewhere
+ *                 every item is a workgroup of its own and [0..2] are 0).
+ *                 On the persistent path the call evaluated every planned
+ *                 item exactly when [0] == 0 and [1] == [2].
+ * Call it on the same stream after the FFN call and before anything else
+ * reuses the workspace.  ws_bytes >= 1024, else MOE_EWORKSPACE.
+ */
+int moe_ffn_status(const void* ws, size_t ws_bytes, int32_t* status, hipStream_t stream);
 
 /*
  * moe_combine - weighted combine back to token order (Algorithm 2).

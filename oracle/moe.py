@@ -380,7 +380,8 @@ def moe_layer_rcep(x, w_r, bias, w_gate_up, w_down, k, p, seg_offsets=None,
 # --------------------------------------------------------------------------
 # A stack of MoE blocks (Algorithm 2's loop over layers)
 # --------------------------------------------------------------------------
-def moe_stack(h, layers, k, p, exit_layer=None, v0=0, v1=0, seg_offsets=None):
+def moe_stack(h, layers, k, p, exit_layer=None, v0=0, v1=0, seg_offsets=None,
+              after_exit="rcep", K_fixed=None):
     """Algorithm 2 over a stack of MoE blocks with the residual stream
     h <- h + MoE_l(h) between blocks (the blocks' attention sublayers are
     not part of this stack).
@@ -392,17 +393,34 @@ def moe_stack(h, layers, k, p, exit_layer=None, v0=0, v1=0, seg_offsets=None):
     rows and layers from it on run the RCEP span (Sec. 3.3).  None: no exit,
     every layer dense.  0 with v0 == v1: RCEP in every layer (decode).
 
+    ``after_exit`` selects what the layers from the exit on run, for the
+    component ablation (Table 2): "rcep" (the prefix of Eq. 12), "dense"
+    (the full expert pool: the visual exit alone) or "fixed" (a given prefix
+    length instead of Eq. 12: ``K_fixed``, one int for every such layer or a
+    sequence indexed by layer; each must satisfy k <= K <= E).
+
     Returns the final hidden rows and, per layer, K (None for dense layers).
     """
+    if after_exit not in ("rcep", "dense", "fixed"):
+        raise ValueError("after_exit is 'rcep', 'dense' or 'fixed'")
+    if after_exit == "fixed" and K_fixed is None:
+        raise ValueError("the fixed prefix needs K_fixed")
     h = np.asarray(h, F64)
     Ks = []
     for l, prm in enumerate(layers):
-        rcep = exit_layer is not None and l >= exit_layer
+        rcep = exit_layer is not None and l >= exit_layer and after_exit != "dense"
         if exit_layer is not None and l == exit_layer:
             h = drop_visual_block(h, v0, v1)
         if rcep:
+            K_over = None
+            if after_exit == "fixed":
+                K_l = int(K_fixed) if np.ndim(K_fixed) == 0 else int(K_fixed[l])
+                if not k <= K_l <= np.asarray(prm["w_r"]).shape[1]:
+                    raise ValueError("need k <= K_fixed <= E")
+                n_seg = 1 if seg_offsets is None else len(seg_offsets) - 1
+                K_over = [K_l] * n_seg
             r = moe_layer_rcep(h, prm["w_r"], prm["bias"], prm["w_gate_up"], prm["w_down"], k, p,
-                               seg_offsets=seg_offsets)
+                               seg_offsets=seg_offsets, K_override=K_over)
             Ks.append(r["K"])
         else:
             r = moe_layer_dense(h, prm["w_r"], prm["bias"], prm["w_gate_up"], prm["w_down"], k)

@@ -28,7 +28,10 @@ EXPORTS = ("moe_status_string", "moe_workspace_size", "moe_route", "moe_route_pa
            "moe_pack_expert_weights",
            "moe_combine", "moe_combine_residual", "drop_visual_block", "moe_permute_experts",
            "moe_savb_workspace_size", "moe_savb_gate", "drop_visual_block_if",
-           "moe_expand_dense_routing")
+           "moe_expand_dense_routing", "moe_ffn_status")
+
+# launch paths of the expert FFN (moe_ffn_status)
+FFN_PATH_PERSISTENT, FFN_PATH_TWO_LAUNCH, FFN_PATH_ROW_MAJOR, FFN_PATH_F32 = 1, 2, 3, 4
 
 
 class MoeError(RuntimeError):
@@ -71,6 +74,7 @@ def load() -> ctypes.CDLL:
         "moe_savb_gate": (_I, [_P, _I, _I, _I, _P, _P, _I, _P, _P, _D, _P, _P, _P, _P, _S, _P]),
         "drop_visual_block_if": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P]),
         "moe_expand_dense_routing": (_I, [_P, _P, _I, _I, _I, _P, _P, _P, _P]),
+        "moe_ffn_status": (_I, [_P, _S, _P, _P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -310,3 +314,11 @@ def moe_expand_dense_routing(topk_idx, topk_w, E, idx_dense, w_dense, K_dev=None
     T, k = topk_idx.shape
     _check("moe_expand_dense_routing", load().moe_expand_dense_routing(
         _i32(topk_idx), _f32(topk_w), T, k, E, _i32(K_dev), _i32(idx_dense), _f32(w_dense), _stream(stream)))
+
+
+def moe_ffn_status(ws, status, stream=None):
+    """status [4] int32 <- (waits that ran out, items completed, items
+    planned, launch path) of the last expert FFN call on ws."""
+    if status.numel() < 4:
+        raise ValueError("status needs 4 int32 entries")
+    _check("moe_ffn_status", load().moe_ffn_status(_p(ws), _nbytes(ws), _i32(status), _stream(stream)))

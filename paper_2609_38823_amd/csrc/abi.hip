@@ -11,6 +11,12 @@ using decomoe::dispatch_ws_bytes;
 using decomoe::ffn_ws_bytes;
 using decomoe::route_ws_bytes;
 
+static_assert(MOE_FFN_PATH_PERSISTENT == decomoe::FFN_PATH_PERSISTENT &&
+                  MOE_FFN_PATH_TWO_LAUNCH == decomoe::FFN_PATH_TWO_LAUNCH &&
+                  MOE_FFN_PATH_ROW_MAJOR == decomoe::FFN_PATH_ROW_MAJOR &&
+                  MOE_FFN_PATH_F32 == decomoe::FFN_PATH_F32,
+              "launch path codes of the header and the kernels agree");
+
 constexpr int kMaxE = 1024;
 constexpr int kMaxK = 32;
 
@@ -273,11 +279,15 @@ int moe_expert_ffn_packed(const void* x_perm, moe_dtype dtype, const int32_t* of
                     w_down_packed, true, y_perm, ws, ws_bytes, stream);
 }
 
-int moe_expert_ffn_packed_gather(const void* x, moe_dtype dtype, int T, int k,
-                                 const int32_t* src_of_row, const int32_t* offsets, int E,
-                                 const int32_t* K_dev, int n_K, int d, int m,
-                                 const void* w_gate_up_packed, const void* w_down_packed,
-                                 void* y_perm, void* ws, size_t ws_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+// Host-side checks of moe_expert_ffn_packed_gather and its allocation-free
+// variant, before the workspace: MOE_OK with *rows_max set, or the status.
+int gather_ffn_args(const void* x, moe_dtype dtype, int T, int k, const int32_t* src_of_row,
+                    const int32_t* offsets, int E, const int32_t* K_dev, int n_K, int d, int m,
+                    const void* w_gate_up_packed, const void* w_down_packed, void* y_perm,
+                    int* rows_max_out) {
   if (!valid_dtype(dtype) || T < 0 || k < 1 || E < 1 || E > kMaxE || k > E || d < 1 || m < 1)
     return MOE_EINVAL;
   if (dtype != MOE_BF16) return MOE_EUNSUPPORTED;
@@ -290,11 +300,19 @@ int moe_expert_ffn_packed_gather(const void* x, moe_dtype dtype, int T, int k,
   if (!offsets || !w_gate_up_packed || !w_down_packed) return MOE_EINVAL;
   const int rows_max = T * k;
   if (rows_max > 0 && (!x || !src_of_row || !y_perm)) return MOE_EINVAL;
-  if (!aligned_all({x, src_of_row, offsets, K_dev, w_gate_up_packed, w_down_packed, y_perm, ws}))
+  if (!aligned_all({x, src_of_row, offsets, K_dev, w_gate_up_packed, w_down_packed, y_perm}))
     return MOE_EINVAL;
-  if (rows_max == 0) return MOE_OK;
-  const size_t need = ffn_ws_bytes(true, rows_max, E, d, m);
-  if (!ws || ws_bytes < need) return MOE_EWORKSPACE;
+  *rows_max_out = rows_max;
+  return MOE_OK;
+}
+
+// Aliasing checks and the launch (ws: the caller's workspace, or the
+// library's scratch array of the allocation-free variant).
+int gather_ffn_launch(const void* x, int T, int k, const int32_t* src_of_row, const int32_t* offsets,
+                      int E, const int32_t* K_dev, int n_K, int d, int m, const void* w_gate_up_packed,
+                      const void* w_down_packed, void* y_perm, void* ws, size_t need,
+                      hipStream_t stream) {
+  const int rows_max = T * k;
   Range o_y = rng(y_perm, (size_t)rows_max * d * 2);
   Range o_ws = rng(ws, need);
   Range in_k = K_dev ? rng(K_dev, (size_t)n_K * 4) : Range{0, 0};
@@ -306,7 +324,35 @@ int moe_expert_ffn_packed_gather(const void* x, moe_dtype dtype, int T, int k,
     return MOE_EALIAS;
   return hip_status(decomoe::launch_expert_ffn(x, true, offsets, E, K_dev, n_K, rows_max, d, m,
                                                w_gate_up_packed, w_down_packed, true, y_perm, ws,
-                                               stream, decomoe::RowGather{src_of_row, k, T}));
+                                               stream, decomoe::RowGather{src_of_row, k, T}, k));
+}
+}  // namespace
+
+extern "C" {
+
+int moe_expert_ffn_packed_gather(const void* x, moe_dtype dtype, int T, int k,
+                                 const int32_t* src_of_row, const int32_t* offsets, int E,
+                                 const int32_t* K_dev, int n_K, int d, int m,
+                                 const void* w_gate_up_packed, const void* w_down_packed,
+                                 void* y_perm, void* ws, size_t ws_bytes, hipStream_t stream) {
+  int rows_max = 0;
+  const int st = gather_ffn_args(x, dtype, T, k, src_of_row, offsets, E, K_dev, n_K, d, m,
+                                 w_gate_up_packed, w_down_packed, y_perm, &rows_max);
+  if (st != MOE_OK) return st;
+  if (!aligned_all({ws})) return MOE_EINVAL;
+  if (rows_max == 0) return MOE_OK;
+  const size_t need = ffn_ws_bytes(true, rows_max, E, d, m);
+  if (!ws || ws_bytes < need) return MOE_EWORKSPACE;
+  return gather_ffn_launch(x, T, k, src_of_row, offsets, E, K_dev, n_K, d, m, w_gate_up_packed,
+                           w_down_packed, y_perm, ws, need, stream);
+}
+
+int moe_ffn_status(const void* ws, size_t ws_bytes, int32_t* status, hipStream_t stream) {
+  if (!ws || !status || !aligned_all({ws, status})) return MOE_EINVAL;
+  // the counter header starts at the first 256-byte boundary of ws
+  if (ws_bytes < 256 + decomoe::ffn_ctr_bytes(0, 1)) return MOE_EWORKSPACE;
+  if (overlap(rng(status, 16), rng(ws, ws_bytes))) return MOE_EALIAS;
+  return hip_status(decomoe::launch_ffn_status(ws, status, stream));
 }
 
 int moe_pack_expert_weights(const void* w, moe_dtype dtype, int E, int rows, int cols,

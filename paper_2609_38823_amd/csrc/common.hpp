@@ -66,6 +66,8 @@ hipError_t launch_dispatch(const int32_t* idx, int T, int k, int E, const void* 
 hipError_t launch_expand_dense(const int32_t* idx, const float* w, int T, int k, int E,
                                const int32_t* K_dev, int32_t* idx_dense, float* w_dense, hipStream_t s);
 size_t ffn_ws_bytes(bool bf16, int rows_max, int E, int d, int m);
+// bytes of the expert FFN's counter header for rows_max rows and E experts
+size_t ffn_ctr_bytes(int rows_max, int E);
 // Token rows of the gate/up GEMM: x_perm [rows_max, d] when src_of_row is
 // NULL; else x [T, d] with dispatched row r read from x[src_of_row[r] / k]
 // (packed weights only)
@@ -73,10 +75,20 @@ struct RowGather {
   const int32_t* src_of_row;
   int k, T;
 };
+// K_dev values are clamped to [kmin, E] (kmin: the routing's k where the
+// entry point knows it)
 hipError_t launch_expert_ffn(const void* a_rows, bool bf16, const int32_t* offsets, int E,
                              const int32_t* K_dev, int n_K, int rows_max, int d, int m,
                              const void* w_gate_up, const void* w_down, bool packed, void* y_perm,
-                             void* ws, hipStream_t s, RowGather gather = RowGather{nullptr, 1, 0});
+                             void* ws, hipStream_t s, RowGather gather = RowGather{nullptr, 1, 0},
+                             int kmin = 1);
+// launch path recorded in the expert FFN's counter header
+constexpr int FFN_PATH_PERSISTENT = 1;  // both GEMMs in one persistent launch
+constexpr int FFN_PATH_TWO_LAUNCH = 2;  // packed weights, one launch per GEMM
+constexpr int FFN_PATH_ROW_MAJOR = 3;   // bf16 row-major weights
+constexpr int FFN_PATH_F32 = 4;         // float32
+// status of the last expert FFN call on a workspace (see ffn_status_kernel)
+hipError_t launch_ffn_status(const void* ws, int32_t* status, hipStream_t s);
 hipError_t launch_pack_weights(const void* w, int E, int R, int K, void* out, hipStream_t s);
 hipError_t launch_combine(const void* y_perm, bool bf16, const int32_t* row_of_slot,
                           const float* w, int T, int k, int d, const void* residual, void* out,

@@ -39,7 +39,8 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 
 // ---------------------------------------------------------------------------
-// Work items.  Experts e < Klim (Klim = max K_dev, or E) with rows
+// Work items.  Experts e < Klim (Klim = max K_dev clamped to [kmin, E], or
+// E) with rows
 // [offsets[e], offsets[e+1]) (clamped to [0, rows_max]) become ceil(rows/bm)
 // M-tiles; with nn n-tiles per GEMM the work list is ordered expert-major,
 // then n-tile, then m-tile, and holds at most max_tiles * nn items.  Every
@@ -55,6 +56,8 @@ struct Tiles {
   const int32_t* offsets;
   const int32_t* K_dev;
   int E, n_K, rows_max, bm, max_tiles, nn;
+  int kmin;  // lower clamp of K (the routing's k where known, so that every
+             // expert the prefix re-route can select is evaluated)
 };
 
 constexpr int NTHR = 256;  // threads per GEMM workgroup (4 wavefronts)
@@ -91,7 +94,7 @@ __device__ __forceinline__ bool find_work(const Tiles& tl, bool xcd, Work& out, 
     }
   }
   __syncthreads();
-  if (tl.K_dev) Klim = clampi(s_klim, 0, tl.E);
+  if (tl.K_dev) Klim = clampi(s_klim, tl.kmin, tl.E);
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     cnt[q] = 4 * tid + q < Klim ? (hi[q] - lo[q] + tl.bm - 1) / tl.bm : 0;
@@ -781,10 +784,18 @@ __global__ __launch_bounds__(NTHR, 2) void ffn_gemm_packed_kernel(
 // The wait always ends: within a queue items are claimed in order, so when a
 // down item is claimed every gate/up item of its range has been claimed by a
 // running workgroup, and gate/up items wait for nothing.  The poll is still
-// bounded (FFN_SPIN_LIMIT) so that a broken invariant cannot hang the device.
-//   ctr[16 x]     claim counter of XCD x (own 64-byte line)
-//   ctr[128 + t]  gate/up items of m-tile t completed
+// bounded (FFN_SPIN_LIMIT) so that a broken invariant cannot hang the device;
+// a wait that runs out is counted, so that moe_ffn_status reports it.
+//   ctr[16 x]      claim counter of XCD x (the 64 bytes from 16 x are written
+//   ctr[16 x + 1]  items completed on XCD x       only by workgroups of XCD x)
+//   ctr[16 x + 2]  waits on XCD x that ran out of polls
+//   ctr[16 x + 3]  items in the whole plan (every workgroup of XCD x stores it)
+//   ctr[FFN_CTR_PATH]  launch path of the call (FFN_PATH_*; set by clear_kernel)
+//   ctr[128 + t]   gate/up items of m-tile t completed
 // ctr (128 + max_tiles ints) is zeroed by clear_kernel before each launch.
+// A call ran every item of its plan exactly when no wait ran out and the
+// completed counts add up to the plan: an XCD that received no workgroup
+// leaves its items unclaimed and the sum short.
 // Cost of a tile: 4 + its active 32-row blocks; the first tile of an expert
 // costs more for the weight fetch that its later m-tiles find in L2: 2 with
 // 128-row tiles, a whole tile's cost with 64-row tiles (few rows per
@@ -796,6 +807,7 @@ __global__ __launch_bounds__(NTHR, 2) void ffn_gemm_packed_kernel(
 constexpr int FFN_MAXE = 1024;
 constexpr int FFN_SPIN_LIMIT = 1 << 22;
 constexpr int FFN_CTR_TILES = 128;  // ctr index of done[0]
+constexpr int FFN_CTR_PATH = 5;     // in XCD 0's block, written only by clear_kernel
 
 struct XcdRange {
   int a0, a1;  // tiles [a0, a1) of this XCD
@@ -828,7 +840,7 @@ __device__ XcdRange plan_tiles(const Tiles& tl, int xcc, int n_xcc, int* tstart,
     }
   }
   __syncthreads();
-  const int Klim = tl.K_dev ? clampi(s_klim, 0, tl.E) : tl.E;
+  const int Klim = tl.K_dev ? clampi(s_klim, tl.kmin, tl.E) : tl.E;
   constexpr int FULL = 4;  // + BM / 32 below
   const int full_cost = FULL + tl.bm / 32, bonus = tl.bm == 64 ? full_cost : 2;
   int cnt[4], cost[4], lc = 0, lw = 0;
@@ -891,8 +903,26 @@ __device__ XcdRange plan_tiles(const Tiles& tl, int xcc, int n_xcc, int* tstart,
   return XcdRange{s_a0, s_a1};
 }
 
-__global__ void clear_kernel(int* __restrict__ p, int n) {
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
+// zeroes the n counters and records the launch path of the call
+__global__ void clear_kernel(int* __restrict__ p, int n, int path) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+    p[i] = i == FFN_CTR_PATH ? path : 0;
+}
+
+// status[0] waits that ran out, [1] items completed, [2] items planned,
+// [3] launch path, summed over the XCD blocks of the counter header
+__global__ void ffn_status_kernel(const int* __restrict__ ctr, int32_t* __restrict__ status) {
+  if (threadIdx.x != 0) return;
+  int gave_up = 0, done = 0, planned = 0;
+  for (int x = 0; x < 8; ++x) {
+    done += ctr[16 * x + 1];
+    gave_up += ctr[16 * x + 2];
+    planned = max(planned, ctr[16 * x + 3]);
+  }
+  status[0] = gave_up;
+  status[1] = done;
+  status[2] = planned;
+  status[3] = ctr[FFN_CTR_PATH];
 }
 
 template <int BM>
@@ -914,6 +944,9 @@ __global__ __launch_bounds__(NTHR, 2) void ffn_fused_kernel(
   const int n_gu = ntile * tl.nn, n_all = n_gu + ntile * nn1;
   const int tid = threadIdx.x;
   int* const claim = ctr + 16 * xcc;
+  if (tid == 0)  // every workgroup of this XCD stores the same value
+    __hip_atomic_store(claim + 3, s_tstart[tl.E] * (tl.nn + nn1), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
   for (;;) {
     __syncthreads();  // the previous item is done with LDS and s_item
     if (tid == 0) s_item = atomicAdd(claim, 1);
@@ -951,14 +984,17 @@ __global__ __launch_bounds__(NTHR, 2) void ffn_fused_kernel(
       if (tid == 0) __hip_atomic_fetch_add(done, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     } else {
       if (tid == 0) {
-        for (int n = 0; n < FFN_SPIN_LIMIT; ++n) {
-          if (__hip_atomic_load(done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= tl.nn) break;
-          __builtin_amdgcn_s_sleep(4);
+        bool ready = false;
+        for (int n = 0; n < FFN_SPIN_LIMIT && !ready; ++n) {
+          ready = __hip_atomic_load(done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= tl.nn;
+          if (!ready) __builtin_amdgcn_s_sleep(4);
         }
+        if (!ready) __hip_atomic_fetch_add(claim + 2, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
       __syncthreads();
       packed_item<1, BM, BN>(H, Wdn, Y, wk, d, m, RowGather{nullptr, 1, 0}, aring);
     }
+    if (tid == 0) __hip_atomic_fetch_add(claim + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
@@ -1033,6 +1069,7 @@ using kern::ffn_gemm_bf16_kernel;
 using kern::ffn_gemm_f32_kernel;
 using kern::FFN_CTR_TILES;
 using kern::clear_kernel;
+using kern::ffn_status_kernel;
 using kern::ffn_fused_kernel;
 using kern::ffn_gemm_packed_kernel;
 using kern::pack_weights_kernel;
@@ -1104,6 +1141,16 @@ bool persistent_shape(int& grid, int& n_xcc) {
   return true;
 }
 
+// zeroes the counter header and the first n_tiles tile counters, and records
+// the launch path (a kernel rather than a memset, so that a captured graph
+// replays it)
+hipError_t clear_counters(int* ctr, int n_tiles, int path, hipStream_t s) {
+  const int n_ctr = FFN_CTR_TILES + n_tiles;
+  const int blocks = (n_ctr + 255) / 256 < 64 ? (n_ctr + 255) / 256 : 64;
+  clear_kernel<<<blocks, 256, 0, s>>>(ctr, n_ctr, path);
+  return hipGetLastError();
+}
+
 #define FFN_PACKED(MODE, BM)                                                      \
   ffn_gemm_packed_kernel<MODE, BM><<<(t.max_tiles * t.nn + 7) & ~7, NTHR, 0, s>>>( \
       A, W, C, t, d, m, g)
@@ -1115,9 +1162,7 @@ hipError_t launch_packed(int bm, const Tiles& t0, int nn1, const uint16_t* X, co
                          const RowGather g0, int* ctr, hipStream_t s) {
   int grid = 0, n_xcc = 0;
   if (persistent_shape(grid, n_xcc)) {
-    const int n_ctr = FFN_CTR_TILES + t0.max_tiles;
-    clear_kernel<<<(n_ctr + 255) / 256 < 64 ? (n_ctr + 255) / 256 : 64, 256, 0, s>>>(ctr, n_ctr);
-    hipError_t e = hipGetLastError();
+    hipError_t e = clear_counters(ctr, t0.max_tiles, FFN_PATH_PERSISTENT, s);
     if (e != hipSuccess) return e;
     if (bm == 128)
       ffn_fused_kernel<128><<<grid, NTHR, 0, s>>>(X, Wgu, Wdn, H, Y, t0, nn1, d, m, g0, n_xcc, ctr);
@@ -1125,6 +1170,8 @@ hipError_t launch_packed(int bm, const Tiles& t0, int nn1, const uint16_t* X, co
       ffn_fused_kernel<64><<<grid, NTHR, 0, s>>>(X, Wgu, Wdn, H, Y, t0, nn1, d, m, g0, n_xcc, ctr);
     return hipGetLastError();
   }
+  hipError_t e = clear_counters(ctr, 0, FFN_PATH_TWO_LAUNCH, s);
+  if (e != hipSuccess) return e;
   {
     const Tiles& t = t0;
     const uint16_t* A = X;
@@ -1133,7 +1180,7 @@ hipError_t launch_packed(int bm, const Tiles& t0, int nn1, const uint16_t* X, co
     const RowGather g = g0;
     if (bm == 128) FFN_PACKED(0, 128); else FFN_PACKED(0, 64);
   }
-  hipError_t e = hipGetLastError();
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   {
     Tiles t = t0;
@@ -1149,34 +1196,51 @@ hipError_t launch_packed(int bm, const Tiles& t0, int nn1, const uint16_t* X, co
 #undef FFN_PACKED
 }  // namespace
 
-// workspace: the intermediate h [rows_max, m], then (bf16) the counters of
-// the persistent kernel, 128 + max_tiles ints (sized for the smaller tile)
+// Workspace, from ws rounded up to a 256-byte boundary: the counters of the
+// persistent kernel (128 + max_tiles ints, sized for the smaller tile), then
+// the intermediate h [rows_max, m].  The rounding keeps every h row block of
+// a tile on whole 128-byte lines whatever the caller's alignment (a down item
+// must never find a line of its tile's h in L1 from a neighbouring tile).
+size_t ffn_ctr_bytes(int rows_max, int E) {
+  return align256((size_t)(kern::FFN_CTR_TILES + max_tiles_for(rows_max, E, 64)) * 4);
+}
 size_t ffn_ws_bytes(bool bf16, int rows_max, int E, int d, int m) {
   (void)d;
-  const size_t h = align256((size_t)rows_max * m * (bf16 ? 2 : 4));
-  return bf16 ? h + align256((size_t)(kern::FFN_CTR_TILES + max_tiles_for(rows_max, E, 64)) * 4) : h;
+  return 256 + ffn_ctr_bytes(rows_max, E) + align256((size_t)rows_max * m * (bf16 ? 2 : 4));
+}
+
+int* ffn_counters(void* ws) {
+  return reinterpret_cast<int*>(align256(reinterpret_cast<uintptr_t>(ws)));
+}
+
+hipError_t launch_ffn_status(const void* ws, int32_t* status, hipStream_t s) {
+  ffn_status_kernel<<<1, 64, 0, s>>>(ffn_counters(const_cast<void*>(ws)), status);
+  return hipGetLastError();
 }
 
 hipError_t launch_expert_ffn(const void* x_perm, bool bf16, const int32_t* offsets, int E,
                              const int32_t* K_dev, int n_K, int rows_max, int d, int m,
                              const void* w_gate_up, const void* w_down, bool packed, void* y_perm,
-                             void* ws, hipStream_t s, RowGather gather) {
+                             void* ws, hipStream_t s, RowGather gather, int kmin) {
   if (gather.src_of_row && !(bf16 && packed)) return hipErrorInvalidValue;
   const int bm = bf16 ? pick_bm(rows_max, E) : FBM;
   int nn0, nn1;
   bool wide0, wide1;
   n_tiles_of(bf16, packed, d, m, nn0, nn1, wide0, wide1);
-  Tiles t0{offsets, K_dev, E, K_dev ? n_K : 0, rows_max, bm, max_tiles_for(rows_max, E, bm), nn0};
+  Tiles t0{offsets, K_dev, E, K_dev ? n_K : 0, rows_max, bm, max_tiles_for(rows_max, E, bm), nn0,
+           kmin};
   Tiles t1 = t0;
   t1.nn = nn1;
-  void* h = ws;
+  int* const ctr = ffn_counters(ws);
+  void* h = reinterpret_cast<char*>(ctr) + ffn_ctr_bytes(rows_max, E);
   hipError_t err;
   if (bf16 && packed) {
-    int* ctr = reinterpret_cast<int*>(static_cast<char*>(ws) + align256((size_t)rows_max * m * 2));
     return launch_packed(bm, t0, nn1, static_cast<const uint16_t*>(x_perm),
                         static_cast<const uint16_t*>(w_gate_up), static_cast<const uint16_t*>(w_down),
                         static_cast<uint16_t*>(h), static_cast<uint16_t*>(y_perm), d, m, gather, ctr, s);
   }
+  err = clear_counters(ctr, 0, bf16 ? FFN_PATH_ROW_MAJOR : FFN_PATH_F32, s);
+  if (err != hipSuccess) return err;
   if (bf16) {
     err = launch_gemm(0, bm, wide0, t0, static_cast<const uint16_t*>(x_perm),
                       static_cast<const uint16_t*>(w_gate_up), static_cast<uint16_t*>(h), d, m, s);

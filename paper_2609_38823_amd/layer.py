@@ -153,6 +153,7 @@ class MoELayer:
             abi.moe_pack_router(self.w_r, self.w_r_packed)
         self.device = device
         self._bufs: dict = {}
+        self._kdev: dict = {}  # device copies of fixed prefix lengths
 
     def _route(self, x, b: Buffers, idx, w, stream=None):
         """Router logits into b.logits and the full-pool Top-k."""
@@ -208,11 +209,25 @@ class MoELayer:
         self._experts(x, b, b.idx, b.w, stream=stream, mark=mark, residual=residual, out=out)
         return b
 
-    def forward_prefix(self, x: torch.Tensor, K_dev: torch.Tensor, b: Buffers | None = None,
+    def prefix_tensor(self, K: int) -> torch.Tensor:
+        """A device copy of a host prefix length, checked against Eq. 12's
+        range k <= K <= E (made once per value and kept, so that a captured
+        graph can read it)."""
+        K = int(K)
+        if not self.k <= K <= self.E:
+            raise ValueError(f"prefix length {K} outside [k, E] = [{self.k}, {self.E}]")
+        if K not in self._kdev:
+            self._kdev[K] = torch.full((4,), K, dtype=torch.int32, device=self.device)[:1]
+        return self._kdev[K]
+
+    def forward_prefix(self, x: torch.Tensor, K, b: Buffers | None = None,
                        stream=None, mark=None, residual=None, out=None) -> Buffers:
         """A given prefix length instead of Eq. 12 (the fixed-prefix variant
-        of the component ablation): logits over all E experts, Top-k inside
-        [0, K_dev[0]), experts [0, K) only."""
+        of the component ablation, Table 2): logits over all E experts, Top-k
+        inside [0, K), experts [0, K) only.  K is a host int (checked:
+        k <= K <= E) or a device int32 tensor holding K (the route and the
+        gathering expert FFN both raise a value below k to k)."""
+        K_dev = K if isinstance(K, torch.Tensor) else self.prefix_tensor(K)
         b = b or self.buffers(x.shape[0])
         if self.w_r_packed is not None:
             abi.moe_route_packed(x, self.w_r_packed, self.bias, self.k, b.logits, b.idx, b.w, K_dev=K_dev,

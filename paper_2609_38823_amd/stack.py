@@ -84,10 +84,11 @@ class MoEStack:
         return self._h[key]
 
     def layer_forward(self, l: int, src: torch.Tensor, dst: torch.Tensor, rcep: bool, p: float,
-                      stream=None, mark=None, K_fixed: torch.Tensor | None = None) -> Buffers:
+                      stream=None, mark=None, K_fixed=None) -> Buffers:
         """One block: dst = src + MoE_l(src); dst may be src (in place).
-        rcep: the RCEP span (Eq. 12's K, or K_fixed when given); else the
-        full expert pool."""
+        rcep: the RCEP span (Eq. 12's K, or the prefix length K_fixed when
+        given: a host int or a device int32 tensor); else the full expert
+        pool."""
         b = self.buffers(src.shape[0])
         layer = self.layers[l]
         if rcep and K_fixed is not None:
@@ -98,8 +99,7 @@ class MoEStack:
         return layer.forward_dense(src, b=b, stream=stream, mark=mark, residual=src, out=dst)
 
     def forward(self, x: torch.Tensor, n_visual: int, p: float, exit_layer: int | None,
-                stream=None, hook=None, after_exit: str = "rcep", K_fixed: torch.Tensor | None = None
-                ) -> torch.Tensor:
+                stream=None, hook=None, after_exit: str = "rcep", K_fixed=None) -> torch.Tensor:
         """Run the stack over x [T, d] (visual rows [0, n_visual) first).
 
         exit_layer is the first text-only layer: the visual rows are removed
@@ -107,10 +107,15 @@ class MoEStack:
         None runs every layer dense.  x itself is not modified.  Returns the
         final hidden rows (a buffer owned by the stack).  ``hook(l, src)``,
         if given, is called before layer l with its input rows.
-        after_exit selects the layers from the exit on (component ablation):
-        "rcep" (Eq. 12), "dense" (all experts: the visual exit alone) or
-        "fixed" (the prefix length K_fixed[0]).
+        after_exit selects the layers from the exit on (component ablation,
+        Table 2): "rcep" (Eq. 12), "dense" (all experts: the visual exit
+        alone) or "fixed" (the prefix length K_fixed: a host int, checked
+        against [k, E], or a device int32 tensor).
         """
+        if after_exit not in ("rcep", "dense", "fixed"):
+            raise ValueError("after_exit is 'rcep', 'dense' or 'fixed'")
+        if after_exit == "fixed" and K_fixed is None:
+            raise ValueError("the fixed prefix needs K_fixed")
         T = x.shape[0]
         src = x
         h = self.hidden(T)

@@ -33,7 +33,8 @@ def test_header_declares_the_boundary():
         "moe_dispatch", "moe_expert_ffn", "moe_expert_ffn_packed", "moe_pack_expert_weights",
         "moe_pack_router", "moe_permute_experts", "moe_route", "moe_route_packed", "moe_savb_gate",
         "moe_savb_workspace_size", "moe_status_string", "moe_workspace_size", "drop_visual_block_if",
-        "moe_expand_dense_routing", "moe_expert_ffn_packed_gather", "moe_calibrate_route_prefix"])
+        "moe_expand_dense_routing", "moe_expert_ffn_packed_gather", "moe_calibrate_route_prefix",
+        "moe_ffn_status"])
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -194,6 +195,17 @@ def test_gather_ffn_rejects(lib):
     assert call(T=1 << 20, d=2048) == EUNSUPPORTED  # T*d*2 >= 2^31
     assert call(T=0) == 0            # nothing to do
     assert call(x=ctypes.c_void_p(0x10002)) == EINVAL  # misaligned
+
+
+def test_ffn_status_rejects(lib):
+    lib.moe_ffn_status.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p]
+    ws = ctypes.c_void_p(0x1000000)
+    st = ctypes.c_void_p(0x2000000)
+    assert lib.moe_ffn_status(NULL, 1 << 20, st, NULL) == EINVAL
+    assert lib.moe_ffn_status(ws, 1 << 20, NULL, NULL) == EINVAL
+    assert lib.moe_ffn_status(ws, 1023, st, NULL) == EWORKSPACE   # smaller than the counter header
+    assert lib.moe_ffn_status(ws, 1 << 20, ctypes.c_void_p(0x1000100), NULL) == EALIAS
+    assert lib.moe_ffn_status(ctypes.c_void_p(0x1000004), 1 << 20, st, NULL) == EINVAL  # misaligned
 
 
 def test_combine_and_drop_reject(lib):

@@ -237,6 +237,60 @@ def test_dense_equivalent_executor_matches_sparse(qwen):
     # the same eight products per element, summed in another order: within
     # a few bf16 units of the sparse result
     assert np.abs(out_dense - out_sparse).max() <= 4 * 2.0 ** -8 * np.abs(out_sparse).max()
+    # and against the oracle's RCEP layer at the GPU's K (teacher-forced on
+    # the GPU's logits), element by element over every text row
+    logits = host(b.logits).astype(np.float64)
+    ref = oracle.moe_layer_rcep(text, rp["w_r"], rp["bias"], rp["w_gate_up"], rp["w_down"], sh.k, 0.9,
+                                logits=logits, K_override=[K])
+    np.testing.assert_array_equal(host(b.idx), ref["idx"])
+    assert rel_inf(out_dense, ref["out"]) <= TOL["bf16"]
+    assert row_rel(out_dense, ref["out"]) <= TOL["bf16"]
+
+
+@pytest.mark.parametrize("K", [8, 50, 85, 128])
+def test_fixed_prefix_layer(qwen, K):
+    """The fixed-prefix variant of the component ablation (Table 2: a prefix
+    of 50 instead of Eq. 12; the keep ratios of the order study): the split
+    router's logits over all 128 experts, Top-k inside [0, K), the expert FFN
+    over experts [0, K) only.  Indices bit-exact and outputs within 2e-2 of
+    the oracle's layer at that K on the GPU's logits, every text row."""
+    wl, x, rp, layer = qwen
+    sh = wl.shape
+    text = x[wl.n_visual:]
+    xd = torch.from_numpy(text).cuda().to(torch.bfloat16)
+    assert layer.w_r_packed is not None  # the bf16 split router path (moe_route_packed with K_dev)
+    b = layer.forward_prefix(xd, K)
+    logits = host(b.logits).astype(np.float64)
+    ref = oracle.moe_layer_rcep(text, rp["w_r"], rp["bias"], rp["w_gate_up"], rp["w_down"], sh.k, 0.9,
+                                logits=logits, K_override=[K])
+    gi = host(b.idx)
+    np.testing.assert_array_equal(gi, ref["idx"])
+    assert gi.max() < K
+    counts = host(b.counts)
+    np.testing.assert_array_equal(counts, ref["counts"])
+    assert (counts[K:] == 0).all()
+    np.testing.assert_array_equal(host(b.row_of_slot), ref["row_of_slot"])
+    np.testing.assert_allclose(host(b.w), ref["w"], rtol=1e-5, atol=1e-7)
+    out = host(b.out)
+    assert rel_inf(out, ref["out"]) <= TOL["bf16"]
+    assert row_rel(out, ref["out"]) <= TOL["bf16"]
+
+
+def test_fixed_prefix_below_k(qwen):
+    """Eq. 12 gives K >= k, so a host prefix below k is rejected; a device
+    value below k is raised to k by the route and by the gathering expert
+    FFN alike (bitwise the result at K = k)."""
+    wl, x, rp, layer = qwen
+    text = x[wl.n_visual:]
+    xd = torch.from_numpy(text).cuda().to(torch.bfloat16)
+    with pytest.raises(ValueError):
+        layer.forward_prefix(xd, wl.shape.k - 1)
+    with pytest.raises(ValueError):
+        layer.forward_prefix(xd, wl.shape.E + 1)
+    ref = host(layer.forward_prefix(xd, wl.shape.k).out).copy()
+    K_dev = torch.full((4,), 3, dtype=torch.int32, device="cuda")[:1]
+    got = host(layer.forward_prefix(xd, K_dev).out)
+    np.testing.assert_array_equal(got, ref)
 
 
 def _sweep_cases():

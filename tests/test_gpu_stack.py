@@ -135,19 +135,26 @@ def check_order(stack, l):
     np.testing.assert_array_equal(stack.orders[l], oracle.mean_mass_order(M[None, :])[0])
 
 
-def check_layer(stack, l, h_in, rcep, p, dt, sample=None):
+def check_layer(stack, l, h_in, rcep, p, dt, sample=None, K_fixed=None):
     """Run layer l on h_in through the stack's call, then compare it with the
-    oracle's layer fed the same rows and the GPU's logits."""
+    oracle's layer fed the same rows and the GPU's logits (K_fixed: a given
+    prefix length instead of Eq. 12)."""
     h0 = host(h_in).copy()
     dst = torch.empty_like(h_in)
-    b = stack.layer_forward(l, h_in, dst, rcep, p)
+    b = stack.layer_forward(l, h_in, dst, rcep, p, K_fixed=K_fixed)
     # the layer's MoE output on its own (same y_perm, rows and weights)
     abi.moe_combine(b.y_perm, b.row_of_slot, b.w, b.out)
     prm = oracle_params(stack, l)
     k = stack.sh.k
     logits = host(b.logits).astype(np.float64)
     rows = np.arange(h0.shape[0]) if sample is None else sample
-    if rcep:
+    if rcep and K_fixed is not None:
+        K = int(K_fixed)
+        ref_idx, _ = oracle.prefix_route(logits, K, k)
+        np.testing.assert_array_equal(host(b.idx), ref_idx)
+        ref = oracle.moe_layer_rcep(h0[rows], prm["w_r"], prm["bias"], prm["w_gate_up"], prm["w_down"],
+                                    k, p, logits=logits[rows], K_override=[K])
+    elif rcep:
         idx_full, w_full = oracle.full_pool_route(logits, k)
         np.testing.assert_array_equal(host(b.idx_full), idx_full)
         mass = oracle.activated_mass(idx_full, w_full, stack.sh.E)
@@ -206,6 +213,45 @@ def test_tiny_stack_f32_teacher_forced_and_free_running():
                                  exit_layer=wl.exit_layer, v0=0, v1=wl.n_visual)
     assert [int(K[0]) for K in Kref[wl.exit_layer:]] == Ks[wl.exit_layer:]
     assert rel_inf(final, ref) <= TOL["f32"]
+
+
+@pytest.mark.parametrize("mode,K_fixed", [("dense", None), ("fixed", 5), ("fixed", 2), ("fixed", 16)])
+def test_tiny_stack_ablation_modes(mode, K_fixed):
+    """The component-ablation modes of the stack (Table 2): the visual exit
+    alone (every expert after the exit) and the exit with a fixed prefix
+    instead of Eq. 12 (K = 5, K = k = 2, K = E = 16).  Every layer
+    teacher-forced against the oracle; the stack's own forward gives the
+    layer-by-layer rows bit for bit; the oracle's free-running stack in the
+    same mode agrees within the fp32 tolerance."""
+    wl = I.WORKLOADS["tiny_stack_f32"]
+    sh = wl.shape
+    st = MoEStack(wl)
+    x_np = I.tokens(sh, wl.T, seed=wl.seed)
+    x = torch.from_numpy(x_np).cuda()
+    h = x
+    for l in range(st.L):
+        if l == wl.exit_layer:
+            ht = torch.empty((wl.T - wl.n_visual, sh.d), dtype=torch.float32, device="cuda")
+            abi.drop_visual_block(h, 0, wl.n_visual, ht)
+            h = ht
+        after = l >= wl.exit_layer
+        h, K = check_layer(st, l, h, after and mode == "fixed", wl.p, "f32",
+                           K_fixed=K_fixed if after else None)
+        if after and mode == "fixed":
+            assert K == K_fixed
+    final = host(h)
+    out = st.forward(x, wl.n_visual, wl.p, wl.exit_layer, after_exit=mode, K_fixed=K_fixed)
+    np.testing.assert_array_equal(host(out), final)
+    ref, Kref = oracle.moe_stack(x_np, [oracle_params(st, l) for l in range(st.L)], sh.k, wl.p,
+                                 exit_layer=wl.exit_layer, v0=0, v1=wl.n_visual, after_exit=mode,
+                                 K_fixed=K_fixed)
+    if mode == "fixed":
+        assert all(int(K[0]) == K_fixed for K in Kref[wl.exit_layer:])
+    else:
+        assert all(K is None for K in Kref)
+    assert rel_inf(final, ref) <= TOL["f32"]
+    with pytest.raises(ValueError):
+        st.forward(x, wl.n_visual, wl.p, wl.exit_layer, after_exit="fixed", K_fixed=sh.k - 1)
 
 
 def test_tiny_stack_gated_exit():

@@ -60,6 +60,21 @@ def f32(shape):
     return torch.full(shape, float("nan"), dtype=torch.float32, device="cuda")
 
 
+def assert_ffn_ran_all(ws):
+    """The last expert FFN call on ws evaluated every item of its plan and
+    no down item gave up waiting for its h (moe_ffn_status)."""
+    st = torch.full((4,), -1, dtype=torch.int32, device="cuda")
+    abi.moe_ffn_status(ws, st)
+    gave_up, done, planned, path = (int(v) for v in host(st))
+    assert path in (abi.FFN_PATH_PERSISTENT, abi.FFN_PATH_TWO_LAUNCH, abi.FFN_PATH_ROW_MAJOR,
+                    abi.FFN_PATH_F32), path
+    assert gave_up == 0
+    assert done == planned
+    if path != abi.FFN_PATH_PERSISTENT:
+        assert done == planned == 0
+    return path, planned
+
+
 def ws_for(T, E, k, d, m=1, n_seg=1):
     """Workspace for any entry point at these sizes (moe_workspace_size)."""
     return torch.empty(abi.moe_workspace_size(max(T, 1), E, k, d, m, n_seg), dtype=torch.uint8,
@@ -531,6 +546,8 @@ def test_expert_ffn(E, d, m, dt, rows, K, cnt):
     K_dev = dev(np.array([K], np.int32)) if K is not None else None
     abi.moe_expert_ffn(dev(xp, TDT[dt]), dev(offsets), dev(prm["w_gate_up"], TDT[dt]),
                        dev(prm["w_down"], TDT[dt]), y, ws, K_dev=K_dev)
+    path, _ = assert_ffn_ran_all(ws)
+    assert path == (abi.FFN_PATH_F32 if dt == "f32" else abi.FFN_PATH_ROW_MAJOR)
     got = host(y)
     live = expert_of_row < (K if K is not None else E)
     ref = oracle.expert_ffn_rows(xp[live], expert_of_row[live], prm["w_gate_up"], prm["w_down"])
@@ -603,12 +620,16 @@ def test_expert_ffn_packed(E, d, m, dt, rows, K, cnt):
     y = torch.full((rows, d), 7.0, dtype=TDT[dt], device="cuda")
     abi.moe_expert_ffn(xp, offsets, wgu, wd, y_ref, ws, K_dev=K_dev)
     abi.moe_expert_ffn_packed(xp, offsets, wgu_p, wd_p, y, ws, K_dev=K_dev)
+    path, planned = assert_ffn_ran_all(ws)
+    assert path == abi.FFN_PATH_PERSISTENT and (planned > 0) == (rows > 0)
     # same fragments, same k order, same float32 accumulation: bitwise equal
     assert torch.equal(y.view(torch.int16), y_ref.view(torch.int16))
     expert_of_row = np.repeat(np.arange(E), counts)
     live = expert_of_row < (K if K is not None else E)
     ref = oracle.expert_ffn_rows(host(xp)[live], expert_of_row[live], prm["w_gate_up"], prm["w_down"])
     assert rel_inf(host(y)[live], ref) <= TOL[dt]
+    assert row_rel(host(y)[live], ref) <= TOL[dt]
+    assert (host(y)[~live] == 7.0).all()  # experts >= K are not evaluated
 
 
 def test_expert_ffn_clamps_offsets_to_rows_max():
@@ -676,15 +697,79 @@ def test_expert_ffn_packed_gather(T, E, k, d, m, K):
     abi.moe_dispatch(dev(idx), E, None, counts2, offsets2, src2, ros2, None, ws)
     assert torch.equal(src2, src) and torch.equal(offsets2, offsets)
     abi.moe_expert_ffn_packed_gather(x, k, src2, offsets2, wgu_p, wd_p, y, ws, K_dev=K_dev)
+    assert_ffn_ran_all(ws)
     assert torch.equal(y.view(torch.int16), y_ref.view(torch.int16))
-    # against the oracle on the live rows (every row when small, else a sample)
+    # against the oracle on every live row
     rs = host(src)
     e_of_row = np.repeat(np.arange(E), host(counts))
     live = np.flatnonzero(e_of_row < (K if K is not None else E))
-    if live.size > 2048:
-        live = np.random.default_rng(T).choice(live, 2048, replace=False)
     ref = oracle.expert_ffn_rows(host(x)[rs[live] // k], e_of_row[live], prm["w_gate_up"], prm["w_down"])
     assert rel_inf(host(y)[live], ref) <= TOL["bf16"]
+    assert row_rel(host(y)[live], ref) <= TOL["bf16"]
+
+
+@pytest.mark.parametrize("shift", [16, 48, 112])
+def test_expert_ffn_packed_gather_unaligned_workspace(shift):
+    """A workspace that starts 16 bytes (not 256) into an allocation gives
+    the bits of an aligned one: the library rounds its h and counters up to
+    a 256-byte boundary, so no h line is shared between token tiles."""
+    T, E, k, d, m = 1024, 32, 4, 512, 256
+    sh = I.LayerShape(d=d, E=E, m=m, k=k, dtype="bf16")
+    prm = I.layer_params(sh, seed=31)
+    idx, _ = I.synthetic_routing(T, E, k, seed=32)
+    x = dev(I.synthetic_rows(T, d, "bf16", seed=33), torch.bfloat16)
+    A = T * k
+    counts, offsets, src, ros = i32((E,)), i32((E + 1,)), i32((A,)), i32((A,))
+    nb = abi.moe_workspace_size(T, E, k, d, m, 1)
+    ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
+    big = torch.empty(nb + 256, dtype=torch.uint8, device="cuda")
+    ws_shift = big[shift:shift + nb]
+    assert ws_shift.data_ptr() % 256 == shift
+    abi.moe_dispatch(dev(idx), E, None, counts, offsets, src, ros, None, ws)
+    wgu, wd = dev(prm["w_gate_up"], torch.bfloat16), dev(prm["w_down"], torch.bfloat16)
+    wgu_p, wd_p = torch.empty_like(wgu), torch.empty_like(wd)
+    abi.moe_pack_expert_weights(wgu, wgu_p)
+    abi.moe_pack_expert_weights(wd, wd_p)
+    y1 = torch.full((A, d), 7.0, dtype=torch.bfloat16, device="cuda")
+    y2 = torch.full((A, d), 7.0, dtype=torch.bfloat16, device="cuda")
+    abi.moe_expert_ffn_packed_gather(x, k, src, offsets, wgu_p, wd_p, y1, ws)
+    assert_ffn_ran_all(ws)
+    for _ in range(3):
+        abi.moe_expert_ffn_packed_gather(x, k, src, offsets, wgu_p, wd_p, y2, ws_shift)
+        assert_ffn_ran_all(ws_shift)
+        assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+        y2.fill_(7.0)
+
+
+def test_gather_ffn_clamps_K_below_k_like_the_route():
+    """A prefix length below k: moe_route raises it to k, and the gathering
+    FFN applies the same clamp, so every expert the re-route selected is
+    evaluated (bitwise the result with K = k)."""
+    T, E, k, d, m = 256, 32, 8, 512, 256
+    sh = I.LayerShape(d=d, E=E, m=m, k=k, dtype="bf16")
+    prm = I.layer_params(sh, seed=41)
+    lg = dev(I.synthetic_rows(T, E, "f32", seed=42), torch.float32)
+    A = T * k
+    wgu, wd = dev(prm["w_gate_up"], torch.bfloat16), dev(prm["w_down"], torch.bfloat16)
+    wgu_p, wd_p = torch.empty_like(wgu), torch.empty_like(wd)
+    abi.moe_pack_expert_weights(wgu, wgu_p)
+    abi.moe_pack_expert_weights(wd, wd_p)
+    x = dev(I.synthetic_rows(T, d, "bf16", seed=43), torch.bfloat16)
+    ws = torch.empty(abi.moe_workspace_size(T, E, k, d, m, 1), dtype=torch.uint8, device="cuda")
+    ys = {}
+    for K in (3, k):
+        K_dev = dev(np.array([K], np.int32))
+        idx, w = i32((T, k)), f32((T, k))
+        abi.moe_route(None, None, None, k, lg, idx, w, K_dev=K_dev)
+        assert int(host(idx).max()) == k - 1  # the route selected all of [0, k)
+        counts, offsets, src, ros = i32((E,)), i32((E + 1,)), i32((A,)), i32((A,))
+        abi.moe_dispatch(idx, E, None, counts, offsets, src, ros, None, ws)
+        y = torch.full((A, d), 7.0, dtype=torch.bfloat16, device="cuda")
+        abi.moe_expert_ffn_packed_gather(x, k, src, offsets, wgu_p, wd_p, y, ws, K_dev=K_dev)
+        assert_ffn_ran_all(ws)
+        ys[K] = y
+    assert torch.equal(ys[3].view(torch.int16), ys[k].view(torch.int16))
+    assert not (host(ys[3]) == 7.0).all(axis=1).any()  # every row written
 
 
 def test_packed_ffn_per_segment_K_uses_the_largest():
@@ -733,10 +818,10 @@ def test_packed_ffn_two_launch_fallback_matches_persistent(T, E, k, d, m, monkey
     y1 = torch.full((A, d), 7.0, dtype=torch.bfloat16, device="cuda")
     y2 = torch.full((A, d), 7.0, dtype=torch.bfloat16, device="cuda")
     abi.moe_expert_ffn_packed_gather(x, k, src, offsets, wgu_p, wd_p, y1, ws)
-    torch.cuda.synchronize()
+    assert assert_ffn_ran_all(ws)[0] == abi.FFN_PATH_PERSISTENT
     monkeypatch.setenv("DECOMOE_FFN_TWO_LAUNCH", "1")
     abi.moe_expert_ffn_packed_gather(x, k, src, offsets, wgu_p, wd_p, y2, ws)
-    torch.cuda.synchronize()
+    assert assert_ffn_ran_all(ws)[0] == abi.FFN_PATH_TWO_LAUNCH
     monkeypatch.delenv("DECOMOE_FFN_TWO_LAUNCH")
     assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
 
@@ -765,13 +850,18 @@ def test_persistent_ffn_repeated_calls_bitwise(T, monkeypatch):
     torch.cuda.synchronize()
     monkeypatch.delenv("DECOMOE_FFN_TWO_LAUNCH")
     ys = [torch.empty((A, d), dtype=torch.bfloat16, device="cuda") for _ in range(4)]
+    st = torch.full((40, 4), -1, dtype=torch.int32, device="cuda")
     for i in range(40):
         abi.moe_expert_ffn_packed_gather(x, k, src, offsets, wgu_p, wd_p, ys[i % 4], ws)
+        abi.moe_ffn_status(ws, st[i])  # no host wait between the calls
         if i % 4 == 3:
             torch.cuda.synchronize()
             for y in ys:
                 assert torch.equal(y.view(torch.int16), ref.view(torch.int16)), i
                 y.fill_(7.0)
+    s_h = host(st)
+    assert (s_h[:, 0] == 0).all() and (s_h[:, 3] == abi.FFN_PATH_PERSISTENT).all()
+    assert (s_h[:, 1] == s_h[:, 2]).all() and (s_h[:, 2] == s_h[0, 2]).all() and s_h[0, 2] > 0
 
 
 def test_expert_ffn_packed_gather_out_of_range_rows_read_token_zero():

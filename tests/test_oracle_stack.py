@@ -10,6 +10,11 @@ with the residual stream), CPU only.
     run over the visual rows, changes K and fails this);
   * at p = 1 with every expert routed, K = E and the RCEP block is the dense
     block (Eq. 12), so the text rows equal those of the all-dense stack.
+  * the component-ablation modes (Table 2): the exit alone ("dense" after the
+    exit) keeps the text rows of the stack without an exit, since a dense
+    block routes each token by itself; a fixed prefix of E is the full pool;
+    a fixed prefix equal, layer by layer, to the K that Eq. 12 chose
+    reproduces the RCEP stack; and a fixed prefix below k is rejected.
 """
 
 import numpy as np
@@ -77,3 +82,44 @@ def test_p_one_with_full_support_is_the_dense_stack():
     dense, Kd = oracle.moe_stack(h, layers, K_TOP, 1.0, exit_layer=None)
     assert all(K is None for K in Kd)
     np.testing.assert_allclose(out, dense[8:], rtol=0, atol=1e-12)
+
+
+def test_exit_alone_keeps_the_text_rows_of_the_dense_stack():
+    rng = np.random.default_rng(8)
+    h = rng.normal(size=(30, D))
+    layers = _layers(4, 9)
+    out, Ks = oracle.moe_stack(h, layers, K_TOP, 0.7, exit_layer=2, v0=0, v1=10, after_exit="dense")
+    assert all(K is None for K in Ks)
+    dense, _ = oracle.moe_stack(h, layers, K_TOP, 0.7, exit_layer=None)
+    np.testing.assert_allclose(out, dense[10:], rtol=0, atol=1e-12)
+    # the mode has power: RCEP after the exit prunes experts and moves the rows
+    rc, Kr = oracle.moe_stack(h, layers, K_TOP, 0.7, exit_layer=2, v0=0, v1=10)
+    assert any(int(K[0]) < E for K in Kr[2:])
+    assert np.abs(rc - out).max() > 1e-6
+
+
+def test_fixed_prefix_modes():
+    rng = np.random.default_rng(12)
+    h = rng.normal(size=(26, D))
+    layers = _layers(4, 13)
+    full, Kf = oracle.moe_stack(h, layers, K_TOP, 0.6, exit_layer=1, v0=0, v1=6, after_exit="fixed",
+                                K_fixed=E)
+    assert all(int(K[0]) == E for K in Kf[1:])
+    ex, _ = oracle.moe_stack(h, layers, K_TOP, 0.6, exit_layer=1, v0=0, v1=6, after_exit="dense")
+    np.testing.assert_allclose(full, ex, rtol=0, atol=1e-12)
+    rc, Kr = oracle.moe_stack(h, layers, K_TOP, 0.6, exit_layer=1, v0=0, v1=6)
+    per_layer = [0] + [int(K[0]) for K in Kr[1:]]
+    assert min(per_layer[1:]) < E  # Eq. 12 prunes somewhere
+    fx, Kx = oracle.moe_stack(h, layers, K_TOP, 0.6, exit_layer=1, v0=0, v1=6, after_exit="fixed",
+                              K_fixed=per_layer)
+    np.testing.assert_array_equal(fx, rc)
+    assert [int(K[0]) for K in Kx[1:]] == per_layer[1:]
+    # a shorter fixed prefix routes inside it only
+    short, Ks = oracle.moe_stack(h, layers, K_TOP, 0.6, exit_layer=1, v0=0, v1=6, after_exit="fixed",
+                                 K_fixed=3)
+    assert all(int(K[0]) == 3 for K in Ks[1:])
+    assert np.abs(short - rc).max() > 1e-6
+    with pytest.raises(ValueError):
+        oracle.moe_stack(h, layers, K_TOP, 0.6, exit_layer=1, v0=0, v1=6, after_exit="fixed", K_fixed=1)
+    with pytest.raises(ValueError):
+        oracle.moe_stack(h, layers, K_TOP, 0.6, exit_layer=1, after_exit="fixed")
