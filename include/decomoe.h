@@ -347,6 +347,32 @@ int moe_expert_ffn_packed_gather(const void* x, moe_dtype dtype, int T, int k,
                                  void* y_perm, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * moe_expert_ffn_packed_gather_noalloc - moe_expert_ffn_packed_gather for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * serving loops, harnesses that forbid hipMalloc): the same arguments
+ * without (ws, ws_bytes), the same checks and bitwise the same y_perm.
+ * Its scratch (the intermediate h and the persistent kernel's counters) is
+ * a device array of MOE_NOALLOC_SCRATCH_BYTES inside the library, one per
+ * GPU, held until the process ends; the call allocates nothing (no
+ * hipMalloc, no hipFree) and on its first use on a device looks up that
+ * device's copy of the array once.  Every call on a GPU shares that GPU's
+ * array: calls that may overlap on one GPU (other streams, other threads)
+ * race and must be serialised by the caller.  The counters are cleared by
+ * each call; nothing else needs to start at zero.
+ * Limit: the workspace moe_expert_ffn_packed_gather would need,
+ * 256 + 4 * (128 + ceil(T*k / 64) + E) rounded up to 256
+ *     + T * k * m * 2 rounded up to 256 bytes,
+ * must fit MOE_NOALLOC_SCRATCH_BYTES, else MOE_EWORKSPACE (nothing is
+ * launched).  With m = 768 that is up to 21 800 dispatched rows (T * k).
+ */
+#define MOE_NOALLOC_SCRATCH_BYTES (32u << 20)
+int moe_expert_ffn_packed_gather_noalloc(const void* x, moe_dtype dtype, int T, int k,
+                                         const int32_t* src_of_row, const int32_t* offsets, int E,
+                                         const int32_t* K_dev, int n_K, int d, int m,
+                                         const void* w_gate_up_packed, const void* w_down_packed,
+                                         void* y_perm, hipStream_t stream);
+
+/*
  * moe_ffn_status - how the last expert FFN call on a workspace ran
  * (Algorithm 2: the first K expert MLPs are all evaluated).
  *

@@ -28,7 +28,10 @@ EXPORTS = ("moe_status_string", "moe_workspace_size", "moe_route", "moe_route_pa
            "moe_pack_expert_weights",
            "moe_combine", "moe_combine_residual", "drop_visual_block", "moe_permute_experts",
            "moe_savb_workspace_size", "moe_savb_gate", "drop_visual_block_if",
-           "moe_expand_dense_routing", "moe_ffn_status")
+           "moe_expand_dense_routing", "moe_ffn_status", "moe_expert_ffn_packed_gather_noalloc")
+
+# size of the library's own scratch array of the allocation-free expert FFN
+NOALLOC_SCRATCH_BYTES = 32 << 20
 
 # launch paths of the expert FFN (moe_ffn_status)
 FFN_PATH_PERSISTENT, FFN_PATH_TWO_LAUNCH, FFN_PATH_ROW_MAJOR, FFN_PATH_F32 = 1, 2, 3, 4
@@ -75,6 +78,8 @@ def load() -> ctypes.CDLL:
         "drop_visual_block_if": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P]),
         "moe_expand_dense_routing": (_I, [_P, _P, _I, _I, _I, _P, _P, _P, _P]),
         "moe_ffn_status": (_I, [_P, _S, _P, _P]),
+        "moe_expert_ffn_packed_gather_noalloc": (_I, [_P, _I, _I, _I, _P, _P, _I, _P, _I, _I, _I, _P, _P,
+                                                      _P, _P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -239,6 +244,18 @@ def moe_expert_ffn_packed_gather(x, k, src_of_row, offsets, w_gate_up_packed, w_
         _p(x), _dt(x), T, k, _i32(src_of_row), _i32(offsets), E, _i32(K_dev), n_K, d, two_m // 2,
         _p(w_gate_up_packed), _p(w_down_packed), _p(y_perm), _p(ws), ws.numel() * ws.element_size(),
         _stream(stream)))
+
+
+def moe_expert_ffn_packed_gather_noalloc(x, k, src_of_row, offsets, w_gate_up_packed, w_down_packed,
+                                         y_perm, K_dev=None, stream=None):
+    """moe_expert_ffn_packed_gather on the library's own scratch array (no
+    workspace; calls on one GPU must not overlap)."""
+    T, d = x.shape
+    E, two_m, _ = w_gate_up_packed.shape
+    n_K = K_dev.numel() if K_dev is not None else 0
+    _check("moe_expert_ffn_packed_gather_noalloc", load().moe_expert_ffn_packed_gather_noalloc(
+        _p(x), _dt(x), T, k, _i32(src_of_row), _i32(offsets), E, _i32(K_dev), n_K, d, two_m // 2,
+        _p(w_gate_up_packed), _p(w_down_packed), _p(y_perm), _stream(stream)))
 
 
 def moe_pack_expert_weights(w, w_packed, stream=None):

@@ -1,5 +1,7 @@
 // Exported C ABI: host-side validation, then the launches.  Nothing here
 // allocates, frees or synchronises.
+#include <mutex>
+
 #include "common.hpp"
 
 #include "../../include/decomoe.h"
@@ -508,3 +510,53 @@ int drop_visual_block(const void* h, moe_dtype dtype, int S, int d, int v0, int 
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Allocation-free expert FFN: the intermediate h and the persistent kernel's
+// counters live in `scratch`, a file-scope device array of fixed size that
+// every GPU the library runs on holds until the process ends.  Host code
+// reaches it only through the address hipGetSymbolAddress returns on that
+// device (the array's name on the host is a stand-in, not a device address).
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) unsigned char scratch[MOE_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices];  // device address of `scratch`, per device
+
+// the current device's address of `scratch`, looked up once per device
+int scratch_on_current_device(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return MOE_EHIP;
+  if (dev >= kMaxDevices) return MOE_EUNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return MOE_EHIP;
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return MOE_OK;
+}
+}  // namespace
+
+extern "C" int moe_expert_ffn_packed_gather_noalloc(const void* x, moe_dtype dtype, int T, int k,
+                                                    const int32_t* src_of_row, const int32_t* offsets,
+                                                    int E, const int32_t* K_dev, int n_K, int d, int m,
+                                                    const void* w_gate_up_packed,
+                                                    const void* w_down_packed, void* y_perm,
+                                                    hipStream_t stream) {
+  int rows_max = 0;
+  const int st = gather_ffn_args(x, dtype, T, k, src_of_row, offsets, E, K_dev, n_K, d, m,
+                                 w_gate_up_packed, w_down_packed, y_perm, &rows_max);
+  if (st != MOE_OK) return st;
+  if (rows_max == 0) return MOE_OK;
+  const size_t need = ffn_ws_bytes(true, rows_max, E, d, m);
+  if (need > (size_t)MOE_NOALLOC_SCRATCH_BYTES) return MOE_EWORKSPACE;
+  void* ws = nullptr;
+  const int sst = scratch_on_current_device(&ws);
+  if (sst != MOE_OK) return sst;
+  return gather_ffn_launch(x, T, k, src_of_row, offsets, E, K_dev, n_K, d, m, w_gate_up_packed,
+                           w_down_packed, y_perm, ws, need, stream);
+}

@@ -34,7 +34,7 @@ def test_header_declares_the_boundary():
         "moe_pack_router", "moe_permute_experts", "moe_route", "moe_route_packed", "moe_savb_gate",
         "moe_savb_workspace_size", "moe_status_string", "moe_workspace_size", "drop_visual_block_if",
         "moe_expand_dense_routing", "moe_expert_ffn_packed_gather", "moe_calibrate_route_prefix",
-        "moe_ffn_status"])
+        "moe_ffn_status", "moe_expert_ffn_packed_gather_noalloc"])
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -195,6 +195,34 @@ def test_gather_ffn_rejects(lib):
     assert call(T=1 << 20, d=2048) == EUNSUPPORTED  # T*d*2 >= 2^31
     assert call(T=0) == 0            # nothing to do
     assert call(x=ctypes.c_void_p(0x10002)) == EINVAL  # misaligned
+
+
+def test_gather_ffn_noalloc_rejects(lib):
+    """The allocation-free expert FFN checks its arguments like the gathering
+    FFN, and rejects sizes whose scratch exceeds its fixed array, all on the
+    host before any HIP call."""
+    from paper_2609_38823_amd import abi
+    f = lib.moe_expert_ffn_packed_gather_noalloc
+    names = ["x", "dt", "T", "k", "src", "off", "E", "K", "nK", "d", "m", "wgu", "wdn", "y", "s"]
+    ok = (P1, BF16, 16, 2, P2, P3, 16, NULL, 0, 256, 256, P4, P5, P6, NULL)
+
+    def call(**kw):
+        a = dict(zip(names, ok))
+        a.update(kw)
+        return f(*[a[n] for n in names])
+
+    assert call(dt=F32) == EUNSUPPORTED
+    assert call(m=128) == EUNSUPPORTED
+    assert call(k=0) == EINVAL and call(T=-1) == EINVAL
+    assert call(src=NULL) == EINVAL and call(y=NULL) == EINVAL
+    assert call(x=ctypes.c_void_p(0x10002)) == EINVAL
+    assert call(T=0) == 0
+    # m = 768: 21 800 dispatched rows fit the scratch, 21 900 do not
+    assert abi.NOALLOC_SCRATCH_BYTES == 32 << 20
+    assert lib.moe_workspace_size(10900, 128, 2, 2048, 768, 1) >= 256 + 21800 * 768 * 2
+    assert call(T=10950, k=2, E=128, d=2048, m=768) == EWORKSPACE
+    assert call(T=4096, k=8, E=128, d=2048, m=768) == EWORKSPACE  # 32 768 rows
+    assert call(T=1 << 20, d=2048) == EUNSUPPORTED  # T*d*2 >= 2^31
 
 
 def test_ffn_status_rejects(lib):
