@@ -27,7 +27,10 @@
  *
  * Conventions shared by every entry point
  *   - Every array pointer is a DEVICE pointer owned by the caller; the
- *     library never allocates, frees or retains device memory.  Arrays are
+ *     library never allocates or frees device memory at run time and
+ *     retains none of the caller's (its only device memory of its own is
+ *     the fixed scratch array of moe_expert_ffn_packed_gather_noalloc,
+ *     part of the loaded code object).  Arrays are
  *     row-major and contiguous.  Scratch memory comes from the caller as
  *     (ws, ws_bytes); moe_workspace_size() returns a sufficient size.  Its
  *     contents need no initialisation and are not preserved between calls
@@ -371,6 +374,63 @@ int moe_expert_ffn_packed_gather_noalloc(const void* x, moe_dtype dtype, int T, 
                                          const int32_t* K_dev, int n_K, int d, int m,
                                          const void* w_gate_up_packed, const void* w_down_packed,
                                          void* y_perm, hipStream_t stream);
+
+/*
+ * Predicated calls (for Algorithm 2's prefill as one captured HIP graph: the
+ * SAVB exit, Sec. 3.2, is decided on the device, so both per-layer variants
+ * are captured and the device state picks the one that runs).
+ *
+ * Each *_if call takes the arguments of the call it is named after, plus
+ *   guard, guard_lo, guard_hi   a device int32 and a half-open range: the
+ *       call's kernels run only if guard_lo <= *guard < guard_hi when they
+ *       execute (the value is read on the device, so a captured graph
+ *       replays the decision with the value of each replay); otherwise they
+ *       return at once and every output, workspace contents included, is
+ *       left as it was.  guard == NULL always runs.  guard must be 4-byte
+ *       aligned (MOE_EINVAL otherwise).  Nothing else in the call may write
+ *       *guard, except moe_savb_gate_if's exit_layer (below).
+ * Host-side checks and errors are those of the plain call; they do not
+ * depend on the predicate.  With guard == NULL the results are bitwise
+ * those of the plain call.  moe_ffn_status after a skipped expert FFN call
+ * reports the previous call.
+ */
+int moe_route_packed_if(const void* x, moe_dtype dtype, const void* w_r_packed, const float* bias,
+                        int T, int d, int E, int k, const int32_t* seg_offsets, int n_seg,
+                        const int32_t* K_dev, float* logits, int32_t* topk_idx, float* topk_w,
+                        void* ws, size_t ws_bytes, const int32_t* guard, int guard_lo, int guard_hi,
+                        hipStream_t stream);
+int moe_calibrate_route_prefix_if(const float* logits, const int32_t* topk_idx_full,
+                                  const float* topk_w_full, int T, int E, int k, double p,
+                                  double* mass, int32_t* K_out, int32_t* topk_idx, float* topk_w,
+                                  void* ws, size_t ws_bytes, const int32_t* guard, int guard_lo,
+                                  int guard_hi, hipStream_t stream);
+int moe_dispatch_if(const int32_t* topk_idx, int T, int k, int E, const void* x, moe_dtype dtype,
+                    int d, int32_t* counts, int32_t* offsets, int32_t* src_of_row,
+                    int32_t* row_of_slot, void* x_perm, void* ws, size_t ws_bytes,
+                    const int32_t* guard, int guard_lo, int guard_hi, hipStream_t stream);
+int moe_expert_ffn_packed_gather_if(const void* x, moe_dtype dtype, int T, int k,
+                                    const int32_t* src_of_row, const int32_t* offsets, int E,
+                                    const int32_t* K_dev, int n_K, int d, int m,
+                                    const void* w_gate_up_packed, const void* w_down_packed,
+                                    void* y_perm, void* ws, size_t ws_bytes, const int32_t* guard,
+                                    int guard_lo, int guard_hi, hipStream_t stream);
+int moe_combine_residual_if(const void* y_perm, moe_dtype dtype, const int32_t* row_of_slot,
+                            const float* topk_w, int T, int k, int d, const void* residual,
+                            void* out, const int32_t* guard, int guard_lo, int guard_hi,
+                            hipStream_t stream);
+/*
+ * moe_savb_gate_if - moe_savb_gate (Eqs. 2, 3) under the predicate, and
+ * when it runs and the gate fires (p_exit >= theta), also *exit_layer =
+ * layer.  With guard == exit_layer and the range [L, L + 1) for a value L
+ * that means "no exit yet", a chain of candidate layers records the first
+ * layer whose gate fires and skips every later gate.  exit_layer must not
+ * overlap p_exit or exit_flag (MOE_EALIAS) and be 4-byte aligned.
+ */
+int moe_savb_gate_if(const void* text_rows, moe_dtype dtype, int n, int d, const float* w1,
+                     const float* b1, int hid, const float* w2, const float* b2, double theta,
+                     float* feature, float* p_exit, int32_t* exit_flag, void* ws, size_t ws_bytes,
+                     const int32_t* guard, int guard_lo, int guard_hi, int32_t* exit_layer,
+                     int layer, hipStream_t stream);
 
 /*
  * moe_ffn_status - how the last expert FFN call on a workspace ran

@@ -28,7 +28,9 @@ EXPORTS = ("moe_status_string", "moe_workspace_size", "moe_route", "moe_route_pa
            "moe_pack_expert_weights",
            "moe_combine", "moe_combine_residual", "drop_visual_block", "moe_permute_experts",
            "moe_savb_workspace_size", "moe_savb_gate", "drop_visual_block_if",
-           "moe_expand_dense_routing", "moe_ffn_status", "moe_expert_ffn_packed_gather_noalloc")
+           "moe_expand_dense_routing", "moe_ffn_status", "moe_expert_ffn_packed_gather_noalloc",
+           "moe_route_packed_if", "moe_calibrate_route_prefix_if", "moe_dispatch_if",
+           "moe_expert_ffn_packed_gather_if", "moe_combine_residual_if", "moe_savb_gate_if")
 
 # size of the library's own scratch array of the allocation-free expert FFN
 NOALLOC_SCRATCH_BYTES = 32 << 20
@@ -78,6 +80,16 @@ def load() -> ctypes.CDLL:
         "drop_visual_block_if": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P]),
         "moe_expand_dense_routing": (_I, [_P, _P, _I, _I, _I, _P, _P, _P, _P]),
         "moe_ffn_status": (_I, [_P, _S, _P, _P]),
+        "moe_route_packed_if": (_I, [_P, _I, _P, _P, _I, _I, _I, _I, _P, _I, _P, _P, _P, _P, _P, _S,
+                                     _P, _I, _I, _P]),
+        "moe_calibrate_route_prefix_if": (_I, [_P, _P, _P, _I, _I, _I, _D, _P, _P, _P, _P, _P, _S,
+                                               _P, _I, _I, _P]),
+        "moe_dispatch_if": (_I, [_P, _I, _I, _I, _P, _I, _I, _P, _P, _P, _P, _P, _P, _S, _P, _I, _I, _P]),
+        "moe_expert_ffn_packed_gather_if": (_I, [_P, _I, _I, _I, _P, _P, _I, _P, _I, _I, _I, _P, _P, _P,
+                                                 _P, _S, _P, _I, _I, _P]),
+        "moe_combine_residual_if": (_I, [_P, _I, _P, _P, _I, _I, _I, _P, _P, _P, _I, _I, _P]),
+        "moe_savb_gate_if": (_I, [_P, _I, _I, _I, _P, _P, _I, _P, _P, _D, _P, _P, _P, _P, _S, _P, _I, _I,
+                                  _P, _I, _P]),
         "moe_expert_ffn_packed_gather_noalloc": (_I, [_P, _I, _I, _I, _P, _P, _I, _P, _I, _I, _I, _P, _P,
                                                       _P, _P]),
     }
@@ -339,3 +351,76 @@ def moe_ffn_status(ws, status, stream=None):
     if status.numel() < 4:
         raise ValueError("status needs 4 int32 entries")
     _check("moe_ffn_status", load().moe_ffn_status(_p(ws), _nbytes(ws), _i32(status), _stream(stream)))
+
+
+# --- predicated calls: the kernels run only while lo <= guard[0] < hi ------
+def _guard(guard):
+    """guard = (int32 device tensor, lo, hi) -> (pointer, lo, hi)."""
+    if guard is None:
+        return None, 0, 0
+    g, lo, hi = guard
+    return _i32(g), int(lo), int(hi)
+
+
+def moe_route_packed_if(x, w_r_packed, bias, k, logits, topk_idx, topk_w, guard, seg_offsets=None,
+                        K_dev=None, ws=None, stream=None):
+    T, E = logits.shape
+    d = x.shape[1]
+    gp, lo, hi = _guard(guard)
+    _check("moe_route_packed_if", load().moe_route_packed_if(
+        _p(x), _dt(x), _p(w_r_packed), _f32(bias), T, d, E, k, _i32(seg_offsets), _nseg(seg_offsets),
+        _i32(K_dev), _f32(logits), _i32(topk_idx), _f32(topk_w), _p(ws), _nbytes(ws), gp, lo, hi,
+        _stream(stream)))
+
+
+def moe_calibrate_route_prefix_if(logits, idx_full, w_full, p, mass, K_out, idx, w, guard, stream=None):
+    T, k = idx_full.shape
+    E = logits.shape[1]
+    gp, lo, hi = _guard(guard)
+    _check("moe_calibrate_route_prefix_if", load().moe_calibrate_route_prefix_if(
+        _f32(logits), _i32(idx_full), _f32(w_full), T, E, k, float(p), _f64(mass), _i32(K_out), _i32(idx),
+        _f32(w), None, 0, gp, lo, hi, _stream(stream)))
+
+
+def moe_dispatch_if(topk_idx, E, x, counts, offsets, src_of_row, row_of_slot, x_perm, ws, guard,
+                    stream=None):
+    T, k = topk_idx.shape
+    d = x.shape[1] if x is not None else 0
+    dt = _dt(x) if x is not None else MOE_F32
+    gp, lo, hi = _guard(guard)
+    _check("moe_dispatch_if", load().moe_dispatch_if(
+        _i32(topk_idx), T, k, E, _p(x), dt, d, _i32(counts), _i32(offsets), _i32(src_of_row),
+        _i32(row_of_slot), _p(x_perm), _p(ws), _nbytes(ws), gp, lo, hi, _stream(stream)))
+
+
+def moe_expert_ffn_packed_gather_if(x, k, src_of_row, offsets, w_gate_up_packed, w_down_packed, y_perm,
+                                    ws, guard, K_dev=None, stream=None):
+    T, d = x.shape
+    E, two_m, _ = w_gate_up_packed.shape
+    n_K = K_dev.numel() if K_dev is not None else 0
+    gp, lo, hi = _guard(guard)
+    _check("moe_expert_ffn_packed_gather_if", load().moe_expert_ffn_packed_gather_if(
+        _p(x), _dt(x), T, k, _i32(src_of_row), _i32(offsets), E, _i32(K_dev), n_K, d, two_m // 2,
+        _p(w_gate_up_packed), _p(w_down_packed), _p(y_perm), _p(ws), _nbytes(ws), gp, lo, hi,
+        _stream(stream)))
+
+
+def moe_combine_residual_if(y_perm, row_of_slot, topk_w, residual, out, guard, stream=None):
+    T, k = topk_w.shape
+    d = out.shape[1]
+    gp, lo, hi = _guard(guard)
+    _check("moe_combine_residual_if", load().moe_combine_residual_if(
+        _p(y_perm), _dt(y_perm), _i32(row_of_slot), _f32(topk_w), T, k, d, _p(residual), _p(out), gp, lo,
+        hi, _stream(stream)))
+
+
+def moe_savb_gate_if(text_rows, w1, b1, w2, b2, theta, p_exit, exit_flag, ws, guard, exit_layer=None,
+                     layer=0, feature=None, stream=None):
+    """moe_savb_gate under the predicate; when it fires, exit_layer[0] = layer."""
+    n, d = text_rows.shape
+    hid = w1.shape[0]
+    gp, lo, hi = _guard(guard)
+    _check("moe_savb_gate_if", load().moe_savb_gate_if(
+        _p(text_rows), _dt(text_rows), n, d, _f32(w1), _f32(b1), hid, _f32(w2), _f32(b2), float(theta),
+        _f32(feature), _f32(p_exit), _i32(exit_flag), _p(ws), _nbytes(ws), gp, lo, hi, _i32(exit_layer),
+        int(layer), _stream(stream)))

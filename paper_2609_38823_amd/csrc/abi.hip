@@ -50,6 +50,8 @@ bool aligned_all(std::initializer_list<const void*> ps) {
   return true;
 }
 int elt_size(moe_dtype dt) { return dt == MOE_BF16 ? 2 : 4; }
+// the predicate of the *_if entry points: a device int32 (4-byte aligned) or NULL
+bool guard_ok(const int32_t* guard) { return (reinterpret_cast<uintptr_t>(guard) & 3u) == 0; }
 bool valid_dtype(moe_dtype dt) { return dt == MOE_F32 || dt == MOE_BF16; }
 int hip_status(hipError_t e) { return e == hipSuccess ? MOE_OK : MOE_EHIP; }
 size_t a256(size_t b) { return (b + 255) & ~size_t(255); }
@@ -116,13 +118,15 @@ size_t moe_workspace_size(int T, int E, int k, int d, int m, int n_seg) {
   return w;
 }
 
+}  // extern "C"
+
 namespace {
 // shared by moe_route (float32 router weights) and moe_route_packed
 // (three-term bf16 split of them, from moe_pack_router)
 int route(const void* x, moe_dtype dtype, const float* w_r, const void* w_r_packed,
           const float* bias, int T, int d, int E, int k, const int32_t* seg_offsets, int n_seg,
           const int32_t* K_dev, float* logits, int32_t* topk_idx, float* topk_w, void* ws,
-          size_t ws_bytes, hipStream_t stream) {
+          size_t ws_bytes, hipStream_t stream, decomoe::Guard g = decomoe::Guard{}) {
   if (T < 0 || E < 1 || E > kMaxE || k < 1 || k > E) return MOE_EINVAL;
   if (k > kMaxK) return MOE_EUNSUPPORTED;
   if (!seg_offsets) n_seg = 1;
@@ -154,9 +158,24 @@ int route(const void* x, moe_dtype dtype, const float* w_r, const void* w_r_pack
   }
   return hip_status(decomoe::launch_route(x, dtype == MOE_BF16, w_r, x ? w_r_packed : nullptr, bias,
                                           T, d, E, k, seg_offsets, n_seg, K_dev, logits, topk_idx,
-                                          topk_w, ws, stream));
+                                          topk_w, ws, stream, g));
+}
+
+int route_packed(const void* x, moe_dtype dtype, const void* w_r_packed, const float* bias, int T,
+                 int d, int E, int k, const int32_t* seg_offsets, int n_seg, const int32_t* K_dev,
+                 float* logits, int32_t* topk_idx, float* topk_w, void* ws, size_t ws_bytes,
+                 hipStream_t stream, decomoe::Guard g) {
+  if (!x || !w_r_packed) return MOE_EINVAL;
+  if (!valid_dtype(dtype)) return MOE_EINVAL;
+  if (dtype != MOE_BF16) return MOE_EUNSUPPORTED;
+  if (E < 1 || d < 1) return MOE_EINVAL;
+  if (!router_packable(d, E)) return MOE_EUNSUPPORTED;
+  return route(x, dtype, nullptr, w_r_packed, bias, T, d, E, k, seg_offsets, n_seg, K_dev, logits,
+               topk_idx, topk_w, ws, ws_bytes, stream, g);
 }
 }  // namespace
+
+extern "C" {
 
 int moe_route(const void* x, moe_dtype dtype, const float* w_r, const float* bias, int T, int d,
               int E, int k, const int32_t* seg_offsets, int n_seg, const int32_t* K_dev,
@@ -171,13 +190,18 @@ int moe_route_packed(const void* x, moe_dtype dtype, const void* w_r_packed, con
                      int T, int d, int E, int k, const int32_t* seg_offsets, int n_seg,
                      const int32_t* K_dev, float* logits, int32_t* topk_idx, float* topk_w,
                      void* ws, size_t ws_bytes, hipStream_t stream) {
-  if (!x || !w_r_packed) return MOE_EINVAL;
-  if (!valid_dtype(dtype)) return MOE_EINVAL;
-  if (dtype != MOE_BF16) return MOE_EUNSUPPORTED;
-  if (E < 1 || d < 1) return MOE_EINVAL;
-  if (!router_packable(d, E)) return MOE_EUNSUPPORTED;
-  return route(x, dtype, nullptr, w_r_packed, bias, T, d, E, k, seg_offsets, n_seg, K_dev, logits,
-               topk_idx, topk_w, ws, ws_bytes, stream);
+  return route_packed(x, dtype, w_r_packed, bias, T, d, E, k, seg_offsets, n_seg, K_dev, logits,
+                      topk_idx, topk_w, ws, ws_bytes, stream, decomoe::Guard{});
+}
+
+int moe_route_packed_if(const void* x, moe_dtype dtype, const void* w_r_packed, const float* bias,
+                        int T, int d, int E, int k, const int32_t* seg_offsets, int n_seg,
+                        const int32_t* K_dev, float* logits, int32_t* topk_idx, float* topk_w,
+                        void* ws, size_t ws_bytes, const int32_t* guard, int guard_lo, int guard_hi,
+                        hipStream_t stream) {
+  if (!guard_ok(guard)) return MOE_EINVAL;
+  return route_packed(x, dtype, w_r_packed, bias, T, d, E, k, seg_offsets, n_seg, K_dev, logits,
+                      topk_idx, topk_w, ws, ws_bytes, stream, decomoe::Guard{guard, guard_lo, guard_hi});
 }
 
 int moe_pack_router(const float* w_r, int d, int E, void* w_r_packed, hipStream_t stream) {
@@ -214,12 +238,13 @@ int moe_calibrate_prefix(const int32_t* topk_idx, const float* topk_w, int T, in
                                               mass, K_out, order, ws, stream));
 }
 
-int moe_calibrate_route_prefix(const float* logits, const int32_t* topk_idx_full,
-                               const float* topk_w_full, int T, int E, int k, double p, double* mass,
-                               int32_t* K_out, int32_t* topk_idx, float* topk_w, void* ws,
-                               size_t ws_bytes, hipStream_t stream) {
-  (void)ws;
-  (void)ws_bytes;
+}  // extern "C"
+
+namespace {
+int calibrate_route_prefix(const float* logits, const int32_t* topk_idx_full,
+                           const float* topk_w_full, int T, int E, int k, double p, double* mass,
+                           int32_t* K_out, int32_t* topk_idx, float* topk_w, hipStream_t stream,
+                           decomoe::Guard g) {
   if (T < 0 || E < 1 || E > kMaxE || k < 1 || k > E) return MOE_EINVAL;
   if (k > kMaxK) return MOE_EUNSUPPORTED;
   if (!(p > 0.0 && p <= 1.0)) return MOE_EINVAL;
@@ -234,13 +259,40 @@ int moe_calibrate_route_prefix(const float* logits, const int32_t* topk_idx_full
   Range o_w = T ? rng(topk_w, nk) : Range{0, 0};
   if (any_alias({rng(mass, (size_t)E * 8), rng(K_out, 4), o_i, o_w}, {in_l, in_i, in_w})) return MOE_EALIAS;
   return hip_status(decomoe::launch_calibrate_route(logits, topk_idx_full, topk_w_full, T, E, k, p, mass,
-                                                    K_out, topk_idx, topk_w, stream));
+                                                    K_out, topk_idx, topk_w, stream, g));
+}
+}  // namespace
+
+extern "C" {
+
+int moe_calibrate_route_prefix(const float* logits, const int32_t* topk_idx_full,
+                               const float* topk_w_full, int T, int E, int k, double p, double* mass,
+                               int32_t* K_out, int32_t* topk_idx, float* topk_w, void* ws,
+                               size_t ws_bytes, hipStream_t stream) {
+  (void)ws;
+  (void)ws_bytes;
+  return calibrate_route_prefix(logits, topk_idx_full, topk_w_full, T, E, k, p, mass, K_out, topk_idx,
+                                topk_w, stream, decomoe::Guard{});
 }
 
-int moe_dispatch(const int32_t* topk_idx, int T, int k, int E, const void* x, moe_dtype dtype,
-                 int d, int32_t* counts, int32_t* offsets, int32_t* src_of_row,
-                 int32_t* row_of_slot, void* x_perm, void* ws, size_t ws_bytes,
-                 hipStream_t stream) {
+int moe_calibrate_route_prefix_if(const float* logits, const int32_t* topk_idx_full,
+                                  const float* topk_w_full, int T, int E, int k, double p,
+                                  double* mass, int32_t* K_out, int32_t* topk_idx, float* topk_w,
+                                  void* ws, size_t ws_bytes, const int32_t* guard, int guard_lo,
+                                  int guard_hi, hipStream_t stream) {
+  (void)ws;
+  (void)ws_bytes;
+  if (!guard_ok(guard)) return MOE_EINVAL;
+  return calibrate_route_prefix(logits, topk_idx_full, topk_w_full, T, E, k, p, mass, K_out, topk_idx,
+                                topk_w, stream, decomoe::Guard{guard, guard_lo, guard_hi});
+}
+
+}  // extern "C"
+
+namespace {
+int dispatch(const int32_t* topk_idx, int T, int k, int E, const void* x, moe_dtype dtype, int d,
+             int32_t* counts, int32_t* offsets, int32_t* src_of_row, int32_t* row_of_slot,
+             void* x_perm, void* ws, size_t ws_bytes, hipStream_t stream, decomoe::Guard g) {
   if (T < 0 || E < 1 || E > kMaxE || k < 1 || k > E) return MOE_EINVAL;
   if ((size_t)T * k > (size_t)INT32_MAX) return MOE_EUNSUPPORTED;
   if (!counts || !offsets) return MOE_EINVAL;
@@ -260,7 +312,27 @@ int moe_dispatch(const int32_t* topk_idx, int T, int k, int E, const void* x, mo
                 {in_i, in_x}))
     return MOE_EALIAS;
   return hip_status(decomoe::launch_dispatch(topk_idx, T, k, E, x, elt_size(dtype), d, counts,
-                                             offsets, src_of_row, row_of_slot, x_perm, ws, stream));
+                                             offsets, src_of_row, row_of_slot, x_perm, ws, stream, g));
+}
+}  // namespace
+
+extern "C" {
+
+int moe_dispatch(const int32_t* topk_idx, int T, int k, int E, const void* x, moe_dtype dtype,
+                 int d, int32_t* counts, int32_t* offsets, int32_t* src_of_row,
+                 int32_t* row_of_slot, void* x_perm, void* ws, size_t ws_bytes,
+                 hipStream_t stream) {
+  return dispatch(topk_idx, T, k, E, x, dtype, d, counts, offsets, src_of_row, row_of_slot, x_perm, ws,
+                  ws_bytes, stream, decomoe::Guard{});
+}
+
+int moe_dispatch_if(const int32_t* topk_idx, int T, int k, int E, const void* x, moe_dtype dtype,
+                    int d, int32_t* counts, int32_t* offsets, int32_t* src_of_row,
+                    int32_t* row_of_slot, void* x_perm, void* ws, size_t ws_bytes,
+                    const int32_t* guard, int guard_lo, int guard_hi, hipStream_t stream) {
+  if (!guard_ok(guard)) return MOE_EINVAL;
+  return dispatch(topk_idx, T, k, E, x, dtype, d, counts, offsets, src_of_row, row_of_slot, x_perm, ws,
+                  ws_bytes, stream, decomoe::Guard{guard, guard_lo, guard_hi});
 }
 
 int moe_expert_ffn(const void* x_perm, moe_dtype dtype, const int32_t* offsets, int E,
@@ -313,7 +385,7 @@ int gather_ffn_args(const void* x, moe_dtype dtype, int T, int k, const int32_t*
 int gather_ffn_launch(const void* x, int T, int k, const int32_t* src_of_row, const int32_t* offsets,
                       int E, const int32_t* K_dev, int n_K, int d, int m, const void* w_gate_up_packed,
                       const void* w_down_packed, void* y_perm, void* ws, size_t need,
-                      hipStream_t stream) {
+                      hipStream_t stream, decomoe::Guard g = decomoe::Guard{}) {
   const int rows_max = T * k;
   Range o_y = rng(y_perm, (size_t)rows_max * d * 2);
   Range o_ws = rng(ws, need);
@@ -326,7 +398,7 @@ int gather_ffn_launch(const void* x, int T, int k, const int32_t* src_of_row, co
     return MOE_EALIAS;
   return hip_status(decomoe::launch_expert_ffn(x, true, offsets, E, K_dev, n_K, rows_max, d, m,
                                                w_gate_up_packed, w_down_packed, true, y_perm, ws,
-                                               stream, decomoe::RowGather{src_of_row, k, T}, k));
+                                               stream, decomoe::RowGather{src_of_row, k, T}, k, g));
 }
 }  // namespace
 
@@ -347,6 +419,26 @@ int moe_expert_ffn_packed_gather(const void* x, moe_dtype dtype, int T, int k,
   if (!ws || ws_bytes < need) return MOE_EWORKSPACE;
   return gather_ffn_launch(x, T, k, src_of_row, offsets, E, K_dev, n_K, d, m, w_gate_up_packed,
                            w_down_packed, y_perm, ws, need, stream);
+}
+
+int moe_expert_ffn_packed_gather_if(const void* x, moe_dtype dtype, int T, int k,
+                                    const int32_t* src_of_row, const int32_t* offsets, int E,
+                                    const int32_t* K_dev, int n_K, int d, int m,
+                                    const void* w_gate_up_packed, const void* w_down_packed,
+                                    void* y_perm, void* ws, size_t ws_bytes, const int32_t* guard,
+                                    int guard_lo, int guard_hi, hipStream_t stream) {
+  if (!guard_ok(guard)) return MOE_EINVAL;
+  int rows_max = 0;
+  const int st = gather_ffn_args(x, dtype, T, k, src_of_row, offsets, E, K_dev, n_K, d, m,
+                                 w_gate_up_packed, w_down_packed, y_perm, &rows_max);
+  if (st != MOE_OK) return st;
+  if (!aligned_all({ws})) return MOE_EINVAL;
+  if (rows_max == 0) return MOE_OK;
+  const size_t need = ffn_ws_bytes(true, rows_max, E, d, m);
+  if (!ws || ws_bytes < need) return MOE_EWORKSPACE;
+  return gather_ffn_launch(x, T, k, src_of_row, offsets, E, K_dev, n_K, d, m, w_gate_up_packed,
+                           w_down_packed, y_perm, ws, need, stream,
+                           decomoe::Guard{guard, guard_lo, guard_hi});
 }
 
 int moe_ffn_status(const void* ws, size_t ws_bytes, int32_t* status, hipStream_t stream) {
@@ -385,9 +477,12 @@ int moe_combine(const void* y_perm, moe_dtype dtype, const int32_t* row_of_slot,
                                             d, nullptr, out, stream));
 }
 
-int moe_combine_residual(const void* y_perm, moe_dtype dtype, const int32_t* row_of_slot,
-                         const float* topk_w, int T, int k, int d, const void* residual,
-                         void* out, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+int combine_residual(const void* y_perm, moe_dtype dtype, const int32_t* row_of_slot,
+                     const float* topk_w, int T, int k, int d, const void* residual, void* out,
+                     hipStream_t stream, decomoe::Guard g) {
   if (!valid_dtype(dtype) || T < 0 || k < 1 || k > kMaxE || d < 1) return MOE_EINVAL;
   if ((size_t)T * k > (size_t)INT32_MAX) return MOE_EUNSUPPORTED;
   if (T == 0) return MOE_OK;
@@ -401,7 +496,26 @@ int moe_combine_residual(const void* y_perm, moe_dtype dtype, const int32_t* row
   if (any_alias({o}, {rng(y_perm, A * d * es), rng(row_of_slot, A * 4), rng(topk_w, A * 4)}))
     return MOE_EALIAS;
   return hip_status(decomoe::launch_combine(y_perm, dtype == MOE_BF16, row_of_slot, topk_w, T, k,
-                                            d, residual, out, stream));
+                                            d, residual, out, stream, g));
+}
+}  // namespace
+
+extern "C" {
+
+int moe_combine_residual(const void* y_perm, moe_dtype dtype, const int32_t* row_of_slot,
+                         const float* topk_w, int T, int k, int d, const void* residual,
+                         void* out, hipStream_t stream) {
+  return combine_residual(y_perm, dtype, row_of_slot, topk_w, T, k, d, residual, out, stream,
+                          decomoe::Guard{});
+}
+
+int moe_combine_residual_if(const void* y_perm, moe_dtype dtype, const int32_t* row_of_slot,
+                            const float* topk_w, int T, int k, int d, const void* residual,
+                            void* out, const int32_t* guard, int guard_lo, int guard_hi,
+                            hipStream_t stream) {
+  if (!guard_ok(guard)) return MOE_EINVAL;
+  return combine_residual(y_perm, dtype, row_of_slot, topk_w, T, k, d, residual, out, stream,
+                          decomoe::Guard{guard, guard_lo, guard_hi});
 }
 
 int moe_permute_experts(const int32_t* order, int E, int d, int m, moe_dtype dtype,
@@ -461,10 +575,13 @@ size_t moe_savb_workspace_size(int n, int d, int hid) {
   return a256(decomoe::savb_ws_bytes(n, d, hid));
 }
 
-int moe_savb_gate(const void* text_rows, moe_dtype dtype, int n, int d, const float* w1,
-                  const float* b1, int hid, const float* w2, const float* b2, double theta,
-                  float* feature, float* p_exit, int32_t* exit_flag, void* ws, size_t ws_bytes,
-                  hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+int savb_gate(const void* text_rows, moe_dtype dtype, int n, int d, const float* w1, const float* b1,
+              int hid, const float* w2, const float* b2, double theta, float* feature, float* p_exit,
+              int32_t* exit_flag, void* ws, size_t ws_bytes, hipStream_t stream, decomoe::Guard g,
+              int32_t* exit_layer, int layer) {
   if (!valid_dtype(dtype) || n < 1 || d < 1 || d > 8192 || hid < 1) return MOE_EINVAL;
   if (!(theta == theta)) return MOE_EINVAL;  // NaN
   if (!text_rows || !w1 || !w2 || !p_exit || !exit_flag || !ws) return MOE_EINVAL;
@@ -477,8 +594,33 @@ int moe_savb_gate(const void* text_rows, moe_dtype dtype, int n, int d, const fl
                  b1 ? rng(b1, (size_t)hid * 4) : Range{0, 0}, rng(w2, (size_t)2 * hid * 4),
                  b2 ? rng(b2, 8) : Range{0, 0}}))
     return MOE_EALIAS;
+  if (exit_layer && (overlap(rng(exit_layer, 4), rng(exit_flag, 4)) ||
+                     overlap(rng(exit_layer, 4), rng(p_exit, 4))))
+    return MOE_EALIAS;
   return hip_status(decomoe::launch_savb_gate(text_rows, dtype == MOE_BF16, n, d, w1, b1, hid, w2, b2,
-                                              theta, feature, p_exit, exit_flag, ws, stream));
+                                              theta, feature, p_exit, exit_flag, ws, stream, g,
+                                              exit_layer, layer));
+}
+}  // namespace
+
+extern "C" {
+
+int moe_savb_gate(const void* text_rows, moe_dtype dtype, int n, int d, const float* w1,
+                  const float* b1, int hid, const float* w2, const float* b2, double theta,
+                  float* feature, float* p_exit, int32_t* exit_flag, void* ws, size_t ws_bytes,
+                  hipStream_t stream) {
+  return savb_gate(text_rows, dtype, n, d, w1, b1, hid, w2, b2, theta, feature, p_exit, exit_flag, ws,
+                   ws_bytes, stream, decomoe::Guard{}, nullptr, 0);
+}
+
+int moe_savb_gate_if(const void* text_rows, moe_dtype dtype, int n, int d, const float* w1,
+                     const float* b1, int hid, const float* w2, const float* b2, double theta,
+                     float* feature, float* p_exit, int32_t* exit_flag, void* ws, size_t ws_bytes,
+                     const int32_t* guard, int guard_lo, int guard_hi, int32_t* exit_layer,
+                     int layer, hipStream_t stream) {
+  if (!guard_ok(guard) || !guard_ok(exit_layer)) return MOE_EINVAL;
+  return savb_gate(text_rows, dtype, n, d, w1, b1, hid, w2, b2, theta, feature, p_exit, exit_flag, ws,
+                   ws_bytes, stream, decomoe::Guard{guard, guard_lo, guard_hi}, exit_layer, layer);
 }
 
 int drop_visual_block_if(const void* h, moe_dtype dtype, int S, int d, int v0, int v1,

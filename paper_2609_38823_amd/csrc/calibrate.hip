@@ -14,7 +14,8 @@ namespace {
 __global__ __launch_bounds__(CAL_THREADS) void segment_mass_kernel(
     const int32_t* __restrict__ idx, const float* __restrict__ w, int T, int E, int k, int key_bits,
     const int32_t* __restrict__ seg_offsets, double p, double* __restrict__ mass,
-    int32_t* __restrict__ K_out) {
+    int32_t* __restrict__ K_out, const Guard g) {
+  if (guard_skip(g)) return;
   __shared__ CalLds L;
   const int seg = blockIdx.x;
   const int tid = threadIdx.x;
@@ -39,7 +40,8 @@ __global__ __launch_bounds__(CAL_THREADS) void segment_mass_kernel(
 // order = argsort descending, ties to the lower expert index.
 __global__ __launch_bounds__(1024) void mean_mass_order_kernel(
     const double* __restrict__ mass, int T, int E, const int32_t* __restrict__ seg_offsets,
-    int n_seg, int32_t* __restrict__ order) {
+    int n_seg, int32_t* __restrict__ order, const Guard g) {
+  if (guard_skip(g)) return;
   __shared__ double mean[1024];
   const int e = threadIdx.x;
   if (e < E) {
@@ -79,15 +81,15 @@ size_t calibrate_ws_bytes(int T, int E) {
 
 hipError_t launch_calibrate(const int32_t* idx, const float* w, int T, int E, int k,
                             const int32_t* seg_offsets, int n_seg, double p, double* mass,
-                            int32_t* K_out, int32_t* order, void* ws, hipStream_t s) {
+                            int32_t* K_out, int32_t* order, void* ws, hipStream_t s, Guard g) {
   (void)ws;
   int key_bits = 0;
   while ((1 << key_bits) < E) ++key_bits;
   segment_mass_kernel<<<n_seg, CAL_THREADS, 0, s>>>(idx, w, T, E, k, key_bits, seg_offsets, p, mass,
-                                                    K_out);
+                                                    K_out, g);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess || !order) return err;
-  mean_mass_order_kernel<<<1, 1024, 0, s>>>(mass, T, E, seg_offsets, n_seg, order);
+  mean_mass_order_kernel<<<1, 1024, 0, s>>>(mass, T, E, seg_offsets, n_seg, order, g);
   return hipGetLastError();
 }
 

@@ -5,18 +5,40 @@
 namespace decomoe {
 namespace {
 
+// 16-byte load with the non-temporal hint: every expert output row is read
+// once, so it should not displace reused lines from the caches (measured at
+// 65 536 rows x top-8, d 2048: 5.1 -> 5.8 TB/s)
+typedef unsigned int u32x4_nt __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 load_stream(const uint4* p) {
+  const u32x4_nt q = __builtin_nontemporal_load(reinterpret_cast<const u32x4_nt*>(p));
+  return make_uint4(q.x, q.y, q.z, q.w);
+}
+// 16-byte store, non-temporal when NT (outputs larger than the memory-side
+// cache: their dirty lines would otherwise have to be written back before
+// the next kernel's reads can use that cache)
+template <bool NT>
+__device__ __forceinline__ void store_out(uint4* p, uint4 v) {
+  if constexpr (NT) {
+    const u32x4_nt q = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(q, reinterpret_cast<u32x4_nt*>(p));
+  } else {
+    *p = v;
+  }
+}
+
 // out[t] = sum_j w[t, j] * y[row_of_slot[t*k + j]], float32 accumulation in
 // slot order; with RES the residual row is added to the float32 sum before
 // the one rounding (res may be out itself: each thread reads its vector of
 // res before it writes the same vector of out).  Each thread owns one 16-byte
 // vector of the row (8 bf16 or 4 f32); a block covers one token row, or
 // several when rows are short.
-template <bool BF16, bool RES>
+template <bool BF16, bool RES, bool NTST>
 __global__ __launch_bounds__(256) void combine_kernel(const uint4* __restrict__ y,
                                                       const int32_t* __restrict__ row_of_slot,
                                                       const float* __restrict__ w, int T, int k,
                                                       int chunks, int rpb, const uint4* res,
-                                                      uint4* out) {
+                                                      uint4* out, const Guard g) {
+  if (guard_skip(g)) return;
   int t, c0, cstep;
   if (chunks >= 256) {
     t = blockIdx.x;
@@ -45,7 +67,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const uint4* __restrict__ 
         const int r = j < k ? row_of_slot[(size_t)t * k + j] : -1;
         ok[u] = r >= 0 && r < A;
         wj[u] = j < k ? w[(size_t)t * k + j] : 0.f;
-        v[u] = y[(size_t)(ok[u] ? r : 0) * chunks + c];
+        v[u] = load_stream(y + (size_t)(ok[u] ? r : 0) * chunks + c);
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
@@ -89,7 +111,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const uint4* __restrict__ 
       o = make_uint4(__float_as_uint(acc[0]), __float_as_uint(acc[1]), __float_as_uint(acc[2]),
                      __float_as_uint(acc[3]));
     }
-    out[(size_t)t * chunks + c] = o;
+    store_out<NTST>(out + (size_t)t * chunks + c, o);
   }
 }
 
@@ -99,7 +121,8 @@ __global__ __launch_bounds__(256) void combine_scalar_kernel(const void* __restr
                                                              const int32_t* __restrict__ row_of_slot,
                                                              const float* __restrict__ w, int T,
                                                              int k, int d, const void* resv,
-                                                             void* outv) {
+                                                             void* outv, const Guard g) {
+  if (guard_skip(g)) return;
   const size_t n = (size_t)T * d;
   const int A = T * k;
   for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) {
@@ -150,7 +173,7 @@ namespace {
 template <bool RES>
 hipError_t combine_launch(const void* y_perm, bool bf16, const int32_t* row_of_slot,
                           const float* w, int T, int k, int d, const void* res, void* out,
-                          hipStream_t s) {
+                          hipStream_t s, Guard g) {
   const size_t row_bytes = (size_t)d * (bf16 ? 2 : 4);
   if (row_bytes % 16 == 0) {
     const int chunks = (int)(row_bytes / 16);
@@ -159,19 +182,25 @@ hipError_t combine_launch(const void* y_perm, bool bf16, const int32_t* row_of_s
     auto y = static_cast<const uint4*>(y_perm);
     auto r = static_cast<const uint4*>(res);
     auto o = static_cast<uint4*>(out);
-    if (bf16)
-      combine_kernel<true, RES><<<grid, 256, 0, s>>>(y, row_of_slot, w, T, k, chunks, rpb, r, o);
+    // outputs beyond 64 MiB are written past the caches (see store_out)
+    const bool nt = (size_t)T * row_bytes > ((size_t)64 << 20);
+    if (bf16 && nt)
+      combine_kernel<true, RES, true><<<grid, 256, 0, s>>>(y, row_of_slot, w, T, k, chunks, rpb, r, o, g);
+    else if (bf16)
+      combine_kernel<true, RES, false><<<grid, 256, 0, s>>>(y, row_of_slot, w, T, k, chunks, rpb, r, o, g);
+    else if (nt)
+      combine_kernel<false, RES, true><<<grid, 256, 0, s>>>(y, row_of_slot, w, T, k, chunks, rpb, r, o, g);
     else
-      combine_kernel<false, RES><<<grid, 256, 0, s>>>(y, row_of_slot, w, T, k, chunks, rpb, r, o);
+      combine_kernel<false, RES, false><<<grid, 256, 0, s>>>(y, row_of_slot, w, T, k, chunks, rpb, r, o, g);
   } else {
     size_t blocks = ((size_t)T * d + 255) / 256;
     if (blocks > 65536) blocks = 65536;
     if (bf16)
       combine_scalar_kernel<true, RES><<<(unsigned)blocks, 256, 0, s>>>(y_perm, row_of_slot, w, T,
-                                                                        k, d, res, out);
+                                                                        k, d, res, out, g);
     else
       combine_scalar_kernel<false, RES><<<(unsigned)blocks, 256, 0, s>>>(y_perm, row_of_slot, w,
-                                                                         T, k, d, res, out);
+                                                                         T, k, d, res, out, g);
   }
   return hipGetLastError();
 }
@@ -179,10 +208,10 @@ hipError_t combine_launch(const void* y_perm, bool bf16, const int32_t* row_of_s
 
 hipError_t launch_combine(const void* y_perm, bool bf16, const int32_t* row_of_slot,
                           const float* w, int T, int k, int d, const void* residual, void* out,
-                          hipStream_t s) {
+                          hipStream_t s, Guard g) {
   if (residual)
-    return combine_launch<true>(y_perm, bf16, row_of_slot, w, T, k, d, residual, out, s);
-  return combine_launch<false>(y_perm, bf16, row_of_slot, w, T, k, d, nullptr, out, s);
+    return combine_launch<true>(y_perm, bf16, row_of_slot, w, T, k, d, residual, out, s, g);
+  return combine_launch<false>(y_perm, bf16, row_of_slot, w, T, k, d, nullptr, out, s, g);
 }
 
 hipError_t launch_drop_rows(const void* h, int elt, int S, int d, int v0, int v1, void* out,

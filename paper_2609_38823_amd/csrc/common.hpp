@@ -35,6 +35,21 @@ __device__ __forceinline__ int find_segment(const int32_t* seg_offsets, int n_se
   return lo;
 }
 
+// ---- launch predicate ----------------------------------------------------
+// A launch runs only when *flag lies in [lo, hi) at the time its kernels
+// execute (read on the device: a predicate that a captured graph keeps); a
+// NULL flag always runs.  A skipped kernel returns at once and writes
+// nothing.
+struct Guard {
+  const int32_t* flag = nullptr;
+  int lo = 0, hi = 0;
+};
+__device__ __forceinline__ bool guard_skip(const Guard& g) {
+  if (!g.flag) return false;
+  const int v = *g.flag;
+  return v < g.lo || v >= g.hi;
+}
+
 // ---- launchers (host side; return hipError_t of the launch) -------------
 size_t route_ws_bytes(int T, int d, int E);
 // logits (x != NULL; from w_r_packed when given, else w_r) and Top-k in one
@@ -42,27 +57,29 @@ size_t route_ws_bytes(int T, int d, int E);
 hipError_t launch_route(const void* x, bool x_bf16, const float* w_r, const void* w_r_packed,
                         const float* bias, int T, int d, int E, int k, const int32_t* seg_offsets,
                         int n_seg, const int32_t* K_dev, float* logits, int32_t* idx, float* w,
-                        void* ws, hipStream_t s);
+                        void* ws, hipStream_t s, Guard g = Guard{});
 // bf16 x (three-term split router weights): packing and the logits kernel;
 // `part`/`S` receive the split partials the Top-k kernel has to add
 size_t route_x3_ws_bytes(int T, int d, int E);
 hipError_t launch_pack_router(const float* w_r, int d, int E, void* out, hipStream_t s);
 hipError_t launch_router_x3(const void* x, const void* w_packed, const float* bias, int T, int d,
-                            int E, float* logits, void* ws, float*& part, int& S, hipStream_t s);
+                            int E, float* logits, void* ws, float*& part, int& S, hipStream_t s,
+                            Guard g = Guard{});
 size_t calibrate_ws_bytes(int T, int E);
 hipError_t launch_calibrate(const int32_t* idx, const float* w, int T, int E, int k,
                             const int32_t* seg_offsets, int n_seg, double p, double* mass,
-                            int32_t* K_out, int32_t* order, void* ws, hipStream_t s);
+                            int32_t* K_out, int32_t* order, void* ws, hipStream_t s, Guard g = Guard{});
 // calibration (one segment) and prefix re-route in one launch when
 // calibrate_route_fused(T, E, k), else the two launches
 bool calibrate_route_fused(int T, int E, int k);
 hipError_t launch_calibrate_route(const float* logits, const int32_t* idx_full, const float* w_full,
                                   int T, int E, int k, double p, double* mass, int32_t* K_out,
-                                  int32_t* idx, float* w, hipStream_t s);
+                                  int32_t* idx, float* w, hipStream_t s, Guard g = Guard{});
 size_t dispatch_ws_bytes(int T, int k, int E);
 hipError_t launch_dispatch(const int32_t* idx, int T, int k, int E, const void* x, int elt, int d,
                            int32_t* counts, int32_t* offsets, int32_t* src_of_row,
-                           int32_t* row_of_slot, void* x_perm, void* ws, hipStream_t s);
+                           int32_t* row_of_slot, void* x_perm, void* ws, hipStream_t s,
+                           Guard g = Guard{});
 hipError_t launch_expand_dense(const int32_t* idx, const float* w, int T, int k, int E,
                                const int32_t* K_dev, int32_t* idx_dense, float* w_dense, hipStream_t s);
 size_t ffn_ws_bytes(bool bf16, int rows_max, int E, int d, int m);
@@ -81,7 +98,7 @@ hipError_t launch_expert_ffn(const void* a_rows, bool bf16, const int32_t* offse
                              const int32_t* K_dev, int n_K, int rows_max, int d, int m,
                              const void* w_gate_up, const void* w_down, bool packed, void* y_perm,
                              void* ws, hipStream_t s, RowGather gather = RowGather{nullptr, 1, 0},
-                             int kmin = 1);
+                             int kmin = 1, Guard g = Guard{});
 // launch path recorded in the expert FFN's counter header
 constexpr int FFN_PATH_PERSISTENT = 1;  // both GEMMs in one persistent launch
 constexpr int FFN_PATH_TWO_LAUNCH = 2;  // packed weights, one launch per GEMM
@@ -92,7 +109,7 @@ hipError_t launch_ffn_status(const void* ws, int32_t* status, hipStream_t s);
 hipError_t launch_pack_weights(const void* w, int E, int R, int K, void* out, hipStream_t s);
 hipError_t launch_combine(const void* y_perm, bool bf16, const int32_t* row_of_slot,
                           const float* w, int T, int k, int d, const void* residual, void* out,
-                          hipStream_t s);
+                          hipStream_t s, Guard g = Guard{});
 // out block j = in block order[j] for E blocks of `block_bytes` (zeros when
 // order[j] lies outside [0, E))
 hipError_t launch_permute_blocks(const void* in, const int32_t* order, int E, size_t block_bytes,
@@ -107,7 +124,8 @@ size_t savb_ws_bytes(int n, int d, int hid);
 hipError_t launch_savb_gate(const void* rows, bool bf16, int n, int d, const float* w1,
                             const float* b1, int hid, const float* w2, const float* b2, double theta,
                             float* feature, float* p_exit, int32_t* exit_flag, void* ws,
-                            hipStream_t s);
+                            hipStream_t s, Guard g = Guard{}, int32_t* exit_layer = nullptr,
+                            int layer = 0);
 hipError_t launch_drop_rows_if(const void* h, int elt, int S, int d, int v0, int v1,
                                const int32_t* flag, void* out, hipStream_t s);
 

@@ -25,7 +25,8 @@ constexpr int DP_PER_WAVE = DP_CHUNK / (DP_THREADS / kWave);
 
 __global__ __launch_bounds__(DP_THREADS) void dispatch_hist_kernel(const int32_t* __restrict__ idx,
                                                                    int A, int E,
-                                                                   int32_t* __restrict__ hist) {
+                                                                   int32_t* __restrict__ hist, const Guard g) {
+  if (guard_skip(g)) return;
   __shared__ int h[1024];
   for (int e = threadIdx.x; e < E; e += DP_THREADS) h[e] = 0;
   __syncthreads();
@@ -52,7 +53,8 @@ __global__ __launch_bounds__(1024) void dispatch_scan_kernel(const int32_t* __re
                                                              int n_chunks, int E,
                                                              int32_t* __restrict__ base,
                                                              int32_t* __restrict__ counts,
-                                                             int32_t* __restrict__ offsets) {
+                                                             int32_t* __restrict__ offsets, const Guard g) {
+  if (guard_skip(g)) return;
   __shared__ int s_cnt[1024];          // [p][e] partial sums, then prefixes over p
   __shared__ int s_off[1024];          // [e] exclusive offsets
   __shared__ int part[1024 / kWave];
@@ -162,7 +164,8 @@ constexpr int DP_FUSE_CHUNKS = 64;  // scan folded into the ranks up to this man
 __global__ __launch_bounds__(DP_THREADS) void dispatch_scan_rank_kernel(
     const int32_t* __restrict__ idx, int A, int E, int key_bits, const int32_t* __restrict__ hist,
     int n_chunks, int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
-    int32_t* __restrict__ src_of_row, int32_t* __restrict__ row_of_slot) {
+    int32_t* __restrict__ src_of_row, int32_t* __restrict__ row_of_slot, const Guard g) {
+  if (guard_skip(g)) return;
   constexpr int NW = DP_THREADS / kWave;
   __shared__ int run[NW][1024];
   __shared__ int s_tot[1024], s_base[1024];
@@ -229,7 +232,8 @@ __global__ __launch_bounds__(DP_THREADS) void dispatch_scan_rank_kernel(
 
 __global__ __launch_bounds__(DP_THREADS) void dispatch_rank_kernel(
     const int32_t* __restrict__ idx, int A, int E, int key_bits, const int32_t* __restrict__ base,
-    int32_t* __restrict__ src_of_row, int32_t* __restrict__ row_of_slot) {
+    int32_t* __restrict__ src_of_row, int32_t* __restrict__ row_of_slot, const Guard g) {
+  if (guard_skip(g)) return;
   constexpr int NW = DP_THREADS / kWave;
   __shared__ int run[NW][1024];
   const int a_chunk = blockIdx.x * DP_CHUNK;
@@ -264,7 +268,8 @@ constexpr int DS_MAX = 8192;  // beyond this the multi-workgroup path is faster
 __global__ __launch_bounds__(DS_THREADS) void dispatch_sort_small_kernel(
     const int32_t* __restrict__ idx, int A, int E, int key_bits, int32_t* __restrict__ counts,
     int32_t* __restrict__ offsets, int32_t* __restrict__ src_of_row,
-    int32_t* __restrict__ row_of_slot) {
+    int32_t* __restrict__ row_of_slot, const Guard g) {
+  if (guard_skip(g)) return;
   __shared__ int wh[DS_WAVES][1024];  // per-wave counts, then per-wave starting rows
   __shared__ int part[DS_WAVES];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -336,7 +341,8 @@ template <typename VEC>
 __global__ __launch_bounds__(256) void dispatch_gather_kernel(const VEC* __restrict__ x, int T,
                                                               int k, int chunks, int rpb,
                                                               const int32_t* __restrict__ row_of_slot,
-                                                              VEC* __restrict__ x_perm) {
+                                                              VEC* __restrict__ x_perm, const Guard g) {
+  if (guard_skip(g)) return;
   const int A = T * k;
   int t, c0, cstep;
   if (chunks >= 256) {
@@ -390,7 +396,7 @@ size_t dispatch_ws_bytes(int T, int k, int E) {
 
 hipError_t launch_dispatch(const int32_t* idx, int T, int k, int E, const void* x, int elt, int d,
                            int32_t* counts, int32_t* offsets, int32_t* src_of_row,
-                           int32_t* row_of_slot, void* x_perm, void* ws, hipStream_t s) {
+                           int32_t* row_of_slot, void* x_perm, void* ws, hipStream_t s, Guard g) {
   const int A = T * k;
   const int n_chunks = (A + DP_CHUNK - 1) / DP_CHUNK;
   int32_t* hist = static_cast<int32_t*>(ws);
@@ -400,22 +406,22 @@ hipError_t launch_dispatch(const int32_t* idx, int T, int k, int E, const void* 
   hipError_t err;
   if (A <= DS_MAX) {
     dispatch_sort_small_kernel<<<1, DS_THREADS, 0, s>>>(idx, A, E, key_bits, counts, offsets,
-                                                        src_of_row, row_of_slot);
+                                                        src_of_row, row_of_slot, g);
     err = hipGetLastError();
     if (err != hipSuccess || A == 0) return err;
   } else {
-    dispatch_hist_kernel<<<n_chunks, DP_THREADS, 0, s>>>(idx, A, E, hist);
+    dispatch_hist_kernel<<<n_chunks, DP_THREADS, 0, s>>>(idx, A, E, hist, g);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
     if (n_chunks <= DP_FUSE_CHUNKS) {
       dispatch_scan_rank_kernel<<<n_chunks, DP_THREADS, 0, s>>>(idx, A, E, key_bits, hist, n_chunks, counts,
-                                                                 offsets, src_of_row, row_of_slot);
+                                                                 offsets, src_of_row, row_of_slot, g);
     } else {
-      dispatch_scan_kernel<<<1, 1024, 0, s>>>(hist, n_chunks, E, base, counts, offsets);
+      dispatch_scan_kernel<<<1, 1024, 0, s>>>(hist, n_chunks, E, base, counts, offsets, g);
       err = hipGetLastError();
       if (err != hipSuccess) return err;
       dispatch_rank_kernel<<<n_chunks, DP_THREADS, 0, s>>>(idx, A, E, key_bits, base, src_of_row,
-                                                            row_of_slot);
+                                                            row_of_slot, g);
     }
     err = hipGetLastError();
     if (err != hipSuccess) return err;
@@ -426,17 +432,17 @@ hipError_t launch_dispatch(const int32_t* idx, int T, int k, int E, const void* 
     int chunks = (int)(row_bytes / 16);
     int rpb = chunks >= 256 ? 1 : 256 / chunks;
     dispatch_gather_kernel<uint4><<<(T + rpb - 1) / rpb, 256, 0, s>>>(
-        static_cast<const uint4*>(x), T, k, chunks, rpb, row_of_slot, static_cast<uint4*>(x_perm));
+        static_cast<const uint4*>(x), T, k, chunks, rpb, row_of_slot, static_cast<uint4*>(x_perm), g);
   } else if (row_bytes % 4 == 0) {
     int chunks = (int)(row_bytes / 4);
     int rpb = chunks >= 256 ? 1 : 256 / chunks;
     dispatch_gather_kernel<uint32_t><<<(T + rpb - 1) / rpb, 256, 0, s>>>(
-        static_cast<const uint32_t*>(x), T, k, chunks, rpb, row_of_slot, static_cast<uint32_t*>(x_perm));
+        static_cast<const uint32_t*>(x), T, k, chunks, rpb, row_of_slot, static_cast<uint32_t*>(x_perm), g);
   } else {
     int chunks = (int)(row_bytes / 2);
     int rpb = chunks >= 256 ? 1 : 256 / chunks;
     dispatch_gather_kernel<uint16_t><<<(T + rpb - 1) / rpb, 256, 0, s>>>(
-        static_cast<const uint16_t*>(x), T, k, chunks, rpb, row_of_slot, static_cast<uint16_t*>(x_perm));
+        static_cast<const uint16_t*>(x), T, k, chunks, rpb, row_of_slot, static_cast<uint16_t*>(x_perm), g);
   }
   return hipGetLastError();
 }

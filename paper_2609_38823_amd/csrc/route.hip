@@ -33,7 +33,8 @@ __global__ __launch_bounds__(256) void router_logits_mfma_kernel(const void* __r
                                                                  const float* __restrict__ bias,
                                                                  int T, int d, int E,
                                                                  float* __restrict__ logits,
-                                                                 float* __restrict__ split_part) {
+                                                                 float* __restrict__ split_part, const Guard g) {
+  if (guard_skip(g)) return;
   __shared__ f32x4 part[4][4][64];  // [wave][n-frag][lane]
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int e0 = blockIdx.x * RM_E, t0 = blockIdx.y * RM_T;
@@ -121,7 +122,8 @@ __global__ __launch_bounds__(256) void router_logits_simt_kernel(const void* __r
                                                                  const float* __restrict__ w_r,
                                                                  const float* __restrict__ bias,
                                                                  int T, int d, int E,
-                                                                 float* __restrict__ logits) {
+                                                                 float* __restrict__ logits, const Guard g) {
+  if (guard_skip(g)) return;
   __shared__ float xs[RT_K][RT_T + 4];  // transposed: xs[k][token]
   __shared__ float wsm[RT_K][RT_E + 4];
   const int tid = threadIdx.x;
@@ -185,6 +187,7 @@ __global__ __launch_bounds__(256) void router_logits_simt_kernel(const void* __r
 // order.  Weights are the softmax of the k selected logits.
 // ---------------------------------------------------------------------------
 constexpr int TK_MAXC = 16;  // E <= 1024 = 16 values per lane (MAXC: per instantiation)
+constexpr int TK_SPLITS = 8;  // d-range splits whose loads are all issued together
 
 // With `part` (split-K router), the logits are first formed here as
 // (part[0] + part[1] + ... + part[S-1]) + b, written to `logits`, and used.
@@ -194,7 +197,8 @@ __global__ __launch_bounds__(256) void topk_kernel(float* __restrict__ logits, i
                                                    int n_seg, const int32_t* __restrict__ K_dev,
                                                    const float* __restrict__ part, int S,
                                                    const float* __restrict__ bias,
-                                                   int32_t* __restrict__ idx, float* __restrict__ w) {
+                                                   int32_t* __restrict__ idx, float* __restrict__ w, const Guard g) {
+  if (guard_skip(g)) return;
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;  // whole wavefront leaves together; no block barrier below
@@ -205,26 +209,53 @@ __global__ __launch_bounds__(256) void topk_kernel(float* __restrict__ logits, i
   }
   float* row = logits + (size_t)t * E;
   if (part) {
-    // the logits are selected from registers (no reload of the stored row)
+    // the logits are selected from registers (no reload of the stored row):
+    // (part[0] + part[1] + ... + part[S-1]) + b per expert
     float v[MAXC];
+    if (MAXC <= 2 && S <= TK_SPLITS) {
+      // every partial's load in flight before the first addition
+      float pv[TK_SPLITS][MAXC];
 #pragma unroll
-    for (int c = 0; c < MAXC; ++c) {
-      const int e = lane + c * 64;
-      v[c] = 0.f;
-      if (e < E) {
-        float a = part[(size_t)t * E + e];
+      for (int sp = 0; sp < TK_SPLITS; ++sp)
+#pragma unroll
+        for (int c = 0; c < MAXC; ++c) {
+          const int e = lane + c * 64;
+          pv[sp][c] = sp < S && e < E ? part[((size_t)sp * T + t) * E + e] : 0.f;
+        }
+#pragma unroll
+      for (int c = 0; c < MAXC; ++c) {
+        float a = pv[0][c];
+#pragma unroll
+        for (int sp = 1; sp < TK_SPLITS; ++sp)
+          if (sp < S) a += pv[sp][c];
+        v[c] = a;
+      }
+    } else {
+#pragma unroll
+      for (int c = 0; c < MAXC; ++c) {
+        const int e = lane + c * 64;
+        float a = e < E ? part[(size_t)t * E + e] : 0.f;
         // partials in order sp = 1..S-1; loads issued four at a time
         for (int sp = 1; sp < S; sp += 4) {
           float pv[4];
 #pragma unroll
           for (int u = 0; u < 4; ++u)
-            pv[u] = sp + u < S ? part[((size_t)(sp + u) * T + t) * E + e] : 0.f;
+            pv[u] = sp + u < S && e < E ? part[((size_t)(sp + u) * T + t) * E + e] : 0.f;
 #pragma unroll
           for (int u = 0; u < 4; ++u)
             if (sp + u < S) a += pv[u];
         }
-        v[c] = a + (bias ? bias[e] : 0.f);
+        v[c] = a;
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+      const int e = lane + c * 64;
+      if (e < E) {
+        v[c] += bias ? bias[e] : 0.f;
         row[e] = v[c];
+      } else {
+        v[c] = 0.f;
       }
     }
     topk_select_vals<MAXC>(v, E, k, Klim, lane, idx + (size_t)t * k, w + (size_t)t * k);
@@ -242,19 +273,6 @@ __global__ __launch_bounds__(256) void topk_kernel(float* __restrict__ logits, i
 // lane r % 16 in slot r / 16 (k <= 32).  Same selection order, tie rule and
 // weights as topk_kernel.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void row_best(float& v, int& i) {
-  dpp_better<0xB1>(v, i);   // quad_perm [1, 0, 3, 2]
-  dpp_better<0x4E>(v, i);   // quad_perm [2, 3, 0, 1]
-  dpp_better<0x141>(v, i);  // row_half_mirror
-  dpp_better<0x140>(v, i);  // row_mirror
-}
-__device__ __forceinline__ float row_sum(float v) {
-  v += dpp_f<0xB1>(v);
-  v += dpp_f<0x4E>(v);
-  v += dpp_f<0x141>(v);
-  v += dpp_f<0x140>(v);
-  return v;
-}
 
 template <int MAXC>
 __global__ __launch_bounds__(256) void topk_row_kernel(float* __restrict__ logits, int T, int E,
@@ -262,7 +280,8 @@ __global__ __launch_bounds__(256) void topk_row_kernel(float* __restrict__ logit
                                                        int n_seg, const int32_t* __restrict__ K_dev,
                                                        const float* __restrict__ part, int S,
                                                        const float* __restrict__ bias,
-                                                       int32_t* __restrict__ idx, float* __restrict__ w) {
+                                                       int32_t* __restrict__ idx, float* __restrict__ w, const Guard g) {
+  if (guard_skip(g)) return;
   const int j = threadIdx.x & 15;
   const int t = blockIdx.x * 16 + (threadIdx.x >> 4);
   if (t >= T) return;  // the whole row of 16 lanes leaves together
@@ -312,41 +331,7 @@ __global__ __launch_bounds__(256) void topk_row_kernel(float* __restrict__ logit
       v[c] = e < E ? row[e] : 0.f;
     }
   }
-  uint32_t alive = 0;
-#pragma unroll
-  for (int c = 0; c < MAXC; ++c)
-    if (j + 16 * c < Klim) alive |= 1u << c;
-  float my_v[2] = {0.f, 0.f};
-  int my_i[2] = {0, 0};
-  float v0 = 0.f;
-  for (int r = 0; r < k; ++r) {
-    float bv = -INFINITY;
-    int bi = 0x7fffffff;
-#pragma unroll
-    for (int c = 0; c < MAXC; ++c)
-      if (alive & (1u << c)) better(bv, bi, v[c], j + 16 * c);
-    row_best(bv, bi);
-    if (bi < E && (bi & 15) == j) alive &= ~(1u << (bi >> 4));
-    if (r == 0) v0 = bv;
-    if ((r & 15) == j) {
-      my_v[r >> 4] = bv;
-      my_i[r >> 4] = bi;
-    }
-  }
-  float ex[2];
-#pragma unroll
-  for (int q = 0; q < 2; ++q) ex[q] = j + 16 * q < k ? expf(my_v[q] - v0) : 0.f;
-  // slots in order r = 0..k-1: lanes hold r = j and r = j + 16; the row sum
-  // adds the k exponentials (the same total in every lane of the row)
-  const float sum = row_sum(ex[0] + ex[1]);
-#pragma unroll
-  for (int q = 0; q < 2; ++q) {
-    const int r = j + 16 * q;
-    if (r < k) {
-      idx[(size_t)t * k + r] = my_i[q];
-      w[(size_t)t * k + r] = ex[q] / sum;
-    }
-  }
+  row_topk_select<MAXC>(v, j, E, k, Klim, idx + (size_t)t * k, w + (size_t)t * k);
 }
 // ---------------------------------------------------------------------------
 // Calibration and prefix re-route of one invocation in one launch (Eqs. 11,
@@ -362,7 +347,8 @@ __global__ __launch_bounds__(CAL_THREADS) void calibrate_route_kernel(
     const float* __restrict__ logits, const int32_t* __restrict__ idx_full,
     const float* __restrict__ w_full, int T, int E, int k, int key_bits, double p,
     double* __restrict__ mass, int32_t* __restrict__ K_out, int32_t* __restrict__ idx,
-    float* __restrict__ w) {
+    float* __restrict__ w, const Guard g) {
+  if (guard_skip(g)) return;
   __shared__ CalLds L;
   const double a = mass_sorted(idx_full, w_full, 0, T * k, E, key_bits, L);
   const int K = prefix_K(E, k, p, L);
@@ -384,27 +370,27 @@ bool calibrate_route_fused(int T, int E, int k) {
 
 hipError_t launch_calibrate_route(const float* logits, const int32_t* idx_full, const float* w_full,
                                   int T, int E, int k, double p, double* mass, int32_t* K_out,
-                                  int32_t* idx, float* w, hipStream_t s) {
+                                  int32_t* idx, float* w, hipStream_t s, Guard g) {
   if (!calibrate_route_fused(T, E, k)) {
     hipError_t err = launch_calibrate(idx_full, w_full, T, E, k, nullptr, 1, p, mass, K_out, nullptr,
-                                      nullptr, s);
+                                      nullptr, s, g);
     if (err != hipSuccess || T == 0) return err;
     // logits are only read when the router is not run (x = NULL)
     return launch_route(nullptr, false, nullptr, nullptr, nullptr, T, 0, E, k, nullptr, 1, K_out,
-                        const_cast<float*>(logits), idx, w, nullptr, s);
+                        const_cast<float*>(logits), idx, w, nullptr, s, g);
   }
   int key_bits = 0;
   while ((1 << key_bits) < E) ++key_bits;
   const unsigned grid = (unsigned)((T + CAL_WAVES - 1) / CAL_WAVES);
   if (E <= 128)
     calibrate_route_kernel<2><<<grid, CAL_THREADS, 0, s>>>(logits, idx_full, w_full, T, E, k, key_bits, p,
-                                                           mass, K_out, idx, w);
+                                                           mass, K_out, idx, w, g);
   else if (E <= 256)
     calibrate_route_kernel<4><<<grid, CAL_THREADS, 0, s>>>(logits, idx_full, w_full, T, E, k, key_bits, p,
-                                                           mass, K_out, idx, w);
+                                                           mass, K_out, idx, w, g);
   else
     calibrate_route_kernel<8><<<grid, CAL_THREADS, 0, s>>>(logits, idx_full, w_full, T, E, k, key_bits, p,
-                                                           mass, K_out, idx, w);
+                                                           mass, K_out, idx, w, g);
   return hipGetLastError();
 }
 
@@ -426,11 +412,11 @@ size_t route_ws_bytes(int T, int d, int E) {
 hipError_t launch_route(const void* x, bool x_bf16, const float* w_r, const void* w_r_packed,
                         const float* bias, int T, int d, int E, int k, const int32_t* seg_offsets,
                         int n_seg, const int32_t* K_dev, float* logits, int32_t* idx, float* w,
-                        void* ws, hipStream_t s) {
+                        void* ws, hipStream_t s, Guard g) {
   float* part = nullptr;
   int S = 1;
   if (x && w_r_packed) {
-    hipError_t err = launch_router_x3(x, w_r_packed, bias, T, d, E, logits, ws, part, S, s);
+    hipError_t err = launch_router_x3(x, w_r_packed, bias, T, d, E, logits, ws, part, S, s, g);
     if (err != hipSuccess) return err;
   } else if (x) {
     if (d % 128 == 0) {
@@ -438,15 +424,15 @@ hipError_t launch_route(const void* x, bool x_bf16, const float* w_r, const void
       if (S > 1) part = static_cast<float*>(ws);
       dim3 grid((E + RM_E - 1) / RM_E, (T + RM_T - 1) / RM_T, S);
       if (x_bf16)
-        router_logits_mfma_kernel<true><<<grid, 256, 0, s>>>(x, w_r, bias, T, d, E, logits, part);
+        router_logits_mfma_kernel<true><<<grid, 256, 0, s>>>(x, w_r, bias, T, d, E, logits, part, g);
       else
-        router_logits_mfma_kernel<false><<<grid, 256, 0, s>>>(x, w_r, bias, T, d, E, logits, part);
+        router_logits_mfma_kernel<false><<<grid, 256, 0, s>>>(x, w_r, bias, T, d, E, logits, part, g);
     } else {
       dim3 grid((E + RT_E - 1) / RT_E, (T + RT_T - 1) / RT_T);
       if (x_bf16)
-        router_logits_simt_kernel<true><<<grid, 256, 0, s>>>(x, w_r, bias, T, d, E, logits);
+        router_logits_simt_kernel<true><<<grid, 256, 0, s>>>(x, w_r, bias, T, d, E, logits, g);
       else
-        router_logits_simt_kernel<false><<<grid, 256, 0, s>>>(x, w_r, bias, T, d, E, logits);
+        router_logits_simt_kernel<false><<<grid, 256, 0, s>>>(x, w_r, bias, T, d, E, logits, g);
     }
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
@@ -456,16 +442,16 @@ hipError_t launch_route(const void* x, bool x_bf16, const float* w_r, const void
   const int blocks = (T + 3) / 4, rblocks = (T + 15) / 16;
   const bool rows = T >= 16384;
   if (E <= 128 && rows)
-    topk_row_kernel<8><<<rblocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w);
+    topk_row_kernel<8><<<rblocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w, g);
   else if (E <= 128)
-    topk_kernel<2><<<blocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w);
+    topk_kernel<2><<<blocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w, g);
   else if (E <= 256 && rows)
-    topk_row_kernel<16><<<rblocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w);
+    topk_row_kernel<16><<<rblocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w, g);
   else if (E <= 256)
-    topk_kernel<4><<<blocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w);
+    topk_kernel<4><<<blocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w, g);
   else
     topk_kernel<TK_MAXC><<<blocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias,
-                                                idx, w);
+                                                idx, w, g);
   return hipGetLastError();
 }
 

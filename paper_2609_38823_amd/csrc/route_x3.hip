@@ -17,13 +17,15 @@
 // experts 32 eb + l % 32, k-values 16 kb + 8 (l / 32) .. + 8 -- the first
 // operand of v_mfma_f32_32x32x16_bf16.
 //
-// Kernel: a workgroup computes 32 MI tokens (MI = 1, 2) x 128 experts (wavefront w: the
-// expert block 4 blockIdx.x + w) over the d-range of split blockIdx.z.  The
-// token rows go global -> LDS in whole 128-byte row segments (stages of 64
-// k-values, ring of four, three stages ahead, chunk c of row r stored at
-// c ^ ((r >> 1) & 7)); each wavefront reads its weight fragments straight
-// from the packed array into registers, one stage ahead.  Per 16-wide
-// k block: 3 MI MFMAs (terms 1, 2, 3 of each token block in that order).
+// Kernel: a workgroup computes 32 MI tokens (MI = 1, 2, 4) x 128 experts
+// (wavefront w: the expert block 4 blockIdx.x + w) over the d-range of split
+// blockIdx.z.  The token rows go global -> LDS in whole 128-byte row segments
+// (stages of 64 k-values, ring of four, three stages ahead, chunk c of row r
+// stored at c ^ ((r >> 1) & 7)); each wavefront reads its weight fragments
+// straight from the packed array into a ring of NR register stages, NR - 1
+// stages ahead (the split weights are shared by every token tile and come
+// from L2).  Per 16-wide k block: 3 MI MFMAs (terms 1, 2, 3 of each token
+// block in that order).
 #include "common.hpp"
 
 #include <type_traits>
@@ -85,12 +87,16 @@ __global__ __launch_bounds__(256) void pack_router_kernel(const float* __restric
   for (int p = 0; p < 3; ++p) out[(f * 3 + p) * 64 + l] = make_uint4(t[p][0], t[p][1], t[p][2], t[p][3]);
 }
 
-template <int MI>
-__global__ __launch_bounds__(256, 2) void router_x3_kernel(const uint16_t* __restrict__ x,
-                                                           const uint16_t* __restrict__ wp,
-                                                           const float* __restrict__ bias, int T,
-                                                           int d, int E, float* __restrict__ logits,
-                                                           float* __restrict__ split_part) {
+// MI: 32-token blocks per workgroup; NR: weight stages in registers (2 or 4);
+// WPC: workgroups per compute unit.
+template <int MI, int NR, int WPC>
+__global__ __launch_bounds__(256, WPC) void router_x3_kernel(const uint16_t* __restrict__ x,
+                                                             const uint16_t* __restrict__ wp,
+                                                             const float* __restrict__ bias, int T,
+                                                             int d, int E, float* __restrict__ logits,
+                                                             float* __restrict__ split_part, const Guard g) {
+  if (guard_skip(g)) return;
+  static_assert(NR == 2 || NR == 4, "weight ring of 2 or 4 stages");
   constexpr int ROWS = 32 * MI;
   constexpr int SLOT = ROWS * XS_BYTES_ROW;
   __shared__ __attribute__((aligned(1024))) char ring[4 * SLOT];
@@ -144,21 +150,26 @@ __global__ __launch_bounds__(256, 2) void router_x3_kernel(const uint16_t* __res
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[i][e] = 0.f;
 
-  // stage st: barrier (every wavefront's token rows of the stage are in
-  // LDS), refill the slot freed by stage st - 1 with stage st + 3
-  // (ISSUE_X), load the weights of stage st + 1 (LOAD_W), then 4 x 3 MI
-  // MFMAs.  The flags are compile-time so that the compiler's waits count
-  // exactly.  The compiler waits for the weight registers, not for global ->
-  // LDS transfers; the vector-memory counter completes in issue order, and
-  // stage st's transfers precede the weights of stage st - 1, which the
-  // MFMAs of stage st - 1 waited for before this barrier.  Stage 0 waits
-  // explicitly (below).
-  auto stage = [&](auto ISSUE_X, auto LOAD_W, int st, const u32x4 (&wc)[4][3], u32x4 (&wn)[4][3]) {
+  // Stage st: wait until this wavefront's token-row transfers of stage st
+  // have landed (WAIT = the loads issued after them), barrier (every
+  // wavefront's have; every read of the slot refilled next is done), refill
+  // the slot of stage st - 1 with stage st + 3 and the weight registers of
+  // stage st - 1 with stage st + NR - 1, then 4 x 3 MI MFMAs.  Every stage
+  // issues its loads, also past the d-range's end (there they stay inside
+  // the buffers or read zeros, into slots and registers no stage uses), so
+  // the counts are the same in every stage: after the transfers of stage st
+  // come the weights of stage st + NR - 4 and the loads of two stages,
+  // 12 + 2 (MI + 12).  The prologue issues x0, w0, x1, w1, x2, w2 (NR = 4)
+  // or x0, x1, x2, w0 (NR = 2, whose stages 0 and 1 wait for fewer).
+  u32x4 wr[NR][4][3];
+  auto stage = [&](auto U, auto WAIT, int st) {
+    constexpr int u = decltype(U)::value;
+    wait_vm<decltype(WAIT)::value>();
     __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's reads of the previous stage
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    if constexpr (decltype(ISSUE_X)::value) issue_x(st + 3);
-    if constexpr (decltype(LOAD_W)::value) load_w(wn, st + 1);
+    issue_x(st + 3);
+    load_w(wr[(u + NR - 1) % NR], st + NR - 1);
     __builtin_amdgcn_sched_barrier(0);
     const char* slot = ring + (st & 3) * SLOT;
 #pragma unroll
@@ -170,50 +181,38 @@ __global__ __launch_bounds__(256, 2) void router_x3_kernel(const uint16_t* __res
       for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
         for (int p = 0; p < 3; ++p)
-          acc[mi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, wc[s4][p]), xf[mi],
+          acc[mi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, wr[u][s4][p]), xf[mi],
                                                             acc[mi], 0, 0, 0);
     }
   };
-  using F = std::integral_constant<bool, false>;
-  using Tr = std::integral_constant<bool, true>;
-
-  u32x4 wA[4][3], wB[4][3];
-  // three stages always (past the split's end the loads stay inside the
-  // buffer or read zeros at its end, into slots no stage reads), so that the
-  // wait for stage 0 counts exactly: 2 MI transfers and 12 weight loads
-  // follow it
-  issue_x(0);
-  issue_x(1);
-  issue_x(2);
-  load_w(wA, 0);
-  wait_vm<2 * MI + 12>();
-  int st = 0;
-  for (; st + 4 < n_st; st += 2) {  // every refill and load in range
-    stage(Tr{}, Tr{}, st, wA, wB);
-    stage(Tr{}, Tr{}, st + 1, wB, wA);
-  }
-  switch (n_st - st) {  // the last 1..4 stages (st is even: stage st uses wA)
-    case 4:
-      stage(Tr{}, Tr{}, st, wA, wB);
-      stage(F{}, Tr{}, st + 1, wB, wA);
-      stage(F{}, Tr{}, st + 2, wA, wB);
-      stage(F{}, F{}, st + 3, wB, wA);
-      break;
-    case 3:
-      stage(F{}, Tr{}, st, wA, wB);
-      stage(F{}, Tr{}, st + 1, wB, wA);
-      stage(F{}, F{}, st + 2, wA, wB);
-      break;
-    case 2:
-      stage(F{}, Tr{}, st, wA, wB);
-      stage(F{}, F{}, st + 1, wB, wA);
-      break;
-    default:
-      stage(F{}, F{}, st, wA, wB);
-      break;
+  using WS = std::integral_constant<int, 36 + 2 * MI>;
+  if constexpr (NR == 4) {
+    issue_x(0);
+    load_w(wr[0], 0);
+    issue_x(1);
+    load_w(wr[1], 1);
+    issue_x(2);
+    load_w(wr[2], 2);
+    for (int st = 0; st < n_st; st += 4) {
+      stage(std::integral_constant<int, 0>{}, WS{}, st);
+      if (st + 1 < n_st) stage(std::integral_constant<int, 1>{}, WS{}, st + 1);
+      if (st + 2 < n_st) stage(std::integral_constant<int, 2>{}, WS{}, st + 2);
+      if (st + 3 < n_st) stage(std::integral_constant<int, 3>{}, WS{}, st + 3);
+    }
+  } else {
+    issue_x(0);
+    issue_x(1);
+    issue_x(2);
+    load_w(wr[0], 0);
+    stage(std::integral_constant<int, 0>{}, std::integral_constant<int, 2 * MI + 12>{}, 0);
+    if (1 < n_st) stage(std::integral_constant<int, 1>{}, std::integral_constant<int, 2 * MI + 24>{}, 1);
+    for (int st = 2; st < n_st; st += 2) {
+      stage(std::integral_constant<int, 0>{}, WS{}, st);
+      if (st + 1 < n_st) stage(std::integral_constant<int, 1>{}, WS{}, st + 1);
+    }
   }
 
-  wait_vm<0>();                // transfers of stages past the split's end
+  wait_vm<0>();  // transfers of stages past the d-range's end
   if (eb_raw >= n_eb) return;  // no barrier follows
   // lane l: token t0 + l % 32 (+ 32 mi), experts 32 eb + 8 g + 4 (l / 32) + 0..3
 #pragma unroll
@@ -241,29 +240,33 @@ __global__ __launch_bounds__(256, 2) void router_x3_kernel(const uint16_t* __res
 }
 }  // namespace
 
-// Token rows per workgroup (32 MI, MI = 2 or 1) and d-splits S: 64-row
-// tiles when their grid, with at most 4 splits, has about 256 workgroups;
-// else 32-row tiles with up to 8 splits (whole 64-wide stages per split;
-// more splits only lengthen the Top-k kernel's partial sums).
-void router_x3_plan(int T, int d, int E, int& MI, int& S) {
+// Launch plan: 128-token tiles over the whole d-range once they give every
+// compute unit two workgroups (the split weights then stream from L2 once
+// per 128 tokens); else 64-token tiles when their grid, with at most 4
+// d-splits, has about 256 workgroups, else 32-token tiles with up to 8
+// splits (whole 64-wide stages per split; the Top-k kernel adds the split
+// partials, so more splits lengthen it).
+struct RouterPlan {
+  int MI, S;
+};
+RouterPlan router_x3_plan(int T, int d, int E) {
   const int groups = (E / 32 + 3) / 4;
+  if (groups * ((T + 127) / 128) >= 512) return RouterPlan{4, 1};
   for (int mi = 2; mi >= 1; mi /= 2) {
     const int tiles = groups * ((T + 32 * mi - 1) / (32 * mi));
     int s = 1;
     while (tiles * s < 256 && s < 4 && d % (XS_K * 2 * s) == 0) s *= 2;
     if (tiles * s >= 256 || mi == 1) {
       while (mi == 1 && tiles * s < 256 && s < 8 && d % (XS_K * 2 * s) == 0) s *= 2;
-      MI = mi;
-      S = s;
-      return;
+      return RouterPlan{mi, s};
     }
   }
+  return RouterPlan{1, 1};
 }
 
 size_t route_x3_ws_bytes(int T, int d, int E) {
-  int MI, S;
-  router_x3_plan(T, d, E, MI, S);
-  return S > 1 ? (size_t)S * T * E * sizeof(float) : 0;
+  const RouterPlan pl = router_x3_plan(T, d, E);
+  return pl.S > 1 ? (size_t)pl.S * T * E * sizeof(float) : 0;
 }
 
 hipError_t launch_pack_router(const float* w_r, int d, int E, void* out, hipStream_t s) {
@@ -274,17 +277,20 @@ hipError_t launch_pack_router(const float* w_r, int d, int E, void* out, hipStre
 }
 
 hipError_t launch_router_x3(const void* x, const void* w_packed, const float* bias, int T, int d,
-                            int E, float* logits, void* ws, float*& part, int& S, hipStream_t s) {
-  int MI;
-  router_x3_plan(T, d, E, MI, S);
+                            int E, float* logits, void* ws, float*& part, int& S, hipStream_t s,
+                            Guard g) {
+  const RouterPlan pl = router_x3_plan(T, d, E);
+  S = pl.S;
   part = S > 1 ? static_cast<float*>(ws) : nullptr;
-  const dim3 grid((E / 32 + 3) / 4, (T + 32 * MI - 1) / (32 * MI), S);
+  const dim3 grid((E / 32 + 3) / 4, (T + 32 * pl.MI - 1) / (32 * pl.MI), S);
   auto xp = static_cast<const uint16_t*>(x);
   auto wp = static_cast<const uint16_t*>(w_packed);
-  if (MI == 2)
-    router_x3_kernel<2><<<grid, 256, 0, s>>>(xp, wp, bias, T, d, E, logits, part);
+  if (pl.MI == 4)
+    router_x3_kernel<4, 2, 2><<<grid, 256, 0, s>>>(xp, wp, bias, T, d, E, logits, part, g);
+  else if (pl.MI == 2)
+    router_x3_kernel<2, 2, 2><<<grid, 256, 0, s>>>(xp, wp, bias, T, d, E, logits, part, g);
   else
-    router_x3_kernel<1><<<grid, 256, 0, s>>>(xp, wp, bias, T, d, E, logits, part);
+    router_x3_kernel<1, 2, 2><<<grid, 256, 0, s>>>(xp, wp, bias, T, d, E, logits, part, g);
   return hipGetLastError();
 }
 

@@ -27,7 +27,8 @@ int savb_splits(int n) {
 // partial[s][c] = sum of rows [s*per, (s+1)*per) of column c (rows < n - 1)
 template <bool BF16>
 __global__ __launch_bounds__(256) void savb_pool_kernel(const void* __restrict__ rows, int n, int d,
-                                                        int per, float* __restrict__ partial) {
+                                                        int per, float* __restrict__ partial, const Guard g) {
+  if (guard_skip(g)) return;
   const int c = blockIdx.x * 256 + threadIdx.x;
   if (c >= d) return;
   const int r0 = blockIdx.y * per, r1 = min(n - 1, r0 + per);
@@ -54,7 +55,8 @@ __global__ __launch_bounds__(256) void savb_pool_kernel(const void* __restrict__
 template <bool BF16>
 __global__ __launch_bounds__(256) void savb_feature_kernel(const void* __restrict__ rows, int n, int d,
                                                            int splits, const float* __restrict__ partial,
-                                                           float* __restrict__ x) {
+                                                           float* __restrict__ x, const Guard g) {
+  if (guard_skip(g)) return;
   const int c = blockIdx.x * 256 + threadIdx.x;
   if (c >= d) return;
   float v[16];
@@ -73,7 +75,8 @@ __global__ __launch_bounds__(256) void savb_feature_kernel(const void* __restric
 __global__ __launch_bounds__(256) void savb_hidden_kernel(const float* __restrict__ x, int d,
                                                           const float* __restrict__ w1,
                                                           const float* __restrict__ b1, int hid,
-                                                          float* __restrict__ hidden) {
+                                                          float* __restrict__ hidden, const Guard g) {
+  if (guard_skip(g)) return;
   extern __shared__ float xs[];  // [2d]
   for (int c = threadIdx.x; c < 2 * d; c += 256) xs[c] = x[c];
   __syncthreads();
@@ -115,7 +118,10 @@ __global__ __launch_bounds__(128) void savb_decide_kernel(const float* __restric
                                                           const float* __restrict__ w2,
                                                           const float* __restrict__ b2, double theta,
                                                           float* __restrict__ p_exit,
-                                                          int32_t* __restrict__ exit_flag) {
+                                                          int32_t* __restrict__ exit_flag,
+                                                          int32_t* __restrict__ exit_layer, int layer,
+                                                          const Guard g) {
+  if (guard_skip(g)) return;
   __shared__ float z[2];
   const int lane = threadIdx.x & 63, cls = threadIdx.x >> 6;
   float acc = 0.f;
@@ -128,7 +134,9 @@ __global__ __launch_bounds__(128) void savb_decide_kernel(const float* __restric
     const float e0 = expf(z[0] - mx), e1 = expf(z[1] - mx);
     const float p = e1 / (e0 + e1);
     *p_exit = p;
-    *exit_flag = static_cast<double>(p) >= theta ? 1 : 0;
+    const bool fire = static_cast<double>(p) >= theta;
+    *exit_flag = fire ? 1 : 0;
+    if (fire && exit_layer) *exit_layer = layer;  // the exit layer of a predicated gate
   }
 }
 
@@ -166,7 +174,7 @@ size_t savb_ws_bytes(int n, int d, int hid) {
 hipError_t launch_savb_gate(const void* rows, bool bf16, int n, int d, const float* w1,
                             const float* b1, int hid, const float* w2, const float* b2, double theta,
                             float* feature, float* p_exit, int32_t* exit_flag, void* ws,
-                            hipStream_t s) {
+                            hipStream_t s, Guard g, int32_t* exit_layer, int layer) {
   const int splits = savb_splits(n);
   float* partial = static_cast<float*>(ws);
   float* hidden = partial + (size_t)splits * d;
@@ -174,9 +182,9 @@ hipError_t launch_savb_gate(const void* rows, bool bf16, int n, int d, const flo
     const dim3 grid((d + 255) / 256, splits);
     const int per = (n - 1 + splits - 1) / splits;  // rows per split (splits * per >= n - 1)
     if (bf16)
-      savb_pool_kernel<true><<<grid, 256, 0, s>>>(rows, n, d, per, partial);
+      savb_pool_kernel<true><<<grid, 256, 0, s>>>(rows, n, d, per, partial, g);
     else
-      savb_pool_kernel<false><<<grid, 256, 0, s>>>(rows, n, d, per, partial);
+      savb_pool_kernel<false><<<grid, 256, 0, s>>>(rows, n, d, per, partial, g);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -184,17 +192,17 @@ hipError_t launch_savb_gate(const void* rows, bool bf16, int n, int d, const flo
   if (feature) x = feature;
   const unsigned fb = (unsigned)((d + 255) / 256);
   if (bf16)
-    savb_feature_kernel<true><<<fb, 256, 0, s>>>(rows, n, d, splits, partial, x);
+    savb_feature_kernel<true><<<fb, 256, 0, s>>>(rows, n, d, splits, partial, x, g);
   else
-    savb_feature_kernel<false><<<fb, 256, 0, s>>>(rows, n, d, splits, partial, x);
+    savb_feature_kernel<false><<<fb, 256, 0, s>>>(rows, n, d, splits, partial, x, g);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const unsigned hb = (unsigned)((hid + 3) / 4);
   const size_t lds = (size_t)2 * d * sizeof(float);
-  savb_hidden_kernel<<<hb, 256, lds, s>>>(x, d, w1, b1, hid, hidden);
+  savb_hidden_kernel<<<hb, 256, lds, s>>>(x, d, w1, b1, hid, hidden, g);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  savb_decide_kernel<<<1, 128, 0, s>>>(hidden, hid, w2, b2, theta, p_exit, exit_flag);
+  savb_decide_kernel<<<1, 128, 0, s>>>(hidden, hid, w2, b2, theta, p_exit, exit_flag, exit_layer, layer, g);
   return hipGetLastError();
 }
 

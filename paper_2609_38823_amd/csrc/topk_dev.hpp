@@ -104,5 +104,68 @@ __device__ __forceinline__ void topk_select(const float* row, int E, int k, int 
   topk_select_vals<MAXC>(v, E, k, Klim, lane, idx_t, w_t);
 }
 
+// ---- one token per row of 16 lanes (four tokens per wavefront) ---------
+// the row's best pair in all 16 lanes: quad swaps, then the half-row and row
+// mirrors (no value leaves the row)
+__device__ __forceinline__ void row_best(float& v, int& i) {
+  dpp_better<0xB1>(v, i);   // quad_perm [1, 0, 3, 2]
+  dpp_better<0x4E>(v, i);   // quad_perm [2, 3, 0, 1]
+  dpp_better<0x141>(v, i);  // row_half_mirror
+  dpp_better<0x140>(v, i);  // row_mirror
+}
+__device__ __forceinline__ float row_sum(float v) {
+  v += dpp_f<0xB1>(v);
+  v += dpp_f<0x4E>(v);
+  v += dpp_f<0x141>(v);
+  v += dpp_f<0x140>(v);
+  return v;
+}
+
+// The k best of one token's logits [0, Klim) held by the 16 lanes of a row:
+// lane j holds experts j, j + 16, ... in v[c] (expert j + 16 c).  Each
+// round's arg-max is a lane-local scan plus row_best; round r's winner is
+// kept by lane r % 16 in slot r / 16 (k <= 32).  Same selection order, tie
+// rule and weights as topk_select_vals: the slots' exponentials are summed
+// by the same butterfly, so for k <= 16 the weights are bitwise equal.
+template <int MAXC>
+__device__ __forceinline__ void row_topk_select(const float (&v)[MAXC], int j, int E, int k, int Klim,
+                                                int32_t* idx_t, float* w_t) {
+  uint32_t alive = 0;
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c)
+    if (j + 16 * c < Klim) alive |= 1u << c;
+  float my_v[2] = {0.f, 0.f};
+  int my_i[2] = {0, 0};
+  float v0 = 0.f;
+  for (int r = 0; r < k; ++r) {
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c)
+      if (alive & (1u << c)) better(bv, bi, v[c], j + 16 * c);
+    row_best(bv, bi);
+    if (bi < E && (bi & 15) == j) alive &= ~(1u << (bi >> 4));
+    if (r == 0) v0 = bv;
+    if ((r & 15) == j) {
+      my_v[r >> 4] = bv;
+      my_i[r >> 4] = bi;
+    }
+  }
+  float ex[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) ex[q] = j + 16 * q < k ? expf(my_v[q] - v0) : 0.f;
+  // slots in order r = 0..k-1: lanes hold r = j and r = j + 16; the row sum
+  // adds the k exponentials (the same total in every lane of the row)
+  const float sum = row_sum(ex[0] + ex[1]);
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int r = j + 16 * q;
+    if (r < k) {
+      idx_t[r] = my_i[q];
+      w_t[r] = ex[q] / sum;
+    }
+  }
+}
+
 }  // namespace
 }  // namespace decomoe

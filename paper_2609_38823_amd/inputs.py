@@ -64,6 +64,8 @@ class Workload:
 
 QWEN3_VL_MOE = LayerShape(d=2048, E=128, m=768, k=8, dtype="bf16", zipf_alpha=0.35)
 TINY = LayerShape(d=256, E=16, m=128, k=2, dtype="f32", zipf_alpha=None)
+# the smallest shape the packed bf16 path takes (d, m multiples of 256, E of 32)
+SMALL_BF16 = LayerShape(d=256, E=32, m=256, k=4, dtype="bf16", zipf_alpha=0.35)
 
 WORKLOADS = {
     # tiny fp32 correctness layer: 384 visual + 128 text rows
@@ -78,6 +80,9 @@ WORKLOADS = {
     # tiny fp32 stack: 6 layers over 384 visual + 128 text rows, exit at layer 3
     "tiny_stack_f32": Workload("tiny_stack_f32", TINY, T=512, n_visual=384, p=0.9, layers=6,
                                exit_layer=3),
+    # small packed bf16 stack: 8 layers over 384 visual + 128 text rows, exit at layer 4
+    "small_stack_bf16": Workload("small_stack_bf16", SMALL_BF16, T=512, n_visual=384, p=0.9, layers=8,
+                                 exit_layer=4),
     # decode: 64 single text tokens through 48 layers
     "qwen3vl_decode64": Workload("qwen3vl_decode64", QWEN3_VL_MOE, T=64, n_visual=0, p=0.85,
                                  layers=48),

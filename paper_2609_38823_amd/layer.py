@@ -155,9 +155,18 @@ class MoELayer:
         self._bufs: dict = {}
         self._kdev: dict = {}  # device copies of fixed prefix lengths
 
-    def _route(self, x, b: Buffers, idx, w, stream=None):
+    def _check_guard(self, guard):
+        # predicated calls exist for the packed bf16 path (the stacks that
+        # capture Algorithm 2's prefill as one graph)
+        if guard is not None and not (self.packed and self.w_r_packed is not None):
+            raise ValueError("predicated layers need packed bf16 router and expert weights")
+
+    def _route(self, x, b: Buffers, idx, w, stream=None, guard=None):
         """Router logits into b.logits and the full-pool Top-k."""
-        if self.w_r_packed is not None:
+        if guard is not None:
+            abi.moe_route_packed_if(x, self.w_r_packed, self.bias, self.k, b.logits, idx, w, guard, ws=b.ws,
+                                    stream=stream)
+        elif self.w_r_packed is not None:
             abi.moe_route_packed(x, self.w_r_packed, self.bias, self.k, b.logits, idx, w, ws=b.ws,
                                  stream=stream)
         else:
@@ -175,8 +184,20 @@ class MoELayer:
     # With `residual`, the combine writes out = residual + MoE(x) into `out`
     # (default b.out); `out` may be `residual` itself (in-place hidden state).
     def _experts(self, x, b: Buffers, idx, w, K_dev=None, stream=None, mark=None, residual=None,
-                 out=None):
+                 out=None, guard=None):
         mark = mark or (lambda: None)
+        if guard is not None:
+            # the same calls, each run only while the predicate holds
+            abi.moe_dispatch_if(idx, self.E, None, b.counts, b.offsets, b.src_of_row, b.row_of_slot, None,
+                                b.ws, guard, stream=stream)
+            abi.moe_expert_ffn_packed_gather_if(x, idx.shape[1], b.src_of_row, b.offsets, self.w_gate_up,
+                                                self.w_down, b.y_perm, b.ws, guard, K_dev=K_dev,
+                                                stream=stream)
+            if residual is None:
+                raise ValueError("predicated layers combine with the residual")
+            abi.moe_combine_residual_if(b.y_perm, b.row_of_slot, w, residual,
+                                        b.out if out is None else out, guard, stream=stream)
+            return
         if self.packed:
             # the expert GEMM reads the token rows through src_of_row: the
             # dispatch only groups the assignments
@@ -200,13 +221,16 @@ class MoELayer:
         mark()
 
     def forward_dense(self, x: torch.Tensor, b: Buffers | None = None, stream=None,
-                      mark=None, residual=None, out=None) -> Buffers:
-        """Full expert pool (layers before the visual exit)."""
+                      mark=None, residual=None, out=None, guard=None) -> Buffers:
+        """Full expert pool (layers before the visual exit).  ``guard`` =
+        (int32 device tensor g, lo, hi): every call runs only while
+        lo <= g[0] < hi (packed layers, with a residual)."""
+        self._check_guard(guard)
         b = b or self.buffers(x.shape[0])
-        self._route(x, b, b.idx, b.w, stream=stream)
+        self._route(x, b, b.idx, b.w, stream=stream, guard=guard)
         if mark:
             mark()
-        self._experts(x, b, b.idx, b.w, stream=stream, mark=mark, residual=residual, out=out)
+        self._experts(x, b, b.idx, b.w, stream=stream, mark=mark, residual=residual, out=out, guard=guard)
         return b
 
     def prefix_tensor(self, K: int) -> torch.Tensor:
@@ -241,15 +265,24 @@ class MoELayer:
         return b
 
     def forward_rcep(self, x: torch.Tensor, p: float, seg_offsets=None, b: Buffers | None = None,
-                     stream=None, mark=None, residual=None, out=None, K_out=None) -> Buffers:
+                     stream=None, mark=None, residual=None, out=None, K_out=None, guard=None) -> Buffers:
         """Prefix-restricted layer (from the visual exit on, Algorithm 2).
-        K_out ([n_seg] int32, default b.K) receives the prefix lengths."""
+        K_out ([n_seg] int32, default b.K) receives the prefix lengths.
+        ``guard``: as in forward_dense (one invocation only)."""
+        self._check_guard(guard)
         n_seg = 1 if seg_offsets is None else seg_offsets.numel() - 1
         b = b or self.buffers(x.shape[0], n_seg)
         K = b.K if K_out is None else K_out
         mk = mark or (lambda: None)
-        self._route(x, b, b.idx_full, b.w_full, stream=stream)
+        self._route(x, b, b.idx_full, b.w_full, stream=stream, guard=guard)
         mk()
+        if guard is not None:
+            if seg_offsets is not None:
+                raise ValueError("predicated RCEP layers take one invocation")
+            abi.moe_calibrate_route_prefix_if(b.logits, b.idx_full, b.w_full, p, b.mass, K, b.idx, b.w, guard,
+                                              stream=stream)
+            self._experts(x, b, b.idx, b.w, K_dev=K, stream=stream, residual=residual, out=out, guard=guard)
+            return b
         if seg_offsets is None:
             # one invocation: masses, K and the prefix re-route in one call
             abi.moe_calibrate_route_prefix(b.logits, b.idx_full, b.w_full, p, b.mass, K, b.idx, b.w,

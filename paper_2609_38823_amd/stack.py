@@ -84,19 +84,20 @@ class MoEStack:
         return self._h[key]
 
     def layer_forward(self, l: int, src: torch.Tensor, dst: torch.Tensor, rcep: bool, p: float,
-                      stream=None, mark=None, K_fixed=None) -> Buffers:
+                      stream=None, mark=None, K_fixed=None, guard=None) -> Buffers:
         """One block: dst = src + MoE_l(src); dst may be src (in place).
         rcep: the RCEP span (Eq. 12's K, or the prefix length K_fixed when
         given: a host int or a device int32 tensor); else the full expert
-        pool."""
+        pool.  guard: (int32 device tensor g, lo, hi), the block runs only
+        while lo <= g[0] < hi (packed layers)."""
         b = self.buffers(src.shape[0])
         layer = self.layers[l]
         if rcep and K_fixed is not None:
             return layer.forward_prefix(src, K_fixed, b=b, stream=stream, mark=mark, residual=src, out=dst)
         if rcep:
             return layer.forward_rcep(src, p, b=b, stream=stream, mark=mark, residual=src, out=dst,
-                                      K_out=self.K_trace[l, :1])
-        return layer.forward_dense(src, b=b, stream=stream, mark=mark, residual=src, out=dst)
+                                      K_out=self.K_trace[l, :1], guard=guard)
+        return layer.forward_dense(src, b=b, stream=stream, mark=mark, residual=src, out=dst, guard=guard)
 
     def forward(self, x: torch.Tensor, n_visual: int, p: float, exit_layer: int | None,
                 stream=None, hook=None, after_exit: str = "rcep", K_fixed=None) -> torch.Tensor:
@@ -173,6 +174,67 @@ class MoEStack:
             src = dst
         return src, exit_layer, trace
 
+    def capture_prefill(self, x: torch.Tensor, n_visual: int, p: float, gates: dict, theta: float):
+        """Algorithm 2's prefill with the SAVB gate as ONE HIP graph over the
+        static input rows x (packed bf16 layers).
+
+        The exit layer is decided on the device, so from the first candidate
+        layer on both variants of every layer are captured, each call
+        predicated on the device int ``exit_layer`` (L = no exit yet):
+          candidate l   moe_savb_gate_if runs while exit_layer == L and, when
+                        it fires, sets exit_layer = l and its own flag; then
+                        drop_visual_block_if copies the text rows when that
+                        flag is set
+          layer l       the dense block over all rows while exit_layer > l,
+                        the RCEP block over the text rows while exit_layer <= l
+        Layers before the first candidate run dense without a predicate.
+        Returns a PrefillGraph: replay() runs the step; result() (one host
+        read, after the replay) gives what forward_gated returns.
+        """
+        if not self.layers or not all(lay.packed and lay.w_r_packed is not None for lay in self.layers):
+            raise ValueError("the captured prefill needs packed bf16 layers")
+        T = x.shape[0]
+        n_text = T - n_visual
+        L = self.L
+        dev = self.device
+        cands = sorted(l for l in gates if 0 <= l < L) if n_visual > 0 and n_text > 0 else []
+        hid = next(iter(gates.values()))["w1"].shape[0] if gates else 1
+        st = _PrefillState(self, x, n_visual, cands, hid, dev)
+        side = torch.cuda.Stream(device=dev)
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):  # every buffer exists before capture
+            self._record_prefill(st, p, gates, theta)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            self._record_prefill(st, p, gates, theta)
+        st.graph = g
+        return st
+
+    def _record_prefill(self, st: "_PrefillState", p: float, gates: dict, theta: float):
+        L, nv = self.L, st.n_visual
+        st.exit_layer.fill_(L)  # fill kernels, not memsets (the graph replays them)
+        st.fire.zero_()
+        st.p_exit.zero_()
+        h_full, h_text = self.hidden(st.T), self.hidden(st.T - nv, "text")
+        first = st.cands[0] if st.cands else L
+        never = (st.exit_layer, L, L + 1)  # no exit yet
+        for l in range(L):
+            src_full = st.x if l == 0 else h_full
+            if l in st.cands:
+                c = st.cands.index(l)
+                gt = gates[l]
+                abi.moe_savb_gate_if(src_full[nv:], gt["w1"], gt["b1"], gt["w2"], gt["b2"], theta,
+                                     st.p_exit[c:c + 1], st.fire[c:c + 1], st.gate_ws, never,
+                                     exit_layer=st.exit_layer, layer=l)
+                abi.drop_visual_block_if(src_full, 0, nv, st.fire[c:c + 1], h_text)
+            if l < first:
+                self.layer_forward(l, src_full, h_full, False, p)
+            else:
+                self.layer_forward(l, src_full, h_full, False, p, guard=(st.exit_layer, l + 1, L + 1))
+                self.layer_forward(l, h_text, h_text, True, p, guard=(st.exit_layer, 0, l + 1))
+
     def capture_decode(self, x: torch.Tensor, p: float):
         """Capture one decode step (RCEP in every layer) over the static
         input rows x as a HIP graph.  Returns (graph, out): replaying the
@@ -187,3 +249,37 @@ class MoEStack:
         with torch.cuda.graph(g):
             out = self.forward(x, 0, p, exit_layer=0)
         return g, out
+
+
+class _PrefillState:
+    """Device state and outputs of a captured prefill (MoEStack.capture_prefill)."""
+
+    def __init__(self, stack: MoEStack, x: torch.Tensor, n_visual: int, cands: list, hid: int, dev):
+        self.stack, self.x, self.n_visual, self.cands = stack, x, n_visual, cands
+        self.T = x.shape[0]
+        # exit_layer, and one flag and p_exit per candidate (16-byte rows)
+        self.exit_layer = torch.empty((4,), dtype=torch.int32, device=dev)[:1]
+        nc = max(len(cands), 1)
+        self._fire = torch.zeros((nc, 4), dtype=torch.int32, device=dev)
+        self._p = torch.zeros((nc, 4), dtype=torch.float32, device=dev)
+        self.fire = self._fire[:, 0]
+        self.p_exit = self._p[:, 0]
+        n_text = self.T - n_visual
+        self.gate_ws = torch.empty((abi.moe_savb_workspace_size(max(n_text, 1), x.shape[1], hid),),
+                                   dtype=torch.uint8, device=dev)
+        self.graph = None
+
+    def replay(self):
+        self.graph.replay()
+
+    def result(self):
+        """(final rows, exit layer or None, [(candidate, p_exit)] evaluated),
+        as MoEStack.forward_gated returns them (reads the device state)."""
+        torch.cuda.current_stream().synchronize()
+        ex = int(self.exit_layer.item())
+        L = self.stack.L
+        ps = self._p[:, 0].cpu().tolist()
+        evaluated = [(l, ps[i]) for i, l in enumerate(self.cands) if ex == L or l <= ex]
+        if ex < L:
+            return self.stack.hidden(self.T - self.n_visual, "text"), ex, evaluated
+        return self.stack.hidden(self.T), None, evaluated

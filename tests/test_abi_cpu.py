@@ -34,12 +34,29 @@ def test_header_declares_the_boundary():
         "moe_pack_router", "moe_permute_experts", "moe_route", "moe_route_packed", "moe_savb_gate",
         "moe_savb_workspace_size", "moe_status_string", "moe_workspace_size", "drop_visual_block_if",
         "moe_expand_dense_routing", "moe_expert_ffn_packed_gather", "moe_calibrate_route_prefix",
-        "moe_ffn_status", "moe_expert_ffn_packed_gather_noalloc"])
+        "moe_ffn_status", "moe_expert_ffn_packed_gather_noalloc",
+        "moe_route_packed_if", "moe_calibrate_route_prefix_if", "moe_dispatch_if",
+        "moe_expert_ffn_packed_gather_if", "moe_combine_residual_if", "moe_savb_gate_if"])
 
 
 def test_every_declared_symbol_is_exported(lib):
     for name in declared_functions():
         assert hasattr(lib, name), name
+
+
+def test_exports_are_exactly_the_declared_functions(lib):
+    """No helper leaks out of the library as a C symbol (read with nm)."""
+    import shutil
+    import subprocess
+    from paper_2609_38823_amd import abi
+    nm = shutil.which("nm")
+    if nm is None:
+        pytest.skip("nm not available")
+    out = subprocess.run([nm, "-D", "--defined-only", abi.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    c_syms = sorted({ln.split()[-1] for ln in out.splitlines()
+                     if " T " in ln and not ln.split()[-1].startswith("_Z")})
+    assert c_syms == declared_functions()
 
 
 def test_binding_names_match_header():
@@ -223,6 +240,42 @@ def test_gather_ffn_noalloc_rejects(lib):
     assert call(T=10950, k=2, E=128, d=2048, m=768) == EWORKSPACE
     assert call(T=4096, k=8, E=128, d=2048, m=768) == EWORKSPACE  # 32 768 rows
     assert call(T=1 << 20, d=2048) == EUNSUPPORTED  # T*d*2 >= 2^31
+
+
+def test_predicated_calls_check_like_the_plain_calls(lib):
+    """The *_if calls reject what the plain calls reject, plus a misaligned
+    predicate, all on the host (only rejected calls are made here)."""
+    bad = ctypes.c_void_p(0x10002)
+    G = ctypes.c_void_p(0x70000)
+    # moe_route_packed_if: float32 x, E not a multiple of 32, misaligned guard
+    rp = lib.moe_route_packed_if
+    base = [P1, BF16, P2, NULL, 16, 64, 32, 2, NULL, 1, NULL, P3, P4, P5, P6, 1 << 30]
+    assert rp(*base[:1], F32, *base[2:], G, 0, 1, NULL) == EUNSUPPORTED
+    a = list(base); a[6] = 48
+    assert rp(*a, G, 0, 1, NULL) == EUNSUPPORTED
+    assert rp(*base, bad, 0, 1, NULL) == EINVAL
+    # moe_dispatch_if: k > E, misaligned guard
+    di = lib.moe_dispatch_if
+    assert di(P1, 16, 9, 8, NULL, F32, 0, P2, P3, P4, P5, NULL, P6, 1 << 20, G, 0, 1, NULL) == EINVAL
+    assert di(P1, 16, 2, 8, NULL, F32, 0, P2, P3, P4, P5, NULL, P6, 1 << 20, bad, 0, 1, NULL) == EINVAL
+    # moe_calibrate_route_prefix_if: p outside (0, 1]
+    cr = lib.moe_calibrate_route_prefix_if
+    assert cr(P1, P2, P3, 16, 32, 2, 0.0, P4, P5, P6, P7, NULL, 0, G, 0, 1, NULL) == EINVAL
+    # moe_expert_ffn_packed_gather_if: m not a multiple of 256
+    fi = lib.moe_expert_ffn_packed_gather_if
+    assert fi(P1, BF16, 16, 2, P2, P3, 16, NULL, 0, 256, 128, P4, P5, P6, ctypes.c_void_p(0x1000000),
+              1 << 30, G, 0, 1, NULL) == EUNSUPPORTED
+    assert fi(P1, BF16, 16, 2, P2, P3, 16, NULL, 0, 256, 256, P4, P5, P6, ctypes.c_void_p(0x1000000),
+              1 << 30, bad, 0, 1, NULL) == EINVAL
+    # moe_combine_residual_if: out shifted onto the residual
+    ci = lib.moe_combine_residual_if
+    assert ci(P1, BF16, P2, P3, 8, 2, 64, P4, ctypes.c_void_p(0x40010), G, 0, 1, NULL) == EALIAS
+    # moe_savb_gate_if: exit_layer on top of the flag, misaligned exit_layer
+    gi = lib.moe_savb_gate_if
+    ws = ctypes.c_void_p(0x1000000)
+    args = [P1, F32, 4, 64, P2, NULL, 8, P3, NULL, 0.5, NULL, P4, P5, ws, 1 << 20, G, 0, 1]
+    assert gi(*args, P5, 3, NULL) == EALIAS
+    assert gi(*args, bad, 3, NULL) == EINVAL
 
 
 def test_ffn_status_rejects(lib):

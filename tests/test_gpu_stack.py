@@ -79,7 +79,7 @@ def test_permute_experts_bitwise(dt, E, d, m):
 
 
 @pytest.mark.parametrize("dt,T,k,d", [("bf16", 300, 8, 2048), ("bf16", 77, 3, 136),
-                                      ("f32", 129, 2, 256), ("bf16", 5, 2, 9)])
+                                      ("f32", 129, 2, 256), ("bf16", 5, 2, 9), ("bf16", 20000, 2, 2048)])
 @pytest.mark.parametrize("in_place", [False, True])
 def test_combine_residual(dt, T, k, d, in_place):
     """out = residual + sum_j w_j y_row(j): against the oracle's combine plus

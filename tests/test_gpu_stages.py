@@ -244,12 +244,15 @@ E96_BF16 = I.LayerShape(d=256, E=96, m=8, k=4, dtype="bf16", zipf_alpha=0.35)  #
 D64_BF16 = I.LayerShape(d=64, E=32, m=8, k=2, dtype="bf16", zipf_alpha=None)   # one 64-wide stage
 
 
-# 64-row tiles at 4096 (4 splits) and 8192 (2) and 65536 (1); 32-row tiles
-# with 8 splits below; the small shapes cover idle wavefronts and S = 1
-# with a single stage
+# 64-row tiles at 4096 (4 splits) and 8192 (2); 32-row tiles with 8 splits
+# below; from 65 536 rows (E <= 128) 128-row tiles over the whole d-range
+# with the Top-k selected in the same launch (ragged last tile, idle
+# wavefronts, a single 64-wide stage); the small shapes cover idle
+# wavefronts and S = 1 with a single stage
 @pytest.mark.parametrize("shape,T", [("qwen", 4096), ("qwen", 8192), ("qwen", 512), ("qwen", 77),
                                      ("qwen", 64), ("qwen", 1), ("e96", 333), ("d64", 50),
-                                     ("qwen", 65536)])
+                                     ("qwen", 65536), ("qwen", 65536 + 77), ("e96", 65536 + 5),
+                                     ("d64", 70000)])
 def test_route_packed(shape, T):
     sh = {"qwen": I.QWEN3_VL_MOE, "e96": E96_BF16, "d64": D64_BF16}[shape]
     rp = I.router_params(sh, seed=3)
@@ -282,6 +285,33 @@ def test_route_packed(shape, T):
     tf_idx, tf_w = oracle.full_pool_route(a_gpu, sh.k)
     np.testing.assert_array_equal(gi, tf_idx)
     np.testing.assert_allclose(host(w)[rows], tf_w, rtol=2e-5, atol=1e-6)
+
+
+@pytest.mark.parametrize("T", [65536 + 300, 4096])
+def test_route_packed_prefix_segments(T):
+    """The split router with per-segment prefix lengths (Top-k inside [0, K)
+    of each token's segment): at 65 836 rows the Top-k is selected in the
+    router's own launch, at 4096 by the separate kernel; indices bit-exact
+    and weights against the oracle on the GPU's logits."""
+    sh = I.QWEN3_VL_MOE
+    rp = I.router_params(sh, seed=5)
+    x = I.tokens(sh, T, seed=T + 1)
+    wp = torch.empty((3 * sh.d * sh.E,), dtype=torch.bfloat16, device="cuda")
+    abi.moe_pack_router(dev(rp["w_r"]), wp)
+    so = np.array([0, 7, T // 3, T // 3, T - 129, T], np.int32)  # an empty segment, short ones
+    Ks = np.array([8, 50, 128, 3, 85], np.int32)  # 3 < k: raised to k
+    logits, idx, w = f32((T, sh.E)), i32((T, sh.k)), f32((T, sh.k))
+    abi.moe_route_packed(dev(x, torch.bfloat16), wp, dev(rp["bias"]), sh.k, logits, idx, w,
+                         seg_offsets=dev(so), K_dev=dev(Ks), ws=ws_for(T, sh.E, sh.k, sh.d, n_seg=5))
+    a_gpu = host(logits).astype(np.float64)
+    gi, gw = host(idx), host(w)
+    for s_, (lo, hi) in enumerate(zip(so[:-1], so[1:])):
+        if hi == lo:
+            continue
+        K = int(np.clip(Ks[s_], sh.k, sh.E))
+        ref_idx, ref_w = oracle.prefix_route(a_gpu[lo:hi], K, sh.k)
+        np.testing.assert_array_equal(gi[lo:hi], ref_idx)
+        np.testing.assert_allclose(gw[lo:hi], ref_w, rtol=2e-5, atol=1e-6)
 
 
 # ---------------------------------------------------------------------------
@@ -894,8 +924,11 @@ def test_expert_ffn_packed_gather_out_of_range_rows_read_token_zero():
 # ---------------------------------------------------------------------------
 # moe_combine
 # ---------------------------------------------------------------------------
+# (20000, 2, 2048) and (9000, 4, 2048, f32) write more than 64 MiB: the
+# output stores bypass the caches
 @pytest.mark.parametrize("T,k,d,dt", [(512, 2, 256, "f32"), (4096, 8, 2048, "bf16"), (1, 8, 2048, "bf16"),
-                                      (33, 3, 10, "f32"), (50, 4, 6, "bf16")])
+                                      (33, 3, 10, "f32"), (50, 4, 6, "bf16"), (20000, 2, 2048, "bf16"),
+                                      (9000, 1, 2048, "f32")])
 def test_combine(T, k, d, dt):
     A = T * k
     y = I.synthetic_rows(A, d, dt, seed=A + d)
@@ -908,7 +941,7 @@ def test_combine(T, k, d, dt):
     assert row_rel(host(out), ref) <= TOL[dt]
 
 
-@pytest.mark.parametrize("T,E,k,d", [(4096, 128, 8, 2048), (77, 16, 2, 256)])
+@pytest.mark.parametrize("T,E,k,d", [(4096, 128, 8, 2048), (77, 16, 2, 256), (20000, 128, 2, 2048)])
 def test_combine_inverts_dispatch(T, E, k, d):
     """Identity experts with unit weights give k*x exactly (k a power of two,
     sums of k bf16 copies exact in float32)."""
