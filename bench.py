@@ -82,6 +82,11 @@ def stage_flops_bytes(stage: str, T: int, d: int, E: int, m: int, k: int, touche
         return 0.0, 2 * T * k * 4 + E * 8 + 4
     if stage == "calibrate_route":  # masses, K and the prefix re-route in one call
         return 0.0, 2 * T * k * 4 + E * 8 + 4 + T * K * 4 + 2 * T * k * 4
+    if stage == "route_rcep":  # router + full-pool Top-k + masses, K, re-route + grouping in one call
+        f, b = stage_flops_bytes("route_full", T, d, E, m, k, touched, K, gather)
+        _, b2 = stage_flops_bytes("calibrate_route", T, d, E, m, k, touched, K, gather)
+        _, b3 = stage_flops_bytes("dispatch", T, d, E, m, k, touched, K, gather)
+        return f, b + b2 + b3
     if stage == "dispatch":
         return 0.0, T * k * 4 + (E + 1) * 8 + 2 * A * 4 + (0 if gather else T * d * 2 + A * d * 2)
     if stage == "ffn":
@@ -261,8 +266,7 @@ def bench_layer(args) -> int:
         return 0
 
     stream = torch.cuda.current_stream()
-    stages = ["route_full", "dispatch", "ffn", "combine", "drop",
-              "r.route_full", "r.calibrate_route", "r.dispatch", "r.ffn", "r.combine"]
+    stages = ["route_full", "dispatch", "ffn", "combine", "drop", "r.route_rcep", "r.ffn", "r.combine"]
 
     def step(ev=None):
         marks = iter(ev) if ev is not None else None
@@ -377,9 +381,9 @@ def bench_layer(args) -> int:
                          paper_dense_equiv_tflops=(2 * d * E + 6 * K * d * m) * (T - V) / rcep_ms / 1e9),
         "rcep@512 experts, dense-equivalent executor": dict(
             ms=round(dense_equiv_ms, 4), K=K, expert_gflop=6 * K * d * m * (T - V) / 1e9,
-            sparse_expert_ms=round(stage_ms["r.dispatch"] + stage_ms["r.ffn"] + stage_ms["r.combine"], 4),
+            sparse_expert_ms=round(stage_ms["r.ffn"] + stage_ms["r.combine"], 4),
             note="expand + dispatch (k = E) + expert FFN over experts [0, K) + combine; the RCEP "
-                 "span's sparse dispatch/FFN/combine for comparison"),
+                 "span's sparse FFN/combine for comparison (its grouping runs inside r.route_rcep)"),
         "dense@512": dict(ms=round(dense512_ms, 4), tokens_per_s=(T - V) / dense512_ms * 1e3,
                           tflops=per_tok_flops * (T - V) / dense512_ms / 1e9, touched_experts=touched_512,
                           paper_dense_equiv_tflops=(2 * d * E + 6 * E * d * m) * (T - V) / dense512_ms / 1e9),
@@ -562,7 +566,7 @@ def bench_stack48(args) -> int:
     if not args.no_cpu_baseline:
         cpu = _oracle_stack_sample(st, x_np, wl)
     names_d = ["route", "dispatch", "ffn", "combine_residual"]
-    names_r = ["route_full", "calibrate_route", "dispatch", "ffn", "combine_residual"]
+    names_r = ["route_rcep", "ffn", "combine_residual"]
     return _line(
         "MoE-stack prefill tokens/s (48 MoE layers, SAVB exit at layer 20, RCEP p 0.9)",
         wl.T / (ms * 1e-3), "tokens/s", args, ms,

@@ -237,6 +237,26 @@ int moe_calibrate_route_prefix(const float* logits, const int32_t* topk_idx_full
                                void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * moe_route_rcep - the RCEP routing of one invocation through the grouping
+ * of its dispatch, in one call (Eq. 1, Eq. 10, Eqs. 11-12, the prefix
+ * re-route after Eq. 12 and Algorithm 2's dispatch): bitwise the outputs of
+ *   moe_route_packed(x, ..., K_dev = NULL)        -> logits, topk_idx_full, topk_w_full
+ *   moe_calibrate_route_prefix(p)                  -> mass, K_out, topk_idx, topk_w
+ *   moe_dispatch(topk_idx, x = NULL)               -> counts, offsets, src_of_row, row_of_slot
+ * with the same arguments, layouts, limits and errors (bf16 x, packed
+ * router weights; 1 <= k <= min(E, 32); p in (0, 1]).  When T*k <= 8192
+ * and E <= 512, the masses, K, the re-route and the grouping run as one
+ * launch after the router's (the last of its workgroups to finish groups
+ * the entries); otherwise the three calls run.  T = 0 gives K = k and empty
+ * counts.  Needs ws (moe_workspace_size).
+ */
+int moe_route_rcep(const void* x, moe_dtype dtype, const void* w_r_packed, const float* bias, int T, int d,
+                   int E, int k, double p, float* logits, int32_t* topk_idx_full, float* topk_w_full,
+                   double* mass, int32_t* K_out, int32_t* topk_idx, float* topk_w, int32_t* counts,
+                   int32_t* offsets, int32_t* src_of_row, int32_t* row_of_slot, void* ws, size_t ws_bytes,
+                   hipStream_t stream);
+
+/*
  * moe_dispatch - group the T*k (token, slot) assignments by expert
  * (Algorithm 2: only the selected experts are evaluated).
  *
@@ -399,6 +419,12 @@ int moe_route_packed_if(const void* x, moe_dtype dtype, const void* w_r_packed, 
                         const int32_t* K_dev, float* logits, int32_t* topk_idx, float* topk_w,
                         void* ws, size_t ws_bytes, const int32_t* guard, int guard_lo, int guard_hi,
                         hipStream_t stream);
+int moe_route_rcep_if(const void* x, moe_dtype dtype, const void* w_r_packed, const float* bias, int T,
+                      int d, int E, int k, double p, float* logits, int32_t* topk_idx_full,
+                      float* topk_w_full, double* mass, int32_t* K_out, int32_t* topk_idx, float* topk_w,
+                      int32_t* counts, int32_t* offsets, int32_t* src_of_row, int32_t* row_of_slot,
+                      void* ws, size_t ws_bytes, const int32_t* guard, int guard_lo, int guard_hi,
+                      hipStream_t stream);
 int moe_calibrate_route_prefix_if(const float* logits, const int32_t* topk_idx_full,
                                   const float* topk_w_full, int T, int E, int k, double p,
                                   double* mass, int32_t* K_out, int32_t* topk_idx, float* topk_w,

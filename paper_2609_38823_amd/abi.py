@@ -30,7 +30,8 @@ EXPORTS = ("moe_status_string", "moe_workspace_size", "moe_route", "moe_route_pa
            "moe_savb_workspace_size", "moe_savb_gate", "drop_visual_block_if",
            "moe_expand_dense_routing", "moe_ffn_status", "moe_expert_ffn_packed_gather_noalloc",
            "moe_route_packed_if", "moe_calibrate_route_prefix_if", "moe_dispatch_if",
-           "moe_expert_ffn_packed_gather_if", "moe_combine_residual_if", "moe_savb_gate_if")
+           "moe_expert_ffn_packed_gather_if", "moe_combine_residual_if", "moe_savb_gate_if",
+           "moe_route_rcep", "moe_route_rcep_if")
 
 # size of the library's own scratch array of the allocation-free expert FFN
 NOALLOC_SCRATCH_BYTES = 32 << 20
@@ -80,6 +81,10 @@ def load() -> ctypes.CDLL:
         "drop_visual_block_if": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P]),
         "moe_expand_dense_routing": (_I, [_P, _P, _I, _I, _I, _P, _P, _P, _P]),
         "moe_ffn_status": (_I, [_P, _S, _P, _P]),
+        "moe_route_rcep": (_I, [_P, _I, _P, _P, _I, _I, _I, _I, _D, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                _P, _S, _P]),
+        "moe_route_rcep_if": (_I, [_P, _I, _P, _P, _I, _I, _I, _I, _D, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                   _P, _P, _S, _P, _I, _I, _P]),
         "moe_route_packed_if": (_I, [_P, _I, _P, _P, _I, _I, _I, _I, _P, _I, _P, _P, _P, _P, _P, _S,
                                      _P, _I, _I, _P]),
         "moe_calibrate_route_prefix_if": (_I, [_P, _P, _P, _I, _I, _I, _D, _P, _P, _P, _P, _P, _S,
@@ -424,3 +429,26 @@ def moe_savb_gate_if(text_rows, w1, b1, w2, b2, theta, p_exit, exit_flag, ws, gu
         _p(text_rows), _dt(text_rows), n, d, _f32(w1), _f32(b1), hid, _f32(w2), _f32(b2), float(theta),
         _f32(feature), _f32(p_exit), _i32(exit_flag), _p(ws), _nbytes(ws), gp, lo, hi, _i32(exit_layer),
         int(layer), _stream(stream)))
+
+
+def moe_route_rcep(x, w_r_packed, bias, k, p, logits, idx_full, w_full, mass, K_out, idx, w, counts, offsets,
+                   src_of_row, row_of_slot, ws, guard=None, stream=None):
+    """The RCEP routing of one invocation through the dispatch grouping:
+    moe_route_packed + moe_calibrate_route_prefix + moe_dispatch(x=None).
+    With ``guard`` = (g, lo, hi) the predicated form (moe_route_rcep_if)."""
+    T, d = x.shape
+    E = logits.shape[1]
+    args = (_p(x), _dt(x), _p(w_r_packed), _f32(bias), T, d, E, k, float(p), _f32(logits), _i32(idx_full),
+            _f32(w_full), _f64(mass), _i32(K_out), _i32(idx), _f32(w), _i32(counts), _i32(offsets),
+            _i32(src_of_row), _i32(row_of_slot), _p(ws), _nbytes(ws))
+    if guard is None:
+        _check("moe_route_rcep", load().moe_route_rcep(*args, _stream(stream)))
+    else:
+        gp, lo, hi = _guard(guard)
+        _check("moe_route_rcep_if", load().moe_route_rcep_if(*args, gp, lo, hi, _stream(stream)))
+
+
+def moe_route_rcep_if(x, w_r_packed, bias, k, p, logits, idx_full, w_full, mass, K_out, idx, w, counts,
+                      offsets, src_of_row, row_of_slot, ws, guard, stream=None):
+    moe_route_rcep(x, w_r_packed, bias, k, p, logits, idx_full, w_full, mass, K_out, idx, w, counts, offsets,
+                   src_of_row, row_of_slot, ws, guard=guard, stream=stream)

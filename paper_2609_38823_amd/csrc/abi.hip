@@ -113,6 +113,7 @@ size_t moe_workspace_size(int T, int E, int k, int d, int m, int n_seg) {
   for (size_t b : {a256(dispatch_ws_bytes(T, k, E)), ffn_ws_bytes(true, (int)rows, E, d, m),
                    ffn_ws_bytes(false, (int)rows, E, d, m), a256(route_ws_bytes(T, d, E)),
                    a256(router_packable(d, E) ? decomoe::route_x3_ws_bytes(T, d, E) : 0),
+                   a256(router_packable(d, E) && T > 0 ? decomoe::route_rcep_ws_bytes(T, d, E, k) : 0),
                    a256(calibrate_ws_bytes(T, E))})
     w = b > w ? b : w;
   return w;
@@ -317,6 +318,76 @@ int dispatch(const int32_t* topk_idx, int T, int k, int E, const void* x, moe_dt
 }  // namespace
 
 extern "C" {
+
+}  // extern "C"
+
+namespace {
+// moe_route_packed (full pool) + moe_calibrate_route_prefix +
+// moe_dispatch (x = NULL) of one invocation
+int route_rcep(const void* x, moe_dtype dtype, const void* w_r_packed, const float* bias, int T, int d,
+               int E, int k, double p, float* logits, int32_t* idx_full, float* w_full, double* mass,
+               int32_t* K_out, int32_t* idx, float* w, int32_t* counts, int32_t* offsets,
+               int32_t* src_of_row, int32_t* row_of_slot, void* ws, size_t ws_bytes, hipStream_t stream,
+               decomoe::Guard g) {
+  if (!valid_dtype(dtype) || T < 0 || d < 1 || E < 1 || E > kMaxE || k < 1 || k > E) return MOE_EINVAL;
+  if (dtype != MOE_BF16 || !router_packable(d, E)) return MOE_EUNSUPPORTED;
+  if (k > kMaxK) return MOE_EUNSUPPORTED;
+  if ((size_t)T * k > (size_t)INT32_MAX) return MOE_EUNSUPPORTED;
+  if (!(p > 0.0 && p <= 1.0)) return MOE_EINVAL;
+  if (!mass || !K_out || !counts || !offsets) return MOE_EINVAL;
+  if (T > 0 && (!x || !w_r_packed || !logits || !idx_full || !w_full || !idx || !w || !src_of_row ||
+                !row_of_slot))
+    return MOE_EINVAL;
+  if (!aligned_all({x, w_r_packed, bias, logits, idx_full, w_full, mass, K_out, idx, w, counts, offsets,
+                    src_of_row, row_of_slot, ws}))
+    return MOE_EINVAL;
+  const size_t need = T > 0 ? decomoe::route_rcep_ws_bytes(T, d, E, k) : 0;
+  if (need && (!ws || ws_bytes < need)) return MOE_EWORKSPACE;
+  const size_t A = (size_t)T * k, nl = (size_t)T * E * 4;
+  if (any_alias({rng(logits, nl), rng(idx_full, A * 4), rng(w_full, A * 4), rng(mass, (size_t)E * 8),
+                 rng(K_out, 4), rng(idx, A * 4), rng(w, A * 4), rng(counts, (size_t)E * 4),
+                 rng(offsets, (size_t)(E + 1) * 4), rng(src_of_row, A * 4), rng(row_of_slot, A * 4),
+                 need ? rng(ws, need) : Range{0, 0}},
+                {rng(x, (size_t)T * d * 2), rng(w_r_packed, (size_t)d * E * 6),
+                 bias ? rng(bias, (size_t)E * 4) : Range{0, 0}}))
+    return MOE_EALIAS;
+  if (T == 0) {  // an empty invocation: K = k, no rows
+    hipError_t e = decomoe::launch_calibrate_route(logits, idx_full, w_full, 0, E, k, p, mass, K_out, idx,
+                                                   w, stream, g);
+    if (e == hipSuccess)
+      e = decomoe::launch_dispatch(idx, 0, k, E, nullptr, 2, 0, counts, offsets, src_of_row, row_of_slot,
+                                   nullptr, ws, stream, g);
+    return hip_status(e);
+  }
+  return hip_status(decomoe::launch_route_rcep(x, w_r_packed, bias, T, d, E, k, p, logits, idx_full, w_full,
+                                               mass, K_out, idx, w, counts, offsets, src_of_row, row_of_slot,
+                                               ws, stream, g));
+}
+}  // namespace
+
+extern "C" {
+
+int moe_route_rcep(const void* x, moe_dtype dtype, const void* w_r_packed, const float* bias, int T, int d,
+                   int E, int k, double p, float* logits, int32_t* topk_idx_full, float* topk_w_full,
+                   double* mass, int32_t* K_out, int32_t* topk_idx, float* topk_w, int32_t* counts,
+                   int32_t* offsets, int32_t* src_of_row, int32_t* row_of_slot, void* ws, size_t ws_bytes,
+                   hipStream_t stream) {
+  return route_rcep(x, dtype, w_r_packed, bias, T, d, E, k, p, logits, topk_idx_full, topk_w_full, mass,
+                    K_out, topk_idx, topk_w, counts, offsets, src_of_row, row_of_slot, ws, ws_bytes, stream,
+                    decomoe::Guard{});
+}
+
+int moe_route_rcep_if(const void* x, moe_dtype dtype, const void* w_r_packed, const float* bias, int T,
+                      int d, int E, int k, double p, float* logits, int32_t* topk_idx_full,
+                      float* topk_w_full, double* mass, int32_t* K_out, int32_t* topk_idx, float* topk_w,
+                      int32_t* counts, int32_t* offsets, int32_t* src_of_row, int32_t* row_of_slot,
+                      void* ws, size_t ws_bytes, const int32_t* guard, int guard_lo, int guard_hi,
+                      hipStream_t stream) {
+  if (!guard_ok(guard)) return MOE_EINVAL;
+  return route_rcep(x, dtype, w_r_packed, bias, T, d, E, k, p, logits, topk_idx_full, topk_w_full, mass,
+                    K_out, topk_idx, topk_w, counts, offsets, src_of_row, row_of_slot, ws, ws_bytes, stream,
+                    decomoe::Guard{guard, guard_lo, guard_hi});
+}
 
 int moe_dispatch(const int32_t* topk_idx, int T, int k, int E, const void* x, moe_dtype dtype,
                  int d, int32_t* counts, int32_t* offsets, int32_t* src_of_row,

@@ -57,7 +57,8 @@ size_t route_ws_bytes(int T, int d, int E);
 hipError_t launch_route(const void* x, bool x_bf16, const float* w_r, const void* w_r_packed,
                         const float* bias, int T, int d, int E, int k, const int32_t* seg_offsets,
                         int n_seg, const int32_t* K_dev, float* logits, int32_t* idx, float* w,
-                        void* ws, hipStream_t s, Guard g = Guard{});
+                        void* ws, hipStream_t s, Guard g = Guard{}, int* ctr_zero = nullptr);
+// (ctr_zero: an int the Top-k launch sets to 0, for a launch that follows)
 // bf16 x (three-term split router weights): packing and the logits kernel;
 // `part`/`S` receive the split partials the Top-k kernel has to add
 size_t route_x3_ws_bytes(int T, int d, int E);
@@ -70,11 +71,31 @@ hipError_t launch_calibrate(const int32_t* idx, const float* w, int T, int E, in
                             const int32_t* seg_offsets, int n_seg, double p, double* mass,
                             int32_t* K_out, int32_t* order, void* ws, hipStream_t s, Guard g = Guard{});
 // calibration (one segment) and prefix re-route in one launch when
-// calibrate_route_fused(T, E, k), else the two launches
+// calibrate_route_fused(T, E, k), else the two launches.  `sort` (one-launch
+// path only): the same launch also groups the re-routed entries by expert;
+// ctr must be 0 when it runs
+struct SortOut {
+  int32_t* counts = nullptr;
+  int32_t* offsets = nullptr;
+  int32_t* src_of_row = nullptr;
+  int32_t* row_of_slot = nullptr;
+  int* ctr = nullptr;
+};
 bool calibrate_route_fused(int T, int E, int k);
 hipError_t launch_calibrate_route(const float* logits, const int32_t* idx_full, const float* w_full,
                                   int T, int E, int k, double p, double* mass, int32_t* K_out,
-                                  int32_t* idx, float* w, hipStream_t s, Guard g = Guard{});
+                                  int32_t* idx, float* w, hipStream_t s, Guard g = Guard{},
+                                  const SortOut* sort = nullptr);
+// RCEP routing of one invocation through the dispatch grouping: the split
+// router and Top-k, then calibration, re-route and grouping in one launch
+// when route_rcep_fused(T, E, k), else route, calibrate_route and dispatch
+bool route_rcep_fused(int T, int E, int k);
+size_t route_rcep_ws_bytes(int T, int d, int E, int k);
+hipError_t launch_route_rcep(const void* x, const void* w_r_packed, const float* bias, int T, int d, int E,
+                             int k, double p, float* logits, int32_t* idx_full, float* w_full, double* mass,
+                             int32_t* K_out, int32_t* idx, float* w, int32_t* counts, int32_t* offsets,
+                             int32_t* src_of_row, int32_t* row_of_slot, void* ws, hipStream_t s,
+                             Guard g = Guard{});
 size_t dispatch_ws_bytes(int T, int k, int E);
 hipError_t launch_dispatch(const int32_t* idx, int T, int k, int E, const void* x, int elt, int d,
                            int32_t* counts, int32_t* offsets, int32_t* src_of_row,

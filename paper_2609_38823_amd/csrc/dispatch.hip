@@ -15,6 +15,7 @@
 // to 64 chunks, steps 2 and 3 run in one launch (every rank workgroup
 // re-derives the totals and its chunk's bases from the histograms).
 #include "common.hpp"
+#include "sort_dev.hpp"
 
 namespace decomoe {
 namespace {
@@ -261,10 +262,6 @@ __global__ __launch_bounds__(DP_THREADS) void dispatch_rank_kernel(
 // expert, and the wavefronts rank their slices with the ballot scheme
 // above.  Same result as the multi-workgroup path (a stable sort).
 // ---------------------------------------------------------------------------
-constexpr int DS_THREADS = 1024;
-constexpr int DS_WAVES = DS_THREADS / kWave;
-constexpr int DS_MAX = 8192;  // beyond this the multi-workgroup path is faster
-
 __global__ __launch_bounds__(DS_THREADS) void dispatch_sort_small_kernel(
     const int32_t* __restrict__ idx, int A, int E, int key_bits, int32_t* __restrict__ counts,
     int32_t* __restrict__ offsets, int32_t* __restrict__ src_of_row,
@@ -272,66 +269,7 @@ __global__ __launch_bounds__(DS_THREADS) void dispatch_sort_small_kernel(
   if (guard_skip(g)) return;
   __shared__ int wh[DS_WAVES][1024];  // per-wave counts, then per-wave starting rows
   __shared__ int part[DS_WAVES];
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int per = (A + DS_WAVES - 1) / DS_WAVES;
-  const int lo = min(A, wv * per), hi = min(A, lo + per);
-  for (int i = tid; i < DS_WAVES * 1024; i += DS_THREADS) (&wh[0][0])[i] = 0;
-  __syncthreads();
-  for (int a = lo + lane; a < hi; a += kWave) {
-    const int e = idx[a];
-    if (e >= 0 && e < E) atomicAdd(&wh[wv][e], 1);
-  }
-  __syncthreads();
-  // thread e: total count, then an exclusive scan over the experts
-  int cnt = 0;
-  if (tid < E)
-#pragma unroll
-    for (int w = 0; w < DS_WAVES; ++w) cnt += wh[w][tid];
-  int incl = cnt;
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const int y = __shfl_up(incl, off, kWave);
-    if (lane >= off) incl += y;
-  }
-  if (lane == kWave - 1) part[wv] = incl;
-  __syncthreads();
-  int base = 0;
-  for (int w = 0; w < wv; ++w) base += part[w];
-  if (tid < E) {
-    int r = base + incl - cnt;  // exclusive offset of expert tid
-    counts[tid] = cnt;
-    offsets[tid] = r;
-    if (tid == E - 1) offsets[E] = r + cnt;
-#pragma unroll
-    for (int w = 0; w < DS_WAVES; ++w) {
-      const int c = wh[w][tid];
-      wh[w][tid] = r;
-      r += c;
-    }
-  }
-  __syncthreads();
-  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  for (int a0 = lo; a0 < hi; a0 += kWave) {
-    const int a = a0 + lane;
-    const int e = a < hi ? idx[a] : -1;
-    const bool valid = e >= 0 && e < E;
-    uint64_t peers = __ballot(valid);
-#pragma unroll 1
-    for (int b = 0; b < key_bits; ++b) {
-      const bool bit = (e >> b) & 1;
-      const uint64_t msk = __ballot(bit);
-      peers &= bit ? msk : ~msk;
-    }
-    if (valid) {
-      const int r = wh[wv][e] + __popcll(peers & lt_mask);
-      src_of_row[r] = a;
-      row_of_slot[a] = r;
-      if ((63 - __clzll(peers)) == lane) wh[wv][e] += __popcll(peers);
-    } else if (a < hi) {
-      row_of_slot[a] = -1;
-    }
-    __builtin_amdgcn_wave_barrier();
-  }
+  sort_small(idx, A, E, key_bits, &wh[0][0], 1024, part, counts, offsets, src_of_row, row_of_slot);
 }
 
 // token-major gather: each token row is read once (VEC-sized vectors, rows

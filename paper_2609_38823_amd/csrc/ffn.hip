@@ -827,23 +827,24 @@ __device__ XcdRange plan_tiles(const Tiles& tl, int xcc, int n_xcc, int* tstart,
   int& s_klim = part[2 * NW];
   int& s_a0 = part[2 * NW + 1];
   int& s_a1 = part[2 * NW + 2];
-  if (tid == 0) s_klim = 0;
-  __syncthreads();
-  if (tl.K_dev) {
-    int mx = 0;
+  // the prefix lengths and the expert offsets are loaded together, before
+  // the first barrier (their latencies overlap)
+  int mx = 0;
+  if (tl.K_dev)
     for (int i = tid; i < tl.n_K; i += NTHR) mx = max(mx, tl.K_dev[i]);
-    if (mx > 0) atomicMax(&s_klim, mx);
-  }
-  int rows[4];
+  // offsets[4 tid .. 4 tid + 4], indices clamped to E (E <= 4 NTHR): five
+  // loads without a branch between them
+  int ofs[5], rows[4];
+#pragma unroll
+  for (int q = 0; q < 5; ++q) ofs[q] = tl.offsets[min(4 * tid + q, tl.E)];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const int e = 4 * tid + q;
-    rows[q] = 0;
-    if (e < tl.E) {
-      const int lo = clampi(tl.offsets[e], 0, tl.rows_max);
-      rows[q] = clampi(tl.offsets[e + 1], lo, tl.rows_max) - lo;
-    }
+    const int lo = clampi(ofs[q], 0, tl.rows_max);
+    rows[q] = 4 * tid + q < tl.E ? clampi(ofs[q + 1], lo, tl.rows_max) - lo : 0;
   }
+  if (tid == 0) s_klim = 0;
+  __syncthreads();
+  if (tl.K_dev && mx > 0) atomicMax(&s_klim, mx);
   __syncthreads();
   const int Klim = tl.K_dev ? clampi(s_klim, tl.kmin, tl.E) : tl.E;
   constexpr int FULL = 4;  // + BM / 32 below

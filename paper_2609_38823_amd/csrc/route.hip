@@ -3,6 +3,7 @@
 #include "common.hpp"
 #include "mass_dev.hpp"
 #include "topk_dev.hpp"
+#include "sort_dev.hpp"
 
 #include <float.h>
 
@@ -197,8 +198,9 @@ __global__ __launch_bounds__(256) void topk_kernel(float* __restrict__ logits, i
                                                    int n_seg, const int32_t* __restrict__ K_dev,
                                                    const float* __restrict__ part, int S,
                                                    const float* __restrict__ bias,
-                                                   int32_t* __restrict__ idx, float* __restrict__ w, const Guard g) {
+                                                   int32_t* __restrict__ idx, float* __restrict__ w, int* __restrict__ ctr_zero, const Guard g) {
   if (guard_skip(g)) return;
+  if (ctr_zero && blockIdx.x == 0 && threadIdx.x == 0) *ctr_zero = 0;
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;  // whole wavefront leaves together; no block barrier below
@@ -280,8 +282,9 @@ __global__ __launch_bounds__(256) void topk_row_kernel(float* __restrict__ logit
                                                        int n_seg, const int32_t* __restrict__ K_dev,
                                                        const float* __restrict__ part, int S,
                                                        const float* __restrict__ bias,
-                                                       int32_t* __restrict__ idx, float* __restrict__ w, const Guard g) {
+                                                       int32_t* __restrict__ idx, float* __restrict__ w, int* __restrict__ ctr_zero, const Guard g) {
   if (guard_skip(g)) return;
+  if (ctr_zero && blockIdx.x == 0 && threadIdx.x == 0) *ctr_zero = 0;
   const int j = threadIdx.x & 15;
   const int t = blockIdx.x * 16 + (threadIdx.x >> 4);
   if (t >= T) return;  // the whole row of 16 lanes leaves together
@@ -339,17 +342,30 @@ __global__ __launch_bounds__(256) void topk_row_kernel(float* __restrict__ logit
 // K itself -- the same float64 sums as segment_mass_kernel (mass_sorted,
 // prefix_K), over at most CAL_STAGE routing entries -- so no second launch
 // waits for one workgroup's result; workgroup 0 writes mass and K.  Then
-// wavefront w of workgroup b re-routes the tokens 16 b + w, 16 (b + grid) +
-// w, ... inside [0, K) exactly as topk_kernel does (topk_select).
+// workgroup b re-routes the tokens 16 b .. 16 b + 15 (stride 16 x grid)
+// inside [0, K) with the selection of topk_kernel: for k <= 16 and E <= 16
+// RMAXC one row of 16 lanes per token in wavefronts 0-3 (row_topk_select,
+// bitwise the same slots and weights), else one wavefront per token
+// (topk_select).
+//
+// With `ctr` (a counter that the Top-k launch before this one zeroed), the
+// re-routed entries are also grouped by expert (Algorithm 2's dispatch,
+// x = NULL): every workgroup publishes its entries and counts itself done;
+// the last one to finish sorts all T k entries (sort_small), so no launch
+// follows for the grouping.
 // ---------------------------------------------------------------------------
-template <int MAXC>
+template <int MAXC, int RMAXC>
 __global__ __launch_bounds__(CAL_THREADS) void calibrate_route_kernel(
     const float* __restrict__ logits, const int32_t* __restrict__ idx_full,
     const float* __restrict__ w_full, int T, int E, int k, int key_bits, double p,
     double* __restrict__ mass, int32_t* __restrict__ K_out, int32_t* __restrict__ idx,
-    float* __restrict__ w, const Guard g) {
+    float* __restrict__ w, int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
+    int32_t* __restrict__ src_of_row, int32_t* __restrict__ row_of_slot, int* __restrict__ ctr,
+    const Guard g) {
+  static_assert(CAL_THREADS == DS_THREADS && CAL_WAVES == DS_WAVES, "the grouping runs on this workgroup");
   if (guard_skip(g)) return;
   __shared__ CalLds L;
+  __shared__ int s_last;
   const double a = mass_sorted(idx_full, w_full, 0, T * k, E, key_bits, L);
   const int K = prefix_K(E, k, p, L);
   const int tid = threadIdx.x;
@@ -357,11 +373,47 @@ __global__ __launch_bounds__(CAL_THREADS) void calibrate_route_kernel(
     if (tid < E) mass[tid] = a;
     if (tid == 0) K_out[0] = K;
   }
-  const int lane = tid & 63;
   const int Klim = clampi(K, k, E);
-  for (int t = blockIdx.x * CAL_WAVES + (tid >> 6); t < T; t += gridDim.x * CAL_WAVES)
-    topk_select<MAXC>(logits + (size_t)t * E, E, k, Klim, lane, idx + (size_t)t * k, w + (size_t)t * k);
+  constexpr int RM = RMAXC > 0 ? RMAXC : 1;
+  if (RMAXC > 0 && k <= 16 && E <= 16 * RMAXC) {
+    if (tid < 256) {
+      const int j = tid & 15;
+      for (int t = blockIdx.x * 16 + (tid >> 4); t < T; t += gridDim.x * 16) {
+        const float* row = logits + (size_t)t * E;
+        float v[RM];
+#pragma unroll
+        for (int c = 0; c < RM; ++c) {
+          const int e = j + 16 * c;
+          v[c] = e < Klim ? row[e] : 0.f;
+        }
+        row_topk_select<RM>(v, j, E, k, Klim, idx + (size_t)t * k, w + (size_t)t * k);
+      }
+    }
+  } else {
+    const int lane = tid & 63;
+    for (int t = blockIdx.x * CAL_WAVES + (tid >> 6); t < T; t += gridDim.x * CAL_WAVES)
+      topk_select<MAXC>(logits + (size_t)t * E, E, k, Klim, lane, idx + (size_t)t * k, w + (size_t)t * k);
+  }
+  if (!ctr) return;
+  // every wavefront's entries have reached the cache (vmcnt 0) before the
+  // barrier; then one thread per workgroup makes them visible device-wide
+  // (release fence) and counts the workgroup done; the last one acquires
+  // every workgroup's entries for the sort
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0) (gfx9 encoding; expcnt, lgkmcnt not waited)
+  __syncthreads();
+  if (tid == 0) {
+    __threadfence();
+    const bool last = __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                      (int)gridDim.x - 1;
+    if (last) __threadfence();
+    s_last = last;
+  }
+  __syncthreads();
+  if (!s_last) return;
+  sort_small(idx, T * k, E, key_bits, reinterpret_cast<int*>(L.table), E, L.part, counts, offsets, src_of_row,
+             row_of_slot);
 }
+
 }  // namespace
 
 bool calibrate_route_fused(int T, int E, int k) {
@@ -370,8 +422,9 @@ bool calibrate_route_fused(int T, int E, int k) {
 
 hipError_t launch_calibrate_route(const float* logits, const int32_t* idx_full, const float* w_full,
                                   int T, int E, int k, double p, double* mass, int32_t* K_out,
-                                  int32_t* idx, float* w, hipStream_t s, Guard g) {
+                                  int32_t* idx, float* w, hipStream_t s, Guard g, const SortOut* sort) {
   if (!calibrate_route_fused(T, E, k)) {
+    if (sort) return hipErrorInvalidValue;  // the grouping needs the one-launch path
     hipError_t err = launch_calibrate(idx_full, w_full, T, E, k, nullptr, 1, p, mass, K_out, nullptr,
                                       nullptr, s, g);
     if (err != hipSuccess || T == 0) return err;
@@ -381,17 +434,55 @@ hipError_t launch_calibrate_route(const float* logits, const int32_t* idx_full, 
   }
   int key_bits = 0;
   while ((1 << key_bits) < E) ++key_bits;
-  const unsigned grid = (unsigned)((T + CAL_WAVES - 1) / CAL_WAVES);
+  const unsigned grid = (unsigned)((T + 15) / 16);
+  const SortOut so = sort ? *sort : SortOut{};
+#define CAL_ROUTE_ARGS                                                                                      \
+  logits, idx_full, w_full, T, E, k, key_bits, p, mass, K_out, idx, w, so.counts, so.offsets, so.src_of_row, \
+      so.row_of_slot, so.ctr, g
   if (E <= 128)
-    calibrate_route_kernel<2><<<grid, CAL_THREADS, 0, s>>>(logits, idx_full, w_full, T, E, k, key_bits, p,
-                                                           mass, K_out, idx, w, g);
+    calibrate_route_kernel<2, 8><<<grid, CAL_THREADS, 0, s>>>(CAL_ROUTE_ARGS);
   else if (E <= 256)
-    calibrate_route_kernel<4><<<grid, CAL_THREADS, 0, s>>>(logits, idx_full, w_full, T, E, k, key_bits, p,
-                                                           mass, K_out, idx, w, g);
+    calibrate_route_kernel<4, 16><<<grid, CAL_THREADS, 0, s>>>(CAL_ROUTE_ARGS);
   else
-    calibrate_route_kernel<8><<<grid, CAL_THREADS, 0, s>>>(logits, idx_full, w_full, T, E, k, key_bits, p,
-                                                           mass, K_out, idx, w, g);
+    calibrate_route_kernel<8, 0><<<grid, CAL_THREADS, 0, s>>>(CAL_ROUTE_ARGS);
+#undef CAL_ROUTE_ARGS
   return hipGetLastError();
+}
+
+bool route_rcep_fused(int T, int E, int k) {
+  return calibrate_route_fused(T, E, k) && (size_t)T * k <= (size_t)DS_MAX && E <= DS_THREADS;
+}
+
+size_t route_rcep_ws_bytes(int T, int d, int E, int k) {
+  if (!route_rcep_fused(T, E, k)) {
+    const size_t a = route_x3_ws_bytes(T, d, E), b = dispatch_ws_bytes(T, k, E);
+    return a > b ? a : b;
+  }
+  return (route_x3_ws_bytes(T, d, E) + 255) / 256 * 256 + 256;  // + the completion counter
+}
+
+hipError_t launch_route_rcep(const void* x, const void* w_r_packed, const float* bias, int T, int d, int E,
+                             int k, double p, float* logits, int32_t* idx_full, float* w_full, double* mass,
+                             int32_t* K_out, int32_t* idx, float* w, int32_t* counts, int32_t* offsets,
+                             int32_t* src_of_row, int32_t* row_of_slot, void* ws, hipStream_t s, Guard g) {
+  if (!route_rcep_fused(T, E, k)) {
+    hipError_t err = launch_route(x, true, nullptr, w_r_packed, bias, T, d, E, k, nullptr, 1, nullptr, logits,
+                                  idx_full, w_full, ws, s, g);
+    if (err == hipSuccess)
+      err = launch_calibrate_route(logits, idx_full, w_full, T, E, k, p, mass, K_out, idx, w, s, g);
+    if (err == hipSuccess)
+      err = launch_dispatch(idx, T, k, E, nullptr, 2, 0, counts, offsets, src_of_row, row_of_slot, nullptr, ws,
+                            s, g);
+    return err;
+  }
+  // the counter sits past the router's partial sums (which the Top-k launch
+  // reads while its first workgroup zeroes the counter)
+  int* ctr = reinterpret_cast<int*>(static_cast<char*>(ws) + (route_x3_ws_bytes(T, d, E) + 255) / 256 * 256);
+  hipError_t err = launch_route(x, true, nullptr, w_r_packed, bias, T, d, E, k, nullptr, 1, nullptr, logits,
+                                idx_full, w_full, ws, s, g, ctr);
+  if (err != hipSuccess) return err;
+  const SortOut so{counts, offsets, src_of_row, row_of_slot, ctr};
+  return launch_calibrate_route(logits, idx_full, w_full, T, E, k, p, mass, K_out, idx, w, s, g, &so);
 }
 
 // Split factor of the router's d-range: enough workgroups to cover the chip
@@ -412,7 +503,7 @@ size_t route_ws_bytes(int T, int d, int E) {
 hipError_t launch_route(const void* x, bool x_bf16, const float* w_r, const void* w_r_packed,
                         const float* bias, int T, int d, int E, int k, const int32_t* seg_offsets,
                         int n_seg, const int32_t* K_dev, float* logits, int32_t* idx, float* w,
-                        void* ws, hipStream_t s, Guard g) {
+                        void* ws, hipStream_t s, Guard g, int* ctr_zero) {
   float* part = nullptr;
   int S = 1;
   if (x && w_r_packed) {
@@ -442,16 +533,16 @@ hipError_t launch_route(const void* x, bool x_bf16, const float* w_r, const void
   const int blocks = (T + 3) / 4, rblocks = (T + 15) / 16;
   const bool rows = T >= 16384;
   if (E <= 128 && rows)
-    topk_row_kernel<8><<<rblocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w, g);
+    topk_row_kernel<8><<<rblocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w, ctr_zero, g);
   else if (E <= 128)
-    topk_kernel<2><<<blocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w, g);
+    topk_kernel<2><<<blocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w, ctr_zero, g);
   else if (E <= 256 && rows)
-    topk_row_kernel<16><<<rblocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w, g);
+    topk_row_kernel<16><<<rblocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w, ctr_zero, g);
   else if (E <= 256)
-    topk_kernel<4><<<blocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w, g);
+    topk_kernel<4><<<blocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w, ctr_zero, g);
   else
     topk_kernel<TK_MAXC><<<blocks, 256, 0, s>>>(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias,
-                                                idx, w, g);
+                                                idx, w, ctr_zero, g);
   return hipGetLastError();
 }
 

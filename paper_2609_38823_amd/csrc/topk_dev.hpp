@@ -11,8 +11,13 @@
 namespace decomoe {
 namespace {
 
+// (ov, oi) replaces (v, i) when its value is larger, or equal with a smaller
+// index; evaluated without short-circuit so that it compiles to compares and
+// selects (no exec-mask branches)
 __device__ __forceinline__ void better(float& v, int& i, float ov, int oi) {
-  if (ov > v || (ov == v && oi < i)) { v = ov; i = oi; }
+  const bool take = (ov > v) | ((ov == v) & (oi < i));
+  v = take ? ov : v;
+  i = take ? oi : i;
 }
 
 // (value, index) of lane l -> the wavefront's best pair in every lane
@@ -57,17 +62,19 @@ __device__ __forceinline__ float wave_sum(float v) {
 // holds experts l, l + 64, ... in vals[c] (expert l + 64 c); k rounds of a
 // wavefront arg-max (value descending, index ascending on ties) pick the
 // slots in order; the weights are the softmax of the k selected logits.
-// Lane r < k writes slot r.  Values at experts >= Klim are never read.
+// Lane r < k writes slot r.  Values at experts >= Klim are never selected.
 template <int MAXC>  // values per lane: E <= 64 MAXC
 __device__ __forceinline__ void topk_select_vals(const float (&vals)[MAXC], int E, int k, int Klim, int lane,
                                                  int32_t* idx_t, float* w_t) {
+  // a taken or absent candidate is (-inf, INT_MAX): `better` never prefers
+  // it, so the rounds need no per-candidate branches
   float v[MAXC];
-  uint32_t alive = 0;
+  int ix[MAXC];
 #pragma unroll
   for (int c = 0; c < MAXC; ++c) {
-    int e = lane + c * 64;
-    v[c] = -FLT_MAX;
-    if (e < Klim) { v[c] = vals[c]; alive |= 1u << c; }
+    const int e = lane + c * 64;
+    v[c] = e < Klim ? vals[c] : -INFINITY;
+    ix[c] = e < Klim ? e : 0x7fffffff;
   }
   float my_v = 0.f;
   int my_i = 0;
@@ -75,10 +82,14 @@ __device__ __forceinline__ void topk_select_vals(const float (&vals)[MAXC], int 
     float bv = -INFINITY;
     int bi = 0x7fffffff;
 #pragma unroll
-    for (int c = 0; c < MAXC; ++c)
-      if (alive & (1u << c)) better(bv, bi, v[c], lane + c * 64);
+    for (int c = 0; c < MAXC; ++c) better(bv, bi, v[c], ix[c]);
     wave_best(bv, bi);
-    if (bi < E && (bi & 63) == lane) alive &= ~(1u << (bi >> 6));
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c)
+      if (ix[c] == bi) {
+        v[c] = -INFINITY;
+        ix[c] = 0x7fffffff;
+      }
     if (lane == r) { my_v = bv; my_i = bi; }
   }
   const float v0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_v), 0));
@@ -127,13 +138,19 @@ __device__ __forceinline__ float row_sum(float v) {
 // kept by lane r % 16 in slot r / 16 (k <= 32).  Same selection order, tie
 // rule and weights as topk_select_vals: the slots' exponentials are summed
 // by the same butterfly, so for k <= 16 the weights are bitwise equal.
-template <int MAXC>
-__device__ __forceinline__ void row_topk_select(const float (&v)[MAXC], int j, int E, int k, int Klim,
-                                                int32_t* idx_t, float* w_t) {
-  uint32_t alive = 0;
+template <int MAXC, typename Out>  // out(slot r, expert, weight) for r < k, by lane r % 16
+__device__ __forceinline__ void row_topk_select_to(const float (&v)[MAXC], int j, int E, int k, int Klim,
+                                                   Out out) {
+  // candidates as in topk_select_vals: a taken or absent one is (-inf,
+  // INT_MAX), which `better` never prefers
+  float cv[MAXC];
+  int ix[MAXC];
 #pragma unroll
-  for (int c = 0; c < MAXC; ++c)
-    if (j + 16 * c < Klim) alive |= 1u << c;
+  for (int c = 0; c < MAXC; ++c) {
+    const int e = j + 16 * c;
+    cv[c] = e < Klim ? v[c] : -INFINITY;
+    ix[c] = e < Klim ? e : 0x7fffffff;
+  }
   float my_v[2] = {0.f, 0.f};
   int my_i[2] = {0, 0};
   float v0 = 0.f;
@@ -141,10 +158,14 @@ __device__ __forceinline__ void row_topk_select(const float (&v)[MAXC], int j, i
     float bv = -INFINITY;
     int bi = 0x7fffffff;
 #pragma unroll
-    for (int c = 0; c < MAXC; ++c)
-      if (alive & (1u << c)) better(bv, bi, v[c], j + 16 * c);
+    for (int c = 0; c < MAXC; ++c) better(bv, bi, cv[c], ix[c]);
     row_best(bv, bi);
-    if (bi < E && (bi & 15) == j) alive &= ~(1u << (bi >> 4));
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c)
+      if (ix[c] == bi) {
+        cv[c] = -INFINITY;
+        ix[c] = 0x7fffffff;
+      }
     if (r == 0) v0 = bv;
     if ((r & 15) == j) {
       my_v[r >> 4] = bv;
@@ -160,11 +181,16 @@ __device__ __forceinline__ void row_topk_select(const float (&v)[MAXC], int j, i
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
     const int r = j + 16 * q;
-    if (r < k) {
-      idx_t[r] = my_i[q];
-      w_t[r] = ex[q] / sum;
-    }
+    if (r < k) out(r, my_i[q], ex[q] / sum);
   }
+}
+template <int MAXC>
+__device__ __forceinline__ void row_topk_select(const float (&v)[MAXC], int j, int E, int k, int Klim,
+                                                int32_t* idx_t, float* w_t) {
+  row_topk_select_to<MAXC>(v, j, E, k, Klim, [&](int r, int e, float wr) {
+    idx_t[r] = e;
+    w_t[r] = wr;
+  });
 }
 
 }  // namespace

@@ -184,12 +184,15 @@ class MoELayer:
     # With `residual`, the combine writes out = residual + MoE(x) into `out`
     # (default b.out); `out` may be `residual` itself (in-place hidden state).
     def _experts(self, x, b: Buffers, idx, w, K_dev=None, stream=None, mark=None, residual=None,
-                 out=None, guard=None):
+                 out=None, guard=None, dispatched=False):
+        """dispatch -> expert FFN -> combine; ``dispatched``: the grouping is
+        already in b (moe_route_rcep did it)."""
         mark = mark or (lambda: None)
         if guard is not None:
             # the same calls, each run only while the predicate holds
-            abi.moe_dispatch_if(idx, self.E, None, b.counts, b.offsets, b.src_of_row, b.row_of_slot, None,
-                                b.ws, guard, stream=stream)
+            if not dispatched:
+                abi.moe_dispatch_if(idx, self.E, None, b.counts, b.offsets, b.src_of_row, b.row_of_slot, None,
+                                    b.ws, guard, stream=stream)
             abi.moe_expert_ffn_packed_gather_if(x, idx.shape[1], b.src_of_row, b.offsets, self.w_gate_up,
                                                 self.w_down, b.y_perm, b.ws, guard, K_dev=K_dev,
                                                 stream=stream)
@@ -201,9 +204,10 @@ class MoELayer:
         if self.packed:
             # the expert GEMM reads the token rows through src_of_row: the
             # dispatch only groups the assignments
-            abi.moe_dispatch(idx, self.E, None, b.counts, b.offsets, b.src_of_row, b.row_of_slot,
-                             None, b.ws, stream=stream)
-            mark()
+            if not dispatched:
+                abi.moe_dispatch(idx, self.E, None, b.counts, b.offsets, b.src_of_row, b.row_of_slot,
+                                 None, b.ws, stream=stream)
+                mark()
             abi.moe_expert_ffn_packed_gather(x, idx.shape[1], b.src_of_row, b.offsets, self.w_gate_up,
                                              self.w_down, b.y_perm, b.ws, K_dev=K_dev, stream=stream)
         else:
@@ -274,15 +278,20 @@ class MoELayer:
         b = b or self.buffers(x.shape[0], n_seg)
         K = b.K if K_out is None else K_out
         mk = mark or (lambda: None)
-        self._route(x, b, b.idx_full, b.w_full, stream=stream, guard=guard)
-        mk()
-        if guard is not None:
-            if seg_offsets is not None:
-                raise ValueError("predicated RCEP layers take one invocation")
-            abi.moe_calibrate_route_prefix_if(b.logits, b.idx_full, b.w_full, p, b.mass, K, b.idx, b.w, guard,
-                                              stream=stream)
-            self._experts(x, b, b.idx, b.w, K_dev=K, stream=stream, residual=residual, out=out, guard=guard)
+        if seg_offsets is None and self.packed and self.w_r_packed is not None:
+            # one invocation on packed weights: routing, masses, K, the
+            # prefix re-route and the grouping in one call
+            abi.moe_route_rcep(x, self.w_r_packed, self.bias, self.k, p, b.logits, b.idx_full, b.w_full, b.mass,
+                               K, b.idx, b.w, b.counts, b.offsets, b.src_of_row, b.row_of_slot, b.ws,
+                               guard=guard, stream=stream)
+            mk()
+            self._experts(x, b, b.idx, b.w, K_dev=K, stream=stream, mark=mark, residual=residual, out=out,
+                          guard=guard, dispatched=True)
             return b
+        if guard is not None:
+            raise ValueError("predicated RCEP layers take one invocation on packed weights")
+        self._route(x, b, b.idx_full, b.w_full, stream=stream)
+        mk()
         if seg_offsets is None:
             # one invocation: masses, K and the prefix re-route in one call
             abi.moe_calibrate_route_prefix(b.logits, b.idx_full, b.w_full, p, b.mass, K, b.idx, b.w,

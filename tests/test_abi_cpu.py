@@ -36,7 +36,8 @@ def test_header_declares_the_boundary():
         "moe_expand_dense_routing", "moe_expert_ffn_packed_gather", "moe_calibrate_route_prefix",
         "moe_ffn_status", "moe_expert_ffn_packed_gather_noalloc",
         "moe_route_packed_if", "moe_calibrate_route_prefix_if", "moe_dispatch_if",
-        "moe_expert_ffn_packed_gather_if", "moe_combine_residual_if", "moe_savb_gate_if"])
+        "moe_expert_ffn_packed_gather_if", "moe_combine_residual_if", "moe_savb_gate_if",
+        "moe_route_rcep", "moe_route_rcep_if"])
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -276,6 +277,31 @@ def test_predicated_calls_check_like_the_plain_calls(lib):
     args = [P1, F32, 4, 64, P2, NULL, 8, P3, NULL, 0.5, NULL, P4, P5, ws, 1 << 20, G, 0, 1]
     assert gi(*args, P5, 3, NULL) == EALIAS
     assert gi(*args, bad, 3, NULL) == EINVAL
+
+
+def test_route_rcep_rejects(lib):
+    f = lib.moe_route_rcep
+    names = ["x", "dt", "wp", "b", "T", "d", "E", "k", "p", "lg", "if_", "wf", "ms", "K", "ix", "w", "cn", "of",
+             "sr", "rs", "ws", "wsb", "s"]
+    base = dict(zip(names, (P1, BF16, P2, NULL, 64, 256, 128, 8, 0.9, P3, P4, P5, P6, P7,
+                            ctypes.c_void_p(0x80000), ctypes.c_void_p(0x90000), ctypes.c_void_p(0xA0000),
+                            ctypes.c_void_p(0xB0000), ctypes.c_void_p(0xC0000), ctypes.c_void_p(0xD0000),
+                            ctypes.c_void_p(0x1000000), 1 << 30, NULL)))
+
+    def call(**kw):
+        a = dict(base)
+        a.update(kw)
+        return f(*[a[n] for n in names])
+
+    assert call(dt=F32) == EUNSUPPORTED
+    assert call(E=100) == EUNSUPPORTED       # not a multiple of 32 (packed router)
+    assert call(k=0) == EINVAL and call(k=129) == EINVAL
+    assert call(p=0.0) == EINVAL and call(p=1.5) == EINVAL
+    assert call(K=NULL) == EINVAL and call(ix=NULL) == EINVAL
+    assert call(wsb=16) == EWORKSPACE
+    assert call(ix=P4) == EALIAS              # re-routed indices on top of the full-pool ones
+    assert call(lg=P1) == EALIAS              # logits on top of x
+    assert call(sr=ctypes.c_void_p(0xC0002)) == EINVAL
 
 
 def test_ffn_status_rejects(lib):

@@ -467,6 +467,63 @@ def test_calibrate_route_prefix_matches_two_calls(T, E, k, p):
 
 
 # ---------------------------------------------------------------------------
+# moe_route_rcep: router, full-pool Top-k, masses, K, prefix re-route and
+# grouping of one invocation in one call, bitwise the separate calls
+# ---------------------------------------------------------------------------
+# up to 8192 entries: the router and Top-k, then calibration, re-route and
+# the grouping in one launch (the last workgroup to finish sorts; one
+# workgroup at 1 row, 64 at 1024); beyond: the separate launches
+@pytest.mark.parametrize("shape,T", [("qwen", 512), ("qwen", 64), ("qwen", 1), ("qwen", 1024),
+                                     ("qwen", 1025), ("qwen", 4096), ("e96", 333), ("d64", 50),
+                                     ("qwen", 0)])
+def test_route_rcep_matches_separate_calls(shape, T):
+    sh = {"qwen": I.QWEN3_VL_MOE, "e96": E96_BF16, "d64": D64_BF16}[shape]
+    E, k, p = sh.E, sh.k, 0.9
+    rp = I.router_params(sh, seed=9)
+    x = dev(I.tokens(sh, max(T, 1), seed=T + 2)[:T], torch.bfloat16)
+    wp = torch.empty((3 * sh.d * E,), dtype=torch.bfloat16, device="cuda")
+    abi.moe_pack_router(dev(rp["w_r"]), wp)
+    bias = dev(rp["bias"]) if rp["bias"] is not None else None
+    ws = ws_for(T, E, k, sh.d)
+    A = T * k
+
+    def outs():
+        return dict(logits=f32((T, E)), idx_full=i32((T, k)), w_full=f32((T, k)),
+                    mass=torch.full((1, E), -1.0, dtype=torch.float64, device="cuda"), K=i32((1,)),
+                    idx=i32((T, k)), w=f32((T, k)), counts=i32((E,)), offsets=i32((E + 1,)),
+                    src=i32((A,)), ros=i32((A,)))
+
+    a = outs()
+    if T:  # the router rejects an empty x without rows to route
+        abi.moe_route_packed(x, wp, bias, k, a["logits"], a["idx_full"], a["w_full"], ws=ws)
+    abi.moe_calibrate_route_prefix(a["logits"], a["idx_full"], a["w_full"], p, a["mass"], a["K"], a["idx"],
+                                   a["w"])
+    abi.moe_dispatch(a["idx"], E, None, a["counts"], a["offsets"], a["src"], a["ros"], None, ws)
+    b = outs()
+    abi.moe_route_rcep(x, wp, bias, k, p, b["logits"], b["idx_full"], b["w_full"], b["mass"], b["K"], b["idx"],
+                       b["w"], b["counts"], b["offsets"], b["src"], b["ros"], ws)
+    torch.cuda.synchronize()
+    for n in a:
+        assert torch.equal(a[n].view(torch.uint8), b[n].view(torch.uint8)), n
+    K = int(host(b["K"])[0])
+    if T == 0:
+        assert K == k and (host(b["counts"]) == 0).all() and (host(b["offsets"]) == 0).all()
+        return
+    # and against the oracle on the same logits (Eqs. 11, 12, Algorithm 1)
+    lg = host(b["logits"]).astype(np.float64)
+    s = oracle.activated_mass(host(b["idx_full"]), host(b["w_full"]).astype(np.float64), E)
+    assert K == int(oracle.prefix_length(s, p, k))
+    ref_idx, ref_w = oracle.prefix_route(lg, K, k)
+    np.testing.assert_array_equal(host(b["idx"]), ref_idx)
+    np.testing.assert_allclose(host(b["w"]), ref_w, rtol=2e-5, atol=1e-6)
+    rc, ro, rs, rr = oracle.dispatch(ref_idx, E)
+    np.testing.assert_array_equal(host(b["counts"]), rc)
+    np.testing.assert_array_equal(host(b["offsets"]), ro)
+    np.testing.assert_array_equal(host(b["src"]), rs)
+    np.testing.assert_array_equal(host(b["ros"]), rr)
+
+
+# ---------------------------------------------------------------------------
 # moe_dispatch: bit-exact counting sort and bitwise gather
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("T,E,k,d,dt,K", [
