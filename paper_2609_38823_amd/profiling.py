@@ -12,6 +12,7 @@ SQ_INSTS_VALU_MFMA_MOPS_BF16) gives the expert GEMM's MFMA work and
 busy cycles.
 
     python -m paper_2609_38823_amd.profiling FETCH_DIR WRITE_DIR OUT_PREFIX [MFMA_DIR]
+    python -m paper_2609_38823_amd.profiling trace TRACE_DIR PREFIX OUT HEADER...
 
 writes OUT_PREFIX.json (read by bench.py) and OUT_PREFIX.txt: the expert
 FFN's bytes per call and, per stage of the dense span at 4096 rows
@@ -88,11 +89,11 @@ N_XCC = 8
 
 # kernels of the dense span at 4096 rows (the --traffic-run layer call)
 STAGES = [
-    ("routing", [("router_x3_kernel<2>", None), ("topk_kernel<2>", 262144)]),
+    ("routing", [("router_x3_kernel<", None), ("topk_kernel<2>", 262144)]),
     ("dispatch", [("dispatch_hist_kernel", None), ("dispatch_scan_rank_kernel", None), ("dispatch_scan_kernel", None),
                   ("dispatch_rank_kernel", None)]),
-    ("expert FFN", [("clear_kernel", None), ("ffn_fused_kernel<128>", None)]),
-    ("combine", [("combine_kernel<true, false>", 1048576)]),
+    ("expert FFN", [("clear_kernel", None), ("ffn_fused_kernel<128", None)]),
+    ("combine", [("combine_kernel<true, false", 1048576)]),
 ]
 
 
@@ -176,7 +177,8 @@ def main(argv) -> int:
     with open(out + ".json", "w") as f:
         json.dump(res, f, indent=1)
     with open(out + ".txt", "w") as f:
-        f.write("# HBM traffic of moe_expert_ffn_packed_gather @ 4096 rows (Qwen3-VL-MoE layer), per call\n")
+        f.write("# L2<->fabric traffic (HBM plus memory-side cache hits) of moe_expert_ffn_packed_gather"
+                " @ 4096 rows (Qwen3-VL-MoE layer), per call\n")
         fd, wd = os.path.relpath(fetch_dir), os.path.relpath(write_dir)
         md = os.path.relpath(mfma_dir) if mfma_dir else None
         f.write("# commands (from the repository root R, one pass each):\n")
@@ -193,8 +195,8 @@ def main(argv) -> int:
                     f"  write {r['write_bytes'] / 1e6:9.1f} MB  (raw {r['fetch_kib_raw']:.0f} / "
                     f"{r['write_kib_raw']:.0f} KiB)\n")
         f.write(f"total per moe_expert_ffn_packed_gather call: {total / 1e6:.1f} MB\n")
-        f.write("\n# per stage of the dense span at 4096 rows: L2<->memory bytes (scaled), the dispatches'\n"
-                "# durations in the FETCH_SIZE run, achieved GB/s against 8 TB/s\n")
+        f.write("\n# per stage of the dense span at 4096 rows: L2<->fabric bytes (scaled), the dispatches'\n"
+                "# durations in the FETCH_SIZE run, achieved GB/s against the 8 TB/s HBM peak\n")
         for r in stages:
             f.write(f"{r['stage']:12s} read {r['read_bytes'] / 1e6:8.1f} MB  write {r['write_bytes'] / 1e6:7.1f} MB"
                     f"  {r['seconds'] * 1e6:7.1f} us  {r['gb_per_s']:7.0f} GB/s  ({r['hbm_frac']:.2f} of peak)"
@@ -214,5 +216,32 @@ def main(argv) -> int:
     return 0
 
 
+def trace_summary(argv) -> int:
+    """trace TRACE_DIR PREFIX OUT HEADER_LINE...: per (kernel, grid) call
+    counts and durations from a `rocprofv3 --kernel-trace --stats
+    --output-format csv -o PREFIX` run, then the --stats table; the header
+    lines (what ran, the command) come first."""
+    trace_dir, prefix, out, header = argv[0], argv[1], argv[2], argv[3:]
+    vals = collections.defaultdict(list)
+    for r in csv.DictReader(open(os.path.join(trace_dir, f"{prefix}_kernel_trace.csv"))):
+        vals[(_short(r["Kernel_Name"]), int(r["Grid_Size_X"]), int(r["Workgroup_Size_X"]))].append(
+            (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    lines = list(header) + ["", f"## per kernel and grid (from {prefix}_kernel_trace.csv; durations in us)",
+                            f"# {'kernel':58s} {'grid(thr)':>10s} {'wg':>4s} {'calls':>5s} {'avg_us':>9s}"
+                            f" {'min_us':>9s} {'max_us':>9s}"]
+    for (n, g, w), v in sorted(vals.items(), key=lambda kv: -sum(kv[1])):
+        lines.append(f"{n[:60]:60s} {g:10d} {w:4d} {len(v):5d} {sum(v) / len(v):9.2f} {min(v):9.2f} {max(v):9.2f}")
+    lines += ["", f"## rocprofv3 --stats ({prefix}_kernel_stats.csv: all launches of a kernel, every grid size)",
+              f"{'kernel':60s} {'calls':>7s} {'avg_us':>9s} {'pct':>6s}"]
+    for r in csv.DictReader(open(os.path.join(trace_dir, f"{prefix}_kernel_stats.csv"))):
+        lines.append(f"{_short(r['Name'])[:60]:60s} {int(r['Calls']):7d} {float(r['AverageNs']) / 1e3:9.2f}"
+                     f" {float(r['Percentage']):6.2f}")
+    with open(out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    return 0
+
+
 if __name__ == "__main__":
+    if sys.argv[1:2] == ["trace"]:
+        sys.exit(trace_summary(sys.argv[2:]))
     sys.exit(main(sys.argv[1:]))
