@@ -554,6 +554,7 @@ def bench_stack48(args) -> int:
         torch.cuda.synchronize()
         g_t.append(g0.elapsed_time(g1))
     gate_us = float(np.median(g_t)) * 1e3
+    graph = _captured_prefill(st, x, wl, d, stream, max(3, args.steps // 2))
     f, b = stage_flops_bytes("ffn", wl.T, d, E, m, k, touched, E)
     ffn_ms = dense_calls[2]
     roof = roofline(f, b, ffn_ms * 1e-3)
@@ -582,7 +583,48 @@ def bench_stack48(args) -> int:
         paper_flops_replay=paper_prefill_flops(wl.T, wl.T - wl.n_visual, wl.exit_layer, Ks, wl.layers, E, d, m,
                                                n_gate=len(range(0, wl.exit_layer, 4)) + 1),
         touched_dense=touched, K_rcep_layer_512=K20, savb_gate_us=round(gate_us, 2),
-        savb_gate_candidates_before_exit=len(range(0, wl.exit_layer, 4)), setup_s=round(setup_s, 1))
+        savb_gate_candidates_before_exit=len(range(0, wl.exit_layer, 4)), captured_prefill=graph,
+        setup_s=round(setup_s, 1))
+
+
+def _captured_prefill(st, x, wl, d, stream, reps):
+    """Algorithm 2's prefill with the SAVB gate as one captured HIP graph
+    (MoEStack.capture_prefill): gates before every fourth layer, biased so
+    that the one before the workload's exit layer fires, timed beside the
+    eager gated prefill (which reads each candidate's flag on the host)."""
+    import torch
+
+    from paper_2609_38823_amd import inputs as I
+    gates = {}
+    for l in range(0, wl.layers, 4):
+        g = {k2: torch.from_numpy(v).cuda() for k2, v in I.gate_params(d, seed=wl.seed, layer=l).items()}
+        hi = 20.0 if l == wl.exit_layer else -20.0
+        g["b2"].copy_(torch.tensor([-hi, hi], dtype=torch.float32))
+        gates[l] = g
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return float(np.median(ts))
+
+    eager_ms = timed(lambda: st.forward_gated(x, wl.n_visual, wl.p, gates, 0.5))
+    out_e, ex_e, _ = st.forward_gated(x, wl.n_visual, wl.p, gates, 0.5)
+    ref = out_e.clone()
+    pg = st.capture_prefill(x, wl.n_visual, wl.p, gates, 0.5)
+    graph_ms = timed(pg.replay)
+    out_g, ex_g, _ = pg.result()
+    same = ex_g == ex_e and torch.equal(out_g.view(torch.int16), ref.view(torch.int16))
+    return dict(graph_ms=round(graph_ms, 3), eager_gated_ms=round(eager_ms, 3), exit_layer=ex_g,
+                candidates=len(gates), bitwise_equal_to_eager=bool(same),
+                tokens_per_s=round(wl.T / (graph_ms * 1e-3), 1))
 
 
 def paper_prefill_flops(S: int, T: int, exit_layer: int, Ks, L: int, E: int, d: int, m: int,
