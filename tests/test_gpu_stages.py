@@ -241,6 +241,8 @@ def pack_router_np(w):
 
 
 E96_BF16 = I.LayerShape(d=256, E=96, m=8, k=4, dtype="bf16", zipf_alpha=0.35)  # 3 of 4 waves busy
+E256_BF16 = I.LayerShape(d=128, E=256, m=8, k=8, dtype="bf16", zipf_alpha=0.35)
+E256_K20 = I.LayerShape(d=128, E=256, m=8, k=20, dtype="bf16", zipf_alpha=0.35)
 D64_BF16 = I.LayerShape(d=64, E=32, m=8, k=2, dtype="bf16", zipf_alpha=None)   # one 64-wide stage
 
 
@@ -438,6 +440,9 @@ def test_calibrate_worked_example_golden():
     (1, 16, 2, 0.5),       # a single token
     (1024, 128, 8, 1.0),   # one launch at the 8192-entry limit, p = 1
     (37, 300, 5, 0.7),     # E > 256: eight values per lane
+    (200, 256, 8, 0.9),    # 128 < E <= 256: rows of 16 lanes, 16 values per lane
+    (150, 200, 20, 0.8),   # k > 16: one wavefront per token
+    (300, 512, 16, 0.95),  # E = 512, the largest one-launch pool
     (2000, 64, 8, 0.9),    # 16000 entries: the two-launch path
     (100, 600, 4, 0.9),    # E > 512: the two-launch path
 ])
@@ -475,9 +480,10 @@ def test_calibrate_route_prefix_matches_two_calls(T, E, k, p):
 # workgroup at 1 row, 64 at 1024); beyond: the separate launches
 @pytest.mark.parametrize("shape,T", [("qwen", 512), ("qwen", 64), ("qwen", 1), ("qwen", 1024),
                                      ("qwen", 1025), ("qwen", 4096), ("e96", 333), ("d64", 50),
-                                     ("qwen", 0)])
+                                     ("e256", 300), ("e256k20", 100), ("e256k20", 500), ("qwen", 0)])
 def test_route_rcep_matches_separate_calls(shape, T):
-    sh = {"qwen": I.QWEN3_VL_MOE, "e96": E96_BF16, "d64": D64_BF16}[shape]
+    sh = {"qwen": I.QWEN3_VL_MOE, "e96": E96_BF16, "d64": D64_BF16, "e256": E256_BF16,
+          "e256k20": E256_K20}[shape]
     E, k, p = sh.E, sh.k, 0.9
     rp = I.router_params(sh, seed=9)
     x = dev(I.tokens(sh, max(T, 1), seed=T + 2)[:T], torch.bfloat16)
