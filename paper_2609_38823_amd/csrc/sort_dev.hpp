@@ -1,7 +1,7 @@
 // Stable counting sort of up to DS_MAX routing entries by expert in one
 // workgroup of DS_THREADS threads (Algorithm 2's dispatch: the rows of one
 // expert keep ascending (token, slot) order).  Device code shared by the
-// dispatch kernel and the fused small-invocation routing kernel.
+// dispatch kernel and the one-launch calibration of moe_route_rcep.
 #pragma once
 
 #include "common.hpp"

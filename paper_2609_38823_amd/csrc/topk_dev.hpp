@@ -138,9 +138,9 @@ __device__ __forceinline__ float row_sum(float v) {
 // kept by lane r % 16 in slot r / 16 (k <= 32).  Same selection order, tie
 // rule and weights as topk_select_vals: the slots' exponentials are summed
 // by the same butterfly, so for k <= 16 the weights are bitwise equal.
-template <int MAXC, typename Out>  // out(slot r, expert, weight) for r < k, by lane r % 16
-__device__ __forceinline__ void row_topk_select_to(const float (&v)[MAXC], int j, int E, int k, int Klim,
-                                                   Out out) {
+template <int MAXC>
+__device__ __forceinline__ void row_topk_select(const float (&v)[MAXC], int j, int E, int k, int Klim,
+                                                int32_t* idx_t, float* w_t) {
   // candidates as in topk_select_vals: a taken or absent one is (-inf,
   // INT_MAX), which `better` never prefers
   float cv[MAXC];
@@ -181,16 +181,11 @@ __device__ __forceinline__ void row_topk_select_to(const float (&v)[MAXC], int j
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
     const int r = j + 16 * q;
-    if (r < k) out(r, my_i[q], ex[q] / sum);
+    if (r < k) {
+      idx_t[r] = my_i[q];
+      w_t[r] = ex[q] / sum;
+    }
   }
-}
-template <int MAXC>
-__device__ __forceinline__ void row_topk_select(const float (&v)[MAXC], int j, int E, int k, int Klim,
-                                                int32_t* idx_t, float* w_t) {
-  row_topk_select_to<MAXC>(v, j, E, k, Klim, [&](int r, int e, float wr) {
-    idx_t[r] = e;
-    w_t[r] = wr;
-  });
 }
 
 }  // namespace
