@@ -247,8 +247,8 @@ D64_BF16 = I.LayerShape(d=64, E=32, m=8, k=2, dtype="bf16", zipf_alpha=None)   #
 
 
 # 64-row tiles at 4096 (4 splits) and 8192 (2); 32-row tiles with 8 splits
-# below; from 65 536 rows (E <= 128) 128-row tiles over the whole d-range
-# with the Top-k selected in the same launch (ragged last tile, idle
+# below; from 65 536 rows (E <= 128) 128-row tiles over the whole d-range,
+# then the four-tokens-per-wavefront Top-k (ragged last tile, idle
 # wavefronts, a single 64-wide stage); the small shapes cover idle
 # wavefronts and S = 1 with a single stage
 @pytest.mark.parametrize("shape,T", [("qwen", 4096), ("qwen", 8192), ("qwen", 512), ("qwen", 77),
@@ -292,9 +292,10 @@ def test_route_packed(shape, T):
 @pytest.mark.parametrize("T", [65536 + 300, 4096])
 def test_route_packed_prefix_segments(T):
     """The split router with per-segment prefix lengths (Top-k inside [0, K)
-    of each token's segment): at 65 836 rows the Top-k is selected in the
-    router's own launch, at 4096 by the separate kernel; indices bit-exact
-    and weights against the oracle on the GPU's logits."""
+    of each token's segment): at 65 836 rows after 128-row router tiles by
+    the four-tokens-per-wavefront Top-k, at 4096 after split router tiles by
+    the one-token-per-wavefront Top-k; indices bit-exact and weights against
+    the oracle on the GPU's logits."""
     sh = I.QWEN3_VL_MOE
     rp = I.router_params(sh, seed=5)
     x = I.tokens(sh, T, seed=T + 1)
