@@ -19,6 +19,7 @@
  *     (same, the dispatch gather folded into the GEMM)            moe_expert_ffn_packed_gather
  *   weighted combine back to token order                          moe_combine
  *     (same, plus the residual of a stack of MoE blocks)          moe_combine_residual
+ *   one whole RCEP layer (routing through combine and residual)   moe_rcep_layer
  *   SAVB visual-block removal from the hidden state (Sec. 3.2)   drop_visual_block
  *   dense-equivalent routing of the paper's executor (App. A.3)   moe_expand_dense_routing
  *   SAVB exit gate (Eqs. 2, 3) and its device-decided removal     moe_savb_gate,
@@ -34,7 +35,8 @@
  *     row-major and contiguous.  Scratch memory comes from the caller as
  *     (ws, ws_bytes); moe_workspace_size() returns a sufficient size.  Its
  *     contents need no initialisation and are not preserved between calls
- *     (the expert FFN clears its own work counters on the stream first).
+ *     (the expert FFN clears its own work counters on the stream first, or
+ *     in moe_rcep_layer the routing launch before it does).
  *     Calls ordered on one stream may share a workspace; calls that can run
  *     concurrently (other streams) need workspaces of their own.
  *   - Activations and expert weights are MOE_F32 or MOE_BF16 (the `dtype`
@@ -257,6 +259,36 @@ int moe_route_rcep(const void* x, moe_dtype dtype, const void* w_r_packed, const
                    hipStream_t stream);
 
 /*
+ * moe_rcep_layer - one RCEP MoE layer over one invocation (Algorithm 2 with
+ * the prefix of Eq. 12), residual included: bitwise the outputs of
+ *   moe_route_rcep(x, ..., p)                     -> logits .. row_of_slot
+ *   moe_expert_ffn_packed_gather(x, T, k, src_of_row, offsets, E,
+ *                                K_dev = K_out, n_K = 1, d, m, ...)
+ *                                                  -> y_perm
+ *   moe_combine_residual(y_perm, row_of_slot, topk_w, residual) -> out
+ * with those calls' arguments, layouts, limits and errors (bf16 only, packed
+ * router and expert weights, 1 <= k <= min(E, 32), d % 256 == 0,
+ * m % 256 == 0).  Every argument is checked before anything is launched.
+ * `out` [T, d] may be `residual`, `x`, or both (the hidden state updated in
+ * place: the combine is the last launch); any other overlap of out with an
+ * input, and any overlap among the other outputs and inputs, is MOE_EALIAS.
+ * When the routing groups its entries in one launch (T*k <= 8192,
+ * E <= 512) and the expert FFN runs persistent, that launch also clears the
+ * expert FFN's work counters, so the layer is four launches (router,
+ * Top-k, calibration with re-route and grouping, expert FFN) plus the
+ * combine; moe_ffn_status afterwards reports the FFN as for
+ * moe_expert_ffn_packed_gather.  T = 0 gives K = k and empty counts and
+ * launches nothing else.  ws needs max(moe_route_rcep's, the expert FFN's)
+ * bytes (moe_workspace_size covers both).
+ */
+int moe_rcep_layer(const void* x, moe_dtype dtype, const void* w_r_packed, const float* bias, int T, int d,
+                   int E, int k, double p, const void* w_gate_up_packed, const void* w_down_packed, int m,
+                   const void* residual, void* out, float* logits, int32_t* topk_idx_full,
+                   float* topk_w_full, double* mass, int32_t* K_out, int32_t* topk_idx, float* topk_w,
+                   int32_t* counts, int32_t* offsets, int32_t* src_of_row, int32_t* row_of_slot,
+                   void* y_perm, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
  * moe_dispatch - group the T*k (token, slot) assignments by expert
  * (Algorithm 2: only the selected experts are evaluated).
  *
@@ -425,6 +457,13 @@ int moe_route_rcep_if(const void* x, moe_dtype dtype, const void* w_r_packed, co
                       int32_t* counts, int32_t* offsets, int32_t* src_of_row, int32_t* row_of_slot,
                       void* ws, size_t ws_bytes, const int32_t* guard, int guard_lo, int guard_hi,
                       hipStream_t stream);
+int moe_rcep_layer_if(const void* x, moe_dtype dtype, const void* w_r_packed, const float* bias, int T,
+                      int d, int E, int k, double p, const void* w_gate_up_packed, const void* w_down_packed,
+                      int m, const void* residual, void* out, float* logits, int32_t* topk_idx_full,
+                      float* topk_w_full, double* mass, int32_t* K_out, int32_t* topk_idx, float* topk_w,
+                      int32_t* counts, int32_t* offsets, int32_t* src_of_row, int32_t* row_of_slot,
+                      void* y_perm, void* ws, size_t ws_bytes, const int32_t* guard, int guard_lo,
+                      int guard_hi, hipStream_t stream);
 int moe_calibrate_route_prefix_if(const float* logits, const int32_t* topk_idx_full,
                                   const float* topk_w_full, int T, int E, int k, double p,
                                   double* mass, int32_t* K_out, int32_t* topk_idx, float* topk_w,

@@ -589,6 +589,102 @@ int moe_combine_residual_if(const void* y_perm, moe_dtype dtype, const int32_t* 
                           decomoe::Guard{guard, guard_lo, guard_hi});
 }
 
+}  // extern "C"
+
+namespace {
+// One RCEP layer of Algorithm 2 over one invocation: moe_route_rcep, then
+// moe_expert_ffn_packed_gather over experts [0, K_out), then
+// moe_combine_residual.  Every check runs before the first launch.
+int rcep_layer(const void* x, moe_dtype dtype, const void* w_r_packed, const float* bias, int T, int d, int E,
+               int k, double p, const void* w_gate_up_packed, const void* w_down_packed, int m,
+               const void* residual, void* out, float* logits, int32_t* idx_full, float* w_full, double* mass,
+               int32_t* K_out, int32_t* idx, float* w, int32_t* counts, int32_t* offsets, int32_t* src_of_row,
+               int32_t* row_of_slot, void* y_perm, void* ws, size_t ws_bytes, hipStream_t stream,
+               decomoe::Guard g) {
+  if (!valid_dtype(dtype) || T < 0 || d < 1 || E < 1 || E > kMaxE || k < 1 || k > E || m < 1)
+    return MOE_EINVAL;
+  if (dtype != MOE_BF16 || !router_packable(d, E)) return MOE_EUNSUPPORTED;
+  if (k > kMaxK) return MOE_EUNSUPPORTED;
+  if (d % 256 != 0 || m % 256 != 0) return MOE_EUNSUPPORTED;
+  if ((size_t)T * k > (size_t)INT32_MAX || (size_t)T * d * 2 > (size_t)INT32_MAX ||
+      (size_t)2 * m * d * 2 > (size_t)INT32_MAX)
+    return MOE_EUNSUPPORTED;
+  if (!(p > 0.0 && p <= 1.0)) return MOE_EINVAL;
+  if (!mass || !K_out || !counts || !offsets || !w_gate_up_packed || !w_down_packed) return MOE_EINVAL;
+  if (T > 0 && (!x || !w_r_packed || !logits || !idx_full || !w_full || !idx || !w || !src_of_row ||
+                !row_of_slot || !y_perm || !residual || !out))
+    return MOE_EINVAL;
+  if (!aligned_all({x, w_r_packed, bias, w_gate_up_packed, w_down_packed, residual, out, logits, idx_full,
+                    w_full, mass, K_out, idx, w, counts, offsets, src_of_row, row_of_slot, y_perm, ws}))
+    return MOE_EINVAL;
+  const int rows = T * k;
+  size_t need = 0;
+  if (T > 0) {
+    const size_t a = decomoe::route_rcep_ws_bytes(T, d, E, k), b = ffn_ws_bytes(true, rows, E, d, m);
+    need = a > b ? a : b;
+  }
+  if (need && (!ws || ws_bytes < need)) return MOE_EWORKSPACE;
+  const size_t A = (size_t)rows, nl = (size_t)T * E * 4, xb = (size_t)T * d * 2;
+  // out may be the residual rows and x themselves (the hidden state updated
+  // in place), but no shifted view of them
+  const Range o = rng(out, xb), r = rng(residual, xb), xi = rng(x, xb);
+  if ((o.lo != r.lo && overlap(o, r)) || (o.lo != xi.lo && overlap(o, xi))) return MOE_EALIAS;
+  const Range wr = rng(w_r_packed, (size_t)d * E * 6), bi = bias ? rng(bias, (size_t)E * 4) : Range{0, 0},
+              wgu = rng(w_gate_up_packed, (size_t)E * 2 * m * d * 2),
+              wdn = rng(w_down_packed, (size_t)E * d * m * 2);
+  if (any_alias({o}, {wr, bi, wgu, wdn}) ||
+      any_alias({rng(logits, nl), rng(idx_full, A * 4), rng(w_full, A * 4), rng(mass, (size_t)E * 8),
+                 rng(K_out, 4), rng(idx, A * 4), rng(w, A * 4), rng(counts, (size_t)E * 4),
+                 rng(offsets, (size_t)(E + 1) * 4), rng(src_of_row, A * 4), rng(row_of_slot, A * 4),
+                 rng(y_perm, A * d * 2), need ? rng(ws, need) : Range{0, 0}},
+                {xi, r, o, wr, bi, wgu, wdn}))
+    return MOE_EALIAS;
+  if (T == 0)  // K = k and empty counts; no rows to evaluate or combine
+    return route_rcep(nullptr, dtype, nullptr, nullptr, 0, d, E, k, p, nullptr, nullptr, nullptr, mass, K_out,
+                      nullptr, nullptr, counts, offsets, nullptr, nullptr, ws, ws_bytes, stream, g);
+  // with the one-launch grouping the calibration launch also clears the
+  // expert FFN's counters in the workspace, and the FFN runs with no
+  // clearing launch of its own
+  const bool fold = decomoe::route_rcep_fused(T, E, k) && decomoe::ffn_persistent_available();
+  const decomoe::ZeroAfter za = fold ? decomoe::ffn_counters_zero(ws, rows, E) : decomoe::ZeroAfter{};
+  hipError_t e = decomoe::launch_route_rcep(x, w_r_packed, bias, T, d, E, k, p, logits, idx_full, w_full, mass,
+                                            K_out, idx, w, counts, offsets, src_of_row, row_of_slot, ws, stream,
+                                            g, za);
+  if (e == hipSuccess)
+    e = decomoe::launch_expert_ffn(x, true, offsets, E, K_out, 1, rows, d, m, w_gate_up_packed, w_down_packed,
+                                   true, y_perm, ws, stream, decomoe::RowGather{src_of_row, k, T}, k, g, fold);
+  if (e == hipSuccess)
+    e = decomoe::launch_combine(y_perm, true, row_of_slot, w, T, k, d, residual, out, stream, g);
+  return hip_status(e);
+}
+}  // namespace
+
+extern "C" {
+
+int moe_rcep_layer(const void* x, moe_dtype dtype, const void* w_r_packed, const float* bias, int T, int d, int E,
+                   int k, double p, const void* w_gate_up_packed, const void* w_down_packed, int m,
+                   const void* residual, void* out, float* logits, int32_t* topk_idx_full, float* topk_w_full,
+                   double* mass, int32_t* K_out, int32_t* topk_idx, float* topk_w, int32_t* counts,
+                   int32_t* offsets, int32_t* src_of_row, int32_t* row_of_slot, void* y_perm, void* ws,
+                   size_t ws_bytes, hipStream_t stream) {
+  return rcep_layer(x, dtype, w_r_packed, bias, T, d, E, k, p, w_gate_up_packed, w_down_packed, m, residual, out,
+                    logits, topk_idx_full, topk_w_full, mass, K_out, topk_idx, topk_w, counts, offsets, src_of_row,
+                    row_of_slot, y_perm, ws, ws_bytes, stream, decomoe::Guard{});
+}
+
+int moe_rcep_layer_if(const void* x, moe_dtype dtype, const void* w_r_packed, const float* bias, int T, int d,
+                      int E, int k, double p, const void* w_gate_up_packed, const void* w_down_packed, int m,
+                      const void* residual, void* out, float* logits, int32_t* topk_idx_full,
+                      float* topk_w_full, double* mass, int32_t* K_out, int32_t* topk_idx, float* topk_w,
+                      int32_t* counts, int32_t* offsets, int32_t* src_of_row, int32_t* row_of_slot,
+                      void* y_perm, void* ws, size_t ws_bytes, const int32_t* guard, int guard_lo,
+                      int guard_hi, hipStream_t stream) {
+  if (!guard_ok(guard)) return MOE_EINVAL;
+  return rcep_layer(x, dtype, w_r_packed, bias, T, d, E, k, p, w_gate_up_packed, w_down_packed, m, residual, out,
+                    logits, topk_idx_full, topk_w_full, mass, K_out, topk_idx, topk_w, counts, offsets, src_of_row,
+                    row_of_slot, y_perm, ws, ws_bytes, stream, decomoe::Guard{guard, guard_lo, guard_hi});
+}
+
 int moe_permute_experts(const int32_t* order, int E, int d, int m, moe_dtype dtype,
                         const float* w_r, const float* bias, const void* w_gate_up,
                         const void* w_down, float* w_r_out, float* bias_out,

@@ -80,6 +80,14 @@ struct SortOut {
   int32_t* src_of_row = nullptr;
   int32_t* row_of_slot = nullptr;
   int* ctr = nullptr;
+  int* zero = nullptr;  // then n_zero ints set to 0 (mark_val at mark_at)
+  int n_zero = 0, mark_at = -1, mark_val = 0;
+};
+// ints a launch sets after its last use of the workspace (0, and mark_val at
+// mark_at): the next call's counters, so that it needs no clearing launch
+struct ZeroAfter {
+  int* p = nullptr;
+  int n = 0, mark_at = -1, mark_val = 0;
 };
 bool calibrate_route_fused(int T, int E, int k);
 hipError_t launch_calibrate_route(const float* logits, const int32_t* idx_full, const float* w_full,
@@ -95,7 +103,7 @@ hipError_t launch_route_rcep(const void* x, const void* w_r_packed, const float*
                              int k, double p, float* logits, int32_t* idx_full, float* w_full, double* mass,
                              int32_t* K_out, int32_t* idx, float* w, int32_t* counts, int32_t* offsets,
                              int32_t* src_of_row, int32_t* row_of_slot, void* ws, hipStream_t s,
-                             Guard g = Guard{});
+                             Guard g = Guard{}, const ZeroAfter& za = ZeroAfter{});
 size_t dispatch_ws_bytes(int T, int k, int E);
 hipError_t launch_dispatch(const int32_t* idx, int T, int k, int E, const void* x, int elt, int d,
                            int32_t* counts, int32_t* offsets, int32_t* src_of_row,
@@ -119,7 +127,13 @@ hipError_t launch_expert_ffn(const void* a_rows, bool bf16, const int32_t* offse
                              const int32_t* K_dev, int n_K, int rows_max, int d, int m,
                              const void* w_gate_up, const void* w_down, bool packed, void* y_perm,
                              void* ws, hipStream_t s, RowGather gather = RowGather{nullptr, 1, 0},
-                             int kmin = 1, Guard g = Guard{});
+                             int kmin = 1, Guard g = Guard{}, bool counters_ready = false);
+// The persistent expert FFN (packed bf16 weights): whether the device runs
+// it, and what a launch before it must write so that it runs with no
+// clearing launch (counters_ready): the counter header of ws, zeroed, with
+// the launch path recorded
+bool ffn_persistent_available();
+ZeroAfter ffn_counters_zero(void* ws, int rows_max, int E);
 // launch path recorded in the expert FFN's counter header
 constexpr int FFN_PATH_PERSISTENT = 1;  // both GEMMs in one persistent launch
 constexpr int FFN_PATH_TWO_LAUNCH = 2;  // packed weights, one launch per GEMM

@@ -1168,11 +1168,13 @@ hipError_t clear_counters(int* ctr, int n_tiles, int path, hipStream_t s, Guard 
 // zeroing its counters), or one launch per GEMM when the XCD layout is unknown
 hipError_t launch_packed(int bm, const Tiles& t0, int nn1, const uint16_t* X, const uint16_t* Wgu,
                          const uint16_t* Wdn, uint16_t* H, uint16_t* Y, int d, int m,
-                         const RowGather g0, int* ctr, hipStream_t s, Guard g) {
+                         const RowGather g0, int* ctr, hipStream_t s, Guard g, bool counters_ready) {
   int grid = 0, n_xcc = 0;
   if (persistent_shape(grid, n_xcc)) {
-    hipError_t e = clear_counters(ctr, t0.max_tiles, FFN_PATH_PERSISTENT, s, g);
-    if (e != hipSuccess) return e;
+    if (!counters_ready) {
+      hipError_t e = clear_counters(ctr, t0.max_tiles, FFN_PATH_PERSISTENT, s, g);
+      if (e != hipSuccess) return e;
+    }
     // few rows per expert (decode): one token tile per expert, so every
     // weight tile is read once and streams with the non-temporal hint
     // (measured at 64 tokens x top-8 over 93 experts: 166 -> 151 us)
@@ -1232,6 +1234,17 @@ int* ffn_counters(void* ws) {
   return reinterpret_cast<int*>(align256(reinterpret_cast<uintptr_t>(ws)));
 }
 
+bool ffn_persistent_available() {
+  int grid = 0, n_xcc = 0;
+  return persistent_shape(grid, n_xcc);
+}
+
+ZeroAfter ffn_counters_zero(void* ws, int rows_max, int E) {
+  // what clear_counters writes, for the largest tile count of either tile height
+  return ZeroAfter{ffn_counters(ws), kern::FFN_CTR_TILES + max_tiles_for(rows_max, E, 64), kern::FFN_CTR_PATH,
+                   FFN_PATH_PERSISTENT};
+}
+
 hipError_t launch_ffn_status(const void* ws, int32_t* status, hipStream_t s) {
   ffn_status_kernel<<<1, 64, 0, s>>>(ffn_counters(const_cast<void*>(ws)), status);
   return hipGetLastError();
@@ -1240,7 +1253,7 @@ hipError_t launch_ffn_status(const void* ws, int32_t* status, hipStream_t s) {
 hipError_t launch_expert_ffn(const void* x_perm, bool bf16, const int32_t* offsets, int E,
                              const int32_t* K_dev, int n_K, int rows_max, int d, int m,
                              const void* w_gate_up, const void* w_down, bool packed, void* y_perm,
-                             void* ws, hipStream_t s, RowGather gather, int kmin, Guard g) {
+                             void* ws, hipStream_t s, RowGather gather, int kmin, Guard g, bool counters_ready) {
   if (gather.src_of_row && !(bf16 && packed)) return hipErrorInvalidValue;
   const int bm = bf16 ? pick_bm(rows_max, E) : FBM;
   int nn0, nn1;
@@ -1256,7 +1269,8 @@ hipError_t launch_expert_ffn(const void* x_perm, bool bf16, const int32_t* offse
   if (bf16 && packed) {
     return launch_packed(bm, t0, nn1, static_cast<const uint16_t*>(x_perm),
                         static_cast<const uint16_t*>(w_gate_up), static_cast<const uint16_t*>(w_down),
-                        static_cast<uint16_t*>(h), static_cast<uint16_t*>(y_perm), d, m, gather, ctr, s, g);
+                        static_cast<uint16_t*>(h), static_cast<uint16_t*>(y_perm), d, m, gather, ctr, s, g,
+                        counters_ready);
   }
   err = clear_counters(ctr, 0, bf16 ? FFN_PATH_ROW_MAJOR : FFN_PATH_F32, s, g);
   if (err != hipSuccess) return err;

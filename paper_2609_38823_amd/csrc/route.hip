@@ -352,7 +352,10 @@ __global__ __launch_bounds__(256) void topk_row_kernel(float* __restrict__ logit
 // re-routed entries are also grouped by expert (Algorithm 2's dispatch,
 // x = NULL): every workgroup publishes its entries and counts itself done;
 // the last one to finish sorts all T k entries (sort_small), so no launch
-// follows for the grouping.
+// follows for the grouping.  It then also writes the n_zero ints at `zero`
+// (0, and mark_val at index mark_at): the expert FFN's counter header in the
+// same workspace, which the call that follows would otherwise clear with a
+// launch of its own.
 // ---------------------------------------------------------------------------
 template <int MAXC, int RMAXC>
 __global__ __launch_bounds__(CAL_THREADS) void calibrate_route_kernel(
@@ -361,7 +364,7 @@ __global__ __launch_bounds__(CAL_THREADS) void calibrate_route_kernel(
     double* __restrict__ mass, int32_t* __restrict__ K_out, int32_t* __restrict__ idx,
     float* __restrict__ w, int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
     int32_t* __restrict__ src_of_row, int32_t* __restrict__ row_of_slot, int* __restrict__ ctr,
-    const Guard g) {
+    int* __restrict__ zero, int n_zero, int mark_at, int mark_val, const Guard g) {
   static_assert(CAL_THREADS == DS_THREADS && CAL_WAVES == DS_WAVES, "the grouping runs on this workgroup");
   if (guard_skip(g)) return;
   __shared__ CalLds L;
@@ -412,6 +415,8 @@ __global__ __launch_bounds__(CAL_THREADS) void calibrate_route_kernel(
   if (!s_last) return;
   sort_small(idx, T * k, E, key_bits, reinterpret_cast<int*>(L.table), E, L.part, counts, offsets, src_of_row,
              row_of_slot);
+  // every other workgroup is done with the workspace
+  for (int i = tid; i < n_zero; i += CAL_THREADS) zero[i] = i == mark_at ? mark_val : 0;
 }
 
 }  // namespace
@@ -438,7 +443,7 @@ hipError_t launch_calibrate_route(const float* logits, const int32_t* idx_full, 
   const SortOut so = sort ? *sort : SortOut{};
 #define CAL_ROUTE_ARGS                                                                                      \
   logits, idx_full, w_full, T, E, k, key_bits, p, mass, K_out, idx, w, so.counts, so.offsets, so.src_of_row, \
-      so.row_of_slot, so.ctr, g
+      so.row_of_slot, so.ctr, so.zero, so.n_zero, so.mark_at, so.mark_val, g
   if (E <= 128)
     calibrate_route_kernel<2, 8><<<grid, CAL_THREADS, 0, s>>>(CAL_ROUTE_ARGS);
   else if (E <= 256)
@@ -464,8 +469,10 @@ size_t route_rcep_ws_bytes(int T, int d, int E, int k) {
 hipError_t launch_route_rcep(const void* x, const void* w_r_packed, const float* bias, int T, int d, int E,
                              int k, double p, float* logits, int32_t* idx_full, float* w_full, double* mass,
                              int32_t* K_out, int32_t* idx, float* w, int32_t* counts, int32_t* offsets,
-                             int32_t* src_of_row, int32_t* row_of_slot, void* ws, hipStream_t s, Guard g) {
+                             int32_t* src_of_row, int32_t* row_of_slot, void* ws, hipStream_t s, Guard g,
+                             const ZeroAfter& za) {
   if (!route_rcep_fused(T, E, k)) {
+    if (za.n) return hipErrorInvalidValue;  // only the one-launch grouping writes it
     hipError_t err = launch_route(x, true, nullptr, w_r_packed, bias, T, d, E, k, nullptr, 1, nullptr, logits,
                                   idx_full, w_full, ws, s, g);
     if (err == hipSuccess)
@@ -481,7 +488,7 @@ hipError_t launch_route_rcep(const void* x, const void* w_r_packed, const float*
   hipError_t err = launch_route(x, true, nullptr, w_r_packed, bias, T, d, E, k, nullptr, 1, nullptr, logits,
                                 idx_full, w_full, ws, s, g, ctr);
   if (err != hipSuccess) return err;
-  const SortOut so{counts, offsets, src_of_row, row_of_slot, ctr};
+  const SortOut so{counts, offsets, src_of_row, row_of_slot, ctr, za.p, za.n, za.mark_at, za.mark_val};
   return launch_calibrate_route(logits, idx_full, w_full, T, E, k, p, mass, K_out, idx, w, s, g, &so);
 }
 

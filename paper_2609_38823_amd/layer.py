@@ -14,7 +14,9 @@ the order of Algorithm 2 of the paper:
       -> moe_route(logits, K) [prefix re-route] -> moe_dispatch
       -> moe_expert_ffn(K) -> moe_combine
       (one invocation: moe_calibrate_route_prefix does s, K and the
-      re-route in one call)
+      re-route in one call; on packed weights moe_route_rcep does the
+      routing through the grouping, and with a residual moe_rcep_layer does
+      the whole layer)
 
 All calls are asynchronous on one stream and K never leaves the device.
 """
@@ -278,6 +280,16 @@ class MoELayer:
         b = b or self.buffers(x.shape[0], n_seg)
         K = b.K if K_out is None else K_out
         mk = mark or (lambda: None)
+        if seg_offsets is None and self.packed and self.w_r_packed is not None and residual is not None \
+                and mark is None:
+            # one invocation on packed weights, residual included: the whole
+            # layer in one call (its routing launch also clears the expert
+            # FFN's counters)
+            abi.moe_rcep_layer(x, self.w_r_packed, self.bias, self.k, p, self.w_gate_up, self.w_down, residual,
+                               b.out if out is None else out, b.logits, b.idx_full, b.w_full, b.mass, K, b.idx,
+                               b.w, b.counts, b.offsets, b.src_of_row, b.row_of_slot, b.y_perm, b.ws,
+                               guard=guard, stream=stream)
+            return b
         if seg_offsets is None and self.packed and self.w_r_packed is not None:
             # one invocation on packed weights: routing, masses, K, the
             # prefix re-route and the grouping in one call

@@ -37,7 +37,7 @@ def test_header_declares_the_boundary():
         "moe_ffn_status", "moe_expert_ffn_packed_gather_noalloc",
         "moe_route_packed_if", "moe_calibrate_route_prefix_if", "moe_dispatch_if",
         "moe_expert_ffn_packed_gather_if", "moe_combine_residual_if", "moe_savb_gate_if",
-        "moe_route_rcep", "moe_route_rcep_if"])
+        "moe_route_rcep", "moe_route_rcep_if", "moe_rcep_layer", "moe_rcep_layer_if"])
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -302,6 +302,41 @@ def test_route_rcep_rejects(lib):
     assert call(ix=P4) == EALIAS              # re-routed indices on top of the full-pool ones
     assert call(lg=P1) == EALIAS              # logits on top of x
     assert call(sr=ctypes.c_void_p(0xC0002)) == EINVAL
+
+
+def test_rcep_layer_rejects(lib):
+    names = ["x", "dt", "wp", "b", "T", "d", "E", "k", "p", "wgu", "wd", "m", "res", "out", "lg", "if_", "wf",
+             "ms", "K", "ix", "w", "cn", "of", "sr", "rs", "yp", "ws", "wsb"]
+    # every array 16 MiB apart (T 64, d 256, E 32, m 256: the largest, w_gate_up, is 8 MiB)
+    arrays = {n: ctypes.c_void_p((i + 1) << 24) for i, n in enumerate(
+        ["x", "wp", "wgu", "wd", "res", "out", "lg", "if_", "wf", "ms", "K", "ix", "w", "cn", "of", "sr", "rs",
+         "yp", "ws"])}
+    base = dict(arrays, dt=BF16, b=NULL, T=64, d=256, E=32, k=8, p=0.9, m=256, wsb=1 << 30)
+
+    def call(f=lib.moe_rcep_layer, extra=(), **kw):
+        a = dict(base)
+        a.update(kw)
+        return f(*[a[n] for n in names], *extra, NULL)
+
+    assert call(dt=F32) == EUNSUPPORTED
+    assert call(m=128) == EUNSUPPORTED         # packed expert FFN: m % 256 == 0
+    assert call(E=48) == EUNSUPPORTED          # packed router: E % 32 == 0
+    assert call(k=0) == EINVAL and call(k=33) == EINVAL
+    assert call(p=0.0) == EINVAL
+    assert call(res=NULL) == EINVAL and call(yp=NULL) == EINVAL
+    assert call(yp=ctypes.c_void_p(arrays["yp"].value + 8)) == EINVAL
+    assert call(wsb=16) == EWORKSPACE
+    # out one row past the residual: neither in place nor disjoint
+    assert call(out=ctypes.c_void_p(arrays["res"].value + 512)) == EALIAS
+    assert call(out=ctypes.c_void_p(arrays["x"].value + 512)) == EALIAS
+    assert call(out=arrays["wgu"]) == EALIAS   # out on top of the expert weights
+    assert call(yp=arrays["x"]) == EALIAS
+    assert call(ws=arrays["res"]) == EALIAS
+    assert call(ix=arrays["if_"]) == EALIAS
+    fi = lib.moe_rcep_layer_if
+    G = ctypes.c_void_p(0x7F000000)
+    assert call(fi, (ctypes.c_void_p(0x7F000002), 0, 1)) == EINVAL   # misaligned guard
+    assert call(fi, (G, 0, 1), wsb=16) == EWORKSPACE
 
 
 def test_ffn_status_rejects(lib):

@@ -531,6 +531,149 @@ def test_route_rcep_matches_separate_calls(shape, T):
 
 
 # ---------------------------------------------------------------------------
+# moe_rcep_layer: one RCEP layer (routing, expert FFN over the prefix,
+# combine and residual) in one call, bitwise the three calls it stands for
+# ---------------------------------------------------------------------------
+D256_E64 = I.LayerShape(d=256, E=64, m=256, k=4, dtype="bf16", zipf_alpha=0.35)
+D256_E256_K20 = I.LayerShape(d=256, E=256, m=256, k=20, dtype="bf16", zipf_alpha=0.35)
+RCEP_LAYER_SHAPES = {"qwen": I.QWEN3_VL_MOE, "e64": D256_E64, "e256k20": D256_E256_K20}
+
+
+class _RcepLayer:
+    """Weights of one shape and the outputs of one call."""
+
+    def __init__(self, sh, seed):
+        self.sh = sh
+        rp = I.router_params(sh, seed=seed)
+        prm = I.layer_params(sh, seed=seed + 1)
+        self.rp, self.prm = rp, prm
+        self.wp = torch.empty((3 * sh.d * sh.E,), dtype=torch.bfloat16, device="cuda")
+        abi.moe_pack_router(dev(rp["w_r"]), self.wp)
+        self.bias = dev(rp["bias"]) if rp["bias"] is not None else None
+        wgu, wd = dev(prm["w_gate_up"], torch.bfloat16), dev(prm["w_down"], torch.bfloat16)
+        self.wgu_p, self.wd_p = torch.empty_like(wgu), torch.empty_like(wd)
+        abi.moe_pack_expert_weights(wgu, self.wgu_p)
+        abi.moe_pack_expert_weights(wd, self.wd_p)
+
+    def outs(self, T):
+        E, k, d = self.sh.E, self.sh.k, self.sh.d
+        A = T * k
+        return dict(logits=f32((T, E)), idx_full=i32((T, k)), w_full=f32((T, k)),
+                    mass=torch.full((1, E), -1.0, dtype=torch.float64, device="cuda"), K=i32((1,)),
+                    idx=i32((T, k)), w=f32((T, k)), counts=i32((E,)), offsets=i32((E + 1,)),
+                    src=i32((A,)), ros=i32((A,)),
+                    y=torch.full((A, d), 7.0, dtype=torch.bfloat16, device="cuda"))
+
+    def separate(self, x, residual, p, ws):
+        o = self.outs(x.shape[0])
+        abi.moe_route_rcep(x, self.wp, self.bias, self.sh.k, p, o["logits"], o["idx_full"], o["w_full"], o["mass"],
+                           o["K"], o["idx"], o["w"], o["counts"], o["offsets"], o["src"], o["ros"], ws)
+        o["out"] = torch.full_like(x, 5.0)
+        if x.shape[0]:
+            abi.moe_expert_ffn_packed_gather(x, self.sh.k, o["src"], o["offsets"], self.wgu_p, self.wd_p, o["y"],
+                                             ws, K_dev=o["K"])
+            abi.moe_combine_residual(o["y"], o["ros"], o["w"], residual, o["out"])
+        return o
+
+    def layer(self, x, residual, out, p, ws, guard=None):
+        o = self.outs(x.shape[0])
+        abi.moe_rcep_layer(x, self.wp, self.bias, self.sh.k, p, self.wgu_p, self.wd_p, residual, out,
+                           o["logits"], o["idx_full"], o["w_full"], o["mass"], o["K"], o["idx"], o["w"],
+                           o["counts"], o["offsets"], o["src"], o["ros"], o["y"], ws, guard=guard)
+        o["out"] = out
+        return o
+
+
+def _assert_same(a, b, names):
+    for n in names:
+        assert torch.equal(a[n].contiguous().view(torch.uint8), b[n].contiguous().view(torch.uint8)), n
+
+
+ALL_OUTS = ("logits", "idx_full", "w_full", "mass", "K", "idx", "w", "counts", "offsets", "src", "ros", "y",
+            "out")
+
+
+# T*k <= 8192: the routing's one-launch grouping also clears the expert
+# FFN's counters (qwen 1, 64, 512, 1024; e64; e256k20); beyond, the
+# separate launches with the FFN's own clearing (qwen 1025, e64 2100)
+@pytest.mark.parametrize("shape,T", [("qwen", 512), ("qwen", 64), ("qwen", 1), ("qwen", 1024), ("qwen", 1025),
+                                     ("e64", 300), ("e64", 2100), ("e256k20", 100), ("e64", 0)])
+def test_rcep_layer_matches_separate_calls(shape, T):
+    sh = RCEP_LAYER_SHAPES[shape]
+    L = _RcepLayer(sh, seed=13)
+    p = 0.9
+    x = dev(I.tokens(sh, max(T, 1), seed=T + 5)[:T], torch.bfloat16)
+    residual = dev(I.synthetic_rows(max(T, 1), sh.d, "bf16", seed=T + 6)[:T], torch.bfloat16)
+    ws = ws_for(T, sh.E, sh.k, sh.d, sh.m)
+    a = L.separate(x, residual, p, ws)
+    ws.fill_(0xA5)  # the composed call starts from a workspace holding stale counters
+    b = L.layer(x, residual, torch.full_like(x, 5.0), p, ws)
+    torch.cuda.synchronize()
+    if T == 0:
+        assert int(host(b["K"])[0]) == sh.k and (host(b["counts"]) == 0).all()
+        _assert_same(a, b, ("mass", "K", "counts", "offsets"))
+        return
+    assert_ffn_ran_all(ws)
+    _assert_same(a, b, ALL_OUTS)
+    K = int(host(b["K"])[0])
+    assert K == int(oracle.prefix_length(
+        oracle.activated_mass(host(b["idx_full"]), host(b["w_full"]).astype(np.float64), sh.E), p, sh.k))
+    if shape != "qwen" or T <= 64:
+        # against the oracle's layer on the same logits and K (Algorithm 2,
+        # Eqs. 10-12 and App. A.3 Eq. 15), plus the residual
+        ref = oracle.moe_layer_rcep(host(x), L.rp["w_r"], L.rp["bias"], L.prm["w_gate_up"], L.prm["w_down"],
+                                    sh.k, p, logits=host(b["logits"]), K_override=[K])
+        np.testing.assert_array_equal(host(b["idx"]), ref["idx"])
+        want = host(residual).astype(np.float64) + ref["out"]
+        assert rel_inf(host(b["out"]), want) <= TOL["bf16"]
+        assert row_rel(host(b["out"]), want) <= TOL["bf16"]
+
+
+@pytest.mark.parametrize("shape,T", [("qwen", 64), ("qwen", 1025), ("e64", 300)])
+def test_rcep_layer_in_place_and_reused_workspace(shape, T):
+    """out == residual == x (the hidden state updated in place), on one
+    workspace reused by a larger then a smaller call: bitwise the separate
+    calls each time, and the expert FFN ran every item."""
+    sh = RCEP_LAYER_SHAPES[shape]
+    L = _RcepLayer(sh, seed=17)
+    ws = ws_for(2 * T, sh.E, sh.k, sh.d, sh.m)
+    for n in (2 * T, T):
+        h = dev(I.tokens(sh, n, seed=n + 3), torch.bfloat16)
+        a = L.separate(h, h, 0.9, ws)
+        b = L.layer(h, h, h, 0.9, ws)
+        torch.cuda.synchronize()
+        assert_ffn_ran_all(ws)
+        _assert_same(a, b, ALL_OUTS)
+
+
+def test_rcep_layer_guard():
+    """moe_rcep_layer_if: with the value inside the range the results of
+    the plain call; outside it nothing is written, moe_ffn_status still
+    reports the previous call."""
+    sh = D256_E64
+    T = 300
+    L = _RcepLayer(sh, seed=19)
+    x = dev(I.tokens(sh, T, seed=1), torch.bfloat16)
+    res = dev(I.synthetic_rows(T, sh.d, "bf16", seed=2), torch.bfloat16)
+    ws = ws_for(T, sh.E, sh.k, sh.d, sh.m)
+    g = dev(np.array([3], np.int32))
+    a = L.layer(x, res, torch.full_like(x, 5.0), 0.9, ws)
+    b = L.layer(x, res, torch.full_like(x, 5.0), 0.9, ws, guard=(g, 3, 4))
+    torch.cuda.synchronize()
+    _assert_same(a, b, ALL_OUTS)
+    st0 = torch.full((4,), -1, dtype=torch.int32, device="cuda")
+    abi.moe_ffn_status(ws, st0)
+    c = L.layer(x, res, torch.full_like(x, 5.0), 0.9, ws, guard=(g, 4, 8))
+    st1 = torch.full((4,), -1, dtype=torch.int32, device="cuda")
+    abi.moe_ffn_status(ws, st1)
+    torch.cuda.synchronize()
+    assert (host(c["out"]).astype(np.float32) == 5.0).all()
+    assert (host(c["K"]) == -7).all() and (host(c["counts"]) == -7).all()
+    assert (host(c["mass"]) == -1.0).all()
+    assert torch.equal(st0, st1)
+
+
+# ---------------------------------------------------------------------------
 # moe_dispatch: bit-exact counting sort and bitwise gather
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("T,E,k,d,dt,K", [
