@@ -478,10 +478,12 @@ def test_calibrate_route_prefix_matches_two_calls(T, E, k, p):
 # ---------------------------------------------------------------------------
 # up to 8192 entries: the router and Top-k, then calibration, re-route and
 # the grouping in one launch (the last workgroup to finish sorts; one
-# workgroup at 1 row, 64 at 1024); beyond: the separate launches
-@pytest.mark.parametrize("shape,T", [("qwen", 512), ("qwen", 64), ("qwen", 1), ("qwen", 1024),
-                                     ("qwen", 1025), ("qwen", 4096), ("e96", 333), ("d64", 50),
-                                     ("e256", 300), ("e256k20", 100), ("e256k20", 500), ("qwen", 0)])
+# workgroup at 1 row, four at 63 and 64, five at 65, 64 at 1024); beyond:
+# the separate launches
+@pytest.mark.parametrize("shape,T", [("qwen", 512), ("qwen", 64), ("qwen", 1), ("qwen", 63), ("qwen", 65),
+                                     ("qwen", 1024), ("qwen", 1025), ("qwen", 4096), ("e96", 333), ("d64", 50),
+                                     ("e256", 300), ("e256", 40), ("e256k20", 100), ("e256k20", 500),
+                                     ("e256k20", 30), ("qwen", 0)])
 def test_route_rcep_matches_separate_calls(shape, T):
     sh = {"qwen": I.QWEN3_VL_MOE, "e96": E96_BF16, "d64": D64_BF16, "e256": E256_BF16,
           "e256k20": E256_K20}[shape]
