@@ -822,7 +822,7 @@ def test_pack_expert_weights_layout(E, R, C):
 # expert holding every row (128-row tiles), a single tile, more XCDs than
 # tiles, empty experts between full ones, and a prefix K with no rows past it
 SKEW_CASES = [
-    (128, 2048, 768, "bf16", 4096, None, [0] * 5 + [4096] + [0] * 122),  # 64-row tiles
+    (128, 2048, 768, "bf16", 4096, None, [0] * 5 + [4096] + [0] * 122),  # 64-row tiles (< 48 rows per expert)
     (8, 2048, 768, "bf16", 4096, None, [0, 0, 0, 4096, 0, 0, 0, 0]),       # 128-row tiles
     (8, 512, 256, "bf16", 20, None, [0, 0, 0, 20, 0, 0, 0, 0]),
     (4, 512, 256, "bf16", 130, None, [0, 65, 0, 65]),
@@ -902,8 +902,9 @@ def test_expert_ffn_clamps_offsets_to_rows_max():
 # ---------------------------------------------------------------------------
 GATHER_CASES = [
     # T, E, k, d, m, K
-    (512, 128, 8, 2048, 768, None),   # 512 text rows, full pool (64-row tiles)
+    (512, 128, 8, 2048, 768, None),   # 512 text rows, full pool (64-row tiles: < 48 rows per expert)
     (512, 128, 8, 2048, 768, 84),     # prefix of 84 experts
+    (1024, 128, 8, 2048, 768, None),  # 1024 rows (128-row tiles, 64 rows per expert)
     (4096, 128, 8, 2048, 768, None),  # 4096 rows (128-row tiles)
     (37, 6, 3, 512, 256, None),       # ragged, few experts
     (1, 16, 2, 256, 256, None),       # a single token
@@ -1065,7 +1066,9 @@ def test_packed_ffn_two_launch_fallback_matches_persistent(T, E, k, d, m, monkey
     assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
 
 
-@pytest.mark.parametrize("T", [4096, 512, 64])
+# 128-row tiles at 4096 and 1024 tokens, 64-row tiles at 512, 64-row tiles
+# streaming the weights at 64
+@pytest.mark.parametrize("T", [4096, 1024, 512, 64])
 def test_persistent_ffn_repeated_calls_bitwise(T, monkeypatch):
     """Back-to-back persistent calls on one workspace (its counters cleared
     and reused every call) keep giving the two-launch path's bits: each of
