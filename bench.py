@@ -871,6 +871,15 @@ def bench_stress(args) -> int:
         f, nb = stage_flops_bytes(n, T, d, E, m, k, E, E, gather=False)
         rep[n] = dict(ms=round(st_ms[n], 4), roofline=roofline(f, nb, st_ms[n] * 1e-3),
                       gflop=round(f / 1e9, 3), mb=round(nb / 1e6, 3))
+    # the router runs the float32 product as three bf16 MFMA terms: its
+    # binding floor is the larger of the stage's HBM bytes and that executed
+    # MFMA work at peak
+    f, nb = stage_flops_bytes("route_full", T, d, E, m, k, E, E, gather=False)
+    sec = st_ms["route_full"] * 1e-3
+    floor = max(nb / (PEAK_HBM_GBS * 1e9), 3 * f / (PEAK_BF16_TFLOPS * 1e12))
+    rep["route_full"]["split_router"] = dict(
+        executed_gflop=round(3 * f / 1e9, 3), executed_mfma_frac=round(3 * f / sec / 1e12 / PEAK_BF16_TFLOPS, 4),
+        floor_us=round(floor * 1e6, 2), frac_of_floor=round(floor / sec, 4))
     f, nb = stage_flops_bytes("dispatch", T, d, E, m, k, E, E, gather=False)
     roof = roofline(f, nb, st_ms["dispatch"] * 1e-3)
     roof["kernel"] = "moe_dispatch @ 65536 rows (counting sort + row gather)"
