@@ -325,6 +325,17 @@ def test_layer_shape_sweep(dt, d, E, m, k, T, p, bias, seed):
     xd = torch.from_numpy(x).cuda().to(TDT[dt])
     check_dense(layer, rp, x, xd, k, dt)
     check_rcep(layer, rp, x, xd, k, p, dt)
+    if layer.packed and layer.w_r_packed is not None:
+        # with the residual the layer is one call (moe_rcep_layer); the
+        # separate calls (forced by a stage marker) give the same bits
+        outs = []
+        for mark in (None, lambda: None):
+            out = torch.empty_like(xd)
+            b = layer.forward_rcep(xd, p, residual=xd, out=out, mark=mark)
+            outs.append((out, b.K.clone(), b.idx.clone()))
+        torch.cuda.synchronize()
+        assert torch.equal(outs[0][0].view(torch.int16), outs[1][0].view(torch.int16))
+        assert torch.equal(outs[0][1], outs[1][1]) and torch.equal(outs[0][2], outs[1][2])
 
 
 @pytest.mark.parametrize("sizes", [[1] * 64, [1, 7, 0, 20, 36]])
