@@ -102,10 +102,11 @@ def test_drop_visual_block_bitwise(dt, S, d, v0, v1):
 # ---------------------------------------------------------------------------
 # moe_route, logits-input mode: Top-k and weights on given logits
 # ---------------------------------------------------------------------------
-# T >= 16384 takes the four-tokens-per-wavefront kernel (8 or 16 values per
+# T >= 4096 takes the four-tokens-per-wavefront kernel (8 or 16 values per
 # lane; k > 16 uses the second slot of every lane)
-ROUTE_CASES = [(1, 16, 2), (37, 16, 2), (5, 7, 7), (129, 64, 1), (512, 128, 8), (4096, 128, 8),
-               (300, 1000, 32), (70, 65, 3), (16384, 128, 8), (16390, 200, 20), (16385, 100, 32)]
+ROUTE_CASES = [(1, 16, 2), (37, 16, 2), (5, 7, 7), (129, 64, 1), (512, 128, 8), (4095, 128, 8),
+               (4096, 128, 8), (300, 1000, 32), (70, 65, 3), (16384, 128, 8), (5000, 200, 20),
+               (16390, 200, 20), (16385, 100, 32)]
 
 
 @pytest.mark.parametrize("ties", [False, True])
