@@ -819,10 +819,11 @@ struct XcdRange {
 };
 
 // tstart[e] = first m-tile of expert e (experts >= Klim have none),
-// tstart[E] = the tile count; returns this XCD's tile range.  part: 2 NTHR /
-// 64 + 3 ints of LDS.
+// tstart[E] = the tile count; returns this XCD's tile range.  NT: threads of
+// the workgroup (E <= 4 NT); part: 2 NT / 64 + 3 ints of LDS.
+template <int NT>
 __device__ XcdRange plan_tiles(const Tiles& tl, int xcc, int n_xcc, int* tstart, int* part) {
-  constexpr int NW = NTHR / 64;
+  constexpr int NW = NT / 64;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   int& s_klim = part[2 * NW];
   int& s_a0 = part[2 * NW + 1];
@@ -831,8 +832,8 @@ __device__ XcdRange plan_tiles(const Tiles& tl, int xcc, int n_xcc, int* tstart,
   // the first barrier (their latencies overlap)
   int mx = 0;
   if (tl.K_dev)
-    for (int i = tid; i < tl.n_K; i += NTHR) mx = max(mx, tl.K_dev[i]);
-  // offsets[4 tid .. 4 tid + 4], indices clamped to E (E <= 4 NTHR): five
+    for (int i = tid; i < tl.n_K; i += NT) mx = max(mx, tl.K_dev[i]);
+  // offsets[4 tid .. 4 tid + 4], indices clamped to E (E <= 4 NT): five
   // loads without a branch between them
   int ofs[5], rows[4];
 #pragma unroll
@@ -932,6 +933,69 @@ __global__ void ffn_status_kernel(const int* __restrict__ ctr, int32_t* __restri
   status[3] = ctr[FFN_CTR_PATH];
 }
 
+// Item j of an XCD's queue (n_gu gate/up items first, then the down items;
+// nn0 / nn1 n-tiles per GEMM): its work item, its m-tile t, and whether its
+// expert's weights stream with the non-temporal hint -- an expert whose
+// rows fit one m-tile has no other tile that reads its weights again (RCEP
+// span, 512 rows over 85 experts: 169 -> 153 us); the weights of experts
+// with several m-tiles keep the default policy, so that the m-tiles that run
+// together share each fetch in L2.
+struct Item {
+  Work wk;
+  int t;
+  bool down, stream;
+};
+__device__ __forceinline__ Item decode_item(const Tiles& tl, const XcdRange& rg, const int* s_tstart, int j,
+                                            int n_gu, int nn1, int bm) {
+  Item it;
+  it.down = j >= n_gu;
+  const int nn = it.down ? nn1 : tl.nn;
+  const int jm = it.down ? j - n_gu : j;
+  // the expert holding tile a0 + jm / nn; its tiles in this range are
+  // [t_lo, t_lo + c), items [nn (t_lo - a0), nn (t_lo - a0 + c))
+  const int tq = rg.a0 + jm / nn;
+  int a = 0, b = tl.E;  // tstart[a] <= tq < tstart[b]
+  while (b - a > 1) {
+    const int mid = (a + b) >> 1;
+    if (s_tstart[mid] <= tq) a = mid; else b = mid;
+  }
+  const int t_lo = max(s_tstart[a], rg.a0);
+  const int c = min(s_tstart[a + 1], rg.a1) - t_lo;
+  const int o = jm - nn * (t_lo - rg.a0);
+  it.t = t_lo + o % c;
+  const int lo = clampi(tl.offsets[a], 0, tl.rows_max);
+  const int hi = clampi(tl.offsets[a + 1], lo, tl.rows_max);
+  const int r0 = lo + (it.t - s_tstart[a]) * bm;
+  it.wk.expert = __builtin_amdgcn_readfirstlane(a);
+  it.wk.row0 = __builtin_amdgcn_readfirstlane(r0);
+  it.wk.rows = __builtin_amdgcn_readfirstlane(min(bm, hi - r0));
+  it.wk.nt = __builtin_amdgcn_readfirstlane(o / c);
+  it.stream = c == 1 && s_tstart[a + 1] - s_tstart[a] == 1;
+  return it;
+}
+
+// gate/up item done: this wavefront's h stores have reached L2 (vmcnt 0),
+// then, after the barrier, one thread counts the item for its tile
+__device__ __forceinline__ void gate_up_done(int* done) {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_fetch_add(done, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// down item: one thread polls its tile's gate/up count (bounded; a wait that
+// runs out is counted in `gave_up`), then the workgroup may load h
+__device__ __forceinline__ void wait_gate_up(const int* done, int nn0, int* gave_up) {
+  if (threadIdx.x == 0) {
+    bool ready = false;
+    for (int n = 0; n < FFN_SPIN_LIMIT && !ready; ++n) {
+      ready = __hip_atomic_load(done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= nn0;
+      if (!ready) __builtin_amdgcn_s_sleep(4);
+    }
+    if (!ready) __hip_atomic_fetch_add(gave_up, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+}
+
 template <int BM, int AUX, int BN1>
 __global__ __launch_bounds__(NTHR, 2) void ffn_fused_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ Wgu, const uint16_t* __restrict__ Wdn,
@@ -947,7 +1011,7 @@ __global__ __launch_bounds__(NTHR, 2) void ffn_fused_kernel(
 
   // the XCD this workgroup runs on (hardware register XCC_ID, bits 3:0)
   const int xcc = (int)(__builtin_amdgcn_s_getreg((3 << 11) | 20) % (unsigned)n_xcc);
-  const XcdRange rg = plan_tiles(tl, xcc, n_xcc, s_tstart, s_part);
+  const XcdRange rg = plan_tiles<NTHR>(tl, xcc, n_xcc, s_tstart, s_part);
   const int ntile = rg.a1 - rg.a0;
   const int n_gu = ntile * tl.nn, n_all = n_gu + ntile * nn1;
   const int tid = threadIdx.x;
@@ -961,58 +1025,272 @@ __global__ __launch_bounds__(NTHR, 2) void ffn_fused_kernel(
     __syncthreads();
     const int j = __builtin_amdgcn_readfirstlane(s_item);
     if (j >= n_all) break;
-    const bool down = j >= n_gu;
-    const int nn = down ? nn1 : tl.nn;
-    const int jm = down ? j - n_gu : j;
-    // the expert holding tile a0 + jm / nn; its tiles in this range are
-    // [t_lo, t_lo + c), items [nn (t_lo - a0), nn (t_lo - a0 + c))
-    const int tq = rg.a0 + jm / nn;
-    int a = 0, b = tl.E;  // tstart[a] <= tq < tstart[b]
-    while (b - a > 1) {
-      const int mid = (a + b) >> 1;
-      if (s_tstart[mid] <= tq) a = mid; else b = mid;
-    }
-    const int t_lo = max(s_tstart[a], rg.a0);
-    const int c = min(s_tstart[a + 1], rg.a1) - t_lo;
-    const int o = jm - nn * (t_lo - rg.a0);
-    const int t = t_lo + o % c;
-    const int lo = clampi(tl.offsets[a], 0, tl.rows_max);
-    const int hi = clampi(tl.offsets[a + 1], lo, tl.rows_max);
-    const int r0 = lo + (t - s_tstart[a]) * BM;
-    Work wk;
-    wk.expert = __builtin_amdgcn_readfirstlane(a);
-    wk.row0 = __builtin_amdgcn_readfirstlane(r0);
-    wk.rows = __builtin_amdgcn_readfirstlane(min(BM, hi - r0));
-    wk.nt = __builtin_amdgcn_readfirstlane(o / c);
-    int* const done = ctr + FFN_CTR_TILES + t;
-    // an expert whose rows fit one m-tile has no other tile that reads its
-    // weights again: they stream with the non-temporal hint (RCEP span, 512
-    // rows over 85 experts: 169 -> 153 us); the weights of experts with
-    // several m-tiles keep the default policy, so that the m-tiles that run
-    // together share each fetch in L2
-    const bool stream = AUX == 2 || (c == 1 && s_tstart[a + 1] - s_tstart[a] == 1);
-    if (!down) {
+    const Item it = decode_item(tl, rg, s_tstart, j, n_gu, nn1, BM);
+    int* const done = ctr + FFN_CTR_TILES + it.t;
+    const bool stream = AUX == 2 || it.stream;
+    if (!it.down) {
       if (stream)
-        packed_item<0, BM, BN, 2>(X, Wgu, H, wk, d, m, gather, aring);
+        packed_item<0, BM, BN, 2>(X, Wgu, H, it.wk, d, m, gather, aring);
       else if constexpr (AUX != 2)
-        packed_item<0, BM, BN, AUX>(X, Wgu, H, wk, d, m, gather, aring);
-      __builtin_amdgcn_s_waitcnt(0);  // this wavefront's h stores are complete (in L2)
-      __syncthreads();
-      if (tid == 0) __hip_atomic_fetch_add(done, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        packed_item<0, BM, BN, AUX>(X, Wgu, H, it.wk, d, m, gather, aring);
+      gate_up_done(done);
     } else {
-      if (tid == 0) {
-        bool ready = false;
-        for (int n = 0; n < FFN_SPIN_LIMIT && !ready; ++n) {
-          ready = __hip_atomic_load(done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= tl.nn;
-          if (!ready) __builtin_amdgcn_s_sleep(4);
-        }
-        if (!ready) __hip_atomic_fetch_add(claim + 2, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
-      __syncthreads();
+      wait_gate_up(done, tl.nn, claim + 2);
       if (stream)
-        packed_item<1, BM, BN1, 2>(H, Wdn, Y, wk, d, m, RowGather{nullptr, 1, 0}, aring);
+        packed_item<1, BM, BN1, 2>(H, Wdn, Y, it.wk, d, m, RowGather{nullptr, 1, 0}, aring);
       else if constexpr (AUX != 2)
-        packed_item<1, BM, BN1, AUX>(H, Wdn, Y, wk, d, m, RowGather{nullptr, 1, 0}, aring);
+        packed_item<1, BM, BN1, AUX>(H, Wdn, Y, it.wk, d, m, RowGather{nullptr, 1, 0}, aring);
+    }
+    if (tid == 0) __hip_atomic_fetch_add(claim + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Persistent expert FFN with alternating wavefronts (128-row token tiles when
+// both weight matrices have a multiple of 512 rows).
+//
+// One workgroup of 8 wavefronts per compute unit computes a 128 x 512 tile
+// (gate/up: 256 gate rows and their 256 up rows; down: 512 rows of w_down).
+// Wavefront w owns all 128 token rows and weight rows [64 w, 64 w + 64) --
+// the same 128 x 64 per wavefront, registers and fragment layout as the
+// four-wavefront items above, so the results are bitwise the same -- and
+// the token tile in LDS is shared by all eight.  Each SIMD holds two of the
+// wavefronts (group 0 and group 1, from the hardware SIMD id).  Per k-step
+// of 32 a wavefront runs a memory phase (refill of a token stage, the
+// weights of k-step + 3, the LDS reads of its token fragments) and an MFMA
+// phase, separated by workgroup barriers; group 1 starts one phase late, so
+// while one wavefront of a SIMD runs its MFMAs the other issues its loads.
+// (Dense Qwen3-VL layer, in-process against the two-workgroup kernel:
+// 2048 rows 292 -> 287 us, 4096 rows 388 -> 377, 8192 rows 659 -> 629,
+// 16384 rows 1220 -> 1153.)
+// The four token stages are separate LDS arrays, so the compiler can tell
+// that a refill does not write the stage being read, and does not wait for
+// the refill's transfers before those reads.
+// ---------------------------------------------------------------------------
+constexpr int PP_THR = 512;
+constexpr int PP_SLOT = 128 * AK * 2;  // one token stage: 128 rows x 64 k-values
+
+template <int MODE, int AUX>
+__device__ __forceinline__ void pingpong_item(const uint16_t* __restrict__ A, const uint16_t* __restrict__ Wp,
+                                              uint16_t* __restrict__ C, const Work wk, int d, int m,
+                                              const RowGather gather, char* st0, char* st1, char* st2,
+                                              char* st3, int grp) {
+  constexpr int MI = 4, NI = 2, AGW = 2, LA = 3;
+  const int nt = wk.nt;
+  const int Kdim = MODE == 0 ? d : m;
+  const int R = MODE == 0 ? 2 * m : d;
+  const int nk = Kdim / BK;  // a multiple of 8
+  const int ldc = MODE == 0 ? m : d;
+  int tid = threadIdx.x;
+  asm volatile("" : "+v"(tid));  // keep the per-item offsets out of the item loop
+  const int lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  // ---- token rows: transfer q of wave wv covers tile rows 8 g .. 8 g + 7,
+  // g = wv + 8 q; lane l fills row 8 g + l / 8, physical chunk l % 8, with
+  // logical chunk (l % 8) ^ ((row >> 1) & 7) (as in packed_item)
+  const bool gat = MODE == 0 && gather.src_of_row != nullptr;
+  const __amdgpu_buffer_rsrc_t a_rs =
+      gat ? make_rsrc(A, (uint32_t)gather.T * Kdim * 2)
+          : make_rsrc(A + (size_t)wk.row0 * Kdim, (uint32_t)wk.rows * Kdim * 2);
+  int a_voff[AGW];
+#pragma unroll
+  for (int q = 0; q < AGW; ++q) {
+    const int row = 8 * (wv + 8 * q) + (lane >> 3);
+    const int c = (lane & 7) ^ ((row >> 1) & 7);
+    int src = 0;
+    if (gat) {
+      if (row < wk.rows) src = gather.src_of_row[wk.row0 + row] / gather.k;
+      if ((unsigned)src >= (unsigned)gather.T) src = 0;
+    } else {
+      src = row < wk.rows ? row : 0;
+    }
+    a_voff[q] = (src * Kdim + c * 8) * 2;
+  }
+  auto issue_a = [&](char* stage, int js) {
+#pragma unroll
+    for (int q = 0; q < AGW; ++q) dma16(a_rs, stage + (wv + 8 * q) * 1024, a_voff[q], js * AK * 2);
+  };
+
+  // ---- weights: gate/up, 32 gate rows and the matching 32 up rows; down,
+  // 64 consecutive rows
+  const __amdgpu_buffer_rsrc_t b_rs =
+      make_rsrc(Wp + (size_t)wk.expert * R * Kdim, (uint32_t)R * Kdim * 2);
+  const int RB = R / 32;
+  const int rb0 = MODE == 0 ? nt * 8 + wv : nt * 16 + 2 * wv;
+  const int rb1 = MODE == 0 ? m / 32 + nt * 8 + wv : rb0 + 1;
+  const int b_voff = lane * 16;
+  auto load_b = [&](u32x4 (&b)[2][NI], int ks) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      b[h][0] = load_frag<AUX>(b_rs, b_voff, ((2 * ks + h) * RB + rb0) * 1024);
+      b[h][1] = load_frag<AUX>(b_rs, b_voff, ((2 * ks + h) * RB + rb1) * 1024);
+    }
+  };
+
+  f32x16 acc[MI][NI];
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int j = 0; j < NI; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  const int r32 = lane & 31, kh = lane >> 5;
+  int a_lane[4];
+#pragma unroll
+  for (int s4 = 0; s4 < 4; ++s4) a_lane[s4] = r32 * 128 + (((2 * s4 + kh) ^ ((r32 >> 1) & 7)) << 4);
+
+  u32x4 bq[4][2][NI];
+  // The wait before reading the next token stage (at odd k-step i, for the
+  // stage read from k-step i + 1) may leave the younger loads outstanding:
+  // at least the weights of the last five k-steps (the fewest, at the end
+  // of the loop; elsewhere also one or two stages' transfers, whose waits
+  // then complete earlier than needed).
+  constexpr int WAIT = 5 * 2 * NI;
+  auto pipeline = [&](auto MAC) {
+    constexpr int MA = decltype(MAC)::value;  // 32-row token blocks holding rows
+    bf16x8 af[2][MI];
+    // k-step i.  Memory phase: the refill of slot `rs` with stage i / 2 + 3
+    // (even i), the weights of k-step i + 3 into `bn`, at odd i the wait for
+    // the next stage, the token fragments of k-step i from stage `cur`.
+    // Then a barrier, the MFMA phase with the weights `bc`, a barrier.
+    auto step = [&](auto ODD, auto REFILL, auto LOADB, int i, char* cur, char* rs,
+                    const u32x4 (&bc)[2][NI], u32x4 (&bn)[2][NI]) {
+      if constexpr (decltype(REFILL)::value) issue_a(rs, i / 2 + 3);
+      if constexpr (decltype(LOADB)::value) load_b(bn, i + LA);
+      if constexpr (decltype(ODD)::value) wait_vmcnt<WAIT>();
+      __builtin_amdgcn_sched_barrier(0);
+      constexpr int so = decltype(ODD)::value ? 2 : 0;
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int mi = 0; mi < MA; ++mi)
+          af[h][mi] = *reinterpret_cast<const bf16x8*>(cur + mi * 32 * 128 + a_lane[so + h]);
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int mi = 0; mi < MA; ++mi)
+#pragma unroll
+          for (int ni = 0; ni < NI; ++ni)
+            acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, bc[h][ni]),
+                                                                  af[h][mi], acc[mi][ni], 0, 0, 0);
+      __builtin_amdgcn_s_setprio(0);
+      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    using F = std::integral_constant<bool, false>;
+    using Tr = std::integral_constant<bool, true>;
+
+    // stages 0..2 here; k-step i (even) refills slot (i / 2 + 3) % 4 with
+    // stage i / 2 + 3 while that stage exists (at i = 0 slot 3 is empty)
+    issue_a(st0, 0);
+    issue_a(st1, 1);
+    issue_a(st2, 2);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int q = 0; q < LA; ++q) load_b(bq[q], q);
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vmcnt<2 * AGW + 2 * NI * LA>();  // stage 0 (younger: stages 1, 2, three k-steps of weights)
+    __builtin_amdgcn_s_barrier();
+    if (grp) __builtin_amdgcn_s_barrier();  // group 1 runs one phase behind
+    __builtin_amdgcn_sched_barrier(0);
+    int i = 0;
+    for (; i + 8 < nk; i += 8) {
+      step(F{}, Tr{}, Tr{}, i + 0, st0, st3, bq[0], bq[3]);
+      step(Tr{}, F{}, Tr{}, i + 1, st0, st0, bq[1], bq[0]);
+      step(F{}, Tr{}, Tr{}, i + 2, st1, st0, bq[2], bq[1]);
+      step(Tr{}, F{}, Tr{}, i + 3, st1, st1, bq[3], bq[2]);
+      step(F{}, Tr{}, Tr{}, i + 4, st2, st1, bq[0], bq[3]);
+      step(Tr{}, F{}, Tr{}, i + 5, st2, st2, bq[1], bq[0]);
+      step(F{}, Tr{}, Tr{}, i + 6, st3, st2, bq[2], bq[1]);
+      step(Tr{}, F{}, Tr{}, i + 7, st3, st3, bq[3], bq[2]);
+    }
+    // last 8 k-steps: the last stage leaves at the first, weights up to nk - 1
+    step(F{}, Tr{}, Tr{}, i + 0, st0, st3, bq[0], bq[3]);
+    step(Tr{}, F{}, Tr{}, i + 1, st0, st0, bq[1], bq[0]);
+    step(F{}, F{}, Tr{}, i + 2, st1, st0, bq[2], bq[1]);
+    step(Tr{}, F{}, Tr{}, i + 3, st1, st1, bq[3], bq[2]);
+    step(F{}, F{}, Tr{}, i + 4, st2, st1, bq[0], bq[3]);
+    step(Tr{}, F{}, F{}, i + 5, st2, st2, bq[1], bq[0]);
+    step(F{}, F{}, F{}, i + 6, st3, st2, bq[2], bq[1]);
+    step(Tr{}, F{}, F{}, i + 7, st3, st3, bq[3], bq[2]);
+    if (!grp) __builtin_amdgcn_s_barrier();  // group 0 catches up: equal barrier counts
+  };
+  const int ma = (wk.rows + 31) >> 5;
+  if (ma >= 4)
+    pipeline(std::integral_constant<int, 4>{});
+  else if (ma == 3)
+    pipeline(std::integral_constant<int, 3>{});
+  else if (ma == 2)
+    pipeline(std::integral_constant<int, 2>{});
+  else
+    pipeline(std::integral_constant<int, 1>{});
+
+  // epilogue: every wavefront has passed the last barrier after its last LDS
+  // read; wavefront w stages its slice through half w / 4 of stage slot w % 4
+  char* reg = ((wv & 3) == 0 ? st0 : (wv & 3) == 1 ? st1 : (wv & 3) == 2 ? st2 : st3) + (wv >> 2) * (PP_SLOT / 2);
+  const int colbase = MODE == 0 ? nt * 256 + 32 * wv : nt * 512 + 64 * wv;
+  store_tile<MODE, MI, NI>(acc, reg, C, ldc, wk, colbase, lane);
+}
+
+// The persistent loop of ffn_fused_kernel with 128 x 512 tiles on
+// pingpong_item: tl.nn = 2 m / 512 gate/up and nn1 = d / 512 down n-tiles.
+__global__ __launch_bounds__(PP_THR, 1) void ffn_pingpong_kernel(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ Wgu, const uint16_t* __restrict__ Wdn,
+    uint16_t* __restrict__ H, uint16_t* __restrict__ Y, const Tiles tl, int nn1, int d, int m,
+    const RowGather gather, int n_xcc, int* __restrict__ ctr, const Guard g) {
+  if (guard_skip(g)) return;
+  constexpr int BM = 128;
+  __shared__ __attribute__((aligned(1024))) char st0[PP_SLOT];
+  __shared__ __attribute__((aligned(1024))) char st1[PP_SLOT];
+  __shared__ __attribute__((aligned(1024))) char st2[PP_SLOT];
+  __shared__ __attribute__((aligned(1024))) char st3[PP_SLOT];
+  __shared__ int s_tstart[FFN_MAXE + 1];
+  __shared__ int s_part[2 * (PP_THR / 64) + 3];
+  __shared__ int s_item;
+  __shared__ int s_simd[PP_THR / 64];
+
+  const int tid = threadIdx.x;
+  // the SIMD of each wavefront (hardware register HW_ID, bits 5:4)
+  if ((tid & 63) == 0) s_simd[tid >> 6] = (int)(__builtin_amdgcn_s_getreg((1 << 11) | (4 << 6) | 4) & 3);
+  const int xcc = (int)(__builtin_amdgcn_s_getreg((3 << 11) | 20) % (unsigned)n_xcc);
+  const XcdRange rg = plan_tiles<PP_THR>(tl, xcc, n_xcc, s_tstart, s_part);  // its barriers publish s_simd
+  // group 1: a lower-numbered wavefront shares this one's SIMD (the barrier
+  // counts of pingpong_item do not depend on the groups)
+  int grp = 0;
+  for (int v = 0; v < (tid >> 6); ++v) grp |= s_simd[v] == s_simd[tid >> 6] ? 1 : 0;
+  grp = __builtin_amdgcn_readfirstlane(grp);
+  const int ntile = rg.a1 - rg.a0;
+  const int n_gu = ntile * tl.nn, n_all = n_gu + ntile * nn1;
+  int* const claim = ctr + 16 * xcc;
+  if (tid == 0)
+    __hip_atomic_store(claim + 3, s_tstart[tl.E] * (tl.nn + nn1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  for (;;) {
+    __syncthreads();  // the previous item is done with LDS and s_item
+    if (tid == 0) s_item = atomicAdd(claim, 1);
+    __syncthreads();
+    const int j = __builtin_amdgcn_readfirstlane(s_item);
+    if (j >= n_all) break;
+    const Item it = decode_item(tl, rg, s_tstart, j, n_gu, nn1, BM);
+    int* const done = ctr + FFN_CTR_TILES + it.t;
+    if (!it.down) {
+      if (it.stream)
+        pingpong_item<0, 2>(X, Wgu, H, it.wk, d, m, gather, st0, st1, st2, st3, grp);
+      else
+        pingpong_item<0, 0>(X, Wgu, H, it.wk, d, m, gather, st0, st1, st2, st3, grp);
+      gate_up_done(done);
+    } else {
+      wait_gate_up(done, tl.nn, claim + 2);
+      if (it.stream)
+        pingpong_item<1, 2>(H, Wdn, Y, it.wk, d, m, RowGather{nullptr, 1, 0}, st0, st1, st2, st3, grp);
+      else
+        pingpong_item<1, 0>(H, Wdn, Y, it.wk, d, m, RowGather{nullptr, 1, 0}, st0, st1, st2, st3, grp);
     }
     if (tid == 0) __hip_atomic_fetch_add(claim + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
@@ -1092,6 +1370,7 @@ using kern::FFN_CTR_TILES;
 using kern::clear_kernel;
 using kern::ffn_status_kernel;
 using kern::ffn_fused_kernel;
+using kern::ffn_pingpong_kernel;
 using kern::ffn_gemm_packed_kernel;
 using kern::pack_weights_kernel;
 
@@ -1201,7 +1480,14 @@ hipError_t launch_packed(int bm, const Tiles& t0, int nn1, const uint16_t* X, co
     // tiles in the down GEMM, twice as many items of half the bytes, so that
     // the queues drain evenly at the end (64 tokens x top-8 through 48
     // layers: 8.26 -> 8.00 ms per step)
-    if (bm == 128)
+    // 128-row tiles: 128 x 512 tiles of eight alternating wavefronts, one
+    // workgroup per compute unit, where 512 divides both weight matrices
+    if (bm == 128 && (2 * m) % 512 == 0 && d % 512 == 0) {
+      Tiles tp = t0;
+      tp.nn = 2 * m / 512;
+      ffn_pingpong_kernel<<<grid / 2, kern::PP_THR, 0, s>>>(X, Wgu, Wdn, H, Y, tp, d / 512, d, m, g0, n_xcc, ctr,
+                                                            g);
+    } else if (bm == 128)
       ffn_fused_kernel<128, 0, 256><<<grid, NTHR, 0, s>>>(X, Wgu, Wdn, H, Y, t0, nn1, d, m, g0, n_xcc, ctr, g);
     else if (stream_weights)
       ffn_fused_kernel<64, 2, 128><<<grid, NTHR, 0, s>>>(X, Wgu, Wdn, H, Y, t0, d / 128, d, m, g0, n_xcc, ctr, g);
