@@ -1081,7 +1081,7 @@ def bench_gemm_ceiling(args) -> int:
     ach = r32["tflops"]
     roof = {"bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
             "frac": ach / PEAK_BF16_TFLOPS, "traffic": None,
-            "kernel": "moe_expert_ffn_packed, 32768 rows on one expert (ffn_fused_kernel<128>)"}
+            "kernel": "moe_expert_ffn_packed, 32768 rows on one expert (ffn_pingpong_kernel)"}
     return _line(
         "Expert FFN TFLOP/s with cache-resident weights, beside the vendor GEMM library on the same shapes",
         ach, "TFLOP/s", args, r32["ms"],

@@ -88,11 +88,15 @@ N_SIMD = 256 * 4
 N_XCC = 8
 
 # kernels of the dense span at 4096 rows (the --traffic-run layer call)
+# the persistent expert FFN at 128-row token tiles: the alternating-wavefront
+# kernel where 512 divides both weight matrices, else the two-workgroup one
+FFN128 = ("ffn_pingpong_kernel", "ffn_fused_kernel<128")
+
 STAGES = [
-    ("routing", [("router_x3_kernel<", None), ("topk_kernel<2>", 262144)]),
+    ("routing", [("router_x3_kernel<", None), ("topk_row_kernel<", None), ("topk_kernel<2>", 262144)]),
     ("dispatch", [("dispatch_hist_kernel", None), ("dispatch_scan_rank_kernel", None), ("dispatch_scan_kernel", None),
                   ("dispatch_rank_kernel", None)]),
-    ("expert FFN", [("clear_kernel", None), ("ffn_fused_kernel<128", None)]),
+    ("expert FFN", [("clear_kernel", None)] + [(k, None) for k in FFN128]),
     ("combine", [("combine_kernel<true, false", 1048576)]),
 ]
 
@@ -122,16 +126,17 @@ def mfma_summary(mfma_dir: str) -> dict | None:
     vals = collections.defaultdict(list)
     for f in glob.glob(os.path.join(mfma_dir, "**", "*counter_collection.csv"), recursive=True):
         for r in csv.DictReader(open(f)):
-            if _short(r["Kernel_Name"]).startswith("ffn_fused_kernel<128"):
+            if _short(r["Kernel_Name"]).startswith(FFN128):
+                name = _short(r["Kernel_Name"])
                 vals[r["Counter_Name"]].append(float(r["Counter_Value"]))
-    times = [v for (n, g), v in per_kernel_time(mfma_dir).items() if n.startswith("ffn_fused_kernel<128")]
+    times = [v for (n, g), v in per_kernel_time(mfma_dir).items() if n.startswith(FFN128)]
     if not vals or not times:
         return None
     mops = sum(vals["SQ_INSTS_VALU_MFMA_MOPS_BF16"]) / len(vals["SQ_INSTS_VALU_MFMA_MOPS_BF16"])
     busy = sum(vals["SQ_VALU_MFMA_BUSY_CYCLES"]) / len(vals["SQ_VALU_MFMA_BUSY_CYCLES"])
     gui = sum(vals["GRBM_GUI_ACTIVE"]) / len(vals["GRBM_GUI_ACTIVE"])
     sec = times[0]
-    return dict(kernel="ffn_fused_kernel<128> @ 4096 rows", mfma_flops_executed=mops * 512,
+    return dict(kernel=f"{name} @ 4096 rows", mfma_flops_executed=mops * 512,
                 mfma_busy_cycles_sum=busy, grbm_gui_active_sum=gui, seconds=sec,
                 # busy cycles per SIMD over the kernel's duration at the peak clock
                 mfma_busy_frac_at_peak_clock=busy / N_SIMD / (sec * CLOCK),
@@ -151,7 +156,7 @@ def main(argv) -> int:
     # the bench's FFN call at 4096 rows (128-row tiles): one persistent launch
     # running both GEMMs, or, where it is not used, the largest grids of the
     # two per-GEMM launches
-    fused = [k for k in fetch if k[0].startswith("ffn_fused_kernel<128")]
+    fused = [k for k in fetch if k[0].startswith(FFN128)]
     if fused:
         keys = [max(fused, key=lambda k: k[1])]
     else:
