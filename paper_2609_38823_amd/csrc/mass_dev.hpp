@@ -67,9 +67,11 @@ __device__ double mass_sorted(const int32_t* __restrict__ idx, const float* __re
       rw[q] = i < n_all ? w[base + i] : 0.f;
     }
 #pragma unroll
-    for (int q = 0; q < SPT; ++q) {
-      L.st_e[tid + q * CAL_THREADS] = re[q];
-      L.st_w[tid + q * CAL_THREADS] = rw[q];
+    for (int q = 0; q < SPT; ++q) {  // only entries below n_all are read below
+      if (tid + q * CAL_THREADS < n_all) {
+        L.st_e[tid + q * CAL_THREADS] = re[q];
+        L.st_w[tid + q * CAL_THREADS] = rw[q];
+      }
     }
   }
   for (int i = tid; i < CAL_WAVES * E; i += CAL_THREADS) wh[i] = 0;
