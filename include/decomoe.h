@@ -20,6 +20,7 @@
  *   weighted combine back to token order                          moe_combine
  *     (same, plus the residual of a stack of MoE blocks)          moe_combine_residual
  *   one whole RCEP layer (routing through combine and residual)   moe_rcep_layer
+ *   the previous layer's combine + one RCEP layer up to its FFN    moe_rcep_layer_chained
  *   SAVB visual-block removal from the hidden state (Sec. 3.2)   drop_visual_block
  *   dense-equivalent routing of the paper's executor (App. A.3)   moe_expand_dense_routing
  *   SAVB exit gate (Eqs. 2, 3) and its device-decided removal     moe_savb_gate,
@@ -287,6 +288,49 @@ int moe_rcep_layer(const void* x, moe_dtype dtype, const void* w_r_packed, const
                    float* topk_w_full, double* mass, int32_t* K_out, int32_t* topk_idx, float* topk_w,
                    int32_t* counts, int32_t* offsets, int32_t* src_of_row, int32_t* row_of_slot,
                    void* y_perm, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * moe_rcep_layer_chained - the next RCEP layer of a stack of MoE blocks,
+ * starting from the previous layer's expert outputs (Algorithm 2's per-layer
+ * loop: the combine with the residual of layer l, then the RCEP layer l + 1
+ * up to its expert FFN).
+ *
+ *   prev_y_perm, prev_row_of_slot, prev_topk_w   the previous layer's y_perm
+ *                [T*k, d] bf16, row_of_slot [T, k] and re-routed topk_w
+ *                [T, k] (the same T and k), or all three NULL (no previous
+ *                layer: the first layer of the stack).
+ *   h            [T, d] bf16, in and out: the residual stream.  With the
+ *                previous arrays, h <- h + sum_j prev_topk_w[t, j] *
+ *                prev_y_perm[prev_row_of_slot[t, j]] (bitwise
+ *                moe_combine_residual with residual = out = h); then h is
+ *                this layer's input x.
+ * The rest as moe_rcep_layer, which this call equals except for its last
+ * step: bitwise the outputs of
+ *   [moe_combine_residual(prev_y_perm, prev_row_of_slot, prev_topk_w, h, h)]
+ *   moe_route_rcep(h, ..., p)                     -> logits .. row_of_slot
+ *   moe_expert_ffn_packed_gather(h, ..., K_dev = K_out, n_K = 1)  -> y_perm
+ * and this layer's combine is left to the next chained call (whose prev_*
+ * are this call's y_perm, row_of_slot, topk_w) or to moe_combine_residual
+ * after the last layer.  Each prev_* array may be this call's array of the
+ * same role (prev_y_perm == y_perm, prev_row_of_slot == row_of_slot,
+ * prev_topk_w == topk_w: the first launch reads them before any launch of
+ * the call writes them); any other overlap of an argument with an output
+ * is MOE_EALIAS.  When the router's plan keeps a token tile of at most
+ * 32 KB per workgroup (one expert group: E <= 128) and the routing groups
+ * its entries in one launch (T*k <= 8192), the combine runs inside the
+ * router's launch: each router workgroup forms the rows and columns of h it
+ * multiplies, writes them and keeps them in LDS; the layer is then four
+ * launches (router with the previous combine, Top-k, calibration with
+ * re-route and grouping, expert FFN).  Otherwise the combine is a launch of
+ * its own.  Same limits, errors and workspace as moe_rcep_layer; T = 0
+ * gives K = k and empty counts.
+ */
+int moe_rcep_layer_chained(const void* prev_y_perm, const int32_t* prev_row_of_slot, const float* prev_topk_w,
+                           void* h, moe_dtype dtype, const void* w_r_packed, const float* bias, int T, int d, int E,
+                           int k, double p, const void* w_gate_up_packed, const void* w_down_packed, int m,
+                           float* logits, int32_t* topk_idx_full, float* topk_w_full, double* mass, int32_t* K_out,
+                           int32_t* topk_idx, float* topk_w, int32_t* counts, int32_t* offsets, int32_t* src_of_row,
+                           int32_t* row_of_slot, void* y_perm, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * moe_dispatch - group the T*k (token, slot) assignments by expert

@@ -31,7 +31,8 @@ EXPORTS = ("moe_status_string", "moe_workspace_size", "moe_route", "moe_route_pa
            "moe_expand_dense_routing", "moe_ffn_status", "moe_expert_ffn_packed_gather_noalloc",
            "moe_route_packed_if", "moe_calibrate_route_prefix_if", "moe_dispatch_if",
            "moe_expert_ffn_packed_gather_if", "moe_combine_residual_if", "moe_savb_gate_if",
-           "moe_route_rcep", "moe_route_rcep_if", "moe_rcep_layer", "moe_rcep_layer_if")
+           "moe_route_rcep", "moe_route_rcep_if", "moe_rcep_layer", "moe_rcep_layer_if",
+           "moe_rcep_layer_chained")
 
 # size of the library's own scratch array of the allocation-free expert FFN
 NOALLOC_SCRATCH_BYTES = 32 << 20
@@ -87,6 +88,8 @@ def load() -> ctypes.CDLL:
                                    _P, _P, _S, _P, _I, _I, _P]),
         "moe_rcep_layer": (_I, [_P, _I, _P, _P, _I, _I, _I, _I, _D, _P, _P, _I, _P, _P, _P, _P, _P, _P, _P,
                                 _P, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
+        "moe_rcep_layer_chained": (_I, [_P, _P, _P, _P, _I, _P, _P, _I, _I, _I, _I, _D, _P, _P, _I, _P, _P,
+                                        _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
         "moe_rcep_layer_if": (_I, [_P, _I, _P, _P, _I, _I, _I, _I, _D, _P, _P, _I, _P, _P, _P, _P, _P, _P,
                                    _P, _P, _P, _P, _P, _P, _P, _P, _P, _S, _P, _I, _I, _P]),
         "moe_route_packed_if": (_I, [_P, _I, _P, _P, _I, _I, _I, _I, _P, _I, _P, _P, _P, _P, _P, _S,
@@ -469,6 +472,23 @@ def moe_rcep_layer(x, w_r_packed, bias, k, p, w_gate_up_packed, w_down_packed, r
     else:
         gp, lo, hi = _guard(guard)
         _check("moe_rcep_layer_if", load().moe_rcep_layer_if(*args, gp, lo, hi, _stream(stream)))
+
+
+def moe_rcep_layer_chained(prev, h, w_r_packed, bias, k, p, w_gate_up_packed, w_down_packed, logits, idx_full,
+                           w_full, mass, K_out, idx, w, counts, offsets, src_of_row, row_of_slot, y_perm, ws,
+                           stream=None):
+    """The previous layer's combine with the residual (prev = (y_perm,
+    row_of_slot, topk_w) of that layer, or None) into h, then this layer's
+    RCEP routing and expert FFN over h; this layer's combine is left to the
+    next chained call or to moe_combine_residual."""
+    T, d = h.shape
+    E, two_m, _ = w_gate_up_packed.shape
+    py, pr, pw = prev if prev is not None else (None, None, None)
+    _check("moe_rcep_layer_chained", load().moe_rcep_layer_chained(
+        _p(py), _i32(pr), _f32(pw), _p(h), _dt(h), _p(w_r_packed), _f32(bias), T, d, E, k, float(p),
+        _p(w_gate_up_packed), _p(w_down_packed), two_m // 2, _f32(logits), _i32(idx_full), _f32(w_full), _f64(mass),
+        _i32(K_out), _i32(idx), _f32(w), _i32(counts), _i32(offsets), _i32(src_of_row), _i32(row_of_slot),
+        _p(y_perm), _p(ws), _nbytes(ws), _stream(stream)))
 
 
 def moe_rcep_layer_if(x, w_r_packed, bias, k, p, w_gate_up_packed, w_down_packed, residual, out, logits,

@@ -657,6 +657,84 @@ int rcep_layer(const void* x, moe_dtype dtype, const void* w_r_packed, const flo
     e = decomoe::launch_combine(y_perm, true, row_of_slot, w, T, k, d, residual, out, stream, g);
   return hip_status(e);
 }
+
+// moe_rcep_layer_chained: see the header
+int rcep_layer_chained(const void* prev_y_perm, const int32_t* prev_row_of_slot, const float* prev_topk_w, void* h,
+                       moe_dtype dtype, const void* w_r_packed, const float* bias, int T, int d, int E, int k,
+                       double p, const void* w_gate_up_packed, const void* w_down_packed, int m, float* logits,
+                       int32_t* idx_full, float* w_full, double* mass, int32_t* K_out, int32_t* idx, float* w,
+                       int32_t* counts, int32_t* offsets, int32_t* src_of_row, int32_t* row_of_slot, void* y_perm,
+                       void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!valid_dtype(dtype) || T < 0 || d < 1 || E < 1 || E > kMaxE || k < 1 || k > E || m < 1)
+    return MOE_EINVAL;
+  if (dtype != MOE_BF16 || !router_packable(d, E)) return MOE_EUNSUPPORTED;
+  if (k > kMaxK) return MOE_EUNSUPPORTED;
+  if (d % 256 != 0 || m % 256 != 0) return MOE_EUNSUPPORTED;
+  if ((size_t)T * k > (size_t)INT32_MAX || (size_t)T * d * 2 > (size_t)INT32_MAX ||
+      (size_t)T * k * d * 2 > (size_t)INT32_MAX || (size_t)2 * m * d * 2 > (size_t)INT32_MAX)
+    return MOE_EUNSUPPORTED;
+  if (!(p > 0.0 && p <= 1.0)) return MOE_EINVAL;
+  const bool prev = prev_y_perm || prev_row_of_slot || prev_topk_w;
+  if (prev && !(prev_y_perm && prev_row_of_slot && prev_topk_w)) return MOE_EINVAL;
+  if (!mass || !K_out || !counts || !offsets || !w_gate_up_packed || !w_down_packed) return MOE_EINVAL;
+  if (T > 0 && (!h || !w_r_packed || !logits || !idx_full || !w_full || !idx || !w || !src_of_row ||
+                !row_of_slot || !y_perm))
+    return MOE_EINVAL;
+  if (!aligned_all({prev_y_perm, prev_row_of_slot, prev_topk_w, h, w_r_packed, bias, w_gate_up_packed,
+                    w_down_packed, logits, idx_full, w_full, mass, K_out, idx, w, counts, offsets, src_of_row,
+                    row_of_slot, y_perm, ws}))
+    return MOE_EINVAL;
+  const int rows = T * k;
+  size_t need = 0;
+  if (T > 0) {
+    const size_t a = decomoe::route_rcep_ws_bytes(T, d, E, k), b = ffn_ws_bytes(true, rows, E, d, m);
+    need = a > b ? a : b;
+  }
+  if (need && (!ws || ws_bytes < need)) return MOE_EWORKSPACE;
+  const size_t A = (size_t)rows, nl = (size_t)T * E * 4, xb = (size_t)T * d * 2;
+  const Range hr = rng(h, xb), wr = rng(w_r_packed, (size_t)d * E * 6),
+              bi = bias ? rng(bias, (size_t)E * 4) : Range{0, 0},
+              wgu = rng(w_gate_up_packed, (size_t)E * 2 * m * d * 2), wdn = rng(w_down_packed, (size_t)E * d * m * 2);
+  const Range o_ws = need ? rng(ws, need) : Range{0, 0}, o_ros = rng(row_of_slot, A * 4), o_w = rng(w, A * 4),
+              o_y = rng(y_perm, A * d * 2);
+  const std::initializer_list<Range> outs_rest = {rng(logits, nl), rng(idx_full, A * 4), rng(w_full, A * 4),
+                                                  rng(mass, (size_t)E * 8), rng(K_out, 4), rng(idx, A * 4),
+                                                  rng(counts, (size_t)E * 4), rng(offsets, (size_t)(E + 1) * 4),
+                                                  rng(src_of_row, A * 4), o_ws};
+  if (any_alias({hr}, {wr, bi, wgu, wdn}) || any_alias(outs_rest, {hr, wr, bi, wgu, wdn}) ||
+      any_alias({o_ros, o_w, o_y}, {hr, wr, bi, wgu, wdn}) || any_alias(outs_rest, {o_ros, o_w, o_y}))
+    return MOE_EALIAS;
+  if (prev && T > 0) {
+    // each previous-layer array is this call's array of the same role or
+    // overlaps nothing of the call (it is read by the first launch, before
+    // any launch of the call writes those arrays)
+    const Range q_y = rng(prev_y_perm, A * d * 2), q_r = rng(prev_row_of_slot, A * 4), q_w = rng(prev_topk_w, A * 4);
+    const Range others[] = {hr, wr, bi, wgu, wdn};
+    for (const Range& q : {q_y, q_r, q_w})
+      for (const Range& o : others)
+        if (overlap(q, o)) return MOE_EALIAS;
+    if (any_alias({q_y, q_r, q_w}, outs_rest)) return MOE_EALIAS;
+    if (overlap(q_y, q_r) || overlap(q_y, q_w) || overlap(q_r, q_w)) return MOE_EALIAS;
+    if ((q_y.lo != o_y.lo && (overlap(q_y, o_y) || overlap(q_y, o_ros) || overlap(q_y, o_w))) ||
+        (q_r.lo != o_ros.lo && (overlap(q_r, o_y) || overlap(q_r, o_ros) || overlap(q_r, o_w))) ||
+        (q_w.lo != o_w.lo && (overlap(q_w, o_y) || overlap(q_w, o_ros) || overlap(q_w, o_w))))
+      return MOE_EALIAS;
+  }
+  if (T == 0)
+    return route_rcep(nullptr, dtype, nullptr, nullptr, 0, d, E, k, p, nullptr, nullptr, nullptr, mass, K_out,
+                      nullptr, nullptr, counts, offsets, nullptr, nullptr, ws, ws_bytes, stream, decomoe::Guard{});
+  const bool fold = decomoe::route_rcep_fused(T, E, k) && decomoe::ffn_persistent_available();
+  const decomoe::ZeroAfter za = fold ? decomoe::ffn_counters_zero(ws, rows, E) : decomoe::ZeroAfter{};
+  hipError_t e = decomoe::launch_route_rcep_chained(prev ? prev_y_perm : nullptr, prev_row_of_slot, prev_topk_w, h,
+                                                    w_r_packed, bias, T, d, E, k, p, logits, idx_full, w_full,
+                                                    mass, K_out, idx, w, counts, offsets, src_of_row, row_of_slot,
+                                                    ws, stream, decomoe::Guard{}, za);
+  if (e == hipSuccess)
+    e = decomoe::launch_expert_ffn(h, true, offsets, E, K_out, 1, rows, d, m, w_gate_up_packed, w_down_packed, true,
+                                   y_perm, ws, stream, decomoe::RowGather{src_of_row, k, T}, k, decomoe::Guard{},
+                                   fold);
+  return hip_status(e);
+}
 }  // namespace
 
 extern "C" {
@@ -683,6 +761,18 @@ int moe_rcep_layer_if(const void* x, moe_dtype dtype, const void* w_r_packed, co
   return rcep_layer(x, dtype, w_r_packed, bias, T, d, E, k, p, w_gate_up_packed, w_down_packed, m, residual, out,
                     logits, topk_idx_full, topk_w_full, mass, K_out, topk_idx, topk_w, counts, offsets, src_of_row,
                     row_of_slot, y_perm, ws, ws_bytes, stream, decomoe::Guard{guard, guard_lo, guard_hi});
+}
+
+int moe_rcep_layer_chained(const void* prev_y_perm, const int32_t* prev_row_of_slot, const float* prev_topk_w,
+                           void* h, moe_dtype dtype, const void* w_r_packed, const float* bias, int T, int d, int E,
+                           int k, double p, const void* w_gate_up_packed, const void* w_down_packed, int m,
+                           float* logits, int32_t* topk_idx_full, float* topk_w_full, double* mass, int32_t* K_out,
+                           int32_t* topk_idx, float* topk_w, int32_t* counts, int32_t* offsets, int32_t* src_of_row,
+                           int32_t* row_of_slot, void* y_perm, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return rcep_layer_chained(prev_y_perm, prev_row_of_slot, prev_topk_w, h, dtype, w_r_packed, bias, T, d, E, k, p,
+                            w_gate_up_packed, w_down_packed, m, logits, topk_idx_full, topk_w_full, mass, K_out,
+                            topk_idx, topk_w, counts, offsets, src_of_row, row_of_slot, y_perm, ws, ws_bytes,
+                            stream);
 }
 
 int moe_permute_experts(const int32_t* order, int E, int d, int m, moe_dtype dtype,

@@ -5,14 +5,6 @@
 namespace decomoe {
 namespace {
 
-// 16-byte load with the non-temporal hint: every expert output row is read
-// once, so it should not displace reused lines from the caches (measured at
-// 65 536 rows x top-8, d 2048: 5.1 -> 5.8 TB/s)
-typedef unsigned int u32x4_nt __attribute__((ext_vector_type(4)));
-__device__ __forceinline__ uint4 load_stream(const uint4* p) {
-  const u32x4_nt q = __builtin_nontemporal_load(reinterpret_cast<const u32x4_nt*>(p));
-  return make_uint4(q.x, q.y, q.z, q.w);
-}
 // 16-byte store, non-temporal when NT (outputs larger than the memory-side
 // cache: their dirty lines would otherwise have to be written back before
 // the next kernel's reads can use that cache)

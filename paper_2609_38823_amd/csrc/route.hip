@@ -492,6 +492,34 @@ hipError_t launch_route_rcep(const void* x, const void* w_r_packed, const float*
   return launch_calibrate_route(logits, idx_full, w_full, T, E, k, p, mass, K_out, idx, w, s, g, &so);
 }
 
+hipError_t launch_route_rcep_chained(const void* y_prev, const int32_t* row_prev, const float* w_prev, void* h,
+                                     const void* w_r_packed, const float* bias, int T, int d, int E, int k,
+                                     double p, float* logits, int32_t* idx_full, float* w_full, double* mass,
+                                     int32_t* K_out, int32_t* idx, float* w, int32_t* counts, int32_t* offsets,
+                                     int32_t* src_of_row, int32_t* row_of_slot, void* ws, hipStream_t s, Guard g,
+                                     const ZeroAfter& za) {
+  if (y_prev && combine_router_fits(T, d, E, k) && route_rcep_fused(T, E, k)) {
+    // the previous combine inside the router launch, then the Top-k (which
+    // zeroes the grouping's counter) and the one-launch calibration
+    int* ctr = reinterpret_cast<int*>(static_cast<char*>(ws) + (route_x3_ws_bytes(T, d, E) + 255) / 256 * 256);
+    float* part = nullptr;
+    int S = 1;
+    hipError_t err = launch_combine_router_x3(y_prev, row_prev, w_prev, k, h, w_r_packed, bias, T, d, E, logits, ws,
+                                              part, S, s, g);
+    if (err == hipSuccess)
+      err = launch_topk(logits, T, E, k, nullptr, 1, nullptr, part, S, bias, idx_full, w_full, s, g, ctr);
+    if (err != hipSuccess) return err;
+    const SortOut so{counts, offsets, src_of_row, row_of_slot, ctr, za.p, za.n, za.mark_at, za.mark_val};
+    return launch_calibrate_route(logits, idx_full, w_full, T, E, k, p, mass, K_out, idx, w, s, g, &so);
+  }
+  if (y_prev) {  // the combine on its own, then the routing of the new rows
+    hipError_t err = launch_combine(y_prev, true, row_prev, w_prev, T, k, d, h, h, s, g);
+    if (err != hipSuccess) return err;
+  }
+  return launch_route_rcep(h, w_r_packed, bias, T, d, E, k, p, logits, idx_full, w_full, mass, K_out, idx, w,
+                           counts, offsets, src_of_row, row_of_slot, ws, s, g, za);
+}
+
 // Split factor of the router's d-range: enough workgroups to cover the chip
 // (about 512), in whole 128-wide quarters of d.  1 = no split.
 int router_splits(int T, int d, int E) {
@@ -535,6 +563,12 @@ hipError_t launch_route(const void* x, bool x_bf16, const float* w_r, const void
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
   }
+  return launch_topk(logits, T, E, k, seg_offsets, n_seg, K_dev, part, S, bias, idx, w, s, g, ctr_zero);
+}
+
+hipError_t launch_topk(float* logits, int T, int E, int k, const int32_t* seg_offsets, int n_seg,
+                       const int32_t* K_dev, const float* part, int S, const float* bias, int32_t* idx, float* w,
+                       hipStream_t s, Guard g, int* ctr_zero) {
   // many tokens: four per wavefront (fewer instructions per token); few
   // tokens: one per wavefront (more independent wavefronts, shorter chains).
   // Router + Top-k, measured (E 128, k 8): four per wavefront from 4096

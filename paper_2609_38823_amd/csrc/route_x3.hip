@@ -238,6 +238,194 @@ __global__ __launch_bounds__(256, WPC) void router_x3_kernel(const uint16_t* __r
     }
   }
 }
+
+// The previous layer's combine with the residual, fused into this layer's
+// router: h[t] <- h[t] + sum_j w_prev[t, j] y_prev[row_prev[t, j]]
+// (Algorithm 2's combine, float32 accumulation in slot order and one
+// rounding, as combine_kernel), then the logits of the new rows as
+// router_x3_kernel.  The router's workgroups own disjoint blocks of (token
+// tile) x (d-range of the split), so each workgroup forms exactly the rows
+// and columns it multiplies: it writes them to h and keeps them in LDS as its
+// whole token tile (all stages of its d-range resident, no ring).  One
+// expert group (E <= 128).  Rows past T are zeros in LDS and are not stored.
+template <int MI>
+__global__ __launch_bounds__(256, 2) void combine_router_x3_kernel(
+    const uint16_t* __restrict__ y_prev, const int32_t* __restrict__ row_prev,
+    const float* __restrict__ w_prev, int k_prev, const uint16_t* res, uint16_t* out,
+    const uint16_t* __restrict__ wp, const float* __restrict__ bias, int T, int d, int E,
+    float* __restrict__ logits, float* __restrict__ split_part, const Guard g) {
+  if (guard_skip(g)) return;
+  constexpr int ROWS = 32 * MI;
+  constexpr int SLOT = ROWS * XS_BYTES_ROW;
+  extern __shared__ __attribute__((aligned(1024))) char tile[];  // n_st slots of SLOT bytes
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int KB = d / 16;
+  const int eb_raw = blockIdx.x * 4 + wv;
+  const int n_eb = E / 32;
+  const int eb = eb_raw < n_eb ? eb_raw : n_eb - 1;
+  const int t0 = blockIdx.y * ROWS;
+  const int dch = d / gridDim.z;
+  const int k_begin = blockIdx.z * dch;
+  const int n_st = dch / XS_K;
+  const int A = T * k_prev;
+
+  // the first weight stage does not depend on the combine
+  const int r32 = lane & 31, kh = lane >> 5;
+  const __amdgpu_buffer_rsrc_t w_rs = rsrc(wp + (size_t)eb * KB * 3 * 512, (uint32_t)KB * 3 * 1024);
+  const int kb0 = k_begin / 16;
+  auto load_w = [&](u32x4 (&wf)[4][3], int st) {
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4)
+#pragma unroll
+      for (int p = 0; p < 3; ++p)
+        wf[s4][p] = __builtin_amdgcn_raw_buffer_load_b128(w_rs, lane * 16, ((kb0 + 4 * st + s4) * 3 + p) * 1024, 0);
+  };
+  u32x4 wr[2][4][3];
+  load_w(wr[0], 0);
+
+  // ---- combine.  The tile's slot rows and weights go to LDS once (a slot
+  // outside [0, T k_prev) as -1: it adds nothing); then each thread takes
+  // CB 16-byte chunks at a time and issues all their row loads before the
+  // accumulation.  Chunk q is columns k_begin + 8 (q % cpr) of tile row
+  // q / cpr; the columns of stage c / 8 sit at the router's swizzled place.
+  int* s_row = reinterpret_cast<int*>(tile + n_st * SLOT);
+  float* s_w = reinterpret_cast<float*>(s_row + ROWS * k_prev);
+  for (int i = threadIdx.x; i < ROWS * k_prev; i += 256) {
+    const int t = t0 + i / k_prev;
+    int rr = -1;
+    float wj = 0.f;
+    if (t < T) {
+      rr = row_prev[(size_t)t0 * k_prev + i];
+      wj = w_prev[(size_t)t0 * k_prev + i];
+      if (rr < 0 || rr >= A) rr = -1;
+    }
+    s_row[i] = rr;
+    s_w[i] = wj;
+  }
+  __syncthreads();
+  const int cpr = dch / 8;  // chunks per row
+  const int nq = ROWS * cpr;
+  constexpr int CB = 2;
+  for (int q0 = threadIdx.x; q0 < nq; q0 += 256 * CB) {
+    int r[CB], c[CB];
+    bool live[CB];
+#pragma unroll
+    for (int b = 0; b < CB; ++b) {
+      const int q = q0 + 256 * b;
+      r[b] = q / cpr;
+      c[b] = q % cpr;
+      live[b] = q < nq && t0 + r[b] < T;
+    }
+    float acc[CB][8] = {};
+    uint4 hv[CB];
+#pragma unroll
+    for (int b = 0; b < CB; ++b)
+      hv[b] = live[b] ? *reinterpret_cast<const uint4*>(res + (size_t)(t0 + r[b]) * d + k_begin + 8 * c[b])
+                      : make_uint4(0u, 0u, 0u, 0u);
+    for (int j0 = 0; j0 < k_prev; j0 += 8) {
+      uint4 v[CB][8];
+      int rj[CB][8];
+#pragma unroll
+      for (int b = 0; b < CB; ++b)
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int j = j0 + u;
+          rj[b][u] = live[b] && j < k_prev ? s_row[r[b] * k_prev + j] : -1;
+          const size_t row = rj[b][u] >= 0 ? (size_t)rj[b][u] : 0;
+          v[b][u] = load_stream(reinterpret_cast<const uint4*>(y_prev + row * d + k_begin + 8 * c[b]));
+        }
+#pragma unroll
+      for (int b = 0; b < CB; ++b)
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          if (rj[b][u] < 0) continue;
+          const float wj = s_w[r[b] * k_prev + j0 + u];
+          const uint32_t q4[4] = {v[b][u].x, v[b][u].y, v[b][u].z, v[b][u].w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            acc[b][2 * e] = fmaf(wj, __uint_as_float(q4[e] << 16), acc[b][2 * e]);
+            acc[b][2 * e + 1] = fmaf(wj, __uint_as_float(q4[e] & 0xffff0000u), acc[b][2 * e + 1]);
+          }
+        }
+    }
+#pragma unroll
+    for (int b = 0; b < CB; ++b) {
+      if (q0 + 256 * b >= nq) continue;
+      uint4 o = make_uint4(0u, 0u, 0u, 0u);
+      if (live[b]) {
+        const uint32_t u4[4] = {hv[b].x, hv[b].y, hv[b].z, hv[b].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc[b][2 * e] += __uint_as_float(u4[e] << 16);
+          acc[b][2 * e + 1] += __uint_as_float(u4[e] & 0xffff0000u);
+        }
+        o = make_uint4(pack_bf16x2(acc[b][0], acc[b][1]), pack_bf16x2(acc[b][2], acc[b][3]),
+                       pack_bf16x2(acc[b][4], acc[b][5]), pack_bf16x2(acc[b][6], acc[b][7]));
+        *reinterpret_cast<uint4*>(out + (size_t)(t0 + r[b]) * d + k_begin + 8 * c[b]) = o;
+      }
+      const int cc = c[b] & 7;
+      *reinterpret_cast<uint4*>(tile + (c[b] >> 3) * SLOT + r[b] * XS_BYTES_ROW + ((cc ^ ((r[b] >> 1) & 7)) << 4)) = o;
+    }
+  }
+  __syncthreads();
+
+  // ---- logits of the tile over this d-range (the MFMA order of
+  // router_x3_kernel, so the partial sums are bitwise the same)
+  int x_lane[4];
+#pragma unroll
+  for (int s4 = 0; s4 < 4; ++s4) x_lane[s4] = r32 * 128 + (((2 * s4 + kh) ^ ((r32 >> 1) & 7)) << 4);
+  f32x16 acc[MI];
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[i][e] = 0.f;
+  auto stage = [&](auto U, int st) {
+    constexpr int u = decltype(U)::value;
+    if (st + 1 < n_st) load_w(wr[u ^ 1], st + 1);
+    const char* slot = tile + st * SLOT;
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4) {
+      bf16x8 xf[MI];
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi) xf[mi] = *reinterpret_cast<const bf16x8*>(slot + mi * 32 * 128 + x_lane[s4]);
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int p = 0; p < 3; ++p)
+          acc[mi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, wr[u][s4][p]), xf[mi],
+                                                            acc[mi], 0, 0, 0);
+    }
+  };
+  for (int st = 0; st < n_st; st += 2) {
+    stage(std::integral_constant<int, 0>{}, st);
+    if (st + 1 < n_st) stage(std::integral_constant<int, 1>{}, st + 1);
+  }
+
+  if (eb_raw >= n_eb) return;
+#pragma unroll
+  for (int mi = 0; mi < MI; ++mi) {
+    const int t = t0 + 32 * mi + r32;
+    if (t >= T) continue;
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      const int e = 32 * eb + 8 * gq + 4 * kh;
+      float4 v = make_float4(acc[mi][4 * gq], acc[mi][4 * gq + 1], acc[mi][4 * gq + 2], acc[mi][4 * gq + 3]);
+      if (split_part) {
+        *reinterpret_cast<float4*>(split_part + ((size_t)blockIdx.z * T + t) * E + e) = v;
+      } else {
+        if (bias) {
+          const float4 b = *reinterpret_cast<const float4*>(bias + e);
+          v.x += b.x;
+          v.y += b.y;
+          v.z += b.z;
+          v.w += b.w;
+        }
+        *reinterpret_cast<float4*>(logits + (size_t)t * E + e) = v;
+      }
+    }
+  }
+}
 }  // namespace
 
 // Launch plan: 128-token tiles over the whole d-range once they give every
@@ -291,6 +479,43 @@ hipError_t launch_router_x3(const void* x, const void* w_packed, const float* bi
     router_x3_kernel<2, 2, 2><<<grid, 256, 0, s>>>(xp, wp, bias, T, d, E, logits, part, g);
   else
     router_x3_kernel<1, 2, 2><<<grid, 256, 0, s>>>(xp, wp, bias, T, d, E, logits, part, g);
+  return hipGetLastError();
+}
+
+// The previous layer's combine fused into the router (one expert group, a
+// token tile of at most 32 KB in LDS): false when the plan does not allow it
+// LDS of the fused launch: the token tile of its d-range, then the slot
+// rows and weights of the tile's rows
+static size_t combine_router_lds(const RouterPlan& pl, int d, int k) {
+  return (size_t)32 * pl.MI * (d / pl.S) * 2 + (size_t)32 * pl.MI * k * 8;
+}
+
+bool combine_router_fits(int T, int d, int E, int k) {
+  if (T < 1 || E > 128 || E % 32 != 0 || d % 256 != 0) return false;
+  const RouterPlan pl = router_x3_plan(T, d, E);
+  return (size_t)32 * pl.MI * (d / pl.S) * 2 <= 32768 && combine_router_lds(pl, d, k) <= 49152;
+}
+
+hipError_t launch_combine_router_x3(const void* y_prev, const int32_t* row_prev, const float* w_prev, int k_prev,
+                                    void* h, const void* w_packed, const float* bias, int T, int d, int E,
+                                    float* logits, void* ws, float*& part, int& S, hipStream_t s, Guard g) {
+  const RouterPlan pl = router_x3_plan(T, d, E);
+  S = pl.S;
+  part = S > 1 ? static_cast<float*>(ws) : nullptr;
+  const dim3 grid((E / 32 + 3) / 4, (T + 32 * pl.MI - 1) / (32 * pl.MI), S);
+  const size_t lds = combine_router_lds(pl, d, k_prev);
+  auto yp = static_cast<const uint16_t*>(y_prev);
+  auto hp = static_cast<uint16_t*>(h);
+  auto wp = static_cast<const uint16_t*>(w_packed);
+  if (pl.MI == 4)
+    combine_router_x3_kernel<4><<<grid, 256, lds, s>>>(yp, row_prev, w_prev, k_prev, hp, hp, wp, bias, T, d, E, logits,
+                                                       part, g);
+  else if (pl.MI == 2)
+    combine_router_x3_kernel<2><<<grid, 256, lds, s>>>(yp, row_prev, w_prev, k_prev, hp, hp, wp, bias, T, d, E, logits,
+                                                       part, g);
+  else
+    combine_router_x3_kernel<1><<<grid, 256, lds, s>>>(yp, row_prev, w_prev, k_prev, hp, hp, wp, bias, T, d, E, logits,
+                                                       part, g);
   return hipGetLastError();
 }
 

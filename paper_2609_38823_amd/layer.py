@@ -270,6 +270,23 @@ class MoELayer:
         self._experts(x, b, b.idx, b.w, K_dev=K_dev, stream=stream, mark=mark, residual=residual, out=out)
         return b
 
+    def forward_rcep_chained(self, h: torch.Tensor, p: float, b: Buffers, chained: bool, stream=None,
+                             K_out=None) -> Buffers:
+        """One RCEP layer of a stack whose combines are chained
+        (moe_rcep_layer_chained): with ``chained`` the previous layer's
+        combine with the residual (its y_perm, row_of_slot and re-routed
+        weights, left in ``b``) first updates h in place; then this layer's
+        routing and expert FFN over h.  Its own combine is left in ``b`` for
+        the next chained layer or for moe_combine_residual."""
+        if not (self.packed and self.w_r_packed is not None):
+            raise ValueError("chained layers need packed bf16 weights")
+        K = b.K if K_out is None else K_out
+        prev = (b.y_perm, b.row_of_slot, b.w) if chained else None
+        abi.moe_rcep_layer_chained(prev, h, self.w_r_packed, self.bias, self.k, p, self.w_gate_up, self.w_down,
+                                   b.logits, b.idx_full, b.w_full, b.mass, K, b.idx, b.w, b.counts, b.offsets,
+                                   b.src_of_row, b.row_of_slot, b.y_perm, b.ws, stream=stream)
+        return b
+
     def forward_rcep(self, x: torch.Tensor, p: float, seg_offsets=None, b: Buffers | None = None,
                      stream=None, mark=None, residual=None, out=None, K_out=None, guard=None) -> Buffers:
         """Prefix-restricted layer (from the visual exit on, Algorithm 2).

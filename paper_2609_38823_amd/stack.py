@@ -235,19 +235,41 @@ class MoEStack:
                 self.layer_forward(l, src_full, h_full, False, p, guard=(st.exit_layer, l + 1, L + 1))
                 self.layer_forward(l, h_text, h_text, True, p, guard=(st.exit_layer, 0, l + 1))
 
+    def chainable(self) -> bool:
+        """Every layer has packed bf16 weights (moe_rcep_layer_chained)."""
+        return all(l.packed and l.w_r_packed is not None for l in self.layers)
+
+    def forward_decode(self, x: torch.Tensor, p: float, stream=None) -> torch.Tensor:
+        """RCEP in every layer over x [T, d] with the layers' combines
+        chained: layer l's combine with the residual runs inside layer
+        l + 1's first launch (moe_rcep_layer_chained), the last layer's as
+        moe_combine_residual.  Bitwise forward(x, 0, p, exit_layer=0).
+        Returns the final hidden rows (a buffer owned by the stack)."""
+        T = x.shape[0]
+        b = self.buffers(T)
+        h = self.hidden(T)
+        h.copy_(x)
+        for l, layer in enumerate(self.layers):
+            layer.forward_rcep_chained(h, p, b, l > 0, stream=stream, K_out=self.K_trace[l, :1])
+        abi.moe_combine_residual(b.y_perm, b.row_of_slot, b.w, h, h, stream=stream)
+        return h
+
     def capture_decode(self, x: torch.Tensor, p: float):
         """Capture one decode step (RCEP in every layer) over the static
-        input rows x as a HIP graph.  Returns (graph, out): replaying the
-        graph reads x and leaves the final hidden rows in out."""
+        input rows x as a HIP graph (the chained layers where every layer is
+        packed, else forward).  Returns (graph, out): replaying the graph
+        reads x and leaves the final hidden rows in out."""
+        run = (lambda: self.forward_decode(x, p)) if self.chainable() else \
+            (lambda: self.forward(x, 0, p, exit_layer=0))
         side = torch.cuda.Stream(device=self.device)
         side.wait_stream(torch.cuda.current_stream())
         with torch.cuda.stream(side):
-            self.forward(x, 0, p, exit_layer=0)  # buffers exist before capture
+            run()  # buffers exist before capture
         torch.cuda.current_stream().wait_stream(side)
         torch.cuda.synchronize()
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
-            out = self.forward(x, 0, p, exit_layer=0)
+            out = run()
         return g, out
 
 

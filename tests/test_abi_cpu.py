@@ -37,7 +37,8 @@ def test_header_declares_the_boundary():
         "moe_ffn_status", "moe_expert_ffn_packed_gather_noalloc",
         "moe_route_packed_if", "moe_calibrate_route_prefix_if", "moe_dispatch_if",
         "moe_expert_ffn_packed_gather_if", "moe_combine_residual_if", "moe_savb_gate_if",
-        "moe_route_rcep", "moe_route_rcep_if", "moe_rcep_layer", "moe_rcep_layer_if"])
+        "moe_route_rcep", "moe_route_rcep_if", "moe_rcep_layer", "moe_rcep_layer_if",
+        "moe_rcep_layer_chained"])
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -337,6 +338,44 @@ def test_rcep_layer_rejects(lib):
     G = ctypes.c_void_p(0x7F000000)
     assert call(fi, (ctypes.c_void_p(0x7F000002), 0, 1)) == EINVAL   # misaligned guard
     assert call(fi, (G, 0, 1), wsb=16) == EWORKSPACE
+
+
+def test_rcep_layer_chained_rejects(lib):
+    names = ["py", "pr", "pw", "h", "dt", "wp", "b", "T", "d", "E", "k", "p", "wgu", "wd", "m", "lg", "if_", "wf",
+             "ms", "K", "ix", "w", "cn", "of", "sr", "rs", "yp", "ws", "wsb"]
+    # every array 16 MiB apart (T 64, d 256, E 32, k 8, m 256)
+    arrays = {n: ctypes.c_void_p((i + 1) << 24) for i, n in enumerate(
+        ["py", "pr", "pw", "h", "wp", "wgu", "wd", "lg", "if_", "wf", "ms", "K", "ix", "w", "cn", "of", "sr", "rs",
+         "yp", "ws"])}
+    base = dict(arrays, dt=BF16, b=NULL, T=64, d=256, E=32, k=8, p=0.9, m=256, wsb=1 << 30)
+
+    def call(**kw):
+        a = dict(base)
+        a.update(kw)
+        return lib.moe_rcep_layer_chained(*[a[n] for n in names], NULL)
+
+    def at(n, off):
+        return ctypes.c_void_p(arrays[n].value + off)
+
+    assert call(dt=F32) == EUNSUPPORTED
+    assert call(d=128) == EUNSUPPORTED         # d % 256 == 0
+    assert call(m=128) == EUNSUPPORTED
+    assert call(E=48) == EUNSUPPORTED
+    assert call(k=0) == EINVAL and call(k=33) == EINVAL
+    assert call(p=0.0) == EINVAL and call(p=1.5) == EINVAL
+    assert call(pr=NULL) == EINVAL             # the previous layer's arrays: all or none
+    assert call(py=NULL, pw=NULL) == EINVAL
+    assert call(h=NULL) == EINVAL and call(yp=NULL) == EINVAL
+    assert call(h=at("h", 8)) == EINVAL        # misaligned
+    assert call(wsb=16) == EWORKSPACE
+    assert call(py=arrays["h"]) == EALIAS      # previous expert outputs on top of h
+    assert call(py=arrays["lg"]) == EALIAS     # ... on top of this call's logits
+    assert call(py=at("yp", 512)) == EALIAS    # ... one row into this call's expert outputs
+    assert call(pr=at("rs", 16)) == EALIAS     # row_of_slot shifted by four slots
+    assert call(pr=arrays["w"]) == EALIAS      # previous row_of_slot on this call's weights
+    assert call(pw=arrays["pr"]) == EALIAS     # two previous arrays on one another
+    assert call(yp=arrays["h"]) == EALIAS
+    assert call(ws=arrays["wgu"]) == EALIAS
 
 
 def test_ffn_status_rejects(lib):

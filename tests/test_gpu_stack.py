@@ -359,6 +359,8 @@ def test_decode64_graph(stack48):
     assert ((Ks >= sh.k) & (Ks <= sh.E)).all()
     out = st.forward(x, 0, wl.p, exit_layer=0)
     np.testing.assert_array_equal(host(out), eager)
+    assert st.chainable()
+    np.testing.assert_array_equal(host(st.forward_decode(x, wl.p)), eager)
     g, gout = st.capture_decode(x, wl.p)
     other = to_device(I.tokens(sh, wl.T, seed=wl.seed + 1, stream="decode"), torch.bfloat16)
     for rep in range(3):

@@ -578,6 +578,23 @@ class _RcepLayer:
             abi.moe_combine_residual(o["y"], o["ros"], o["w"], residual, o["out"])
         return o
 
+    def routed(self, x, p, ws, o=None):
+        """The routing and expert FFN of one call, no combine."""
+        o = o if o is not None else self.outs(x.shape[0])
+        abi.moe_route_rcep(x, self.wp, self.bias, self.sh.k, p, o["logits"], o["idx_full"], o["w_full"], o["mass"],
+                           o["K"], o["idx"], o["w"], o["counts"], o["offsets"], o["src"], o["ros"], ws)
+        abi.moe_expert_ffn_packed_gather(x, self.sh.k, o["src"], o["offsets"], self.wgu_p, self.wd_p, o["y"], ws,
+                                         K_dev=o["K"])
+        return o
+
+    def chained(self, prev, h, p, ws, o=None):
+        o = o if o is not None else self.outs(h.shape[0])
+        pv = (prev["y"], prev["ros"], prev["w"]) if prev is not None else None
+        abi.moe_rcep_layer_chained(pv, h, self.wp, self.bias, self.sh.k, p, self.wgu_p, self.wd_p, o["logits"],
+                                   o["idx_full"], o["w_full"], o["mass"], o["K"], o["idx"], o["w"], o["counts"],
+                                   o["offsets"], o["src"], o["ros"], o["y"], ws)
+        return o
+
     def layer(self, x, residual, out, p, ws, guard=None):
         o = self.outs(x.shape[0])
         abi.moe_rcep_layer(x, self.wp, self.bias, self.sh.k, p, self.wgu_p, self.wd_p, residual, out,
@@ -630,6 +647,43 @@ def test_rcep_layer_matches_separate_calls(shape, T):
         want = host(residual).astype(np.float64) + ref["out"]
         assert rel_inf(host(b["out"]), want) <= TOL["bf16"]
         assert row_rel(host(b["out"]), want) <= TOL["bf16"]
+
+
+# qwen 1, 64, 512, e64: the previous combine inside the router's launch;
+# qwen 1025 (T*k > 8192) and e256k20 (E > 128): the combine on its own first
+@pytest.mark.parametrize("shape,T", [("qwen", 64), ("qwen", 512), ("qwen", 1), ("qwen", 1025), ("e64", 300),
+                                     ("e256k20", 100)])
+@pytest.mark.parametrize("shared", [False, True])
+def test_rcep_layer_chained_matches_separate_calls(shape, T, shared):
+    """Two layers through moe_rcep_layer_chained (the first without a
+    previous layer, the second combining the first's expert outputs into h
+    before its routing) against moe_route_rcep + the expert FFN and
+    moe_combine_residual between them: bitwise every output and h.  With
+    `shared` the second call writes the arrays the first wrote (a stack's
+    one set of buffers), on a workspace left holding stale counters."""
+    sh = RCEP_LAYER_SHAPES[shape]
+    L0, L1 = _RcepLayer(sh, seed=23), _RcepLayer(sh, seed=29)
+    p = 0.9
+    x = dev(I.tokens(sh, T, seed=T + 9), torch.bfloat16)
+    ws = ws_for(T, sh.E, sh.k, sh.d, sh.m)
+    h_ref = x.clone()
+    a0 = L0.routed(h_ref, p, ws)
+    abi.moe_combine_residual(a0["y"], a0["ros"], a0["w"], h_ref, h_ref)
+    a1 = L1.routed(h_ref, p, ws)
+    torch.cuda.synchronize()
+    a0 = {n: v.clone() for n, v in a0.items()}
+    ws.fill_(0xA5)
+    h = x.clone()
+    b0 = L0.chained(None, h, p, ws)
+    torch.cuda.synchronize()
+    assert_ffn_ran_all(ws)
+    _assert_same(a0, b0, ALL_OUTS[:-1])
+    assert torch.equal(h.view(torch.uint8), x.view(torch.uint8))
+    b1 = L1.chained(b0, h, p, ws, o=b0 if shared else None)
+    torch.cuda.synchronize()
+    assert_ffn_ran_all(ws)
+    assert torch.equal(h.view(torch.uint8), h_ref.view(torch.uint8))
+    _assert_same(a1, b1, ALL_OUTS[:-1])
 
 
 @pytest.mark.parametrize("shape,T", [("qwen", 64), ("qwen", 1025), ("e64", 300)])
