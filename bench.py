@@ -10,16 +10,17 @@ resident in HBM:
                moe_expert_ffn_packed_gather reading the token rows itself)
                over 4096 rows (3584 visual + 512 text), all 128 experts
   SAVB exit    drop_visual_block removes the 3584 visual rows
-  RCEP span    moe_route (full pool) -> moe_calibrate_route_prefix (s, K
-               with p = 0.9, then the prefix re-route, in one call)
-               -> moe_dispatch -> moe_expert_ffn (experts [0, K))
-               -> moe_combine over the 512 text rows (bf16: the same packed
-               calls)
+  RCEP span    moe_rcep_layer over the 512 text rows: full-pool routing,
+               s and K with p = 0.9, the prefix re-route and the grouping,
+               the expert FFN over experts [0, K), the combine
 
 value = MoE-layer tokens per second over the step (4096 + 512 rows per
-step).  Every ABI call is bracketed by HIP events on the stream it runs on,
-giving per-stage times and the roofline of the dominant kernel (the expert
-FFN).  The CPU oracle is timed on the same step as the CPU baseline.
+step).  In the timed steps every call of the dense span is bracketed by HIP
+events on the stream it runs on, giving its stage times and the roofline of
+the dominant kernel (the expert FFN); the RCEP span's stages are timed in a
+second pass that runs them as separate calls (moe_route_rcep,
+moe_expert_ffn_packed_gather, moe_combine).  The CPU oracle is timed on the
+same step as the CPU baseline.
 
 Other workloads (one JSON line each, same fields):
 
@@ -268,7 +269,12 @@ def bench_layer(args) -> int:
     stream = torch.cuda.current_stream()
     stages = ["route_full", "dispatch", "ffn", "combine", "drop", "r.route_rcep", "r.ffn", "r.combine"]
 
-    def step(ev=None):
+    def step(ev=None, rcep_stages=False):
+        """One step.  With `ev` (len(stages) + 1 events): an event at the
+        start, after each stage of the dense span and the drop, and at the
+        end; with rcep_stages also between the RCEP span's stages, which then
+        run as separate calls (routing, FFN, combine) instead of the one-call
+        layer."""
         marks = iter(ev) if ev is not None else None
 
         def mark():
@@ -279,12 +285,20 @@ def bench_layer(args) -> int:
         layer.forward_dense(x, bd, mark=mark)
         abi.drop_visual_block(x, 0, V, h_text)
         mark()
-        layer.forward_rcep(h_text, p, b=br, mark=mark)
+        layer.forward_rcep(h_text, p, b=br, mark=mark if rcep_stages else None)
+        if ev is not None and not rcep_stages:
+            ev[-1].record(stream)
+
+    def events(n):
+        return [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)] for _ in range(n)]
+
+    def mean_ms(evl, i, j):
+        return float(np.mean([e[i].elapsed_time(e[j]) for e in evl]))
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)] for _ in range(args.steps)]
+    evs = events(args.steps)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
@@ -292,24 +306,31 @@ def bench_layer(args) -> int:
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = wall * 1e3 / args.steps
-    stage_ms = {}
-    for i, name in enumerate(stages):
-        stage_ms[name] = float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs]))
+    # the RCEP span's stages: the same steps again with events between them
+    evp = events(args.steps)
+    for s in range(args.steps):
+        step(evp[s], rcep_stages=True)
+    torch.cuda.synchronize()
+    n_dense = stages.index("r.route_rcep")
+    stage_ms = {name: mean_ms(evs if i < n_dense else evp, i, i + 1) for i, name in enumerate(stages)}
+    rcep_span_ms = mean_ms(evs, n_dense, len(stages))
 
     # the same step with the caches flushed first: a 512 MiB fill (twice the
     # memory-side cache) before each step, each step timed by its own events
     flush = torch.empty((512 << 20,), dtype=torch.uint8, device="cuda")
     n_cold = min(args.steps, 10)
-    evc = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)] for _ in range(n_cold)]
+    evc, evcp = events(n_cold), events(n_cold)
     for s in range(n_cold):
         flush.fill_(s & 0xFF)
         step(evc[s])
+    for s in range(n_cold):
+        flush.fill_(s & 0xFF)
+        step(evcp[s], rcep_stages=True)
     torch.cuda.synchronize()
     del flush
-    warm_span = float(np.mean([e[0].elapsed_time(e[-1]) for e in evs]))
-    cold_span = float(np.mean([e[0].elapsed_time(e[-1]) for e in evc]))
-    cold_stage = {name: round(float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evc])), 4)
-                  for i, name in enumerate(stages)}
+    warm_span = mean_ms(evs, 0, len(stages))
+    cold_span = mean_ms(evc, 0, len(stages))
+    cold_stage = {name: round(mean_ms(evc if i < n_dense else evcp, i, i + 1), 4) for i, name in enumerate(stages)}
     cache = {"warm_event_ms_per_step": round(warm_span, 4), "cold_event_ms_per_step": round(cold_span, 4),
              "cold_tokens_per_s": (T + (T - V)) / (cold_span * 1e-3),
              "cold_stage_ms": cold_stage, "cold_steps": n_cold,
@@ -372,13 +393,14 @@ def bench_layer(args) -> int:
 
     per_tok_flops = 2 * d * E + 6 * k * d * m
     dense_ms = sum(stage_ms[s] for s in ["route_full", "dispatch", "ffn", "combine"])
-    rcep_ms = sum(stage_ms[s] for s in stages if s.startswith("r."))
+    rcep_ms = rcep_span_ms  # the one-call layer, as the timed step runs it
     spans = {
         "dense@4096": dict(ms=round(dense_ms, 4), tokens_per_s=T / dense_ms * 1e3,
                            tflops=per_tok_flops * T / dense_ms / 1e9, touched_experts=touched_d),
         "rcep@512": dict(ms=round(rcep_ms, 4), tokens_per_s=(T - V) / rcep_ms * 1e3,
                          tflops=per_tok_flops * (T - V) / rcep_ms / 1e9, K=K, touched_experts=touched_r,
-                         paper_dense_equiv_tflops=(2 * d * E + 6 * K * d * m) * (T - V) / rcep_ms / 1e9),
+                         paper_dense_equiv_tflops=(2 * d * E + 6 * K * d * m) * (T - V) / rcep_ms / 1e9,
+                         separate_calls_ms=round(sum(stage_ms[s] for s in stages if s.startswith("r.")), 4)),
         "rcep@512 experts, dense-equivalent executor": dict(
             ms=round(dense_equiv_ms, 4), K=K, expert_gflop=6 * K * d * m * (T - V) / 1e9,
             sparse_expert_ms=round(stage_ms["r.ffn"] + stage_ms["r.combine"], 4),

@@ -19,6 +19,7 @@
  *     (same, the dispatch gather folded into the GEMM)            moe_expert_ffn_packed_gather
  *   weighted combine back to token order                          moe_combine
  *     (same, plus the residual of a stack of MoE blocks)          moe_combine_residual
+ *   one whole dense layer (routing through combine and residual)  moe_dense_layer
  *   one whole RCEP layer (routing through combine and residual)   moe_rcep_layer
  *   the previous layer's combine + one RCEP layer up to its FFN    moe_rcep_layer_chained
  *   SAVB visual-block removal from the hidden state (Sec. 3.2)   drop_visual_block
@@ -260,13 +261,43 @@ int moe_route_rcep(const void* x, moe_dtype dtype, const void* w_r_packed, const
                    hipStream_t stream);
 
 /*
+ * moe_dense_layer - one MoE layer over the full expert pool (the layers
+ * before the visual exit in Algorithm 2; Eqs. 1, 10 and App. A.3 Eq. 15),
+ * optionally with the residual: bitwise the outputs of
+ *   moe_route_packed(x, ..., K_dev = NULL)          -> logits, topk_idx, topk_w
+ *   moe_dispatch(topk_idx, ..., x = NULL)           -> counts .. row_of_slot
+ *   moe_expert_ffn_packed_gather(x, T, k, src_of_row, offsets, E,
+ *                                K_dev = NULL, ...) -> y_perm
+ *   moe_combine_residual(y_perm, row_of_slot, topk_w, residual) -> out
+ *   (residual = NULL: moe_combine(y_perm, row_of_slot, topk_w) -> out)
+ * with those calls' arguments, layouts, limits and errors (bf16 only, packed
+ * router and expert weights, 1 <= k <= min(E, 32), d % 256 == 0,
+ * m % 256 == 0).  Every argument is checked before anything is launched.
+ * `out` [T, d] may be `residual`, `x`, or both; any other overlap of out with
+ * an input, and any overlap among the other outputs and inputs, is
+ * MOE_EALIAS.  The router's partial logits and the dispatch's histograms are
+ * placed in ws past the expert FFN's work counters, so the dispatch's first
+ * launch zeroes those counters and the FFN needs no clearing launch of its
+ * own; moe_ffn_status afterwards reports the FFN as for
+ * moe_expert_ffn_packed_gather.  T = 0 writes empty counts and offsets and
+ * launches nothing else.  ws needs moe_workspace_size(T, E, k, d, m, 1)
+ * bytes.
+ */
+int moe_dense_layer(const void* x, moe_dtype dtype, const void* w_r_packed, const float* bias, int T, int d, int E,
+                    int k, const void* w_gate_up_packed, const void* w_down_packed, int m, const void* residual,
+                    void* out, float* logits, int32_t* topk_idx, float* topk_w, int32_t* counts, int32_t* offsets,
+                    int32_t* src_of_row, int32_t* row_of_slot, void* y_perm, void* ws, size_t ws_bytes,
+                    hipStream_t stream);
+
+/*
  * moe_rcep_layer - one RCEP MoE layer over one invocation (Algorithm 2 with
- * the prefix of Eq. 12), residual included: bitwise the outputs of
+ * the prefix of Eq. 12), optionally with the residual: bitwise the outputs of
  *   moe_route_rcep(x, ..., p)                     -> logits .. row_of_slot
  *   moe_expert_ffn_packed_gather(x, T, k, src_of_row, offsets, E,
  *                                K_dev = K_out, n_K = 1, d, m, ...)
  *                                                  -> y_perm
  *   moe_combine_residual(y_perm, row_of_slot, topk_w, residual) -> out
+ *   (residual = NULL: moe_combine(y_perm, row_of_slot, topk_w) -> out)
  * with those calls' arguments, layouts, limits and errors (bf16 only, packed
  * router and expert weights, 1 <= k <= min(E, 32), d % 256 == 0,
  * m % 256 == 0).  Every argument is checked before anything is launched.

@@ -32,7 +32,7 @@ EXPORTS = ("moe_status_string", "moe_workspace_size", "moe_route", "moe_route_pa
            "moe_route_packed_if", "moe_calibrate_route_prefix_if", "moe_dispatch_if",
            "moe_expert_ffn_packed_gather_if", "moe_combine_residual_if", "moe_savb_gate_if",
            "moe_route_rcep", "moe_route_rcep_if", "moe_rcep_layer", "moe_rcep_layer_if",
-           "moe_rcep_layer_chained")
+           "moe_rcep_layer_chained", "moe_dense_layer")
 
 # size of the library's own scratch array of the allocation-free expert FFN
 NOALLOC_SCRATCH_BYTES = 32 << 20
@@ -90,6 +90,8 @@ def load() -> ctypes.CDLL:
                                 _P, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
         "moe_rcep_layer_chained": (_I, [_P, _P, _P, _P, _I, _P, _P, _I, _I, _I, _I, _D, _P, _P, _I, _P, _P,
                                         _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
+        "moe_dense_layer": (_I, [_P, _I, _P, _P, _I, _I, _I, _I, _P, _P, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                 _P, _P, _S, _P]),
         "moe_rcep_layer_if": (_I, [_P, _I, _P, _P, _I, _I, _I, _I, _D, _P, _P, _I, _P, _P, _P, _P, _P, _P,
                                    _P, _P, _P, _P, _P, _P, _P, _P, _P, _S, _P, _I, _I, _P]),
         "moe_route_packed_if": (_I, [_P, _I, _P, _P, _I, _I, _I, _I, _P, _I, _P, _P, _P, _P, _P, _S,
@@ -459,7 +461,8 @@ def moe_rcep_layer(x, w_r_packed, bias, k, p, w_gate_up_packed, w_down_packed, r
                    idx_full, w_full, mass, K_out, idx, w, counts, offsets, src_of_row, row_of_slot, y_perm, ws,
                    guard=None, stream=None):
     """One RCEP layer: moe_route_rcep + moe_expert_ffn_packed_gather (K_dev =
-    K_out) + moe_combine_residual.  `out` may be `residual` and/or `x`.
+    K_out) + moe_combine_residual (residual = None: moe_combine).  `out` may
+    be `residual` and/or `x`.
     With ``guard`` = (g, lo, hi) the predicated form (moe_rcep_layer_if)."""
     T, d = x.shape
     E, two_m, _ = w_gate_up_packed.shape
@@ -472,6 +475,19 @@ def moe_rcep_layer(x, w_r_packed, bias, k, p, w_gate_up_packed, w_down_packed, r
     else:
         gp, lo, hi = _guard(guard)
         _check("moe_rcep_layer_if", load().moe_rcep_layer_if(*args, gp, lo, hi, _stream(stream)))
+
+
+def moe_dense_layer(x, w_r_packed, bias, k, w_gate_up_packed, w_down_packed, residual, out, logits, idx, w,
+                    counts, offsets, src_of_row, row_of_slot, y_perm, ws, stream=None):
+    """One full-pool layer: moe_route_packed + moe_dispatch (x = None) +
+    moe_expert_ffn_packed_gather + moe_combine_residual (residual = None:
+    moe_combine).  `out` may be `residual` and/or `x`."""
+    T, d = x.shape
+    E, two_m, _ = w_gate_up_packed.shape
+    _check("moe_dense_layer", load().moe_dense_layer(
+        _p(x), _dt(x), _p(w_r_packed), _f32(bias), T, d, E, k, _p(w_gate_up_packed), _p(w_down_packed),
+        two_m // 2, _p(residual), _p(out), _f32(logits), _i32(idx), _f32(w), _i32(counts), _i32(offsets),
+        _i32(src_of_row), _i32(row_of_slot), _p(y_perm), _p(ws), _nbytes(ws), _stream(stream)))
 
 
 def moe_rcep_layer_chained(prev, h, w_r_packed, bias, k, p, w_gate_up_packed, w_down_packed, logits, idx_full,

@@ -57,6 +57,7 @@ int hip_status(hipError_t e) { return e == hipSuccess ? MOE_OK : MOE_EHIP; }
 size_t a256(size_t b) { return (b + 255) & ~size_t(255); }
 // shapes of the three-term bf16 router (32-expert blocks, 64-wide k stages)
 bool router_packable(int d, int E) { return E % 32 == 0 && d % 64 == 0; }
+size_t dense_layer_ws_bytes(int T, int d, int E, int k, int m);
 
 // validation shared by the row-major and packed expert FFN entry points
 int expert_ffn(const void* x_perm, moe_dtype dtype, const int32_t* offsets, int E,
@@ -114,7 +115,8 @@ size_t moe_workspace_size(int T, int E, int k, int d, int m, int n_seg) {
                    ffn_ws_bytes(false, (int)rows, E, d, m), a256(route_ws_bytes(T, d, E)),
                    a256(router_packable(d, E) ? decomoe::route_x3_ws_bytes(T, d, E) : 0),
                    a256(router_packable(d, E) && T > 0 ? decomoe::route_rcep_ws_bytes(T, d, E, k) : 0),
-                   a256(calibrate_ws_bytes(T, E))})
+                   a256(calibrate_ws_bytes(T, E)),
+                   router_packable(d, E) && T > 0 ? dense_layer_ws_bytes(T, d, E, k, m) : 0})
     w = b > w ? b : w;
   return w;
 }
@@ -612,7 +614,7 @@ int rcep_layer(const void* x, moe_dtype dtype, const void* w_r_packed, const flo
   if (!(p > 0.0 && p <= 1.0)) return MOE_EINVAL;
   if (!mass || !K_out || !counts || !offsets || !w_gate_up_packed || !w_down_packed) return MOE_EINVAL;
   if (T > 0 && (!x || !w_r_packed || !logits || !idx_full || !w_full || !idx || !w || !src_of_row ||
-                !row_of_slot || !y_perm || !residual || !out))
+                !row_of_slot || !y_perm || !out))
     return MOE_EINVAL;
   if (!aligned_all({x, w_r_packed, bias, w_gate_up_packed, w_down_packed, residual, out, logits, idx_full,
                     w_full, mass, K_out, idx, w, counts, offsets, src_of_row, row_of_slot, y_perm, ws}))
@@ -627,8 +629,8 @@ int rcep_layer(const void* x, moe_dtype dtype, const void* w_r_packed, const flo
   const size_t A = (size_t)rows, nl = (size_t)T * E * 4, xb = (size_t)T * d * 2;
   // out may be the residual rows and x themselves (the hidden state updated
   // in place), but no shifted view of them
-  const Range o = rng(out, xb), r = rng(residual, xb), xi = rng(x, xb);
-  if ((o.lo != r.lo && overlap(o, r)) || (o.lo != xi.lo && overlap(o, xi))) return MOE_EALIAS;
+  const Range o = rng(out, xb), r = residual ? rng(residual, xb) : Range{0, 0}, xi = rng(x, xb);
+  if ((residual && o.lo != r.lo && overlap(o, r)) || (o.lo != xi.lo && overlap(o, xi))) return MOE_EALIAS;
   const Range wr = rng(w_r_packed, (size_t)d * E * 6), bi = bias ? rng(bias, (size_t)E * 4) : Range{0, 0},
               wgu = rng(w_gate_up_packed, (size_t)E * 2 * m * d * 2),
               wdn = rng(w_down_packed, (size_t)E * d * m * 2);
@@ -655,6 +657,73 @@ int rcep_layer(const void* x, moe_dtype dtype, const void* w_r_packed, const flo
                                    true, y_perm, ws, stream, decomoe::RowGather{src_of_row, k, T}, k, g, fold);
   if (e == hipSuccess)
     e = decomoe::launch_combine(y_perm, true, row_of_slot, w, T, k, d, residual, out, stream, g);
+  return hip_status(e);
+}
+
+// moe_dense_layer: see the header
+size_t dense_layer_ws_bytes(int T, int d, int E, int k, int m) {
+  const int rows = T * k;
+  const size_t r = a256(decomoe::route_x3_ws_bytes(T, d, E)), q = a256(dispatch_ws_bytes(T, k, E));
+  const size_t early = decomoe::ffn_counter_span(rows, E) + (r > q ? r : q);
+  const size_t f = ffn_ws_bytes(true, rows, E, d, m);
+  return early > f ? early : f;
+}
+
+int dense_layer(const void* x, moe_dtype dtype, const void* w_r_packed, const float* bias, int T, int d, int E,
+                int k, const void* w_gate_up_packed, const void* w_down_packed, int m, const void* residual,
+                void* out, float* logits, int32_t* idx, float* w, int32_t* counts, int32_t* offsets,
+                int32_t* src_of_row, int32_t* row_of_slot, void* y_perm, void* ws, size_t ws_bytes,
+                hipStream_t stream) {
+  if (!valid_dtype(dtype) || T < 0 || d < 1 || E < 1 || E > kMaxE || k < 1 || k > E || m < 1)
+    return MOE_EINVAL;
+  if (dtype != MOE_BF16 || !router_packable(d, E)) return MOE_EUNSUPPORTED;
+  if (k > kMaxK) return MOE_EUNSUPPORTED;
+  if (d % 256 != 0 || m % 256 != 0) return MOE_EUNSUPPORTED;
+  if ((size_t)T * k > (size_t)INT32_MAX || (size_t)T * d * 2 > (size_t)INT32_MAX ||
+      (size_t)T * k * d * 2 > (size_t)INT32_MAX || (size_t)2 * m * d * 2 > (size_t)INT32_MAX)
+    return MOE_EUNSUPPORTED;
+  if (!counts || !offsets || !w_gate_up_packed || !w_down_packed) return MOE_EINVAL;
+  if (T > 0 && (!x || !w_r_packed || !logits || !idx || !w || !src_of_row || !row_of_slot || !y_perm || !out))
+    return MOE_EINVAL;
+  if (!aligned_all({x, w_r_packed, bias, w_gate_up_packed, w_down_packed, residual, out, logits, idx, w, counts,
+                    offsets, src_of_row, row_of_slot, y_perm, ws}))
+    return MOE_EINVAL;
+  const size_t need = T > 0 ? dense_layer_ws_bytes(T, d, E, k, m) : 0;
+  if (need && (!ws || ws_bytes < need)) return MOE_EWORKSPACE;
+  const size_t A = (size_t)T * k, xb = (size_t)T * d * 2;
+  // out may be the residual rows and x themselves, but no shifted view of them
+  const Range o = rng(out, xb), r = residual ? rng(residual, xb) : Range{0, 0}, xi = rng(x, xb);
+  if ((residual && o.lo != r.lo && overlap(o, r)) || (o.lo != xi.lo && overlap(o, xi))) return MOE_EALIAS;
+  const Range wr = rng(w_r_packed, (size_t)d * E * 6), bi = bias ? rng(bias, (size_t)E * 4) : Range{0, 0},
+              wgu = rng(w_gate_up_packed, (size_t)E * 2 * m * d * 2),
+              wdn = rng(w_down_packed, (size_t)E * d * m * 2);
+  if (any_alias({o}, {wr, bi, wgu, wdn}) ||
+      any_alias({rng(logits, (size_t)T * E * 4), rng(idx, A * 4), rng(w, A * 4), rng(counts, (size_t)E * 4),
+                 rng(offsets, (size_t)(E + 1) * 4), rng(src_of_row, A * 4), rng(row_of_slot, A * 4),
+                 rng(y_perm, A * d * 2), need ? rng(ws, need) : Range{0, 0}},
+                {xi, r, o, wr, bi, wgu, wdn}))
+    return MOE_EALIAS;
+  if (T == 0)  // empty counts and offsets; nothing else to do
+    return hip_status(decomoe::launch_dispatch(nullptr, 0, k, E, nullptr, 2, 0, counts, offsets, nullptr, nullptr,
+                                               nullptr, nullptr, stream));
+  // the router's partial logits and the dispatch's histograms sit past the
+  // expert FFN's counters, which the dispatch's first launch then zeroes:
+  // the FFN runs without a clearing launch of its own
+  const int rows = T * k;
+  void* early = static_cast<char*>(ws) + decomoe::ffn_counter_span(rows, E);
+  const bool fold = decomoe::ffn_persistent_available();
+  const decomoe::ZeroAfter za = fold ? decomoe::ffn_counters_zero(ws, rows, E) : decomoe::ZeroAfter{};
+  hipError_t e = decomoe::launch_route(x, true, nullptr, w_r_packed, bias, T, d, E, k, nullptr, 1, nullptr, logits,
+                                       idx, w, early, stream);
+  if (e == hipSuccess)
+    e = decomoe::launch_dispatch(idx, T, k, E, nullptr, 2, 0, counts, offsets, src_of_row, row_of_slot, nullptr,
+                                 early, stream, decomoe::Guard{}, za);
+  if (e == hipSuccess)
+    e = decomoe::launch_expert_ffn(x, true, offsets, E, nullptr, 0, rows, d, m, w_gate_up_packed, w_down_packed,
+                                   true, y_perm, ws, stream, decomoe::RowGather{src_of_row, k, T}, k,
+                                   decomoe::Guard{}, fold);
+  if (e == hipSuccess) e = decomoe::launch_combine(y_perm, true, row_of_slot, w, T, k, d, residual, out, stream,
+                                                   decomoe::Guard{});
   return hip_status(e);
 }
 
@@ -761,6 +830,15 @@ int moe_rcep_layer_if(const void* x, moe_dtype dtype, const void* w_r_packed, co
   return rcep_layer(x, dtype, w_r_packed, bias, T, d, E, k, p, w_gate_up_packed, w_down_packed, m, residual, out,
                     logits, topk_idx_full, topk_w_full, mass, K_out, topk_idx, topk_w, counts, offsets, src_of_row,
                     row_of_slot, y_perm, ws, ws_bytes, stream, decomoe::Guard{guard, guard_lo, guard_hi});
+}
+
+int moe_dense_layer(const void* x, moe_dtype dtype, const void* w_r_packed, const float* bias, int T, int d, int E,
+                    int k, const void* w_gate_up_packed, const void* w_down_packed, int m, const void* residual,
+                    void* out, float* logits, int32_t* topk_idx, float* topk_w, int32_t* counts, int32_t* offsets,
+                    int32_t* src_of_row, int32_t* row_of_slot, void* y_perm, void* ws, size_t ws_bytes,
+                    hipStream_t stream) {
+  return dense_layer(x, dtype, w_r_packed, bias, T, d, E, k, w_gate_up_packed, w_down_packed, m, residual, out,
+                     logits, topk_idx, topk_w, counts, offsets, src_of_row, row_of_slot, y_perm, ws, ws_bytes, stream);
 }
 
 int moe_rcep_layer_chained(const void* prev_y_perm, const int32_t* prev_row_of_slot, const float* prev_topk_w,

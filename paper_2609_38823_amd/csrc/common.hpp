@@ -102,8 +102,9 @@ struct SortOut {
   int* zero = nullptr;  // then n_zero ints set to 0 (mark_val at mark_at)
   int n_zero = 0, mark_at = -1, mark_val = 0;
 };
-// ints a launch sets after its last use of the workspace (0, and mark_val at
-// mark_at): the next call's counters, so that it needs no clearing launch
+// ints a launch sets where it no longer uses, or never uses, that part of the
+// workspace (0, and mark_val at mark_at): the counters of the call that
+// follows, so that it needs no clearing launch
 struct ZeroAfter {
   int* p = nullptr;
   int n = 0, mark_at = -1, mark_val = 0;
@@ -136,12 +137,16 @@ size_t dispatch_ws_bytes(int T, int k, int E);
 hipError_t launch_dispatch(const int32_t* idx, int T, int k, int E, const void* x, int elt, int d,
                            int32_t* counts, int32_t* offsets, int32_t* src_of_row,
                            int32_t* row_of_slot, void* x_perm, void* ws, hipStream_t s,
-                           Guard g = Guard{});
+                           Guard g = Guard{}, const ZeroAfter& za = ZeroAfter{});
 hipError_t launch_expand_dense(const int32_t* idx, const float* w, int T, int k, int E,
                                const int32_t* K_dev, int32_t* idx_dense, float* w_dense, hipStream_t s);
 size_t ffn_ws_bytes(bool bf16, int rows_max, int E, int d, int m);
 // bytes of the expert FFN's counter header for rows_max rows and E experts
 size_t ffn_ctr_bytes(int rows_max, int E);
+// bytes from the start of the workspace past the expert FFN's counters (a
+// multiple of 256): scratch of earlier launches placed there leaves the
+// counters alone
+size_t ffn_counter_span(int rows_max, int E);
 // Token rows of the gate/up GEMM: x_perm [rows_max, d] when src_of_row is
 // NULL; else x [T, d] with dispatched row r read from x[src_of_row[r] / k]
 // (packed weights only)

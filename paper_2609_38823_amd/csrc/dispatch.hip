@@ -24,10 +24,20 @@ constexpr int DP_CHUNK = 1024;  // assignments per chunk
 constexpr int DP_THREADS = 256;  // 4 wavefronts, 256 assignments each
 constexpr int DP_PER_WAVE = DP_CHUNK / (DP_THREADS / kWave);
 
+// zero[0, n_zero) <- 0, mark_val at mark_at: the counters of a launch that
+// follows (the expert FFN's), set by the first workgroup
+__device__ __forceinline__ void zero_ints(int* zero, int n_zero, int mark_at, int mark_val, int nthr) {
+  if (blockIdx.x != 0) return;
+  for (int i = threadIdx.x; i < n_zero; i += nthr) zero[i] = i == mark_at ? mark_val : 0;
+}
+
 __global__ __launch_bounds__(DP_THREADS) void dispatch_hist_kernel(const int32_t* __restrict__ idx,
                                                                    int A, int E,
-                                                                   int32_t* __restrict__ hist, const Guard g) {
+                                                                   int32_t* __restrict__ hist, int* zero,
+                                                                   int n_zero, int mark_at, int mark_val,
+                                                                   const Guard g) {
   if (guard_skip(g)) return;
+  zero_ints(zero, n_zero, mark_at, mark_val, DP_THREADS);
   __shared__ int h[1024];
   for (int e = threadIdx.x; e < E; e += DP_THREADS) h[e] = 0;
   __syncthreads();
@@ -265,8 +275,9 @@ __global__ __launch_bounds__(DP_THREADS) void dispatch_rank_kernel(
 __global__ __launch_bounds__(DS_THREADS) void dispatch_sort_small_kernel(
     const int32_t* __restrict__ idx, int A, int E, int key_bits, int32_t* __restrict__ counts,
     int32_t* __restrict__ offsets, int32_t* __restrict__ src_of_row,
-    int32_t* __restrict__ row_of_slot, const Guard g) {
+    int32_t* __restrict__ row_of_slot, int* zero, int n_zero, int mark_at, int mark_val, const Guard g) {
   if (guard_skip(g)) return;
+  zero_ints(zero, n_zero, mark_at, mark_val, DS_THREADS);
   __shared__ int wh[DS_WAVES][1024];  // per-wave counts, then per-wave starting rows
   __shared__ int part[DS_WAVES];
   sort_small(idx, A, E, key_bits, &wh[0][0], 1024, part, counts, offsets, src_of_row, row_of_slot);
@@ -334,7 +345,8 @@ size_t dispatch_ws_bytes(int T, int k, int E) {
 
 hipError_t launch_dispatch(const int32_t* idx, int T, int k, int E, const void* x, int elt, int d,
                            int32_t* counts, int32_t* offsets, int32_t* src_of_row,
-                           int32_t* row_of_slot, void* x_perm, void* ws, hipStream_t s, Guard g) {
+                           int32_t* row_of_slot, void* x_perm, void* ws, hipStream_t s, Guard g,
+                           const ZeroAfter& za) {
   const int A = T * k;
   const int n_chunks = (A + DP_CHUNK - 1) / DP_CHUNK;
   int32_t* hist = static_cast<int32_t*>(ws);
@@ -343,12 +355,13 @@ hipError_t launch_dispatch(const int32_t* idx, int T, int k, int E, const void* 
   while ((1 << key_bits) < E) ++key_bits;
   hipError_t err;
   if (A <= DS_MAX) {
-    dispatch_sort_small_kernel<<<1, DS_THREADS, 0, s>>>(idx, A, E, key_bits, counts, offsets,
-                                                        src_of_row, row_of_slot, g);
+    dispatch_sort_small_kernel<<<1, DS_THREADS, 0, s>>>(idx, A, E, key_bits, counts, offsets, src_of_row,
+                                                        row_of_slot, za.p, za.n, za.mark_at, za.mark_val, g);
     err = hipGetLastError();
     if (err != hipSuccess || A == 0) return err;
   } else {
-    dispatch_hist_kernel<<<n_chunks, DP_THREADS, 0, s>>>(idx, A, E, hist, g);
+    dispatch_hist_kernel<<<n_chunks, DP_THREADS, 0, s>>>(idx, A, E, hist, za.p, za.n, za.mark_at, za.mark_val,
+                                                         g);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
     if (n_chunks <= DP_FUSE_CHUNKS) {

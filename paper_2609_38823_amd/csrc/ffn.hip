@@ -1529,6 +1529,8 @@ hipError_t launch_packed(int bm, const Tiles& t0, int nn1, const uint16_t* X, co
 size_t ffn_ctr_bytes(int rows_max, int E) {
   return align256((size_t)(kern::FFN_CTR_TILES + max_tiles_for(rows_max, E, 64)) * 4);
 }
+size_t ffn_counter_span(int rows_max, int E) { return 256 + ffn_ctr_bytes(rows_max, E); }
+
 size_t ffn_ws_bytes(bool bf16, int rows_max, int E, int d, int m) {
   (void)d;
   return 256 + ffn_ctr_bytes(rows_max, E) + align256((size_t)rows_max * m * (bf16 ? 2 : 4));

@@ -174,6 +174,12 @@ class MoELayer:
         else:
             abi.moe_route(x, self.w_r, self.bias, self.k, b.logits, idx, w, ws=b.ws, stream=stream)
 
+    @property
+    def one_call(self) -> bool:
+        """Packed weights of the shapes the one-call layers take
+        (moe_dense_layer, moe_rcep_layer)."""
+        return self.packed and self.w_r_packed is not None and self.k <= 32
+
     def buffers(self, T: int, n_seg: int = 1) -> Buffers:
         key = (T, n_seg)
         if key not in self._bufs:
@@ -233,6 +239,13 @@ class MoELayer:
         lo <= g[0] < hi (packed layers, with a residual)."""
         self._check_guard(guard)
         b = b or self.buffers(x.shape[0])
+        if self.one_call and mark is None and guard is None:
+            # the whole layer in one call (the dispatch also clears the
+            # expert FFN's counters)
+            abi.moe_dense_layer(x, self.w_r_packed, self.bias, self.k, self.w_gate_up, self.w_down, residual,
+                                b.out if out is None else out, b.logits, b.idx, b.w, b.counts, b.offsets,
+                                b.src_of_row, b.row_of_slot, b.y_perm, b.ws, stream=stream)
+            return b
         self._route(x, b, b.idx, b.w, stream=stream, guard=guard)
         if mark:
             mark()
@@ -278,7 +291,7 @@ class MoELayer:
         weights, left in ``b``) first updates h in place; then this layer's
         routing and expert FFN over h.  Its own combine is left in ``b`` for
         the next chained layer or for moe_combine_residual."""
-        if not (self.packed and self.w_r_packed is not None):
+        if not self.one_call:
             raise ValueError("chained layers need packed bf16 weights")
         K = b.K if K_out is None else K_out
         prev = (b.y_perm, b.row_of_slot, b.w) if chained else None
@@ -297,11 +310,9 @@ class MoELayer:
         b = b or self.buffers(x.shape[0], n_seg)
         K = b.K if K_out is None else K_out
         mk = mark or (lambda: None)
-        if seg_offsets is None and self.packed and self.w_r_packed is not None and residual is not None \
-                and mark is None:
-            # one invocation on packed weights, residual included: the whole
-            # layer in one call (its routing launch also clears the expert
-            # FFN's counters)
+        if seg_offsets is None and self.one_call and mark is None:
+            # one invocation on packed weights: the whole layer in one call
+            # (its routing launch also clears the expert FFN's counters)
             abi.moe_rcep_layer(x, self.w_r_packed, self.bias, self.k, p, self.w_gate_up, self.w_down, residual,
                                b.out if out is None else out, b.logits, b.idx_full, b.w_full, b.mass, K, b.idx,
                                b.w, b.counts, b.offsets, b.src_of_row, b.row_of_slot, b.y_perm, b.ws,

@@ -237,7 +237,7 @@ class MoEStack:
 
     def chainable(self) -> bool:
         """Every layer has packed bf16 weights (moe_rcep_layer_chained)."""
-        return all(l.packed and l.w_r_packed is not None for l in self.layers)
+        return all(l.one_call for l in self.layers)
 
     def forward_decode(self, x: torch.Tensor, p: float, stream=None) -> torch.Tensor:
         """RCEP in every layer over x [T, d] with the layers' combines

@@ -38,7 +38,7 @@ def test_header_declares_the_boundary():
         "moe_route_packed_if", "moe_calibrate_route_prefix_if", "moe_dispatch_if",
         "moe_expert_ffn_packed_gather_if", "moe_combine_residual_if", "moe_savb_gate_if",
         "moe_route_rcep", "moe_route_rcep_if", "moe_rcep_layer", "moe_rcep_layer_if",
-        "moe_rcep_layer_chained"])
+        "moe_rcep_layer_chained", "moe_dense_layer"])
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -324,7 +324,7 @@ def test_rcep_layer_rejects(lib):
     assert call(E=48) == EUNSUPPORTED          # packed router: E % 32 == 0
     assert call(k=0) == EINVAL and call(k=33) == EINVAL
     assert call(p=0.0) == EINVAL
-    assert call(res=NULL) == EINVAL and call(yp=NULL) == EINVAL
+    assert call(out=NULL) == EINVAL and call(yp=NULL) == EINVAL
     assert call(yp=ctypes.c_void_p(arrays["yp"].value + 8)) == EINVAL
     assert call(wsb=16) == EWORKSPACE
     # out one row past the residual: neither in place nor disjoint
@@ -338,6 +338,35 @@ def test_rcep_layer_rejects(lib):
     G = ctypes.c_void_p(0x7F000000)
     assert call(fi, (ctypes.c_void_p(0x7F000002), 0, 1)) == EINVAL   # misaligned guard
     assert call(fi, (G, 0, 1), wsb=16) == EWORKSPACE
+
+
+def test_dense_layer_rejects(lib):
+    names = ["x", "dt", "wp", "b", "T", "d", "E", "k", "wgu", "wd", "m", "res", "out", "lg", "ix", "w", "cn", "of",
+             "sr", "rs", "yp", "ws", "wsb"]
+    # every array 16 MiB apart (T 64, d 256, E 32, k 8, m 256)
+    arrays = {n: ctypes.c_void_p((i + 1) << 24) for i, n in enumerate(
+        ["x", "wp", "wgu", "wd", "res", "out", "lg", "ix", "w", "cn", "of", "sr", "rs", "yp", "ws"])}
+    base = dict(arrays, dt=BF16, b=NULL, T=64, d=256, E=32, k=8, m=256, wsb=1 << 30)
+
+    def call(**kw):
+        a = dict(base)
+        a.update(kw)
+        return lib.moe_dense_layer(*[a[n] for n in names], NULL)
+
+    assert call(dt=F32) == EUNSUPPORTED
+    assert call(d=128) == EUNSUPPORTED and call(m=128) == EUNSUPPORTED
+    assert call(E=48) == EUNSUPPORTED         # packed router: E % 32 == 0
+    assert call(k=0) == EINVAL and call(k=33) == EINVAL
+    assert call(out=NULL) == EINVAL and call(yp=NULL) == EINVAL and call(sr=NULL) == EINVAL
+    assert call(yp=ctypes.c_void_p(arrays["yp"].value + 8)) == EINVAL
+    assert call(wsb=16) == EWORKSPACE
+    assert call(out=ctypes.c_void_p(arrays["res"].value + 512)) == EALIAS   # one row past the residual
+    assert call(out=ctypes.c_void_p(arrays["x"].value + 512)) == EALIAS
+    assert call(out=arrays["wgu"]) == EALIAS
+    assert call(yp=arrays["x"]) == EALIAS
+    assert call(ws=arrays["res"]) == EALIAS
+    assert call(ix=arrays["w"]) == EALIAS
+    assert call(lg=arrays["wp"]) == EALIAS
 
 
 def test_rcep_layer_chained_rejects(lib):

@@ -575,7 +575,10 @@ class _RcepLayer:
         if x.shape[0]:
             abi.moe_expert_ffn_packed_gather(x, self.sh.k, o["src"], o["offsets"], self.wgu_p, self.wd_p, o["y"],
                                              ws, K_dev=o["K"])
-            abi.moe_combine_residual(o["y"], o["ros"], o["w"], residual, o["out"])
+            if residual is None:
+                abi.moe_combine(o["y"], o["ros"], o["w"], o["out"])
+            else:
+                abi.moe_combine_residual(o["y"], o["ros"], o["w"], residual, o["out"])
         return o
 
     def routed(self, x, p, ws, o=None):
@@ -616,14 +619,17 @@ ALL_OUTS = ("logits", "idx_full", "w_full", "mass", "K", "idx", "w", "counts", "
 # T*k <= 8192: the routing's one-launch grouping also clears the expert
 # FFN's counters (qwen 1, 64, 512, 1024; e64; e256k20); beyond, the
 # separate launches with the FFN's own clearing (qwen 1025, e64 2100)
-@pytest.mark.parametrize("shape,T", [("qwen", 512), ("qwen", 64), ("qwen", 1), ("qwen", 1024), ("qwen", 1025),
-                                     ("e64", 300), ("e64", 2100), ("e256k20", 100), ("e64", 0)])
-def test_rcep_layer_matches_separate_calls(shape, T):
+# (no_res: residual NULL, the plain combine)
+@pytest.mark.parametrize("shape,T,no_res", [("qwen", 512, False), ("qwen", 64, False), ("qwen", 1, False),
+                                            ("qwen", 1024, False), ("qwen", 1025, False), ("e64", 300, False),
+                                            ("e64", 2100, False), ("e256k20", 100, False), ("e64", 0, False),
+                                            ("qwen", 512, True), ("qwen", 1025, True), ("e64", 300, True)])
+def test_rcep_layer_matches_separate_calls(shape, T, no_res):
     sh = RCEP_LAYER_SHAPES[shape]
     L = _RcepLayer(sh, seed=13)
     p = 0.9
     x = dev(I.tokens(sh, max(T, 1), seed=T + 5)[:T], torch.bfloat16)
-    residual = dev(I.synthetic_rows(max(T, 1), sh.d, "bf16", seed=T + 6)[:T], torch.bfloat16)
+    residual = None if no_res else dev(I.synthetic_rows(max(T, 1), sh.d, "bf16", seed=T + 6)[:T], torch.bfloat16)
     ws = ws_for(T, sh.E, sh.k, sh.d, sh.m)
     a = L.separate(x, residual, p, ws)
     ws.fill_(0xA5)  # the composed call starts from a workspace holding stale counters
@@ -644,9 +650,61 @@ def test_rcep_layer_matches_separate_calls(shape, T):
         ref = oracle.moe_layer_rcep(host(x), L.rp["w_r"], L.rp["bias"], L.prm["w_gate_up"], L.prm["w_down"],
                                     sh.k, p, logits=host(b["logits"]), K_override=[K])
         np.testing.assert_array_equal(host(b["idx"]), ref["idx"])
-        want = host(residual).astype(np.float64) + ref["out"]
+        want = ref["out"] if residual is None else host(residual).astype(np.float64) + ref["out"]
         assert rel_inf(host(b["out"]), want) <= TOL["bf16"]
         assert row_rel(host(b["out"]), want) <= TOL["bf16"]
+
+
+def _dense_outs(T, sh):
+    E, k, d = sh.E, sh.k, sh.d
+    A = T * k
+    return dict(logits=f32((T, E)), idx=i32((T, k)), w=f32((T, k)), counts=i32((E,)), offsets=i32((E + 1,)),
+                src=i32((A,)), ros=i32((A,)), y=torch.full((A, d), 7.0, dtype=torch.bfloat16, device="cuda"))
+
+
+DENSE_OUTS = ("logits", "idx", "w", "counts", "offsets", "src", "ros", "y", "out")
+
+
+# T*k <= 8192: the one-workgroup grouping (qwen 1, 64, 1024; e64; e256k20);
+# up to 64 chunks of 1024 entries the fused scan and rank (qwen 1025, 4096),
+# beyond, histogram, scan and rank launches (qwen 9000)
+@pytest.mark.parametrize("shape,T,no_res", [("qwen", 64, False), ("qwen", 1, False), ("qwen", 1024, False),
+                                            ("qwen", 1025, False), ("qwen", 4096, True), ("qwen", 9000, False),
+                                            ("e64", 300, True), ("e256k20", 100, False), ("e64", 0, False)])
+def test_dense_layer_matches_separate_calls(shape, T, no_res):
+    """moe_dense_layer against moe_route_packed + moe_dispatch + the
+    gathering expert FFN + the combine (with the residual, or without):
+    bitwise every output, on a workspace left holding stale counters, and
+    the FFN ran every item with no clearing launch of its own."""
+    sh = RCEP_LAYER_SHAPES[shape]
+    L = _RcepLayer(sh, seed=31)
+    x = dev(I.tokens(sh, max(T, 1), seed=T + 11)[:T], torch.bfloat16)
+    residual = None if no_res else dev(I.synthetic_rows(max(T, 1), sh.d, "bf16", seed=T + 12)[:T], torch.bfloat16)
+    ws = ws_for(T, sh.E, sh.k, sh.d, sh.m)
+    a = _dense_outs(T, sh)
+    a["out"] = torch.full_like(x, 5.0)
+    if T:
+        abi.moe_route_packed(x, L.wp, L.bias, sh.k, a["logits"], a["idx"], a["w"], ws=ws)
+    abi.moe_dispatch(a["idx"], sh.E, None, a["counts"], a["offsets"], a["src"], a["ros"], None, ws)
+    if T:
+        abi.moe_expert_ffn_packed_gather(x, sh.k, a["src"], a["offsets"], L.wgu_p, L.wd_p, a["y"], ws)
+        if residual is None:
+            abi.moe_combine(a["y"], a["ros"], a["w"], a["out"])
+        else:
+            abi.moe_combine_residual(a["y"], a["ros"], a["w"], residual, a["out"])
+    torch.cuda.synchronize()
+    ws.fill_(0xA5)
+    b = _dense_outs(T, sh)
+    b["out"] = torch.full_like(x, 5.0)
+    abi.moe_dense_layer(x, L.wp, L.bias, sh.k, L.wgu_p, L.wd_p, residual, b["out"], b["logits"], b["idx"], b["w"],
+                        b["counts"], b["offsets"], b["src"], b["ros"], b["y"], ws)
+    torch.cuda.synchronize()
+    if T == 0:
+        _assert_same(a, b, ("counts", "offsets"))
+        return
+    path, _ = assert_ffn_ran_all(ws)
+    assert path == abi.FFN_PATH_PERSISTENT
+    _assert_same(a, b, DENSE_OUTS)
 
 
 # qwen 1, 64, 512, e64: the previous combine inside the router's launch;
