@@ -112,6 +112,11 @@ class MoEStack:
         Table 2): "rcep" (Eq. 12), "dense" (all experts: the visual exit
         alone) or "fixed" (the prefix length K_fixed: a host int, checked
         against [k, E], or a device int32 tensor).
+        With packed weights and no hook, the RCEP layers are chained
+        (moe_rcep_layer_chained): layer l's combine with the residual runs
+        inside layer l + 1's first launch, the last one's as
+        moe_combine_residual; the results are bitwise those of the separate
+        calls.
         """
         if after_exit not in ("rcep", "dense", "fixed"):
             raise ValueError("after_exit is 'rcep', 'dense' or 'fixed'")
@@ -120,6 +125,8 @@ class MoEStack:
         T = x.shape[0]
         src = x
         h = self.hidden(T)
+        chain = hook is None and after_exit == "rcep" and exit_layer is not None and exit_layer < self.L \
+            and self.chainable()
         for l in range(self.L):
             if exit_layer is not None and l == exit_layer and n_visual > 0:
                 ht = self.hidden(T - n_visual, "text")
@@ -128,10 +135,20 @@ class MoEStack:
             if hook:
                 hook(l, src)
             rcep = exit_layer is not None and l >= exit_layer and after_exit != "dense"
+            if chain and rcep:
+                if src is x:  # no layer before the exit: the rows are updated in a copy
+                    h.copy_(x)
+                    src = h
+                self.layers[l].forward_rcep_chained(src, p, self.buffers(src.shape[0]), l > exit_layer,
+                                                    stream=stream, K_out=self.K_trace[l, :1])
+                continue
             dst = h if src is x else src
             self.layer_forward(l, src, dst, rcep, p, stream=stream,
                                K_fixed=K_fixed if after_exit == "fixed" else None)
             src = dst
+        if chain:
+            b = self.buffers(src.shape[0])
+            abi.moe_combine_residual(b.y_perm, b.row_of_slot, b.w, src, src, stream=stream)
         return src
 
     def forward_gated(self, x: torch.Tensor, n_visual: int, p: float, gates: dict, theta: float,
@@ -241,26 +258,21 @@ class MoEStack:
 
     def forward_decode(self, x: torch.Tensor, p: float, stream=None) -> torch.Tensor:
         """RCEP in every layer over x [T, d] with the layers' combines
-        chained: layer l's combine with the residual runs inside layer
-        l + 1's first launch (moe_rcep_layer_chained), the last layer's as
-        moe_combine_residual.  Bitwise forward(x, 0, p, exit_layer=0).
-        Returns the final hidden rows (a buffer owned by the stack)."""
-        T = x.shape[0]
-        b = self.buffers(T)
-        h = self.hidden(T)
-        h.copy_(x)
-        for l, layer in enumerate(self.layers):
-            layer.forward_rcep_chained(h, p, b, l > 0, stream=stream, K_out=self.K_trace[l, :1])
-        abi.moe_combine_residual(b.y_perm, b.row_of_slot, b.w, h, h, stream=stream)
-        return h
+        chained (forward with exit_layer 0 on a stack of packed layers):
+        layer l's combine with the residual runs inside layer l + 1's first
+        launch (moe_rcep_layer_chained), the last layer's as
+        moe_combine_residual.  Returns the final hidden rows (a buffer owned
+        by the stack)."""
+        if not self.chainable():
+            raise ValueError("chained decode needs packed bf16 layers")
+        return self.forward(x, 0, p, exit_layer=0, stream=stream)
 
     def capture_decode(self, x: torch.Tensor, p: float):
-        """Capture one decode step (RCEP in every layer) over the static
-        input rows x as a HIP graph (the chained layers where every layer is
-        packed, else forward).  Returns (graph, out): replaying the graph
+        """Capture one decode step (RCEP in every layer, forward with
+        exit_layer 0: the chained layers where every layer is packed) over
+        the static input rows x as a HIP graph.  Returns (graph, out): replaying the graph
         reads x and leaves the final hidden rows in out."""
-        run = (lambda: self.forward_decode(x, p)) if self.chainable() else \
-            (lambda: self.forward(x, 0, p, exit_layer=0))
+        run = lambda: self.forward(x, 0, p, exit_layer=0)  # noqa: E731
         side = torch.cuda.Stream(device=self.device)
         side.wait_stream(torch.cuda.current_stream())
         with torch.cuda.stream(side):
