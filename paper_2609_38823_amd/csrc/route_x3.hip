@@ -246,8 +246,9 @@ __global__ __launch_bounds__(256, WPC) void router_x3_kernel(const uint16_t* __r
 // router_x3_kernel.  The router's workgroups own disjoint blocks of (token
 // tile) x (d-range of the split), so each workgroup forms exactly the rows
 // and columns it multiplies: it writes them to h and keeps them in LDS as its
-// whole token tile (all stages of its d-range resident, no ring).  One
-// expert group (E <= 128).  Rows past T are zeros in LDS and are not stored.
+// whole token tile (all stages of its d-range resident, no ring), after the
+// tile's slot rows and weights (32 MI k_prev of each).  One expert group
+// (E <= 128).  Rows past T are zeros in LDS and are not stored.
 template <int MI>
 __global__ __launch_bounds__(256, 2) void combine_router_x3_kernel(
     const uint16_t* __restrict__ y_prev, const int32_t* __restrict__ row_prev,
